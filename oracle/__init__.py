@@ -1,0 +1,311 @@
+"""Python view of the CPU oracle (oracle.c) for the gauge-coded KV-cache codec.
+
+TEST INFRASTRUCTURE ONLY: the test-suite, the smoke check and the CPU-baseline leg of the
+benchmark use it; the product library never imports, links or runs it, and this package
+imports nothing from the product package.
+
+Every entry mirrors the codec-wrapper equations of the paper's section 3
+(Z = G X, B_c = C(Z), Zhat = D(B_c), Xhat = G^T Zhat), the gauge parameterisation of
+section 4.1 (G = exp(A - A^T), G^-1 = G^T) and the block-uniform / KIVI-style backends of
+section 4.3.  The arithmetic itself lives in oracle.c; this file only marshals numpy arrays
+and states the byte layouts the codec writes (a library contract the oracle mirrors).
+"""
+from __future__ import annotations
+
+import ctypes as C
+import dataclasses
+import os
+
+import numpy as np
+
+from . import build as _build
+
+PASSTHROUGH, BLOCK_UNIFORM, KIVI = 0, 1, 2
+GAUGE_IDENTITY, GAUGE_HAAR, GAUGE_DCT2, GAUGE_HADAMARD, GAUGE_EXPM, GAUGE_USER = range(6)
+FLAG_NONFINITE, FLAG_SIDE_OVERFLOW = 1, 2
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        path = _build.LIB
+        if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_build.SRC):
+            _build.build()
+        L = C.CDLL(path)
+        vp, i, u64 = C.c_void_p, C.c_int, C.c_uint64
+        L.orc_philox4x32_10.argtypes = [vp, vp, vp]
+        L.orc_gaussian.argtypes = [u64, u64, u64]
+        L.orc_gaussian.restype = C.c_double
+        L.orc_f16_round_dir.argtypes = [C.c_double, i]
+        L.orc_f16_round_dir.restype = C.c_double
+        L.orc_f16_bits.argtypes = [C.c_double]
+        L.orc_f16_bits.restype = C.c_uint16
+        L.orc_f16_value.argtypes = [C.c_uint16]
+        L.orc_f16_value.restype = C.c_double
+        L.orc_bf16_to_f32.argtypes = [C.c_uint16]
+        L.orc_bf16_to_f32.restype = C.c_float
+        L.orc_f32_to_bf16.argtypes = [C.c_float]
+        L.orc_f32_to_bf16.restype = C.c_uint16
+        L.orc_orthogonality_error.argtypes = [i, vp]
+        L.orc_orthogonality_error.restype = C.c_double
+        L.orc_gauge_make.argtypes = [i, i, i, i, i, u64, vp, vp]
+        L.orc_gauge_apply.argtypes = [i, i, vp, vp, vp]
+        L.orc_gauge_inverse.argtypes = [i, i, vp, vp, vp]
+        L.orc_quantize_block.argtypes = [vp, i, i, vp, vp, vp]
+        L.orc_dequantize_block.argtypes = [vp, i, C.c_uint16, C.c_uint16, vp]
+        L.orc_pack_codes.argtypes = [vp, i, i, vp]
+        L.orc_unpack_codes.argtypes = [vp, i, i, vp]
+        L.orc_kv_encode.argtypes = [i] * 13 + [i, vp, vp, i, vp, vp, vp, i]
+        L.orc_kv_decode.argtypes = [i] * 12 + [vp, i, vp, vp, vp, vp, i, i, i, vp]
+        L.orc_kv_append.argtypes = [i] * 12 + [i, vp, vp, i, vp, vp, vp, vp]
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(C.c_void_p)
+
+
+# ------------------------------------------------------------------------------------------
+# number formats and the counter-based generator
+# ------------------------------------------------------------------------------------------
+
+def philox4x32_10(ctr, key):
+    c = np.asarray(ctr, dtype=np.uint32).copy()
+    k = np.asarray(key, dtype=np.uint32).copy()
+    out = np.zeros(4, dtype=np.uint32)
+    lib().orc_philox4x32_10(_p(c), _p(k), _p(out))
+    return out
+
+
+def gaussian(seed: int, index: int, k: int) -> float:
+    return lib().orc_gaussian(seed, index, k)
+
+
+def f16_round_dir(v: float, direction: int) -> float:
+    return lib().orc_f16_round_dir(float(v), int(direction))
+
+
+def f16_bits(v: float) -> int:
+    return int(lib().orc_f16_bits(float(v)))
+
+
+def f16_value(bits: int) -> float:
+    return lib().orc_f16_value(int(bits))
+
+
+def bf16_to_f32(bits: int) -> float:
+    return lib().orc_bf16_to_f32(int(bits))
+
+
+def f32_to_bf16(v: float) -> int:
+    return int(lib().orc_f32_to_bf16(float(v)))
+
+
+# ------------------------------------------------------------------------------------------
+# gauges (section 3 Table 1; section 4.1; section 4.3 controls)
+# ------------------------------------------------------------------------------------------
+
+def gauge_make(kind: int, L: int, H: int, d: int, g: int, seed: int = 0, params=None) -> np.ndarray:
+    """Every gauge of a cache as float32 [L][2][H][R][g][g], R = d / g."""
+    R = d // g
+    G = np.zeros((L, 2, H, R, g, g), dtype=np.float32)
+    par = None if params is None else np.ascontiguousarray(params, dtype=np.float32)
+    rc = lib().orc_gauge_make(kind, L, H, d, g, seed, _p(par), _p(G))
+    if rc != 0:
+        raise ValueError(f"orc_gauge_make failed with {rc}")
+    return G
+
+
+def orthogonality_error(Gblock: np.ndarray) -> float:
+    Gb = np.ascontiguousarray(Gblock, dtype=np.float32)
+    return lib().orc_orthogonality_error(Gb.shape[-1], _p(Gb))
+
+
+def gauge_apply(Gs: np.ndarray, x: np.ndarray) -> np.ndarray:
+    """z = G x for one vector; Gs holds the R gauges [R][g][g] of its (l, s, h)."""
+    Gs = np.ascontiguousarray(Gs, dtype=np.float32)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    z = np.zeros_like(x)
+    lib().orc_gauge_apply(x.shape[0], Gs.shape[-1], _p(Gs), _p(x), _p(z))
+    return z
+
+
+def gauge_inverse(Gs: np.ndarray, z: np.ndarray) -> np.ndarray:
+    Gs = np.ascontiguousarray(Gs, dtype=np.float32)
+    z = np.ascontiguousarray(z, dtype=np.float32)
+    x = np.zeros_like(z)
+    lib().orc_gauge_inverse(z.shape[0], Gs.shape[-1], _p(Gs), _p(z), _p(x))
+    return x
+
+
+# ------------------------------------------------------------------------------------------
+# quantiser and packing (section 4.3)
+# ------------------------------------------------------------------------------------------
+
+def quantize_block(z: np.ndarray, bits: int):
+    z = np.ascontiguousarray(z, dtype=np.float32)
+    q = np.zeros(z.shape[0], dtype=np.uint8)
+    mn = np.zeros(1, dtype=np.uint16)
+    sc = np.zeros(1, dtype=np.uint16)
+    flags = lib().orc_quantize_block(_p(z), z.shape[0], bits, _p(q), _p(mn), _p(sc))
+    return q, int(mn[0]), int(sc[0]), flags
+
+
+def dequantize_block(q: np.ndarray, mn_bits: int, sc_bits: int) -> np.ndarray:
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    out = np.zeros(q.shape[0], dtype=np.float32)
+    lib().orc_dequantize_block(_p(q), q.shape[0], mn_bits, sc_bits, _p(out))
+    return out
+
+
+def pack_codes(q: np.ndarray, bits: int) -> np.ndarray:
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    out = np.zeros((q.shape[0] * bits + 7) // 8, dtype=np.uint8)
+    lib().orc_pack_codes(_p(q), q.shape[0], bits, _p(out))
+    return out
+
+
+def unpack_codes(packed: np.ndarray, n: int, bits: int) -> np.ndarray:
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    q = np.zeros(n, dtype=np.uint8)
+    lib().orc_unpack_codes(_p(packed), n, bits, _p(q))
+    return q
+
+
+# ------------------------------------------------------------------------------------------
+# whole-cache codec over the library's byte layouts
+# ------------------------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class Codec:
+    backend: int = BLOCK_UNIFORM
+    bits: int = 4
+    block_c: int = 64          # block-uniform channel block n
+    key_tokens: int = 32       # KIVI key token group
+    val_channels: int = 64     # KIVI value channel group
+    residual: int = 128        # KIVI full-precision window
+
+    def args(self):
+        return [self.backend, self.bits, self.block_c, self.key_tokens, self.val_channels, self.residual]
+
+
+def cache_layout(codec: Codec, s: int, L: int, B: int, H: int, T_cap: int, d: int) -> dict:
+    """Shapes and dtypes of the (codes, side, residual) buffers of one K or V cache."""
+    b = codec.bits
+    if codec.backend == PASSTHROUGH:
+        return {"codes": ((L, B, H, T_cap, d), np.float32), "side": None, "residual": None}
+    if codec.backend == BLOCK_UNIFORM:
+        n = codec.block_c
+        return {"codes": ((L, B, H, T_cap, d * b // 8), np.uint8),
+                "side": ((L, B, H, T_cap, d // n, 2), np.uint16), "residual": None}
+    kg, kvc, win = codec.key_tokens, codec.val_channels, codec.residual
+    ring = ((L, B, H, win + kg, d), np.uint16)
+    if s == 0:
+        return {"codes": ((L, B, H, T_cap // kg, d, kg * b // 8), np.uint8),
+                "side": ((L, B, H, T_cap // kg, d, 2), np.uint16), "residual": ring}
+    return {"codes": ((L, B, H, T_cap, d * b // 8), np.uint8),
+            "side": ((L, B, H, T_cap, d // kvc, 2), np.uint16), "residual": ring}
+
+
+def empty_cache(codec: Codec, s: int, L: int, B: int, H: int, T_cap: int, d: int) -> dict:
+    lay = cache_layout(codec, s, L, B, H, T_cap, d)
+    return {k: (None if v is None else np.zeros(v[0], dtype=v[1])) for k, v in lay.items()}
+
+
+def kivi_tq(T: int, codec: Codec) -> int:
+    """Tokens quantised when a KIVI cache holds T tokens."""
+    if T < codec.residual:
+        return 0
+    return ((T - codec.residual) // codec.key_tokens) * codec.key_tokens
+
+
+def kv_encode(codec: Codec, s: int, X: np.ndarray, G: np.ndarray, T_cap: int, cache: dict | None = None,
+              t0: int = 0):
+    """Encode X[L][B][H][T][d] (uint16 bf16 bits or float32) at positions [t0, t0+T)."""
+    L_, B, H, T, d = X.shape
+    g = G.shape[-1]
+    x_bf16 = 1 if X.dtype == np.uint16 else 0
+    X = np.ascontiguousarray(X)
+    Gc = np.ascontiguousarray(G, dtype=np.float32)
+    if cache is None:
+        cache = empty_cache(codec, s, L_, B, H, T_cap, d)
+    flags = lib().orc_kv_encode(*codec.args(), s, L_, B, H, T, d, g, x_bf16, _p(X), _p(Gc), T_cap,
+                                _p(cache["codes"]), _p(cache["side"]), _p(cache["residual"]), t0)
+    if flags < 0:
+        raise ValueError(f"orc_kv_encode rejected its arguments ({flags})")
+    return cache, flags
+
+
+def kv_decode(codec: Codec, s: int, G: np.ndarray, cache: dict, t0: int, Tout: int, lens=None,
+              out_bf16: bool = True) -> np.ndarray:
+    """Decode tokens [t0, t0+Tout) into Xhat[L][B][H][Tout][d] (uint16 bf16 bits or float32)."""
+    L_, B, H = cache["codes"].shape[:3]
+    d = G.shape[-3] * G.shape[-1]
+    g = G.shape[-1]
+    if codec.backend == KIVI and s == 0:
+        T_cap = cache["codes"].shape[3] * codec.key_tokens
+    else:
+        T_cap = cache["codes"].shape[3]
+    Gc = np.ascontiguousarray(G, dtype=np.float32)
+    out = np.zeros((L_, B, H, Tout, d), dtype=np.uint16 if out_bf16 else np.float32)
+    ln = None if lens is None else np.ascontiguousarray(lens, dtype=np.int32)
+    rc = lib().orc_kv_decode(*codec.args(), s, L_, B, H, d, g, _p(Gc), T_cap, _p(cache["codes"]),
+                             _p(cache["side"]), _p(cache["residual"]), _p(ln), t0, Tout, 1 if out_bf16 else 0,
+                             _p(out))
+    if rc < 0:
+        raise ValueError(f"orc_kv_decode rejected its arguments ({rc})")
+    return out
+
+
+def kv_append(codec: Codec, s: int, Xnew: np.ndarray, G: np.ndarray, cache: dict, pos) -> int:
+    """Rolling append of Xnew[L][B][H][d] at pos[b]; returns the flags."""
+    L_, B, H, d = Xnew.shape
+    g = G.shape[-1]
+    x_bf16 = 1 if Xnew.dtype == np.uint16 else 0
+    if codec.backend == KIVI and s == 0:
+        T_cap = cache["codes"].shape[3] * codec.key_tokens
+    else:
+        T_cap = cache["codes"].shape[3]
+    Xn = np.ascontiguousarray(Xnew)
+    Gc = np.ascontiguousarray(G, dtype=np.float32)
+    ps = np.ascontiguousarray(pos, dtype=np.int32)
+    flags = lib().orc_kv_append(*codec.args(), s, L_, B, H, d, g, x_bf16, _p(Xn), _p(Gc), T_cap,
+                                _p(cache["codes"]), _p(cache["side"]), _p(cache["residual"]), _p(ps))
+    if flags < 0:
+        raise ValueError(f"orc_kv_append rejected its arguments ({flags})")
+    return flags
+
+
+# ------------------------------------------------------------------------------------------
+# cache metrics (section 4.4 and the metric-definition table of the appendix)
+# ------------------------------------------------------------------------------------------
+
+def nrmse(ref: np.ndarray, got: np.ndarray) -> float:
+    """sqrt(sum SSE / sum reference SSE) over all elements, in binary64."""
+    r = np.asarray(ref, dtype=np.float64)
+    e = np.asarray(got, dtype=np.float64) - r
+    return float(np.sqrt(np.sum(e * e) / np.sum(r * r)))
+
+
+def live_bytes(codec: Codec, s: int, T: int, d: int) -> int:
+    """Bytes one (l, b, h) slice of a K or V cache holding T tokens occupies: codes, side info
+    and the full-precision window (the gauge itself is a per-checkpoint object, not counted)."""
+    b = codec.bits
+    if codec.backend == PASSTHROUGH:
+        return T * d * 4
+    if codec.backend == BLOCK_UNIFORM:
+        return T * (d * b // 8 + (d // codec.block_c) * 4)
+    tq = kivi_tq(T, codec)
+    win = (T - tq) * d * 2
+    if s == 0:
+        return tq * d * b // 8 + (tq // codec.key_tokens) * d * 4 + win
+    return tq * (d * b // 8 + (d // codec.val_channels) * 4) + win
+
+
+def bits_per_value(codec: Codec, T: int, d: int) -> float:
+    """Measured bits per represented K/V value for one (l, b, h) slice pair."""
+    tot = live_bytes(codec, 0, T, d) + live_bytes(codec, 1, T, d)
+    return 8.0 * tot / (2.0 * T * d)

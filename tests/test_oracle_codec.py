@@ -1,0 +1,253 @@
+"""Pins of the oracle's quantisation backends (paper section 4.3: block-uniform ranges and
+KIVI-style per-channel key / per-token value ranges, same bit settings) and of the rolling
+compressed-history path (section 4.4), against bounds, brute force, numpy's bit unpacking,
+structural equivalences between the backends and closed-form byte counts."""
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2607_20538_amd import synth
+
+BITS = [2, 3, 4, 6, 8]
+
+
+def _f16(bits):
+    return O.f16_value(bits)
+
+
+def _blocks(rng, n, count):
+    out = []
+    for k in range(count):
+        kind = k % 6
+        if kind == 0:
+            z = rng.standard_normal(n)
+        elif kind == 1:
+            z = rng.standard_normal(n) * 20.0 + 5.0
+        elif kind == 2:
+            z = rng.standard_normal(n) * 1e-3
+        elif kind == 3:
+            z = np.where(rng.random(n) < 0.1, 40.0, 1.0) * rng.standard_normal(n)
+        elif kind == 4:
+            z = rng.uniform(100.0, 101.0, n)
+        else:
+            z = -np.abs(rng.standard_normal(n)) * 300.0
+        out.append(z.astype(np.float32))
+    return out
+
+
+@pytest.mark.parametrize("bits", BITS)
+@pytest.mark.parametrize("n", [16, 32, 64])
+def test_quantiser_error_bound_and_side_info(bits, n):
+    """|z - zhat| <= sc_h / 2 (up to binary32 rounding of the reconstruction), codes in range,
+    mn_h is the largest binary16 <= min and the grid covers [min, max]."""
+    rng = np.random.default_rng(bits * 100 + n)
+    qmax = (1 << bits) - 1
+    for z in _blocks(rng, n, 60):
+        q, mnb, scb, flags = O.quantize_block(z, bits)
+        assert flags == 0
+        assert q.max() <= qmax
+        mn, sc = _f16(mnb), _f16(scb)
+        assert mn <= z.min()
+        assert np.float16(mn) == mn and np.float16(sc) == sc
+        nxt = float(np.nextafter(np.float16(mn), np.float16(np.inf), dtype=np.float16))
+        assert nxt > z.min()
+        assert sc >= 0 and not (mn == 0 and np.signbit(mn))
+        zh = O.dequantize_block(q, mnb, scb)
+        bound = sc / 2 * (1 + 2.0 ** -20) + 2.0 ** -22 * np.abs(z).max()
+        assert np.abs(z.astype(np.float64) - zh).max() <= bound
+
+
+@pytest.mark.parametrize("bits", BITS)
+def test_constant_block(bits):
+    for v in (0.0, 1.5, -3.25, 1000.0, 0.1):
+        z = np.full(32, v, np.float32)
+        q, mnb, scb, _ = O.quantize_block(z, bits)
+        assert np.all(q == q[0])
+        zh = O.dequantize_block(q, mnb, scb)
+        if float(np.float16(v)) == v:   # min representable in binary16: code 0, exact
+            assert np.all(q == 0)
+            assert _f16(scb) == 0.0
+            np.testing.assert_array_equal(zh, z)
+        else:
+            assert np.abs(zh - z).max() <= _f16(scb) / 2 * (1 + 2.0 ** -20)
+
+
+@pytest.mark.parametrize("n,bits", list(itertools.product([2, 4, 8], [2, 3])))
+def test_quantiser_brute_force_nearest_code(n, bits):
+    """Each code is the nearest grid point mn_h + q sc_h over all 2^b codes, except inside
+    a rounding tie where both neighbours are equally near."""
+    rng = np.random.default_rng(n * 7 + bits)
+    for z in _blocks(rng, n, 300):
+        q, mnb, scb, _ = O.quantize_block(z, bits)
+        mn, sc = np.float32(_f16(mnb)), np.float32(_f16(scb))
+        grid = mn.astype(np.float64) + np.arange(1 << bits) * sc.astype(np.float64)
+        for i in range(n):
+            dist = np.abs(grid - z[i])
+            best = dist.min()
+            if dist[q[i]] != best:
+                t = (np.float32(z[i] - mn) * (np.float32(1.0) / sc)) if sc else 0.0
+                assert abs(abs(t - np.floor(t)) - 0.5) < 1e-5, (z, i, q[i], dist)
+
+
+def test_quantiser_grid_aligned_block_is_idempotent():
+    for bits in BITS:
+        qmax = (1 << bits) - 1
+        mn, sc = np.float32(-2.0), np.float32(0.125)
+        q0 = np.arange(qmax + 1) % (qmax + 1)
+        z = (mn + q0.astype(np.float32) * sc).astype(np.float32)
+        q, mnb, scb, _ = O.quantize_block(z, bits)
+        np.testing.assert_array_equal(q, q0)
+        np.testing.assert_array_equal(O.dequantize_block(q, mnb, scb), z)
+
+
+def test_quantiser_flags_nonfinite_and_overflow():
+    z = np.ones(16, np.float32)
+    z[3] = np.inf
+    assert O.quantize_block(z, 4)[3] & O.FLAG_NONFINITE
+    z = np.array([-70000.0] + [0.0] * 15, np.float32)
+    assert O.quantize_block(z, 4)[3] & O.FLAG_SIDE_OVERFLOW
+    z = np.array([0.0] * 15 + [2e6], np.float32)
+    assert O.quantize_block(z, 4)[3] & O.FLAG_SIDE_OVERFLOW
+    assert O.quantize_block(np.array([0.0] * 15 + [6e4], np.float32), 4)[3] == 0
+
+
+@pytest.mark.parametrize("bits", BITS)
+def test_pack_order_matches_numpy_little_endian_bits(bits):
+    rng = np.random.default_rng(bits)
+    patterns = [rng.integers(0, 1 << bits, 64), np.zeros(64, int), np.full(64, (1 << bits) - 1),
+                np.arange(64) % 2 * ((1 << bits) - 1)]
+    for codes in patterns:
+        codes = codes.astype(np.uint8)
+        packed = O.pack_codes(codes, bits)
+        assert packed.size == 64 * bits // 8
+        stream = np.unpackbits(packed, bitorder="little")
+        rebuilt = np.array([sum(int(stream[i * bits + k]) << k for k in range(bits)) for i in range(64)])
+        np.testing.assert_array_equal(rebuilt, codes)
+        np.testing.assert_array_equal(O.unpack_codes(packed, 64, bits), codes)
+
+
+def _tensor(T, d=128, L=1, B=2, H=2, seed=0xABC, dtype="bf16"):
+    w = synth.Workload("t", L=L, B=B, H=H, T=T, d=d, dtype=dtype, g=32, backend="bu", bits=4, data_seed=seed)
+    return w, synth.kv_tensor(w, 0), synth.kv_tensor(w, 1)
+
+
+def test_block_uniform_row_layout():
+    """A BU code row holds the d/n blocks of one token in channel order, each its own
+    LSB-first stream; side rows hold (min, scale) per block."""
+    w, K, _ = _tensor(8, d=128)
+    G = O.gauge_make(O.GAUGE_HAAR, 1, 2, 128, 32, seed=1)
+    codec = O.Codec(backend=O.BLOCK_UNIFORM, bits=3, block_c=32)
+    cache, flags = O.kv_encode(codec, 0, K, G, T_cap=8)
+    assert flags == 0
+    for (b, h, t) in [(0, 0, 0), (1, 1, 7), (0, 1, 3)]:
+        x = np.array([O.bf16_to_f32(v) for v in K[0, b, h, t]], np.float32)
+        z = O.gauge_apply(G[0, 0, h], x)
+        for k in range(4):
+            q, mnb, scb, _ = O.quantize_block(z[32 * k:32 * k + 32], 3)
+            np.testing.assert_array_equal(cache["codes"][0, b, h, t, 12 * k:12 * k + 12], O.pack_codes(q, 3))
+            assert tuple(cache["side"][0, b, h, t, k]) == (mnb, scb)
+
+
+def test_kivi_values_equal_block_uniform_with_value_group():
+    w, K, V = _tensor(256 + 40)
+    T = V.shape[3]
+    G = O.gauge_make(O.GAUGE_HAAR, 1, 2, 128, 32, seed=4)
+    kivi = O.Codec(backend=O.KIVI, bits=3, key_tokens=32, val_channels=64, residual=128)
+    bu = O.Codec(backend=O.BLOCK_UNIFORM, bits=3, block_c=64)
+    ck, _ = O.kv_encode(kivi, 1, V, G, T_cap=320)
+    cb, _ = O.kv_encode(bu, 1, V, G, T_cap=320)
+    tq = O.kivi_tq(T, kivi)
+    assert tq == 160
+    np.testing.assert_array_equal(ck["codes"][:, :, :, :tq], cb["codes"][:, :, :, :tq])
+    np.testing.assert_array_equal(ck["side"][:, :, :, :tq], cb["side"][:, :, :, :tq])
+    assert not ck["codes"][:, :, :, tq:].any()
+
+
+def test_kivi_keys_equal_block_uniform_on_transposed_tile():
+    w, K, _ = _tensor(256)
+    G = O.gauge_make(O.GAUGE_HAAR, 1, 2, 128, 32, seed=4)
+    kivi = O.Codec(backend=O.KIVI, bits=3, key_tokens=32, val_channels=64, residual=128)
+    ck, _ = O.kv_encode(kivi, 0, K, G, T_cap=256)
+    assert O.kivi_tq(256, kivi) == 128
+    b, h = 1, 0
+    for grp in range(4):
+        Z = np.stack([O.gauge_apply(G[0, 0, h], np.array([O.bf16_to_f32(v) for v in K[0, b, h, 32 * grp + u]],
+                                                          np.float32)) for u in range(32)])
+        for c in (0, 5, 127):
+            q, mnb, scb, _ = O.quantize_block(Z[:, c], 3)
+            np.testing.assert_array_equal(ck["codes"][0, b, h, grp, c], O.pack_codes(q, 3))
+            assert tuple(ck["side"][0, b, h, grp, c]) == (mnb, scb)
+
+
+def test_kivi_short_cache_is_all_window_and_decodes_bit_exact():
+    w, K, V = _tensor(100)
+    G = O.gauge_make(O.GAUGE_HAAR, 1, 2, 128, 32, seed=4)
+    kivi = O.Codec(backend=O.KIVI, bits=3)
+    for s, X in ((0, K), (1, V)):
+        c, _ = O.kv_encode(kivi, s, X, G, T_cap=128)
+        assert not c["codes"].any()
+        Xh = O.kv_decode(kivi, s, G, c, 0, 100, lens=[100, 100])
+        np.testing.assert_array_equal(Xh, X)
+
+
+@pytest.mark.parametrize("backend", [O.BLOCK_UNIFORM, O.KIVI, O.PASSTHROUGH])
+def test_rolling_append_equals_batch_encode(backend):
+    """Appending tokens one at a time (section 4.4 rolling history) leaves the same cache
+    and decodes the same history as one batch encode of all tokens."""
+    T0, steps = 150, 50
+    w, K, V = _tensor(T0 + steps, B=2)
+    G = O.gauge_make(O.GAUGE_HAAR, 1, 2, 128, 32, seed=6)
+    codec = O.Codec(backend=backend, bits=4, block_c=32, residual=128)
+    T_cap = 224
+    for s, X in ((0, K), (1, V)):
+        roll, _ = O.kv_encode(codec, s, X[:, :, :, :T0], G, T_cap=T_cap)
+        for t in range(T0, T0 + steps):
+            O.kv_append(codec, s, np.ascontiguousarray(X[:, :, :, t]), G, roll, [t, t])
+        full, _ = O.kv_encode(codec, s, X, G, T_cap=T_cap)
+        T = T0 + steps
+        if backend == O.KIVI:
+            tq = O.kivi_tq(T, codec)
+            if s == 0:
+                np.testing.assert_array_equal(roll["codes"][:, :, :, :tq // 32], full["codes"][:, :, :, :tq // 32])
+                np.testing.assert_array_equal(roll["side"][:, :, :, :tq // 32], full["side"][:, :, :, :tq // 32])
+            else:
+                np.testing.assert_array_equal(roll["codes"][:, :, :, :tq], full["codes"][:, :, :, :tq])
+                np.testing.assert_array_equal(roll["side"][:, :, :, :tq], full["side"][:, :, :, :tq])
+        else:
+            np.testing.assert_array_equal(roll["codes"], full["codes"])
+            if backend == O.BLOCK_UNIFORM:
+                np.testing.assert_array_equal(roll["side"], full["side"])
+        a = O.kv_decode(codec, s, G, roll, 0, T, lens=[T, T])
+        b = O.kv_decode(codec, s, G, full, 0, T, lens=[T, T])
+        np.testing.assert_array_equal(a, b)
+
+
+def test_bits_per_value_closed_forms():
+    """Block-uniform: b + 32/n (two binary16 per block); KIVI: keys b + 32/G_k, values
+    b + 32/n_v on the quantised tokens, 16 bits on the window tokens."""
+    bu = lambda b, n: O.Codec(backend=O.BLOCK_UNIFORM, bits=b, block_c=n)
+    assert O.bits_per_value(bu(4, 32), 256, 64) == 5.0          # tiny
+    assert O.bits_per_value(bu(4, 64), 8192, 128) == 4.5        # Llama-3-8B shaped
+    for b, ref in ((3, 3.5), (4, 4.5), (6, 6.5)):               # 27B sweep
+        assert O.bits_per_value(bu(b, 64), 16384, 128) == ref
+    kivi = O.Codec(backend=O.KIVI, bits=3, key_tokens=32, val_channels=64, residual=128)
+    T, tq = 32768, 32640
+    ref = (tq * (3 + 1.0) + tq * (3 + 0.5) + 2 * (T - tq) * 16) / (2 * T)
+    assert abs(O.bits_per_value(kivi, T, 128) - ref) < 1e-12
+    assert round(ref, 4) == 3.7979
+
+
+def test_lossy_codec_error_is_bounded_per_block():
+    """End to end, BU decode error in gauge space stays within the per-block half-step, so
+    the bf16 output is within half a step plus bf16 rounding (the gauge is an isometry)."""
+    w, K, V = _tensor(64, B=1, H=1)
+    G = O.gauge_make(O.GAUGE_HAAR, 1, 1, 128, 128, seed=8)
+    codec = O.Codec(backend=O.BLOCK_UNIFORM, bits=4, block_c=64)
+    cache, _ = O.kv_encode(codec, 0, K, G, T_cap=64)
+    Xh = O.kv_decode(codec, 0, G, cache, 0, 64, out_bf16=False)
+    x = np.array([[O.bf16_to_f32(v) for v in row] for row in K[0, 0, 0]], np.float64)
+    sc = np.vectorize(O.f16_value)(cache["side"][0, 0, 0, :, :, 1])
+    err = np.linalg.norm(Xh[0, 0, 0] - x, axis=1)
+    assert np.all(err <= np.sqrt(64 * (sc[:, 0] / 2) ** 2 + 64 * (sc[:, 1] / 2) ** 2) * (1 + 1e-5))
