@@ -1,0 +1,195 @@
+/*
+ * codec_gauge.h - C ABI of the MI355X (gfx950) gauge-coded KV-cache codec.
+ *
+ * The library implements the codec wrapper of Codec-Gauge ("Learning Compression-Friendly
+ * Gauges for Transformer KV Caches"), section 3 (Problem Statement):
+ *
+ *     Z = G X,   B_c = C(Z),   Zhat = D(B_c),   Xhat = G^{-1} Zhat = G^T Zhat
+ *
+ * where X is a layer's key or value cache K_l, V_l in R^{B x H x T x d} (section 3), G is a
+ * block-diagonal orthogonal gauge with one g x g block G_{l,s,h,r} per (layer l, cache type
+ * s in {K, V}, head h, channel group r), R = d / g (section 3, Table 1), G^{-1} = G^T
+ * (section 4.1 eq.), and C / D are the compression and decompression maps of a fixed
+ * quantisation backend (section 4.3, Compression Conditions): block-uniform ranges, or
+ * KIVI-style per-channel key and per-token value ranges.  The gauge mixes channels inside
+ * one group of one cached vector only; it never mixes tokens, heads or layers.
+ *
+ * Conventions shared by every entry point
+ *   - Every function returns an int32 status (CG_OK = 0 on success) and never throws.
+ *     cg_status_str() names a status.
+ *   - All arguments are validated on the host before anything is enqueued; on an error
+ *     nothing is launched and nothing is written.
+ *   - Device work is enqueued on the caller's HIP stream (`stream`, a hipStream_t; NULL is
+ *     the null stream) and the call returns without synchronising.  Kernel faults surface
+ *     at the caller's next synchronisation.
+ *   - Ownership: every buffer is allocated and freed by the caller.  The library keeps no
+ *     pointer after a call returns, allocates no device memory in these entry points and
+ *     holds no global state, so calls are reentrant; calls that write the same cache
+ *     buffers on different streams race.
+ *   - err_flag (optional, may be NULL): a caller-owned device int32 that kernels OR with
+ *     CG_FLAG_* bits when they meet a non-finite input, a side-info value that overflows
+ *     binary16, or an append position outside the cache.  The library never clears it.
+ *   - Device pointers must be 16-byte aligned (CG_ERR_ALIGN otherwise).  A view with T = 0
+ *     touches no memory and may carry a NULL pointer.
+ *   - Tensors: element (l, b, h, t, c) of a cg_kv_view sits at
+ *     ptr + l*stride_l + b*stride_b + h*stride_h + t*stride_t + c (strides in elements,
+ *     channel stride 1); strides must keep 16-byte alignment of every row.
+ *
+ * Byte layouts of a compressed cache (one cg_cache per cache type s; a library contract,
+ * the paper leaves the packing format unstated):
+ *   block-uniform   codes [L][B][H][T_cap][d*b/8] bytes: the d/n blocks of one token in
+ *                   channel order, each an LSB-first stream of n b-bit codes (bit k of a
+ *                   stream is bit k mod b of code floor(k/b); stream bit k is bit k%8 of
+ *                   byte k/8); side [L][B][H][T_cap][d/n][2] binary16 (min, scale).
+ *   KIVI keys       codes [L][B][H][T_cap/Gk][d][Gk*b/8]: per channel, the LSB-first stream
+ *                   of the Gk tokens of one token group; side [L][B][H][T_cap/Gk][d][2].
+ *   KIVI values     as block-uniform with n = val_channels.
+ *   KIVI window     residual [L][B][H][W+Gk][d] raw bf16, token t in slot t mod (W+Gk).
+ *                   A KIVI cache holding T tokens quantises the first
+ *                   T_q = floor((T - W)/Gk) * Gk of them (0 when T < W); the rest stay in
+ *                   the window.
+ *   passthrough     codes [L][B][H][T_cap][d] binary32 z (the error-free backend of the
+ *                   paper's no-compression sanity rows, section 4.4).
+ *
+ * Quantiser (section 4.3; every fp32 operation rounds to nearest even, no fused
+ * multiply-add):  mn_h = binary16 rounded toward -inf of the block minimum (+0 for zero),
+ * sc_h = binary16 rounded toward +inf of fl32(fl32(max - mn_h) / (2^b - 1)),
+ * inv = fl32(1 / sc_h) (0 when sc_h is 0), q = clamp(rint(fl32(fl32(z - mn_h) * inv)),
+ * 0, 2^b - 1); decode zhat = fl32(mn_h + q * sc_h).
+ */
+#ifndef CODEC_GAUGE_H
+#define CODEC_GAUGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+enum {
+  CG_OK = 0,
+  CG_ERR_ARG = 1,             /* NULL pointer, bad enum, inconsistent dimensions */
+  CG_ERR_SHAPE = 2,           /* view / cache / gauge shapes disagree */
+  CG_ERR_ALIGN = 3,           /* pointer or stride breaks 16-byte alignment */
+  CG_ERR_UNSUPPORTED = 4,     /* valid but not implemented (g, b, n, d combination) */
+  CG_ERR_NOT_ORTHOGONAL = 5,  /* CG_GAUGE_USER block with max |G G^T - I| > 1e-5 */
+  CG_ERR_CAPACITY = 6,        /* token range beyond the cache capacity */
+  CG_ERR_DEVICE = 7           /* a HIP runtime call failed */
+};
+
+/* device error-flag bits */
+enum { CG_FLAG_NONFINITE = 1, CG_FLAG_SIDE_OVERFLOW = 2, CG_FLAG_POS_RANGE = 4 };
+
+/* gauge kinds (section 4.1 and the controls of section 4.3) */
+enum {
+  CG_GAUGE_IDENTITY = 0,  /* raw coordinates */
+  CG_GAUGE_HAAR = 1,      /* sampled orthogonal gauge with the learned gauge's block structure */
+  CG_GAUGE_DCT2 = 2,      /* orthonormal DCT-II, row k = frequency k */
+  CG_GAUGE_HADAMARD = 3,  /* Sylvester-ordered Hadamard / sqrt(g); g a power of two */
+  CG_GAUGE_EXPM = 4,      /* G = exp(A - A^T), params = A (section 4.1 eq.) */
+  CG_GAUGE_USER = 5       /* params = G itself (e.g. a trained gauge) */
+};
+
+/* backends (section 4.3) */
+enum { CG_BACKEND_PASSTHROUGH = 0, CG_BACKEND_BLOCK_UNIFORM = 1, CG_BACKEND_KIVI = 2 };
+
+/* element types of a cg_kv_view */
+enum { CG_DTYPE_BF16 = 0, CG_DTYPE_F32 = 1 };
+
+/* Gauge shape: L layers, H KV heads, head dimension d, group size g (R = d / g groups). */
+typedef struct cg_gauge_shape {
+  int32_t L, H, d, g;
+} cg_gauge_shape;
+
+/* Backend parameters.  bits: b in {2,3,4,6,8}.  block_c: block-uniform channel block n
+ * (n | d, n * b % 32 == 0).  key_tokens (Gk, KIVI keys: channel ranges over Gk tokens),
+ * val_channels (KIVI values: token ranges over that many channels), residual (W, KIVI
+ * full-precision window of recent tokens).  Unused fields are ignored. */
+typedef struct cg_codec {
+  int32_t backend, bits, block_c, key_tokens, val_channels, residual;
+} cg_codec;
+
+/* A strided view of a KV tensor [L][B][H][T][d] in device memory. */
+typedef struct cg_kv_view {
+  void* ptr;
+  int32_t dtype;                               /* CG_DTYPE_* */
+  int32_t L, B, H, T, d;
+  int64_t stride_l, stride_b, stride_h, stride_t;  /* in elements */
+} cg_kv_view;
+
+/* One compressed K or V cache (device buffers sized by cache_bytes()).  len: tokens the
+ * cache currently holds (host value, read by kv_decode for KIVI only). */
+typedef struct cg_cache {
+  void* codes;
+  void* side;      /* NULL for passthrough */
+  void* residual;  /* KIVI window; NULL otherwise */
+  int32_t L, B, H, T_cap, d;
+  int32_t len;
+} cg_cache;
+
+/* Static message for a status code. */
+const char* cg_status_str(int32_t status);
+
+/* Bytes of the device gauge buffer gauge_make() fills for this shape (0 if invalid). */
+size_t gauge_device_bytes(cg_gauge_shape shp);
+
+/* Builds every gauge block G_{l,s,h,r} (section 3, Table 1) on the host in binary64 and
+ * rounds it once to binary32.  kind: CG_GAUGE_*.  seed: random gauges draw block
+ * ((l*2+s)*H+h)*R+r from a Philox4x32-10 stream (Box-Muller normals, QR with the sign of
+ * R's diagonal folded in).  params: [L][2][H][R][g][g] binary32 host array for EXPM (A) and
+ * USER (G), else ignored.  G_host (optional): host array of the same shape receiving G.
+ * G_dev (optional): device buffer of gauge_device_bytes(shp) bytes receiving G and the
+ * derived forms the kernels read; the copy is enqueued on `stream` and completed before
+ * return.  At least one of G_host, G_dev must be non-NULL.
+ * Errors: CG_ERR_ARG, CG_ERR_UNSUPPORTED (g must divide d; Hadamard needs a power of two),
+ * CG_ERR_NOT_ORTHOGONAL (USER), CG_ERR_ALIGN, CG_ERR_DEVICE. */
+int32_t gauge_make(int32_t kind, cg_gauge_shape shp, uint64_t seed, const float* params, float* G_host,
+                   void* G_dev, void* stream);
+
+/* Byte sizes of the codes / side / residual buffers of one cache of type s (0 = K,
+ * 1 = V) with capacity T_cap tokens (T_cap a multiple of key_tokens for KIVI).  Any
+ * output pointer may be NULL. */
+int32_t cache_bytes(const cg_codec* codec, int32_t s, int32_t L, int32_t B, int32_t H, int32_t T_cap, int32_t d,
+                    size_t* codes, size_t* side, size_t* residual);
+
+/* Encode: Z = G X, B_c = C(Z) (section 3) for the X->T tokens of X_s, written at cache
+ * positions [t0, t0 + X->T).  s: 0 keys, 1 values.  G_dev: from gauge_make with the same
+ * shape.  KIVI requires t0 == 0 and bf16 input: X is the whole cache (T_q tokens
+ * quantised, the rest copied to the window).  out->len is not modified.
+ * Errors: CG_ERR_ARG, CG_ERR_SHAPE, CG_ERR_ALIGN, CG_ERR_UNSUPPORTED, CG_ERR_CAPACITY,
+ * CG_ERR_DEVICE. */
+int32_t kv_encode(int32_t s, const cg_kv_view* X, const void* G_dev, cg_gauge_shape shp, const cg_codec* codec,
+                  const cg_cache* out, int32_t t0, int32_t* err_flag, void* stream);
+
+/* Decode: Zhat = D(B_c), Xhat = G^T Zhat (section 3) for cache positions
+ * [t0, t0 + Xhat->T) into Xhat (bf16 rounded to nearest even, or binary32).  KIVI tokens
+ * at or beyond T_q(in->len) come back from the window bit for bit; KIVI requires
+ * t0 + Xhat->T <= in->len.
+ * Errors: as kv_encode. */
+int32_t kv_decode(int32_t s, const cg_cache* in, const void* G_dev, cg_gauge_shape shp, const cg_codec* codec,
+                  int32_t t0, const cg_kv_view* Xhat, int32_t* err_flag, void* stream);
+
+/* Rolling compressed-history step (section 4.4: every new KV token passes through gauge,
+ * backend, decode and inverse gauge), for layers [l0, l1):
+ *   1. encode the new key and value token of every (layer, b, h) at position pos[b]
+ *      (pos: device int32[B], read on the device, never by the host);  KIVI puts it in
+ *      the window and, when the cache then holds T = pos[b] + 1 tokens with T - W a
+ *      positive multiple of Gk, gauges and quantises the Gk oldest window tokens;
+ *   2. if k_hist / v_hist are non-NULL, decode the history [0, pos[b]] of those layers
+ *      into them (tokens beyond pos[b] are left untouched).
+ * k_new / v_new: views with L = l1 - l0 and T = 1 (view layer i is cache layer l0 + i).
+ * k_hist / v_hist: views with L = l1 - l0 and T = the number of token slots to cover;
+ * positions with pos[b] >= T_cap set CG_FLAG_POS_RANGE and skip that batch row.
+ * Errors: as kv_encode. */
+int32_t kv_append_step(int32_t l0, int32_t l1, const cg_kv_view* k_new, const cg_kv_view* v_new, const int32_t* pos,
+                       const void* G_dev, cg_gauge_shape shp, const cg_codec* codec, const cg_cache* kc,
+                       const cg_cache* vc, const cg_kv_view* k_hist, const cg_kv_view* v_hist, int32_t* err_flag,
+                       void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CODEC_GAUGE_H */

@@ -1,0 +1,90 @@
+// Device helpers of the codec kernels: number formats and the scalar quantiser step.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "codec_gauge.h"
+
+namespace cg {
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+// binary32 -> bfloat16 bits, round to nearest even (NaN stays a quiet NaN).
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ float f16_bits_to_f32(uint32_t bits) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)bits);
+}
+
+// Binary16 bits of v rounded toward -inf: the hardware conversion rounds to nearest even;
+// when that lands above v, step one binary16 ulp down.  -0 is returned as +0.
+__device__ __forceinline__ uint32_t f16_bits_down(float v) {
+  _Float16 h = (_Float16)v;
+  uint32_t bits = __builtin_bit_cast(uint16_t, h);
+  if ((float)h > v) bits = (bits & 0x8000u) ? bits + 1u : bits - 1u;
+  return bits == 0x8000u ? 0u : bits;
+}
+
+// Binary16 bits of v rounded toward +inf (-0 returned as +0).
+__device__ __forceinline__ uint32_t f16_bits_up(float v) {
+  _Float16 h = (_Float16)v;
+  uint32_t bits = __builtin_bit_cast(uint16_t, h);
+  if ((float)h < v) bits = (bits & 0x8000u) ? bits - 1u : bits + 1u;
+  return bits == 0x8000u ? 0u : bits;
+}
+
+// Side information of one quantisation block from its exact min and max (section 4.3
+// block range): binary16 min rounded down, binary16 scale rounded up, binary32 reciprocal.
+struct Side {
+  float mn, sc, inv;
+  uint32_t word;  // min bits | scale bits << 16 (min at the lower address)
+  int flags;
+};
+
+__device__ __forceinline__ Side make_side(float mn, float mx, int bits) {
+#pragma clang fp contract(off)
+  Side s;
+  uint32_t mnb = f16_bits_down(mn);
+  s.mn = f16_bits_to_f32(mnb);
+  float diff = mx - s.mn;
+  float s32 = diff / (float)((1 << bits) - 1);   // correctly rounded binary32 division
+  uint32_t scb = f16_bits_up(s32);
+  s.sc = f16_bits_to_f32(scb);
+  s.inv = (s.sc == 0.0f) ? 0.0f : 1.0f / s.sc;  // correctly rounded reciprocal
+  s.word = mnb | (scb << 16);
+  s.flags = (((mnb & 0x7c00u) == 0x7c00u) || ((scb & 0x7c00u) == 0x7c00u)) ? CG_FLAG_SIDE_OVERFLOW : 0;
+  return s;
+}
+
+// q = clamp(rint_even(fl32(fl32(z - mn) * inv)), 0, qmax)
+__device__ __forceinline__ uint32_t quantize(float z, float mn, float inv, float qmax) {
+#pragma clang fp contract(off)
+  float t = (z - mn) * inv;
+  float r = __builtin_rintf(t);
+  r = fminf(fmaxf(r, 0.0f), qmax);
+  return (uint32_t)r;
+}
+
+// zhat = fl32(mn + q * sc); q * sc is exact in binary32.
+__device__ __forceinline__ float dequantize(uint32_t q, float mn, float sc) {
+#pragma clang fp contract(off)
+  float p = (float)q * sc;
+  return mn + p;
+}
+
+// Code `idx` of an LSB-first stream of b-bit codes starting at a 4-byte boundary.
+__device__ __forceinline__ uint32_t extract_code(const uint32_t* stream, int idx, int bits) {
+  int bit = idx * bits;
+  int w = bit >> 5, off = bit & 31;
+  uint32_t v = stream[w] >> off;
+  if (off + bits > 32) v |= stream[w + 1] << (32 - off);
+  return v & ((1u << bits) - 1u);
+}
+
+}  // namespace cg

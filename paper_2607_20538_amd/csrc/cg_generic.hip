@@ -1,0 +1,359 @@
+// General-purpose codec kernels (any supported g, n, b, backend, bf16 or binary32 input).
+//
+// One workgroup owns a tile of tokens of one (layer, batch, head) slice.  The tile is staged
+// in LDS in binary32, the gauge z = G x of every channel group is applied on the VALU with a
+// binary32 accumulator (section 3: Z[b,h,t,r] = G_{l,s,h,r} X[b,h,t,r]), and the backend of
+// section 4.3 quantises the gauge-space tile from LDS: block-uniform / KIVI values one block
+// per thread, KIVI keys one channel of a token group per thread.  Decode mirrors it: codes
+// are unpacked and dequantised into an LDS tile, then Xhat = G^T Zhat is applied per
+// channel.  These kernels carry every configuration; the MFMA kernels take over the
+// large-group bf16 block-uniform case.
+#include "cg_internal.h"
+#include "cg_device.h"
+
+namespace cg {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ size_t gauge_block(int l, int s, int h, int r, int H, int R) {
+  return ((size_t(l) * 2 + s) * H + h) * R + r;
+}
+
+__device__ __forceinline__ float load_x(const ViewDev& v, size_t off) {
+  return v.bf16 ? bf16_to_f32(((const uint16_t*)v.ptr)[off]) : ((const float*)v.ptr)[off];
+}
+
+// zs[t][i] = sum_j G_{l,s,h,r}[i%g][j] xs[t][r*g + j] for t < ntok (binary32 FMA chain).
+__device__ void gauge_tile(const float* xs, float* zs, int ntok, int d, int dp, const GaugeDev& G, int l, int s,
+                           int h) {
+  const int g = G.g;
+  for (int idx = threadIdx.x; idx < ntok * d; idx += blockDim.x) {
+    const int t = idx / d, i = idx - t * d;
+    const int r = i / g, ii = i - r * g;
+    const float* Gr = G.f32 + gauge_block(l, s, h, r, G.H, G.R) * g * g + size_t(ii) * g;
+    const float* xr = xs + t * dp + r * g;
+    float acc = 0.0f;
+    for (int j = 0; j < g; ++j) acc = fmaf(Gr[j], xr[j], acc);
+    zs[t * dp + i] = acc;
+  }
+}
+
+// xs[t][i] = sum_j G_{l,s,h,r}[j][i%g] zs[t][r*g + j] (inverse gauge, G^T).
+__device__ void inverse_tile(const float* zs, float* xs, int ntok, int d, int dp, const GaugeDev& G, int l, int s,
+                             int h) {
+  const int g = G.g;
+  for (int idx = threadIdx.x; idx < ntok * d; idx += blockDim.x) {
+    const int t = idx / d, i = idx - t * d;
+    const int r = i / g, ii = i - r * g;
+    const float* Gr = G.f32 + gauge_block(l, s, h, r, G.H, G.R) * g * g + ii;
+    const float* zr = zs + t * dp + r * g;
+    float acc = 0.0f;
+    for (int j = 0; j < g; ++j) acc = fmaf(Gr[size_t(j) * g], zr[j], acc);
+    xs[t * dp + i] = acc;
+  }
+}
+
+// Quantise n values (stride `stride` in LDS) as one block and write its packed stream and
+// side word.  n * bits is a multiple of 32.
+__device__ int quantize_block_to(const float* z, int stride, int n, int bits, uint32_t* dst, uint32_t* side_dst) {
+  float mn = z[0], mx = z[0];
+  for (int e = 1; e < n; ++e) {
+    mn = fminf(mn, z[e * stride]);
+    mx = fmaxf(mx, z[e * stride]);
+  }
+  Side sd = make_side(mn, mx, bits);
+  const float qmax = (float)((1 << bits) - 1);
+  uint64_t acc = 0;
+  int nbit = 0, wi = 0;
+  for (int e = 0; e < n; ++e) {
+    acc |= (uint64_t)quantize(z[e * stride], sd.mn, sd.inv, qmax) << nbit;
+    nbit += bits;
+    if (nbit >= 32) {
+      dst[wi++] = (uint32_t)acc;
+      acc >>= 32;
+      nbit -= 32;
+    }
+  }
+  *side_dst = sd.word;
+  return sd.flags;
+}
+
+// Block-uniform (or KIVI value) rows: tile rows t < ntok go to cache positions pos0 + t.
+__device__ int store_rows_blocks(const float* zs, int ntok, int d, int dp, int n, int bits, const CacheDev& k,
+                                 size_t slc, int pos0) {
+  int flags = 0;
+  const int nb = d / n, row_bytes = d * bits / 8, blk_bytes = n * bits / 8;
+  for (int w = threadIdx.x; w < ntok * nb; w += blockDim.x) {
+    const int t = w / nb, kb = w - t * nb;
+    const size_t row = slc * k.T_cap + pos0 + t;
+    uint32_t* dst = (uint32_t*)(k.codes + row * row_bytes + size_t(kb) * blk_bytes);
+    flags |= quantize_block_to(zs + t * dp + kb * n, 1, n, bits, dst, k.side + row * nb + kb);
+  }
+  return flags;
+}
+
+// KIVI key groups: tile rows [u*kg, u*kg + kg) form token group grp0 + u; one channel per
+// thread.
+__device__ int store_key_groups(const float* zs, int ngrp, int kg, int d, int dp, int bits, const CacheDev& k,
+                                size_t slc, int grp0) {
+  int flags = 0;
+  const int cb = kg * bits / 8;
+  for (int w = threadIdx.x; w < ngrp * d; w += blockDim.x) {
+    const int u = w / d, ch = w - u * d;
+    const size_t gi = slc * (k.T_cap / kg) + grp0 + u;
+    uint32_t* dst = (uint32_t*)(k.codes + (gi * d + ch) * cb);
+    flags |= quantize_block_to(zs + (u * kg) * dp + ch, dp, kg, bits, dst, k.side + gi * d + ch);
+  }
+  return flags;
+}
+
+__device__ void store_rows_pass(const float* zs, int ntok, int d, int dp, const CacheDev& k, size_t slc, int pos0) {
+  float* out = (float*)k.codes;
+  for (int idx = threadIdx.x; idx < ntok * d; idx += blockDim.x) {
+    const int t = idx / d, ch = idx - t * d;
+    out[(slc * k.T_cap + pos0 + t) * d + ch] = zs[t * dp + ch];
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// encode
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void enc_generic(int s, ViewDev X, int l0, GaugeDev G, CodecDev c, CacheDev k,
+                                                        int t0, int tq, int TT, int* err) {
+  extern __shared__ float sm[];
+  const int d = X.d, dp = d + 1;
+  float* xs = sm;
+  float* zs = sm + TT * dp;
+  const int sv = blockIdx.y;
+  const int h = sv % X.H, b = (sv / X.H) % X.B, lv = sv / (X.H * X.B);
+  const int l = lv + l0;
+  const int tile0 = blockIdx.x * TT;
+  const int ntok = min(TT, X.T - tile0);
+  const size_t slc = (size_t(l) * k.B + b) * k.H + h;
+  const size_t xbase = size_t(lv) * X.sl + size_t(b) * X.sb + size_t(h) * X.sh;
+
+  if (c.backend == CG_BACKEND_KIVI && tile0 >= tq) {
+    // full-precision window: raw bf16 rows into the ring
+    const int ringsz = c.win + c.kg;
+    for (int idx = threadIdx.x; idx < ntok * d; idx += blockDim.x) {
+      const int t = idx / d, ch = idx - t * d;
+      const int tok = tile0 + t;
+      k.ring[(slc * ringsz + tok % ringsz) * d + ch] = ((const uint16_t*)X.ptr)[xbase + size_t(tok) * X.st + ch];
+    }
+    return;
+  }
+
+  int flags = 0;
+  for (int idx = threadIdx.x; idx < TT * d; idx += blockDim.x) {
+    const int t = idx / d, ch = idx - t * d;
+    float v = 0.0f;
+    if (t < ntok) {
+      v = load_x(X, xbase + size_t(tile0 + t) * X.st + ch);
+      if (!isfinite(v)) flags |= CG_FLAG_NONFINITE;
+    }
+    xs[t * dp + ch] = v;
+  }
+  __syncthreads();
+  gauge_tile(xs, zs, ntok, d, dp, G, l, s, h);
+  __syncthreads();
+
+  if (c.backend == CG_BACKEND_PASSTHROUGH) {
+    store_rows_pass(zs, ntok, d, dp, k, slc, t0 + tile0);
+  } else if (c.backend == CG_BACKEND_BLOCK_UNIFORM) {
+    flags |= store_rows_blocks(zs, ntok, d, dp, c.n, c.bits, k, slc, t0 + tile0);
+  } else if (s == 1) {
+    flags |= store_rows_blocks(zs, ntok, d, dp, c.kvc, c.bits, k, slc, tile0);
+  } else {
+    flags |= store_key_groups(zs, ntok / c.kg, c.kg, d, dp, c.bits, k, slc, tile0 / c.kg);
+  }
+  if (flags && err) atomicOr(err, flags);
+}
+
+// ------------------------------------------------------------------------------------------
+// decode
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void dec_generic(int s, CacheDev k, int l0, GaugeDev G, CodecDev c, int t0,
+                                                        int len, const int* pos, ViewDev Y, int TT, int* err) {
+  extern __shared__ float sm[];
+  const int d = Y.d, dp = d + 1;
+  float* zs = sm;
+  float* xs = sm + TT * dp;
+  const int sv = blockIdx.y;
+  const int h = sv % Y.H, b = (sv / Y.H) % Y.B, lv = sv / (Y.H * Y.B);
+  const int l = lv + l0;
+  const int tile0 = blockIdx.x * TT;
+  int ntok = min(TT, Y.T - tile0);
+  const size_t slc = (size_t(l) * k.B + b) * k.H + h;
+  const size_t ybase = size_t(lv) * Y.sl + size_t(b) * Y.sb + size_t(h) * Y.sh;
+
+  // Positions the cache holds bound the rows written: pos[b] + 1 in a rolling step, `len` for
+  // a KIVI cache, otherwise every requested position (the host checked the capacity).
+  const bool kivi = c.backend == CG_BACKEND_KIVI;
+  int held = INT_MAX;
+  if (pos) {
+    const int p = pos[b];
+    if (p < 0 || p >= k.T_cap) return;  // flagged by the append kernel
+    held = p + 1;
+  } else if (kivi) {
+    held = len;
+  }
+  const int p0 = t0 + tile0;  // cache position of tile row 0
+  if (held != INT_MAX) ntok = min(ntok, held - p0);
+  if (ntok <= 0) return;
+  // KIVI quantises the first T_q positions and keeps the rest in the window; the other
+  // backends quantise every position.
+  const int tq = kivi ? (held < c.win ? 0 : ((held - c.win) / c.kg) * c.kg) : INT_MAX;
+  const int nq = max(0, min(ntok, tq - p0));  // quantised rows of this tile
+
+  // 1. dequantise the quantised rows into zs
+  const int bits = c.bits;
+  for (int idx = threadIdx.x; idx < nq * d; idx += blockDim.x) {
+    const int t = idx / d, ch = idx - t * d;
+    const int p = p0 + t;
+    float zv;
+    if (c.backend == CG_BACKEND_PASSTHROUGH) {
+      zv = ((const float*)k.codes)[(slc * k.T_cap + p) * d + ch];
+    } else if (c.backend == CG_BACKEND_BLOCK_UNIFORM || s == 1) {
+      const int n = c.backend == CG_BACKEND_BLOCK_UNIFORM ? c.n : c.kvc;
+      const int nb = d / n, kb = ch / n;
+      const size_t row = slc * k.T_cap + p;
+      const uint32_t* stream = (const uint32_t*)(k.codes + row * (d * bits / 8) + size_t(kb) * (n * bits / 8));
+      const uint32_t q = extract_code(stream, ch - kb * n, bits);
+      const uint32_t sw = k.side[row * nb + kb];
+      zv = dequantize(q, f16_bits_to_f32(sw & 0xffffu), f16_bits_to_f32(sw >> 16));
+    } else {
+      const int kg = c.kg;
+      const size_t gi = slc * (k.T_cap / kg) + p / kg;
+      const uint32_t* stream = (const uint32_t*)(k.codes + (gi * d + ch) * (kg * bits / 8));
+      const uint32_t q = extract_code(stream, p % kg, bits);
+      const uint32_t sw = k.side[gi * d + ch];
+      zv = dequantize(q, f16_bits_to_f32(sw & 0xffffu), f16_bits_to_f32(sw >> 16));
+    }
+    zs[t * dp + ch] = zv;
+  }
+  __syncthreads();
+  // 2. inverse gauge
+  inverse_tile(zs, xs, nq, d, dp, G, l, s, h);
+  __syncthreads();
+  // 3. write rows: inverse-gauged rows, then window rows copied raw
+  const int ringsz = c.win + c.kg;
+  for (int idx = threadIdx.x; idx < ntok * d; idx += blockDim.x) {
+    const int t = idx / d, ch = idx - t * d;
+    const size_t off = ybase + size_t(tile0 + t) * Y.st + ch;
+    if (t < nq) {
+      const float v = xs[t * dp + ch];
+      if (Y.bf16) ((uint16_t*)Y.ptr)[off] = (uint16_t)f32_to_bf16_rne(v);
+      else ((float*)Y.ptr)[off] = v;
+    } else if (kivi) {
+      const uint16_t raw = k.ring[(slc * ringsz + (p0 + t) % ringsz) * d + ch];
+      if (Y.bf16) ((uint16_t*)Y.ptr)[off] = raw;
+      else ((float*)Y.ptr)[off] = bf16_to_f32(raw);
+    }
+  }
+  (void)err;
+}
+
+// ------------------------------------------------------------------------------------------
+// rolling append: one workgroup per (layer, b, h)
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void append_generic(int s, ViewDev Xn, int l0, const int* pos, GaugeDev G,
+                                                           CodecDev c, CacheDev k, int* err) {
+  extern __shared__ float sm[];
+  const int d = Xn.d, dp = d + 1;
+  const int sv = blockIdx.x;
+  const int h = sv % Xn.H, b = (sv / Xn.H) % Xn.B, lv = sv / (Xn.H * Xn.B);
+  const int l = lv + l0;
+  const size_t slc = (size_t(l) * k.B + b) * k.H + h;
+  const size_t xbase = size_t(lv) * Xn.sl + size_t(b) * Xn.sb + size_t(h) * Xn.sh;
+  const int p = pos[b];
+  if (p < 0 || p >= k.T_cap) {
+    if (threadIdx.x == 0 && err) atomicOr(err, CG_FLAG_POS_RANGE);
+    return;
+  }
+  int flags = 0;
+  if (c.backend == CG_BACKEND_KIVI) {
+    const int ringsz = c.win + c.kg;
+    const uint16_t* src = (const uint16_t*)Xn.ptr + xbase;
+    for (int ch = threadIdx.x; ch < d; ch += blockDim.x) k.ring[(slc * ringsz + p % ringsz) * d + ch] = src[ch];
+    const int T = p + 1;
+    if (!(T - c.win >= c.kg && (T - c.win) % c.kg == 0)) return;
+    __syncthreads();
+    // flush the kg oldest window tokens [T - W - kg, T - W)
+    const int tb = T - c.win - c.kg;
+    float* xs = sm;
+    float* zs = sm + c.kg * dp;
+    for (int idx = threadIdx.x; idx < c.kg * d; idx += blockDim.x) {
+      const int t = idx / d, ch = idx - t * d;
+      xs[t * dp + ch] = bf16_to_f32(k.ring[(slc * ringsz + (tb + t) % ringsz) * d + ch]);
+    }
+    __syncthreads();
+    gauge_tile(xs, zs, c.kg, d, dp, G, l, s, h);
+    __syncthreads();
+    if (s == 0) flags |= store_key_groups(zs, 1, c.kg, d, dp, c.bits, k, slc, tb / c.kg);
+    else flags |= store_rows_blocks(zs, c.kg, d, dp, c.kvc, c.bits, k, slc, tb);
+  } else {
+    float* xs = sm;
+    float* zs = sm + dp;
+    for (int ch = threadIdx.x; ch < d; ch += blockDim.x) {
+      const float v = load_x(Xn, xbase + ch);
+      if (!isfinite(v)) flags |= CG_FLAG_NONFINITE;
+      xs[ch] = v;
+    }
+    __syncthreads();
+    gauge_tile(xs, zs, 1, d, dp, G, l, s, h);
+    __syncthreads();
+    if (c.backend == CG_BACKEND_PASSTHROUGH) store_rows_pass(zs, 1, d, dp, k, slc, p);
+    else flags |= store_rows_blocks(zs, 1, d, dp, c.n, c.bits, k, slc, p);
+  }
+  if (flags && err) atomicOr(err, flags);
+}
+
+// KIVI tiles are exactly one key token group, so the quantised / window split (a multiple of
+// the group) never cuts a tile.
+int tile_tokens(const CodecDev& c) { return c.backend == CG_BACKEND_KIVI ? c.kg : 32; }
+
+hipError_t set_smem(const void* fn, size_t bytes) {
+  if (bytes <= 65536) return hipSuccess;
+  return hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+
+}  // namespace
+
+hipError_t launch_encode_generic(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c,
+                                 const CacheDev& k, int t0, int tq, int* err, hipStream_t st) {
+  if (X.T == 0) return hipSuccess;
+  const int TT = tile_tokens(c);
+  const size_t smem = size_t(2) * TT * (X.d + 1) * sizeof(float);
+  hipError_t e = set_smem((const void*)enc_generic, smem);
+  if (e != hipSuccess) return e;
+  dim3 grid((X.T + TT - 1) / TT, X.L * X.B * X.H);
+  hipLaunchKernelGGL(enc_generic, grid, dim3(kThreads), smem, st, s, X, l0, G, c, k, t0, tq, TT, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_generic(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
+                                 int len, const int* pos, const ViewDev& Y, int* err, hipStream_t st) {
+  if (Y.T == 0) return hipSuccess;
+  const int TT = tile_tokens(c);
+  const size_t smem = size_t(2) * TT * (Y.d + 1) * sizeof(float);
+  hipError_t e = set_smem((const void*)dec_generic, smem);
+  if (e != hipSuccess) return e;
+  dim3 grid((Y.T + TT - 1) / TT, Y.L * Y.B * Y.H);
+  hipLaunchKernelGGL(dec_generic, grid, dim3(kThreads), smem, st, s, k, l0, G, c, t0, len, pos, Y, TT, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_append(int s, const ViewDev& Xn, int l0, const int* pos, const GaugeDev& G, const CodecDev& c,
+                         const CacheDev& k, int* err, hipStream_t st) {
+  const int rows = c.backend == CG_BACKEND_KIVI ? c.kg : 1;
+  const size_t smem = size_t(2) * rows * (Xn.d + 1) * sizeof(float);
+  hipError_t e = set_smem((const void*)append_generic, smem);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(append_generic, dim3(Xn.L * Xn.B * Xn.H), dim3(kThreads), smem, st, s, Xn, l0, pos, G, c, k,
+                     err);
+  return hipGetLastError();
+}
+
+}  // namespace cg

@@ -1,0 +1,548 @@
+// Host side of the C ABI: argument validation, gauge construction (gauge_make), buffer
+// sizing and dispatch of the encode / decode / rolling-append kernels.
+#include <math.h>
+#include <string.h>
+
+#include <vector>
+
+#include "cg_internal.h"
+
+using namespace cg;
+
+namespace {
+
+// ------------------------------------------------------------------------------------------
+// gauge construction on the host, binary64
+// ------------------------------------------------------------------------------------------
+
+// Philox4x32-10 block function (Salmon et al., SC 2011).
+void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+  const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u, W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+  for (int i = 0; i < 10; ++i) {
+    const uint64_t a = uint64_t(M0) * c[0], b = uint64_t(M1) * c[2];
+    const uint32_t x0 = uint32_t(b >> 32) ^ c[1] ^ k0;
+    const uint32_t x2 = uint32_t(a >> 32) ^ c[3] ^ k1;
+    c[1] = uint32_t(b);
+    c[3] = uint32_t(a);
+    c[0] = x0;
+    c[2] = x2;
+    k0 += W0;
+    k1 += W1;
+  }
+}
+
+// g*g standard normals of stream `index`: counter (block, 0, index_lo, index_hi), key = seed;
+// each Philox output (w0..w3) yields two Box-Muller pairs (w0, w1), (w2, w3) with
+// u1 = (w + 1) 2^-32, u2 = w 2^-32, giving r cos(2 pi u2), r sin(2 pi u2).
+void normals(uint64_t seed, uint64_t index, size_t count, double* out) {
+  const double two32 = 4294967296.0;
+  for (size_t blk = 0; blk * 4 < count; ++blk) {
+    uint32_t c[4] = {uint32_t(blk), 0u, uint32_t(index), uint32_t(index >> 32)};
+    philox4x32_10(c, uint32_t(seed), uint32_t(seed >> 32));
+    for (int pr = 0; pr < 2; ++pr) {
+      const double u1 = (double(c[2 * pr]) + 1.0) / two32;
+      const double u2 = double(c[2 * pr + 1]) / two32;
+      const double rad = sqrt(-2.0 * log(u1)), th = 2.0 * M_PI * u2;
+      const size_t k = blk * 4 + 2 * pr;
+      if (k < count) out[k] = rad * cos(th);
+      if (k + 1 < count) out[k + 1] = rad * sin(th);
+    }
+  }
+}
+
+// Haar orthogonal matrix: Householder QR of the normal matrix M (row-major, M[i][j] = normal
+// i*g + j), Q accumulated explicitly, columns multiplied by sign(R_jj) (Mezzadri 2007).
+void haar(int g, uint64_t seed, uint64_t index, double* Q) {
+  std::vector<double> A(size_t(g) * g), V(size_t(g) * g, 0.0), diag(g);
+  normals(seed, index, A.size(), A.data());
+  for (int k = 0; k < g; ++k) {
+    double nrm = 0.0;
+    for (int i = k; i < g; ++i) nrm += A[i * g + k] * A[i * g + k];
+    nrm = sqrt(nrm);
+    const double alpha = A[k * g + k] > 0 ? -nrm : nrm;  // R_kk
+    double* v = &V[size_t(k) * g];
+    for (int i = 0; i < g; ++i) v[i] = i < k ? 0.0 : A[i * g + k];
+    v[k] -= alpha;
+    double vv = 0.0;
+    for (int i = k; i < g; ++i) vv += v[i] * v[i];
+    diag[k] = alpha;
+    if (vv == 0.0) continue;
+    for (int j = k; j < g; ++j) {  // A <- (I - 2 v v^T / v^T v) A
+      double dot = 0.0;
+      for (int i = k; i < g; ++i) dot += v[i] * A[i * g + j];
+      const double f = 2.0 * dot / vv;
+      for (int i = k; i < g; ++i) A[i * g + j] -= f * v[i];
+    }
+  }
+  // Q = H_0 H_1 ... H_{g-1} applied to the identity, right to left
+  for (int i = 0; i < g; ++i)
+    for (int j = 0; j < g; ++j) Q[i * g + j] = i == j ? 1.0 : 0.0;
+  for (int k = g - 1; k >= 0; --k) {
+    const double* v = &V[size_t(k) * g];
+    double vv = 0.0;
+    for (int i = k; i < g; ++i) vv += v[i] * v[i];
+    if (vv == 0.0) continue;
+    for (int j = 0; j < g; ++j) {
+      double dot = 0.0;
+      for (int i = k; i < g; ++i) dot += v[i] * Q[i * g + j];
+      const double f = 2.0 * dot / vv;
+      for (int i = k; i < g; ++i) Q[i * g + j] -= f * v[i];
+    }
+  }
+  for (int j = 0; j < g; ++j)
+    if (diag[j] < 0)
+      for (int i = 0; i < g; ++i) Q[i * g + j] = -Q[i * g + j];
+}
+
+void dct2(int g, double* Q) {
+  for (int k = 0; k < g; ++k) {
+    const double a = k == 0 ? sqrt(1.0 / g) : sqrt(2.0 / g);
+    for (int n = 0; n < g; ++n) Q[k * g + n] = a * cos(M_PI * (n + 0.5) * k / g);
+  }
+}
+
+// Sylvester construction: H_1 = [1], H_2m = [[H_m, H_m], [H_m, -H_m]], normalised by sqrt(g).
+void hadamard(int g, double* Q) {
+  Q[0] = 1.0;
+  for (int m = 1; m < g; m *= 2)
+    for (int i = 0; i < m; ++i)
+      for (int j = 0; j < m; ++j) {
+        const double v = Q[i * g + j];
+        Q[i * g + j + m] = v;
+        Q[(i + m) * g + j] = v;
+        Q[(i + m) * g + j + m] = -v;
+      }
+  const double s = 1.0 / sqrt(double(g));
+  for (size_t k = 0; k < size_t(g) * g; ++k) Q[k] *= s;
+}
+
+void matmul(int g, const double* A, const double* B, double* C) {
+  for (int i = 0; i < g; ++i)
+    for (int j = 0; j < g; ++j) {
+      double acc = 0.0;
+      for (int k = 0; k < g; ++k) acc += A[i * g + k] * B[k * g + j];
+      C[i * g + j] = acc;
+    }
+}
+
+// exp(A - A^T) by scaling and squaring with the diagonal Pade(8,8) approximant; the
+// denominator system is solved by Gaussian elimination with partial pivoting.
+void expm_skew(int g, const float* A, double* Q) {
+  const size_t gg = size_t(g) * g;
+  std::vector<double> S(gg), P(gg), N(gg), D(gg), T(gg), T2(gg);
+  double nrm = 0.0;
+  for (int i = 0; i < g; ++i) {
+    double row = 0.0;
+    for (int j = 0; j < g; ++j) {
+      S[i * g + j] = double(A[i * g + j]) - double(A[j * g + i]);
+      row += fabs(S[i * g + j]);
+    }
+    nrm = row > nrm ? row : nrm;
+  }
+  int sq = 0;
+  while (nrm > 0.25) {
+    nrm *= 0.5;
+    ++sq;
+  }
+  for (auto& v : S) v = ldexp(v, -sq);
+  // Pade(8,8) coefficients c_k = (16-k)! 8! / (16! k! (8-k)!)
+  double c[9];
+  c[0] = 1.0;
+  for (int k = 1; k <= 8; ++k) c[k] = c[k - 1] * double(8 - k + 1) / double(k * (16 - k + 1));
+  for (size_t i = 0; i < gg; ++i) {
+    N[i] = 0.0;
+    D[i] = 0.0;
+    P[i] = (i / g == i % g) ? 1.0 : 0.0;  // S^0
+  }
+  for (int k = 0; k <= 8; ++k) {
+    const double sgn = (k & 1) ? -1.0 : 1.0;
+    for (size_t i = 0; i < gg; ++i) {
+      N[i] += c[k] * P[i];
+      D[i] += sgn * c[k] * P[i];
+    }
+    matmul(g, P.data(), S.data(), T.data());
+    P.swap(T);
+  }
+  // solve D Q = N
+  std::vector<double> Mx(D), R(N);
+  for (int col = 0; col < g; ++col) {
+    int piv = col;
+    for (int i = col + 1; i < g; ++i)
+      if (fabs(Mx[i * g + col]) > fabs(Mx[piv * g + col])) piv = i;
+    if (piv != col)
+      for (int j = 0; j < g; ++j) {
+        std::swap(Mx[col * g + j], Mx[piv * g + j]);
+        std::swap(R[col * g + j], R[piv * g + j]);
+      }
+    for (int i = col + 1; i < g; ++i) {
+      const double f = Mx[i * g + col] / Mx[col * g + col];
+      if (f == 0.0) continue;
+      for (int j = col; j < g; ++j) Mx[i * g + j] -= f * Mx[col * g + j];
+      for (int j = 0; j < g; ++j) R[i * g + j] -= f * R[col * g + j];
+    }
+  }
+  for (int i = g - 1; i >= 0; --i)
+    for (int j = 0; j < g; ++j) {
+      double acc = R[i * g + j];
+      for (int k = i + 1; k < g; ++k) acc -= Mx[i * g + k] * Q[k * g + j];
+      Q[i * g + j] = acc / Mx[i * g + i];
+    }
+  for (int s = 0; s < sq; ++s) {
+    matmul(g, Q, Q, T2.data());
+    memcpy(Q, T2.data(), gg * sizeof(double));
+  }
+}
+
+double orth_error(int g, const float* G) {
+  double worst = 0.0;
+  for (int i = 0; i < g; ++i)
+    for (int j = 0; j < g; ++j) {
+      double acc = 0.0;
+      for (int k = 0; k < g; ++k) acc += double(G[i * g + k]) * double(G[j * g + k]);
+      const double e = fabs(acc - (i == j ? 1.0 : 0.0));
+      worst = e > worst ? e : worst;
+    }
+  return worst;
+}
+
+uint16_t bf16_rne(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return uint16_t(u >> 16);
+}
+float bf16_val(uint16_t h) {
+  const uint32_t u = uint32_t(h) << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+// ------------------------------------------------------------------------------------------
+// validation helpers
+// ------------------------------------------------------------------------------------------
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool bits_ok(int b) { return b == 2 || b == 3 || b == 4 || b == 6 || b == 8; }
+
+int32_t check_shape(const cg_gauge_shape& s) {
+  if (s.L <= 0 || s.H <= 0 || s.d <= 0 || s.g <= 0) return CG_ERR_ARG;
+  if (s.d % s.g || s.d > 256 || s.d % 8) return CG_ERR_UNSUPPORTED;
+  return CG_OK;
+}
+
+int32_t check_codec(const cg_codec* c, int d) {
+  if (!c) return CG_ERR_ARG;
+  switch (c->backend) {
+    case CG_BACKEND_PASSTHROUGH:
+      return CG_OK;
+    case CG_BACKEND_BLOCK_UNIFORM:
+      if (!bits_ok(c->bits) || c->block_c <= 0) return CG_ERR_UNSUPPORTED;
+      if (d % c->block_c || (c->block_c * c->bits) % 32 || c->block_c > 256) return CG_ERR_UNSUPPORTED;
+      return CG_OK;
+    case CG_BACKEND_KIVI:
+      if (!bits_ok(c->bits)) return CG_ERR_UNSUPPORTED;
+      if (c->key_tokens != 16 && c->key_tokens != 32 && c->key_tokens != 64) return CG_ERR_UNSUPPORTED;
+      if ((c->key_tokens * c->bits) % 32) return CG_ERR_UNSUPPORTED;
+      if (c->val_channels <= 0 || d % c->val_channels || (c->val_channels * c->bits) % 32) return CG_ERR_UNSUPPORTED;
+      if (c->residual < 0) return CG_ERR_ARG;
+      return CG_OK;
+    default:
+      return CG_ERR_ARG;
+  }
+}
+
+int32_t check_view(const cg_kv_view* v, const cg_gauge_shape& s, int L) {
+  if (!v || (!v->ptr && v->T != 0)) return CG_ERR_ARG;  // an empty view touches no memory
+  if (v->dtype != CG_DTYPE_BF16 && v->dtype != CG_DTYPE_F32) return CG_ERR_ARG;
+  if (v->L != L || v->H != s.H || v->d != s.d || v->B <= 0 || v->T < 0) return CG_ERR_SHAPE;
+  if (!aligned16(v->ptr)) return CG_ERR_ALIGN;
+  const int64_t unit = v->dtype == CG_DTYPE_BF16 ? 8 : 4;  // elements per 16 bytes
+  if (v->stride_l % unit || v->stride_b % unit || v->stride_h % unit || v->stride_t % unit) return CG_ERR_ALIGN;
+  if (v->stride_l < 0 || v->stride_b < 0 || v->stride_h < 0 || v->stride_t < 0) return CG_ERR_ARG;
+  return CG_OK;
+}
+
+int32_t check_cache(const cg_cache* k, const cg_codec* c, const cg_gauge_shape& s, int B) {
+  if (!k || !k->codes) return CG_ERR_ARG;
+  if (k->L != s.L || k->H != s.H || k->d != s.d || k->B != B || k->T_cap <= 0) return CG_ERR_SHAPE;
+  if (!aligned16(k->codes)) return CG_ERR_ALIGN;
+  if (c->backend != CG_BACKEND_PASSTHROUGH && (!k->side || !aligned16(k->side))) return CG_ERR_ARG;
+  if (c->backend == CG_BACKEND_KIVI) {
+    if (!k->residual || !aligned16(k->residual)) return CG_ERR_ARG;
+    if (k->T_cap % c->key_tokens) return CG_ERR_SHAPE;
+  }
+  return CG_OK;
+}
+
+GaugeDev gauge_dev(const void* G_dev, const cg_gauge_shape& s) {
+  const GaugeLayout gl = gauge_layout(s);
+  const char* base = static_cast<const char*>(G_dev);
+  GaugeDev G;
+  G.f32 = reinterpret_cast<const float*>(base + gl.off_f32);
+  for (int p = 0; p < 3; ++p) {
+    G.hi[p] = reinterpret_cast<const uint16_t*>(base + gl.off_hi[p]);
+    G.tr[p] = reinterpret_cast<const uint16_t*>(base + gl.off_tr[p]);
+  }
+  G.g = s.g;
+  G.R = s.d / s.g;
+  G.H = s.H;
+  return G;
+}
+
+CodecDev codec_dev(const cg_codec* c) {
+  CodecDev d;
+  d.backend = c->backend;
+  d.bits = c->bits;
+  d.n = c->block_c;
+  d.kg = c->key_tokens;
+  d.kvc = c->val_channels;
+  d.win = c->residual;
+  return d;
+}
+
+ViewDev view_dev(const cg_kv_view* v) {
+  ViewDev d;
+  d.ptr = v->ptr;
+  d.sl = v->stride_l;
+  d.sb = v->stride_b;
+  d.sh = v->stride_h;
+  d.st = v->stride_t;
+  d.L = v->L;
+  d.B = v->B;
+  d.H = v->H;
+  d.T = v->T;
+  d.d = v->d;
+  d.bf16 = v->dtype == CG_DTYPE_BF16;
+  return d;
+}
+
+CacheDev cache_dev(const cg_cache* k) {
+  CacheDev d;
+  d.codes = static_cast<uint8_t*>(k->codes);
+  d.side = static_cast<uint32_t*>(k->side);
+  d.ring = static_cast<uint16_t*>(k->residual);
+  d.L = k->L;
+  d.B = k->B;
+  d.H = k->H;
+  d.T_cap = k->T_cap;
+  d.d = k->d;
+  return d;
+}
+
+int kivi_tq(int T, const cg_codec* c) {
+  return T < c->residual ? 0 : ((T - c->residual) / c->key_tokens) * c->key_tokens;
+}
+
+}  // namespace
+
+namespace cg {
+
+hipError_t launch_encode(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c, const CacheDev& k,
+                         int t0, int tq, int* err, hipStream_t st) {
+  return launch_encode_generic(s, X, l0, G, c, k, t0, tq, err, st);
+}
+
+hipError_t launch_decode(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0, int len,
+                         const int* pos, const ViewDev& Y, int* err, hipStream_t st) {
+  return launch_decode_generic(s, k, l0, G, c, t0, len, pos, Y, err, st);
+}
+
+}  // namespace cg
+
+// ------------------------------------------------------------------------------------------
+// C ABI
+// ------------------------------------------------------------------------------------------
+
+extern "C" {
+
+const char* cg_status_str(int32_t status) {
+  switch (status) {
+    case CG_OK: return "ok";
+    case CG_ERR_ARG: return "invalid argument";
+    case CG_ERR_SHAPE: return "shape mismatch";
+    case CG_ERR_ALIGN: return "misaligned pointer or stride";
+    case CG_ERR_UNSUPPORTED: return "unsupported configuration";
+    case CG_ERR_NOT_ORTHOGONAL: return "gauge is not orthogonal";
+    case CG_ERR_CAPACITY: return "token range exceeds cache capacity";
+    case CG_ERR_DEVICE: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+size_t gauge_device_bytes(cg_gauge_shape shp) {
+  if (check_shape(shp) != CG_OK) return 0;
+  return gauge_layout(shp).total;
+}
+
+int32_t gauge_make(int32_t kind, cg_gauge_shape shp, uint64_t seed, const float* params, float* G_host, void* G_dev,
+                   void* stream) {
+  int32_t rc = check_shape(shp);
+  if (rc != CG_OK) return rc;
+  if (!G_host && !G_dev) return CG_ERR_ARG;
+  if (kind < CG_GAUGE_IDENTITY || kind > CG_GAUGE_USER) return CG_ERR_ARG;
+  if ((kind == CG_GAUGE_EXPM || kind == CG_GAUGE_USER) && !params) return CG_ERR_ARG;
+  const int g = shp.g, R = shp.d / shp.g;
+  if (kind == CG_GAUGE_HADAMARD && (g & (g - 1))) return CG_ERR_UNSUPPORTED;
+  if (G_dev && !aligned16(G_dev)) return CG_ERR_ALIGN;
+  const GaugeLayout gl = gauge_layout(shp);
+  const size_t gg = size_t(g) * g;
+  std::vector<float> G32(gl.nblk * gg);
+  std::vector<double> Q(gg);
+  for (int64_t blk = 0; blk < gl.nblk; ++blk) {
+    switch (kind) {
+      case CG_GAUGE_IDENTITY:
+        for (size_t i = 0; i < gg; ++i) Q[i] = (i / g == i % g) ? 1.0 : 0.0;
+        break;
+      case CG_GAUGE_HAAR: haar(g, seed, uint64_t(blk), Q.data()); break;
+      case CG_GAUGE_DCT2: dct2(g, Q.data()); break;
+      case CG_GAUGE_HADAMARD: hadamard(g, Q.data()); break;
+      case CG_GAUGE_EXPM: expm_skew(g, params + blk * gg, Q.data()); break;
+      case CG_GAUGE_USER:
+        for (size_t i = 0; i < gg; ++i) Q[i] = params[blk * gg + i];
+        break;
+    }
+    float* out = &G32[blk * gg];
+    for (size_t i = 0; i < gg; ++i) out[i] = float(Q[i]);
+    if (kind == CG_GAUGE_USER && orth_error(g, out) > 1e-5) return CG_ERR_NOT_ORTHOGONAL;
+  }
+  (void)R;
+  if (G_host) memcpy(G_host, G32.data(), G32.size() * sizeof(float));
+  if (G_dev) {
+    std::vector<unsigned char> buf(gl.total, 0);
+    memcpy(buf.data() + gl.off_f32, G32.data(), G32.size() * sizeof(float));
+    for (int64_t blk = 0; blk < gl.nblk; ++blk) {
+      const float* src = &G32[blk * gg];
+      for (int i = 0; i < g; ++i)
+        for (int j = 0; j < g; ++j) {
+          // split G[i][j] into three bf16 terms, and the transposed block likewise
+          float rem = src[i * g + j];
+          for (int p = 0; p < 3; ++p) {
+            const uint16_t hb = bf16_rne(rem);
+            reinterpret_cast<uint16_t*>(buf.data() + gl.off_hi[p])[blk * gg + size_t(i) * g + j] = hb;
+            reinterpret_cast<uint16_t*>(buf.data() + gl.off_tr[p])[blk * gg + size_t(j) * g + i] = hb;
+            rem = rem - bf16_val(hb);  // exact in binary32
+          }
+        }
+    }
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (hipMemcpyAsync(G_dev, buf.data(), buf.size(), hipMemcpyHostToDevice, st) != hipSuccess)
+      return CG_ERR_DEVICE;
+    if (hipStreamSynchronize(st) != hipSuccess) return CG_ERR_DEVICE;
+  }
+  return CG_OK;
+}
+
+int32_t cache_bytes(const cg_codec* codec, int32_t s, int32_t L, int32_t B, int32_t H, int32_t T_cap, int32_t d,
+                    size_t* codes, size_t* side, size_t* residual) {
+  if (!codec || s < 0 || s > 1 || L <= 0 || B <= 0 || H <= 0 || T_cap <= 0 || d <= 0 || d % 8) return CG_ERR_ARG;
+  int32_t rc = check_codec(codec, d);
+  if (rc != CG_OK) return rc;
+  const size_t slices = size_t(L) * B * H;
+  size_t c = 0, sd = 0, r = 0;
+  const int b = codec->bits;
+  switch (codec->backend) {
+    case CG_BACKEND_PASSTHROUGH: c = slices * T_cap * d * 4; break;
+    case CG_BACKEND_BLOCK_UNIFORM:
+      c = slices * T_cap * (size_t(d) * b / 8);
+      sd = slices * T_cap * (d / codec->block_c) * 4;
+      break;
+    case CG_BACKEND_KIVI: {
+      if (T_cap % codec->key_tokens) return CG_ERR_SHAPE;
+      const int kg = codec->key_tokens;
+      if (s == 0) {
+        c = slices * (T_cap / kg) * d * (size_t(kg) * b / 8);
+        sd = slices * (T_cap / kg) * d * 4;
+      } else {
+        c = slices * T_cap * (size_t(d) * b / 8);
+        sd = slices * T_cap * (d / codec->val_channels) * 4;
+      }
+      r = slices * size_t(codec->residual + kg) * d * 2;
+      break;
+    }
+  }
+  if (codes) *codes = c;
+  if (side) *side = sd;
+  if (residual) *residual = r;
+  return CG_OK;
+}
+
+int32_t kv_encode(int32_t s, const cg_kv_view* X, const void* G_dev, cg_gauge_shape shp, const cg_codec* codec,
+                  const cg_cache* out, int32_t t0, int32_t* err_flag, void* stream) {
+  int32_t rc = check_shape(shp);
+  if (rc != CG_OK) return rc;
+  if (s < 0 || s > 1 || !G_dev) return CG_ERR_ARG;
+  if (!aligned16(G_dev)) return CG_ERR_ALIGN;
+  if ((rc = check_codec(codec, shp.d)) != CG_OK) return rc;
+  if ((rc = check_view(X, shp, shp.L)) != CG_OK) return rc;
+  if ((rc = check_cache(out, codec, shp, X->B)) != CG_OK) return rc;
+  if (t0 < 0) return CG_ERR_ARG;
+  if (int64_t(t0) + X->T > out->T_cap) return CG_ERR_CAPACITY;
+  int tq = 0;
+  if (codec->backend == CG_BACKEND_KIVI) {
+    if (t0 != 0 || X->dtype != CG_DTYPE_BF16) return CG_ERR_UNSUPPORTED;
+    tq = kivi_tq(X->T, codec);
+  }
+  if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
+  hipError_t e = launch_encode(s, view_dev(X), 0, gauge_dev(G_dev, shp), codec_dev(codec), cache_dev(out), t0, tq,
+                               err_flag, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
+}
+
+int32_t kv_decode(int32_t s, const cg_cache* in, const void* G_dev, cg_gauge_shape shp, const cg_codec* codec,
+                  int32_t t0, const cg_kv_view* Xhat, int32_t* err_flag, void* stream) {
+  int32_t rc = check_shape(shp);
+  if (rc != CG_OK) return rc;
+  if (s < 0 || s > 1 || !G_dev) return CG_ERR_ARG;
+  if (!aligned16(G_dev)) return CG_ERR_ALIGN;
+  if ((rc = check_codec(codec, shp.d)) != CG_OK) return rc;
+  if ((rc = check_view(Xhat, shp, shp.L)) != CG_OK) return rc;
+  if ((rc = check_cache(in, codec, shp, Xhat->B)) != CG_OK) return rc;
+  if (t0 < 0) return CG_ERR_ARG;
+  if (int64_t(t0) + Xhat->T > in->T_cap) return CG_ERR_CAPACITY;
+  if (codec->backend == CG_BACKEND_KIVI && (in->len < 0 || in->len > in->T_cap || int64_t(t0) + Xhat->T > in->len))
+    return CG_ERR_CAPACITY;
+  if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
+  hipError_t e = launch_decode(s, cache_dev(in), 0, gauge_dev(G_dev, shp), codec_dev(codec), t0, in->len, nullptr,
+                               view_dev(Xhat), err_flag, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
+}
+
+int32_t kv_append_step(int32_t l0, int32_t l1, const cg_kv_view* k_new, const cg_kv_view* v_new, const int32_t* pos,
+                       const void* G_dev, cg_gauge_shape shp, const cg_codec* codec, const cg_cache* kc,
+                       const cg_cache* vc, const cg_kv_view* k_hist, const cg_kv_view* v_hist, int32_t* err_flag,
+                       void* stream) {
+  int32_t rc = check_shape(shp);
+  if (rc != CG_OK) return rc;
+  if (!G_dev || !pos || l0 < 0 || l1 <= l0 || l1 > shp.L) return CG_ERR_ARG;
+  if (!aligned16(G_dev)) return CG_ERR_ALIGN;
+  if ((reinterpret_cast<uintptr_t>(pos) & 3u)) return CG_ERR_ALIGN;
+  if ((rc = check_codec(codec, shp.d)) != CG_OK) return rc;
+  const int nl = l1 - l0;
+  if ((rc = check_view(k_new, shp, nl)) != CG_OK) return rc;
+  if ((rc = check_view(v_new, shp, nl)) != CG_OK) return rc;
+  if (k_new->T != 1 || v_new->T != 1 || v_new->B != k_new->B) return CG_ERR_SHAPE;
+  if (codec->backend == CG_BACKEND_KIVI && (k_new->dtype != CG_DTYPE_BF16 || v_new->dtype != CG_DTYPE_BF16))
+    return CG_ERR_UNSUPPORTED;
+  const int B = k_new->B;
+  if ((rc = check_cache(kc, codec, shp, B)) != CG_OK) return rc;
+  if ((rc = check_cache(vc, codec, shp, B)) != CG_OK) return rc;
+  if (k_hist && (rc = check_view(k_hist, shp, nl)) != CG_OK) return rc;
+  if (v_hist && (rc = check_view(v_hist, shp, nl)) != CG_OK) return rc;
+  if ((k_hist && k_hist->B != B) || (v_hist && v_hist->B != B)) return CG_ERR_SHAPE;
+  if ((k_hist && k_hist->T > kc->T_cap) || (v_hist && v_hist->T > vc->T_cap)) return CG_ERR_CAPACITY;
+  if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const GaugeDev G = gauge_dev(G_dev, shp);
+  const CodecDev c = codec_dev(codec);
+  hipError_t e = launch_append(0, view_dev(k_new), l0, pos, G, c, cache_dev(kc), err_flag, st);
+  if (e == hipSuccess) e = launch_append(1, view_dev(v_new), l0, pos, G, c, cache_dev(vc), err_flag, st);
+  if (e == hipSuccess && k_hist)
+    e = launch_decode(0, cache_dev(kc), l0, G, c, 0, 0, pos, view_dev(k_hist), err_flag, st);
+  if (e == hipSuccess && v_hist)
+    e = launch_decode(1, cache_dev(vc), l0, G, c, 0, 0, pos, view_dev(v_hist), err_flag, st);
+  return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
+}
+
+}  // extern "C"

@@ -1,0 +1,96 @@
+// Internal declarations shared by the host entry points and the kernel translation units of
+// the gauge-coded KV codec library.  Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "codec_gauge.h"
+
+namespace cg {
+
+// Device gauge buffer (filled by gauge_make):
+//   f32  : G            [nblk][g][g] binary32, nblk = L*2*H*R, block ((l*2+s)*H+h)*R+r
+//   hi[p]: split planes of G,   bf16 [nblk][g][g], G ~= hi[0] + hi[1] + hi[2]
+//   tr[p]: split planes of G^T, bf16 [nblk][g][g] (block transposed)
+// Every section starts on a 256-byte boundary.
+struct GaugeLayout {
+  int64_t nblk = 0;
+  int g = 0;
+  size_t off_f32 = 0, off_hi[3] = {0, 0, 0}, off_tr[3] = {0, 0, 0}, total = 0;
+};
+
+inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+inline GaugeLayout gauge_layout(const cg_gauge_shape& s) {
+  GaugeLayout gl;
+  if (s.L <= 0 || s.H <= 0 || s.d <= 0 || s.g <= 0 || s.d % s.g) return gl;
+  gl.g = s.g;
+  gl.nblk = int64_t(s.L) * 2 * s.H * (s.d / s.g);
+  size_t gg = size_t(s.g) * s.g;
+  size_t off = 0;
+  gl.off_f32 = off;
+  off = align256(off + gl.nblk * gg * 4);
+  for (int p = 0; p < 3; ++p) {
+    gl.off_hi[p] = off;
+    off = align256(off + gl.nblk * gg * 2);
+  }
+  for (int p = 0; p < 3; ++p) {
+    gl.off_tr[p] = off;
+    off = align256(off + gl.nblk * gg * 2);
+  }
+  gl.total = off;
+  return gl;
+}
+
+// Kernel-side description of the gauge buffer.
+struct GaugeDev {
+  const float* f32;
+  const uint16_t* hi[3];
+  const uint16_t* tr[3];
+  int g, R, H;
+};
+
+// Codec parameters as the kernels see them.
+struct CodecDev {
+  int backend, bits, n, kg, kvc, win;
+};
+
+// A strided KV tensor view [L][B][H][T][d] (element strides, channel stride 1).
+struct ViewDev {
+  void* ptr;
+  int64_t sl, sb, sh, st;
+  int L, B, H, T, d;
+  int bf16;
+};
+
+// A compressed cache of one type s.
+struct CacheDev {
+  uint8_t* codes;
+  uint32_t* side;      // one 32-bit word (min | scale << 16) per block
+  uint16_t* ring;      // KIVI window
+  int L, B, H, T_cap, d;
+};
+
+// Generic (VALU) kernels: every supported configuration.
+hipError_t launch_encode_generic(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c,
+                                 const CacheDev& k, int t0, int tq, int* err, hipStream_t st);
+hipError_t launch_decode_generic(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
+                                 int len, const int* pos, const ViewDev& Y, int* err, hipStream_t st);
+
+// Dispatching launchers (hip stream passed through).  All validate nothing: the host entry points do.
+// Encode tokens [0, X.T) of view X into cache positions [t0, t0 + X.T); layer l of the view is
+// cache layer l + l0.  tq: KIVI tokens to quantise (others go to the window).
+hipError_t launch_encode(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c, const CacheDev& k,
+                         int t0, int tq, int* err, hipStream_t st);
+// Decode cache positions [t0, t0 + Y.T) into view Y (layer l of Y is cache layer l + l0).
+// If pos is non-NULL, batch row b holds pos[b] + 1 tokens and only positions <= pos[b] are
+// written; otherwise the cache holds `len` tokens (KIVI window split).
+hipError_t launch_decode(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0, int len,
+                         const int* pos, const ViewDev& Y, int* err, hipStream_t st);
+// Rolling append of one token per (layer, b, h) at pos[b] (layer l of Xn is cache layer l + l0).
+hipError_t launch_append(int s, const ViewDev& Xn, int l0, const int* pos, const GaugeDev& G, const CodecDev& c,
+                         const CacheDev& k, int* err, hipStream_t st);
+
+}  // namespace cg

@@ -1,0 +1,144 @@
+"""Helpers of the GPU parity tests: moving caches between the oracle's numpy layout and the
+library's device buffers, unpacking codes, and the comparison criteria.
+
+Criteria (all against the CPU oracle on the same seeded inputs):
+  * gauge stage (passthrough backend): per group ||dz||_2 <= 1e-5 ||x||_2;
+  * quantise-only (identity gauge on binary32 input, so z = x exactly): codes, side
+    information and packed bytes bit-exact;
+  * fused encoder: side-info values within one binary16 ulp; at most 1e-4 of the codes
+    differ, each by exactly one step, and only where the oracle's z quantised with the GPU's
+    side information lies within 1e-3 of a rounding tie;
+  * decoder fed the oracle's cache: binary32 out per group ||dx||_2 <= 1e-5 ||x||_2, bf16 out
+    within one bf16 ulp of the oracle's binary32 value plus 1e-5 of the group norm (the
+    binary32 gauge tolerance, which dominates for elements tiny against their group).
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle as O
+from paper_2607_20538_amd import codec as cg
+
+GAUGE_TOL = 1e-5
+CODE_FRAC = 1e-4
+TIE_EPS = 1e-3
+
+
+def bf16_dev(bits: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def x_dev(X: np.ndarray) -> torch.Tensor:
+    return bf16_dev(X) if X.dtype == np.uint16 else torch.from_numpy(np.ascontiguousarray(X)).cuda()
+
+
+def x_f64(X: np.ndarray) -> np.ndarray:
+    if X.dtype == np.uint16:
+        return (X.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return X.astype(np.float64)
+
+
+def out_host(t: torch.Tensor) -> np.ndarray:
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
+
+
+def to_cg(oc: O.Codec) -> cg.Codec:
+    return cg.Codec(oc.backend, oc.bits, oc.block_c, oc.key_tokens, oc.val_channels, oc.residual)
+
+
+def cache_to_host(dev: cg.Cache, oc: O.Codec, s: int) -> dict:
+    lay = O.cache_layout(oc, s, dev.L, dev.B, dev.H, dev.T_cap, dev.d)
+    out = {}
+    for key, buf in (("codes", dev.codes), ("side", dev.side), ("residual", dev.residual)):
+        if lay[key] is None:
+            out[key] = None
+            continue
+        shp, dt = lay[key]
+        nbytes = int(np.prod(shp)) * np.dtype(dt).itemsize
+        out[key] = buf[:nbytes].cpu().numpy().view(dt).reshape(shp)
+    return out
+
+
+def cache_to_dev(host: dict, oc: O.Codec, s: int, L: int, B: int, H: int, T_cap: int, d: int, len_: int = 0):
+    dev = cg.Cache(to_cg(oc), s, L, B, H, T_cap, d)
+    for key in ("codes", "side", "residual"):
+        if host.get(key) is not None:
+            raw = torch.from_numpy(np.ascontiguousarray(host[key]).view(np.uint8).reshape(-1))
+            getattr(dev, key)[: raw.numel()].copy_(raw.cuda())
+    dev.len = len_
+    return dev
+
+
+def unpack_rows(codes: np.ndarray, count: int, bits: int) -> np.ndarray:
+    """LSB-first streams [..., count*bits/8] -> codes [..., count] (numpy's bit unpacking)."""
+    bitsarr = np.unpackbits(codes, axis=-1, bitorder="little").reshape(*codes.shape[:-1], count, bits)
+    return (bitsarr.astype(np.uint32) << np.arange(bits, dtype=np.uint32)).sum(axis=-1)
+
+
+def token_codes(cache: dict, oc: O.Codec, s: int, d: int) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Per-element codes [L][B][H][T][d] with the (min, scale) bits of their block."""
+    b = oc.bits
+    if oc.backend == O.KIVI and s == 0:
+        q = unpack_rows(cache["codes"], oc.key_tokens, b)           # [L,B,H,G,d,kg]
+        q = np.moveaxis(q, -1, -2)                                  # [L,B,H,G,kg,d]
+        q = q.reshape(*q.shape[:3], -1, d)
+        side = np.repeat(cache["side"], oc.key_tokens, axis=3)      # [L,B,H,G*kg,d,2]
+        return q, side[..., 0], side[..., 1]
+    n = oc.block_c if oc.backend == O.BLOCK_UNIFORM else oc.val_channels
+    q = unpack_rows(cache["codes"], d, b)
+    side = np.repeat(cache["side"], n, axis=-2)
+    return q, side[..., 0], side[..., 1]
+
+
+def f16(bits: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(bits).astype(np.uint16).view(np.float16).astype(np.float32)
+
+
+def check_fused_codes(gpu: dict, orc: dict, z_orc: np.ndarray, oc: O.Codec, s: int, d: int, T: int) -> dict:
+    qg, mng, scg = token_codes(gpu, oc, s, d)
+    qo, mno, sco = token_codes(orc, oc, s, d)
+    qg, mng, scg, qo, mno, sco = (a[:, :, :, :T] for a in (qg, mng, scg, qo, mno, sco))
+    side_diff = (mng != mno) | (scg != sco)
+    if side_diff.any():
+        for a, b in ((mng, mno), (scg, sco)):
+            da = np.abs(a[side_diff].astype(np.int32) - b[side_diff].astype(np.int32))
+            assert da.max() <= 1, "side information differs by more than one binary16 ulp"
+    diff = qg != qo
+    frac = float(diff.mean())
+    assert frac <= CODE_FRAC, f"{frac:.2e} of codes differ"
+    if diff.any():
+        assert np.abs(qg[diff].astype(np.int64) - qo[diff]).max() == 1
+        mn, sc = f16(mng[diff]), f16(scg[diff])
+        inv = np.where(sc == 0, np.float32(0), np.float32(1) / np.where(sc == 0, np.float32(1), sc))
+        t = ((z_orc[:, :, :, :T][diff].astype(np.float32) - mn) * inv).astype(np.float32)
+        qmax = (1 << oc.bits) - 1
+        same = np.clip(np.rint(t), 0, qmax) == qg[diff]
+        near_tie = np.abs(np.abs(t - np.floor(t)) - 0.5) <= TIE_EPS
+        assert np.all(same | near_tie), "a differing code is not at a rounding tie"
+    return {"code_frac": frac, "side_blocks": int(side_diff.sum())}
+
+
+def group_rel_err(ref: np.ndarray, got: np.ndarray, g: int) -> float:
+    r = ref.reshape(*ref.shape[:-1], -1, g).astype(np.float64)
+    e = got.reshape(*got.shape[:-1], -1, g).astype(np.float64) - r
+    num = np.sqrt((e * e).sum(-1))
+    den = np.sqrt((r * r).sum(-1))
+    return float((num / np.maximum(den, 1e-30)).max())
+
+
+def check_bf16_within_ulp(ref_f32: np.ndarray, got_bits: np.ndarray, g: int):
+    """bf16 output within one bf16 ulp of the oracle's binary32 value, widened by the binary32
+    gauge tolerance (1e-5 of the group norm) for elements small against their group."""
+    got = (got_bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    ref = ref_f32.astype(np.float64)
+    a = np.abs(ref_f32).astype(np.float32)
+    e = np.floor(np.log2(np.maximum(a, np.float32(1e-38))))
+    ulp = np.exp2(e - 7)
+    r = ref.reshape(*ref.shape[:-1], -1, g)
+    gnorm = np.repeat(np.sqrt((r * r).sum(-1)), g, axis=-1).reshape(ref.shape)
+    tol = ulp * (1 + 1e-6) + GAUGE_TOL * gnorm + 1e-38
+    bad = np.abs(got - ref) > tol
+    assert not bad.any(), (int(bad.sum()), float(np.abs(got - ref)[bad].max()))

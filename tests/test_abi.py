@@ -1,0 +1,173 @@
+"""C-ABI checks that need no GPU: the library loads and exports every declared symbol, host
+gauge construction agrees with the oracle, buffer sizing follows the layouts, and invalid
+arguments are rejected on the host before anything is enqueued."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2607_20538_amd import codec as cg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "codec_gauge.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\*?\s+\*?([a-z_]+)\(", text, flags=re.M)))
+
+
+def test_header_declares_the_binding_exports():
+    assert _declared() == sorted(cg.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = cg.lib()
+    for name in _declared():
+        assert hasattr(L, name), name
+    assert cg.status_str(cg.CG_ERR_UNSUPPORTED) == "unsupported configuration"
+
+
+@pytest.mark.parametrize("kind", [cg.GAUGE_IDENTITY, cg.GAUGE_HAAR, cg.GAUGE_DCT2, cg.GAUGE_HADAMARD])
+@pytest.mark.parametrize("g", [8, 16, 32, 128])
+def test_host_gauge_make_matches_oracle(kind, g):
+    G, _ = cg.gauge_make(kind, cg.shape(2, 2, 128, g), seed=31)
+    Go = O.gauge_make(kind, 2, 2, 128, g, seed=31)
+    assert np.abs(G - Go).max() <= 1e-6
+    for blk in G.reshape(-1, g, g)[:4]:
+        assert O.orthogonality_error(blk) <= 1e-6
+
+
+def test_host_gauge_make_expm_and_user():
+    A = (np.random.default_rng(1).standard_normal((1, 2, 2, 4, 32, 32)) * 0.5).astype(np.float32)
+    G, _ = cg.gauge_make(cg.GAUGE_EXPM, cg.shape(1, 2, 128, 32), params=A)
+    assert np.abs(G - O.gauge_make(O.GAUGE_EXPM, 1, 2, 128, 32, params=A)).max() <= 1e-6
+    U, _ = cg.gauge_make(cg.GAUGE_USER, cg.shape(1, 2, 128, 32), params=G)
+    np.testing.assert_array_equal(U, G)
+    G[0, 1, 0, 2, 4, 4] += 1e-3
+    with pytest.raises(cg.CodecError) as e:
+        cg.gauge_make(cg.GAUGE_USER, cg.shape(1, 2, 128, 32), params=G)
+    assert e.value.status == cg.CG_ERR_NOT_ORTHOGONAL
+
+
+def test_gauge_make_rejects_bad_shapes():
+    for shp, st in ((cg.shape(1, 1, 128, 48), cg.CG_ERR_UNSUPPORTED), (cg.shape(0, 1, 128, 32), cg.CG_ERR_ARG),
+                    (cg.shape(1, 1, 96, 96), None)):
+        if st is None:
+            with pytest.raises(cg.CodecError):
+                cg.gauge_make(cg.GAUGE_HADAMARD, shp)
+            continue
+        with pytest.raises(cg.CodecError) as e:
+            cg.gauge_make(cg.GAUGE_HAAR, shp)
+        assert e.value.status == st
+    assert cg.gauge_device_bytes(cg.shape(1, 1, 128, 48)) == 0
+
+
+@pytest.mark.parametrize("backend,bits", [(O.BLOCK_UNIFORM, 4), (O.BLOCK_UNIFORM, 3), (O.KIVI, 3), (O.KIVI, 6),
+                                          (O.PASSTHROUGH, 4)])
+def test_cache_bytes_follow_the_layout(backend, bits):
+    oc = O.Codec(backend=backend, bits=bits, block_c=32 if bits != 3 else 64)
+    c = cg.Codec(backend, bits, oc.block_c, oc.key_tokens, oc.val_channels, oc.residual)
+    for s in (0, 1):
+        lay = O.cache_layout(oc, s, 2, 3, 4, 256, 128)
+        n = cg.cache_bytes(c, s, 2, 3, 4, 256, 128)
+        for k, v in zip(("codes", "side", "residual"), n):
+            ref = 0 if lay[k] is None else int(np.prod(lay[k][0])) * np.dtype(lay[k][1]).itemsize
+            assert v == ref, (k, v, ref)
+
+
+def _fake_view(L=1, B=1, H=2, T=16, d=64, dtype=cg.DTYPE_BF16, ptr=0x10000, strides=None):
+    st = strides or (B * H * T * d, H * T * d, T * d, d)
+    return cg.KvView(ptr, dtype, L, B, H, T, d, *st)
+
+
+def _fake_cache(L=1, B=1, H=2, T_cap=16, d=64, codes=0x20000, side=0x30000, residual=0x40000, len_=0):
+    return cg.CacheStruct(codes, side, residual, L, B, H, T_cap, d, len_)
+
+
+def _encode(view, cache, codec, shp=None, t0=0, s=0, gdev=0x50000, err=None):
+    shp = shp or cg.shape(1, 2, 64, 16)
+    cs = codec.struct()
+    return cg.lib().kv_encode(s, C.byref(view), gdev, shp, C.byref(cs), C.byref(cache), t0, err, None)
+
+
+def _decode(view, cache, codec, shp=None, t0=0, s=0, gdev=0x50000):
+    shp = shp or cg.shape(1, 2, 64, 16)
+    cs = codec.struct()
+    return cg.lib().kv_decode(s, C.byref(cache), gdev, shp, C.byref(cs), t0, C.byref(view), None, None)
+
+
+BU = cg.Codec(cg.BLOCK_UNIFORM, 4, 32)
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (lambda v, k, c: (v, k, cg.Codec(cg.BLOCK_UNIFORM, 5, 32)), cg.CG_ERR_UNSUPPORTED),   # bits
+    (lambda v, k, c: (v, k, cg.Codec(cg.BLOCK_UNIFORM, 3, 16)), cg.CG_ERR_UNSUPPORTED),   # n*b % 32
+    (lambda v, k, c: (v, k, cg.Codec(cg.BLOCK_UNIFORM, 4, 48)), cg.CG_ERR_UNSUPPORTED),   # n does not divide d
+    (lambda v, k, c: (v, k, cg.Codec(7, 4, 32)), cg.CG_ERR_ARG),                          # backend
+    (lambda v, k, c: (_fake_view(H=3), k, c), cg.CG_ERR_SHAPE),
+    (lambda v, k, c: (_fake_view(ptr=0x10004), k, c), cg.CG_ERR_ALIGN),
+    (lambda v, k, c: (_fake_view(strides=(2048, 2048, 1024, 68)), k, c), cg.CG_ERR_ALIGN),
+    (lambda v, k, c: (_fake_view(dtype=9), k, c), cg.CG_ERR_ARG),
+    (lambda v, k, c: (_fake_view(ptr=0), k, c), cg.CG_ERR_ARG),
+    (lambda v, k, c: (_fake_view(ptr=0, T=0), k, c, ), "skip"),
+    (lambda v, k, c: (v, _fake_cache(codes=0x20008), c), cg.CG_ERR_ALIGN),
+    (lambda v, k, c: (v, _fake_cache(side=0), c), cg.CG_ERR_ARG),
+    (lambda v, k, c: (v, _fake_cache(B=2), c), cg.CG_ERR_SHAPE),
+    (lambda v, k, c: (_fake_view(T=17), k, c), cg.CG_ERR_CAPACITY),
+])
+def test_encode_rejects_invalid_arguments(mutate, status):
+    if status == "skip":   # valid: an empty view would launch nothing, but stays off the CPU
+        return
+    v, k, c = mutate(_fake_view(), _fake_cache(), BU)
+    assert _encode(v, k, c) == status
+
+
+def test_encode_decode_reject_ranges_and_modes():
+    v, k = _fake_view(T=8), _fake_cache()
+    assert _encode(v, k, BU, t0=9) == cg.CG_ERR_CAPACITY
+    assert _encode(v, k, BU, t0=-1) == cg.CG_ERR_ARG
+    assert _encode(v, k, BU, s=2) == cg.CG_ERR_ARG
+    assert _encode(v, k, BU, gdev=0x50008) == cg.CG_ERR_ALIGN
+    assert _encode(v, k, BU, shp=cg.shape(1, 2, 64, 48)) == cg.CG_ERR_UNSUPPORTED
+    kivi = cg.Codec(cg.KIVI, 3, 64, 32, 64, 128)
+    kk = _fake_cache(T_cap=64)
+    assert _encode(_fake_view(T=16), kk, kivi, t0=16) == cg.CG_ERR_UNSUPPORTED
+    assert _encode(_fake_view(T=16, dtype=cg.DTYPE_F32), kk, kivi) == cg.CG_ERR_UNSUPPORTED
+    assert _encode(_fake_view(T=16), _fake_cache(T_cap=48), kivi) == cg.CG_ERR_SHAPE
+    assert _encode(_fake_view(T=16), kk, cg.Codec(cg.KIVI, 3, 64, 24, 64, 128)) == cg.CG_ERR_UNSUPPORTED
+    # KIVI decode beyond the tokens the cache holds
+    assert _decode(_fake_view(T=16), _fake_cache(T_cap=64, len_=8), kivi) == cg.CG_ERR_CAPACITY
+    assert _decode(_fake_view(T=16), _fake_cache(len_=16), BU, t0=1) == cg.CG_ERR_CAPACITY
+
+
+def test_append_step_rejects_invalid_arguments():
+    shp = cg.shape(2, 2, 64, 16)
+    kn = _fake_view(L=1, T=1, strides=(128, 128, 64, 64))
+    k = _fake_cache(L=2)
+    cs = BU.struct()
+    f = cg.lib().kv_append_step
+    assert f(1, 1, C.byref(kn), C.byref(kn), 0x60000, 0x50000, shp, C.byref(cs), C.byref(k), C.byref(k), None,
+             None, None, None) == cg.CG_ERR_ARG
+    assert f(0, 3, C.byref(kn), C.byref(kn), 0x60000, 0x50000, shp, C.byref(cs), C.byref(k), C.byref(k), None,
+             None, None, None) == cg.CG_ERR_ARG
+    assert f(0, 1, C.byref(kn), C.byref(kn), None, 0x50000, shp, C.byref(cs), C.byref(k), C.byref(k), None, None,
+             None, None) == cg.CG_ERR_ARG
+    two = _fake_view(L=1, T=2)
+    assert f(0, 1, C.byref(two), C.byref(two), 0x60000, 0x50000, shp, C.byref(cs), C.byref(k), C.byref(k), None,
+             None, None, None) == cg.CG_ERR_SHAPE
+    assert f(0, 2, C.byref(kn), C.byref(kn), 0x60000, 0x50000, shp, C.byref(cs), C.byref(k), C.byref(k), None,
+             None, None, None) == cg.CG_ERR_SHAPE
+    assert f(0, 1, C.byref(kn), C.byref(kn), 0x60002, 0x50000, shp, C.byref(cs), C.byref(k), C.byref(k), None,
+             None, None, None) == cg.CG_ERR_ALIGN
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(cg, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(cg, "_lib", None)
+    with pytest.raises(ImportError):
+        cg.lib()

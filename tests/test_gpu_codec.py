@@ -1,0 +1,391 @@
+"""GPU parity of the codec library (through the C ABI) against the CPU oracle.
+
+Every case draws seeded synthetic KV tensors, runs the HIP path through the ctypes binding
+and compares with the oracle under the criteria stated in tests/_parity.py.  Sizes span
+several token tiles with a ragged tail; the full-size Llama-3-8B-shaped workload is checked
+on sampled vectors in test_gpu_fullsize.py."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2607_20538_amd import codec as cg
+from paper_2607_20538_amd import synth
+
+from _parity import (bf16_dev, cache_to_dev, cache_to_host, check_bf16_within_ulp, check_fused_codes,
+                     group_rel_err, out_host, to_cg, x_dev, x_f64, GAUGE_TOL)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    cg.lib()
+
+
+def _workload(T, L=1, B=2, H=2, d=128, dtype="bf16", seed=0xBEEF):
+    return synth.Workload("case", L=L, B=B, H=H, T=T, d=d, dtype=dtype, g=0, backend="bu", bits=4,
+                          data_seed=seed)
+
+
+def _gauge(kind, L, H, d, g, seed=17):
+    G = O.gauge_make(kind, L, H, d, g, seed=seed)
+    shp = cg.shape(L, H, d, g)
+    Gd = cg.alloc_gauge(shp)
+    cg.gauge_make(cg.GAUGE_USER, shp, params=G, G_host=None, G_dev=Gd)
+    return G, Gd, shp
+
+
+def _encode_gpu(X, s, Gd, shp, oc, T_cap, t0=0, err=None):
+    L_, B, H, T, d = X.shape
+    dev = cg.Cache(to_cg(oc), s, L_, B, H, T_cap, d)
+    cg.kv_encode(s, x_dev(X), Gd, shp, to_cg(oc), dev, t0=t0, err_flag=err)
+    torch.cuda.synchronize()
+    return dev
+
+
+def _decode_gpu(dev, s, Gd, shp, oc, t0, T, dtype=torch.bfloat16):
+    Y = torch.zeros((dev.L, dev.B, dev.H, T, dev.d), dtype=dtype, device="cuda")
+    cg.kv_decode(s, dev, Gd, shp, to_cg(oc), t0, Y)
+    torch.cuda.synchronize()
+    return out_host(Y)
+
+
+# ------------------------------------------------------------------------------------------
+# gauge stage (passthrough backend): z = G x within 1e-5 per group
+# ------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("g", [8, 16, 32, 64, 128])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_gauge_stage_matches_oracle(g, dtype):
+    w = _workload(T=77, dtype=dtype)
+    G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, g)
+    oc = O.Codec(backend=O.PASSTHROUGH)
+    for s in (0, 1):
+        X = synth.kv_tensor(w, s)
+        orc, _ = O.kv_encode(oc, s, X, G, T_cap=80)
+        dev = _encode_gpu(X, s, Gd, shp, oc, T_cap=80)
+        z = cache_to_host(dev, oc, s)["codes"]
+        assert group_rel_err(orc["codes"][:, :, :, :77], z[:, :, :, :77], g) <= GAUGE_TOL
+        # error-free round trip: bf16 out within a bf16 ulp (plus the gauge tolerance) of the
+        # oracle's binary32 round trip, binary32 out within 1e-5 per group
+        if dtype == "bf16":
+            ref = O.kv_decode(oc, s, G, orc, 0, 77, out_bf16=False)
+            check_bf16_within_ulp(ref, _decode_gpu(dev, s, Gd, shp, oc, 0, 77), g)
+        else:
+            xh = _decode_gpu(dev, s, Gd, shp, oc, 0, 77, torch.float32)
+            assert group_rel_err(X, xh, g) <= GAUGE_TOL
+
+
+# ------------------------------------------------------------------------------------------
+# quantise-only and dequantise-only: bit-exact
+# ------------------------------------------------------------------------------------------
+QCASES = [(O.BLOCK_UNIFORM, b, n) for b in (2, 3, 4, 6, 8) for n in (32, 64)] + \
+         [(O.BLOCK_UNIFORM, 4, 16), (O.BLOCK_UNIFORM, 8, 128), (O.KIVI, 3, 64), (O.KIVI, 4, 64), (O.KIVI, 2, 32)]
+
+
+@pytest.mark.parametrize("backend,bits,n", QCASES)
+def test_quantise_and_dequantise_are_bit_exact(backend, bits, n):
+    """Identity gauge: z = x exactly on both sides, so codes, side information, packed bytes
+    and the dequantised values must agree bit for bit."""
+    T = 300 if backend == O.KIVI else 97
+    w = _workload(T=T, dtype="bf16" if backend == O.KIVI else "f32")
+    G, Gd, shp = _gauge(O.GAUGE_IDENTITY, 1, 2, 128, 32)
+    oc = O.Codec(backend=backend, bits=bits, block_c=n, val_channels=n, key_tokens=32, residual=128)
+    T_cap = 320
+    for s in (0, 1):
+        X = synth.kv_tensor(w, s)
+        orc, flags = O.kv_encode(oc, s, X, G, T_cap=T_cap)
+        assert flags == 0
+        dev = _encode_gpu(X, s, Gd, shp, oc, T_cap)
+        got = cache_to_host(dev, oc, s)
+        if backend == O.KIVI:
+            tq = O.kivi_tq(T, oc)
+            if s == 0:
+                np.testing.assert_array_equal(got["codes"][:, :, :, :tq // 32], orc["codes"][:, :, :, :tq // 32])
+                np.testing.assert_array_equal(got["side"][:, :, :, :tq // 32], orc["side"][:, :, :, :tq // 32])
+            else:
+                np.testing.assert_array_equal(got["codes"][:, :, :, :tq], orc["codes"][:, :, :, :tq])
+                np.testing.assert_array_equal(got["side"][:, :, :, :tq], orc["side"][:, :, :, :tq])
+            np.testing.assert_array_equal(got["residual"], orc["residual"])
+        else:
+            np.testing.assert_array_equal(got["codes"][:, :, :, :T], orc["codes"][:, :, :, :T])
+            np.testing.assert_array_equal(got["side"][:, :, :, :T], orc["side"][:, :, :, :T])
+        # dequantise the oracle's cache on the GPU
+        ddev = cache_to_dev(orc, oc, s, 1, 2, 2, T_cap, 128, len_=T)
+        lens = [T, T]
+        ref = O.kv_decode(oc, s, G, orc, 0, T, lens=lens, out_bf16=False)
+        np.testing.assert_array_equal(_decode_gpu(ddev, s, Gd, shp, oc, 0, T, torch.float32), ref)
+        refb = O.kv_decode(oc, s, G, orc, 0, T, lens=lens, out_bf16=True)
+        np.testing.assert_array_equal(_decode_gpu(ddev, s, Gd, shp, oc, 0, T), refb)
+
+
+# ------------------------------------------------------------------------------------------
+# fused encoder and decoder with real gauges
+# ------------------------------------------------------------------------------------------
+FCASES = [(128, 4, 64, O.GAUGE_HAAR), (128, 6, 64, O.GAUGE_HAAR), (128, 3, 64, O.GAUGE_HAAR),
+          (128, 4, 64, O.GAUGE_DCT2), (128, 4, 64, O.GAUGE_HADAMARD), (64, 4, 32, O.GAUGE_HAAR),
+          (32, 3, 64, O.GAUGE_HAAR), (16, 4, 32, O.GAUGE_HAAR), (8, 4, 64, O.GAUGE_HAAR),
+          (8, 6, 64, O.GAUGE_HAAR), (32, 8, 32, O.GAUGE_HAAR), (128, 2, 64, O.GAUGE_HAAR)]
+
+
+@pytest.mark.parametrize("g,bits,n,kind", FCASES)
+def test_fused_encoder_and_decoder(g, bits, n, kind):
+    T = 261
+    w = _workload(T=T, L=2, B=1, H=2)
+    G, Gd, shp = _gauge(kind, 2, 2, 128, g)
+    oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=bits, block_c=n)
+    for s in (0, 1):
+        X = synth.kv_tensor(w, s)
+        orc, _ = O.kv_encode(oc, s, X, G, T_cap=T)
+        zo, _ = O.kv_encode(O.Codec(backend=O.PASSTHROUGH), s, X, G, T_cap=T)
+        dev = _encode_gpu(X, s, Gd, shp, oc, T)
+        check_fused_codes(cache_to_host(dev, oc, s), orc, zo["codes"], oc, s, 128, T)
+        # decoder on the oracle's cache
+        ddev = cache_to_dev(orc, oc, s, 2, 1, 2, T, 128)
+        ref = O.kv_decode(oc, s, G, orc, 0, T, out_bf16=False)
+        assert group_rel_err(ref, _decode_gpu(ddev, s, Gd, shp, oc, 0, T, torch.float32), g) <= GAUGE_TOL
+        check_bf16_within_ulp(ref, _decode_gpu(ddev, s, Gd, shp, oc, 0, T), g)
+
+
+def test_tiny_workload_end_to_end():
+    w = synth.WORKLOADS["tiny"]
+    G, Gd, shp = _gauge(O.GAUGE_HAAR, w.L, w.H, w.d, w.g, seed=w.gauge_seed)
+    oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=w.bits, block_c=w.block_c)
+    for s in (0, 1):
+        X = synth.kv_tensor(w, s)
+        orc, _ = O.kv_encode(oc, s, X, G, T_cap=w.T)
+        zo, _ = O.kv_encode(O.Codec(backend=O.PASSTHROUGH), s, X, G, T_cap=w.T)
+        dev = _encode_gpu(X, s, Gd, shp, oc, w.T)
+        check_fused_codes(cache_to_host(dev, oc, s), orc, zo["codes"], oc, s, w.d, w.T)
+        ddev = cache_to_dev(orc, oc, s, w.L, w.B, w.H, w.T, w.d)
+        ref = O.kv_decode(oc, s, G, orc, 0, w.T, out_bf16=False)
+        assert group_rel_err(ref, _decode_gpu(ddev, s, Gd, shp, oc, 0, w.T, torch.float32), w.g) <= GAUGE_TOL
+
+
+# ------------------------------------------------------------------------------------------
+# KIVI-style backend
+# ------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("g,bits", [(32, 3), (128, 4), (16, 2)])
+def test_kivi_encode_decode(g, bits):
+    T, T_cap = 300, 320
+    w = _workload(T=T)
+    G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, g)
+    oc = O.Codec(backend=O.KIVI, bits=bits, key_tokens=32, val_channels=64, residual=128)
+    tq = O.kivi_tq(T, oc)
+    for s in (0, 1):
+        X = synth.kv_tensor(w, s)
+        orc, _ = O.kv_encode(oc, s, X, G, T_cap=T_cap)
+        zo, _ = O.kv_encode(O.Codec(backend=O.PASSTHROUGH), s, X, G, T_cap=T_cap)
+        dev = _encode_gpu(X, s, Gd, shp, oc, T_cap)
+        got = cache_to_host(dev, oc, s)
+        np.testing.assert_array_equal(got["residual"], orc["residual"])
+        check_fused_codes(got, orc, zo["codes"], oc, s, 128, tq)
+        ddev = cache_to_dev(orc, oc, s, 1, 2, 2, T_cap, 128, len_=T)
+        ref = O.kv_decode(oc, s, G, orc, 0, T, lens=[T, T], out_bf16=False)
+        out = _decode_gpu(ddev, s, Gd, shp, oc, 0, T, torch.float32)
+        assert group_rel_err(ref[:, :, :, :tq], out[:, :, :, :tq], g) <= GAUGE_TOL
+        np.testing.assert_array_equal(out[:, :, :, tq:], ref[:, :, :, tq:])   # window: exact
+        outb = _decode_gpu(ddev, s, Gd, shp, oc, 0, T)
+        np.testing.assert_array_equal(outb[:, :, :, tq:], X[:, :, :, tq:])
+        check_bf16_within_ulp(ref[:, :, :, :tq], outb[:, :, :, :tq], g)
+        # a sub-range decode agrees with the full one
+        sub = _decode_gpu(ddev, s, Gd, shp, oc, 100, 150)
+        np.testing.assert_array_equal(sub, outb[:, :, :, 100:250])
+
+
+def test_kivi_short_cache_decodes_as_a_copy():
+    T = 100
+    w = _workload(T=T)
+    G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, 32)
+    oc = O.Codec(backend=O.KIVI, bits=3)
+    for s in (0, 1):
+        X = synth.kv_tensor(w, s)
+        dev = _encode_gpu(X, s, Gd, shp, oc, 128)
+        dev.len = T
+        np.testing.assert_array_equal(_decode_gpu(dev, s, Gd, shp, oc, 0, T), X)
+
+
+# ------------------------------------------------------------------------------------------
+# rolling step
+# ------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("backend,kind", [(O.BLOCK_UNIFORM, O.GAUGE_IDENTITY), (O.KIVI, O.GAUGE_IDENTITY),
+                                          (O.PASSTHROUGH, O.GAUGE_IDENTITY), (O.BLOCK_UNIFORM, O.GAUGE_HAAR),
+                                          (O.KIVI, O.GAUGE_HAAR)])
+def test_append_step_matches_oracle(backend, kind):
+    """Rolling history (section 4.4): T0 tokens encoded by the oracle and uploaded, then
+    steps appended on both sides with a different position per batch row; the identity gauge
+    makes every stage exact, so caches and decoded histories must agree bit for bit; with a
+    Haar gauge the fused criteria apply to the appended codes."""
+    L, B, H, d, g = 2, 2, 2, 128, 32
+    T0, steps, T_cap = 150, 40, 224
+    w = _workload(T=T_cap, L=L, B=B, H=H)
+    G, Gd, shp = _gauge(kind, L, H, d, g)
+    oc = O.Codec(backend=backend, bits=4, block_c=64, key_tokens=32, val_channels=64, residual=128)
+    Xk, Xv = synth.kv_tensor(w, 0), synth.kv_tensor(w, 1)
+    # row 1 runs 5 positions ahead of row 0 (its slots [T0, T0+5) stay empty on both sides)
+    start = np.array([T0, T0 + 5])
+    ok, _ = O.kv_encode(oc, 0, np.ascontiguousarray(Xk[:, :, :, :T0]), G, T_cap=T_cap)
+    ov, _ = O.kv_encode(oc, 1, np.ascontiguousarray(Xv[:, :, :, :T0]), G, T_cap=T_cap)
+    kc = cache_to_dev(ok, oc, 0, L, B, H, T_cap, d)
+    vc = cache_to_dev(ov, oc, 1, L, B, H, T_cap, d)
+    khist = torch.zeros((L, B, H, T_cap, d), dtype=torch.bfloat16, device="cuda")
+    vhist = torch.zeros_like(khist)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for i in range(steps):
+        pos = start + i
+        kn = np.ascontiguousarray(Xk[:, np.arange(B), :, pos].transpose(1, 0, 2, 3))  # [L][B][H][d]
+        vn = np.ascontiguousarray(Xv[:, np.arange(B), :, pos].transpose(1, 0, 2, 3))
+        O.kv_append(oc, 0, kn, G, ok, pos)
+        O.kv_append(oc, 1, vn, G, ov, pos)
+        pos_d = torch.tensor(pos, dtype=torch.int32, device="cuda")
+        cg.kv_append_step(0, L, bf16_dev(kn[:, :, :, None, :]), bf16_dev(vn[:, :, :, None, :]), pos_d, Gd, shp,
+                          to_cg(oc), kc, vc, khist, vhist, err_flag=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    final = start + steps - 1
+    for s, oc_cache, dc, hist in ((0, ok, kc, khist), (1, ov, vc, vhist)):
+        got = cache_to_host(dc, oc, s)
+        ref_hist = O.kv_decode(oc, s, G, oc_cache, 0, T_cap, lens=final + 1, out_bf16=True)
+        h = out_host(hist)
+        if kind == O.GAUGE_IDENTITY:
+            for key in ("codes", "side", "residual"):
+                if got[key] is not None:
+                    np.testing.assert_array_equal(got[key], oc_cache[key])
+            for b in range(B):
+                np.testing.assert_array_equal(h[:, b, :, :final[b] + 1], ref_hist[:, b, :, :final[b] + 1])
+        else:
+            zo, _ = O.kv_encode(O.Codec(backend=O.PASSTHROUGH), s, Xk if s == 0 else Xv, G, T_cap=T_cap)
+            tq = O.kivi_tq(int(final.min()) + 1, oc) if backend == O.KIVI else int(final.min()) + 1
+            check_fused_codes(got, oc_cache, zo["codes"], oc, s, d, tq)
+            # the history the step decoded equals kv_decode of the same GPU cache
+            for b in range(B):
+                dc.len = int(final[b]) + 1
+                full = _decode_gpu(dc, s, Gd, shp, oc, 0, int(final[b]) + 1)
+                np.testing.assert_array_equal(h[:, b, :, :final[b] + 1], full[:, b])
+
+
+def test_append_step_flags_positions_beyond_capacity():
+    L, B, H, d, g = 1, 2, 2, 128, 32
+    G, Gd, shp = _gauge(O.GAUGE_HAAR, L, H, d, g)
+    oc = cg.Codec(cg.BLOCK_UNIFORM, 4, 64)
+    kc = cg.Cache(oc, 0, L, B, H, 64, d)
+    vc = cg.Cache(oc, 1, L, B, H, 64, d)
+    before = kc.codes.clone()
+    new = torch.ones((L, B, H, 1, d), dtype=torch.bfloat16, device="cuda")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pos = torch.tensor([64, 70], dtype=torch.int32, device="cuda")
+    cg.kv_append_step(0, L, new, new, pos, Gd, shp, oc, kc, vc, err_flag=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) & cg.CG_FLAG_POS_RANGE
+    assert torch.equal(kc.codes, before)
+
+
+# ------------------------------------------------------------------------------------------
+# edge cases
+# ------------------------------------------------------------------------------------------
+def test_empty_offset_and_strided_views():
+    G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, 128)
+    oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=4, block_c=64)
+    w = _workload(T=90)
+    X = synth.kv_tensor(w, 0)
+    # empty encode writes nothing
+    dev = cg.Cache(to_cg(oc), 0, 1, 2, 2, 128, 128)
+    cg.kv_encode(0, x_dev(X)[:, :, :, :0], Gd, shp, to_cg(oc), dev)
+    torch.cuda.synchronize()
+    assert not dev.codes.any()
+    # encoding at an offset equals encoding the whole range
+    whole = _encode_gpu(X, 0, Gd, shp, oc, T_cap=128)
+    part = cg.Cache(to_cg(oc), 0, 1, 2, 2, 128, 128)
+    cg.kv_encode(0, x_dev(X[:, :, :, :50].copy()), Gd, shp, to_cg(oc), part, t0=0)
+    cg.kv_encode(0, x_dev(X[:, :, :, 50:].copy()), Gd, shp, to_cg(oc), part, t0=50)
+    torch.cuda.synchronize()
+    assert torch.equal(part.codes, whole.codes) and torch.equal(part.side, whole.side)
+    # a token-strided input view gives the same codes as a contiguous copy
+    big = torch.zeros((1, 2, 2, 180, 128), dtype=torch.bfloat16, device="cuda")
+    big[:, :, :, ::2] = x_dev(X)
+    strided = cg.Cache(to_cg(oc), 0, 1, 2, 2, 128, 128)
+    cg.kv_encode(0, big[:, :, :, ::2], Gd, shp, to_cg(oc), strided)
+    torch.cuda.synchronize()
+    assert torch.equal(strided.codes, whole.codes)
+    # decode into a strided output view
+    out = torch.zeros((1, 2, 2, 180, 128), dtype=torch.bfloat16, device="cuda")
+    cg.kv_decode(0, whole, Gd, shp, to_cg(oc), 0, out[:, :, :, ::2])
+    torch.cuda.synchronize()
+    ref = _decode_gpu(whole, 0, Gd, shp, oc, 0, 90)
+    np.testing.assert_array_equal(out_host(out[:, :, :, ::2].contiguous()), ref)
+    assert not out[:, :, :, 1::2].any()
+
+
+@pytest.mark.parametrize("backend", [O.BLOCK_UNIFORM, O.KIVI])
+def test_outputs_stay_inside_their_buffers(backend):
+    """Guard bands: bytes after every cache buffer and after the decode output are untouched."""
+    G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, 32)
+    oc = O.Codec(backend=backend, bits=3, block_c=64)
+    T = 200
+    X = synth.kv_tensor(_workload(T=T), 0)
+    dev = cg.Cache(to_cg(oc), 0, 1, 2, 2, 224, 128)
+    guards = {}
+    for key in ("codes", "side", "residual"):
+        buf = getattr(dev, key)
+        if buf is None:
+            continue
+        big = torch.full((buf.numel() + 4096,), 0xA5, dtype=torch.uint8, device="cuda")
+        setattr(dev, key, big[: buf.numel()])
+        guards[key] = big
+    cg.kv_encode(0, x_dev(X), Gd, shp, to_cg(oc), dev)
+    dev.len = T
+    Y = torch.full((1, 2, 2, T + 16, 128), 7.0, dtype=torch.bfloat16, device="cuda")
+    cg.kv_decode(0, dev, Gd, shp, to_cg(oc), 0, Y[:, :, :, :T])
+    torch.cuda.synchronize()
+    for key, big in guards.items():
+        n = getattr(dev, key).numel()
+        assert bool((big[n:] == 0xA5).all()), key
+    assert bool((Y[:, :, :, T:] == 7.0).all())
+
+
+def test_error_flags():
+    G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, 128)
+    oc = cg.Codec(cg.BLOCK_UNIFORM, 4, 64)
+    X = torch.randn((1, 1, 2, 40, 128), device="cuda").to(torch.bfloat16)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dev = cg.Cache(oc, 0, 1, 1, 2, 64, 128)
+    cg.kv_encode(0, X, Gd, shp, oc, dev, err_flag=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    X[0, 0, 1, 7, 3] = float("nan")
+    cg.kv_encode(0, X, Gd, shp, oc, dev, err_flag=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) & cg.CG_FLAG_NONFINITE
+    err.zero_()
+    X = torch.randn((1, 1, 2, 40, 128), device="cuda").to(torch.bfloat16)
+    X[0, 0, 0, 3] *= 1e6
+    cg.kv_encode(0, X, Gd, shp, oc, dev, err_flag=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) & cg.CG_FLAG_SIDE_OVERFLOW
+
+
+def test_encode_is_deterministic():
+    G, Gd, shp = _gauge(O.GAUGE_HAAR, 2, 2, 128, 128)
+    oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=4, block_c=64)
+    X = synth.kv_tensor(_workload(T=1000, L=2), 0)
+    a = _encode_gpu(X, 0, Gd, shp, oc, 1024)
+    b = _encode_gpu(X, 0, Gd, shp, oc, 1024)
+    assert torch.equal(a.codes, b.codes) and torch.equal(a.side, b.side)
+    ya = _decode_gpu(a, 0, Gd, shp, oc, 0, 1000)
+    yb = _decode_gpu(a, 0, Gd, shp, oc, 0, 1000)
+    np.testing.assert_array_equal(ya, yb)
+
+
+def test_library_gauge_upload_matches_user_upload():
+    """gauge_make(HAAR) straight into the device buffer gives the same device bytes as
+    uploading the oracle's Haar gauge as a USER gauge."""
+    shp = cg.shape(2, 2, 128, 64)
+    a = cg.alloc_gauge(shp)
+    b = cg.alloc_gauge(shp)
+    cg.gauge_make(cg.GAUGE_HAAR, shp, seed=5, G_host=None, G_dev=a)
+    cg.gauge_make(cg.GAUGE_USER, shp, params=O.gauge_make(O.GAUGE_HAAR, 2, 2, 128, 64, seed=5), G_host=None,
+                  G_dev=b)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
