@@ -1,0 +1,172 @@
+"""Benchmark of the gauge-coded KV codec hot path on one MI355X.
+
+A step is one full pass of the hot path over the Llama-3-8B-shaped KV cache (32 layers,
+8 KV heads, head_dim 128, batch 1, 8192 tokens, bf16; Haar gauge with g = 128; block-uniform
+4-bit, block 64): encode K, encode V (gauge -> block range -> quantise -> bit-pack), then
+decode K, decode V (unpack -> dequantise -> inverse gauge -> bf16).  Inputs are seeded
+synthetic tensors already resident in HBM.
+
+Prints one JSON line.  `value` is the round-trip throughput in logical bf16 bytes
+(2 bytes per K/V element) per second; `roofline` describes the dominant kernel against the
+HBM peak, with its algorithmic bytes per launch and the average launch time measured with
+HIP events on the stream the kernels run on; `cpu_baseline` times the CPU oracle on a
+bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+WORKLOAD = "llama8b"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-layers", type=int, default=2)
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic_llama8b.json"),
+                    help="HBM traffic per launch measured with rocprofv3 counters (optional)")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(w, s_count=1):
+    """Bytes one launch must move: per element bf16 in (2) + codes (b/8) + side (4/n),
+    plus the binary32 gauge blocks of the launch's cache type (4 g^2 per (l, h, r))."""
+    per_elem = 2.0 + w.bits / 8.0 + 4.0 / w.block_c
+    elems = w.L * w.B * w.H * w.T * w.d
+    gauge = 4.0 * w.g * w.g * w.L * w.H * (w.d // w.g)
+    return s_count * (elems * per_elem + gauge)
+
+
+def cpu_baseline(w, G_host, layers):
+    """The oracle (single thread, as written) encoding and decoding `layers` layers of K and V."""
+    import numpy as np
+
+    import oracle as O
+    from paper_2607_20538_amd import synth
+
+    oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=w.bits, block_c=w.block_c)
+    t_total = 0.0
+    elems = 0
+    for s in (0, 1):
+        X = synth.kv_tensor(w, s, L=layers)
+        Gs = np.ascontiguousarray(G_host[:layers])
+        t0 = time.perf_counter()
+        cache, _ = O.kv_encode(oc, s, X, Gs, T_cap=w.T)
+        O.kv_decode(oc, s, Gs, cache, 0, w.T, out_bf16=True)
+        t_total += time.perf_counter() - t0
+        elems += X.size
+    gbs = elems * 2 / t_total / 1e9
+    return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{layers} of {w.L} layers of K and V ({elems} elements), encode+decode, "
+                      f"{t_total:.1f} s single-threaded"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: the codec path has no "
+              f"cross-GPU step (every (layer, head, batch) slice is independent).", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2607_20538_amd import codec as cg
+    from paper_2607_20538_amd import synth
+
+    torch.cuda.set_device(0)
+    w = synth.WORKLOADS[WORKLOAD]
+    shp = cg.shape(w.L, w.H, w.d, w.g)
+    codec = cg.Codec(cg.BLOCK_UNIFORM, w.bits, w.block_c)
+    Gd = cg.alloc_gauge(shp)
+    G_host, _ = cg.gauge_make(cg.GAUGE_HAAR, shp, seed=w.gauge_seed, G_dev=Gd)
+
+    X, Y, caches = [], [], []
+    for s in (0, 1):
+        bits = synth.kv_tensor(w, s)
+        X.append(torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).cuda())
+        del bits
+        Y.append(torch.empty_like(X[-1]))
+        caches.append(cg.Cache(codec, s, w.L, w.B, w.H, w.T, w.d))
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    enc_ev, dec_ev = [], []
+
+    def step(record):
+        for s in (0, 1):
+            if record:
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+            cg.kv_encode(s, X[s], Gd, shp, codec, caches[s], err_flag=err, stream=stream.cuda_stream)
+            if record:
+                b.record(stream)
+                enc_ev.append((a, b))
+        for s in (0, 1):
+            if record:
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+            cg.kv_decode(s, caches[s], Gd, shp, codec, 0, Y[s], err_flag=err, stream=stream.cuda_stream)
+            if record:
+                b.record(stream)
+                dec_ev.append((a, b))
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    assert int(err.item()) == 0, f"device error flag {int(err.item())}"
+
+    enc_ms = float(np.mean([a.elapsed_time(b) for a, b in enc_ev]))
+    dec_ms = float(np.mean([a.elapsed_time(b) for a, b in dec_ev]))
+    ms_step = elapsed * 1e3 / args.steps
+    n_elem = w.n_elements
+    value = n_elem * 2 / (ms_step * 1e-3) / 1e9           # logical bf16 GB/s, encode+decode
+
+    alg = algorithmic_bytes(w)                             # one launch = one of K or V
+    dom_name, dom_ms = ("kv_encode", enc_ms) if enc_ms >= dec_ms else ("kv_decode", dec_ms)
+    achieved = alg / (dom_ms * 1e-3) / 1e9
+    traffic = None
+    if os.path.exists(args.traffic):
+        try:
+            tr = json.load(open(args.traffic))
+            traffic = tr.get(dom_name)
+        except (OSError, ValueError):
+            traffic = None
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": dom_name,
+                "kernel_ms": round(dom_ms, 4), "encode_ms": round(enc_ms, 4), "decode_ms": round(dec_ms, 4),
+                "alg_bytes_per_launch": int(alg)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, G_host, args.cpu_sample_layers)
+
+    line = {
+        "metric": "KV encode+decode GB/s (bf16 in) and % of MI355X HBM peak, 4-bit g=128",
+        "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "llama3-8b-shaped KV: L=32 B=1 H=8 T=8192 d=128 bf16, Haar g=128, "
+                               "block-uniform 4-bit n=64",
+                   "elements": n_elem, "global_batch": w.B, "seq_len": w.T, "parallelism": "none"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

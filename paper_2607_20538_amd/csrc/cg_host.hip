@@ -1,6 +1,7 @@
 // Host side of the C ABI: argument validation, gauge construction (gauge_make), buffer
 // sizing and dispatch of the encode / decode / rolling-append kernels.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <vector>
@@ -339,13 +340,24 @@ int kivi_tq(int T, const cg_codec* c) {
 
 namespace cg {
 
+// Matrix-core kernels take bf16 block-uniform (and passthrough) caches of head dimension 128;
+// everything else runs on the general kernels.  The environment variable CG_KERNELS=generic,
+// read at every launch, forces the general kernels (the tests run both paths on one input).
+static bool force_generic() {
+  const char* e = getenv("CG_KERNELS");
+  return e && strcmp(e, "generic") == 0;
+}
+
 hipError_t launch_encode(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c, const CacheDev& k,
                          int t0, int tq, int* err, hipStream_t st) {
+  if (!force_generic() && mfma_encode_supported(X, G, c)) return launch_encode_mfma(s, X, l0, G, c, k, t0, err, st);
   return launch_encode_generic(s, X, l0, G, c, k, t0, tq, err, st);
 }
 
 hipError_t launch_decode(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0, int len,
                          const int* pos, const ViewDev& Y, int* err, hipStream_t st) {
+  if (!force_generic() && mfma_decode_supported(Y, G, c))
+    return launch_decode_mfma(s, k, l0, G, c, t0, pos, Y, err, st);
   return launch_decode_generic(s, k, l0, G, c, t0, len, pos, Y, err, st);
 }
 

@@ -79,6 +79,14 @@ hipError_t launch_encode_generic(int s, const ViewDev& X, int l0, const GaugeDev
 hipError_t launch_decode_generic(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
                                  int len, const int* pos, const ViewDev& Y, int* err, hipStream_t st);
 
+// Matrix-core kernels: bf16, head dimension 128, block-uniform (n in {16, 32, 64}) or passthrough.
+bool mfma_encode_supported(const ViewDev& X, const GaugeDev& G, const CodecDev& c);
+bool mfma_decode_supported(const ViewDev& Y, const GaugeDev& G, const CodecDev& c);
+hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c,
+                              const CacheDev& k, int t0, int* err, hipStream_t st);
+hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
+                              const int* pos, const ViewDev& Y, int* err, hipStream_t st);
+
 // Dispatching launchers (hip stream passed through).  All validate nothing: the host entry points do.
 // Encode tokens [0, X.T) of view X into cache positions [t0, t0 + X.T); layer l of the view is
 // cache layer l + l0.  tq: KIVI tokens to quantise (others go to the window).

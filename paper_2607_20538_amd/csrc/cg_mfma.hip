@@ -1,0 +1,657 @@
+// Matrix-core codec kernels for bf16 caches with head dimension 128 and the block-uniform
+// backend (the configuration the paper's Llama-class KV caches take).
+//
+// The gauge (section 3: z = G_{l,s,h,r} x per channel group) is a dense contraction over the
+// channel axis, so it runs on the gfx950 matrix cores with v_mfma_f32_32x32x16_bf16.  The
+// input x is exact in bf16; the binary32 gauge is split into three bf16 planes
+// G = G0 + G1 + G2 (about 24 significant bits), each multiplied on the matrix core with a
+// binary32 accumulator.
+//
+// Work split: a workgroup of four wave64s owns a range of 32-token tiles of one
+// (layer, batch, head) slice; wave w computes output channels [32w, 32w+32) (one 32-row MFMA
+// tile) for the tile's 32 tokens.  The wave keeps its 32 rows of every split plane in VGPRs
+// for the whole range, so the matrix core never re-reads G.  Output rows are permuted so
+// that lane (token n, half hc) ends up with the 16 consecutive channels 32w + 16hc + [0, 16):
+// its codes form one contiguous stretch of the packed row.  Tokens are staged through LDS
+// with an XOR swizzle of the 16-byte granules of each 256-byte row, so the B-operand reads
+// (lane n reads granule j of row n) hit distinct banks.
+//
+// Encode epilogue (section 4.3 block-uniform): block minimum / maximum in-lane, across the
+// two lane halves (n = 32) and across the wave pair through LDS (n = 64); binary16 side
+// information; binary32 quantisation without contraction; LSB-first packing; stores.
+//
+// Decode: the B operand is the centred integer code q - c, c = 2^(b-1) (exact in bf16), so
+// per block k, with the grid midpoint m_k = mn_k + c sc_k,
+//   xhat_i = sum_k ( m_k * colsum_k(G^T)_i + sc_k * (G^T (q - c))_{k,i} )
+// with block-local accumulation on the matrix core and the column sums of each block
+// computed once per workgroup in binary64.  Centring keeps the two terms small when a block
+// spans a group whose values sit far from the block's minimum (an outlier in another group
+// of the same block), where mn * colsum and sc * G^T q would cancel.
+#include "cg_internal.h"
+#include "cg_device.h"
+
+namespace cg {
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kD = 128;          // head dimension handled here
+constexpr int kTok = 32;         // tokens per tile (MFMA N)
+constexpr int kThreads = 256;    // four waves
+constexpr int kRowBytes = kD * 2;
+
+struct MfmaArgs {
+  // view (input for encode, output for decode)
+  char* x;
+  int64_t sl, sb, sh, st;        // element strides
+  int L, B, H, T;                // view dims (L = layers of the view)
+  int l0;                        // cache layer of view layer 0
+  int s;                         // 0 keys, 1 values
+  int t0;                        // cache position of view token 0
+  // gauge planes ([nblk][g][g] bf16) and binary32 blocks
+  const uint16_t* gp[3];
+  const float* g32;
+  int g, R;                      // group size, groups per head
+  int Hg;                        // heads of the gauge shape
+  // cache
+  uint8_t* codes;
+  uint32_t* side;
+  int T_cap, cB, cH;             // cache capacity and dims
+  // work split
+  int nslices, chunks, tiles_per_wg;
+  const int* pos;                // decode only: batch row b holds positions [0, pos[b]]
+  int* err;
+};
+
+__device__ __forceinline__ int xcd_remap(int bid, int nwg) {
+  // workgroups are dealt round-robin to the 8 XCDs; give each XCD a contiguous range of
+  // logical workgroups so that the ranges of one slice share an L2
+  const int per = nwg >> 3;
+  return (bid & 7) * per + (bid >> 3);
+}
+
+// physical 16-byte granule of logical granule j in token row n
+__device__ __forceinline__ int swz(int n, int j) { return j ^ (n & 15); }
+
+__device__ __forceinline__ f32x16_t mfma(const bf16x8_t& a, const bf16x8_t& b, const f32x16_t& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(const u32x4_t& v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+// Load the wave's A fragments: plane p, K-step kk: 8 bf16 of row `ch` (an output channel of
+// this wave) at input channels j0..j0+7 of the full block-diagonal matrix (zero outside the
+// row's group).  `tr` selects G^T planes (decode).
+template <int NP, int KS>
+__device__ void load_a(bf16x8_t (&A)[NP][KS], const MfmaArgs& a, int l, int h, int ch, int kbase, int kh) {
+  const int g = a.g;
+  const int r = ch / g;
+  const size_t blk = ((size_t(l) * 2 + a.s) * a.Hg + h) * a.R + r;
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) {
+    const int j0 = kbase + 16 * kk + 8 * kh;
+    const bool in_group = (j0 / g) == r;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      u32x4_t v = {0u, 0u, 0u, 0u};
+      if (in_group) v = *(const u32x4_t*)(a.gp[p] + blk * g * g + size_t(ch % g) * g + (j0 % g));
+      A[p][kk] = as_bf16x8(v);
+    }
+  }
+}
+
+// Packs 16 codes of BITS bits into 16*BITS/32 words (BITS even) LSB-first.
+template <int BITS>
+__device__ __forceinline__ void pack16(const uint32_t (&q)[16], uint32_t* out) {
+  constexpr int NW = (16 * BITS + 31) / 32;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) out[w] = 0;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int bit = e * BITS, w = bit >> 5, off = bit & 31;
+    out[w] |= q[e] << off;
+    if (off + BITS > 32) out[w + 1] |= q[e] >> (32 - off);
+  }
+}
+
+template <int NW>
+__device__ __forceinline__ void store_words(uint32_t* dst, const uint32_t* v) {
+  // dst is 4-byte aligned; use the widest aligned vector stores available
+  if constexpr (NW == 4) {
+    *(u32x4_t*)dst = u32x4_t{v[0], v[1], v[2], v[3]};
+  } else if constexpr (NW == 2) {
+    *(uint2*)dst = make_uint2(v[0], v[1]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) dst[i] = v[i];
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// encode
+// ------------------------------------------------------------------------------------------
+template <int NP, int KS, int BITS, int NB, bool PASS>
+__global__ __launch_bounds__(kThreads, 2) void enc_mfma(MfmaArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t xtile[2][kTok * kRowBytes];
+  __shared__ float2 red[4][kTok];  // per-wave (min, max) of each token, for 64-channel blocks
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n = lane & 31, hc = lane >> 5;
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int slice = logical / a.chunks, chunk = logical - slice * a.chunks;
+  if (slice >= a.nslices) return;
+  const int h = slice % a.H, b = (slice / a.H) % a.B, lv = slice / (a.H * a.B);
+  const int l = lv + a.l0;
+  const int ntiles = (a.T + kTok - 1) / kTok;
+  const int tb = chunk * a.tiles_per_wg;
+  const int te = min(ntiles, tb + a.tiles_per_wg);
+  if (tb >= te) return;
+
+  const char* xs = a.x + 2 * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
+  const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
+
+  // K range of this wave's rows: the group of channels 32w.. (whole head for g = 128)
+  const int kbase = a.g >= 32 ? (32 * w / a.g) * a.g : 32 * w;
+  // A row m of this wave computes output channel 32w + 16*((m/4)%2) + 4*(m/8) + m%4
+  const int chA = 32 * w + 16 * ((n >> 2) & 1) + 4 * (n >> 3) + (n & 3);
+  bf16x8_t A[NP][KS];
+  load_a<NP, KS>(A, a, l, h, chA, kbase, hc);
+
+  // global -> register staging: thread owns granules c = tid and tid + 256 of the 512-granule tile
+  u32x4_t stage[2];
+  auto fetch = [&](int tile) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int c = threadIdx.x + q * kThreads;
+      const int tok = min(tile * kTok + (c >> 4), a.T - 1);
+      stage[q] = *(const u32x4_t*)(xs + 2 * size_t(tok) * a.st + 16 * (c & 15));
+    }
+  };
+  auto put = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int c = threadIdx.x + q * kThreads;
+      const int row = c >> 4;
+      *(u32x4_t*)(&xtile[buf][row * kRowBytes + 16 * swz(row, c & 15)]) = stage[q];
+    }
+  };
+
+  int flags = 0;
+  fetch(tb);
+  put(0);
+  if (tb + 1 < te) fetch(tb + 1);
+  __syncthreads();
+
+  const float qmax = float((1 << BITS) - 1);
+  for (int tile = tb; tile < te; ++tile) {
+    const int buf = (tile - tb) & 1;
+    if (tile + 1 < te) {
+      put(buf ^ 1);
+      if (tile + 2 < te) fetch(tile + 2);
+    }
+    // B fragments: token n, input channels kbase + 16kk + 8hc .. +8
+    const uint8_t* rowp = &xtile[buf][n * kRowBytes];
+    f32x16_t acc0 = {}, acc1 = {};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const int j = (kbase >> 3) + 2 * kk + hc;
+      const bf16x8_t bv = as_bf16x8(*(const u32x4_t*)(rowp + 16 * swz(n, j)));
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        if ((kk * NP + p) & 1) acc1 = mfma(A[p][kk], bv, acc1);
+        else acc0 = mfma(A[p][kk], bv, acc0);
+      }
+    }
+    float z[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) z[e] = acc0[e] + acc1[e];
+
+    const int tok = tile * kTok + n;
+    const bool live = tok < a.T;
+    const size_t crow = cslice * a.T_cap + size_t(a.t0 + tok);
+
+    if constexpr (PASS) {
+      if (live) {
+        float* dst = (float*)a.codes + crow * kD + 32 * w + 16 * hc;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) *(float4*)(dst + 4 * q) = make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
+      }
+    } else {
+      bool bad = false;
+      float mn = z[0], mx = z[0];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        bad |= z[e] != z[e];
+        mn = fminf(mn, z[e]);
+        mx = fmaxf(mx, z[e]);
+      }
+      if constexpr (NB >= 32) {
+        mn = fminf(mn, __shfl_xor(mn, 32));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+      }
+      if constexpr (NB == 64) {
+        if (hc == 0) red[w][n] = make_float2(mn, mx);
+        __syncthreads();
+        const float2 o = red[w ^ 1][n];
+        mn = fminf(mn, o.x);
+        mx = fmaxf(mx, o.y);
+      }
+      if (!(mn >= -3.0e38f && mx <= 3.0e38f)) bad = true;  // +-inf in the block
+      const Side sd = make_side(mn, mx, BITS);
+      uint32_t q[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) q[e] = quantize(z[e], sd.mn, sd.inv, qmax);
+      uint8_t* crowp = a.codes + crow * (kD * BITS / 8);
+      if constexpr ((BITS & 1) == 0) {
+        if (live) {
+          uint32_t words[BITS / 2];
+          pack16<BITS>(q, words);
+          store_words<BITS / 2>((uint32_t*)(crowp + (4 * w + 2 * hc) * BITS), words);
+        }
+      } else {
+        // 16 odd-width codes span 1.5 words: the lane pair of a token packs its 32 codes
+        // (BITS words) together and the lower half stores them
+        uint32_t hq[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) hq[e] = __shfl_xor(q[e], 32);
+        if (live && hc == 0) {
+          uint32_t words[BITS];
+#pragma unroll
+          for (int i = 0; i < BITS; ++i) words[i] = 0;
+#pragma unroll
+          for (int e = 0; e < 32; ++e) {
+            const uint32_t v = e < 16 ? q[e] : hq[e - 16];
+            const int bit = e * BITS, wd = bit >> 5, off = bit & 31;
+            words[wd] |= v << off;
+            if (off + BITS > 32) words[wd + 1] |= v >> (32 - off);
+          }
+          uint32_t* dst = (uint32_t*)(crowp + (4 * w) * BITS);
+#pragma unroll
+          for (int i = 0; i < BITS; ++i) dst[i] = words[i];
+        }
+      }
+      if (live) {
+        flags |= sd.flags | (bad ? CG_FLAG_NONFINITE : 0);
+        const int nbk = kD / NB;
+        if constexpr (NB == 16) {
+          a.side[crow * nbk + 2 * w + hc] = sd.word;
+        } else if constexpr (NB == 32) {
+          if (hc == 0) a.side[crow * nbk + w] = sd.word;
+        } else {
+          if (hc == 0 && (w & 1) == 0) a.side[crow * nbk + (w >> 1)] = sd.word;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (flags && a.err) atomicOr(a.err, flags);
+}
+
+// ------------------------------------------------------------------------------------------
+// decode
+// ------------------------------------------------------------------------------------------
+template <int NP, int KS, int BITS, int NB, bool OUT_BF16>
+__global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
+  constexpr int NBK = kD / NB;                      // blocks per token row
+  __shared__ __attribute__((aligned(16))) uint8_t qtile[2][kTok * kRowBytes];  // codes as bf16
+  __shared__ uint32_t stile[2][kTok * NBK];         // side words
+  __shared__ __attribute__((aligned(16))) float colsum[NBK][kD];
+  __shared__ float mtile[2][kTok][kD / 8];         // per (token, group) centre grid points
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n = lane & 31, hc = lane >> 5;
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int slice = logical / a.chunks, chunk = logical - slice * a.chunks;
+  if (slice >= a.nslices) return;
+  const int h = slice % a.H, b = (slice / a.H) % a.B, lv = slice / (a.H * a.B);
+  const int l = lv + a.l0;
+  int Tv = a.T;  // view tokens to write
+  if (a.pos) {
+    const int p = a.pos[b];
+    if (p < 0 || p >= a.T_cap) return;  // flagged by the append kernel
+    Tv = min(Tv, p + 1 - a.t0);
+  }
+  const int ntiles = (Tv + kTok - 1) / kTok;
+  const int tb = chunk * a.tiles_per_wg;
+  const int te = min(ntiles, tb + a.tiles_per_wg);
+  if (tb >= te) return;
+  char* ys = a.x + (OUT_BF16 ? 2 : 4) * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
+  const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
+
+  const int kbase = a.g >= 32 ? (32 * w / a.g) * a.g : 32 * w;
+  const int chA = 32 * w + 16 * ((n >> 2) & 1) + 4 * (n >> 3) + (n & 3);
+  bf16x8_t A[NP][KS];
+  load_a<NP, KS>(A, a, l, h, chA, kbase, hc);  // a.gp holds the G^T planes for decode
+
+  // Centring: with groups no smaller than blocks every block is centred on its grid midpoint
+  // (code 2^(b-1)); with groups smaller than blocks (only g <= 32) every (token, group) is
+  // centred on the code of the group's first channel, so a group whose codes are all equal
+  // decodes from the midpoint term alone.
+  const bool gc = KS == 2 && a.g < NB;
+  // column sums: per block (colsum[k][i] = sum_{j in block k} G[j][i]) or, when centring per
+  // group, per group (colsum[0][i] = sum_{j in group(i)} G[j][i]); binary64 sums
+  for (int idx = threadIdx.x; idx < NBK * kD; idx += kThreads) {
+    const int k = idx / kD, i = idx - k * kD;
+    const int g = a.g, r = i / g;
+    const float* Gb = a.g32 + (((size_t(l) * 2 + a.s) * a.Hg + h) * a.R + r) * g * g;
+    double acc = 0.0;
+    const int j0 = gc ? r * g : k * NB, j1 = gc ? (r + 1) * g : (k + 1) * NB;
+    if (!gc || k == 0) {
+      for (int j = j0; j < j1; ++j)
+        if (j / g == r) acc += double(Gb[size_t(j % g) * g + (i % g)]);
+      colsum[k][i] = float(acc);
+    }
+  }
+
+  // staging of a tile's code rows: thread owns token tid/8, channels 16*(tid%8) .. +16
+  const int st_tok = threadIdx.x >> 3, st_seg = threadIdx.x & 7;
+  const int st_blk = (16 * st_seg) / NB;           // block of the thread's channels
+  constexpr int SEGW = (16 * BITS + 31) / 32 + 1;  // words covering one 16-code segment
+  uint32_t cw[SEGW];
+  uint32_t sw = 0, cfirst = 0;
+  auto fetch = [&](int tile) {
+    const int tok = min(tile * kTok + st_tok, Tv - 1);
+    const size_t crow = cslice * a.T_cap + size_t(a.t0 + tok);
+    const uint32_t* row = (const uint32_t*)(a.codes + crow * (kD * BITS / 8));
+    const int bit0 = 16 * st_seg * BITS;
+#pragma unroll
+    for (int i = 0; i < SEGW; ++i) {
+      const int wi = (bit0 >> 5) + i;
+      cw[i] = wi < kD * BITS / 32 ? row[wi] : 0u;
+    }
+    // shift the segment down to bit 0 (odd widths start mid-word)
+#pragma unroll
+    for (int i = 0; i + 1 < SEGW; ++i) cw[i] = __builtin_amdgcn_alignbit(cw[i + 1], cw[i], bit0 & 31);
+    sw = a.side[crow * NBK + st_blk];
+    // first code of a 32-channel group that starts in the previous segment (word aligned)
+    if (gc && a.g == 32 && (st_seg & 1)) cfirst = row[(32 * (st_seg >> 1) * BITS) >> 5] & ((1u << BITS) - 1u);
+  };
+  auto put = [&](int buf) {
+    uint32_t q[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int bit = e * BITS, wd = bit >> 5, off = bit & 31;
+      uint32_t v = cw[wd] >> off;
+      if (off + BITS > 32) v |= cw[wd + 1] << (32 - off);
+      q[e] = v & ((1u << BITS) - 1u);
+    }
+    // centre of the first and second half of the segment
+    int c0 = 1 << (BITS - 1), c1 = c0;
+    if (gc) {
+      c0 = (a.g == 32 && (st_seg & 1)) ? int(cfirst) : int(q[0]);
+      c1 = a.g == 8 ? int(q[8]) : c0;
+    }
+    uint32_t v[8];
+#pragma unroll
+    for (int e = 0; e < 16; e += 2) {
+      const int c = e < 8 ? c0 : c1;
+      // bf16 of q - c: exact, |q - c| <= 255
+      v[e >> 1] = (__float_as_uint(float(int(q[e]) - c)) >> 16) |
+                  ((__float_as_uint(float(int(q[e + 1]) - c)) >> 16) << 16);
+    }
+    uint8_t* rowp = &qtile[buf][st_tok * kRowBytes];
+    *(u32x4_t*)(rowp + 16 * swz(st_tok, 2 * st_seg)) = u32x4_t{v[0], v[1], v[2], v[3]};
+    *(u32x4_t*)(rowp + 16 * swz(st_tok, 2 * st_seg + 1)) = u32x4_t{v[4], v[5], v[6], v[7]};
+    if ((16 * st_seg) % NB == 0) stile[buf][st_tok * NBK + st_blk] = sw;
+    if (gc) {
+      // grid point of each group's centre code, written by the thread holding the group start
+      const float mn = f16_bits_to_f32(sw & 0xffffu), sc = f16_bits_to_f32(sw >> 16);
+      if (a.g == 8) {
+        mtile[buf][st_tok][2 * st_seg] = mn + float(c0) * sc;
+        mtile[buf][st_tok][2 * st_seg + 1] = mn + float(c1) * sc;
+      } else if (a.g == 16) {
+        mtile[buf][st_tok][st_seg] = mn + float(c0) * sc;
+      } else if ((st_seg & 1) == 0) {
+        mtile[buf][st_tok][st_seg >> 1] = mn + float(c0) * sc;
+      }
+    }
+  };
+
+  fetch(tb);
+  put(0);
+  if (tb + 1 < te) fetch(tb + 1);
+  __syncthreads();
+
+  // K range split into block segments of KSS K-steps each
+  constexpr int KR = KS * 16;
+  constexpr int SEG = (KR < NB ? KR : NB) / 16;
+  constexpr int NSEG = KS / SEG;
+  for (int tile = tb; tile < te; ++tile) {
+    const int buf = (tile - tb) & 1;
+    if (tile + 1 < te) {
+      put(buf ^ 1);
+      if (tile + 2 < te) fetch(tile + 2);
+    }
+    const uint8_t* rowp = &qtile[buf][n * kRowBytes];
+    float y[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) y[e] = 0.0f;
+#pragma unroll
+    for (int sgi = 0; sgi < NSEG; ++sgi) {
+      f32x16_t acc0 = {}, acc1 = {};
+#pragma unroll
+      for (int u = 0; u < SEG; ++u) {
+        const int kk = sgi * SEG + u;
+        const int j = (kbase >> 3) + 2 * kk + hc;
+        const bf16x8_t bv = as_bf16x8(*(const u32x4_t*)(rowp + 16 * swz(n, j)));
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          if ((u * NP + p) & 1) acc1 = mfma(A[p][kk], bv, acc1);
+          else acc0 = mfma(A[p][kk], bv, acc0);
+        }
+      }
+      const int blk = (kbase + 16 * SEG * sgi) / NB;
+      const uint32_t swd = stile[buf][n * NBK + blk];
+      const float sc = f16_bits_to_f32(swd >> 16);
+      if (gc) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) y[e] = fmaf(sc, acc0[e] + acc1[e], y[e]);
+      } else {
+        const float mid = f16_bits_to_f32(swd & 0xffffu) + float(1 << (BITS - 1)) * sc;  // grid midpoint
+        const float4* cs = (const float4*)&colsum[blk][32 * w + 16 * hc];
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 c = cs[q4];
+          const float cc[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int e = 4 * q4 + u;
+            y[e] = fmaf(sc, acc0[e] + acc1[e], fmaf(mid, cc[u], y[e]));
+          }
+        }
+      }
+    }
+    if (gc) {
+      // centre term of the row's group (one group per lane, two for g = 8)
+      const int ch0 = 32 * w + 16 * hc;
+      const float m0 = mtile[buf][n][ch0 / a.g];
+      const float m1 = mtile[buf][n][(ch0 + 8) / a.g];
+      const float4* cs = (const float4*)&colsum[0][ch0];
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const float4 c = cs[q4];
+        const float cc[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int e = 4 * q4 + u;
+          y[e] = fmaf(e < 8 ? m0 : m1, cc[u], y[e]);
+        }
+      }
+    }
+    const int tok = tile * kTok + n;
+    if (tok < Tv) {
+      if constexpr (OUT_BF16) {
+        uint32_t pk[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pk[e] = f32_to_bf16_rne(y[2 * e]) | (f32_to_bf16_rne(y[2 * e + 1]) << 16);
+        uint16_t* dst = (uint16_t*)ys + size_t(tok) * a.st + 32 * w + 16 * hc;
+        *(u32x4_t*)dst = u32x4_t{pk[0], pk[1], pk[2], pk[3]};
+        *(u32x4_t*)(dst + 8) = u32x4_t{pk[4], pk[5], pk[6], pk[7]};
+      } else {
+        float* dst = (float*)ys + size_t(tok) * a.st + 32 * w + 16 * hc;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) *(float4*)(dst + 4 * q) = make_float4(y[4 * q], y[4 * q + 1], y[4 * q + 2], y[4 * q + 3]);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// dispatch
+// ------------------------------------------------------------------------------------------
+constexpr int kNP = 3;
+
+int cu_count() {
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      cus = 256;
+  }
+  return cus;
+}
+
+// Split the (slice, tile) space into workgroups: about two resident workgroups per CU, each a
+// contiguous tile range of one slice; the count is padded to a multiple of 8 (XCD remap).
+void plan(MfmaArgs& m, int nslices, int T) {
+  const int ntiles = (T + kTok - 1) / kTok;
+  const int target = 2 * cu_count();
+  int chunks = (target + nslices - 1) / nslices;
+  chunks = chunks < 1 ? 1 : (chunks > ntiles ? ntiles : chunks);
+  m.tiles_per_wg = (ntiles + chunks - 1) / chunks;
+  m.chunks = (ntiles + m.tiles_per_wg - 1) / m.tiles_per_wg;
+  m.nslices = nslices;
+}
+
+template <int KS, int BITS, int NB>
+void* enc_kernel(bool pass) {
+  if (pass) return (void*)enc_mfma<kNP, KS, 8, 64, true>;
+  return (void*)enc_mfma<kNP, KS, BITS, NB, false>;
+}
+
+template <int KS, int BITS>
+void* enc_by_nb(int nb, bool pass) {
+  switch (nb) {
+    case 16: return enc_kernel<KS, BITS, 16>(pass);
+    case 32: return enc_kernel<KS, BITS, 32>(pass);
+    case 64: return enc_kernel<KS, BITS, 64>(pass);
+  }
+  return nullptr;
+}
+
+template <int KS>
+void* enc_by_bits(int bits, int nb, bool pass) {
+  switch (bits) {
+    case 2: return enc_by_nb<KS, 2>(nb, pass);
+    case 3: return enc_by_nb<KS, 3>(nb, pass);
+    case 4: return enc_by_nb<KS, 4>(nb, pass);
+    case 6: return enc_by_nb<KS, 6>(nb, pass);
+    case 8: return enc_by_nb<KS, 8>(nb, pass);
+  }
+  return nullptr;
+}
+
+template <int KS, int BITS, int NB>
+void* dec_kernel(bool bf16) {
+  if (bf16) return (void*)dec_mfma<kNP, KS, BITS, NB, true>;
+  return (void*)dec_mfma<kNP, KS, BITS, NB, false>;
+}
+
+template <int KS, int BITS>
+void* dec_by_nb(int nb, bool bf16) {
+  switch (nb) {
+    case 16: return dec_kernel<KS, BITS, 16>(bf16);
+    case 32: return dec_kernel<KS, BITS, 32>(bf16);
+    case 64: return dec_kernel<KS, BITS, 64>(bf16);
+  }
+  return nullptr;
+}
+
+template <int KS>
+void* dec_by_bits(int bits, int nb, bool bf16) {
+  switch (bits) {
+    case 2: return dec_by_nb<KS, 2>(nb, bf16);
+    case 3: return dec_by_nb<KS, 3>(nb, bf16);
+    case 4: return dec_by_nb<KS, 4>(nb, bf16);
+    case 6: return dec_by_nb<KS, 6>(nb, bf16);
+    case 8: return dec_by_nb<KS, 8>(nb, bf16);
+  }
+  return nullptr;
+}
+
+int ksteps(int g) { return g >= 128 ? 8 : (g == 64 ? 4 : 2); }
+
+bool group_ok(int g) { return g == 8 || g == 16 || g == 32 || g == 64 || g == 128; }
+
+bool bits_ok(int b) { return b == 2 || b == 3 || b == 4 || b == 6 || b == 8; }
+
+}  // namespace
+
+bool mfma_encode_supported(const ViewDev& X, const GaugeDev& G, const CodecDev& c) {
+  if (!X.bf16 || X.d != kD || !group_ok(G.g)) return false;
+  if (c.backend == CG_BACKEND_PASSTHROUGH) return true;
+  return c.backend == CG_BACKEND_BLOCK_UNIFORM && bits_ok(c.bits) && (c.n == 16 || c.n == 32 || c.n == 64);
+}
+
+bool mfma_decode_supported(const ViewDev& Y, const GaugeDev& G, const CodecDev& c) {
+  if (Y.d != kD || !group_ok(G.g)) return false;
+  return c.backend == CG_BACKEND_BLOCK_UNIFORM && bits_ok(c.bits) && (c.n == 16 || c.n == 32 || c.n == 64);
+}
+
+hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c,
+                              const CacheDev& k, int t0, int* err, hipStream_t st) {
+  if (X.T == 0) return hipSuccess;
+  MfmaArgs m{};
+  m.x = (char*)X.ptr;
+  m.sl = X.sl; m.sb = X.sb; m.sh = X.sh; m.st = X.st;
+  m.L = X.L; m.B = X.B; m.H = X.H; m.T = X.T;
+  m.l0 = l0; m.s = s; m.t0 = t0;
+  for (int p = 0; p < 3; ++p) m.gp[p] = G.hi[p];
+  m.g32 = G.f32; m.g = G.g; m.R = G.R; m.Hg = G.H;
+  m.codes = k.codes; m.side = k.side; m.T_cap = k.T_cap; m.cB = k.B; m.cH = k.H;
+  m.err = err;
+  plan(m, X.L * X.B * X.H, X.T);
+  void* fn = nullptr;
+  const bool pass = c.backend == CG_BACKEND_PASSTHROUGH;
+  switch (ksteps(G.g)) {
+    case 2: fn = enc_by_bits<2>(pass ? 8 : c.bits, pass ? 64 : c.n, pass); break;
+    case 4: fn = enc_by_bits<4>(pass ? 8 : c.bits, pass ? 64 : c.n, pass); break;
+    case 8: fn = enc_by_bits<8>(pass ? 8 : c.bits, pass ? 64 : c.n, pass); break;
+  }
+  if (!fn) return hipErrorInvalidValue;
+  const int nwg = ((m.nslices * m.chunks + 7) / 8) * 8;
+  void* args[] = {&m};
+  return hipLaunchKernel(fn, dim3(nwg), dim3(kThreads), args, 0, st);
+}
+
+hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
+                              const int* pos, const ViewDev& Y, int* err, hipStream_t st) {
+  if (Y.T == 0) return hipSuccess;
+  MfmaArgs m{};
+  m.x = (char*)Y.ptr;
+  m.sl = Y.sl; m.sb = Y.sb; m.sh = Y.sh; m.st = Y.st;
+  m.L = Y.L; m.B = Y.B; m.H = Y.H; m.T = Y.T;
+  m.l0 = l0; m.s = s; m.t0 = t0;
+  for (int p = 0; p < 3; ++p) m.gp[p] = G.tr[p];
+  m.g32 = G.f32; m.g = G.g; m.R = G.R; m.Hg = G.H;
+  m.codes = k.codes; m.side = k.side; m.T_cap = k.T_cap; m.cB = k.B; m.cH = k.H;
+  m.pos = pos;
+  m.err = err;
+  plan(m, Y.L * Y.B * Y.H, Y.T);
+  void* fn = nullptr;
+  switch (ksteps(G.g)) {
+    case 2: fn = dec_by_bits<2>(c.bits, c.n, Y.bf16); break;
+    case 4: fn = dec_by_bits<4>(c.bits, c.n, Y.bf16); break;
+    case 8: fn = dec_by_bits<8>(c.bits, c.n, Y.bf16); break;
+  }
+  if (!fn) return hipErrorInvalidValue;
+  const int nwg = ((m.nslices * m.chunks + 7) / 8) * 8;
+  void* args[] = {&m};
+  return hipLaunchKernel(fn, dim3(nwg), dim3(kThreads), args, 0, st);
+}
+
+}  // namespace cg

@@ -17,6 +17,7 @@ Streams are numpy Philox generators keyed through a SeedSequence of
 from __future__ import annotations
 
 import dataclasses
+import os
 
 import numpy as np
 
@@ -128,10 +129,20 @@ def kv_tensor(w: Workload, s: int, L: int | None = None, B: int | None = None, H
     H = w.H if H is None else H
     T = w.T if T is None else T
     f = np.empty((L, B, H, T, w.d), dtype=np.float32)
-    for li in range(L):
-        for b in range(B):
-            for h in range(H):
-                f[li, b, h] = kv_slice(w.data_seed, s, l0 + li, b, h, T, w.d, w.keys, t_offset)
+
+    def fill(idx):
+        li, b, h = idx
+        f[li, b, h] = kv_slice(w.data_seed, s, l0 + li, b, h, T, w.d, w.keys, t_offset)
+
+    jobs = [(li, b, h) for li in range(L) for b in range(B) for h in range(H)]
+    if len(jobs) * T * w.d >= (1 << 22):
+        from concurrent.futures import ThreadPoolExecutor
+
+        with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(fill, jobs))
+    else:
+        for j in jobs:
+            fill(j)
     if w.dtype == "bf16":
         return round_bf16_bits(f)
     return f

@@ -25,6 +25,16 @@ def _gpu():
     cg.lib()
 
 
+@pytest.fixture(params=["mfma", "generic"])
+def kernels(request, monkeypatch):
+    """Run a case on the matrix-core kernels (the default dispatch) and on the general ones."""
+    if request.param == "generic":
+        monkeypatch.setenv("CG_KERNELS", "generic")
+    else:
+        monkeypatch.delenv("CG_KERNELS", raising=False)
+    return request.param
+
+
 def _workload(T, L=1, B=2, H=2, d=128, dtype="bf16", seed=0xBEEF):
     return synth.Workload("case", L=L, B=B, H=H, T=T, d=d, dtype=dtype, g=0, backend="bu", bits=4,
                           data_seed=seed)
@@ -58,7 +68,7 @@ def _decode_gpu(dev, s, Gd, shp, oc, t0, T, dtype=torch.bfloat16):
 # ------------------------------------------------------------------------------------------
 @pytest.mark.parametrize("g", [8, 16, 32, 64, 128])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_gauge_stage_matches_oracle(g, dtype):
+def test_gauge_stage_matches_oracle(g, dtype, kernels):
     w = _workload(T=77, dtype=dtype)
     G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, g)
     oc = O.Codec(backend=O.PASSTHROUGH)
@@ -86,11 +96,14 @@ QCASES = [(O.BLOCK_UNIFORM, b, n) for b in (2, 3, 4, 6, 8) for n in (32, 64)] + 
 
 
 @pytest.mark.parametrize("backend,bits,n", QCASES)
-def test_quantise_and_dequantise_are_bit_exact(backend, bits, n):
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_quantise_and_dequantise_are_bit_exact(backend, bits, n, dtype, kernels):
     """Identity gauge: z = x exactly on both sides, so codes, side information, packed bytes
     and the dequantised values must agree bit for bit."""
+    if backend == O.KIVI and dtype == "f32":
+        pytest.skip("KIVI caches are bf16")
     T = 300 if backend == O.KIVI else 97
-    w = _workload(T=T, dtype="bf16" if backend == O.KIVI else "f32")
+    w = _workload(T=T, dtype=dtype)
     G, Gd, shp = _gauge(O.GAUGE_IDENTITY, 1, 2, 128, 32)
     oc = O.Codec(backend=backend, bits=bits, block_c=n, val_channels=n, key_tokens=32, residual=128)
     T_cap = 320
@@ -131,7 +144,7 @@ FCASES = [(128, 4, 64, O.GAUGE_HAAR), (128, 6, 64, O.GAUGE_HAAR), (128, 3, 64, O
 
 
 @pytest.mark.parametrize("g,bits,n,kind", FCASES)
-def test_fused_encoder_and_decoder(g, bits, n, kind):
+def test_fused_encoder_and_decoder(g, bits, n, kind, kernels):
     T = 261
     w = _workload(T=T, L=2, B=1, H=2)
     G, Gd, shp = _gauge(kind, 2, 2, 128, g)
@@ -213,7 +226,7 @@ def test_kivi_short_cache_decodes_as_a_copy():
 @pytest.mark.parametrize("backend,kind", [(O.BLOCK_UNIFORM, O.GAUGE_IDENTITY), (O.KIVI, O.GAUGE_IDENTITY),
                                           (O.PASSTHROUGH, O.GAUGE_IDENTITY), (O.BLOCK_UNIFORM, O.GAUGE_HAAR),
                                           (O.KIVI, O.GAUGE_HAAR)])
-def test_append_step_matches_oracle(backend, kind):
+def test_append_step_matches_oracle(backend, kind, kernels):
     """Rolling history (section 4.4): T0 tokens encoded by the oracle and uploaded, then
     steps appended on both sides with a different position per batch row; the identity gauge
     makes every stage exact, so caches and decoded histories must agree bit for bit; with a
@@ -285,7 +298,7 @@ def test_append_step_flags_positions_beyond_capacity():
 # ------------------------------------------------------------------------------------------
 # edge cases
 # ------------------------------------------------------------------------------------------
-def test_empty_offset_and_strided_views():
+def test_empty_offset_and_strided_views(kernels):
     G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, 128)
     oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=4, block_c=64)
     w = _workload(T=90)
@@ -319,7 +332,7 @@ def test_empty_offset_and_strided_views():
 
 
 @pytest.mark.parametrize("backend", [O.BLOCK_UNIFORM, O.KIVI])
-def test_outputs_stay_inside_their_buffers(backend):
+def test_outputs_stay_inside_their_buffers(backend, kernels):
     """Guard bands: bytes after every cache buffer and after the decode output are untouched."""
     G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, 32)
     oc = O.Codec(backend=backend, bits=3, block_c=64)
@@ -345,7 +358,7 @@ def test_outputs_stay_inside_their_buffers(backend):
     assert bool((Y[:, :, :, T:] == 7.0).all())
 
 
-def test_error_flags():
+def test_error_flags(kernels):
     G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, 128)
     oc = cg.Codec(cg.BLOCK_UNIFORM, 4, 64)
     X = torch.randn((1, 1, 2, 40, 128), device="cuda").to(torch.bfloat16)
@@ -366,7 +379,7 @@ def test_error_flags():
     assert int(err.item()) & cg.CG_FLAG_SIDE_OVERFLOW
 
 
-def test_encode_is_deterministic():
+def test_encode_is_deterministic(kernels):
     G, Gd, shp = _gauge(O.GAUGE_HAAR, 2, 2, 128, 128)
     oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=4, block_c=64)
     X = synth.kv_tensor(_workload(T=1000, L=2), 0)
