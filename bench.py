@@ -34,6 +34,8 @@ def parse():
     ap.add_argument("--cpu-sample-layers", type=int, default=2)
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic_llama8b.json"),
                     help="HBM traffic per launch measured with rocprofv3 counters (optional)")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="after the timed region, run one plain 512 MiB device copy (counter calibration)")
     return ap.parse_args()
 
 
@@ -149,6 +151,13 @@ def main():
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": dom_name,
                 "kernel_ms": round(dom_ms, 4), "encode_ms": round(enc_ms, 4), "decode_ms": round(dec_ms, 4),
                 "alg_bytes_per_launch": int(alg)}
+
+    if args.copy_probe:
+        src = torch.empty(256 << 20, dtype=torch.int16, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:

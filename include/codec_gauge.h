@@ -188,6 +188,16 @@ int32_t kv_append_step(int32_t l0, int32_t l1, const cg_kv_view* k_new, const cg
                        const cg_cache* vc, const cg_kv_view* k_hist, const cg_kv_view* v_hist, int32_t* err_flag,
                        void* stream);
 
+/* Device self-test of the two binary32 steps of the quantiser the kernels compute without a
+ * division (section 4.3 block range; the oracle divides): which = 0 compares the reciprocal
+ * of every positive finite binary16 scale with correctly rounded 1/s; which = 1 compares the
+ * block range divided by 2^b - 1, b in {2,3,4,6,8}, with correctly rounded division for every
+ * binary32 significand in the lowest four binades, binades 100..103, binade 127 and the top
+ * five, and counts the ranges whose binary16 scale (rounded up) would differ.  Adds the
+ * number of mismatches to the caller-zeroed device uint64 *mismatches_dev (8-byte aligned)
+ * on `stream`; a correct build adds 0.  Errors: CG_ERR_ARG, CG_ERR_ALIGN, CG_ERR_DEVICE. */
+int32_t cg_selftest(int32_t which, uint64_t* mismatches_dev, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,7 +24,7 @@ PASSTHROUGH, BLOCK_UNIFORM, KIVI = 0, 1, 2
 DTYPE_BF16, DTYPE_F32 = 0, 1
 
 EXPORTS = ["cg_status_str", "gauge_device_bytes", "gauge_make", "cache_bytes", "kv_encode", "kv_decode",
-           "kv_append_step"]
+           "kv_append_step", "cg_selftest"]
 
 
 class GaugeShape(C.Structure):
@@ -81,6 +81,8 @@ def lib() -> C.CDLL:
                                      C.POINTER(CodecStruct), C.POINTER(CacheStruct), C.POINTER(CacheStruct),
                                      C.POINTER(KvView), C.POINTER(KvView), p, p]
         L.kv_append_step.restype = i32
+        L.cg_selftest.argtypes = [i32, p, p]
+        L.cg_selftest.restype = i32
         _lib = L
     return _lib
 
@@ -205,6 +207,12 @@ def kv_decode(s: int, cache: Cache, G_dev, shp: GaugeShape, codec: Codec, t0: in
     rc = lib().kv_decode(s, C.byref(ks), _ptr(G_dev), shp, C.byref(cs), t0, C.byref(v), _ptr(err_flag),
                          _stream(stream))
     _check("kv_decode", rc)
+
+
+def cg_selftest(which: int, mismatches_dev, stream=None):
+    """Adds the mismatch count of device self-test `which` to the uint64 device tensor."""
+    rc = lib().cg_selftest(which, _ptr(mismatches_dev), _stream(stream))
+    _check("cg_selftest", rc)
 
 
 def kv_append_step(l0: int, l1: int, k_new, v_new, pos, G_dev, shp: GaugeShape, codec: Codec, kc: Cache,

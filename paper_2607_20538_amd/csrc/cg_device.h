@@ -39,6 +39,26 @@ __device__ __forceinline__ uint32_t f16_bits_up(float v) {
   return bits == 0x8000u ? 0u : bits;
 }
 
+// RN(a / (2^b - 1)) without a division: q0 = RN(a r) with r = RN(1 / d), the exact residual
+// e = a - q0 d (one FMA), then RN(q0 + e r) (Markstein's correction step).  cg_selftest(1)
+// checks it against correctly rounded division for every binary32 mantissa of the binades
+// the quantiser meets.
+__device__ __forceinline__ float div_by_qmax(float a, int bits) {
+  const float d = float((1 << bits) - 1);
+  const float r = 1.0f / d;
+  const float q0 = a * r;
+  const float e = fmaf(-q0, d, a);
+  return fmaf(e, r, q0);
+}
+
+// RN(1 / s) for a positive binary16 value s: hardware estimate, then one Newton step on the
+// exact residual.  cg_selftest(0) checks it for every positive finite binary16 value.
+__device__ __forceinline__ float rcp_of_f16(float s) {
+  const float y = __builtin_amdgcn_rcpf(s);
+  const float e = fmaf(-s, y, 1.0f);
+  return fmaf(e, y, y);
+}
+
 // Side information of one quantisation block from its exact min and max (section 4.3
 // block range): binary16 min rounded down, binary16 scale rounded up, binary32 reciprocal.
 struct Side {
@@ -53,10 +73,10 @@ __device__ __forceinline__ Side make_side(float mn, float mx, int bits) {
   uint32_t mnb = f16_bits_down(mn);
   s.mn = f16_bits_to_f32(mnb);
   float diff = mx - s.mn;
-  float s32 = diff / (float)((1 << bits) - 1);   // correctly rounded binary32 division
+  float s32 = div_by_qmax(diff, bits);           // = RN(diff / (2^b - 1))
   uint32_t scb = f16_bits_up(s32);
   s.sc = f16_bits_to_f32(scb);
-  s.inv = (s.sc == 0.0f) ? 0.0f : 1.0f / s.sc;  // correctly rounded reciprocal
+  s.inv = (s.sc == 0.0f) ? 0.0f : rcp_of_f16(s.sc);  // = RN(1 / sc)
   s.word = mnb | (scb << 16);
   s.flags = (((mnb & 0x7c00u) == 0x7c00u) || ((scb & 0x7c00u) == 0x7c00u)) ? CG_FLAG_SIDE_OVERFLOW : 0;
   return s;
@@ -69,6 +89,16 @@ __device__ __forceinline__ uint32_t quantize(float z, float mn, float inv, float
   float r = __builtin_rintf(t);
   r = fminf(fmaxf(r, 0.0f), qmax);
   return (uint32_t)r;
+}
+
+// rint_even(fl32(fl32(z - mn) * inv)) as an integer-valued float.  No clamp is needed: with
+// mn_h <= min z the difference is >= 0, and with sc_h >= RN(range / qmax) the product is at
+// most qmax (1 + 4 * 2^-24) < qmax + 1/2, so the rounded value lies in [0, qmax] for finite
+// blocks (non-finite blocks raise an error flag and their codes are unspecified).
+__device__ __forceinline__ float quantize_rint(float z, float mn, float inv) {
+#pragma clang fp contract(off)
+  float t = (z - mn) * inv;
+  return __builtin_rintf(t);
 }
 
 // zhat = fl32(mn + q * sc); q * sc is exact in binary32.

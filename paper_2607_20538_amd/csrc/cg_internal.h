@@ -87,6 +87,9 @@ hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G
 hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
                               const int* pos, const ViewDev& Y, int* err, hipStream_t st);
 
+// Device self-test of the quantiser's division-free steps (which: 0 reciprocal, 1 division).
+hipError_t launch_selftest(int which, unsigned long long* bad, hipStream_t st);
+
 // Dispatching launchers (hip stream passed through).  All validate nothing: the host entry points do.
 // Encode tokens [0, X.T) of view X into cache positions [t0, t0 + X.T); layer l of the view is
 // cache layer l + l0.  tq: KIVI tokens to quantise (others go to the window).

@@ -27,6 +27,8 @@
 // computed once per workgroup in binary64.  Centring keeps the two terms small when a block
 // spans a group whose values sit far from the block's minimum (an outlier in another group
 // of the same block), where mn * colsum and sc * G^T q would cancel.
+#include <type_traits>
+
 #include "cg_internal.h"
 #include "cg_device.h"
 
@@ -42,6 +44,11 @@ constexpr int kD = 128;          // head dimension handled here
 constexpr int kTok = 32;         // tokens per tile (MFMA N)
 constexpr int kThreads = 256;    // four waves
 constexpr int kRowBytes = kD * 2;
+constexpr int kStages = 6;       // encoder LDS ring: tiles in flight + the one being read
+// s_waitcnt immediate (gfx9 encoding: vmcnt[3:0] and [15:14], expcnt[6:4], lgkmcnt[11:8])
+// waiting until at most `vm` vector-memory operations are outstanding, with lgkmcnt = 0 (all
+// LDS operations of the wave done) and no wait on expcnt
+constexpr int waitcnt_imm(int vm) { return (vm & 15) | ((vm >> 4) << 14) | (7 << 4) | (0 << 8); }
 
 struct MfmaArgs {
   // view (input for encode, output for decode)
@@ -133,10 +140,30 @@ __device__ __forceinline__ void store_words(uint32_t* dst, const uint32_t* v) {
 // ------------------------------------------------------------------------------------------
 // encode
 // ------------------------------------------------------------------------------------------
+
+// z (32 rows x 32 tokens) of one tile: the NP split planes times the tile, one chain.
+template <int NP, int KS>
+__device__ __forceinline__ f32x16_t mfma_chain(const bf16x8_t (&A)[NP][KS], const bf16x8_t (&Bf)[KS]) {
+  f32x16_t acc = {};
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+    for (int p = 0; p < NP; ++p) acc = mfma(A[p][kk], Bf[kk], acc);
+  return acc;
+}
+
+// Software pipeline over 32-token tiles, one barrier per tile.  Iteration t:
+//   1. block-range partials of tile t from its accumulator (64-channel blocks: wave-pair
+//      exchange through red[t & 1]);
+//   2. wait for tile t+1's LDS-direct loads, barrier, issue the loads of tile t+kStages-1
+//      into the buffer tile t-1 used, read the B fragments of tile t+1;
+//   3. matrix-core chain of tile t+1 interleaved with side info, quantisation, packing and
+//      stores of tile t.
+// kStages - 1 tiles are in flight between global memory and LDS.
 template <int NP, int KS, int BITS, int NB, bool PASS>
 __global__ __launch_bounds__(kThreads, 2) void enc_mfma(MfmaArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t xtile[2][kTok * kRowBytes];
-  __shared__ float2 red[4][kTok];  // per-wave (min, max) of each token, for 64-channel blocks
+  __shared__ __attribute__((aligned(16))) uint8_t xtile[kStages][kTok * kRowBytes];
+  __shared__ float2 red[2][4][kTok];  // per-wave (min, max) of each token, for 64-channel blocks
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n = lane & 31, hc = lane >> 5;
@@ -160,68 +187,73 @@ __global__ __launch_bounds__(kThreads, 2) void enc_mfma(MfmaArgs a) {
   bf16x8_t A[NP][KS];
   load_a<NP, KS>(A, a, l, h, chA, kbase, hc);
 
-  // global -> register staging: thread owns granules c = tid and tid + 256 of the 512-granule tile
-  u32x4_t stage[2];
-  auto fetch = [&](int tile) {
+  // Tiles stream global -> LDS without VGPRs (LDS-direct loads): wave w moves rows
+  // 8w .. 8w+7 of a tile with two 1 KB instructions whose lanes write consecutive 16-byte
+  // LDS granules; lane l of instruction q fetches the logical granule that the XOR swizzle
+  // puts at physical granule l % 16 of row 8w + 4q + l / 16.
+  int drow[2], dcol[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    drow[q] = 8 * w + 4 * q + (lane >> 4);
+    dcol[q] = 16 * swz(drow[q], lane & 15);
+  }
+  const int64_t tstride = 2 * a.st;  // bytes between tokens
+  auto issue = [&](int tile) {
+    uint8_t* dst = xtile[(tile - tb) % kStages];
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const int c = threadIdx.x + q * kThreads;
-      const int tok = min(tile * kTok + (c >> 4), a.T - 1);
-      stage[q] = *(const u32x4_t*)(xs + 2 * size_t(tok) * a.st + 16 * (c & 15));
+      const int tok = min(tile * kTok + drow[q], a.T - 1);
+      __builtin_amdgcn_global_load_lds(xs + tok * tstride + dcol[q],
+                                       (__attribute__((address_space(3))) void*)(dst + (8 * w + 4 * q) * kRowBytes),
+                                       16, 0, 0);
     }
   };
-  auto put = [&](int buf) {
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int c = threadIdx.x + q * kThreads;
-      const int row = c >> 4;
-      *(u32x4_t*)(&xtile[buf][row * kRowBytes + 16 * swz(row, c & 15)]) = stage[q];
+  // Before a barrier: wait until this wave's loads of tile X have landed while the loads of
+  // tiles X+1 .. I (the last one issued) may stay in flight, and until its LDS writes are
+  // done.  VMEM operations complete in issue order; stores issued after those loads only make
+  // the count stricter.
+  auto wait_tile = [&](int X, int I) {
+    switch (I - X) {
+      case 0: __builtin_amdgcn_s_waitcnt(waitcnt_imm(0)); break;
+      case 1: __builtin_amdgcn_s_waitcnt(waitcnt_imm(2)); break;
+      case 2: __builtin_amdgcn_s_waitcnt(waitcnt_imm(4)); break;
+      case 3: __builtin_amdgcn_s_waitcnt(waitcnt_imm(6)); break;
+      default: __builtin_amdgcn_s_waitcnt(waitcnt_imm(8)); break;
     }
+  };
+  int boff[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) boff[kk] = n * kRowBytes + 16 * swz(n, (kbase >> 3) + 2 * kk + hc);
+  bf16x8_t Bf[KS];
+  auto bfrags = [&](int tile) {
+    const uint8_t* src = xtile[(tile - tb) % kStages];
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) Bf[kk] = as_bf16x8(*(const u32x4_t*)(src + boff[kk]));
   };
 
+  // prologue: tiles tb .. tb+kStages-2 in flight, tile tb on the matrix core
+  for (int t = tb; t < min(te, tb + kStages - 1); ++t) issue(t);
+  wait_tile(tb, min(te - 1, tb + kStages - 2));
+  __builtin_amdgcn_s_barrier();
+  bfrags(tb);
+  f32x16_t acc[2];
+  acc[0] = mfma_chain<NP, KS>(A, Bf);
   int flags = 0;
-  fetch(tb);
-  put(0);
-  if (tb + 1 < te) fetch(tb + 1);
-  __syncthreads();
-
-  const float qmax = float((1 << BITS) - 1);
-  for (int tile = tb; tile < te; ++tile) {
-    const int buf = (tile - tb) & 1;
-    if (tile + 1 < te) {
-      put(buf ^ 1);
-      if (tile + 2 < te) fetch(tile + 2);
-    }
-    // B fragments: token n, input channels kbase + 16kk + 8hc .. +8
-    const uint8_t* rowp = &xtile[buf][n * kRowBytes];
-    f32x16_t acc0 = {}, acc1 = {};
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-      const int j = (kbase >> 3) + 2 * kk + hc;
-      const bf16x8_t bv = as_bf16x8(*(const u32x4_t*)(rowp + 16 * swz(n, j)));
-#pragma unroll
-      for (int p = 0; p < NP; ++p) {
-        if ((kk * NP + p) & 1) acc1 = mfma(A[p][kk], bv, acc1);
-        else acc0 = mfma(A[p][kk], bv, acc0);
-      }
-    }
+  // one pipeline step; P = parity of (tile - tb) selects the accumulator, LDS buffer, register
+  // stage and exchange slot at compile time
+  auto step = [&](int tile, auto parity) {
+    constexpr int P = decltype(parity)::value;
     float z[16];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) z[e] = acc0[e] + acc1[e];
-
+    for (int e = 0; e < 16; ++e) z[e] = acc[P][e];
     const int tok = tile * kTok + n;
     const bool live = tok < a.T;
     const size_t crow = cslice * a.T_cap + size_t(a.t0 + tok);
 
-    if constexpr (PASS) {
-      if (live) {
-        float* dst = (float*)a.codes + crow * kD + 32 * w + 16 * hc;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) *(float4*)(dst + 4 * q) = make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
-      }
-    } else {
-      bool bad = false;
-      float mn = z[0], mx = z[0];
+    // 1. block-range partials
+    bool bad = false;
+    float mn = z[0], mx = z[0];
+    if constexpr (!PASS) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         bad |= z[e] != z[e];
@@ -233,32 +265,77 @@ __global__ __launch_bounds__(kThreads, 2) void enc_mfma(MfmaArgs a) {
         mx = fmaxf(mx, __shfl_xor(mx, 32));
       }
       if constexpr (NB == 64) {
-        if (hc == 0) red[w][n] = make_float2(mn, mx);
-        __syncthreads();
-        const float2 o = red[w ^ 1][n];
+        if (hc == 0) red[P][w][n] = make_float2(mn, mx);
+      }
+    }
+    // 2. tile+1 landed in every wave (and every wave is done with tile-1's buffer), refill
+    //    that buffer with tile+kStages-1, read tile+1's B fragments
+    if (tile + 1 < te) wait_tile(tile + 1, min(te - 1, tile + kStages - 2));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_imm(63));  // LDS writes only
+    __builtin_amdgcn_s_barrier();
+    if (tile + kStages - 1 < te) issue(tile + kStages - 1);
+    bfrags(tile + 1);
+    // 5. next tile on the matrix core (past the range it reads a stale buffer and is unused),
+    //    this tile's epilogue on the VALU; no branch until the stores
+    acc[P ^ 1] = mfma_chain<NP, KS>(A, Bf);
+
+    if constexpr (PASS) {
+#pragma unroll
+      for (int i = 0; i < KS * NP; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+      }
+      if (live) {
+        float* dst = (float*)a.codes + crow * kD + 32 * w + 16 * hc;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) *(float4*)(dst + 4 * q) = make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
+      }
+    } else {
+      if constexpr (NB == 64) {
+        const float2 o = red[P][w ^ 1][n];
         mn = fminf(mn, o.x);
         mx = fmaxf(mx, o.y);
       }
-      if (!(mn >= -3.0e38f && mx <= 3.0e38f)) bad = true;  // +-inf in the block
+      bad = bad || !(mn >= -3.0e38f && mx <= 3.0e38f);  // NaN or +-inf in the block
       const Side sd = make_side(mn, mx, BITS);
-      uint32_t q[16];
+      float r[16];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) q[e] = quantize(z[e], sd.mn, sd.inv, qmax);
-      uint8_t* crowp = a.codes + crow * (kD * BITS / 8);
-      if constexpr ((BITS & 1) == 0) {
-        if (live) {
-          uint32_t words[BITS / 2];
-          pack16<BITS>(q, words);
-          store_words<BITS / 2>((uint32_t*)(crowp + (4 * w + 2 * hc) * BITS), words);
+      for (int e = 0; e < 16; ++e) r[e] = quantize_rint(z[e], sd.mn, sd.inv);
+      constexpr int NW = (BITS & 1) ? BITS : BITS / 2;  // words this lane stores
+      uint32_t words[NW];
+      // integer-valued floats to bytes (exact), bytes to b-bit fields of the LSB-first stream
+      auto pk4 = [](float c0, float c1, float c2, float c3) {
+        uint32_t v = __builtin_amdgcn_cvt_pk_u8_f32(c0, 0, 0u);
+        v = __builtin_amdgcn_cvt_pk_u8_f32(c1, 1, v);
+        v = __builtin_amdgcn_cvt_pk_u8_f32(c2, 2, v);
+        return __builtin_amdgcn_cvt_pk_u8_f32(c3, 3, v);
+      };
+      if constexpr (BITS == 8) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) words[i] = pk4(r[4 * i], r[4 * i + 1], r[4 * i + 2], r[4 * i + 3]);
+      } else if constexpr (BITS == 4) {
+        // byte j of the word holds codes 2j (low nibble) and 2j+1 (high nibble)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const float* c = r + 8 * i;
+          words[i] = pk4(c[0], c[2], c[4], c[6]) | (pk4(c[1], c[3], c[5], c[7]) << 4);
         }
+      } else if constexpr (BITS == 2) {
+        // byte j holds codes 4j .. 4j+3 in 2-bit fields
+        words[0] = pk4(r[0], r[4], r[8], r[12]) | (pk4(r[1], r[5], r[9], r[13]) << 2) |
+                   (pk4(r[2], r[6], r[10], r[14]) << 4) | (pk4(r[3], r[7], r[11], r[15]) << 6);
       } else {
-        // 16 odd-width codes span 1.5 words: the lane pair of a token packs its 32 codes
-        // (BITS words) together and the lower half stores them
-        uint32_t hq[16];
+        uint32_t q[16];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) hq[e] = __shfl_xor(q[e], 32);
-        if (live && hc == 0) {
-          uint32_t words[BITS];
+        for (int e = 0; e < 16; ++e) q[e] = uint32_t(r[e]);
+        if constexpr (BITS == 6) {
+          pack16<BITS>(q, words);
+        } else {
+          // 16 odd-width codes span 1.5 words: the lane pair of a token packs its 32 codes
+          // (BITS words) together and the lower half stores them
+          uint32_t hq[16];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) hq[e] = __shfl_xor(q[e], 32);
 #pragma unroll
           for (int i = 0; i < BITS; ++i) words[i] = 0;
 #pragma unroll
@@ -268,12 +345,27 @@ __global__ __launch_bounds__(kThreads, 2) void enc_mfma(MfmaArgs a) {
             words[wd] |= v << off;
             if (off + BITS > 32) words[wd + 1] |= v >> (32 - off);
           }
+        }
+      }
+      // keep the epilogue in this block (not sunk into the store branch) so the scheduler can
+      // interleave it with the matrix-core chain
+#pragma unroll
+      for (int i = 0; i < NW; ++i) asm volatile("" ::"v"(words[i]));
+      asm volatile("" ::"v"(sd.word));
+#pragma unroll
+      for (int i = 0; i < KS * NP; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+      }
+      if (live) {
+        uint8_t* crowp = a.codes + crow * (kD * BITS / 8);
+        if constexpr ((BITS & 1) == 0) {
+          store_words<NW>((uint32_t*)(crowp + (4 * w + 2 * hc) * BITS), words);
+        } else if (hc == 0) {
           uint32_t* dst = (uint32_t*)(crowp + (4 * w) * BITS);
 #pragma unroll
           for (int i = 0; i < BITS; ++i) dst[i] = words[i];
         }
-      }
-      if (live) {
         flags |= sd.flags | (bad ? CG_FLAG_NONFINITE : 0);
         const int nbk = kD / NB;
         if constexpr (NB == 16) {
@@ -285,7 +377,10 @@ __global__ __launch_bounds__(kThreads, 2) void enc_mfma(MfmaArgs a) {
         }
       }
     }
-    __syncthreads();
+  };
+  for (int tile = tb; tile < te; tile += 2) {
+    step(tile, std::integral_constant<int, 0>());
+    if (tile + 1 < te) step(tile + 1, std::integral_constant<int, 1>());
   }
   if (flags && a.err) atomicOr(a.err, flags);
 }

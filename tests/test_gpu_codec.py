@@ -402,3 +402,14 @@ def test_library_gauge_upload_matches_user_upload():
                   G_dev=b)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("which", [0, 1])
+def test_division_free_quantiser_steps_are_correctly_rounded(which):
+    """The kernels replace two binary32 divisions of the quantiser (range / (2^b - 1) and
+    1 / scale) by multiply-and-correct sequences; the device self-test compares them with
+    correctly rounded division over every binary16 scale and every binary32 significand."""
+    bad = torch.zeros(1, dtype=torch.int64, device="cuda")
+    cg.cg_selftest(which, bad)
+    torch.cuda.synchronize()
+    assert int(bad.item()) == 0
