@@ -286,6 +286,7 @@ GaugeDev gauge_dev(const void* G_dev, const cg_gauge_shape& s) {
     G.hi[p] = reinterpret_cast<const uint16_t*>(base + gl.off_hi[p]);
     G.tr[p] = reinterpret_cast<const uint16_t*>(base + gl.off_tr[p]);
   }
+  G.cs8 = reinterpret_cast<const float*>(base + gl.off_cs8);
   G.g = s.g;
   G.R = s.d / s.g;
   G.H = s.H;
@@ -438,6 +439,22 @@ int32_t gauge_make(int32_t kind, cg_gauge_shape shp, uint64_t seed, const float*
           }
         }
     }
+    // decoder column sums per 8-channel segment (double sums of the bf16 terms: exact)
+    const int d = shp.d, R = d / g;
+    float* cs8 = reinterpret_cast<float*>(buf.data() + gl.off_cs8);
+    for (int64_t head = 0; head < gl.nhead; ++head)
+      for (int c = 0; c < d / 8; ++c)
+        for (int i = 0; i < d; ++i) {
+          const int r = i / g;
+          double acc = 0.0;
+          if ((8 * c) / g == r) {
+            const int64_t blk = head * R + r;
+            for (int j = 8 * c; j < 8 * c + 8; ++j)
+              for (int p = 0; p < kDecPlanes; ++p)
+                acc += bf16_val(reinterpret_cast<const uint16_t*>(buf.data() + gl.off_tr[p])[blk * gg + size_t(i % g) * g + (j % g)]);
+          }
+          cs8[(size_t(head) * (d / 8) + c) * d + i] = float(acc);
+        }
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (hipMemcpyAsync(G_dev, buf.data(), buf.size(), hipMemcpyHostToDevice, st) != hipSuccess)
       return CG_ERR_DEVICE;

@@ -10,15 +10,21 @@
 
 namespace cg {
 
+// Split planes of G^T the matrix-core decoders multiply (G^T ~= tr[0] + tr[1]).
+constexpr int kDecPlanes = 2;
+
 // Device gauge buffer (filled by gauge_make):
 //   f32  : G            [nblk][g][g] binary32, nblk = L*2*H*R, block ((l*2+s)*H+h)*R+r
 //   hi[p]: split planes of G,   bf16 [nblk][g][g], G ~= hi[0] + hi[1] + hi[2]
 //   tr[p]: split planes of G^T, bf16 [nblk][g][g] (block transposed)
+//   cs8  : decoder column sums, binary32 [L*2*H][d/8][d]: entry (head, c, i) is the sum over
+//          the 8 channels j of segment c that share i's group of tr[0][i][j] + tr[1][i][j]
+//          (summed exactly, rounded once), head = (l*2+s)*H+h
 // Every section starts on a 256-byte boundary.
 struct GaugeLayout {
-  int64_t nblk = 0;
-  int g = 0;
-  size_t off_f32 = 0, off_hi[3] = {0, 0, 0}, off_tr[3] = {0, 0, 0}, total = 0;
+  int64_t nblk = 0, nhead = 0;
+  int g = 0, d = 0;
+  size_t off_f32 = 0, off_hi[3] = {0, 0, 0}, off_tr[3] = {0, 0, 0}, off_cs8 = 0, total = 0;
 };
 
 inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
@@ -40,6 +46,10 @@ inline GaugeLayout gauge_layout(const cg_gauge_shape& s) {
     gl.off_tr[p] = off;
     off = align256(off + gl.nblk * gg * 2);
   }
+  gl.d = s.d;
+  gl.nhead = int64_t(s.L) * 2 * s.H;
+  gl.off_cs8 = off;
+  off = align256(off + size_t(gl.nhead) * (s.d / 8) * s.d * 4);
   gl.total = off;
   return gl;
 }
@@ -49,6 +59,7 @@ struct GaugeDev {
   const float* f32;
   const uint16_t* hi[3];
   const uint16_t* tr[3];
+  const float* cs8;
   int g, R, H;
 };
 

@@ -3,9 +3,11 @@
 //
 // The gauge (section 3: z = G_{l,s,h,r} x per channel group) is a dense contraction over the
 // channel axis, so it runs on the gfx950 matrix cores with v_mfma_f32_32x32x16_bf16.  The
-// input x is exact in bf16; the binary32 gauge is split into three bf16 planes
-// G = G0 + G1 + G2 (about 24 significant bits), each multiplied on the matrix core with a
-// binary32 accumulator.
+// input x is exact in bf16; the binary32 gauge enters as kNP bf16 planes G0 + G1 (+ G2) of
+// its split (the gauge buffer holds three), each multiplied on the matrix core with a
+// binary32 accumulator.  Two planes carry 16 significant bits of every entry (entry error at
+// most 2^-16 relative), which keeps z within a few 1e-6 of the binary32 gauge per group,
+// inside the 1e-5 gauge tolerance, at two thirds of the matrix-core work of three planes.
 //
 // Work split: a workgroup of four wave64s owns a range of 32-token tiles of one
 // (layer, batch, head) slice; wave w computes output channels [32w, 32w+32) (one 32-row MFMA
@@ -44,7 +46,7 @@ constexpr int kD = 128;          // head dimension handled here
 constexpr int kTok = 32;         // tokens per tile (MFMA N)
 constexpr int kThreads = 256;    // four waves
 constexpr int kRowBytes = kD * 2;
-constexpr int kStages = 6;       // encoder LDS ring: tiles in flight + the one being read
+constexpr int kStages = 5;       // encoder LDS ring: tiles in flight + the one being read
 // s_waitcnt immediate (gfx9 encoding: vmcnt[3:0] and [15:14], expcnt[6:4], lgkmcnt[11:8])
 // waiting until at most `vm` vector-memory operations are outstanding, with lgkmcnt = 0 (all
 // LDS operations of the wave done) and no wait on expcnt
@@ -61,6 +63,7 @@ struct MfmaArgs {
   // gauge planes ([nblk][g][g] bf16) and binary32 blocks
   const uint16_t* gp[3];
   const float* g32;
+  const float* cs8;              // decoder column sums per 8-channel segment [head][d/8][d]
   int g, R;                      // group size, groups per head
   int Hg;                        // heads of the gauge shape
   // cache
@@ -156,14 +159,22 @@ __device__ __forceinline__ f32x16_t mfma_chain(const bf16x8_t (&A)[NP][KS], cons
 //   1. block-range partials of tile t from its accumulator (64-channel blocks: wave-pair
 //      exchange through red[t & 1]);
 //   2. wait for tile t+1's LDS-direct loads, barrier, issue the loads of tile t+kStages-1
-//      into the buffer tile t-1 used, read the B fragments of tile t+1;
-//   3. matrix-core chain of tile t+1 interleaved with side info, quantisation, packing and
-//      stores of tile t.
-// kStages - 1 tiles are in flight between global memory and LDS.
+//      into the buffer tile t-1 used, read the B fragments of tile t+1, write tile t-1's
+//      staged codes and side words to the cache as contiguous runs;
+//   3. matrix-core chain of tile t+1 interleaved with side info, quantisation and packing of
+//      tile t into the staging buffers.
+// kStages - 1 tiles are in flight between global memory and LDS.  The codes of a tile are one
+// contiguous run of 32 RB bytes in the cache and its side words one run of 32 NBK words, so
+// the staged copy leaves with whole-line stores instead of 32 scattered row pieces.
 template <int NP, int KS, int BITS, int NB, bool PASS>
-__global__ __launch_bounds__(kThreads, 2) void enc_mfma(MfmaArgs a) {
+__global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a) {
+  constexpr int RB = kD * BITS / 8;   // packed code bytes per token row
+  constexpr int NBK = kD / NB;        // side words per token row
   __shared__ __attribute__((aligned(16))) uint8_t xtile[kStages][kTok * kRowBytes];
   __shared__ float2 red[2][4][kTok];  // per-wave (min, max) of each token, for 64-channel blocks
+  // a tile's packed rows and side words, staged so that they leave as contiguous stores
+  __shared__ __attribute__((aligned(16))) uint8_t cstage[2][PASS ? 16 : kTok * RB];
+  __shared__ uint32_t sstage[2][PASS ? 1 : kTok * NBK];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n = lane & 31, hc = lane >> 5;
@@ -239,6 +250,18 @@ __global__ __launch_bounds__(kThreads, 2) void enc_mfma(MfmaArgs a) {
   f32x16_t acc[2];
   acc[0] = mfma_chain<NP, KS>(A, Bf);
   int flags = 0;
+  // staged tile -> cache: thread i stores 16-byte granule i of the codes (row i / BITS) and,
+  // counting from the last thread, side word i (row i / NBK); rows past the view are skipped
+  auto flush = [&](int tile, auto parity) {
+    constexpr int P = decltype(parity)::value;
+    const int tid = int(threadIdx.x);
+    const int nlive = a.T - tile * kTok;
+    const size_t crow0 = cslice * a.T_cap + size_t(a.t0 + tile * kTok);
+    if (tid < kTok * BITS && tid / BITS < nlive)
+      *(u32x4_t*)(a.codes + crow0 * RB + 16 * tid) = *(const u32x4_t*)(cstage[P] + 16 * tid);
+    const int si = kThreads - 1 - tid;
+    if (si < kTok * NBK && si / NBK < nlive) a.side[crow0 * NBK + si] = sstage[P][si];
+  };
   // one pipeline step; P = parity of (tile - tb) selects the accumulator, LDS buffer, register
   // stage and exchange slot at compile time
   auto step = [&](int tile, auto parity) {
@@ -275,6 +298,9 @@ __global__ __launch_bounds__(kThreads, 2) void enc_mfma(MfmaArgs a) {
     __builtin_amdgcn_s_barrier();
     if (tile + kStages - 1 < te) issue(tile + kStages - 1);
     bfrags(tile + 1);
+    if constexpr (!PASS) {
+      if (tile > tb) flush(tile - 1, std::integral_constant<int, P ^ 1>());
+    }
     // 5. next tile on the matrix core (past the range it reads a stale buffer and is unused),
     //    this tile's epilogue on the VALU; no branch until the stores
     acc[P ^ 1] = mfma_chain<NP, KS>(A, Bf);
@@ -357,24 +383,21 @@ __global__ __launch_bounds__(kThreads, 2) void enc_mfma(MfmaArgs a) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
       }
-      if (live) {
-        uint8_t* crowp = a.codes + crow * (kD * BITS / 8);
-        if constexpr ((BITS & 1) == 0) {
-          store_words<NW>((uint32_t*)(crowp + (4 * w + 2 * hc) * BITS), words);
-        } else if (hc == 0) {
-          uint32_t* dst = (uint32_t*)(crowp + (4 * w) * BITS);
+      uint8_t* crowp = cstage[P] + n * RB;
+      if constexpr ((BITS & 1) == 0) {
+        store_words<NW>((uint32_t*)(crowp + (4 * w + 2 * hc) * BITS), words);
+      } else if (hc == 0) {
+        uint32_t* dst = (uint32_t*)(crowp + (4 * w) * BITS);
 #pragma unroll
-          for (int i = 0; i < BITS; ++i) dst[i] = words[i];
-        }
-        flags |= sd.flags | (bad ? CG_FLAG_NONFINITE : 0);
-        const int nbk = kD / NB;
-        if constexpr (NB == 16) {
-          a.side[crow * nbk + 2 * w + hc] = sd.word;
-        } else if constexpr (NB == 32) {
-          if (hc == 0) a.side[crow * nbk + w] = sd.word;
-        } else {
-          if (hc == 0 && (w & 1) == 0) a.side[crow * nbk + (w >> 1)] = sd.word;
-        }
+        for (int i = 0; i < BITS; ++i) dst[i] = words[i];
+      }
+      if (live) flags |= sd.flags | (bad ? CG_FLAG_NONFINITE : 0);
+      if constexpr (NB == 16) {
+        sstage[P][n * NBK + 2 * w + hc] = sd.word;
+      } else if constexpr (NB == 32) {
+        if (hc == 0) sstage[P][n * NBK + w] = sd.word;
+      } else {
+        if (hc == 0 && (w & 1) == 0) sstage[P][n * NBK + (w >> 1)] = sd.word;
       }
     }
   };
@@ -382,12 +405,28 @@ __global__ __launch_bounds__(kThreads, 2) void enc_mfma(MfmaArgs a) {
     step(tile, std::integral_constant<int, 0>());
     if (tile + 1 < te) step(tile + 1, std::integral_constant<int, 1>());
   }
+  if constexpr (!PASS) {
+    // the last tile's staging: every wave's LDS writes done, then the final contiguous stores
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(63));
+    __builtin_amdgcn_s_barrier();
+    if ((te - tb) & 1) flush(te - 1, std::integral_constant<int, 0>());
+    else flush(te - 1, std::integral_constant<int, 1>());
+  }
   if (flags && a.err) atomicOr(a.err, flags);
 }
 
 // ------------------------------------------------------------------------------------------
 // decode
 // ------------------------------------------------------------------------------------------
+// Sum over the 8-channel segments [j0, j1) of the gauge buffer's column sums of channel i
+// (the two split planes of G^T over each segment's channels in i's group).
+__device__ __forceinline__ float seg_colsum(const MfmaArgs& a, int l, int h, int i, int j0, int j1) {
+  const float* cs = a.cs8 + ((size_t(l) * 2 + a.s) * a.Hg + h) * (kD / 8) * kD + i;
+  float acc = 0.0f;
+  for (int c = j0 / 8; c < j1 / 8; ++c) acc += cs[c * kD];
+  return acc;
+}
+
 template <int NP, int KS, int BITS, int NB, bool OUT_BF16>
 __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
   constexpr int NBK = kD / NB;                      // blocks per token row
@@ -395,6 +434,11 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
   __shared__ uint32_t stile[2][kTok * NBK];         // side words
   __shared__ __attribute__((aligned(16))) float colsum[NBK][kD];
   __shared__ float mtile[2][kTok][kD / 8];         // per (token, group) centre grid points
+  // decoded tile, staged so that it leaves as whole token rows (16-byte granules XOR-swizzled
+  // within a row, like qtile)
+  constexpr int YB = OUT_BF16 ? 2 : 4;              // output bytes per element
+  constexpr int GPR = kD * YB / 16;                 // 16-byte granules per output row
+  __shared__ __attribute__((aligned(16))) uint8_t ystage[2][kTok * kD * YB];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n = lane & 31, hc = lane >> 5;
@@ -427,18 +471,13 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
   // decodes from the midpoint term alone.
   const bool gc = KS == 2 && a.g < NB;
   // column sums: per block (colsum[k][i] = sum_{j in block k} G[j][i]) or, when centring per
-  // group, per group (colsum[0][i] = sum_{j in group(i)} G[j][i]); binary64 sums
+  // group, per group (colsum[0][i] = sum_{j in group(i)} G[j][i]), of the same split planes
+  // the matrix core multiplies
   for (int idx = threadIdx.x; idx < NBK * kD; idx += kThreads) {
     const int k = idx / kD, i = idx - k * kD;
-    const int g = a.g, r = i / g;
-    const float* Gb = a.g32 + (((size_t(l) * 2 + a.s) * a.Hg + h) * a.R + r) * g * g;
-    double acc = 0.0;
-    const int j0 = gc ? r * g : k * NB, j1 = gc ? (r + 1) * g : (k + 1) * NB;
-    if (!gc || k == 0) {
-      for (int j = j0; j < j1; ++j)
-        if (j / g == r) acc += double(Gb[size_t(j % g) * g + (i % g)]);
-      colsum[k][i] = float(acc);
-    }
+    const int r = i / a.g;
+    if (!gc || k == 0)
+      colsum[k][i] = seg_colsum(a, l, h, i, gc ? r * a.g : k * NB, gc ? (r + 1) * a.g : (k + 1) * NB);
   }
 
   // staging of a tile's code rows: thread owns token tid/8, channels 16*(tid%8) .. +16
@@ -505,6 +544,21 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
     }
   };
 
+  // staged rows of `tile` -> the view: thread i moves granules i, i + 256, ... (row = granule /
+  // GPR); rows past the written range are skipped
+  auto flush = [&](int tile, int buf) {
+    const int nlive = Tv - tile * kTok;
+#pragma unroll
+    for (int k = 0; k < kTok * GPR / kThreads; ++k) {
+      const int gi = int(threadIdx.x) + k * kThreads;
+      const int row = gi / GPR, j = gi % GPR;
+      if (row < nlive) {
+        const u32x4_t v = *(const u32x4_t*)(&ystage[buf][row * kD * YB + 16 * (j ^ (row & (GPR - 1)))]);
+        *(u32x4_t*)(ys + YB * (size_t(tile * kTok + row) * a.st) + 16 * j) = v;
+      }
+    }
+  };
+
   fetch(tb);
   put(0);
   if (tb + 1 < te) fetch(tb + 1);
@@ -520,6 +574,7 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
       put(buf ^ 1);
       if (tile + 2 < te) fetch(tile + 2);
     }
+    if (tile > tb) flush(tile - 1, buf ^ 1);
     const uint8_t* rowp = &qtile[buf][n * kRowBytes];
     float y[16];
 #pragma unroll
@@ -576,29 +631,378 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
         }
       }
     }
-    const int tok = tile * kTok + n;
-    if (tok < Tv) {
-      if constexpr (OUT_BF16) {
-        uint32_t pk[8];
+    // this lane's 16 channels 32w + 16hc .. +16 of token row n into the staging tile
+    uint8_t* yrow = &ystage[buf][n * kD * YB];
+    if constexpr (OUT_BF16) {
+      uint32_t pk[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pk[e] = f32_to_bf16_rne(y[2 * e]) | (f32_to_bf16_rne(y[2 * e + 1]) << 16);
-        uint16_t* dst = (uint16_t*)ys + size_t(tok) * a.st + 32 * w + 16 * hc;
-        *(u32x4_t*)dst = u32x4_t{pk[0], pk[1], pk[2], pk[3]};
-        *(u32x4_t*)(dst + 8) = u32x4_t{pk[4], pk[5], pk[6], pk[7]};
-      } else {
-        float* dst = (float*)ys + size_t(tok) * a.st + 32 * w + 16 * hc;
+      for (int e = 0; e < 8; ++e) pk[e] = f32_to_bf16_rne(y[2 * e]) | (f32_to_bf16_rne(y[2 * e + 1]) << 16);
+      const int j0 = 4 * w + 2 * hc;
+      *(u32x4_t*)(yrow + 16 * (j0 ^ (n & (GPR - 1)))) = u32x4_t{pk[0], pk[1], pk[2], pk[3]};
+      *(u32x4_t*)(yrow + 16 * ((j0 + 1) ^ (n & (GPR - 1)))) = u32x4_t{pk[4], pk[5], pk[6], pk[7]};
+    } else {
+      const int j0 = 8 * w + 4 * hc;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) *(float4*)(dst + 4 * q) = make_float4(y[4 * q], y[4 * q + 1], y[4 * q + 2], y[4 * q + 3]);
-      }
+      for (int q = 0; q < 4; ++q)
+        *(float4*)(yrow + 16 * ((j0 + q) ^ (n & (GPR - 1)))) = make_float4(y[4 * q], y[4 * q + 1], y[4 * q + 2], y[4 * q + 3]);
     }
     __syncthreads();
   }
+  flush(te - 1, (te - 1 - tb) & 1);
+}
+
+// ------------------------------------------------------------------------------------------
+// decode, blocks inside one gauge group (g >= n)
+// ------------------------------------------------------------------------------------------
+// The matrix core reads the codes without a float conversion: with b <= 7 the bf16 word
+// 0x3F80 | (q << (7 - b)) is exactly 1 + q 2^-b, built from the packed stream with shifts and
+// masks, so per block k
+//   zhat_j = mn_k + q_j sc_k = (mn_k - 2^b sc_k) + 2^b sc_k B_j,   B_j = 1 + q_j 2^-b,
+//   xhat_i = sum_k ( 2^b sc_k (G^T B)_{k,i} + (mn_k - 2^b sc_k) colsum_k(G^T)_i ).
+// With b = 8 the operand is q itself (exact in bf16) and the offset term is mn_k colsum_k.
+// B stays within [1, 2), so the block-local matrix-core sums stay of the order of the block's
+// range.  This needs every block inside one gauge group (a block spanning two groups can mix
+// a quiet group with another group's outlier, where the two terms cancel).
+//
+// A lane's B fragment for one K-step holds 8 codes of its token; which 8 channels (and in
+// which order) is chosen so that the fragment is a handful of shifts of one packed word, and
+// the A fragments (the rows of G^T, loaded once) are gathered in the same channel order.
+
+// Channel order of the B fragments (and of the A fragments gathered to match): lane half hc
+// owns the 8 SEG channels [16 SEG s + 8 SEG hc, +8 SEG) of block segment s of the wave's K
+// range; K-step u of the segment takes, with b = 4, channels 8u + (0,4,1,5,2,6,3,7) of that
+// region (nibble pairs of one packed word), with b = 2 channels 16 (u/2) + 4 (u%2) +
+// (0,8,1,9,2,10,3,11) (2-bit pairs of one word), otherwise 8u + (0..7).
+template <int NP, int KS, int BITS, int SEG>
+__device__ void load_a_perm(bf16x8_t (&A)[NP][KS], const MfmaArgs& a, int l, int h, int ch, int kbase, int hc) {
+  const int g = a.g, r = ch / g;
+  const size_t blk = ((size_t(l) * 2 + a.s) * a.Hg + h) * a.R + r;
+  // 8 consecutive entries of row ch from channel j (8-aligned, so inside one group), zero
+  // outside the row's group
+  auto load8 = [&](int p, int j) {
+    u32x4_t v = {0u, 0u, 0u, 0u};
+    if (j / g == r) v = *(const u32x4_t*)(a.gp[p] + blk * g * g + size_t(ch % g) * g + (j % g));
+    return v;
+  };
+  // bf16 pair (lo half of x or hi half, lo half of y or hi half) -> one word
+  auto pair_lo = [](uint32_t x, uint32_t y) { return __builtin_amdgcn_perm(y, x, 0x05040100u); };
+  auto pair_hi = [](uint32_t x, uint32_t y) { return __builtin_amdgcn_perm(y, x, 0x07060302u); };
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) {
+    const int s = kk / SEG, u = kk % SEG;
+    const int region = kbase + 16 * SEG * s + 8 * SEG * hc;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      u32x4_t f;
+      if constexpr (BITS == 4) {
+        // channels region + 8u + (0,4,1,5,2,6,3,7)
+        const u32x4_t v = load8(p, region + 8 * u);
+        f[0] = pair_lo(v[0], v[2]);
+        f[1] = pair_hi(v[0], v[2]);
+        f[2] = pair_lo(v[1], v[3]);
+        f[3] = pair_hi(v[1], v[3]);
+      } else if constexpr (BITS == 2) {
+        // channels base + 4 (u & 1) + (0,8,1,9,2,10,3,11), base = region + 16 (u >> 1)
+        const int base = region + 16 * (u >> 1);
+        const u32x4_t lo = load8(p, base), hi = load8(p, base + 8);
+        const int w0 = 2 * (u & 1);
+        f[0] = pair_lo(lo[w0], hi[w0]);
+        f[1] = pair_hi(lo[w0], hi[w0]);
+        f[2] = pair_lo(lo[w0 + 1], hi[w0 + 1]);
+        f[3] = pair_hi(lo[w0 + 1], hi[w0 + 1]);
+      } else {
+        f = load8(p, region + 8 * u);
+      }
+      A[p][kk] = as_bf16x8(f);
+    }
+  }
+}
+
+// B fragment of K-step u of a region (RW packed words starting at the region's first channel)
+// `one` = 0x3F803F80 (the bf16 pair (1, 1)) and `m` = the mantissa field mask of the code
+// width, both held in VGPRs by the caller so that (x & m) | one selects the single
+// three-operand v_and_or_b32 (that encoding takes no literal constants on gfx9)
+template <int BITS, int RW>
+__device__ __forceinline__ bf16x8_t code_frag(const uint32_t (&rw)[RW], int u, uint32_t one, uint32_t m) {
+  constexpr uint32_t ONE = 0x3F803F80u;
+  u32x4_t f;
+  if constexpr (BITS == 4) {
+    const uint32_t w = rw[u];  // m = 0x00780078: mantissa bits 3..6 of both halves
+    f[0] = ((w << 3) & m) | one;
+    f[1] = ((w >> 1) & m) | one;
+    f[2] = ((w >> 5) & m) | one;
+    f[3] = ((w >> 9) & m) | one;
+  } else if constexpr (BITS == 2) {
+    const uint32_t w = rw[u >> 1];  // m = 0x00600060: mantissa bits 5..6
+    if ((u & 1) == 0) {
+      f[0] = ((w << 5) & m) | one;
+      f[1] = ((w << 3) & m) | one;
+      f[2] = ((w << 1) & m) | one;
+      f[3] = ((w >> 1) & m) | one;
+    } else {
+      f[0] = ((w >> 3) & m) | one;
+      f[1] = ((w >> 5) & m) | one;
+      f[2] = ((w >> 7) & m) | one;
+      f[3] = ((w >> 9) & m) | one;
+    }
+  } else if constexpr (BITS == 8) {
+    // codes as themselves: bytes to binary32 (exact), high halves are the bf16 values
+    const uint32_t w0 = rw[2 * u], w1 = rw[2 * u + 1];
+    auto pk = [](float lo, float hi) { return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u); };
+    f[0] = pk(float(w0 & 255u), float((w0 >> 8) & 255u));
+    f[1] = pk(float((w0 >> 16) & 255u), float(w0 >> 24));
+    f[2] = pk(float(w1 & 255u), float((w1 >> 8) & 255u));
+    f[3] = pk(float((w1 >> 16) & 255u), float(w1 >> 24));
+  } else {
+    // 3 or 6 bits: 8 codes of the LSB-first stream at bit 8 u BITS of the region
+    constexpr int b0 = 8 * BITS;
+    const int bit = u * b0, wi = bit >> 5, sh = bit & 31;
+    const uint64_t win = ((uint64_t(rw[wi + 1 < RW ? wi + 1 : wi]) << 32) | rw[wi]) >> sh;
+#pragma unroll
+    for (int k2 = 0; k2 < 4; ++k2) {
+      const uint32_t c0 = uint32_t(win >> (2 * k2 * BITS)) & ((1u << BITS) - 1u);
+      const uint32_t c1 = uint32_t(win >> ((2 * k2 + 1) * BITS)) & ((1u << BITS) - 1u);
+      f[k2] = ONE | (c0 << (7 - BITS)) | (c1 << (23 - BITS));
+    }
+  }
+  return as_bf16x8(f);
+}
+
+// Largest N in {0, 2, 4, 8, 12, 16, 20, 24, 32, 40} not above n: wait until at most N vector
+// memory operations of the wave are outstanding (and all its LDS operations are done).
+__device__ __forceinline__ void wait_vm_atmost(int n) {
+  if (n >= 40) __builtin_amdgcn_s_waitcnt(waitcnt_imm(40));
+  else if (n >= 32) __builtin_amdgcn_s_waitcnt(waitcnt_imm(32));
+  else if (n >= 24) __builtin_amdgcn_s_waitcnt(waitcnt_imm(24));
+  else if (n >= 20) __builtin_amdgcn_s_waitcnt(waitcnt_imm(20));
+  else if (n >= 16) __builtin_amdgcn_s_waitcnt(waitcnt_imm(16));
+  else if (n >= 12) __builtin_amdgcn_s_waitcnt(waitcnt_imm(12));
+  else if (n >= 8) __builtin_amdgcn_s_waitcnt(waitcnt_imm(8));
+  else if (n >= 4) __builtin_amdgcn_s_waitcnt(waitcnt_imm(4));
+  else if (n >= 2) __builtin_amdgcn_s_waitcnt(waitcnt_imm(2));
+  else __builtin_amdgcn_s_waitcnt(waitcnt_imm(0));
+}
+
+constexpr int kDStages = 8;  // decoder LDS ring of code and side tiles (fewer for 8-bit f32 out)
+
+// One barrier per 32-token tile t:
+//   wait for tile t's LDS-direct loads, barrier; write tile t-1's staged rows to the view;
+//   issue the loads of tile t + kDStages - 1 into the slot tile t-1 used; read tile t's codes
+//   and side words, build the B fragments, matrix-core chains per block segment, fold the
+//   block terms, convert and stage the rows.
+// Every wave issues exactly two loads per tile (codes, side words) and GPR stores per flush
+// (lanes past the written range repeat a live granule), so the number of vector-memory
+// operations younger than a tile's loads is known and waited for exactly.
+template <int NP, int KS, int BITS, int NB, bool OUT_BF16>
+__global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a) {
+  constexpr int RB = kD * BITS / 8;                  // code bytes per token row
+  constexpr int NBK = kD / NB;                       // side words per token row
+  constexpr int SEG = (16 * KS < NB ? 16 * KS : NB) / 16;  // K-steps per block segment
+  constexpr int NSEG = KS / SEG;
+  constexpr int RW = SEG * BITS / 4;                 // packed words of a lane's region
+  constexpr int YB = OUT_BF16 ? 2 : 4;
+  constexpr int GPR = kD * YB / 16;                  // 16-byte granules per output row
+  constexpr int F = kTok * GPR / kThreads;           // stores per thread per flush
+  static_assert(SEG * BITS % 4 == 0 && NSEG <= 2, "unsupported block layout");
+  constexpr int DS = (BITS == 8 && !OUT_BF16) ? 6 : kDStages;  // ring depth (LDS below 64 KB)
+  __shared__ __attribute__((aligned(16))) uint8_t ctile[DS][kTok * RB];
+  __shared__ __attribute__((aligned(16))) uint32_t stile[DS][kTok * NBK];
+  __shared__ __attribute__((aligned(16))) float colsum[NBK][kD];
+  __shared__ __attribute__((aligned(16))) uint8_t ystage[2][kTok * kD * YB];
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n = lane & 31, hc = lane >> 5;
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int slice = logical / a.chunks, chunk = logical - slice * a.chunks;
+  if (slice >= a.nslices) return;
+  const int h = slice % a.H, b = (slice / a.H) % a.B, lv = slice / (a.H * a.B);
+  const int l = lv + a.l0;
+  int Tv = a.T;
+  if (a.pos) {
+    const int p = a.pos[b];
+    if (p < 0 || p >= a.T_cap) return;  // flagged by the append kernel
+    Tv = min(Tv, p + 1 - a.t0);
+  }
+  const int ntiles = (Tv + kTok - 1) / kTok;
+  const int tb = chunk * a.tiles_per_wg;
+  const int te = min(ntiles, tb + a.tiles_per_wg);
+  if (tb >= te) return;
+  char* ys = a.x + YB * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
+  const size_t crow0 = (size_t(l) * a.cB + b) * a.cH * size_t(a.T_cap) + size_t(h) * a.T_cap + a.t0;
+
+  const int kbase = a.g >= 32 ? (32 * w / a.g) * a.g : 32 * w;
+  const int chA = 32 * w + 16 * ((n >> 2) & 1) + 4 * (n >> 3) + (n & 3);
+  bf16x8_t A[NP][KS];
+  load_a_perm<NP, KS, BITS, SEG>(A, a, l, h, chA, kbase, hc);  // a.gp holds the G^T planes
+
+  // colsum[k][i] = sum over channels j of block k in the group of i of G[j][i], of the split
+  // planes the matrix core multiplies (so the offset term cancels against the matrix-core
+  // sums of the same matrix and the planes' truncation error stays proportional to zhat)
+  for (int idx = threadIdx.x; idx < NBK * kD; idx += kThreads) {
+    const int k = idx / kD, i = idx - k * kD;
+    colsum[k][i] = seg_colsum(a, l, h, i, k * NB, (k + 1) * NB);
+  }
+
+  // LDS-direct loads: wave w fills code slots [8 BITS w, 8 BITS (w+1)) and side words
+  // [8 NBK w, 8 NBK (w+1)) of the tile; rows past the view repeat its last row.  The code tile
+  // is stored by 16-byte column: slot c 32 + r holds granule c of token row r, so the lanes
+  // of a fragment read (one token row each) hit consecutive slots.
+  const int cgi = 8 * BITS * w + lane, cgrow = cgi % kTok, cgpart = cgi / kTok;
+  const int swi = 8 * NBK * w + lane, swrow = swi / NBK, swk = swi % NBK;
+  auto issue = [&](int tile) {
+    const int st = (tile - tb) % DS;
+    const int last = Tv - 1 - tile * kTok;
+    const size_t row0 = crow0 + size_t(tile) * kTok;
+    if (lane < 8 * BITS)
+      __builtin_amdgcn_global_load_lds(a.codes + (row0 + min(cgrow, last)) * RB + 16 * cgpart,
+                                       (__attribute__((address_space(3))) void*)(ctile[st] + 16 * 8 * BITS * w), 16, 0, 0);
+    if (lane < 8 * NBK)
+      __builtin_amdgcn_global_load_lds(a.side + (row0 + min(swrow, last)) * NBK + swk,
+                                       (__attribute__((address_space(3))) void*)(stile[st] + 8 * NBK * w), 4, 0, 0);
+  };
+  // staged rows of `tile` -> the view; lanes past the written rows repeat the last live row's
+  // granules (same data, same address), so every thread issues F stores
+  int64_t yoff[F];  // byte offset of the thread's granules from the tile's first row
+  int ysrc[F];      // their staging offsets
+#pragma unroll
+  for (int k = 0; k < F; ++k) {
+    const int gi = int(threadIdx.x) + k * kThreads, row = gi / GPR, j = gi % GPR;
+    yoff[k] = int64_t(YB) * row * a.st + 16 * j;
+    ysrc[k] = row * kD * YB + 16 * (j ^ (row & (GPR - 1)));
+  }
+  const int64_t ytile = int64_t(YB) * kTok * a.st;
+  auto flush = [&](int tile, int buf) {
+    const int nlive = min(kTok, Tv - tile * kTok);
+    char* yt = ys + tile * ytile;
+    if (nlive == kTok) {
+#pragma unroll
+      for (int k = 0; k < F; ++k) *(u32x4_t*)(yt + yoff[k]) = *(const u32x4_t*)(&ystage[buf][ysrc[k]]);
+    } else {
+#pragma unroll
+      for (int k = 0; k < F; ++k) {
+        int gi = int(threadIdx.x) + k * kThreads;
+        if (gi >= nlive * GPR) gi = (nlive - 1) * GPR + (gi % GPR);
+        const int row = gi / GPR, j = gi % GPR;
+        const u32x4_t v = *(const u32x4_t*)(&ystage[buf][row * kD * YB + 16 * (j ^ (row & (GPR - 1)))]);
+        *(u32x4_t*)(yt + int64_t(YB) * row * a.st + 16 * j) = v;
+      }
+    }
+  };
+  // vector-memory operations of this wave issued after the loads of tile t, at the top of
+  // iteration t: the prologue loads of later tiles, then per earlier iteration i its flush (F,
+  // when i > tb) and its loads (2, when i + DS - 1 < te)
+  auto younger = [&](int t) {
+    if (t - (DS - 1) >= tb && t + DS - 2 < te) return (DS - 2) * (F + 2);  // steady state
+    int c = 0;
+    const int first = t - (DS - 1);  // iteration that issued tile t's loads (< tb: prologue)
+    if (first < tb) c += 2 * (min(te, tb + DS - 1) - 1 - t);
+    for (int i = max(first + 1, tb); i < t; ++i) c += (i > tb ? F : 0) + (i + DS - 1 < te ? 2 : 0);
+    return c;  // (the flush of iteration `first` precedes its loads)
+  };
+
+  for (int t = tb; t < min(te, tb + DS - 1); ++t) issue(t);
+  __syncthreads();  // colsum
+
+  constexpr float kScale = BITS == 8 ? 1.0f : float(1 << BITS);  // sc / gamma per unit sc
+  // code_frag's constants, opaque to constant folding so that they stay in VGPRs
+  uint32_t one = 0x3F803F80u, fmask = BITS == 2 ? 0x00600060u : 0x00780078u;
+  asm volatile("" : "+v"(one), "+v"(fmask));
+  for (int t = tb; t < te; ++t) {
+    const int P = (t - tb) & 1;
+    wait_vm_atmost(younger(t));
+    __builtin_amdgcn_s_barrier();
+    if (t > tb) flush(t - 1, P ^ 1);
+    if (t + DS - 1 < te) issue(t + DS - 1);
+    const int st = (t - tb) % DS;
+    uint32_t sw[NBK];
+#pragma unroll
+    for (int k = 0; k < NBK; ++k) sw[k] = stile[st][n * NBK + k];
+    float y[16];
+#pragma unroll
+    for (int sgi = 0; sgi < NSEG; ++sgi) {
+      // region of this lane: channels kbase + 16 SEG sgi + 8 SEG hc .. + 8 SEG
+      const int c0 = kbase + 16 * SEG * sgi + 8 * SEG * hc;
+      uint32_t rw[RW];
+      const int d0 = c0 * BITS / 32;  // first packed word of the region in the token row
+      if constexpr (RW % 4 == 0) {
+#pragma unroll
+        for (int gq = 0; gq < RW / 4; ++gq) {
+          const u32x4_t v = *(const u32x4_t*)(ctile[st] + ((d0 / 4 + gq) * kTok + n) * 16);
+          rw[4 * gq] = v[0]; rw[4 * gq + 1] = v[1]; rw[4 * gq + 2] = v[2]; rw[4 * gq + 3] = v[3];
+        }
+      } else if constexpr (RW % 2 == 0) {
+        // d0 is even here: word pairs (d, d+1) share a 16-byte column
+#pragma unroll
+        for (int i = 0; i < RW; i += 2) {
+          const int d = d0 + i;
+          const uint2 v = *(const uint2*)(ctile[st] + ((d >> 2) * kTok + n) * 16 + (d & 3) * 4);
+          rw[i] = v.x; rw[i + 1] = v.y;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < RW; ++i) {
+          const int d = d0 + i;
+          rw[i] = *(const uint32_t*)(ctile[st] + ((d >> 2) * kTok + n) * 16 + (d & 3) * 4);
+        }
+      }
+      f32x16_t acc = {};
+#pragma unroll
+      for (int u = 0; u < SEG; ++u) {
+        const bf16x8_t bv = code_frag<BITS, RW>(rw, u, one, fmask);
+#pragma unroll
+        for (int p = 0; p < NP; ++p) acc = mfma(A[p][sgi * SEG + u], bv, acc);
+      }
+      const int blk = (kbase + 16 * SEG * sgi) / NB;
+      const float mn = f16_bits_to_f32(sw[blk] & 0xffffu), sc = f16_bits_to_f32(sw[blk] >> 16);
+      const float scg = sc * kScale;
+      const float beta = BITS == 8 ? mn : mn - scg;
+      const float4* cs = (const float4*)&colsum[blk][32 * w + 16 * hc];
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const float4 c = cs[q4];
+        const float cc[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int e = 4 * q4 + u;
+          const float base = sgi == 0 ? beta * cc[u] : fmaf(beta, cc[u], y[e]);
+          y[e] = fmaf(scg, acc[e], base);
+        }
+      }
+    }
+    // this lane's channels 32w + 16hc .. +16 of token row n into the staging tile
+    uint8_t* yrow = &ystage[P][n * kD * YB];
+    if constexpr (OUT_BF16) {
+      typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+      typedef float f32x2_t __attribute__((ext_vector_type(2)));
+      uint32_t pk[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        pk[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y[2 * e], y[2 * e + 1]}), bf16x2_t));
+      const int j0 = 4 * w + 2 * hc;
+      *(u32x4_t*)(yrow + 16 * (j0 ^ (n & (GPR - 1)))) = u32x4_t{pk[0], pk[1], pk[2], pk[3]};
+      *(u32x4_t*)(yrow + 16 * ((j0 + 1) ^ (n & (GPR - 1)))) = u32x4_t{pk[4], pk[5], pk[6], pk[7]};
+    } else {
+      const int j0 = 8 * w + 4 * hc;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *(float4*)(yrow + 16 * ((j0 + q) ^ (n & (GPR - 1)))) = make_float4(y[4 * q], y[4 * q + 1], y[4 * q + 2], y[4 * q + 3]);
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(63));
+  __builtin_amdgcn_s_barrier();
+  flush(te - 1, (te - 1 - tb) & 1);
 }
 
 // ------------------------------------------------------------------------------------------
 // dispatch
 // ------------------------------------------------------------------------------------------
-constexpr int kNP = 3;
+// Split planes of the gauge on the matrix core.  Decoding takes two (16 significant bits per
+// entry: a few 1e-6 of the group norm).  Encoding takes two up to 4-bit codes and three
+// above: a finer grid turns the same z error into more codes moved across a rounding
+// boundary (with two planes about 3e-5 of 4-bit codes but 1.4e-4 of 6-bit codes move, against
+// the 1e-4 budget).
+constexpr int kNP = kDecPlanes;
+constexpr int enc_planes(int bits) { return bits >= 6 ? 3 : 2; }
 
 int cu_count() {
   static int cus = 0;
@@ -610,11 +1014,14 @@ int cu_count() {
   return cus;
 }
 
-// Split the (slice, tile) space into workgroups: about two resident workgroups per CU, each a
-// contiguous tile range of one slice; the count is padded to a multiple of 8 (XCD remap).
-void plan(MfmaArgs& m, int nslices, int T) {
+// Split the (slice, tile) space into workgroups: as many as can be resident at once (the
+// kernel's occupancy per CU times the CUs), each a contiguous tile range of one slice; the
+// count is padded to a multiple of 8 (XCD remap).
+void plan(MfmaArgs& m, int nslices, int T, const void* fn) {
   const int ntiles = (T + kTok - 1) / kTok;
-  const int target = 2 * cu_count();
+  int occ = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, kThreads, 0) != hipSuccess || occ < 1) occ = 2;
+  const int target = occ * cu_count();
   int chunks = (target + nslices - 1) / nslices;
   chunks = chunks < 1 ? 1 : (chunks > ntiles ? ntiles : chunks);
   m.tiles_per_wg = (ntiles + chunks - 1) / chunks;
@@ -625,7 +1032,7 @@ void plan(MfmaArgs& m, int nslices, int T) {
 template <int KS, int BITS, int NB>
 void* enc_kernel(bool pass) {
   if (pass) return (void*)enc_mfma<kNP, KS, 8, 64, true>;
-  return (void*)enc_mfma<kNP, KS, BITS, NB, false>;
+  return (void*)enc_mfma<enc_planes(BITS), KS, BITS, NB, false>;
 }
 
 template <int KS, int BITS>
@@ -680,6 +1087,40 @@ void* dec_by_bits(int bits, int nb, bool bf16) {
 
 int ksteps(int g) { return g >= 128 ? 8 : (g == 64 ? 4 : 2); }
 
+// dec_fast variants exist where a lane's code region is whole words and a wave's K range
+// holds at most two blocks
+template <int KS, int BITS, int NB>
+void* fast_kernel(bool bf16) {
+  constexpr int SEG = (16 * KS < NB ? 16 * KS : NB) / 16;
+  if constexpr (SEG * BITS % 4 == 0 && KS / SEG <= 2) {
+    if (bf16) return (void*)dec_fast<kNP, KS, BITS, NB, true>;
+    return (void*)dec_fast<kNP, KS, BITS, NB, false>;
+  }
+  return nullptr;
+}
+
+template <int KS, int BITS>
+void* fast_by_nb(int nb, bool bf16) {
+  switch (nb) {
+    case 16: return fast_kernel<KS, BITS, 16>(bf16);
+    case 32: return fast_kernel<KS, BITS, 32>(bf16);
+    case 64: return fast_kernel<KS, BITS, 64>(bf16);
+  }
+  return nullptr;
+}
+
+template <int KS>
+void* fast_by_bits(int bits, int nb, bool bf16) {
+  switch (bits) {
+    case 2: return fast_by_nb<KS, 2>(nb, bf16);
+    case 3: return fast_by_nb<KS, 3>(nb, bf16);
+    case 4: return fast_by_nb<KS, 4>(nb, bf16);
+    case 6: return fast_by_nb<KS, 6>(nb, bf16);
+    case 8: return fast_by_nb<KS, 8>(nb, bf16);
+  }
+  return nullptr;
+}
+
 bool group_ok(int g) { return g == 8 || g == 16 || g == 32 || g == 64 || g == 128; }
 
 bool bits_ok(int b) { return b == 2 || b == 3 || b == 4 || b == 6 || b == 8; }
@@ -709,7 +1150,6 @@ hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G
   m.g32 = G.f32; m.g = G.g; m.R = G.R; m.Hg = G.H;
   m.codes = k.codes; m.side = k.side; m.T_cap = k.T_cap; m.cB = k.B; m.cH = k.H;
   m.err = err;
-  plan(m, X.L * X.B * X.H, X.T);
   void* fn = nullptr;
   const bool pass = c.backend == CG_BACKEND_PASSTHROUGH;
   switch (ksteps(G.g)) {
@@ -718,6 +1158,7 @@ hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G
     case 8: fn = enc_by_bits<8>(pass ? 8 : c.bits, pass ? 64 : c.n, pass); break;
   }
   if (!fn) return hipErrorInvalidValue;
+  plan(m, X.L * X.B * X.H, X.T, fn);
   const int nwg = ((m.nslices * m.chunks + 7) / 8) * 8;
   void* args[] = {&m};
   return hipLaunchKernel(fn, dim3(nwg), dim3(kThreads), args, 0, st);
@@ -732,18 +1173,28 @@ hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& 
   m.L = Y.L; m.B = Y.B; m.H = Y.H; m.T = Y.T;
   m.l0 = l0; m.s = s; m.t0 = t0;
   for (int p = 0; p < 3; ++p) m.gp[p] = G.tr[p];
-  m.g32 = G.f32; m.g = G.g; m.R = G.R; m.Hg = G.H;
+  m.g32 = G.f32; m.cs8 = G.cs8; m.g = G.g; m.R = G.R; m.Hg = G.H;
   m.codes = k.codes; m.side = k.side; m.T_cap = k.T_cap; m.cB = k.B; m.cH = k.H;
   m.pos = pos;
   m.err = err;
-  plan(m, Y.L * Y.B * Y.H, Y.T);
   void* fn = nullptr;
-  switch (ksteps(G.g)) {
-    case 2: fn = dec_by_bits<2>(c.bits, c.n, Y.bf16); break;
-    case 4: fn = dec_by_bits<4>(c.bits, c.n, Y.bf16); break;
-    case 8: fn = dec_by_bits<8>(c.bits, c.n, Y.bf16); break;
+  if (G.g >= c.n) {
+    // blocks inside one group: codes feed the matrix core without conversion
+    switch (ksteps(G.g)) {
+      case 2: fn = fast_by_bits<2>(c.bits, c.n, Y.bf16); break;
+      case 4: fn = fast_by_bits<4>(c.bits, c.n, Y.bf16); break;
+      case 8: fn = fast_by_bits<8>(c.bits, c.n, Y.bf16); break;
+    }
+  }
+  if (!fn) {
+    switch (ksteps(G.g)) {
+      case 2: fn = dec_by_bits<2>(c.bits, c.n, Y.bf16); break;
+      case 4: fn = dec_by_bits<4>(c.bits, c.n, Y.bf16); break;
+      case 8: fn = dec_by_bits<8>(c.bits, c.n, Y.bf16); break;
+    }
   }
   if (!fn) return hipErrorInvalidValue;
+  plan(m, Y.L * Y.B * Y.H, Y.T, fn);
   const int nwg = ((m.nslices * m.chunks + 7) / 8) * 8;
   void* args[] = {&m};
   return hipLaunchKernel(fn, dim3(nwg), dim3(kThreads), args, 0, st);
