@@ -48,6 +48,22 @@ def algorithmic_bytes(w, s_count=1):
     return s_count * (elems * per_elem + gauge)
 
 
+def measured_traffic(path, kernel):
+    """HBM bytes per launch of `kernel` from the rocprofv3 FETCH_SIZE / WRITE_SIZE summary (scaled
+    by the copy-kernel calibration), or None when there is none or the kernel source has changed
+    since the counters were taken."""
+    import hashlib
+
+    try:
+        tr = json.load(open(path))
+        src = os.path.join(ROOT, "paper_2607_20538_amd", "csrc", "cg_mfma.hip")
+        if hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != tr.get("source_sha256_16"):
+            return None
+        return int(tr[kernel]["bytes"])
+    except (OSError, ValueError, KeyError, TypeError):
+        return None
+
+
 def cpu_baseline(w, G_host, layers):
     """The oracle (single thread, as written) encoding and decoding `layers` layers of K and V."""
     import numpy as np
@@ -140,13 +156,7 @@ def main():
     alg = algorithmic_bytes(w)                             # one launch = one of K or V
     dom_name, dom_ms = ("kv_encode", enc_ms) if enc_ms >= dec_ms else ("kv_decode", dec_ms)
     achieved = alg / (dom_ms * 1e-3) / 1e9
-    traffic = None
-    if os.path.exists(args.traffic):
-        try:
-            tr = json.load(open(args.traffic))
-            traffic = tr.get(dom_name)
-        except (OSError, ValueError):
-            traffic = None
+    traffic = measured_traffic(args.traffic, dom_name)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": dom_name,
                 "kernel_ms": round(dom_ms, 4), "encode_ms": round(enc_ms, 4), "decode_ms": round(dec_ms, 4),
