@@ -101,6 +101,13 @@ __device__ __forceinline__ float quantize_rint(float z, float mn, float inv) {
   return __builtin_rintf(t);
 }
 
+// t = fl32(fl32(z - mn) * inv) before rounding: for consumers that round to nearest even
+// themselves (v_cvt_pk_u8_f32 rounds to nearest even and saturates to [0, 255]).
+__device__ __forceinline__ float quantize_t(float z, float mn, float inv) {
+#pragma clang fp contract(off)
+  return (z - mn) * inv;
+}
+
 // zhat = fl32(mn + q * sc); q * sc is exact in binary32.
 __device__ __forceinline__ float dequantize(uint32_t q, float mn, float sc) {
 #pragma clang fp contract(off)

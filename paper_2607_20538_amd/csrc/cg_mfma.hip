@@ -202,21 +202,31 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
   // 8w .. 8w+7 of a tile with two 1 KB instructions whose lanes write consecutive 16-byte
   // LDS granules; lane l of instruction q fetches the logical granule that the XOR swizzle
   // puts at physical granule l % 16 of row 8w + 4q + l / 16.
-  int drow[2], dcol[2];
+  const int wu = __builtin_amdgcn_readfirstlane(w);  // the wave index as a scalar
+  int drow[2];
+  const char* dsrc[2];  // this lane's source granule in tile 0
+  const int64_t tstride = 2 * a.st;  // bytes between tokens
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     drow[q] = 8 * w + 4 * q + (lane >> 4);
-    dcol[q] = 16 * swz(drow[q], lane & 15);
+    dsrc[q] = xs + drow[q] * tstride + 16 * swz(drow[q], lane & 15);
   }
-  const int64_t tstride = 2 * a.st;  // bytes between tokens
   auto issue = [&](int tile) {
-    uint8_t* dst = xtile[(tile - tb) % kStages];
+    uint8_t* dst = xtile[(tile - tb) % kStages] + 8 * wu * kRowBytes;
+    if ((tile + 1) * kTok <= a.T) {
+      const int64_t off = int64_t(tile) * kTok * tstride;
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int tok = min(tile * kTok + drow[q], a.T - 1);
-      __builtin_amdgcn_global_load_lds(xs + tok * tstride + dcol[q],
-                                       (__attribute__((address_space(3))) void*)(dst + (8 * w + 4 * q) * kRowBytes),
-                                       16, 0, 0);
+      for (int q = 0; q < 2; ++q)
+        __builtin_amdgcn_global_load_lds(dsrc[q] + off, (__attribute__((address_space(3))) void*)(dst + 4 * q * kRowBytes),
+                                         16, 0, 0);
+    } else {
+      // ragged last tile: rows past the view repeat its last token
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int tok = min(tile * kTok + drow[q], a.T - 1);
+        __builtin_amdgcn_global_load_lds(dsrc[q] + (int64_t(tok) - drow[q]) * tstride,
+                                         (__attribute__((address_space(3))) void*)(dst + 4 * q * kRowBytes), 16, 0, 0);
+      }
     }
   };
   // Before a barrier: wait until this wave's loads of tile X have landed while the loads of
@@ -326,10 +336,16 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
       const Side sd = make_side(mn, mx, BITS);
       float r[16];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) r[e] = quantize_rint(z[e], sd.mn, sd.inv);
+      for (int e = 0; e < 16; ++e) {
+        // the byte packing below rounds to nearest even itself (2, 4, 8 bits)
+        if constexpr (BITS == 2 || BITS == 4 || BITS == 8) r[e] = quantize_t(z[e], sd.mn, sd.inv);
+        else r[e] = quantize_rint(z[e], sd.mn, sd.inv);
+      }
       constexpr int NW = (BITS & 1) ? BITS : BITS / 2;  // words this lane stores
       uint32_t words[NW];
-      // integer-valued floats to bytes (exact), bytes to b-bit fields of the LSB-first stream
+      // v_cvt_pk_u8_f32 rounds to nearest even (the quantiser's rint) and saturates to
+      // [0, 255] (codes are in [0, 2^b - 1] by construction of the side information); bytes
+      // then go to b-bit fields of the LSB-first stream
       auto pk4 = [](float c0, float c1, float c2, float c3) {
         uint32_t v = __builtin_amdgcn_cvt_pk_u8_f32(c0, 0, 0u);
         v = __builtin_amdgcn_cvt_pk_u8_f32(c1, 1, v);
