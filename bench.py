@@ -36,6 +36,9 @@ def parse():
                     help="HBM traffic per launch measured with rocprofv3 counters (optional)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the timed region, run one plain 512 MiB device copy (counter calibration)")
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b"]),
+                    help="llama8b (default) prints the headline line; the others print per-kernel timings of "
+                         "the KIVI, rolling-step and 27B-sweep workloads")
     return ap.parse_args()
 
 
@@ -88,8 +91,133 @@ def cpu_baseline(w, G_host, layers):
                       f"{t_total:.1f} s single-threaded"}
 
 
+def _timed(fn, steps, warmup, stream):
+    """Average milliseconds of fn() over `steps` launches (after `warmup`), HIP events on `stream`."""
+    import torch
+
+    for _ in range(warmup):
+        fn()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(steps):
+        fn()
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / steps
+
+
+def other_workload(name, steps, warmup):
+    """Per-kernel timings of the KIVI, rolling and 27B workloads at their full shapes, from seeded
+    synthetic K/V (synth.kv_tensor): eight distinct layers repeated to L layers for the KIVI and
+    27B inputs; for the rolling step the history is encoded from one layer viewed with layer
+    stride 0 (each layer's own gauge makes its cache distinct), and the timed step appends one
+    token per (layer, batch, head) and decodes the whole history into bf16."""
+    import numpy as np
+    import torch
+
+    from paper_2607_20538_amd import codec as cg
+    from paper_2607_20538_amd import synth
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    w = synth.WORKLOADS[name]
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out = {"workload": name, "shape": {"L": w.L, "B": w.B, "H": w.H, "T": w.T, "d": w.d}, "steps": steps}
+
+    def layer_input(s):
+        # the workload's first min(8, L) layers, repeated: 8 distinct layers of these shapes span
+        # more than the chip's caches, so every layer is read from HBM
+        nd = min(8, w.L)
+        xs = synth.kv_tensor(w, s, L=nd)
+        xs = torch.from_numpy(xs.view(np.int16)).view(torch.bfloat16).cuda()
+        X = torch.empty((w.L, w.B, w.H, w.T, w.d), dtype=torch.bfloat16, device="cuda")
+        for l0 in range(0, w.L, nd):
+            X[l0:l0 + nd] = xs[: min(nd, w.L - l0)]
+        return X
+
+    def layer_view(s):
+        # one layer viewed with layer stride 0 (history construction of the rolling workload)
+        x1 = synth.kv_tensor(w, s, L=1)
+        x1 = torch.from_numpy(x1.view(np.int16)).view(torch.bfloat16).cuda()
+        return x1.expand(w.L, w.B, w.H, w.T, w.d)
+
+    def bytes_per_elem(bits, n, kivi=False):
+        return 2.0 + bits / 8.0 + (4.0 / n if not kivi else 0.0)
+
+    if name in ("kivi", "gemma27b"):
+        combos = [(w.g, w.bits)] if name == "kivi" else [(g, b) for g in (8, 32, 128) for b in (3, 4, 6)]
+        rows = []
+        for g, bits in combos:
+            shp = cg.shape(w.L, w.H, w.d, g)
+            Gd = cg.alloc_gauge(shp)
+            cg.gauge_make(cg.GAUGE_HAAR, shp, seed=w.gauge_seed, G_host=None, G_dev=Gd)
+            if name == "kivi":
+                codec = cg.Codec(cg.KIVI, bits, 64, w.key_tokens, w.val_channels, w.residual)
+            else:
+                codec = cg.Codec(cg.BLOCK_UNIFORM, bits, w.block_c)
+            row = {"g": g, "bits": bits}
+            for s, tag in ((0, "K"), (1, "V")):
+                X = layer_input(s)
+                cache = cg.Cache(codec, s, w.L, w.B, w.H, w.T, w.d)
+                Y = torch.empty((w.L, w.B, w.H, w.T, w.d), dtype=torch.bfloat16, device="cuda")
+                enc = _timed(lambda: cg.kv_encode(s, X, Gd, shp, codec, cache, err_flag=err,
+                                                  stream=stream.cuda_stream), steps, warmup, stream)
+                if name == "kivi":
+                    cache.len = w.T
+                dec = _timed(lambda: cg.kv_decode(s, cache, Gd, shp, codec, 0, Y, err_flag=err,
+                                                  stream=stream.cuda_stream), steps, warmup, stream)
+                nelem = w.L * w.B * w.H * w.T * w.d
+                nc, ns, nr = cache.nbytes
+                alg = nelem * 2 + nc + ns + nr
+                row[tag] = {"encode_ms": round(enc, 3), "decode_ms": round(dec, 3),
+                            "encode_GBps": round(alg / enc / 1e6, 1), "decode_GBps": round(alg / dec / 1e6, 1)}
+                del X, Y, cache
+                torch.cuda.empty_cache()
+            rows.append(row)
+        out["runs"] = rows
+    else:  # rolling decode step
+        shp = cg.shape(w.L, w.H, w.d, w.g)
+        codec = cg.Codec(cg.BLOCK_UNIFORM, w.bits, w.block_c)
+        Gd = cg.alloc_gauge(shp)
+        cg.gauge_make(cg.GAUGE_HAAR, shp, seed=w.gauge_seed, G_host=None, G_dev=Gd)
+        T_cap = w.T + warmup + steps
+        caches, news, hists = [], [], []
+        for s in (0, 1):
+            X = layer_view(s)
+            c = cg.Cache(codec, s, w.L, w.B, w.H, T_cap, w.d)
+            cg.kv_encode(s, X, Gd, shp, codec, c, err_flag=err, stream=stream.cuda_stream)
+            torch.cuda.synchronize()
+            del X
+            caches.append(c)
+            nt = synth.kv_tensor(w, s, L=1, T=1, t_offset=w.T)          # one new token per (b, h)
+            nt = torch.from_numpy(nt.view(np.int16)).view(torch.bfloat16).cuda()
+            news.append(nt.expand(w.L, w.B, w.H, 1, w.d))
+            hists.append(torch.empty((w.L, w.B, w.H, T_cap, w.d), dtype=torch.bfloat16, device="cuda"))
+        pos = torch.full((w.B,), w.T, dtype=torch.int32, device="cuda")
+
+        def step():
+            cg.kv_append_step(0, w.L, news[0], news[1], pos, Gd, shp, codec, caches[0], caches[1],
+                              hists[0], hists[1], err_flag=err, stream=stream.cuda_stream)
+            pos.add_(1)
+
+        ms = _timed(step, steps, warmup, stream)
+        hist_elems = 2 * w.L * w.B * w.H * (w.T + warmup + steps // 2) * w.d
+        alg = hist_elems * bytes_per_elem(w.bits, w.block_c)
+        out["step_ms"] = round(ms, 3)
+        out["history_tokens"] = w.T
+        out["decode_GBps"] = round(alg / ms / 1e6, 1)
+    assert int(err.item()) == 0, f"device error flag {int(err.item())}"
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
+    if args.workload != WORKLOAD:
+        if args.gpus != 1:
+            print("bench.py measures one GPU", file=sys.stderr)
+            sys.exit(2)
+        other_workload(args.workload, args.steps, args.warmup)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: the codec path has no "
               f"cross-GPU step (every (layer, head, batch) slice is independent).", file=sys.stderr)
