@@ -351,14 +351,14 @@ static bool force_generic() {
 
 hipError_t launch_encode(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c, const CacheDev& k,
                          int t0, int tq, int* err, hipStream_t st) {
-  if (!force_generic() && mfma_encode_supported(X, G, c)) return launch_encode_mfma(s, X, l0, G, c, k, t0, err, st);
+  if (!force_generic() && mfma_encode_supported(X, G, c)) return launch_encode_mfma(s, X, l0, G, c, k, t0, tq, err, st);
   return launch_encode_generic(s, X, l0, G, c, k, t0, tq, err, st);
 }
 
 hipError_t launch_decode(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0, int len,
                          const int* pos, const ViewDev& Y, int* err, hipStream_t st) {
-  if (!force_generic() && mfma_decode_supported(Y, G, c))
-    return launch_decode_mfma(s, k, l0, G, c, t0, pos, Y, err, st);
+  if (!force_generic() && mfma_decode_supported(s, Y, G, c))
+    return launch_decode_mfma(s, k, l0, G, c, t0, len, pos, Y, err, st);
   return launch_decode_generic(s, k, l0, G, c, t0, len, pos, Y, err, st);
 }
 

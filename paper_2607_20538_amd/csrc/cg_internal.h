@@ -92,11 +92,11 @@ hipError_t launch_decode_generic(int s, const CacheDev& k, int l0, const GaugeDe
 
 // Matrix-core kernels: bf16, head dimension 128, block-uniform (n in {16, 32, 64}) or passthrough.
 bool mfma_encode_supported(const ViewDev& X, const GaugeDev& G, const CodecDev& c);
-bool mfma_decode_supported(const ViewDev& Y, const GaugeDev& G, const CodecDev& c);
+bool mfma_decode_supported(int s, const ViewDev& Y, const GaugeDev& G, const CodecDev& c);
 hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c,
-                              const CacheDev& k, int t0, int* err, hipStream_t st);
+                              const CacheDev& k, int t0, int tq, int* err, hipStream_t st);
 hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
-                              const int* pos, const ViewDev& Y, int* err, hipStream_t st);
+                              int len, const int* pos, const ViewDev& Y, int* err, hipStream_t st);
 
 // Device self-test of the quantiser's division-free steps (which: 0 reciprocal, 1 division).
 hipError_t launch_selftest(int which, unsigned long long* bad, hipStream_t st);

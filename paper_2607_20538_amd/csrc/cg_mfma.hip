@@ -70,6 +70,11 @@ struct MfmaArgs {
   uint8_t* codes;
   uint32_t* side;
   int T_cap, cB, cH;             // cache capacity and dims
+  // KIVI: tokens [0, tq) are quantised, [tq, T) go raw into the ring of ring_slots rows;
+  // the decoders derive tq from the positions the cache holds (len, or pos[b] + 1)
+  int tq, ring_slots;
+  uint16_t* ring;
+  int kivi, win, kg, len;
   // work split
   int nslices, chunks, tiles_per_wg;
   const int* pos;                // decode only: batch row b holds positions [0, pos[b]]
@@ -145,15 +150,22 @@ __device__ __forceinline__ void store_words(uint32_t* dst, const uint32_t* v) {
 // ------------------------------------------------------------------------------------------
 
 // z (32 rows x 32 tokens) of one tile: the NP split planes times the tile, one chain.
-template <int NP, int KS>
+// TR: the tile as the A operand and the gauge rows as the B operand, so the accumulator holds
+// z transposed (lane (n, hc): tokens 8i + 4hc + j of channel row n).
+template <int NP, int KS, bool TR = false>
 __device__ __forceinline__ f32x16_t mfma_chain(const bf16x8_t (&A)[NP][KS], const bf16x8_t (&Bf)[KS]) {
   f32x16_t acc = {};
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk)
 #pragma unroll
-    for (int p = 0; p < NP; ++p) acc = mfma(A[p][kk], Bf[kk], acc);
+    for (int p = 0; p < NP; ++p) acc = TR ? mfma(Bf[kk], A[p][kk], acc) : mfma(A[p][kk], Bf[kk], acc);
   return acc;
 }
+
+// encoder modes
+constexpr int kModeBU = 0;     // block-uniform (or KIVI values: n = value channel group)
+constexpr int kModePass = 1;   // error-free backend: binary32 z
+constexpr int kModeKeys = 2;   // KIVI keys: one block per channel over a 32-token group
 
 // Software pipeline over 32-token tiles, one barrier per tile.  Iteration t:
 //   1. block-range partials of tile t from its accumulator (64-channel blocks: wave-pair
@@ -166,15 +178,16 @@ __device__ __forceinline__ f32x16_t mfma_chain(const bf16x8_t (&A)[NP][KS], cons
 // kStages - 1 tiles are in flight between global memory and LDS.  The codes of a tile are one
 // contiguous run of 32 RB bytes in the cache and its side words one run of 32 NBK words, so
 // the staged copy leaves with whole-line stores instead of 32 scattered row pieces.
-template <int NP, int KS, int BITS, int NB, bool PASS>
+template <int NP, int KS, int BITS, int NB, int MODE>
 __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a) {
+  constexpr bool PASS = MODE == kModePass, KEYS = MODE == kModeKeys;
   constexpr int RB = kD * BITS / 8;   // packed code bytes per token row
   constexpr int NBK = kD / NB;        // side words per token row
   __shared__ __attribute__((aligned(16))) uint8_t xtile[kStages][kTok * kRowBytes];
   __shared__ float2 red[2][4][kTok];  // per-wave (min, max) of each token, for 64-channel blocks
   // a tile's packed rows and side words, staged so that they leave as contiguous stores
   __shared__ __attribute__((aligned(16))) uint8_t cstage[2][PASS ? 16 : kTok * RB];
-  __shared__ uint32_t sstage[2][PASS ? 1 : kTok * NBK];
+  __shared__ uint32_t sstage[2][PASS ? 1 : kTok * NBK];  // KIVI keys: NB = 32, one word per channel
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n = lane & 31, hc = lane >> 5;
@@ -185,11 +198,33 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
   const int l = lv + a.l0;
   const int ntiles = (a.T + kTok - 1) / kTok;
   const int tb = chunk * a.tiles_per_wg;
-  const int te = min(ntiles, tb + a.tiles_per_wg);
-  if (tb >= te) return;
+  const int te_all = min(ntiles, tb + a.tiles_per_wg);
+  if (tb >= te_all) return;
+  // tiles below tq / 32 are quantised (tq is a multiple of 32 for KIVI, T otherwise)
+  const int te = min(te_all, (a.tq + kTok - 1) / kTok);
 
   const char* xs = a.x + 2 * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
   const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
+  const int64_t tstride = 2 * a.st;  // bytes between tokens
+
+  // KIVI full-precision window: rows of tiles [max(tb, te), te_all) copied raw into the ring
+  // (slot = position mod ring_slots; 32-token tiles never wrap since ring_slots is a multiple
+  // of 32)
+  auto ring_copy = [&]() {
+    for (int tile = max(tb, te); tile < te_all; ++tile) {
+      const int nlive = min(kTok, a.T - tile * kTok);
+      uint16_t* dst = a.ring + (cslice * a.ring_slots + (tile * kTok) % a.ring_slots) * kD;
+      for (int gi = int(threadIdx.x); gi < nlive * (kRowBytes / 16); gi += kThreads) {
+        const int row = gi / (kRowBytes / 16), j = gi % (kRowBytes / 16);
+        *(u32x4_t*)((char*)dst + row * kRowBytes + 16 * j) =
+            *(const u32x4_t*)(xs + int64_t(tile * kTok + row) * tstride + 16 * j);
+      }
+    }
+  };
+  if (tb >= te) {
+    ring_copy();
+    return;
+  }
 
   // K range of this wave's rows: the group of channels 32w.. (whole head for g = 128)
   const int kbase = a.g >= 32 ? (32 * w / a.g) * a.g : 32 * w;
@@ -205,7 +240,6 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
   const int wu = __builtin_amdgcn_readfirstlane(w);  // the wave index as a scalar
   int drow[2];
   const char* dsrc[2];  // this lane's source granule in tile 0
-  const int64_t tstride = 2 * a.st;  // bytes between tokens
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     drow[q] = 8 * w + 4 * q + (lane >> 4);
@@ -258,7 +292,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
   __builtin_amdgcn_s_barrier();
   bfrags(tb);
   f32x16_t acc[2];
-  acc[0] = mfma_chain<NP, KS>(A, Bf);
+  acc[0] = mfma_chain<NP, KS, KEYS>(A, Bf);
   int flags = 0;
   // staged tile -> cache: thread i stores 16-byte granule i of the codes (row i / BITS) and,
   // counting from the last thread, side word i (row i / NBK); rows past the view are skipped
@@ -313,7 +347,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
     }
     // 5. next tile on the matrix core (past the range it reads a stale buffer and is unused),
     //    this tile's epilogue on the VALU; no branch until the stores
-    acc[P ^ 1] = mfma_chain<NP, KS>(A, Bf);
+    acc[P ^ 1] = mfma_chain<NP, KS, KEYS>(A, Bf);
 
     if constexpr (PASS) {
 #pragma unroll
@@ -326,6 +360,47 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
 #pragma unroll
         for (int q = 0; q < 4; ++q) *(float4*)(dst + 4 * q) = make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
       }
+    } else if constexpr (KEYS) {
+      // z^T: lane (n, hc) holds tokens 8i + 4hc + j (e = 4i + j) of channel chA; the block is
+      // the channel over the tile's 32 tokens (in-lane 16 + the other half-wave's 16)
+      bad = bad || !(mn >= -3.0e38f && mx <= 3.0e38f);
+      const Side sd = make_side(mn, mx, BITS);
+      // the channel's LSB-first stream of 32 codes in token order (BITS words): this lane's
+      // codes placed as if hc = 0 (token 8i + j at bit (8i + j) BITS), shifted by 4 BITS bits
+      // for hc = 1, then the two half-wave patterns OR-ed together
+      uint32_t words[BITS];
+#pragma unroll
+      for (int i = 0; i < BITS; ++i) words[i] = 0;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const uint32_t q = uint32_t(quantize_rint(z[e], sd.mn, sd.inv));
+        const int bit = (8 * (e >> 2) + (e & 3)) * BITS, wd = bit >> 5, off = bit & 31;
+        words[wd] |= q << off;
+        if (off + BITS > 32) words[wd + 1] |= q >> (32 - off);
+      }
+      if (hc) {
+        constexpr int SH = 4 * BITS;  // <= 32
+#pragma unroll
+        for (int i = BITS - 1; i >= 0; --i) {
+          const uint32_t lo = i > 0 ? words[i - 1] : 0u;
+          words[i] = SH == 32 ? lo : ((words[i] << (SH & 31)) | (lo >> ((32 - SH) & 31)));
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < BITS; ++i) words[i] |= __shfl_xor(words[i], 32);
+#pragma unroll
+      for (int i = 0; i < BITS; ++i) asm volatile("" ::"v"(words[i]));
+      asm volatile("" ::"v"(sd.word));
+#pragma unroll
+      for (int i = 0; i < KS * NP; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+      }
+      if (hc == 0) {
+        store_words<BITS>((uint32_t*)(cstage[P] + chA * 4 * BITS), words);
+        sstage[P][chA] = sd.word;
+      }
+      flags |= sd.flags | (bad ? CG_FLAG_NONFINITE : 0);
     } else {
       if constexpr (NB == 64) {
         const float2 o = red[P][w ^ 1][n];
@@ -428,12 +503,42 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
     if ((te - tb) & 1) flush(te - 1, std::integral_constant<int, 0>());
     else flush(te - 1, std::integral_constant<int, 1>());
   }
+  ring_copy();
   if (flags && a.err) atomicOr(a.err, flags);
 }
 
 // ------------------------------------------------------------------------------------------
 // decode
 // ------------------------------------------------------------------------------------------
+// KIVI decode: of a cache holding positions [0, held), [0, tq) are quantised and [tq, held)
+// sit raw in the window ring, tq = floor((held - W) / kg) kg (0 below W).  Returns the view
+// rows [0, Tq) that are quantised (view row r is position t0 + r), Tq <= Tv.
+__device__ __forceinline__ int kivi_quantised_rows(const MfmaArgs& a, int held, int Tv) {
+  const int tq = held < a.win ? 0 : ((held - a.win) / a.kg) * a.kg;
+  return max(0, min(Tv, tq - a.t0));
+}
+
+// View rows [r0, r1) copied from the window ring (bf16, slot = position mod ring_slots).
+template <bool OUT_BF16>
+__device__ void ring_rows(const MfmaArgs& a, size_t cslice, char* ys, int r0, int r1) {
+  constexpr int YB = OUT_BF16 ? 2 : 4;
+  for (int gi = r0 * 16 + int(threadIdx.x); gi < r1 * 16; gi += kThreads) {
+    const int row = gi >> 4, j = gi & 15;
+    const int slot = (a.t0 + row) % a.ring_slots;
+    const u32x4_t v = *(const u32x4_t*)(a.ring + (cslice * a.ring_slots + slot) * kD + 8 * j);
+    char* dst = ys + YB * (int64_t(row) * a.st + 8 * j);
+    if constexpr (OUT_BF16) {
+      *(u32x4_t*)dst = v;
+    } else {
+      float4 lo = make_float4(bf16_to_f32(v[0] & 0xffffu), bf16_to_f32(v[0] >> 16), bf16_to_f32(v[1] & 0xffffu), bf16_to_f32(v[1] >> 16));
+      float4 hi = make_float4(bf16_to_f32(v[2] & 0xffffu), bf16_to_f32(v[2] >> 16), bf16_to_f32(v[3] & 0xffffu), bf16_to_f32(v[3] >> 16));
+      *(float4*)dst = lo;
+      *(float4*)(dst + 16) = hi;
+    }
+  }
+}
+
+
 // Sum over the 8-channel segments [j0, j1) of the gauge buffer's column sums of channel i
 // (the two split planes of G^T over each segment's channels in i's group).
 __device__ __forceinline__ float seg_colsum(const MfmaArgs& a, int l, int h, int i, int j0, int j1) {
@@ -464,17 +569,28 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
   const int h = slice % a.H, b = (slice / a.H) % a.B, lv = slice / (a.H * a.B);
   const int l = lv + a.l0;
   int Tv = a.T;  // view tokens to write
+  int held = a.kivi ? a.len : INT_MAX;  // positions the cache holds
   if (a.pos) {
     const int p = a.pos[b];
     if (p < 0 || p >= a.T_cap) return;  // flagged by the append kernel
+    held = p + 1;
     Tv = min(Tv, p + 1 - a.t0);
   }
   const int ntiles = (Tv + kTok - 1) / kTok;
   const int tb = chunk * a.tiles_per_wg;
-  const int te = min(ntiles, tb + a.tiles_per_wg);
-  if (tb >= te) return;
+  const int te_all = min(ntiles, tb + a.tiles_per_wg);
+  if (tb >= te_all) return;
   char* ys = a.x + (OUT_BF16 ? 2 : 4) * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
   const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
+  // KIVI: the quantised view rows [0, Tq) go through the pipeline, the window rows after it
+  const int Tq = a.kivi ? kivi_quantised_rows(a, held, Tv) : Tv;
+  const int te = min(te_all, (Tq + kTok - 1) / kTok);
+  if (tb >= te) {
+    ring_rows<OUT_BF16>(a, cslice, ys, max(Tq, tb * kTok), min(Tv, te_all * kTok));
+    return;
+  }
+  const int Tv_all = Tv;
+  Tv = Tq;  // rows the pipeline writes
 
   const int kbase = a.g >= 32 ? (32 * w / a.g) * a.g : 32 * w;
   const int chA = 32 * w + 16 * ((n >> 2) & 1) + 4 * (n >> 3) + (n & 3);
@@ -665,6 +781,7 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
     __syncthreads();
   }
   flush(te - 1, (te - 1 - tb) & 1);
+  ring_rows<OUT_BF16>(a, cslice, ys, max(Tq, tb * kTok), min(Tv_all, te_all * kTok));
 }
 
 // ------------------------------------------------------------------------------------------
@@ -834,17 +951,29 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
   const int h = slice % a.H, b = (slice / a.H) % a.B, lv = slice / (a.H * a.B);
   const int l = lv + a.l0;
   int Tv = a.T;
+  int held = a.kivi ? a.len : INT_MAX;  // positions the cache holds
   if (a.pos) {
     const int p = a.pos[b];
     if (p < 0 || p >= a.T_cap) return;  // flagged by the append kernel
+    held = p + 1;
     Tv = min(Tv, p + 1 - a.t0);
   }
   const int ntiles = (Tv + kTok - 1) / kTok;
   const int tb = chunk * a.tiles_per_wg;
-  const int te = min(ntiles, tb + a.tiles_per_wg);
-  if (tb >= te) return;
+  const int te_all = min(ntiles, tb + a.tiles_per_wg);
+  if (tb >= te_all) return;
   char* ys = a.x + YB * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
-  const size_t crow0 = (size_t(l) * a.cB + b) * a.cH * size_t(a.T_cap) + size_t(h) * a.T_cap + a.t0;
+  const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
+  const size_t crow0 = cslice * size_t(a.T_cap) + a.t0;
+  // KIVI: the quantised view rows [0, Tq) go through the pipeline, the window rows after it
+  const int Tq = a.kivi ? kivi_quantised_rows(a, held, Tv) : Tv;
+  const int te = min(te_all, (Tq + kTok - 1) / kTok);
+  if (tb >= te) {
+    ring_rows<OUT_BF16>(a, cslice, ys, max(Tq, tb * kTok), min(Tv, te_all * kTok));
+    return;
+  }
+  const int Tv_all = Tv;
+  Tv = Tq;  // rows the pipeline writes
 
   const int kbase = a.g >= 32 ? (32 * w / a.g) * a.g : 32 * w;
   const int chA = 32 * w + 16 * ((n >> 2) & 1) + 4 * (n >> 3) + (n & 3);
@@ -1007,6 +1136,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
   __builtin_amdgcn_s_waitcnt(waitcnt_imm(63));
   __builtin_amdgcn_s_barrier();
   flush(te - 1, (te - 1 - tb) & 1);
+  ring_rows<OUT_BF16>(a, cslice, ys, max(Tq, tb * kTok), min(Tv_all, te_all * kTok));
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1046,29 +1176,30 @@ void plan(MfmaArgs& m, int nslices, int T, const void* fn) {
 }
 
 template <int KS, int BITS, int NB>
-void* enc_kernel(bool pass) {
-  if (pass) return (void*)enc_mfma<kNP, KS, 8, 64, true>;
-  return (void*)enc_mfma<enc_planes(BITS), KS, BITS, NB, false>;
+void* enc_kernel(int mode) {
+  if (mode == kModePass) return (void*)enc_mfma<kNP, KS, 8, 64, kModePass>;
+  if (mode == kModeKeys) return (void*)enc_mfma<enc_planes(BITS), KS, BITS, 32, kModeKeys>;
+  return (void*)enc_mfma<enc_planes(BITS), KS, BITS, NB, kModeBU>;
 }
 
 template <int KS, int BITS>
-void* enc_by_nb(int nb, bool pass) {
+void* enc_by_nb(int nb, int mode) {
   switch (nb) {
-    case 16: return enc_kernel<KS, BITS, 16>(pass);
-    case 32: return enc_kernel<KS, BITS, 32>(pass);
-    case 64: return enc_kernel<KS, BITS, 64>(pass);
+    case 16: return enc_kernel<KS, BITS, 16>(mode);
+    case 32: return enc_kernel<KS, BITS, 32>(mode);
+    case 64: return enc_kernel<KS, BITS, 64>(mode);
   }
   return nullptr;
 }
 
 template <int KS>
-void* enc_by_bits(int bits, int nb, bool pass) {
+void* enc_by_bits(int bits, int nb, int mode) {
   switch (bits) {
-    case 2: return enc_by_nb<KS, 2>(nb, pass);
-    case 3: return enc_by_nb<KS, 3>(nb, pass);
-    case 4: return enc_by_nb<KS, 4>(nb, pass);
-    case 6: return enc_by_nb<KS, 6>(nb, pass);
-    case 8: return enc_by_nb<KS, 8>(nb, pass);
+    case 2: return enc_by_nb<KS, 2>(nb, mode);
+    case 3: return enc_by_nb<KS, 3>(nb, mode);
+    case 4: return enc_by_nb<KS, 4>(nb, mode);
+    case 6: return enc_by_nb<KS, 6>(nb, mode);
+    case 8: return enc_by_nb<KS, 8>(nb, mode);
   }
   return nullptr;
 }
@@ -1146,16 +1277,20 @@ bool bits_ok(int b) { return b == 2 || b == 3 || b == 4 || b == 6 || b == 8; }
 bool mfma_encode_supported(const ViewDev& X, const GaugeDev& G, const CodecDev& c) {
   if (!X.bf16 || X.d != kD || !group_ok(G.g)) return false;
   if (c.backend == CG_BACKEND_PASSTHROUGH) return true;
+  if (c.backend == CG_BACKEND_KIVI)
+    return bits_ok(c.bits) && c.kg == kTok && (c.kvc == 16 || c.kvc == 32 || c.kvc == 64) && c.win % kTok == 0;
   return c.backend == CG_BACKEND_BLOCK_UNIFORM && bits_ok(c.bits) && (c.n == 16 || c.n == 32 || c.n == 64);
 }
 
-bool mfma_decode_supported(const ViewDev& Y, const GaugeDev& G, const CodecDev& c) {
-  if (Y.d != kD || !group_ok(G.g)) return false;
-  return c.backend == CG_BACKEND_BLOCK_UNIFORM && bits_ok(c.bits) && (c.n == 16 || c.n == 32 || c.n == 64);
+bool mfma_decode_supported(int s, const ViewDev& Y, const GaugeDev& G, const CodecDev& c) {
+  if (Y.d != kD || !group_ok(G.g) || !bits_ok(c.bits)) return false;
+  if (c.backend == CG_BACKEND_KIVI)  // values: block-uniform rows plus the window ring
+    return s == 1 && (c.kvc == 16 || c.kvc == 32 || c.kvc == 64) && c.win % kTok == 0;
+  return c.backend == CG_BACKEND_BLOCK_UNIFORM && (c.n == 16 || c.n == 32 || c.n == 64);
 }
 
 hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c,
-                              const CacheDev& k, int t0, int* err, hipStream_t st) {
+                              const CacheDev& k, int t0, int tq, int* err, hipStream_t st) {
   if (X.T == 0) return hipSuccess;
   MfmaArgs m{};
   m.x = (char*)X.ptr;
@@ -1166,12 +1301,17 @@ hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G
   m.g32 = G.f32; m.g = G.g; m.R = G.R; m.Hg = G.H;
   m.codes = k.codes; m.side = k.side; m.T_cap = k.T_cap; m.cB = k.B; m.cH = k.H;
   m.err = err;
+  const bool pass = c.backend == CG_BACKEND_PASSTHROUGH, kivi = c.backend == CG_BACKEND_KIVI;
+  m.tq = kivi ? tq : X.T;
+  m.ring = k.ring;
+  m.ring_slots = kivi ? c.win + c.kg : 0;
+  const int mode = pass ? kModePass : (kivi && s == 0 ? kModeKeys : kModeBU);
+  const int nb = pass ? 64 : (kivi ? c.kvc : c.n), bits = pass ? 8 : c.bits;
   void* fn = nullptr;
-  const bool pass = c.backend == CG_BACKEND_PASSTHROUGH;
   switch (ksteps(G.g)) {
-    case 2: fn = enc_by_bits<2>(pass ? 8 : c.bits, pass ? 64 : c.n, pass); break;
-    case 4: fn = enc_by_bits<4>(pass ? 8 : c.bits, pass ? 64 : c.n, pass); break;
-    case 8: fn = enc_by_bits<8>(pass ? 8 : c.bits, pass ? 64 : c.n, pass); break;
+    case 2: fn = enc_by_bits<2>(bits, nb, mode); break;
+    case 4: fn = enc_by_bits<4>(bits, nb, mode); break;
+    case 8: fn = enc_by_bits<8>(bits, nb, mode); break;
   }
   if (!fn) return hipErrorInvalidValue;
   plan(m, X.L * X.B * X.H, X.T, fn);
@@ -1181,7 +1321,7 @@ hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G
 }
 
 hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
-                              const int* pos, const ViewDev& Y, int* err, hipStream_t st) {
+                              int len, const int* pos, const ViewDev& Y, int* err, hipStream_t st) {
   if (Y.T == 0) return hipSuccess;
   MfmaArgs m{};
   m.x = (char*)Y.ptr;
@@ -1193,20 +1333,27 @@ hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& 
   m.codes = k.codes; m.side = k.side; m.T_cap = k.T_cap; m.cB = k.B; m.cH = k.H;
   m.pos = pos;
   m.err = err;
+  m.kivi = c.backend == CG_BACKEND_KIVI;
+  m.win = c.win;
+  m.kg = c.kg;
+  m.len = len;
+  m.ring = k.ring;
+  m.ring_slots = c.win + c.kg;
+  const int nb = m.kivi ? c.kvc : c.n;
   void* fn = nullptr;
-  if (G.g >= c.n) {
+  if (G.g >= nb) {
     // blocks inside one group: codes feed the matrix core without conversion
     switch (ksteps(G.g)) {
-      case 2: fn = fast_by_bits<2>(c.bits, c.n, Y.bf16); break;
-      case 4: fn = fast_by_bits<4>(c.bits, c.n, Y.bf16); break;
-      case 8: fn = fast_by_bits<8>(c.bits, c.n, Y.bf16); break;
+      case 2: fn = fast_by_bits<2>(c.bits, nb, Y.bf16); break;
+      case 4: fn = fast_by_bits<4>(c.bits, nb, Y.bf16); break;
+      case 8: fn = fast_by_bits<8>(c.bits, nb, Y.bf16); break;
     }
   }
   if (!fn) {
     switch (ksteps(G.g)) {
-      case 2: fn = dec_by_bits<2>(c.bits, c.n, Y.bf16); break;
-      case 4: fn = dec_by_bits<4>(c.bits, c.n, Y.bf16); break;
-      case 8: fn = dec_by_bits<8>(c.bits, c.n, Y.bf16); break;
+      case 2: fn = dec_by_bits<2>(c.bits, nb, Y.bf16); break;
+      case 4: fn = dec_by_bits<4>(c.bits, nb, Y.bf16); break;
+      case 8: fn = dec_by_bits<8>(c.bits, nb, Y.bf16); break;
     }
   }
   if (!fn) return hipErrorInvalidValue;

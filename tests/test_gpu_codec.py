@@ -181,7 +181,7 @@ def test_tiny_workload_end_to_end():
 # KIVI-style backend
 # ------------------------------------------------------------------------------------------
 @pytest.mark.parametrize("g,bits", [(32, 3), (128, 4), (16, 2)])
-def test_kivi_encode_decode(g, bits):
+def test_kivi_encode_decode(g, bits, kernels):
     T, T_cap = 300, 320
     w = _workload(T=T)
     G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, g)
@@ -208,7 +208,7 @@ def test_kivi_encode_decode(g, bits):
         np.testing.assert_array_equal(sub, outb[:, :, :, 100:250])
 
 
-def test_kivi_short_cache_decodes_as_a_copy():
+def test_kivi_short_cache_decodes_as_a_copy(kernels):
     T = 100
     w = _workload(T=T)
     G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, 32)
