@@ -1140,6 +1140,210 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
 }
 
 // ------------------------------------------------------------------------------------------
+// decode, KIVI keys (per-channel ranges over 32-token groups), groups of at most 32 channels
+// ------------------------------------------------------------------------------------------
+// LDS ring depth: code + side stages within what is left of 52 KB (three workgroups per CU)
+// for bf16 output, of 64 KB for binary32 output, at most kDStages
+constexpr int keys_stages(int bits, bool bf16) {
+  const int fixed = 2 * kTok * kD * (bf16 ? 2 : 4);
+  const int room = (bf16 ? 52 : 64) * 1024 - fixed, stage = kD * 4 * bits + kD * 4;
+  return room / stage > kDStages ? kDStages : room / stage;
+}
+
+// One tile is one key group (cache positions 32k .. 32k + 31); with gauge groups of at most 32
+// channels, wave w's contraction runs over its own 32 channels, so each wave dequantises
+// exactly the codes it multiplies.  Lane (n, hc) rebuilds zhat = fl(mn + q sc) of token n for
+// its 16 K-channels in binary32 (the dequantised value itself), splits it into three bf16
+// planes (exact: a binary32 value holds 24 significant bits), and the matrix core multiplies
+// them by the two G^T planes (plane products below 2^-24 of the leading term dropped).  The
+// error is thus relative to the group norm of zhat, whatever the channels' offsets; with the
+// identity gauge the result is zhat bit for bit.
+template <int NP, int KS, int BITS, bool OUT_BF16>
+__global__ __launch_bounds__(kThreads, OUT_BF16 ? 3 : 2) void dec_keys(MfmaArgs a) {
+  static_assert(KS == 2 && NP == 2, "groups of at most 32 channels, two gauge planes");
+  constexpr int CB = 4 * BITS;                       // bytes of one channel's 32 codes
+  constexpr int YB = OUT_BF16 ? 2 : 4;
+  constexpr int GPR = kD * YB / 16;
+  constexpr int F = kTok * GPR / kThreads;
+  constexpr int DS = keys_stages(BITS, OUT_BF16);
+  static_assert(DS >= 3, "LDS ring too shallow");
+  __shared__ __attribute__((aligned(16))) uint8_t ctile[DS][kD * CB];   // code block of a group
+  __shared__ __attribute__((aligned(16))) uint32_t stile[DS][kD];       // side word per channel
+  __shared__ __attribute__((aligned(16))) uint8_t ystage[2][kTok * kD * YB];
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n = lane & 31, hc = lane >> 5;
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int slice = logical / a.chunks, chunk = logical - slice * a.chunks;
+  if (slice >= a.nslices) return;
+  const int h = slice % a.H, b = (slice / a.H) % a.B, lv = slice / (a.H * a.B);
+  const int l = lv + a.l0;
+  int Tv = a.T;
+  int held = a.len;
+  if (a.pos) {
+    const int p = a.pos[b];
+    if (p < 0 || p >= a.T_cap) return;  // flagged by the append kernel
+    held = p + 1;
+    Tv = min(Tv, p + 1 - a.t0);
+  }
+  if (Tv <= 0) return;
+  char* ys = a.x + YB * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
+  const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
+  const int Tq = kivi_quantised_rows(a, held, Tv);  // quantised view rows [0, Tq)
+  // tiles u = key groups g0 + u; tile u holds view rows 32 (g0 + u) - t0 + j, j < 32
+  const int g0 = a.t0 / kTok;
+  const int ntiles = (a.t0 + Tv + kTok - 1) / kTok - g0;
+  const int tb = chunk * a.tiles_per_wg;
+  const int te_all = min(ntiles, tb + a.tiles_per_wg);
+  if (tb >= te_all) return;
+  const int te = min(te_all, (a.t0 + Tq + kTok - 1) / kTok - g0);
+  const int row_lo = max(0, kTok * (g0 + tb) - a.t0), row_hi = min(Tv, kTok * (g0 + te_all) - a.t0);
+  if (tb >= te) {
+    ring_rows<OUT_BF16>(a, cslice, ys, max(Tq, row_lo), row_hi);
+    return;
+  }
+
+  const int kbase = 32 * w;  // groups of at most 32 channels: the wave's own channels
+  const int chA = 32 * w + 16 * ((n >> 2) & 1) + 4 * (n >> 3) + (n & 3);
+  bf16x8_t A[NP][KS];
+  load_a<NP, KS>(A, a, l, h, chA, kbase, hc);  // rows chA of the G^T planes, natural K order
+
+  // LDS-direct loads of a group: wave w moves code granules [8 BITS w, +8 BITS) and side words
+  // [32 w, +32) of the group block (contiguous in the cache)
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  const size_t grp0 = cslice * size_t(a.T_cap / kTok) + g0;
+  auto issue = [&](int tile) {
+    const int st = (tile - tb) % DS;
+    const size_t gi = grp0 + tile;
+    if (lane < 8 * BITS)
+      __builtin_amdgcn_global_load_lds(a.codes + gi * (kD * CB) + 16 * (8 * BITS * w + lane),
+                                       (__attribute__((address_space(3))) void*)(ctile[st] + 16 * 8 * BITS * wu), 16, 0, 0);
+    if (lane < 32)
+      __builtin_amdgcn_global_load_lds(a.side + gi * kD + 32 * w + lane,
+                                       (__attribute__((address_space(3))) void*)(stile[st] + 32 * wu), 4, 0, 0);
+  };
+  // staged rows -> the view: tile row j is view row 32 (g0 + tile) - t0 + j; rows outside the
+  // quantised range repeat a live row's granule (same data, same address)
+  int64_t yoff[F];
+  int ysrc[F];
+#pragma unroll
+  for (int k = 0; k < F; ++k) {
+    const int gi = int(threadIdx.x) + k * kThreads, row = gi / GPR, j = gi % GPR;
+    yoff[k] = int64_t(YB) * row * a.st + 16 * j;
+    ysrc[k] = row * kD * YB + 16 * (j ^ (row & (GPR - 1)));
+  }
+  auto flush = [&](int tile, const uint8_t* stage) {
+    const int r0 = kTok * (g0 + tile) - a.t0;          // view row of tile row 0 (may be < 0)
+    const int lo = max(0, -r0), hi = min(kTok, Tq - r0);  // live tile rows
+    char* yt = ys + int64_t(YB) * r0 * a.st;
+    if (lo == 0 && hi == kTok) {
+#pragma unroll
+      for (int k = 0; k < F; ++k) *(u32x4_t*)(yt + yoff[k]) = *(const u32x4_t*)(stage + ysrc[k]);
+    } else {
+#pragma unroll
+      for (int k = 0; k < F; ++k) {
+        const int gi = int(threadIdx.x) + k * kThreads, j = gi % GPR;
+        int row = gi / GPR;
+        row = row < lo ? lo : (row >= hi ? hi - 1 : row);
+        const u32x4_t v = *(const u32x4_t*)(stage + row * kD * YB + 16 * (j ^ (row & (GPR - 1))));
+        *(u32x4_t*)(yt + int64_t(YB) * row * a.st + 16 * j) = v;
+      }
+    }
+  };
+  // vector-memory operations a wave has issued after tile X's two loads, at the wait of
+  // iteration t: the prologue's later loads, then per iteration i the flush of tile i - 1 (F
+  // stores) and the loads of tile i + DS - 1
+  const int pe = min(te, tb + DS - 1);
+  auto younger = [&](int X, int t) {
+    if (X - (DS - 1) >= tb && t + DS - 2 < te) return (t - (X - (DS - 1)) - 1) * (F + 2);
+    int c = 0, i = tb;
+    if (X < pe) c = 2 * (pe - 1 - X);
+    else i = X - (DS - 1) + 1;
+    for (; i < t; ++i) c += (i > tb ? F : 0) + (i + DS - 1 < te ? 2 : 0);
+    return c;
+  };
+  // this lane's code of token n in a channel stream: word wd, bit offset off
+  constexpr uint32_t MASK = (1u << BITS) - 1u;
+  const int cbit = n * BITS, cwd = cbit >> 5, coff = cbit & 31;
+
+  for (int t = tb; t < pe; ++t) issue(t);
+  for (int t = tb; t < te; ++t) {
+    const int P = (t - tb) & 1;
+    wait_vm_atmost(younger(t, t));
+    __builtin_amdgcn_s_barrier();
+    if (t > tb) flush(t - 1, ystage[P ^ 1]);
+    if (t + DS - 1 < te) issue(t + DS - 1);
+    const uint8_t* ct = ctile[(t - tb) % DS];
+    const uint32_t* sw = stile[(t - tb) % DS];
+    f32x16_t acc = {};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const int j0 = kbase + 16 * kk + 8 * hc;
+      const u32x4_t s0 = *(const u32x4_t*)(sw + j0), s1 = *(const u32x4_t*)(sw + j0 + 4);
+      const uint32_t swd[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+      float zh[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t* cw = (const uint32_t*)(ct + (j0 + e) * CB);
+        uint32_t v;
+        if constexpr (32 % BITS == 0) {
+          v = cw[cwd] >> coff;
+        } else {  // the code may straddle two words (never past the stream's last word)
+          const uint32_t lo = cw[cwd], hi = coff + BITS > 32 ? cw[cwd + 1] : 0u;
+          v = uint32_t(((uint64_t(hi) << 32) | lo) >> coff);
+        }
+        const float mn = f16_bits_to_f32(swd[e] & 0xffffu), sc = f16_bits_to_f32(swd[e] >> 16);
+        zh[e] = fmaf(float(v & MASK), sc, mn);  // q sc is exact: one rounding, as dequantised
+      }
+      // three bf16 planes of zhat by truncation (each residual exact in binary32)
+      uint32_t bp[3][4];
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        uint32_t x0 = __float_as_uint(zh[2 * e2]), x1 = __float_as_uint(zh[2 * e2 + 1]);
+#pragma unroll
+        for (int p = 0; p < 3; ++p) {
+          bp[p][e2] = __builtin_amdgcn_perm(x1, x0, 0x07060302u);
+          if (p < 2) {
+            x0 = __float_as_uint(__uint_as_float(x0) - __uint_as_float(x0 & 0xffff0000u));
+            x1 = __float_as_uint(__uint_as_float(x1) - __uint_as_float(x1 & 0xffff0000u));
+          }
+        }
+      }
+      bf16x8_t B[3];
+#pragma unroll
+      for (int p = 0; p < 3; ++p) B[p] = as_bf16x8(u32x4_t{bp[p][0], bp[p][1], bp[p][2], bp[p][3]});
+      // plane products, smallest first: (1,1) (0,2) (1,0) (0,1) (0,0)
+      acc = mfma(A[1][kk], B[1], acc);
+      acc = mfma(A[0][kk], B[2], acc);
+      acc = mfma(A[1][kk], B[0], acc);
+      acc = mfma(A[0][kk], B[1], acc);
+      acc = mfma(A[0][kk], B[0], acc);
+    }
+    uint8_t* yrow = ystage[P] + n * kD * YB;
+    if constexpr (OUT_BF16) {
+      typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+      typedef float f32x2_t __attribute__((ext_vector_type(2)));
+      uint32_t pk[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        pk[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{acc[2 * e], acc[2 * e + 1]}), bf16x2_t));
+      const int j0 = 4 * w + 2 * hc;
+      *(u32x4_t*)(yrow + 16 * (j0 ^ (n & (GPR - 1)))) = u32x4_t{pk[0], pk[1], pk[2], pk[3]};
+      *(u32x4_t*)(yrow + 16 * ((j0 + 1) ^ (n & (GPR - 1)))) = u32x4_t{pk[4], pk[5], pk[6], pk[7]};
+    } else {
+      const int j0 = 8 * w + 4 * hc;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *(float4*)(yrow + 16 * ((j0 + q) ^ (n & (GPR - 1)))) = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(63));
+  __builtin_amdgcn_s_barrier();
+  flush(te - 1, ystage[(te - 1 - tb) & 1]);
+  ring_rows<OUT_BF16>(a, cslice, ys, max(Tq, row_lo), row_hi);
+}
+
+// ------------------------------------------------------------------------------------------
 // dispatch
 // ------------------------------------------------------------------------------------------
 // Split planes of the gauge on the matrix core.  Decoding takes two (16 significant bits per
@@ -1268,6 +1472,23 @@ void* fast_by_bits(int bits, int nb, bool bf16) {
   return nullptr;
 }
 
+template <int BITS>
+void* keys_kernel(bool bf16) {
+  if (bf16) return (void*)dec_keys<kNP, 2, BITS, true>;
+  return (void*)dec_keys<kNP, 2, BITS, false>;
+}
+
+void* keys_by_bits(int bits, bool bf16) {
+  switch (bits) {
+    case 2: return keys_kernel<2>(bf16);
+    case 3: return keys_kernel<3>(bf16);
+    case 4: return keys_kernel<4>(bf16);
+    case 6: return keys_kernel<6>(bf16);
+    case 8: return keys_kernel<8>(bf16);
+  }
+  return nullptr;
+}
+
 bool group_ok(int g) { return g == 8 || g == 16 || g == 32 || g == 64 || g == 128; }
 
 bool bits_ok(int b) { return b == 2 || b == 3 || b == 4 || b == 6 || b == 8; }
@@ -1284,8 +1505,11 @@ bool mfma_encode_supported(const ViewDev& X, const GaugeDev& G, const CodecDev& 
 
 bool mfma_decode_supported(int s, const ViewDev& Y, const GaugeDev& G, const CodecDev& c) {
   if (Y.d != kD || !group_ok(G.g) || !bits_ok(c.bits)) return false;
-  if (c.backend == CG_BACKEND_KIVI)  // values: block-uniform rows plus the window ring
-    return s == 1 && (c.kvc == 16 || c.kvc == 32 || c.kvc == 64) && c.win % kTok == 0;
+  if (c.backend == CG_BACKEND_KIVI) {
+    if (c.win % kTok) return false;
+    if (s == 0) return c.kg == kTok && G.g <= 32;  // key groups, gauge groups within one K-step pair
+    return c.kvc == 16 || c.kvc == 32 || c.kvc == 64;  // values: block-uniform rows
+  }
   return c.backend == CG_BACKEND_BLOCK_UNIFORM && (c.n == 16 || c.n == 32 || c.n == 64);
 }
 
@@ -1339,6 +1563,15 @@ hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& 
   m.len = len;
   m.ring = k.ring;
   m.ring_slots = c.win + c.kg;
+  if (m.kivi && s == 0) {
+    // one tile per 32-position key group: the first may start before t0
+    void* fn = keys_by_bits(c.bits, Y.bf16);
+    if (!fn) return hipErrorInvalidValue;
+    plan(m, Y.L * Y.B * Y.H, t0 % kTok + Y.T, fn);
+    const int nwg = ((m.nslices * m.chunks + 7) / 8) * 8;
+    void* args[] = {&m};
+    return hipLaunchKernel(fn, dim3(nwg), dim3(kThreads), args, 0, st);
+  }
   const int nb = m.kivi ? c.kvc : c.n;
   void* fn = nullptr;
   if (G.g >= nb) {

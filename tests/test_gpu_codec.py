@@ -92,7 +92,8 @@ def test_gauge_stage_matches_oracle(g, dtype, kernels):
 # quantise-only and dequantise-only: bit-exact
 # ------------------------------------------------------------------------------------------
 QCASES = [(O.BLOCK_UNIFORM, b, n) for b in (2, 3, 4, 6, 8) for n in (32, 64)] + \
-         [(O.BLOCK_UNIFORM, 4, 16), (O.BLOCK_UNIFORM, 8, 128), (O.KIVI, 3, 64), (O.KIVI, 4, 64), (O.KIVI, 2, 32)]
+         [(O.BLOCK_UNIFORM, 4, 16), (O.BLOCK_UNIFORM, 8, 128), (O.KIVI, 3, 64), (O.KIVI, 4, 64), (O.KIVI, 2, 32),
+          (O.KIVI, 6, 64), (O.KIVI, 8, 16)]
 
 
 @pytest.mark.parametrize("backend,bits,n", QCASES)
@@ -218,6 +219,34 @@ def test_kivi_short_cache_decodes_as_a_copy(kernels):
         dev = _encode_gpu(X, s, Gd, shp, oc, 128)
         dev.len = T
         np.testing.assert_array_equal(_decode_gpu(dev, s, Gd, shp, oc, 0, T), X)
+
+
+@pytest.mark.parametrize("g", [8, 32])
+@pytest.mark.parametrize("bits", [2, 3, 4, 6, 8])
+def test_kivi_key_decoder(g, bits):
+    """Key groups through the matrix-core key decoder (gauge groups of at most 32 channels)
+    at every width: binary32 out within the gauge tolerance of the oracle, bf16 out within a
+    bf16 ulp, window rows copied exactly, and sub-range decodes that start inside a key group
+    or cover a single row agree with the full decode."""
+    T, T_cap = 300, 320
+    w = _workload(T=T, seed=0x5EED + bits)
+    G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, g, seed=bits)
+    oc = O.Codec(backend=O.KIVI, bits=bits, key_tokens=32, val_channels=64, residual=128)
+    tq = O.kivi_tq(T, oc)
+    X = synth.kv_tensor(w, 0)
+    orc, flags = O.kv_encode(oc, 0, X, G, T_cap=T_cap)
+    assert flags == 0
+    ddev = cache_to_dev(orc, oc, 0, 1, 2, 2, T_cap, 128, len_=T)
+    ref = O.kv_decode(oc, 0, G, orc, 0, T, lens=[T, T], out_bf16=False)
+    out = _decode_gpu(ddev, 0, Gd, shp, oc, 0, T, torch.float32)
+    assert group_rel_err(ref[:, :, :, :tq], out[:, :, :, :tq], g) <= GAUGE_TOL
+    np.testing.assert_array_equal(out[:, :, :, tq:], ref[:, :, :, tq:])
+    outb = _decode_gpu(ddev, 0, Gd, shp, oc, 0, T)
+    check_bf16_within_ulp(ref[:, :, :, :tq], outb[:, :, :, :tq], g)
+    np.testing.assert_array_equal(outb[:, :, :, tq:], X[:, :, :, tq:])
+    for t0, n in ((37, 203), (64, 1), (5, 27), (tq - 3, 6)):
+        np.testing.assert_array_equal(_decode_gpu(ddev, 0, Gd, shp, oc, t0, n), outb[:, :, :, t0:t0 + n])
+        np.testing.assert_array_equal(_decode_gpu(ddev, 0, Gd, shp, oc, t0, n, torch.float32), out[:, :, :, t0:t0 + n])
 
 
 # ------------------------------------------------------------------------------------------
