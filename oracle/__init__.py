@@ -57,9 +57,9 @@ def lib():
         L.orc_dequantize_block.argtypes = [vp, i, C.c_uint16, C.c_uint16, vp]
         L.orc_pack_codes.argtypes = [vp, i, i, vp]
         L.orc_unpack_codes.argtypes = [vp, i, i, vp]
-        L.orc_kv_encode.argtypes = [i] * 13 + [i, vp, vp, i, vp, vp, vp, i]
-        L.orc_kv_decode.argtypes = [i] * 12 + [vp, i, vp, vp, vp, vp, i, i, i, vp]
-        L.orc_kv_append.argtypes = [i] * 12 + [i, vp, vp, i, vp, vp, vp, vp]
+        L.orc_kv_encode.argtypes = [i] * 14 + [i, vp, vp, i, vp, vp, vp, i]
+        L.orc_kv_decode.argtypes = [i] * 13 + [vp, i, vp, vp, vp, vp, i, i, i, vp]
+        L.orc_kv_append.argtypes = [i] * 13 + [i, vp, vp, i, vp, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -187,9 +187,11 @@ class Codec:
     key_tokens: int = 32       # KIVI key token group
     val_channels: int = 64     # KIVI value channel group
     residual: int = 128        # KIVI full-precision window
+    block_t: int = 1           # block-uniform tile tokens Tb (1: one token per block)
 
     def args(self):
-        return [self.backend, self.bits, self.block_c, self.key_tokens, self.val_channels, self.residual]
+        return [self.backend, self.bits, self.block_c, self.key_tokens, self.val_channels, self.residual,
+                self.block_t]
 
 
 def cache_layout(codec: Codec, s: int, L: int, B: int, H: int, T_cap: int, d: int) -> dict:
@@ -198,9 +200,10 @@ def cache_layout(codec: Codec, s: int, L: int, B: int, H: int, T_cap: int, d: in
     if codec.backend == PASSTHROUGH:
         return {"codes": ((L, B, H, T_cap, d), np.float32), "side": None, "residual": None}
     if codec.backend == BLOCK_UNIFORM:
-        n = codec.block_c
+        n, bt = codec.block_c, codec.block_t
+        staging = ((L, B, H, bt, d), np.uint16) if bt > 1 else None
         return {"codes": ((L, B, H, T_cap, d * b // 8), np.uint8),
-                "side": ((L, B, H, T_cap, d // n, 2), np.uint16), "residual": None}
+                "side": ((L, B, H, T_cap // bt, d // n, 2), np.uint16), "residual": staging}
     kg, kvc, win = codec.key_tokens, codec.val_channels, codec.residual
     ring = ((L, B, H, win + kg, d), np.uint16)
     if s == 0:
@@ -213,6 +216,11 @@ def cache_layout(codec: Codec, s: int, L: int, B: int, H: int, T_cap: int, d: in
 def empty_cache(codec: Codec, s: int, L: int, B: int, H: int, T_cap: int, d: int) -> dict:
     lay = cache_layout(codec, s, L, B, H, T_cap, d)
     return {k: (None if v is None else np.zeros(v[0], dtype=v[1])) for k, v in lay.items()}
+
+
+def tile_tq(T: int, codec: Codec) -> int:
+    """Tokens quantised when a block-uniform cache of Tb-token tiles holds T tokens."""
+    return (T // codec.block_t) * codec.block_t
 
 
 def kivi_tq(T: int, codec: Codec) -> int:
@@ -297,7 +305,8 @@ def live_bytes(codec: Codec, s: int, T: int, d: int) -> int:
     if codec.backend == PASSTHROUGH:
         return T * d * 4
     if codec.backend == BLOCK_UNIFORM:
-        return T * (d * b // 8 + (d // codec.block_c) * 4)
+        tq = tile_tq(T, codec)
+        return tq * d * b // 8 + (tq // codec.block_t) * (d // codec.block_c) * 4 + (T - tq) * d * 2
     tq = kivi_tq(T, codec)
     win = (T - tq) * d * 2
     if s == 0:

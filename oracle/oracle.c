@@ -14,7 +14,10 @@
  *
  * Backends (section 4.3, Compression Conditions):
  *   - error-free passthrough (the no-compression sanity rows of section 4.4),
- *   - block-uniform b-bit quantisation with one (min, scale) range per block,
+ *   - block-uniform b-bit quantisation with one (min, scale) range per block: a block is
+ *     n channels of one token vector, or, in the token-channel tiles the paper names, the
+ *     same n channels over T_b consecutive tokens (an unfinished tile waits in a bf16
+ *     staging window),
  *   - KIVI-style quantisation: per-channel key ranges over token groups and
  *     per-token value ranges over channel groups, with a full-precision window
  *     of recent tokens.
@@ -411,7 +414,9 @@ void orc_unpack_codes(const uint8_t* in, int n, int bits, uint8_t* q) {
 /* Whole-cache encode / decode / rolling append, over the byte layouts of the codec library:  */
 /*   X, Xhat     [L][B][H][T][d] contiguous, bf16 bits or binary32                            */
 /*   BU codes    [L][B][H][T_cap][d*b/8]  (blocks of n channels, LSB-first streams)           */
-/*   BU side     [L][B][H][T_cap][d/n][2] binary16 (min, scale)                               */
+/*   BU side     [L][B][H][T_cap/Tb][d/n][2] binary16 (min, scale); Tb = 1: per token         */
+/*   BU staging  (Tb > 1) [L][B][H][Tb][d] raw bf16, slot = t mod Tb; a cache holding T       */
+/*               tokens quantises the first floor(T / Tb) Tb of them                          */
 /*   passthrough [L][B][H][T_cap][d] binary32 z                                               */
 /*   KIVI keys   codes [L][B][H][T_cap/G][d][G*b/8], side [L][B][H][T_cap/G][d][2]            */
 /*   KIVI values as BU with n = value channel group                                           */
@@ -422,6 +427,7 @@ void orc_unpack_codes(const uint8_t* in, int n, int bits, uint8_t* q) {
 
 typedef struct {
   int backend, bits, n, kg, kvc, win;   /* n: BU block; kg: key token group; kvc: value channel group */
+  int bt;                               /* BU tile tokens Tb (1: one token per block) */
   int L, B, H, d, g, T_cap;
 } orc_layout;
 
@@ -437,6 +443,7 @@ static int check_layout(const orc_layout* o) {
   if (o->bits < 1 || o->bits > 8) return ORC_EARG;
   if (o->backend == ORC_BACKEND_BLOCK_UNIFORM) {
     if (o->n <= 0 || o->n > 256 || o->d % o->n || (o->n * o->bits) % 8) return ORC_EARG;
+    if (o->bt < 1 || o->bt > 256 || o->T_cap % o->bt) return ORC_EARG;
     return 0;
   }
   if (o->backend == ORC_BACKEND_KIVI) {
@@ -458,6 +465,24 @@ static int encode_row(const float* z, int d, int n, int bits, uint8_t* code_row,
     flags |= orc_quantize_block(z + k * n, n, bits, q, &side_row[2 * k], &side_row[2 * k + 1]);
     orc_pack_codes(q, n, bits, code_row + (size_t)k * row_block_bytes);
   }
+  return flags;
+}
+
+/* Block-uniform token-channel tile: the bt gauge-space rows zt[bt][d] of consecutive tokens
+ * share one range per block of n channels (the bt x n values quantised as one block, token
+ * by token); each token keeps its own code row, blocks in channel order as for bt = 1. */
+static int encode_tile(const float* zt, int bt, int d, int n, int bits, uint8_t* code_rows, uint16_t* side_tile) {
+  int flags = 0, row_bytes = d * bits / 8, blk_bytes = n * bits / 8;
+  float* vals = (float*)malloc(sizeof(float) * (size_t)bt * n);
+  uint8_t* q = (uint8_t*)malloc((size_t)bt * n);
+  for (int k = 0; k < d / n; ++k) {
+    for (int u = 0; u < bt; ++u)
+      for (int c = 0; c < n; ++c) vals[u * n + c] = zt[(size_t)u * d + k * n + c];
+    flags |= orc_quantize_block(vals, bt * n, bits, q, &side_tile[2 * k], &side_tile[2 * k + 1]);
+    for (int u = 0; u < bt; ++u)
+      orc_pack_codes(q + u * n, n, bits, code_rows + (size_t)u * row_bytes + (size_t)k * blk_bytes);
+  }
+  free(vals); free(q);
   return flags;
 }
 
@@ -526,15 +551,35 @@ static int kivi_flush(const orc_layout* o, int s, size_t sl, const float* Gs, in
   return flags;
 }
 
+/* Quantise the staged tokens [t_begin, t_begin + Tb) of one slice as one tile. */
+static int tile_flush(const orc_layout* o, size_t sl, const float* Gs, int t_begin, uint8_t* codes, uint16_t* side,
+                      const uint16_t* staging) {
+  int d = o->d, bt = o->bt, flags = 0;
+  float* x = (float*)malloc(sizeof(float) * d);
+  float* zt = (float*)malloc(sizeof(float) * (size_t)bt * d);
+  for (int u = 0; u < bt; ++u) {
+    const uint16_t* srow = staging + (sl * bt + (size_t)((t_begin + u) % bt)) * d;
+    for (int c = 0; c < d; ++c) x[c] = orc_bf16_to_f32(srow[c]);
+    orc_gauge_apply(d, o->g, Gs, x, zt + (size_t)u * d);
+  }
+  int row_bytes = d * o->bits / 8, nb = d / o->n;
+  flags |= encode_tile(zt, bt, d, o->n, o->bits, codes + (sl * o->T_cap + (size_t)t_begin) * row_bytes,
+                       side + (sl * (o->T_cap / bt) + (size_t)(t_begin / bt)) * nb * 2);
+  free(x); free(zt);
+  return flags;
+}
+
 /* Encode tokens [t0, t0 + T) of X (s: 0 = keys, 1 = values) into the cache.  KIVI requires
  * t0 == 0: the T tokens form the whole cache, T_q of them quantised, the rest in the ring.
  * Returns the OR of ORC_FLAG_* over all blocks, or a negative error. */
-int orc_kv_encode(int backend, int bits, int n, int kg, int kvc, int win, int s, int L, int B, int H, int T, int d,
-                  int g, int x_bf16, const void* X, const float* Gall, int T_cap, void* codes, void* side,
+int orc_kv_encode(int backend, int bits, int n, int kg, int kvc, int win, int bt, int s, int L, int B, int H, int T,
+                  int d, int g, int x_bf16, const void* X, const float* Gall, int T_cap, void* codes, void* side,
                   void* residual, int t0) {
-  orc_layout o = {backend, bits, n, kg, kvc, win, L, B, H, d, g, T_cap};
+  orc_layout o = {backend, bits, n, kg, kvc, win, bt, L, B, H, d, g, T_cap};
   if (check_layout(&o) || s < 0 || s > 1 || T < 0 || t0 < 0 || t0 + T > T_cap) return ORC_EARG;
   if (backend == ORC_BACKEND_KIVI && (t0 != 0 || !x_bf16)) return ORC_EARG;
+  const int tile = backend == ORC_BACKEND_BLOCK_UNIFORM && bt > 1;
+  if (tile && (t0 % bt || !x_bf16)) return ORC_EARG;
   int R = d / g, flags = 0;
   size_t gsz = (size_t)R * g * g;
   float* x = (float*)malloc(sizeof(float) * d);
@@ -575,6 +620,28 @@ int orc_kv_encode(int backend, int bits, int n, int kg, int kvc, int win, int s,
           free(zt);
           continue;
         }
+        if (tile) {
+          /* whole tiles quantised (positions t0 + [0, T_q)), the unfinished one staged raw */
+          int tq = (T / bt) * bt;
+          uint16_t* staging = (uint16_t*)residual;
+          for (int t = tq; t < T; ++t)
+            memcpy(staging + (sl * bt + (size_t)((t0 + t) % bt)) * d, (const uint16_t*)X + xbase + (size_t)t * d,
+                   sizeof(uint16_t) * d);
+          float* zt = (float*)malloc(sizeof(float) * (size_t)bt * d);
+          for (int t = 0; t < tq; t += bt) {
+            for (int u = 0; u < bt; ++u) {
+              for (int c = 0; c < d; ++c) x[c] = load_x(X, 1, xbase + (size_t)(t + u) * d + c);
+              for (int c = 0; c < d; ++c)
+                if (!isfinite(x[c])) flags |= ORC_FLAG_NONFINITE;
+              orc_gauge_apply(d, g, Gs, x, zt + (size_t)u * d);
+            }
+            int row_bytes = d * bits / 8, nb = d / n;
+            flags |= encode_tile(zt, bt, d, n, bits, (uint8_t*)codes + (sl * T_cap + (size_t)(t0 + t)) * row_bytes,
+                                 (uint16_t*)side + (sl * (T_cap / bt) + (size_t)((t0 + t) / bt)) * nb * 2);
+          }
+          free(zt);
+          continue;
+        }
         for (int t = 0; t < T; ++t) {
           for (int c = 0; c < d; ++c) x[c] = load_x(X, x_bf16, xbase + (size_t)t * d + c);
           for (int c = 0; c < d; ++c)
@@ -594,15 +661,16 @@ int orc_kv_encode(int backend, int bits, int n, int kg, int kvc, int win, int s,
 }
 
 /* Decode tokens [t0, t0 + Tout) of every slice into Xhat[L][B][H][Tout][d] (bf16 bits when
- * out_bf16, else binary32).  KIVI needs the number of tokens the cache holds for each batch
- * row, lens[b]; tokens at or beyond lens[b] are left untouched.  lens may be NULL for the
- * other backends. */
-int orc_kv_decode(int backend, int bits, int n, int kg, int kvc, int win, int s, int L, int B, int H, int d, int g,
-                  const float* Gall, int T_cap, const void* codes, const void* side, const void* residual,
+ * out_bf16, else binary32).  KIVI and token-channel tiles need the number of tokens the cache
+ * holds for each batch row, lens[b]; tokens at or beyond lens[b] are left untouched.  lens
+ * may be NULL for the other backends. */
+int orc_kv_decode(int backend, int bits, int n, int kg, int kvc, int win, int bt, int s, int L, int B, int H, int d,
+                  int g, const float* Gall, int T_cap, const void* codes, const void* side, const void* residual,
                   const int* lens, int t0, int Tout, int out_bf16, void* Xhat) {
-  orc_layout o = {backend, bits, n, kg, kvc, win, L, B, H, d, g, T_cap};
+  orc_layout o = {backend, bits, n, kg, kvc, win, bt, L, B, H, d, g, T_cap};
   if (check_layout(&o) || s < 0 || s > 1 || t0 < 0 || Tout < 0 || t0 + Tout > T_cap) return ORC_EARG;
-  if (backend == ORC_BACKEND_KIVI && !lens) return ORC_EARG;
+  const int tile = backend == ORC_BACKEND_BLOCK_UNIFORM && bt > 1;
+  if ((backend == ORC_BACKEND_KIVI || tile) && !lens) return ORC_EARG;
   int R = d / g;
   size_t gsz = (size_t)R * g * g;
   float* zh = (float*)malloc(sizeof(float) * d);
@@ -613,13 +681,14 @@ int orc_kv_decode(int backend, int bits, int n, int kg, int kvc, int win, int s,
         size_t sl = slice_index(&o, l, b, h);
         const float* Gs = Gall + (((size_t)l * 2 + s) * H + h) * gsz;
         int len = lens ? lens[b] : T_cap;
-        int tq = backend == ORC_BACKEND_KIVI ? kivi_tq(len, win, kg) : len;
+        int tq = backend == ORC_BACKEND_KIVI ? kivi_tq(len, win, kg) : (tile ? (len / bt) * bt : len);
         for (int u = 0; u < Tout; ++u) {
           int t = t0 + u;
           if (t >= len) continue;
           size_t obase = (sl * (size_t)Tout + u) * d;
-          if (backend == ORC_BACKEND_KIVI && t >= tq) {
-            const uint16_t* rrow = (const uint16_t*)residual + (sl * (size_t)(win + kg) + (size_t)(t % (win + kg))) * d;
+          if ((backend == ORC_BACKEND_KIVI || tile) && t >= tq) {
+            const int slots = tile ? bt : win + kg;
+            const uint16_t* rrow = (const uint16_t*)residual + (sl * (size_t)slots + (size_t)(t % slots)) * d;
             for (int c = 0; c < d; ++c) {
               if (out_bf16) ((uint16_t*)Xhat)[obase + c] = rrow[c];
               else ((float*)Xhat)[obase + c] = orc_bf16_to_f32(rrow[c]);
@@ -631,7 +700,8 @@ int orc_kv_decode(int backend, int bits, int n, int kg, int kvc, int win, int s,
             memcpy(zh, (const float*)codes + row * d, sizeof(float) * d);
           } else if (backend == ORC_BACKEND_BLOCK_UNIFORM) {
             int row_bytes = d * bits / 8, nb = d / n;
-            decode_row((const uint8_t*)codes + row * row_bytes, (const uint16_t*)side + row * nb * 2, d, n, bits, zh);
+            size_t srow = sl * (T_cap / bt) + (size_t)(t / bt);
+            decode_row((const uint8_t*)codes + row * row_bytes, (const uint16_t*)side + srow * nb * 2, d, n, bits, zh);
           } else if (s == 0) {
             int cb = kg * bits / 8;
             size_t gbase = sl * (T_cap / kg) + t / kg;
@@ -655,15 +725,17 @@ int orc_kv_decode(int backend, int bits, int n, int kg, int kvc, int win, int s,
 
 /* Rolling step (section 4.4: every new KV token passes through gauge, backend, decode and
  * inverse gauge): append the token Xnew[L][B][H][d] at position pos[b] of each batch row.
- * Block-uniform / passthrough encode it in place; KIVI puts it in the ring and, when the
- * cache then holds T = pos + 1 tokens with T - W a positive multiple of G, gauges and
- * quantises the G oldest ring tokens [T - W - G, T - W). */
-int orc_kv_append(int backend, int bits, int n, int kg, int kvc, int win, int s, int L, int B, int H, int d, int g,
-                  int x_bf16, const void* Xnew, const float* Gall, int T_cap, void* codes, void* side,
+ * Block-uniform (one token per block) / passthrough encode it in place; KIVI puts it in the
+ * ring and, when the cache then holds T = pos + 1 tokens with T - W a positive multiple of G,
+ * gauges and quantises the G oldest ring tokens [T - W - G, T - W); token-channel tiles stage
+ * it and quantise the tile once its Tb-th token arrives. */
+int orc_kv_append(int backend, int bits, int n, int kg, int kvc, int win, int bt, int s, int L, int B, int H, int d,
+                  int g, int x_bf16, const void* Xnew, const float* Gall, int T_cap, void* codes, void* side,
                   void* residual, const int* pos) {
-  orc_layout o = {backend, bits, n, kg, kvc, win, L, B, H, d, g, T_cap};
+  orc_layout o = {backend, bits, n, kg, kvc, win, bt, L, B, H, d, g, T_cap};
   if (check_layout(&o) || s < 0 || s > 1) return ORC_EARG;
-  if (backend == ORC_BACKEND_KIVI && !x_bf16) return ORC_EARG;
+  const int tile = backend == ORC_BACKEND_BLOCK_UNIFORM && bt > 1;
+  if ((backend == ORC_BACKEND_KIVI || tile) && !x_bf16) return ORC_EARG;
   for (int b = 0; b < B; ++b)
     if (pos[b] < 0 || pos[b] >= T_cap) return ORC_EARG;
   int R = d / g, flags = 0;
@@ -684,6 +756,14 @@ int orc_kv_append(int backend, int bits, int n, int kg, int kvc, int win, int s,
           int T = t + 1;
           if (T - win >= kg && (T - win) % kg == 0)
             flags |= kivi_flush(&o, s, sl, Gs, T - win - kg, (uint8_t*)codes, (uint16_t*)side, ring);
+          continue;
+        }
+        if (tile) {
+          uint16_t* staging = (uint16_t*)residual;
+          memcpy(staging + (sl * bt + (size_t)(t % bt)) * d, (const uint16_t*)Xnew + xin, sizeof(uint16_t) * d);
+          for (int c = 0; c < d; ++c)
+            if (!isfinite(orc_bf16_to_f32(((const uint16_t*)Xnew)[xin + c]))) flags |= ORC_FLAG_NONFINITE;
+          if ((t + 1) % bt == 0) flags |= tile_flush(&o, sl, Gs, t + 1 - bt, (uint8_t*)codes, (uint16_t*)side, staging);
           continue;
         }
         for (int c = 0; c < d; ++c) x[c] = load_x(Xnew, x_bf16, xin + c);

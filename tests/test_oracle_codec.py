@@ -251,3 +251,126 @@ def test_lossy_codec_error_is_bounded_per_block():
     sc = np.vectorize(O.f16_value)(cache["side"][0, 0, 0, :, :, 1])
     err = np.linalg.norm(Xh[0, 0, 0] - x, axis=1)
     assert np.all(err <= np.sqrt(64 * (sc[:, 0] / 2) ** 2 + 64 * (sc[:, 1] / 2) ** 2) * (1 + 1e-5))
+
+
+# ------------------------------------------------------------------------------------------
+# block-uniform token-channel tiles (section 4.3: one range per T_b x d block, T_b = 16 in the
+# experimental setup of section 5): the same n channels of Tb consecutive tokens share a range
+# ------------------------------------------------------------------------------------------
+def _tile(bits=4, n=128, bt=16):
+    return O.Codec(backend=O.BLOCK_UNIFORM, bits=bits, block_c=n, block_t=bt)
+
+
+def _z_rows(K, G, b, h, t0, t1, s=0):
+    return np.stack([O.gauge_apply(G[0, s, h], np.array([O.bf16_to_f32(v) for v in K[0, b, h, t]], np.float32))
+                     for t in range(t0, t1)])
+
+
+@pytest.mark.parametrize("bits,n", [(4, 128), (3, 64), (6, 32), (2, 128)])
+def test_tile_range_covers_the_whole_tile(bits, n):
+    """The side information of a tile is the binary16 range of all its Tb x n gauge-space
+    values (checked in numpy against the passthrough z): mn_h is the largest binary16 at or
+    below the tile minimum, the grid reaches the maximum, and every token of the tile is
+    within half a step of its reconstruction."""
+    bt = 16
+    w, K, _ = _tensor(64)
+    G = O.gauge_make(O.GAUGE_HAAR, 1, 2, 128, 32, seed=11)
+    codec = _tile(bits, n, bt)
+    cache, flags = O.kv_encode(codec, 0, K, G, T_cap=64)
+    assert flags == 0
+    zpass, _ = O.kv_encode(O.Codec(backend=O.PASSTHROUGH), 0, K, G, T_cap=64)
+    zh = O.kv_decode(O.Codec(backend=O.BLOCK_UNIFORM, bits=bits, block_c=n, block_t=bt), 0,
+                     O.gauge_make(O.GAUGE_IDENTITY, 1, 2, 128, 32), cache, 0, 64, lens=[64, 64], out_bf16=False)
+    qmax = (1 << bits) - 1
+    for b in range(2):
+        for h in range(2):
+            for tile in range(4):
+                for k in range(128 // n):
+                    blk = zpass["codes"][0, b, h, bt * tile:bt * tile + bt, n * k:n * k + n].astype(np.float64)
+                    mnb, scb = cache["side"][0, b, h, tile, k]
+                    mn, sc = _f16(mnb), _f16(scb)
+                    assert mn <= blk.min()
+                    nxt = float(np.nextafter(np.float16(mn), np.float16(np.inf), dtype=np.float16))
+                    assert nxt > blk.min()
+                    assert mn + qmax * sc >= blk.max() * (1 - 2.0 ** -22) - 2.0 ** -22
+                    rec = zh[0, b, h, bt * tile:bt * tile + bt, n * k:n * k + n].astype(np.float64)
+                    assert np.abs(rec - blk).max() <= sc / 2 * (1 + 2.0 ** -20) + 2.0 ** -22 * np.abs(blk).max()
+
+
+def test_tile_of_repeated_token_equals_per_token_block():
+    """A tile whose Tb tokens are one vector repeated has that vector's own block range, so
+    its codes and side words equal the per-token block-uniform ones."""
+    w, K, _ = _tensor(4)
+    Kr = np.ascontiguousarray(np.repeat(K[:, :, :, :1], 16, axis=3))
+    G = O.gauge_make(O.GAUGE_HAAR, 1, 2, 128, 32, seed=12)
+    for bits, n in ((4, 128), (3, 32)):
+        tile, _ = O.kv_encode(_tile(bits, n, 16), 0, Kr, G, T_cap=16)
+        per, _ = O.kv_encode(O.Codec(backend=O.BLOCK_UNIFORM, bits=bits, block_c=n), 0, Kr, G, T_cap=16)
+        np.testing.assert_array_equal(tile["codes"], per["codes"])
+        for t in range(16):
+            np.testing.assert_array_equal(tile["side"][:, :, :, 0], per["side"][:, :, :, t])
+
+
+def test_tile_equals_quantiser_on_the_token_channel_block():
+    """A tile's codes are those of one block made of its Tb x n values, token by token, with
+    each token's n codes in its own row at the block's place."""
+    w, K, _ = _tensor(48)
+    G = O.gauge_make(O.GAUGE_HAAR, 1, 2, 128, 32, seed=13)
+    cache, _ = O.kv_encode(_tile(3, 64, 16), 0, K, G, T_cap=48)
+    b, h = 1, 1
+    for tile in range(3):
+        Z = _z_rows(K, G, b, h, 16 * tile, 16 * tile + 16)
+        for k in range(2):
+            q, mnb, scb, _ = O.quantize_block(np.ascontiguousarray(Z[:, 64 * k:64 * k + 64]).reshape(-1), 3)
+            assert tuple(cache["side"][0, b, h, tile, k]) == (mnb, scb)
+            for u in range(16):
+                np.testing.assert_array_equal(cache["codes"][0, b, h, 16 * tile + u, 24 * k:24 * k + 24],
+                                              O.pack_codes(q[64 * u:64 * u + 64], 3))
+
+
+def test_tile_unfinished_tokens_stay_raw():
+    """Tokens past the last whole tile wait in the bf16 staging window and decode bit for bit;
+    a cache shorter than one tile is all staging."""
+    G = O.gauge_make(O.GAUGE_HAAR, 1, 2, 128, 32, seed=14)
+    codec = _tile(4, 128, 16)
+    for T in (40, 9):
+        w, K, V = _tensor(T)
+        for s, X in ((0, K), (1, V)):
+            c, _ = O.kv_encode(codec, s, X, G, T_cap=48)
+            tq = O.tile_tq(T, codec)
+            assert tq == (32 if T == 40 else 0)
+            assert not c["codes"][:, :, :, tq:].any()
+            Xh = O.kv_decode(codec, s, G, c, 0, T, lens=[T, T])
+            np.testing.assert_array_equal(Xh[:, :, :, tq:], X[:, :, :, tq:])
+            for t in range(tq, T):
+                np.testing.assert_array_equal(c["residual"][:, :, :, t % 16], X[:, :, :, t])
+
+
+def test_tile_rolling_append_equals_batch_encode():
+    """Appending tokens one at a time (staged until a tile is whole) leaves the same codes,
+    side information and staging window as one batch encode, and decodes the same history."""
+    T0, steps = 37, 46
+    w, K, V = _tensor(T0 + steps, B=2)
+    G = O.gauge_make(O.GAUGE_HAAR, 1, 2, 128, 32, seed=15)
+    codec = _tile(4, 64, 16)
+    T_cap, T = 96, T0 + steps
+    for s, X in ((0, K), (1, V)):
+        roll, _ = O.kv_encode(codec, s, np.ascontiguousarray(X[:, :, :, :T0]), G, T_cap=T_cap)
+        for t in range(T0, T):
+            O.kv_append(codec, s, np.ascontiguousarray(X[:, :, :, t]), G, roll, [t, t])
+        full, _ = O.kv_encode(codec, s, X, G, T_cap=T_cap)
+        for key in ("codes", "side"):
+            np.testing.assert_array_equal(roll[key], full[key])
+        for t in range(O.tile_tq(T, codec), T):   # slots of flushed tokens keep stale rows
+            np.testing.assert_array_equal(roll["residual"][:, :, :, t % 16], full["residual"][:, :, :, t % 16])
+        np.testing.assert_array_equal(O.kv_decode(codec, s, G, roll, 0, T, lens=[T, T]),
+                                      O.kv_decode(codec, s, G, full, 0, T, lens=[T, T]))
+
+
+def test_tile_bits_per_value_closed_form():
+    """Tiles carry two binary16 per Tb x n values: b + 32 / (Tb n) bits per value, e.g.
+    4 + 1/64 for the 16 x 128 tile at 4 bits; unfinished tokens count 16 bits."""
+    for b in (3, 4, 6):
+        assert O.bits_per_value(_tile(b, 128, 16), 8192, 128) == b + 32 / 2048
+    ref = (8192 * (4 + 32 / 2048) + 8 * 16) / 8200
+    assert abs(O.bits_per_value(_tile(4, 128, 16), 8200, 128) - ref) < 1e-12
