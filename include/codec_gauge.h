@@ -40,7 +40,12 @@
  *   block-uniform   codes [L][B][H][T_cap][d*b/8] bytes: the d/n blocks of one token in
  *                   channel order, each an LSB-first stream of n b-bit codes (bit k of a
  *                   stream is bit k mod b of code floor(k/b); stream bit k is bit k%8 of
- *                   byte k/8); side [L][B][H][T_cap][d/n][2] binary16 (min, scale).
+ *                   byte k/8); side [L][B][H][T_cap/Tb][d/n][2] binary16 (min, scale), one
+ *                   pair per block of n channels over Tb consecutive tokens (Tb = block_t;
+ *                   Tb = 1: per token).  With Tb > 1, staging [L][B][H][Tb][d] raw bf16
+ *                   (the residual buffer) holds the tokens of the unfinished tile, token t
+ *                   in slot t mod Tb: a cache holding T tokens quantises the first
+ *                   floor(T/Tb) * Tb of them.
  *   KIVI keys       codes [L][B][H][T_cap/Gk][d][Gk*b/8]: per channel, the LSB-first stream
  *                   of the Gk tokens of one token group; side [L][B][H][T_cap/Gk][d][2].
  *   KIVI values     as block-uniform with n = val_channels.
@@ -106,9 +111,14 @@ typedef struct cg_gauge_shape {
 /* Backend parameters.  bits: b in {2,3,4,6,8}.  block_c: block-uniform channel block n
  * (n | d, n * b % 32 == 0).  key_tokens (Gk, KIVI keys: channel ranges over Gk tokens),
  * val_channels (KIVI values: token ranges over that many channels), residual (W, KIVI
- * full-precision window of recent tokens).  Unused fields are ignored. */
+ * full-precision window of recent tokens).  block_t: block-uniform tile tokens Tb in
+ * {1, 2, 4, 8, 16, 32}; 1 gives one range per n channels of each token vector, Tb > 1 one
+ * range per n channels of Tb consecutive tokens (the token-channel tiles of section 4.3,
+ * Tb = 16 in the paper's setup), quantised once the tile's last token is there (bf16 input
+ * only).  Unused fields are ignored. */
 typedef struct cg_codec {
   int32_t backend, bits, block_c, key_tokens, val_channels, residual;
+  int32_t block_t;
 } cg_codec;
 
 /* A strided view of a KV tensor [L][B][H][T][d] in device memory. */
@@ -120,11 +130,11 @@ typedef struct cg_kv_view {
 } cg_kv_view;
 
 /* One compressed K or V cache (device buffers sized by cache_bytes()).  len: tokens the
- * cache currently holds (host value, read by kv_decode for KIVI only). */
+ * cache currently holds (host value, read by kv_decode for KIVI and block-uniform tiles). */
 typedef struct cg_cache {
   void* codes;
   void* side;      /* NULL for passthrough */
-  void* residual;  /* KIVI window; NULL otherwise */
+  void* residual;  /* KIVI window or tile staging; NULL otherwise */
   int32_t L, B, H, T_cap, d;
   int32_t len;
 } cg_cache;
@@ -149,15 +159,17 @@ int32_t gauge_make(int32_t kind, cg_gauge_shape shp, uint64_t seed, const float*
                    void* G_dev, void* stream);
 
 /* Byte sizes of the codes / side / residual buffers of one cache of type s (0 = K,
- * 1 = V) with capacity T_cap tokens (T_cap a multiple of key_tokens for KIVI).  Any
- * output pointer may be NULL. */
+ * 1 = V) with capacity T_cap tokens (T_cap a multiple of key_tokens for KIVI, of block_t
+ * for block-uniform tiles).  Any output pointer may be NULL. */
 int32_t cache_bytes(const cg_codec* codec, int32_t s, int32_t L, int32_t B, int32_t H, int32_t T_cap, int32_t d,
                     size_t* codes, size_t* side, size_t* residual);
 
 /* Encode: Z = G X, B_c = C(Z) (section 3) for the X->T tokens of X_s, written at cache
  * positions [t0, t0 + X->T).  s: 0 keys, 1 values.  G_dev: from gauge_make with the same
  * shape.  KIVI requires t0 == 0 and bf16 input: X is the whole cache (T_q tokens
- * quantised, the rest copied to the window).  out->len is not modified.
+ * quantised, the rest copied to the window).  Block-uniform tiles (block_t = Tb > 1)
+ * require t0 % Tb == 0 and bf16 input: the floor(X->T / Tb) whole tiles are quantised and
+ * the remaining tokens staged.  out->len is not modified.
  * Errors: CG_ERR_ARG, CG_ERR_SHAPE, CG_ERR_ALIGN, CG_ERR_UNSUPPORTED, CG_ERR_CAPACITY,
  * CG_ERR_DEVICE. */
 int32_t kv_encode(int32_t s, const cg_kv_view* X, const void* G_dev, cg_gauge_shape shp, const cg_codec* codec,
@@ -165,8 +177,8 @@ int32_t kv_encode(int32_t s, const cg_kv_view* X, const void* G_dev, cg_gauge_sh
 
 /* Decode: Zhat = D(B_c), Xhat = G^T Zhat (section 3) for cache positions
  * [t0, t0 + Xhat->T) into Xhat (bf16 rounded to nearest even, or binary32).  KIVI tokens
- * at or beyond T_q(in->len) come back from the window bit for bit; KIVI requires
- * t0 + Xhat->T <= in->len.
+ * at or beyond T_q(in->len), and staged tokens of block-uniform tiles (at or beyond
+ * floor(in->len / Tb) * Tb), come back bit for bit; both require t0 + Xhat->T <= in->len.
  * Errors: as kv_encode. */
 int32_t kv_decode(int32_t s, const cg_cache* in, const void* G_dev, cg_gauge_shape shp, const cg_codec* codec,
                   int32_t t0, const cg_kv_view* Xhat, int32_t* err_flag, void* stream);
@@ -177,6 +189,8 @@ int32_t kv_decode(int32_t s, const cg_cache* in, const void* G_dev, cg_gauge_sha
  *      (pos: device int32[B], read on the device, never by the host);  KIVI puts it in
  *      the window and, when the cache then holds T = pos[b] + 1 tokens with T - W a
  *      positive multiple of Gk, gauges and quantises the Gk oldest window tokens;
+ *      block-uniform tiles stage it and, when it is the last token of its tile
+ *      (pos[b] + 1 a multiple of Tb), gauge and quantise the tile;
  *   2. if k_hist / v_hist are non-NULL, decode the history [0, pos[b]] of those layers
  *      into them (tokens beyond pos[b] are left untouched).
  * k_new / v_new: views with L = l1 - l0 and T = 1 (view layer i is cache layer l0 + i).

@@ -624,9 +624,12 @@ int orc_kv_encode(int backend, int bits, int n, int kg, int kvc, int win, int bt
           /* whole tiles quantised (positions t0 + [0, T_q)), the unfinished one staged raw */
           int tq = (T / bt) * bt;
           uint16_t* staging = (uint16_t*)residual;
-          for (int t = tq; t < T; ++t)
+          for (int t = tq; t < T; ++t) {
             memcpy(staging + (sl * bt + (size_t)((t0 + t) % bt)) * d, (const uint16_t*)X + xbase + (size_t)t * d,
                    sizeof(uint16_t) * d);
+            for (int c = 0; c < d; ++c)
+              if (!isfinite(load_x(X, 1, xbase + (size_t)t * d + c))) flags |= ORC_FLAG_NONFINITE;
+          }
           float* zt = (float*)malloc(sizeof(float) * (size_t)bt * d);
           for (int t = 0; t < tq; t += bt) {
             for (int u = 0; u < bt; ++u) {

@@ -33,7 +33,7 @@ class GaugeShape(C.Structure):
 
 class CodecStruct(C.Structure):
     _fields_ = [("backend", C.c_int32), ("bits", C.c_int32), ("block_c", C.c_int32), ("key_tokens", C.c_int32),
-                ("val_channels", C.c_int32), ("residual", C.c_int32)]
+                ("val_channels", C.c_int32), ("residual", C.c_int32), ("block_t", C.c_int32)]
 
 
 class KvView(C.Structure):
@@ -104,9 +104,11 @@ class Codec:
     key_tokens: int = 32
     val_channels: int = 64
     residual: int = 128
+    block_t: int = 1
 
     def struct(self) -> CodecStruct:
-        return CodecStruct(self.backend, self.bits, self.block_c, self.key_tokens, self.val_channels, self.residual)
+        return CodecStruct(self.backend, self.bits, self.block_c, self.key_tokens, self.val_channels, self.residual,
+                           self.block_t)
 
 
 def shape(L: int, H: int, d: int, g: int) -> GaugeShape:

@@ -94,6 +94,45 @@ __device__ int store_rows_blocks(const float* zs, int ntok, int d, int dp, int n
   return flags;
 }
 
+// Block-uniform token-channel tiles: tile rows [u*bt, u*bt + bt) form tile (pos0 / bt) + u; one
+// (tile, channel block) per thread takes the range of its bt x n values and packs every token's
+// n codes into that token's row.
+__device__ int store_tiles(const float* zs, int ntile, int bt, int d, int dp, int n, int bits, const CacheDev& k,
+                           size_t slc, int pos0) {
+  int flags = 0;
+  const int nb = d / n, row_bytes = d * bits / 8, blk_bytes = n * bits / 8;
+  for (int w = threadIdx.x; w < ntile * nb; w += blockDim.x) {
+    const int u = w / nb, kb = w - u * nb;
+    const float* zt = zs + (u * bt) * dp + kb * n;
+    float mn = zt[0], mx = zt[0];
+    for (int v = 0; v < bt; ++v)
+      for (int e = 0; e < n; ++e) {
+        mn = fminf(mn, zt[v * dp + e]);
+        mx = fmaxf(mx, zt[v * dp + e]);
+      }
+    const Side sd = make_side(mn, mx, bits);
+    const float qmax = (float)((1 << bits) - 1);
+    for (int v = 0; v < bt; ++v) {
+      const size_t row = slc * k.T_cap + pos0 + u * bt + v;
+      uint32_t* dst = (uint32_t*)(k.codes + row * row_bytes + size_t(kb) * blk_bytes);
+      uint64_t acc = 0;
+      int nbit = 0, wi = 0;
+      for (int e = 0; e < n; ++e) {
+        acc |= (uint64_t)quantize(zt[v * dp + e], sd.mn, sd.inv, qmax) << nbit;
+        nbit += bits;
+        if (nbit >= 32) {
+          dst[wi++] = (uint32_t)acc;
+          acc >>= 32;
+          nbit -= 32;
+        }
+      }
+    }
+    k.side[(slc * (k.T_cap / bt) + (pos0 / bt + u)) * nb + kb] = sd.word;
+    flags |= sd.flags;
+  }
+  return flags;
+}
+
 // KIVI key groups: tile rows [u*kg, u*kg + kg) form token group grp0 + u; one channel per
 // thread.
 __device__ int store_key_groups(const float* zs, int ngrp, int kg, int d, int dp, int bits, const CacheDev& k,
@@ -144,6 +183,18 @@ __global__ __launch_bounds__(kThreads) void enc_generic(int s, ViewDev X, int l0
     }
     return;
   }
+  // block-uniform tiles: rows of the unfinished tile (view rows >= tq) wait raw in the
+  // staging window (slot = cache position mod bt; t0 is a multiple of bt)
+  const bool tiles = c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt > 1;
+  const int nq = tiles ? max(0, min(ntok, tq - tile0)) : ntok;
+  if (tiles) {
+    for (int idx = nq * d + threadIdx.x; idx < ntok * d; idx += blockDim.x) {
+      const int t = idx / d, ch = idx - t * d;
+      const int tok = tile0 + t;
+      k.ring[(slc * c.bt + (t0 + tok) % c.bt) * d + ch] = ((const uint16_t*)X.ptr)[xbase + size_t(tok) * X.st + ch];
+    }
+    if (nq == 0) return;
+  }
 
   int flags = 0;
   for (int idx = threadIdx.x; idx < TT * d; idx += blockDim.x) {
@@ -161,6 +212,8 @@ __global__ __launch_bounds__(kThreads) void enc_generic(int s, ViewDev X, int l0
 
   if (c.backend == CG_BACKEND_PASSTHROUGH) {
     store_rows_pass(zs, ntok, d, dp, k, slc, t0 + tile0);
+  } else if (tiles) {
+    flags |= store_tiles(zs, nq / c.bt, c.bt, d, dp, c.n, c.bits, k, slc, t0 + tile0);
   } else if (c.backend == CG_BACKEND_BLOCK_UNIFORM) {
     flags |= store_rows_blocks(zs, ntok, d, dp, c.n, c.bits, k, slc, t0 + tile0);
   } else if (s == 1) {
@@ -189,22 +242,24 @@ __global__ __launch_bounds__(kThreads) void dec_generic(int s, CacheDev k, int l
   const size_t ybase = size_t(lv) * Y.sl + size_t(b) * Y.sb + size_t(h) * Y.sh;
 
   // Positions the cache holds bound the rows written: pos[b] + 1 in a rolling step, `len` for
-  // a KIVI cache, otherwise every requested position (the host checked the capacity).
+  // a KIVI or tile cache, otherwise every requested position (the host checked the capacity).
   const bool kivi = c.backend == CG_BACKEND_KIVI;
+  const bool tiles = c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt > 1;
   int held = INT_MAX;
   if (pos) {
     const int p = pos[b];
     if (p < 0 || p >= k.T_cap) return;  // flagged by the append kernel
     held = p + 1;
-  } else if (kivi) {
+  } else if (kivi || tiles) {
     held = len;
   }
   const int p0 = t0 + tile0;  // cache position of tile row 0
   if (held != INT_MAX) ntok = min(ntok, held - p0);
   if (ntok <= 0) return;
-  // KIVI quantises the first T_q positions and keeps the rest in the window; the other
-  // backends quantise every position.
-  const int tq = kivi ? (held < c.win ? 0 : ((held - c.win) / c.kg) * c.kg) : INT_MAX;
+  // KIVI quantises the first T_q positions and keeps the rest in the window, tiles the whole
+  // tiles and keep the unfinished one staged; the other backends quantise every position.
+  const int tq = kivi ? (held < c.win ? 0 : ((held - c.win) / c.kg) * c.kg)
+                      : (tiles ? (held / c.bt) * c.bt : INT_MAX);
   const int nq = max(0, min(ntok, tq - p0));  // quantised rows of this tile
 
   // 1. dequantise the quantised rows into zs
@@ -221,7 +276,7 @@ __global__ __launch_bounds__(kThreads) void dec_generic(int s, CacheDev k, int l
       const size_t row = slc * k.T_cap + p;
       const uint32_t* stream = (const uint32_t*)(k.codes + row * (d * bits / 8) + size_t(kb) * (n * bits / 8));
       const uint32_t q = extract_code(stream, ch - kb * n, bits);
-      const uint32_t sw = k.side[row * nb + kb];
+      const uint32_t sw = k.side[(tiles ? slc * (k.T_cap / c.bt) + p / c.bt : row) * nb + kb];
       zv = dequantize(q, f16_bits_to_f32(sw & 0xffffu), f16_bits_to_f32(sw >> 16));
     } else {
       const int kg = c.kg;
@@ -237,8 +292,8 @@ __global__ __launch_bounds__(kThreads) void dec_generic(int s, CacheDev k, int l
   // 2. inverse gauge
   inverse_tile(zs, xs, nq, d, dp, G, l, s, h);
   __syncthreads();
-  // 3. write rows: inverse-gauged rows, then window rows copied raw
-  const int ringsz = c.win + c.kg;
+  // 3. write rows: inverse-gauged rows, then window / staged rows copied raw
+  const int ringsz = tiles ? c.bt : c.win + c.kg;
   for (int idx = threadIdx.x; idx < ntok * d; idx += blockDim.x) {
     const int t = idx / d, ch = idx - t * d;
     const size_t off = ybase + size_t(tile0 + t) * Y.st + ch;
@@ -246,7 +301,7 @@ __global__ __launch_bounds__(kThreads) void dec_generic(int s, CacheDev k, int l
       const float v = xs[t * dp + ch];
       if (Y.bf16) ((uint16_t*)Y.ptr)[off] = (uint16_t)f32_to_bf16_rne(v);
       else ((float*)Y.ptr)[off] = v;
-    } else if (kivi) {
+    } else if (kivi || tiles) {
       const uint16_t raw = k.ring[(slc * ringsz + (p0 + t) % ringsz) * d + ch];
       if (Y.bf16) ((uint16_t*)Y.ptr)[off] = raw;
       else ((float*)Y.ptr)[off] = bf16_to_f32(raw);
@@ -293,6 +348,28 @@ __global__ __launch_bounds__(kThreads) void append_generic(int s, ViewDev Xn, in
     __syncthreads();
     if (s == 0) flags |= store_key_groups(zs, 1, c.kg, d, dp, c.bits, k, slc, tb / c.kg);
     else flags |= store_rows_blocks(zs, c.kg, d, dp, c.kvc, c.bits, k, slc, tb);
+  } else if (c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt > 1) {
+    // stage the token; its tile is quantised once the tile's last token is there
+    const uint16_t* src = (const uint16_t*)Xn.ptr + xbase;
+    for (int ch = threadIdx.x; ch < d; ch += blockDim.x) {
+      const uint16_t v = src[ch];
+      if (!isfinite(bf16_to_f32(v))) flags |= CG_FLAG_NONFINITE;
+      k.ring[(slc * c.bt + p % c.bt) * d + ch] = v;
+    }
+    if ((p + 1) % c.bt == 0) {
+      __syncthreads();
+      const int tb = p + 1 - c.bt;
+      float* xs = sm;
+      float* zs = sm + c.bt * dp;
+      for (int idx = threadIdx.x; idx < c.bt * d; idx += blockDim.x) {
+        const int t = idx / d, ch = idx - t * d;
+        xs[t * dp + ch] = bf16_to_f32(k.ring[(slc * c.bt + (tb + t) % c.bt) * d + ch]);
+      }
+      __syncthreads();
+      gauge_tile(xs, zs, c.bt, d, dp, G, l, s, h);
+      __syncthreads();
+      flags |= store_tiles(zs, 1, c.bt, d, dp, c.n, c.bits, k, slc, tb);
+    }
   } else {
     float* xs = sm;
     float* zs = sm + dp;
@@ -347,7 +424,7 @@ hipError_t launch_decode_generic(int s, const CacheDev& k, int l0, const GaugeDe
 
 hipError_t launch_append(int s, const ViewDev& Xn, int l0, const int* pos, const GaugeDev& G, const CodecDev& c,
                          const CacheDev& k, int* err, hipStream_t st) {
-  const int rows = c.backend == CG_BACKEND_KIVI ? c.kg : 1;
+  const int rows = c.backend == CG_BACKEND_KIVI ? c.kg : c.bt;
   const size_t smem = size_t(2) * rows * (Xn.d + 1) * sizeof(float);
   hipError_t e = set_smem((const void*)append_generic, smem);
   if (e != hipSuccess) return e;

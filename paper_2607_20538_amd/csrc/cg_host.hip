@@ -241,6 +241,7 @@ int32_t check_codec(const cg_codec* c, int d) {
     case CG_BACKEND_BLOCK_UNIFORM:
       if (!bits_ok(c->bits) || c->block_c <= 0) return CG_ERR_UNSUPPORTED;
       if (d % c->block_c || (c->block_c * c->bits) % 32 || c->block_c > 256) return CG_ERR_UNSUPPORTED;
+      if (c->block_t < 1 || c->block_t > 32 || (c->block_t & (c->block_t - 1))) return CG_ERR_UNSUPPORTED;
       return CG_OK;
     case CG_BACKEND_KIVI:
       if (!bits_ok(c->bits)) return CG_ERR_UNSUPPORTED;
@@ -274,6 +275,10 @@ int32_t check_cache(const cg_cache* k, const cg_codec* c, const cg_gauge_shape& 
     if (!k->residual || !aligned16(k->residual)) return CG_ERR_ARG;
     if (k->T_cap % c->key_tokens) return CG_ERR_SHAPE;
   }
+  if (c->backend == CG_BACKEND_BLOCK_UNIFORM && c->block_t > 1) {
+    if (!k->residual || !aligned16(k->residual)) return CG_ERR_ARG;
+    if (k->T_cap % c->block_t) return CG_ERR_SHAPE;
+  }
   return CG_OK;
 }
 
@@ -301,6 +306,7 @@ CodecDev codec_dev(const cg_codec* c) {
   d.kg = c->key_tokens;
   d.kvc = c->val_channels;
   d.win = c->residual;
+  d.bt = c->backend == CG_BACKEND_BLOCK_UNIFORM ? c->block_t : 1;
   return d;
 }
 
@@ -473,10 +479,14 @@ int32_t cache_bytes(const cg_codec* codec, int32_t s, int32_t L, int32_t B, int3
   const int b = codec->bits;
   switch (codec->backend) {
     case CG_BACKEND_PASSTHROUGH: c = slices * T_cap * d * 4; break;
-    case CG_BACKEND_BLOCK_UNIFORM:
+    case CG_BACKEND_BLOCK_UNIFORM: {
+      const int bt = codec->block_t;
+      if (T_cap % bt) return CG_ERR_SHAPE;
       c = slices * T_cap * (size_t(d) * b / 8);
-      sd = slices * T_cap * (d / codec->block_c) * 4;
+      sd = slices * (T_cap / bt) * (d / codec->block_c) * 4;
+      r = bt > 1 ? slices * size_t(bt) * d * 2 : 0;
       break;
+    }
     case CG_BACKEND_KIVI: {
       if (T_cap % codec->key_tokens) return CG_ERR_SHAPE;
       const int kg = codec->key_tokens;
@@ -512,6 +522,9 @@ int32_t kv_encode(int32_t s, const cg_kv_view* X, const void* G_dev, cg_gauge_sh
   if (codec->backend == CG_BACKEND_KIVI) {
     if (t0 != 0 || X->dtype != CG_DTYPE_BF16) return CG_ERR_UNSUPPORTED;
     tq = kivi_tq(X->T, codec);
+  } else if (codec->backend == CG_BACKEND_BLOCK_UNIFORM && codec->block_t > 1) {
+    if (t0 % codec->block_t || X->dtype != CG_DTYPE_BF16) return CG_ERR_UNSUPPORTED;
+    tq = (X->T / codec->block_t) * codec->block_t;
   }
   if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
   hipError_t e = launch_encode(s, view_dev(X), 0, gauge_dev(G_dev, shp), codec_dev(codec), cache_dev(out), t0, tq,
@@ -530,8 +543,8 @@ int32_t kv_decode(int32_t s, const cg_cache* in, const void* G_dev, cg_gauge_sha
   if ((rc = check_cache(in, codec, shp, Xhat->B)) != CG_OK) return rc;
   if (t0 < 0) return CG_ERR_ARG;
   if (int64_t(t0) + Xhat->T > in->T_cap) return CG_ERR_CAPACITY;
-  if (codec->backend == CG_BACKEND_KIVI && (in->len < 0 || in->len > in->T_cap || int64_t(t0) + Xhat->T > in->len))
-    return CG_ERR_CAPACITY;
+  const bool held = codec->backend == CG_BACKEND_KIVI || (codec->backend == CG_BACKEND_BLOCK_UNIFORM && codec->block_t > 1);
+  if (held && (in->len < 0 || in->len > in->T_cap || int64_t(t0) + Xhat->T > in->len)) return CG_ERR_CAPACITY;
   if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
   hipError_t e = launch_decode(s, cache_dev(in), 0, gauge_dev(G_dev, shp), codec_dev(codec), t0, in->len, nullptr,
                                view_dev(Xhat), err_flag, static_cast<hipStream_t>(stream));
@@ -552,8 +565,8 @@ int32_t kv_append_step(int32_t l0, int32_t l1, const cg_kv_view* k_new, const cg
   if ((rc = check_view(k_new, shp, nl)) != CG_OK) return rc;
   if ((rc = check_view(v_new, shp, nl)) != CG_OK) return rc;
   if (k_new->T != 1 || v_new->T != 1 || v_new->B != k_new->B) return CG_ERR_SHAPE;
-  if (codec->backend == CG_BACKEND_KIVI && (k_new->dtype != CG_DTYPE_BF16 || v_new->dtype != CG_DTYPE_BF16))
-    return CG_ERR_UNSUPPORTED;
+  const bool staged = codec->backend == CG_BACKEND_KIVI || (codec->backend == CG_BACKEND_BLOCK_UNIFORM && codec->block_t > 1);
+  if (staged && (k_new->dtype != CG_DTYPE_BF16 || v_new->dtype != CG_DTYPE_BF16)) return CG_ERR_UNSUPPORTED;
   const int B = k_new->B;
   if ((rc = check_cache(kc, codec, shp, B)) != CG_OK) return rc;
   if ((rc = check_cache(vc, codec, shp, B)) != CG_OK) return rc;

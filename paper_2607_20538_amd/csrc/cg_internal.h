@@ -66,6 +66,7 @@ struct GaugeDev {
 // Codec parameters as the kernels see them.
 struct CodecDev {
   int backend, bits, n, kg, kvc, win;
+  int bt;  // block-uniform tile tokens (1: one token per block); 1 for the other backends
 };
 
 // A strided KV tensor view [L][B][H][T][d] (element strides, channel stride 1).
@@ -80,7 +81,7 @@ struct ViewDev {
 struct CacheDev {
   uint8_t* codes;
   uint32_t* side;      // one 32-bit word (min | scale << 16) per block
-  uint16_t* ring;      // KIVI window
+  uint16_t* ring;      // KIVI window, or the staging window of block-uniform tiles
   int L, B, H, T_cap, d;
 };
 
@@ -103,7 +104,7 @@ hipError_t launch_selftest(int which, unsigned long long* bad, hipStream_t st);
 
 // Dispatching launchers (hip stream passed through).  All validate nothing: the host entry points do.
 // Encode tokens [0, X.T) of view X into cache positions [t0, t0 + X.T); layer l of the view is
-// cache layer l + l0.  tq: KIVI tokens to quantise (others go to the window).
+// cache layer l + l0.  tq: KIVI / tile tokens to quantise (others go to the window).
 hipError_t launch_encode(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c, const CacheDev& k,
                          int t0, int tq, int* err, hipStream_t st);
 // Decode cache positions [t0, t0 + Y.T) into view Y (layer l of Y is cache layer l + l0).

@@ -1496,7 +1496,7 @@ bool bits_ok(int b) { return b == 2 || b == 3 || b == 4 || b == 6 || b == 8; }
 }  // namespace
 
 bool mfma_encode_supported(const ViewDev& X, const GaugeDev& G, const CodecDev& c) {
-  if (!X.bf16 || X.d != kD || !group_ok(G.g)) return false;
+  if (!X.bf16 || X.d != kD || !group_ok(G.g) || c.bt != 1) return false;
   if (c.backend == CG_BACKEND_PASSTHROUGH) return true;
   if (c.backend == CG_BACKEND_KIVI)
     return bits_ok(c.bits) && c.kg == kTok && (c.kvc == 16 || c.kvc == 32 || c.kvc == 64) && c.win % kTok == 0;
@@ -1504,7 +1504,7 @@ bool mfma_encode_supported(const ViewDev& X, const GaugeDev& G, const CodecDev& 
 }
 
 bool mfma_decode_supported(int s, const ViewDev& Y, const GaugeDev& G, const CodecDev& c) {
-  if (Y.d != kD || !group_ok(G.g) || !bits_ok(c.bits)) return false;
+  if (Y.d != kD || !group_ok(G.g) || !bits_ok(c.bits) || c.bt != 1) return false;
   if (c.backend == CG_BACKEND_KIVI) {
     if (c.win % kTok) return false;
     if (s == 0) return c.kg == kTok && G.g <= 32;  // key groups, gauge groups within one K-step pair

@@ -46,7 +46,7 @@ def out_host(t: torch.Tensor) -> np.ndarray:
 
 
 def to_cg(oc: O.Codec) -> cg.Codec:
-    return cg.Codec(oc.backend, oc.bits, oc.block_c, oc.key_tokens, oc.val_channels, oc.residual)
+    return cg.Codec(oc.backend, oc.bits, oc.block_c, oc.key_tokens, oc.val_channels, oc.residual, oc.block_t)
 
 
 def cache_to_host(dev: cg.Cache, oc: O.Codec, s: int) -> dict:
@@ -90,6 +90,8 @@ def token_codes(cache: dict, oc: O.Codec, s: int, d: int) -> tuple[np.ndarray, n
     n = oc.block_c if oc.backend == O.BLOCK_UNIFORM else oc.val_channels
     q = unpack_rows(cache["codes"], d, b)
     side = np.repeat(cache["side"], n, axis=-2)
+    if oc.backend == O.BLOCK_UNIFORM and oc.block_t > 1:               # one side row per tile
+        side = np.repeat(side, oc.block_t, axis=3)
     return q, side[..., 0], side[..., 1]
 
 

@@ -67,11 +67,12 @@ def test_gauge_make_rejects_bad_shapes():
     assert cg.gauge_device_bytes(cg.shape(1, 1, 128, 48)) == 0
 
 
-@pytest.mark.parametrize("backend,bits", [(O.BLOCK_UNIFORM, 4), (O.BLOCK_UNIFORM, 3), (O.KIVI, 3), (O.KIVI, 6),
-                                          (O.PASSTHROUGH, 4)])
-def test_cache_bytes_follow_the_layout(backend, bits):
-    oc = O.Codec(backend=backend, bits=bits, block_c=32 if bits != 3 else 64)
-    c = cg.Codec(backend, bits, oc.block_c, oc.key_tokens, oc.val_channels, oc.residual)
+@pytest.mark.parametrize("backend,bits,bt", [(O.BLOCK_UNIFORM, 4, 1), (O.BLOCK_UNIFORM, 3, 1), (O.KIVI, 3, 1),
+                                             (O.KIVI, 6, 1), (O.PASSTHROUGH, 4, 1), (O.BLOCK_UNIFORM, 4, 16),
+                                             (O.BLOCK_UNIFORM, 6, 32)])
+def test_cache_bytes_follow_the_layout(backend, bits, bt):
+    oc = O.Codec(backend=backend, bits=bits, block_c=32 if bits != 3 else 64, block_t=bt)
+    c = cg.Codec(backend, bits, oc.block_c, oc.key_tokens, oc.val_channels, oc.residual, bt)
     for s in (0, 1):
         lay = O.cache_layout(oc, s, 2, 3, 4, 256, 128)
         n = cg.cache_bytes(c, s, 2, 3, 4, 256, 128)
@@ -143,6 +144,20 @@ def test_encode_decode_reject_ranges_and_modes():
     # KIVI decode beyond the tokens the cache holds
     assert _decode(_fake_view(T=16), _fake_cache(T_cap=64, len_=8), kivi) == cg.CG_ERR_CAPACITY
     assert _decode(_fake_view(T=16), _fake_cache(len_=16), BU, t0=1) == cg.CG_ERR_CAPACITY
+    # block-uniform tiles: Tb a power of two up to 32, t0 on a tile boundary, bf16 input, a
+    # staging buffer, T_cap a multiple of Tb, decode within the tokens held
+    tile = cg.Codec(cg.BLOCK_UNIFORM, 4, 32, block_t=16)
+    kt = _fake_cache(T_cap=64)
+    assert _encode(_fake_view(T=16), kt, cg.Codec(cg.BLOCK_UNIFORM, 4, 32, block_t=12)) == cg.CG_ERR_UNSUPPORTED
+    assert _encode(_fake_view(T=16), kt, cg.Codec(cg.BLOCK_UNIFORM, 4, 32, block_t=64)) == cg.CG_ERR_UNSUPPORTED
+    assert _encode(_fake_view(T=16), kt, tile, t0=8) == cg.CG_ERR_UNSUPPORTED
+    assert _encode(_fake_view(T=16, dtype=cg.DTYPE_F32), kt, tile) == cg.CG_ERR_UNSUPPORTED
+    assert _encode(_fake_view(T=16), _fake_cache(T_cap=64, residual=0), tile) == cg.CG_ERR_ARG
+    assert _encode(_fake_view(T=16), _fake_cache(T_cap=40), tile) == cg.CG_ERR_SHAPE
+    with pytest.raises(cg.CodecError) as e:
+        cg.cache_bytes(tile, 0, 1, 1, 2, 40, 64)
+    assert e.value.status == cg.CG_ERR_SHAPE
+    assert _decode(_fake_view(T=16), _fake_cache(T_cap=64, len_=8), tile) == cg.CG_ERR_CAPACITY
 
 
 def test_append_step_rejects_invalid_arguments():

@@ -250,12 +250,73 @@ def test_kivi_key_decoder(g, bits):
 
 
 # ------------------------------------------------------------------------------------------
+# block-uniform token-channel tiles (one range per Tb x n block, unfinished tiles staged)
+# ------------------------------------------------------------------------------------------
+TILE_CASES = [(4, 128, 16), (3, 64, 16), (6, 32, 16), (2, 128, 32), (8, 64, 16)]
+
+
+@pytest.mark.parametrize("bits,n,bt", TILE_CASES)
+def test_tile_quantise_and_dequantise_are_bit_exact(bits, n, bt, kernels):
+    """Identity gauge: the tiles' codes, side words and staged rows equal the oracle's bit for
+    bit, and so does the decode of the oracle's cache (staged rows copied raw)."""
+    T, T_cap = 300, 320
+    w = _workload(T=T)
+    G, Gd, shp = _gauge(O.GAUGE_IDENTITY, 1, 2, 128, 32)
+    oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=bits, block_c=n, block_t=bt)
+    tq = O.tile_tq(T, oc)
+    for s in (0, 1):
+        X = synth.kv_tensor(w, s)
+        orc, flags = O.kv_encode(oc, s, X, G, T_cap=T_cap)
+        assert flags == 0
+        got = cache_to_host(_encode_gpu(X, s, Gd, shp, oc, T_cap), oc, s)
+        np.testing.assert_array_equal(got["codes"][:, :, :, :tq], orc["codes"][:, :, :, :tq])
+        np.testing.assert_array_equal(got["side"][:, :, :, :tq // bt], orc["side"][:, :, :, :tq // bt])
+        for t in range(tq, T):
+            np.testing.assert_array_equal(got["residual"][:, :, :, t % bt], orc["residual"][:, :, :, t % bt])
+        ddev = cache_to_dev(orc, oc, s, 1, 2, 2, T_cap, 128, len_=T)
+        for bf in (False, True):
+            ref = O.kv_decode(oc, s, G, orc, 0, T, lens=[T, T], out_bf16=bf)
+            out = _decode_gpu(ddev, s, Gd, shp, oc, 0, T, torch.bfloat16 if bf else torch.float32)
+            np.testing.assert_array_equal(out, ref)
+
+
+@pytest.mark.parametrize("g", [8, 32, 128])
+@pytest.mark.parametrize("bits,n,bt", TILE_CASES[:3])
+def test_tile_fused_encoder_and_decoder(g, bits, n, bt, kernels):
+    T, T_cap = 277, 288
+    w = _workload(T=T, L=2, B=1, H=2)
+    G, Gd, shp = _gauge(O.GAUGE_HAAR, 2, 2, 128, g)
+    oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=bits, block_c=n, block_t=bt)
+    tq = O.tile_tq(T, oc)
+    for s in (0, 1):
+        X = synth.kv_tensor(w, s)
+        orc, _ = O.kv_encode(oc, s, X, G, T_cap=T_cap)
+        zo, _ = O.kv_encode(O.Codec(backend=O.PASSTHROUGH), s, X, G, T_cap=T_cap)
+        err = torch.zeros(1, dtype=torch.int32, device="cuda")
+        dev = _encode_gpu(X, s, Gd, shp, oc, T_cap, err=err)
+        assert int(err.item()) == 0
+        check_fused_codes(cache_to_host(dev, oc, s), orc, zo["codes"], oc, s, 128, tq)
+        ddev = cache_to_dev(orc, oc, s, 2, 1, 2, T_cap, 128, len_=T)
+        ref = O.kv_decode(oc, s, G, orc, 0, T, lens=[T], out_bf16=False)
+        out = _decode_gpu(ddev, s, Gd, shp, oc, 0, T, torch.float32)
+        assert group_rel_err(ref[:, :, :, :tq], out[:, :, :, :tq], g) <= GAUGE_TOL
+        np.testing.assert_array_equal(out[:, :, :, tq:], ref[:, :, :, tq:])
+        outb = _decode_gpu(ddev, s, Gd, shp, oc, 0, T)
+        check_bf16_within_ulp(ref[:, :, :, :tq], outb[:, :, :, :tq], g)
+        np.testing.assert_array_equal(outb[:, :, :, tq:], X[:, :, :, tq:])
+        # sub-ranges that start inside a tile agree with the full decode
+        for t0, nn in ((5, 100), (tq - 7, 9), (17, 1)):
+            np.testing.assert_array_equal(_decode_gpu(ddev, s, Gd, shp, oc, t0, nn), outb[:, :, :, t0:t0 + nn])
+
+
+# ------------------------------------------------------------------------------------------
 # rolling step
 # ------------------------------------------------------------------------------------------
-@pytest.mark.parametrize("backend,kind", [(O.BLOCK_UNIFORM, O.GAUGE_IDENTITY), (O.KIVI, O.GAUGE_IDENTITY),
-                                          (O.PASSTHROUGH, O.GAUGE_IDENTITY), (O.BLOCK_UNIFORM, O.GAUGE_HAAR),
-                                          (O.KIVI, O.GAUGE_HAAR)])
-def test_append_step_matches_oracle(backend, kind, kernels):
+@pytest.mark.parametrize("backend,kind,bt", [(O.BLOCK_UNIFORM, O.GAUGE_IDENTITY, 1), (O.KIVI, O.GAUGE_IDENTITY, 1),
+                                             (O.PASSTHROUGH, O.GAUGE_IDENTITY, 1), (O.BLOCK_UNIFORM, O.GAUGE_HAAR, 1),
+                                             (O.KIVI, O.GAUGE_HAAR, 1), (O.BLOCK_UNIFORM, O.GAUGE_IDENTITY, 16),
+                                             (O.BLOCK_UNIFORM, O.GAUGE_HAAR, 16)])
+def test_append_step_matches_oracle(backend, kind, bt, kernels):
     """Rolling history (section 4.4): T0 tokens encoded by the oracle and uploaded, then
     steps appended on both sides with a different position per batch row; the identity gauge
     makes every stage exact, so caches and decoded histories must agree bit for bit; with a
@@ -264,7 +325,7 @@ def test_append_step_matches_oracle(backend, kind, kernels):
     T0, steps, T_cap = 150, 40, 224
     w = _workload(T=T_cap, L=L, B=B, H=H)
     G, Gd, shp = _gauge(kind, L, H, d, g)
-    oc = O.Codec(backend=backend, bits=4, block_c=64, key_tokens=32, val_channels=64, residual=128)
+    oc = O.Codec(backend=backend, bits=4, block_c=64, key_tokens=32, val_channels=64, residual=128, block_t=bt)
     Xk, Xv = synth.kv_tensor(w, 0), synth.kv_tensor(w, 1)
     # row 1 runs 5 positions ahead of row 0 (its slots [T0, T0+5) stay empty on both sides)
     start = np.array([T0, T0 + 5])
@@ -299,7 +360,7 @@ def test_append_step_matches_oracle(backend, kind, kernels):
                 np.testing.assert_array_equal(h[:, b, :, :final[b] + 1], ref_hist[:, b, :, :final[b] + 1])
         else:
             zo, _ = O.kv_encode(O.Codec(backend=O.PASSTHROUGH), s, Xk if s == 0 else Xv, G, T_cap=T_cap)
-            tq = O.kivi_tq(int(final.min()) + 1, oc) if backend == O.KIVI else int(final.min()) + 1
+            tq = O.kivi_tq(int(final.min()) + 1, oc) if backend == O.KIVI else O.tile_tq(int(final.min()) + 1, oc)
             check_fused_codes(got, oc_cache, zo["codes"], oc, s, d, tq)
             # the history the step decoded equals kv_decode of the same GPU cache
             for b in range(B):
