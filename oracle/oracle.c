@@ -559,7 +559,10 @@ static int tile_flush(const orc_layout* o, size_t sl, const float* Gs, int t_beg
   float* zt = (float*)malloc(sizeof(float) * (size_t)bt * d);
   for (int u = 0; u < bt; ++u) {
     const uint16_t* srow = staging + (sl * bt + (size_t)((t_begin + u) % bt)) * d;
-    for (int c = 0; c < d; ++c) x[c] = orc_bf16_to_f32(srow[c]);
+    for (int c = 0; c < d; ++c) {
+      x[c] = orc_bf16_to_f32(srow[c]);
+      if (!isfinite(x[c])) flags |= ORC_FLAG_NONFINITE;
+    }
     orc_gauge_apply(d, o->g, Gs, x, zt + (size_t)u * d);
   }
   int row_bytes = d * o->bits / 8, nb = d / o->n;
@@ -621,15 +624,13 @@ int orc_kv_encode(int backend, int bits, int n, int kg, int kvc, int win, int bt
           continue;
         }
         if (tile) {
-          /* whole tiles quantised (positions t0 + [0, T_q)), the unfinished one staged raw */
+          /* whole tiles quantised (positions t0 + [0, T_q)), the unfinished one staged raw;
+           * as for the KIVI window, staged tokens are checked when their tile is quantised */
           int tq = (T / bt) * bt;
           uint16_t* staging = (uint16_t*)residual;
-          for (int t = tq; t < T; ++t) {
+          for (int t = tq; t < T; ++t)
             memcpy(staging + (sl * bt + (size_t)((t0 + t) % bt)) * d, (const uint16_t*)X + xbase + (size_t)t * d,
                    sizeof(uint16_t) * d);
-            for (int c = 0; c < d; ++c)
-              if (!isfinite(load_x(X, 1, xbase + (size_t)t * d + c))) flags |= ORC_FLAG_NONFINITE;
-          }
           float* zt = (float*)malloc(sizeof(float) * (size_t)bt * d);
           for (int t = 0; t < tq; t += bt) {
             for (int u = 0; u < bt; ++u) {
@@ -764,8 +765,6 @@ int orc_kv_append(int backend, int bits, int n, int kg, int kvc, int win, int bt
         if (tile) {
           uint16_t* staging = (uint16_t*)residual;
           memcpy(staging + (sl * bt + (size_t)(t % bt)) * d, (const uint16_t*)Xnew + xin, sizeof(uint16_t) * d);
-          for (int c = 0; c < d; ++c)
-            if (!isfinite(orc_bf16_to_f32(((const uint16_t*)Xnew)[xin + c]))) flags |= ORC_FLAG_NONFINITE;
           if ((t + 1) % bt == 0) flags |= tile_flush(&o, sl, Gs, t + 1 - bt, (uint8_t*)codes, (uint16_t*)side, staging);
           continue;
         }

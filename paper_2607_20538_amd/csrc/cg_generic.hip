@@ -202,7 +202,7 @@ __global__ __launch_bounds__(kThreads) void enc_generic(int s, ViewDev X, int l0
     float v = 0.0f;
     if (t < ntok) {
       v = load_x(X, xbase + size_t(tile0 + t) * X.st + ch);
-      if (!isfinite(v)) flags |= CG_FLAG_NONFINITE;
+      if (t < nq && !isfinite(v)) flags |= CG_FLAG_NONFINITE;  // staged rows: checked when quantised
     }
     xs[t * dp + ch] = v;
   }
@@ -351,11 +351,7 @@ __global__ __launch_bounds__(kThreads) void append_generic(int s, ViewDev Xn, in
   } else if (c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt > 1) {
     // stage the token; its tile is quantised once the tile's last token is there
     const uint16_t* src = (const uint16_t*)Xn.ptr + xbase;
-    for (int ch = threadIdx.x; ch < d; ch += blockDim.x) {
-      const uint16_t v = src[ch];
-      if (!isfinite(bf16_to_f32(v))) flags |= CG_FLAG_NONFINITE;
-      k.ring[(slc * c.bt + p % c.bt) * d + ch] = v;
-    }
+    for (int ch = threadIdx.x; ch < d; ch += blockDim.x) k.ring[(slc * c.bt + p % c.bt) * d + ch] = src[ch];
     if ((p + 1) % c.bt == 0) {
       __syncthreads();
       const int tb = p + 1 - c.bt;
@@ -363,7 +359,9 @@ __global__ __launch_bounds__(kThreads) void append_generic(int s, ViewDev Xn, in
       float* zs = sm + c.bt * dp;
       for (int idx = threadIdx.x; idx < c.bt * d; idx += blockDim.x) {
         const int t = idx / d, ch = idx - t * d;
-        xs[t * dp + ch] = bf16_to_f32(k.ring[(slc * c.bt + (tb + t) % c.bt) * d + ch]);
+        const float v = bf16_to_f32(k.ring[(slc * c.bt + (tb + t) % c.bt) * d + ch]);
+        if (!isfinite(v)) flags |= CG_FLAG_NONFINITE;
+        xs[t * dp + ch] = v;
       }
       __syncthreads();
       gauge_tile(xs, zs, c.bt, d, dp, G, l, s, h);

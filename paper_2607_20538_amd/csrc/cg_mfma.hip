@@ -162,6 +162,24 @@ __device__ __forceinline__ f32x16_t mfma_chain(const bf16x8_t (&A)[NP][KS], cons
   return acc;
 }
 
+// min / max over the 16 lanes of a DPP row (quad swaps, then rotations by 4 and 8 lanes)
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row16_min(float v) {
+  v = fminf(v, dpp_mov<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = fminf(v, dpp_mov<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = fminf(v, dpp_mov<0x124>(v));  // row_ror:4
+  return fminf(v, dpp_mov<0x128>(v));  // row_ror:8
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_mov<0xB1>(v));
+  v = fmaxf(v, dpp_mov<0x4E>(v));
+  v = fmaxf(v, dpp_mov<0x124>(v));
+  return fmaxf(v, dpp_mov<0x128>(v));
+}
+
 // encoder modes
 constexpr int kModeBU = 0;     // block-uniform (or KIVI values: n = value channel group)
 constexpr int kModePass = 1;   // error-free backend: binary32 z
@@ -178,11 +196,14 @@ constexpr int kModeKeys = 2;   // KIVI keys: one block per channel over a 32-tok
 // kStages - 1 tiles are in flight between global memory and LDS.  The codes of a tile are one
 // contiguous run of 32 RB bytes in the cache and its side words one run of 32 NBK words, so
 // the staged copy leaves with whole-line stores instead of 32 scattered row pieces.
-template <int NP, int KS, int BITS, int NB, int MODE>
+template <int NP, int KS, int BITS, int NB, int MODE, int TB = 1>
 __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a) {
   constexpr bool PASS = MODE == kModePass, KEYS = MODE == kModeKeys;
+  // token-channel tiles: one range per TB tokens x NB channels (NB spans whole waves)
+  constexpr bool TILE = TB > 1;
+  static_assert(!TILE || (TB == 16 && MODE == kModeBU && (NB == 64 || NB == 128)), "tile shape");
   constexpr int RB = kD * BITS / 8;   // packed code bytes per token row
-  constexpr int NBK = kD / NB;        // side words per token row
+  constexpr int NBK = kD / NB;        // side words per token row (per tile row of tiles)
   __shared__ __attribute__((aligned(16))) uint8_t xtile[kStages][kTok * kRowBytes];
   __shared__ float2 red[2][4][kTok];  // per-wave (min, max) of each token, for 64-channel blocks
   // a tile's packed rows and side words, staged so that they leave as contiguous stores
@@ -207,18 +228,15 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
   const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
   const int64_t tstride = 2 * a.st;  // bytes between tokens
 
-  // KIVI full-precision window: rows of tiles [max(tb, te), te_all) copied raw into the ring
-  // (slot = position mod ring_slots; 32-token tiles never wrap since ring_slots is a multiple
-  // of 32)
+  // KIVI full-precision window / staged tokens of an unfinished tile: this workgroup's rows
+  // at or past tq copied raw into the ring (slot = cache position mod ring_slots)
   auto ring_copy = [&]() {
-    for (int tile = max(tb, te); tile < te_all; ++tile) {
-      const int nlive = min(kTok, a.T - tile * kTok);
-      uint16_t* dst = a.ring + (cslice * a.ring_slots + (tile * kTok) % a.ring_slots) * kD;
-      for (int gi = int(threadIdx.x); gi < nlive * (kRowBytes / 16); gi += kThreads) {
-        const int row = gi / (kRowBytes / 16), j = gi % (kRowBytes / 16);
-        *(u32x4_t*)((char*)dst + row * kRowBytes + 16 * j) =
-            *(const u32x4_t*)(xs + int64_t(tile * kTok + row) * tstride + 16 * j);
-      }
+    constexpr int GR = kRowBytes / 16;  // granules per row
+    const int r0 = max(a.tq, tb * kTok), r1 = min(a.T, te_all * kTok);
+    for (int gi = r0 * GR + int(threadIdx.x); gi < r1 * GR; gi += kThreads) {
+      const int row = gi / GR, j = gi % GR;
+      uint16_t* dst = a.ring + (cslice * a.ring_slots + (a.t0 + row) % a.ring_slots) * kD;
+      *(u32x4_t*)((char*)dst + 16 * j) = *(const u32x4_t*)(xs + int64_t(row) * tstride + 16 * j);
     }
   };
   if (tb >= te) {
@@ -299,12 +317,13 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
   auto flush = [&](int tile, auto parity) {
     constexpr int P = decltype(parity)::value;
     const int tid = int(threadIdx.x);
-    const int nlive = a.T - tile * kTok;
+    const int nlive = min(a.T, a.tq) - tile * kTok;  // quantised rows of the tile
     const size_t crow0 = cslice * a.T_cap + size_t(a.t0 + tile * kTok);
     if (tid < kTok * BITS && tid / BITS < nlive)
       *(u32x4_t*)(a.codes + crow0 * RB + 16 * tid) = *(const u32x4_t*)(cstage[P] + 16 * tid);
+    // side words: one per (row, block), or per (tile of TB rows, block); t0 % TB == 0
     const int si = kThreads - 1 - tid;
-    if (si < kTok * NBK && si / NBK < nlive) a.side[crow0 * NBK + si] = sstage[P][si];
+    if (si < (kTok / TB) * NBK && (si / NBK) * TB < nlive) a.side[crow0 / TB * NBK + si] = sstage[P][si];
   };
   // one pipeline step; P = parity of (tile - tb) selects the accumulator, LDS buffer, register
   // stage and exchange slot at compile time
@@ -314,7 +333,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
 #pragma unroll
     for (int e = 0; e < 16; ++e) z[e] = acc[P][e];
     const int tok = tile * kTok + n;
-    const bool live = tok < a.T;
+    const bool live = tok < (TILE ? a.tq : a.T);
     const size_t crow = cslice * a.T_cap + size_t(a.t0 + tok);
 
     // 1. block-range partials
@@ -327,11 +346,17 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
         mn = fminf(mn, z[e]);
         mx = fmaxf(mx, z[e]);
       }
+      if constexpr (TILE) {  // the 16 tokens of the lane's tile: one DPP row
+        mn = row16_min(mn);
+        mx = row16_max(mx);
+      }
       if constexpr (NB >= 32) {
         mn = fminf(mn, __shfl_xor(mn, 32));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
       }
-      if constexpr (NB == 64) {
+      if constexpr (TILE) {
+        if (hc == 0 && (n & 15) == 0) red[P][w][n >> 4] = make_float2(mn, mx);
+      } else if constexpr (NB == 64) {
         if (hc == 0) red[P][w][n] = make_float2(mn, mx);
       }
     }
@@ -402,7 +427,14 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
       }
       flags |= sd.flags | (bad ? CG_FLAG_NONFINITE : 0);
     } else {
-      if constexpr (NB == 64) {
+      if constexpr (TILE) {  // the other waves of the tile's channel block
+#pragma unroll
+        for (int o = 1; o < NB / 32; ++o) {
+          const float2 v = red[P][w ^ o][n >> 4];
+          mn = fminf(mn, v.x);
+          mx = fmaxf(mx, v.y);
+        }
+      } else if constexpr (NB == 64) {
         const float2 o = red[P][w ^ 1][n];
         mn = fminf(mn, o.x);
         mx = fmaxf(mx, o.y);
@@ -483,7 +515,9 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
         for (int i = 0; i < BITS; ++i) dst[i] = words[i];
       }
       if (live) flags |= sd.flags | (bad ? CG_FLAG_NONFINITE : 0);
-      if constexpr (NB == 16) {
+      if constexpr (TILE) {
+        if (hc == 0 && (n & 15) == 0 && w % (NB / 32) == 0) sstage[P][(n >> 4) * NBK + w / (NB / 32)] = sd.word;
+      } else if constexpr (NB == 16) {
         sstage[P][n * NBK + 2 * w + hc] = sd.word;
       } else if constexpr (NB == 32) {
         if (hc == 0) sstage[P][n * NBK + w] = sd.word;
@@ -926,10 +960,11 @@ constexpr int kDStages = 8;  // decoder LDS ring of code and side tiles (fewer f
 // Every wave issues exactly two loads per tile (codes, side words) and GPR stores per flush
 // (lanes past the written range repeat a live granule), so the number of vector-memory
 // operations younger than a tile's loads is known and waited for exactly.
-template <int NP, int KS, int BITS, int NB, bool OUT_BF16>
+template <int NP, int KS, int BITS, int NB, bool OUT_BF16, int TB = 1>
 __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a) {
   constexpr int RB = kD * BITS / 8;                  // code bytes per token row
-  constexpr int NBK = kD / NB;                       // side words per token row
+  constexpr int NBK = kD / NB;                       // side words per token row (per tile)
+  static_assert(TB == 1 || TB == 16, "token-channel tiles of 16 tokens");
   constexpr int SEG = (16 * KS < NB ? 16 * KS : NB) / 16;  // K-steps per block segment
   constexpr int NSEG = KS / SEG;
   constexpr int RW = SEG * BITS / 4;                 // packed words of a lane's region
@@ -951,7 +986,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
   const int h = slice % a.H, b = (slice / a.H) % a.B, lv = slice / (a.H * a.B);
   const int l = lv + a.l0;
   int Tv = a.T;
-  int held = a.kivi ? a.len : INT_MAX;  // positions the cache holds
+  int held = a.kivi || TB > 1 ? a.len : INT_MAX;  // positions the cache holds
   if (a.pos) {
     const int p = a.pos[b];
     if (p < 0 || p >= a.T_cap) return;  // flagged by the append kernel
@@ -965,8 +1000,9 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
   char* ys = a.x + YB * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
   const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
   const size_t crow0 = cslice * size_t(a.T_cap) + a.t0;
-  // KIVI: the quantised view rows [0, Tq) go through the pipeline, the window rows after it
-  const int Tq = a.kivi ? kivi_quantised_rows(a, held, Tv) : Tv;
+  // KIVI / tiles: the quantised view rows [0, Tq) go through the pipeline, the window or
+  // staged rows after it
+  const int Tq = a.kivi ? kivi_quantised_rows(a, held, Tv) : (TB > 1 ? max(0, min(Tv, held / TB * TB - a.t0)) : Tv);
   const int te = min(te_all, (Tq + kTok - 1) / kTok);
   if (tb >= te) {
     ring_rows<OUT_BF16>(a, cslice, ys, max(Tq, tb * kTok), min(Tv, te_all * kTok));
@@ -1001,9 +1037,17 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
     if (lane < 8 * BITS)
       __builtin_amdgcn_global_load_lds(a.codes + (row0 + min(cgrow, last)) * RB + 16 * cgpart,
                                        (__attribute__((address_space(3))) void*)(ctile[st] + 16 * 8 * BITS * w), 16, 0, 0);
-    if (lane < 8 * NBK)
+    if constexpr (TB > 1) {
+      // the (at most three) tiles the 32 rows touch, into this wave's own slots; tiles past
+      // the quantised rows repeat the last one
+      const size_t blk0 = row0 / TB, blast = (row0 + last) / TB;
+      if (lane < 3 * NBK)
+        __builtin_amdgcn_global_load_lds(a.side + min(blk0 + lane / NBK, blast) * NBK + lane % NBK,
+                                         (__attribute__((address_space(3))) void*)(stile[st] + 3 * NBK * w), 4, 0, 0);
+    } else if (lane < 8 * NBK) {
       __builtin_amdgcn_global_load_lds(a.side + (row0 + min(swrow, last)) * NBK + swk,
                                        (__attribute__((address_space(3))) void*)(stile[st] + 8 * NBK * w), 4, 0, 0);
+    }
   };
   // staged rows of `tile` -> the view; lanes past the written rows repeat the last live row's
   // granules (same data, same address), so every thread issues F stores
@@ -1060,8 +1104,15 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
     if (t + DS - 1 < te) issue(t + DS - 1);
     const int st = (t - tb) % DS;
     uint32_t sw[NBK];
+    if constexpr (TB > 1) {
+      const size_t row0 = crow0 + size_t(t) * kTok;
+      const int bi = int((row0 + n) / TB - row0 / TB);
 #pragma unroll
-    for (int k = 0; k < NBK; ++k) sw[k] = stile[st][n * NBK + k];
+      for (int k = 0; k < NBK; ++k) sw[k] = stile[st][3 * NBK * w + bi * NBK + k];
+    } else {
+#pragma unroll
+      for (int k = 0; k < NBK; ++k) sw[k] = stile[st][n * NBK + k];
+    }
     float y[16];
 #pragma unroll
     for (int sgi = 0; sgi < NSEG; ++sgi) {
@@ -1380,30 +1431,37 @@ void plan(MfmaArgs& m, int nslices, int T, const void* fn) {
 }
 
 template <int KS, int BITS, int NB>
-void* enc_kernel(int mode) {
+void* enc_kernel(int mode, int bt) {
   if (mode == kModePass) return (void*)enc_mfma<kNP, KS, 8, 64, kModePass>;
   if (mode == kModeKeys) return (void*)enc_mfma<enc_planes(BITS), KS, BITS, 32, kModeKeys>;
-  return (void*)enc_mfma<enc_planes(BITS), KS, BITS, NB, kModeBU>;
+  if constexpr (NB >= 64) {
+    if (bt == 16) return (void*)enc_mfma<enc_planes(BITS), KS, BITS, NB, kModeBU, 16>;
+  }
+  if constexpr (NB <= 64) {
+    if (bt == 1) return (void*)enc_mfma<enc_planes(BITS), KS, BITS, NB, kModeBU>;
+  }
+  return nullptr;
 }
 
 template <int KS, int BITS>
-void* enc_by_nb(int nb, int mode) {
+void* enc_by_nb(int nb, int mode, int bt) {
   switch (nb) {
-    case 16: return enc_kernel<KS, BITS, 16>(mode);
-    case 32: return enc_kernel<KS, BITS, 32>(mode);
-    case 64: return enc_kernel<KS, BITS, 64>(mode);
+    case 16: return enc_kernel<KS, BITS, 16>(mode, bt);
+    case 32: return enc_kernel<KS, BITS, 32>(mode, bt);
+    case 64: return enc_kernel<KS, BITS, 64>(mode, bt);
+    case 128: return enc_kernel<KS, BITS, 128>(mode, bt);
   }
   return nullptr;
 }
 
 template <int KS>
-void* enc_by_bits(int bits, int nb, int mode) {
+void* enc_by_bits(int bits, int nb, int mode, int bt) {
   switch (bits) {
-    case 2: return enc_by_nb<KS, 2>(nb, mode);
-    case 3: return enc_by_nb<KS, 3>(nb, mode);
-    case 4: return enc_by_nb<KS, 4>(nb, mode);
-    case 6: return enc_by_nb<KS, 6>(nb, mode);
-    case 8: return enc_by_nb<KS, 8>(nb, mode);
+    case 2: return enc_by_nb<KS, 2>(nb, mode, bt);
+    case 3: return enc_by_nb<KS, 3>(nb, mode, bt);
+    case 4: return enc_by_nb<KS, 4>(nb, mode, bt);
+    case 6: return enc_by_nb<KS, 6>(nb, mode, bt);
+    case 8: return enc_by_nb<KS, 8>(nb, mode, bt);
   }
   return nullptr;
 }
@@ -1440,34 +1498,46 @@ int ksteps(int g) { return g >= 128 ? 8 : (g == 64 ? 4 : 2); }
 
 // dec_fast variants exist where a lane's code region is whole words and a wave's K range
 // holds at most two blocks
+// (token-channel tiles: blocks of 64 or 128 channels inside the gauge group)
 template <int KS, int BITS, int NB>
-void* fast_kernel(bool bf16) {
+void* fast_kernel(bool bf16, int bt) {
   constexpr int SEG = (16 * KS < NB ? 16 * KS : NB) / 16;
   if constexpr (SEG * BITS % 4 == 0 && KS / SEG <= 2) {
-    if (bf16) return (void*)dec_fast<kNP, KS, BITS, NB, true>;
-    return (void*)dec_fast<kNP, KS, BITS, NB, false>;
+    if constexpr (NB >= 64 && 16 * KS >= NB) {
+      if (bt == 16) {
+        if (bf16) return (void*)dec_fast<kNP, KS, BITS, NB, true, 16>;
+        return (void*)dec_fast<kNP, KS, BITS, NB, false, 16>;
+      }
+    }
+    if constexpr (NB <= 64) {
+      if (bt == 1) {
+        if (bf16) return (void*)dec_fast<kNP, KS, BITS, NB, true>;
+        return (void*)dec_fast<kNP, KS, BITS, NB, false>;
+      }
+    }
   }
   return nullptr;
 }
 
 template <int KS, int BITS>
-void* fast_by_nb(int nb, bool bf16) {
+void* fast_by_nb(int nb, bool bf16, int bt) {
   switch (nb) {
-    case 16: return fast_kernel<KS, BITS, 16>(bf16);
-    case 32: return fast_kernel<KS, BITS, 32>(bf16);
-    case 64: return fast_kernel<KS, BITS, 64>(bf16);
+    case 16: return fast_kernel<KS, BITS, 16>(bf16, bt);
+    case 32: return fast_kernel<KS, BITS, 32>(bf16, bt);
+    case 64: return fast_kernel<KS, BITS, 64>(bf16, bt);
+    case 128: return fast_kernel<KS, BITS, 128>(bf16, bt);
   }
   return nullptr;
 }
 
 template <int KS>
-void* fast_by_bits(int bits, int nb, bool bf16) {
+void* fast_by_bits(int bits, int nb, bool bf16, int bt) {
   switch (bits) {
-    case 2: return fast_by_nb<KS, 2>(nb, bf16);
-    case 3: return fast_by_nb<KS, 3>(nb, bf16);
-    case 4: return fast_by_nb<KS, 4>(nb, bf16);
-    case 6: return fast_by_nb<KS, 6>(nb, bf16);
-    case 8: return fast_by_nb<KS, 8>(nb, bf16);
+    case 2: return fast_by_nb<KS, 2>(nb, bf16, bt);
+    case 3: return fast_by_nb<KS, 3>(nb, bf16, bt);
+    case 4: return fast_by_nb<KS, 4>(nb, bf16, bt);
+    case 6: return fast_by_nb<KS, 6>(nb, bf16, bt);
+    case 8: return fast_by_nb<KS, 8>(nb, bf16, bt);
   }
   return nullptr;
 }
@@ -1496,15 +1566,19 @@ bool bits_ok(int b) { return b == 2 || b == 3 || b == 4 || b == 6 || b == 8; }
 }  // namespace
 
 bool mfma_encode_supported(const ViewDev& X, const GaugeDev& G, const CodecDev& c) {
-  if (!X.bf16 || X.d != kD || !group_ok(G.g) || c.bt != 1) return false;
+  if (!X.bf16 || X.d != kD || !group_ok(G.g)) return false;
   if (c.backend == CG_BACKEND_PASSTHROUGH) return true;
   if (c.backend == CG_BACKEND_KIVI)
     return bits_ok(c.bits) && c.kg == kTok && (c.kvc == 16 || c.kvc == 32 || c.kvc == 64) && c.win % kTok == 0;
-  return c.backend == CG_BACKEND_BLOCK_UNIFORM && bits_ok(c.bits) && (c.n == 16 || c.n == 32 || c.n == 64);
+  if (c.backend != CG_BACKEND_BLOCK_UNIFORM || !bits_ok(c.bits)) return false;
+  if (c.bt == 16) return c.n == 64 || c.n == 128;  // token-channel tiles
+  return c.bt == 1 && (c.n == 16 || c.n == 32 || c.n == 64);
 }
 
 bool mfma_decode_supported(int s, const ViewDev& Y, const GaugeDev& G, const CodecDev& c) {
-  if (Y.d != kD || !group_ok(G.g) || !bits_ok(c.bits) || c.bt != 1) return false;
+  if (Y.d != kD || !group_ok(G.g) || !bits_ok(c.bits)) return false;
+  if (c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt != 1)  // tiles: fast decoder only (blocks in a group)
+    return c.bt == 16 && (c.n == 64 || c.n == 128) && G.g >= c.n;
   if (c.backend == CG_BACKEND_KIVI) {
     if (c.win % kTok) return false;
     if (s == 0) return c.kg == kTok && G.g <= 32;  // key groups, gauge groups within one K-step pair
@@ -1526,16 +1600,17 @@ hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G
   m.codes = k.codes; m.side = k.side; m.T_cap = k.T_cap; m.cB = k.B; m.cH = k.H;
   m.err = err;
   const bool pass = c.backend == CG_BACKEND_PASSTHROUGH, kivi = c.backend == CG_BACKEND_KIVI;
-  m.tq = kivi ? tq : X.T;
+  const bool tiles = c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt > 1;
+  m.tq = kivi || tiles ? tq : X.T;
   m.ring = k.ring;
-  m.ring_slots = kivi ? c.win + c.kg : 0;
+  m.ring_slots = kivi ? c.win + c.kg : (tiles ? c.bt : 0);
   const int mode = pass ? kModePass : (kivi && s == 0 ? kModeKeys : kModeBU);
-  const int nb = pass ? 64 : (kivi ? c.kvc : c.n), bits = pass ? 8 : c.bits;
+  const int nb = pass ? 64 : (kivi ? c.kvc : c.n), bits = pass ? 8 : c.bits, bt = tiles ? c.bt : 1;
   void* fn = nullptr;
   switch (ksteps(G.g)) {
-    case 2: fn = enc_by_bits<2>(bits, nb, mode); break;
-    case 4: fn = enc_by_bits<4>(bits, nb, mode); break;
-    case 8: fn = enc_by_bits<8>(bits, nb, mode); break;
+    case 2: fn = enc_by_bits<2>(bits, nb, mode, bt); break;
+    case 4: fn = enc_by_bits<4>(bits, nb, mode, bt); break;
+    case 8: fn = enc_by_bits<8>(bits, nb, mode, bt); break;
   }
   if (!fn) return hipErrorInvalidValue;
   plan(m, X.L * X.B * X.H, X.T, fn);
@@ -1562,7 +1637,8 @@ hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& 
   m.kg = c.kg;
   m.len = len;
   m.ring = k.ring;
-  m.ring_slots = c.win + c.kg;
+  const int bt = c.backend == CG_BACKEND_BLOCK_UNIFORM ? c.bt : 1;
+  m.ring_slots = bt > 1 ? bt : c.win + c.kg;
   if (m.kivi && s == 0) {
     // one tile per 32-position key group: the first may start before t0
     void* fn = keys_by_bits(c.bits, Y.bf16);
@@ -1577,12 +1653,12 @@ hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& 
   if (G.g >= nb) {
     // blocks inside one group: codes feed the matrix core without conversion
     switch (ksteps(G.g)) {
-      case 2: fn = fast_by_bits<2>(c.bits, nb, Y.bf16); break;
-      case 4: fn = fast_by_bits<4>(c.bits, nb, Y.bf16); break;
-      case 8: fn = fast_by_bits<8>(c.bits, nb, Y.bf16); break;
+      case 2: fn = fast_by_bits<2>(c.bits, nb, Y.bf16, bt); break;
+      case 4: fn = fast_by_bits<4>(c.bits, nb, Y.bf16, bt); break;
+      case 8: fn = fast_by_bits<8>(c.bits, nb, Y.bf16, bt); break;
     }
   }
-  if (!fn) {
+  if (!fn && bt == 1) {
     switch (ksteps(G.g)) {
       case 2: fn = dec_by_bits<2>(c.bits, nb, Y.bf16); break;
       case 4: fn = dec_by_bits<4>(c.bits, nb, Y.bf16); break;
