@@ -36,7 +36,7 @@ def parse():
                     help="HBM traffic per launch measured with rocprofv3 counters (optional)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the timed region, run one plain 512 MiB device copy (counter calibration)")
-    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b"]),
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles"]),
                     help="llama8b (default) prints the headline line; the others print per-kernel timings of "
                          "the KIVI, rolling-step and 27B-sweep workloads")
     return ap.parse_args()
@@ -107,11 +107,13 @@ def _timed(fn, steps, warmup, stream):
 
 
 def other_workload(name, steps, warmup):
-    """Per-kernel timings of the KIVI, rolling and 27B workloads at their full shapes, from seeded
-    synthetic K/V (synth.kv_tensor): eight distinct layers repeated to L layers for the KIVI and
-    27B inputs; for the rolling step the history is encoded from one layer viewed with layer
-    stride 0 (each layer's own gauge makes its cache distinct), and the timed step appends one
-    token per (layer, batch, head) and decodes the whole history into bf16."""
+    """Per-kernel timings of the KIVI, rolling, 27B and token-channel tile workloads at their
+    full shapes, from seeded synthetic K/V (synth.kv_tensor): eight distinct layers repeated to
+    L layers for the KIVI, 27B and tile inputs (the tiles use the Llama-3-8B shape with one
+    range per 16 tokens x 128 channels); for the rolling step the history is encoded from one
+    layer viewed with layer stride 0 (each layer's own gauge makes its cache distinct), and the
+    timed step appends one token per (layer, batch, head) and decodes the whole history into
+    bf16."""
     import numpy as np
     import torch
 
@@ -120,7 +122,7 @@ def other_workload(name, steps, warmup):
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    w = synth.WORKLOADS[name]
+    w = synth.WORKLOADS["llama8b" if name == "tiles" else name]
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     out = {"workload": name, "shape": {"L": w.L, "B": w.B, "H": w.H, "T": w.T, "d": w.d}, "steps": steps}
 
@@ -144,8 +146,9 @@ def other_workload(name, steps, warmup):
     def bytes_per_elem(bits, n, kivi=False):
         return 2.0 + bits / 8.0 + (4.0 / n if not kivi else 0.0)
 
-    if name in ("kivi", "gemma27b"):
-        combos = [(w.g, w.bits)] if name == "kivi" else [(g, b) for g in (8, 32, 128) for b in (3, 4, 6)]
+    if name in ("kivi", "gemma27b", "tiles"):
+        combos = {"kivi": [(w.g, w.bits)], "tiles": [(128, 4), (128, 3), (32, 4)]}.get(
+            name, [(g, b) for g in (8, 32, 128) for b in (3, 4, 6)])
         rows = []
         for g, bits in combos:
             shp = cg.shape(w.L, w.H, w.d, g)
@@ -153,6 +156,8 @@ def other_workload(name, steps, warmup):
             cg.gauge_make(cg.GAUGE_HAAR, shp, seed=w.gauge_seed, G_host=None, G_dev=Gd)
             if name == "kivi":
                 codec = cg.Codec(cg.KIVI, bits, 64, w.key_tokens, w.val_channels, w.residual)
+            elif name == "tiles":
+                codec = cg.Codec(cg.BLOCK_UNIFORM, bits, 128, block_t=16)
             else:
                 codec = cg.Codec(cg.BLOCK_UNIFORM, bits, w.block_c)
             row = {"g": g, "bits": bits}
@@ -162,7 +167,7 @@ def other_workload(name, steps, warmup):
                 Y = torch.empty((w.L, w.B, w.H, w.T, w.d), dtype=torch.bfloat16, device="cuda")
                 enc = _timed(lambda: cg.kv_encode(s, X, Gd, shp, codec, cache, err_flag=err,
                                                   stream=stream.cuda_stream), steps, warmup, stream)
-                if name == "kivi":
+                if name in ("kivi", "tiles"):
                     cache.len = w.T
                 dec = _timed(lambda: cg.kv_decode(s, cache, Gd, shp, codec, 0, Y, err_flag=err,
                                                   stream=stream.cuda_stream), steps, warmup, stream)
