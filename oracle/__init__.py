@@ -318,3 +318,64 @@ def bits_per_value(codec: Codec, T: int, d: int) -> float:
     """Measured bits per represented K/V value for one (l, b, h) slice pair."""
     tot = live_bytes(codec, 0, T, d) + live_bytes(codec, 1, T, d)
     return 8.0 * tot / (2.0 * T * d)
+
+
+# ------------------------------------------------------------------------------------------
+# codec-facing spectral statistics (section 4.2, gauge training objective)
+# ------------------------------------------------------------------------------------------
+
+def dct2_matrix(N: int) -> np.ndarray:
+    """Orthonormal DCT-II as a matrix, row k the k-th frequency (binary64):
+    C[k][n] = sqrt((1 if k == 0 else 2) / N) cos(pi (2n + 1) k / (2N))."""
+    k = np.arange(N, dtype=np.float64)[:, None]
+    n = np.arange(N, dtype=np.float64)[None, :]
+    C = np.cos(np.pi * (2.0 * n + 1.0) * k / (2.0 * N)) * np.sqrt(2.0 / N)
+    C[0, :] = np.sqrt(1.0 / N)
+    return C
+
+
+def spectral_radius(Tb: int, d: int) -> np.ndarray:
+    """rho(u, v) = sqrt((u / (Tb - 1))^2 + (v / (d - 1))^2) / sqrt(2), the normalised radius of
+    coefficient (u, v) of a Tb x d token-channel block (section 4.2)."""
+    u = np.arange(Tb, dtype=np.float64)[:, None] / (Tb - 1)
+    v = np.arange(d, dtype=np.float64)[None, :] / (d - 1)
+    return np.sqrt(u * u + v * v) / np.sqrt(2.0)
+
+
+def spectral_stats(X: np.ndarray, G: np.ndarray, s: int, Tb: int = 16, tau: float = 0.04, eps: float = 1e-12):
+    """Spectral statistics of the gauge-transformed cache X' = G X of type s (section 4.2), per
+    layer, in binary64.  The token axis is cut into blocks of Tb tokens (tokens past the last
+    whole block are ignored); each Tb x d block of X' goes through the orthonormal 2-D DCT-II,
+    U = C_Tb Z C_d^T.  With E = U^2 summed over the layer's blocks (every batch row, head and
+    token block), returns (stats [L][4], energy [L][Tb][d]) where
+        stats[l] = (L_freq, L_rate, 1 - L_freq, sum E),
+        L_freq = sum E rho / (sum E + eps),
+        L_rate = mean over the layer's coefficients of log(1 + |U| / tau)."""
+    L_, B, H, T, d = X.shape
+    R, g = G.shape[-3], G.shape[-1]
+    if X.dtype == np.uint16:
+        x = (X.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    else:
+        x = X.astype(np.float64)
+    nblk = T // Tb
+    Ct, Cd = dct2_matrix(Tb), dct2_matrix(d)
+    rho = spectral_radius(Tb, d)
+    stats = np.zeros((L_, 4))
+    energy = np.zeros((L_, Tb, d))
+    for l in range(L_):
+        lsum, count = 0.0, 0
+        for h in range(H):
+            Gd = np.zeros((d, d))
+            for r in range(R):
+                Gd[r * g:(r + 1) * g, r * g:(r + 1) * g] = G[l, s, h, r].astype(np.float64)
+            for b in range(B):
+                Z = x[l, b, h, :nblk * Tb] @ Gd.T                     # z_t = G x_t, [T][d]
+                for k in range(nblk):
+                    U = Ct @ Z[k * Tb:(k + 1) * Tb] @ Cd.T
+                    energy[l] += U * U
+                    lsum += float(np.log1p(np.abs(U) / tau).sum())
+                    count += U.size
+        tot = float(energy[l].sum())
+        lf = float((energy[l] * rho).sum()) / (tot + eps)
+        stats[l] = (lf, lsum / max(count, 1), 1.0 - lf, tot)
+    return stats, energy

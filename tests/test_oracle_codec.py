@@ -374,3 +374,74 @@ def test_tile_bits_per_value_closed_form():
         assert O.bits_per_value(_tile(b, 128, 16), 8192, 128) == b + 32 / 2048
     ref = (8192 * (4 + 32 / 2048) + 8 * 16) / 8200
     assert abs(O.bits_per_value(_tile(4, 128, 16), 8200, 128) - ref) < 1e-12
+
+
+# ------------------------------------------------------------------------------------------
+# spectral statistics of the gauge training objective (section 4.2)
+# ------------------------------------------------------------------------------------------
+def _bits(x: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bits (x exactly representable in bf16 here)."""
+    return (np.ascontiguousarray(x, dtype=np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
+def test_spectral_dct_matches_scipy_and_radius_closed_form():
+    from scipy.fft import dctn
+
+    rng = np.random.default_rng(3)
+    Z = rng.standard_normal((16, 64))
+    U = O.dct2_matrix(16) @ Z @ O.dct2_matrix(64).T
+    np.testing.assert_allclose(U, dctn(Z, type=2, norm="ortho"), rtol=0, atol=1e-12)
+    rho = O.spectral_radius(16, 64)
+    assert rho[0, 0] == 0.0 and abs(rho[15, 63] - 1.0) < 1e-15
+    assert abs(rho[15, 0] - np.sqrt(0.5)) < 1e-15
+
+
+def test_spectral_stats_of_a_constant_cache():
+    """A cache whose every vector is one constant: all energy at the DC coefficient, so
+    L_freq = 0, concentration 1, sum E = the field's energy, and L_rate is the DC term over
+    the Tb d coefficients of a block."""
+    L, B, H, T, d = 1, 2, 2, 40, 64
+    X = _bits(np.full((L, B, H, T, d), 0.75, np.float32))
+    G = O.gauge_make(O.GAUGE_IDENTITY, L, H, d, 16)
+    st, en = O.spectral_stats(X, G, 0, Tb=16)
+    assert st[0, 0] < 1e-20 and abs(st[0, 2] - 1.0) < 1e-20     # off-DC energy is rounding only
+    nblk = T // 16
+    assert abs(st[0, 3] - B * H * nblk * 16 * d * 0.75 ** 2) < 1e-9
+    dc = 0.75 * np.sqrt(16 * d)
+    assert abs(st[0, 1] - np.log1p(dc / 0.04) / (16 * d)) < 1e-12
+    assert np.count_nonzero(np.abs(en[0]) > 1e-20) == 1 and en[0, 0, 0] > 0
+
+
+@pytest.mark.parametrize("u0,v0", [(3, 5), (15, 63), (0, 7), (9, 0)])
+def test_spectral_stats_of_a_single_frequency(u0, v0):
+    """x[t][c] = cos(pi (2t+1) u0 / 32) cos(pi (2c+1) v0 / 128) (identity gauge) is one basis
+    function: L_freq = rho(u0, v0) and the only coefficient is 1 / (s_u0 s_v0) with
+    s_k = sqrt((1 if k == 0 else 2) / N)."""
+    Tb, d = 16, 64
+    t = np.arange(Tb)[:, None]
+    c = np.arange(d)[None, :]
+    blk = np.cos(np.pi * (2 * t + 1) * u0 / (2 * Tb)) * np.cos(np.pi * (2 * c + 1) * v0 / (2 * d))
+    Z = O.dct2_matrix(Tb) @ blk @ O.dct2_matrix(d).T
+    s_u = np.sqrt((1.0 if u0 == 0 else 2.0) / Tb)
+    s_v = np.sqrt((1.0 if v0 == 0 else 2.0) / d)
+    assert abs(Z[u0, v0] - 1.0 / (s_u * s_v)) < 1e-9
+    # through the statistics (float32 input, exact float64 gauge)
+    X = blk.astype(np.float32)[None, None, None]
+    G = O.gauge_make(O.GAUGE_IDENTITY, 1, 1, d, 16)
+    st, _ = O.spectral_stats(X, G, 0, Tb=Tb)
+    rho = np.sqrt((u0 / 15) ** 2 + (v0 / 63) ** 2) / np.sqrt(2)
+    assert abs(st[0, 0] - rho) < 1e-6
+
+
+def test_spectral_energy_is_preserved_by_gauge_and_dct():
+    """Parseval: with an orthogonal gauge and the orthonormal DCT, the layer energy equals the
+    energy of X over the whole blocks, and so does its split across layers."""
+    w, K, V = _tensor(50, L=2)
+    G = O.gauge_make(O.GAUGE_HAAR, 2, 2, 128, 32, seed=21)
+    x = (K.astype(np.uint32) << 16).view(np.float32).astype(np.float64)[:, :, :, :48]
+    st, en = O.spectral_stats(K, G, 0, Tb=16)
+    for l in range(2):
+        # the binary32 gauge is orthogonal to 1e-6 (its own pin), the DCT to rounding
+        assert abs(st[l, 3] - float((x[l] ** 2).sum())) <= 2e-6 * st[l, 3]
+        assert abs(en[l].sum() - st[l, 3]) <= 1e-9 * st[l, 3]
+        assert 0.0 < st[l, 0] < 1.0 and st[l, 1] > 0.0
