@@ -202,6 +202,32 @@ int32_t kv_append_step(int32_t l0, int32_t l1, const cg_kv_view* k_new, const cg
                        const cg_cache* vc, const cg_kv_view* k_hist, const cg_kv_view* v_hist, int32_t* err_flag,
                        void* stream);
 
+/* Bytes of the device workspace kv_spectral_stats needs for this shape and token block
+ * (0 if either is invalid). */
+size_t spectral_workspace_bytes(cg_gauge_shape shp, int32_t block_t);
+
+/* Codec-facing spectral statistics of the gauge training objective (section 4.2) for the
+ * gauge-transformed cache X' = G X of type s (G from G_dev, cache type s = 0 keys, 1 values).
+ * X: a view [L][B][H][T][d] with L = shp.L (bf16 or binary32).  The token axis is cut into
+ * blocks of block_t = Tb tokens (Tb in {2, 4, 8, 16, 32}; tokens past the last whole block are
+ * not used) and every Tb x d block of X' goes through the orthonormal 2-D DCT-II
+ * U = C_Tb Z C_d^T (u: token frequency, v: channel-layout frequency; C_N[k][n] =
+ * sqrt((k == 0 ? 1 : 2) / N) cos(pi (2n + 1) k / (2N))).  With E_uv the sum of U_uv^2 over a
+ * layer's blocks (all batch rows, heads and token blocks) and
+ * rho(u, v) = sqrt((u / (Tb - 1))^2 + (v / (d - 1))^2) / sqrt(2), writes per layer l
+ *   stats[4 l + 0] = L_freq = sum E rho / (sum E + 1e-12)
+ *   stats[4 l + 1] = L_rate = mean over the layer's coefficients of log(1 + |U| / tau)
+ *   stats[4 l + 2] = 1 - L_freq (spectral concentration)
+ *   stats[4 l + 3] = sum E (the energy of the used tokens of X', G and the DCT being orthogonal)
+ * stats: device binary64 [L][4].  energy (optional, may be NULL): device binary64 [L][Tb][d]
+ * receiving the energy maps E.  workspace: caller-owned device buffer of
+ * spectral_workspace_bytes(shp, block_t) bytes, 16-byte aligned, whose contents the call
+ * overwrites (calls sharing one workspace on different streams race).  tau > 0 (the paper
+ * uses 0.04).  Errors: CG_ERR_ARG, CG_ERR_SHAPE, CG_ERR_ALIGN, CG_ERR_UNSUPPORTED,
+ * CG_ERR_DEVICE. */
+int32_t kv_spectral_stats(int32_t s, const cg_kv_view* X, const void* G_dev, cg_gauge_shape shp, int32_t block_t,
+                          float tau, void* workspace, double* stats, double* energy, void* stream);
+
 /* Device self-test of the two binary32 steps of the quantiser the kernels compute without a
  * division (section 4.3 block range; the oracle divides): which = 0 compares the reciprocal
  * of every positive finite binary16 scale with correctly rounded 1/s; which = 1 compares the

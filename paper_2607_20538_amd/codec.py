@@ -24,7 +24,7 @@ PASSTHROUGH, BLOCK_UNIFORM, KIVI = 0, 1, 2
 DTYPE_BF16, DTYPE_F32 = 0, 1
 
 EXPORTS = ["cg_status_str", "gauge_device_bytes", "gauge_make", "cache_bytes", "kv_encode", "kv_decode",
-           "kv_append_step", "cg_selftest"]
+           "kv_append_step", "spectral_workspace_bytes", "kv_spectral_stats", "cg_selftest"]
 
 
 class GaugeShape(C.Structure):
@@ -81,6 +81,10 @@ def lib() -> C.CDLL:
                                      C.POINTER(CodecStruct), C.POINTER(CacheStruct), C.POINTER(CacheStruct),
                                      C.POINTER(KvView), C.POINTER(KvView), p, p]
         L.kv_append_step.restype = i32
+        L.spectral_workspace_bytes.argtypes = [GaugeShape, i32]
+        L.spectral_workspace_bytes.restype = C.c_size_t
+        L.kv_spectral_stats.argtypes = [i32, C.POINTER(KvView), p, GaugeShape, i32, C.c_float, p, p, p, p]
+        L.kv_spectral_stats.restype = i32
         L.cg_selftest.argtypes = [i32, p, p]
         L.cg_selftest.restype = i32
         _lib = L
@@ -225,3 +229,17 @@ def kv_append_step(l0: int, l1: int, k_new, v_new, pos, G_dev, shp: GaugeShape, 
     rc = lib().kv_append_step(l0, l1, C.byref(kn), C.byref(vn), _ptr(pos), _ptr(G_dev), shp, C.byref(cs),
                               C.byref(kcs), C.byref(vcs), kh, vh, _ptr(err_flag), _stream(stream))
     _check("kv_append_step", rc)
+
+
+def spectral_workspace_bytes(shp: GaugeShape, block_t: int) -> int:
+    return int(lib().spectral_workspace_bytes(shp, block_t))
+
+
+def kv_spectral_stats(s: int, X, G_dev, shp: GaugeShape, block_t: int, tau: float, workspace, stats, energy=None,
+                      stream=None):
+    """Spectral statistics of G X (section 4.2) into the device float64 tensors stats [L][4] and,
+    if given, energy [L][block_t][d]; workspace: device buffer of spectral_workspace_bytes."""
+    v = view(X)
+    rc = lib().kv_spectral_stats(s, C.byref(v), _ptr(G_dev), shp, block_t, tau, _ptr(workspace), _ptr(stats),
+                                 _ptr(energy), _stream(stream))
+    _check("kv_spectral_stats", rc)

@@ -587,6 +587,28 @@ int32_t kv_append_step(int32_t l0, int32_t l1, const cg_kv_view* k_new, const cg
   return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
 }
 
+size_t spectral_workspace_bytes(cg_gauge_shape shp, int32_t block_t) {
+  if (check_shape(shp) != CG_OK || block_t < 2 || block_t > 32 || (block_t & (block_t - 1))) return 0;
+  return spec_layout(shp, block_t).total;
+}
+
+int32_t kv_spectral_stats(int32_t s, const cg_kv_view* X, const void* G_dev, cg_gauge_shape shp, int32_t block_t,
+                          float tau, void* workspace, double* stats, double* energy, void* stream) {
+  int32_t rc = check_shape(shp);
+  if (rc != CG_OK) return rc;
+  if (s < 0 || s > 1 || !G_dev || !workspace || !stats) return CG_ERR_ARG;
+  if (block_t < 2 || block_t > 32 || (block_t & (block_t - 1))) return CG_ERR_UNSUPPORTED;
+  if (!(tau > 0.0f) || !isfinite(tau)) return CG_ERR_ARG;
+  if (!aligned16(G_dev) || !aligned16(workspace) || (reinterpret_cast<uintptr_t>(stats) & 7u) ||
+      (reinterpret_cast<uintptr_t>(energy) & 7u))
+    return CG_ERR_ALIGN;
+  if ((rc = check_view(X, shp, shp.L)) != CG_OK) return rc;
+  if (X->T > 0 && !X->ptr) return CG_ERR_ARG;
+  hipError_t e = launch_spectral(s, view_dev(X), gauge_dev(G_dev, shp), block_t, tau, workspace, stats, energy,
+                                 force_generic(), static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
+}
+
 int32_t cg_selftest(int32_t which, uint64_t* mismatches_dev, void* stream) {
   if ((which != 0 && which != 1) || !mismatches_dev) return CG_ERR_ARG;
   if (reinterpret_cast<uintptr_t>(mismatches_dev) & 7u) return CG_ERR_ALIGN;

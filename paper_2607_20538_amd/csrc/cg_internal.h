@@ -99,6 +99,16 @@ hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G
 hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
                               int len, const int* pos, const ViewDev& Y, int* err, hipStream_t st);
 
+// Spectral statistics (section 4.2): workspace sections (bytes from the start, 256-aligned):
+// energy sums binary64 [L][Tb][d], log sums binary64 [L], DCT-II rows binary64 [d][d], and for
+// d = 128 the two bf16 planes of M = C_d G, [L][H][d][d] each.
+struct SpecLayout {
+  size_t off_acc = 0, off_lsum = 0, off_cd = 0, off_m[2] = {0, 0}, total = 0;
+};
+SpecLayout spec_layout(const cg_gauge_shape& s, int Tb);
+hipError_t launch_spectral(int s, const ViewDev& X, const GaugeDev& G, int Tb, float tau, void* ws, double* stats,
+                           double* energy, bool force_generic, hipStream_t st);
+
 // Device self-test of the quantiser's division-free steps (which: 0 reciprocal, 1 division).
 hipError_t launch_selftest(int which, unsigned long long* bad, hipStream_t st);
 

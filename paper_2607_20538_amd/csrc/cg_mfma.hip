@@ -33,24 +33,13 @@
 
 #include "cg_internal.h"
 #include "cg_device.h"
+#include "cg_mfma_util.h"
 
 namespace cg {
 
 namespace {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-
-constexpr int kD = 128;          // head dimension handled here
-constexpr int kTok = 32;         // tokens per tile (MFMA N)
-constexpr int kThreads = 256;    // four waves
-constexpr int kRowBytes = kD * 2;
 constexpr int kStages = 5;       // encoder LDS ring: tiles in flight + the one being read
-// s_waitcnt immediate (gfx9 encoding: vmcnt[3:0] and [15:14], expcnt[6:4], lgkmcnt[11:8])
-// waiting until at most `vm` vector-memory operations are outstanding, with lgkmcnt = 0 (all
-// LDS operations of the wave done) and no wait on expcnt
-constexpr int waitcnt_imm(int vm) { return (vm & 15) | ((vm >> 4) << 14) | (7 << 4) | (0 << 8); }
 
 struct MfmaArgs {
   // view (input for encode, output for decode)
@@ -81,21 +70,6 @@ struct MfmaArgs {
   int* err;
 };
 
-__device__ __forceinline__ int xcd_remap(int bid, int nwg) {
-  // workgroups are dealt round-robin to the 8 XCDs; give each XCD a contiguous range of
-  // logical workgroups so that the ranges of one slice share an L2
-  const int per = nwg >> 3;
-  return (bid & 7) * per + (bid >> 3);
-}
-
-// physical 16-byte granule of logical granule j in token row n
-__device__ __forceinline__ int swz(int n, int j) { return j ^ (n & 15); }
-
-__device__ __forceinline__ f32x16_t mfma(const bf16x8_t& a, const bf16x8_t& b, const f32x16_t& c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-}
-
-__device__ __forceinline__ bf16x8_t as_bf16x8(const u32x4_t& v) { return __builtin_bit_cast(bf16x8_t, v); }
 
 // Load the wave's A fragments: plane p, K-step kk: 8 bf16 of row `ch` (an output channel of
 // this wave) at input channels j0..j0+7 of the full block-diagonal matrix (zero outside the
@@ -163,10 +137,6 @@ __device__ __forceinline__ f32x16_t mfma_chain(const bf16x8_t (&A)[NP][KS], cons
 }
 
 // min / max over the 16 lanes of a DPP row (quad swaps, then rotations by 4 and 8 lanes)
-template <int CTRL>
-__device__ __forceinline__ float dpp_mov(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
-}
 __device__ __forceinline__ float row16_min(float v) {
   v = fminf(v, dpp_mov<0xB1>(v));   // quad_perm [1,0,3,2]
   v = fminf(v, dpp_mov<0x4E>(v));   // quad_perm [2,3,0,1]

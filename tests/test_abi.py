@@ -181,6 +181,30 @@ def test_append_step_rejects_invalid_arguments():
              None, None, None) == cg.CG_ERR_ALIGN
 
 
+def test_spectral_stats_reject_invalid_arguments():
+    shp = cg.shape(1, 2, 64, 16)
+    v = _fake_view(T=32)
+    assert cg.spectral_workspace_bytes(shp, 16) > 0
+    assert cg.spectral_workspace_bytes(shp, 3) == 0 and cg.spectral_workspace_bytes(shp, 64) == 0
+    f = cg.lib().kv_spectral_stats
+    ok = dict(s=0, blk=16, tau=0.04, ws=0x70000, stats=0x80000)
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["s"], C.byref(a.get("view", v)), 0x50000, a.get("shp", shp), a["blk"], a["tau"], a["ws"],
+                 a["stats"], None, None)
+    assert call(blk=3) == cg.CG_ERR_UNSUPPORTED
+    assert call(blk=1) == cg.CG_ERR_UNSUPPORTED
+    assert call(tau=0.0) == cg.CG_ERR_ARG
+    assert call(tau=float("nan")) == cg.CG_ERR_ARG
+    assert call(s=2) == cg.CG_ERR_ARG
+    assert call(ws=None) == cg.CG_ERR_ARG
+    assert call(stats=None) == cg.CG_ERR_ARG
+    assert call(ws=0x70008) == cg.CG_ERR_ALIGN
+    assert call(stats=0x80004) == cg.CG_ERR_ALIGN
+    assert call(view=_fake_view(H=3)) == cg.CG_ERR_SHAPE
+    assert call(shp=cg.shape(1, 2, 64, 48)) == cg.CG_ERR_UNSUPPORTED
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(cg, "LIB_PATH", str(tmp_path / "missing.so"))
     monkeypatch.setattr(cg, "_lib", None)

@@ -1,0 +1,89 @@
+"""GPU parity of the spectral statistics of the gauge training objective (section 4.2) against
+the oracle: layer energy maps of the 2-D DCT of Tb x d token-channel blocks of G X, L_freq,
+L_rate, concentration and total energy, on the matrix-core path (bf16, d = 128, Tb = 16) and
+the general path (other shapes, binary32 input, other Tb)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2607_20538_amd import codec as cg
+from paper_2607_20538_amd import synth
+
+from _parity import x_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    cg.lib()
+
+
+@pytest.fixture(params=["mfma", "generic"])
+def kernels(request, monkeypatch):
+    if request.param == "generic":
+        monkeypatch.setenv("CG_KERNELS", "generic")
+    else:
+        monkeypatch.delenv("CG_KERNELS", raising=False)
+    return request.param
+
+
+def _run(X, G, s, Tb, tau=0.04):
+    L, B, H, T, d = X.shape
+    g = G.shape[-1]
+    shp = cg.shape(L, H, d, g)
+    Gd = cg.alloc_gauge(shp)
+    cg.gauge_make(cg.GAUGE_USER, shp, params=G, G_host=None, G_dev=Gd)
+    ws = torch.empty(cg.spectral_workspace_bytes(shp, Tb), dtype=torch.uint8, device="cuda")
+    stats = torch.full((L, 4), float("nan"), dtype=torch.float64, device="cuda")
+    energy = torch.full((L, Tb, d), float("nan"), dtype=torch.float64, device="cuda")
+    cg.kv_spectral_stats(s, x_dev(X), Gd, shp, Tb, tau, ws, stats, energy)
+    torch.cuda.synchronize()
+    return stats.cpu().numpy(), energy.cpu().numpy()
+
+
+def _check(got, ref, rtol=5e-5):
+    st, en = got
+    rs, re = ref
+    np.testing.assert_allclose(st[:, 0], rs[:, 0], rtol=rtol, atol=1e-12)     # L_freq
+    np.testing.assert_allclose(st[:, 1], rs[:, 1], rtol=rtol, atol=1e-12)     # L_rate
+    np.testing.assert_allclose(st[:, 2], rs[:, 2], rtol=rtol, atol=1e-12)     # concentration
+    np.testing.assert_allclose(st[:, 3], rs[:, 3], rtol=rtol, atol=1e-12)     # energy
+    scale = re.reshape(re.shape[0], -1).max(axis=1)[:, None, None]
+    assert np.all(np.abs(en - re) <= 1e-4 * scale + 1e-3 * np.abs(re))
+
+
+@pytest.mark.parametrize("g", [128, 32, 8])
+@pytest.mark.parametrize("s", [0, 1])
+def test_spectral_stats_match_oracle(g, s, kernels):
+    w = synth.Workload("spec", L=2, B=2, H=2, T=100, d=128, dtype="bf16", g=g, backend="bu", bits=4,
+                       data_seed=0x5EC + g)
+    X = synth.kv_tensor(w, s)
+    G = O.gauge_make(O.GAUGE_HAAR, 2, 2, 128, g, seed=g)
+    _check(_run(X, G, s, 16), O.spectral_stats(X, G, s, Tb=16))
+
+
+@pytest.mark.parametrize("Tb,d,dtype", [(8, 64, "f32"), (32, 128, "bf16"), (16, 64, "bf16"), (4, 128, "f32")])
+def test_spectral_stats_other_shapes(Tb, d, dtype):
+    w = synth.Workload("spec", L=1, B=1, H=2, T=70, d=d, dtype=dtype, g=16, backend="bu", bits=4, data_seed=77)
+    X = synth.kv_tensor(w, 0)
+    G = O.gauge_make(O.GAUGE_DCT2, 1, 2, d, 16)
+    _check(_run(X, G, 0, Tb), O.spectral_stats(X, G, 0, Tb=Tb))
+
+
+def test_spectral_stats_of_short_caches_and_closed_forms(kernels):
+    """No whole block: zero energy, L_freq 0, concentration 1.  A constant cache (identity
+    gauge): all energy at the DC coefficient."""
+    L, B, H, d = 1, 1, 2, 128
+    G = O.gauge_make(O.GAUGE_IDENTITY, L, H, d, 32)
+    X = np.full((L, B, H, 9, d), 0x3F40, np.uint16)                 # 0.75, fewer than 16 tokens
+    st, en = _run(X, G, 0, 16)
+    assert np.all(st[:, [0, 1, 3]] == 0.0) and np.all(st[:, 2] == 1.0) and not en.any()
+    X = np.full((L, B, H, 48, d), 0x3F40, np.uint16)
+    st, en = _run(X, G, 0, 16)
+    # (the matrix-core path multiplies two bf16 planes of C_d G: 2^-17 per entry)
+    assert st[0, 0] < 1e-6 and abs(st[0, 3] - B * H * 48 * d * 0.5625) < 2e-5 * st[0, 3]
+    assert en[0, 0, 0] > 0.999 * st[0, 3]
