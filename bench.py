@@ -36,7 +36,7 @@ def parse():
                     help="HBM traffic per launch measured with rocprofv3 counters (optional)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the timed region, run one plain 512 MiB device copy (counter calibration)")
-    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles"]),
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral"]),
                     help="llama8b (default) prints the headline line; the others print per-kernel timings of "
                          "the KIVI, rolling-step and 27B-sweep workloads")
     return ap.parse_args()
@@ -122,7 +122,7 @@ def other_workload(name, steps, warmup):
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    w = synth.WORKLOADS["llama8b" if name == "tiles" else name]
+    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral") else name]
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     out = {"workload": name, "shape": {"L": w.L, "B": w.B, "H": w.H, "T": w.T, "d": w.d}, "steps": steps}
 
@@ -146,7 +146,25 @@ def other_workload(name, steps, warmup):
     def bytes_per_elem(bits, n, kivi=False):
         return 2.0 + bits / 8.0 + (4.0 / n if not kivi else 0.0)
 
-    if name in ("kivi", "gemma27b", "tiles"):
+    if name == "spectral":
+        # section 4.2 statistics of G X on the Llama-3-8B shape, 16-token blocks, tau = 0.04
+        shp = cg.shape(w.L, w.H, w.d, w.g)
+        Gd = cg.alloc_gauge(shp)
+        cg.gauge_make(cg.GAUGE_HAAR, shp, seed=w.gauge_seed, G_host=None, G_dev=Gd)
+        ws = torch.empty(cg.spectral_workspace_bytes(shp, 16), dtype=torch.uint8, device="cuda")
+        stats = torch.empty((w.L, 4), dtype=torch.float64, device="cuda")
+        rows = {}
+        for s, tag in ((0, "K"), (1, "V")):
+            X = layer_input(s)
+            ms = _timed(lambda: cg.kv_spectral_stats(s, X, Gd, shp, 16, 0.04, ws, stats, stream=stream.cuda_stream),
+                        steps, warmup, stream)
+            st = stats.cpu().numpy()
+            rows[tag] = {"ms": round(ms, 3), "GBps_bf16_in": round(X.numel() * 2 / ms / 1e6, 1),
+                         "L_freq_mean": round(float(st[:, 0].mean()), 6), "L_rate_mean": round(float(st[:, 1].mean()), 6)}
+            del X
+            torch.cuda.empty_cache()
+        out["runs"] = rows
+    elif name in ("kivi", "gemma27b", "tiles"):
         combos = {"kivi": [(w.g, w.bits)], "tiles": [(128, 4), (128, 3), (32, 4)]}.get(
             name, [(g, b) for g in (8, 32, 128) for b in (3, 4, 6)])
         rows = []

@@ -45,21 +45,53 @@ __global__ void spec_init(double* acc, size_t nacc, double* lsum, int L, double*
   }
 }
 
-// M = C_d G_{l,s,h} (G block-diagonal over its R groups) in binary64, rounded to binary32 and
-// split into two bf16 planes; block (l*H + h, i) computes row i.
-__global__ void spec_mprep(int s, GaugeDev G, int H, const double* cd, uint16_t* m0, uint16_t* m1) {
-  const int lh = blockIdx.x, i = blockIdx.y, j = threadIdx.x;
-  const int l = lh / H, h = lh - l * H;
-  const int g = G.g, r = j / g, jj = j - r * g;
-  const float* Gr = G.f32 + (((size_t(l) * 2 + s) * G.H + h) * G.R + r) * g * g;
-  double acc = 0.0;
-  for (int a = 0; a < g; ++a) acc += cd[size_t(i) * kD + r * g + a] * double(Gr[size_t(a) * g + jj]);
-  const float v = float(acc);
-  const uint32_t hi = f32_to_bf16_rne(v);
-  const uint32_t lo = f32_to_bf16_rne(v - __uint_as_float(hi << 16));
-  const size_t off = (size_t(lh) * kD + i) * kD + j;
-  m0[off] = uint16_t(hi);
-  m1[off] = uint16_t(lo);
+// M = C_d G_{l,s,h} (G block-diagonal over its R groups), products and sums in binary64 from
+// the binary32 DCT rows and gauge, rounded to binary32 and split into two bf16 planes.  One
+// workgroup per (l, h) stages C_d and the gauge blocks in LDS; thread t accumulates the 8 x 8
+// outputs rows 8 (t / 16) .., columns 8 (t % 16) .. (one gauge group: 8 | g).
+__global__ __launch_bounds__(256) void spec_mprep(int s, GaugeDev G, int H, const double* cd, uint16_t* m0,
+                                                   uint16_t* m1) {
+  __shared__ float cds[kD * kD];   // C_d rows
+  __shared__ float gs[kD * kD];    // gs[a_global][j]: G_{r}[a][j - r g] for j in group r, a = a_global - r g
+  const int lh = blockIdx.x, l = lh / H, h = lh - l * H;
+  const int g = G.g;
+  for (int idx = threadIdx.x; idx < kD * kD; idx += blockDim.x) {
+    cds[idx] = float(cd[idx]);
+    const int ag = idx / kD, j = idx - ag * kD, r = j / g;
+    const int a = ag - r * g;
+    float v = 0.0f;
+    if (a >= 0 && a < g) v = G.f32[((((size_t(l) * 2 + s) * G.H + h) * G.R + r) * g + a) * g + (j - r * g)];
+    gs[idx] = v;
+  }
+  __syncthreads();
+  const int i0 = 8 * (threadIdx.x / 16), j0 = 8 * (threadIdx.x % 16), r = j0 / g;
+  double acc[8][8];
+#pragma unroll
+  for (int p = 0; p < 8; ++p)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[p][q] = 0.0;
+  for (int a = r * g; a < r * g + g; ++a) {
+    double cv[8], gv[8];
+#pragma unroll
+    for (int p = 0; p < 8; ++p) cv[p] = double(cds[(i0 + p) * kD + a]);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) gv[q] = double(gs[a * kD + j0 + q]);
+#pragma unroll
+    for (int p = 0; p < 8; ++p)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) acc[p][q] = fma(cv[p], gv[q], acc[p][q]);
+  }
+#pragma unroll
+  for (int p = 0; p < 8; ++p)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const float v = float(acc[p][q]);
+      const uint32_t hi = f32_to_bf16_rne(v);
+      const uint32_t lo = f32_to_bf16_rne(v - __uint_as_float(hi << 16));
+      const size_t off = (size_t(lh) * kD + i0 + p) * kD + j0 + q;
+      m0[off] = uint16_t(hi);
+      m1[off] = uint16_t(lo);
+    }
 }
 
 struct SpecArgs {
@@ -357,7 +389,7 @@ hipError_t launch_spectral(int s, const ViewDev& X, const GaugeDev& G, int Tb, f
     if (!force_generic && X.bf16 && X.d == kD && Tb == kSpecTb) {
       uint16_t* m0 = reinterpret_cast<uint16_t*>(base + lay.off_m[0]);
       uint16_t* m1 = reinterpret_cast<uint16_t*>(base + lay.off_m[1]);
-      hipLaunchKernelGGL(spec_mprep, dim3(X.L * X.H, kD), dim3(kD), 0, st, s, G, X.H, cd, m0, m1);
+      hipLaunchKernelGGL(spec_mprep, dim3(X.L * X.H), dim3(256), 0, st, s, G, X.H, cd, m0, m1);
       if ((e = hipGetLastError()) != hipSuccess) return e;
       SpecArgs a{};
       a.x = static_cast<const char*>(X.ptr);
