@@ -552,8 +552,9 @@ __device__ __forceinline__ float seg_colsum(const MfmaArgs& a, int l, int h, int
   return acc;
 }
 
-template <int NP, int KS, int BITS, int NB, bool OUT_BF16>
+template <int NP, int KS, int BITS, int NB, bool OUT_BF16, int TB = 1>
 __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
+  static_assert(TB == 1 || TB == 16, "token-channel tiles of 16 tokens");
   constexpr int NBK = kD / NB;                      // blocks per token row
   __shared__ __attribute__((aligned(16))) uint8_t qtile[2][kTok * kRowBytes];  // codes as bf16
   __shared__ uint32_t stile[2][kTok * NBK];         // side words
@@ -573,7 +574,7 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
   const int h = slice % a.H, b = (slice / a.H) % a.B, lv = slice / (a.H * a.B);
   const int l = lv + a.l0;
   int Tv = a.T;  // view tokens to write
-  int held = a.kivi ? a.len : INT_MAX;  // positions the cache holds
+  int held = a.kivi || TB > 1 ? a.len : INT_MAX;  // positions the cache holds
   if (a.pos) {
     const int p = a.pos[b];
     if (p < 0 || p >= a.T_cap) return;  // flagged by the append kernel
@@ -586,8 +587,9 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
   if (tb >= te_all) return;
   char* ys = a.x + (OUT_BF16 ? 2 : 4) * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
   const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
-  // KIVI: the quantised view rows [0, Tq) go through the pipeline, the window rows after it
-  const int Tq = a.kivi ? kivi_quantised_rows(a, held, Tv) : Tv;
+  // KIVI / tiles: the quantised view rows [0, Tq) go through the pipeline, the window or
+  // staged rows after it
+  const int Tq = a.kivi ? kivi_quantised_rows(a, held, Tv) : (TB > 1 ? max(0, min(Tv, held / TB * TB - a.t0)) : Tv);
   const int te = min(te_all, (Tq + kTok - 1) / kTok);
   if (tb >= te) {
     ring_rows<OUT_BF16>(a, cslice, ys, max(Tq, tb * kTok), min(Tv, te_all * kTok));
@@ -635,7 +637,7 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
     // shift the segment down to bit 0 (odd widths start mid-word)
 #pragma unroll
     for (int i = 0; i + 1 < SEGW; ++i) cw[i] = __builtin_amdgcn_alignbit(cw[i + 1], cw[i], bit0 & 31);
-    sw = a.side[crow * NBK + st_blk];
+    sw = a.side[crow / TB * NBK + st_blk];  // the token's block, or its tile's
     // first code of a 32-channel group that starts in the previous segment (word aligned)
     if (gc && a.g == 32 && (st_seg & 1)) cfirst = row[(32 * (st_seg >> 1) * BITS) >> 5] & ((1u << BITS) - 1u);
   };
@@ -1436,30 +1438,44 @@ void* enc_by_bits(int bits, int nb, int mode, int bt) {
   return nullptr;
 }
 
+// (token-channel tiles: blocks of 64 or 128 channels over groups of at most 32, centred per
+// (token, group))
 template <int KS, int BITS, int NB>
-void* dec_kernel(bool bf16) {
-  if (bf16) return (void*)dec_mfma<kNP, KS, BITS, NB, true>;
-  return (void*)dec_mfma<kNP, KS, BITS, NB, false>;
+void* dec_kernel(bool bf16, int bt) {
+  if constexpr (KS == 2 && NB >= 64) {
+    if (bt == 16) {
+      if (bf16) return (void*)dec_mfma<kNP, KS, BITS, NB, true, 16>;
+      return (void*)dec_mfma<kNP, KS, BITS, NB, false, 16>;
+    }
+  }
+  if constexpr (NB <= 64) {
+    if (bt == 1) {
+      if (bf16) return (void*)dec_mfma<kNP, KS, BITS, NB, true>;
+      return (void*)dec_mfma<kNP, KS, BITS, NB, false>;
+    }
+  }
+  return nullptr;
 }
 
 template <int KS, int BITS>
-void* dec_by_nb(int nb, bool bf16) {
+void* dec_by_nb(int nb, bool bf16, int bt) {
   switch (nb) {
-    case 16: return dec_kernel<KS, BITS, 16>(bf16);
-    case 32: return dec_kernel<KS, BITS, 32>(bf16);
-    case 64: return dec_kernel<KS, BITS, 64>(bf16);
+    case 16: return dec_kernel<KS, BITS, 16>(bf16, bt);
+    case 32: return dec_kernel<KS, BITS, 32>(bf16, bt);
+    case 64: return dec_kernel<KS, BITS, 64>(bf16, bt);
+    case 128: return dec_kernel<KS, BITS, 128>(bf16, bt);
   }
   return nullptr;
 }
 
 template <int KS>
-void* dec_by_bits(int bits, int nb, bool bf16) {
+void* dec_by_bits(int bits, int nb, bool bf16, int bt) {
   switch (bits) {
-    case 2: return dec_by_nb<KS, 2>(nb, bf16);
-    case 3: return dec_by_nb<KS, 3>(nb, bf16);
-    case 4: return dec_by_nb<KS, 4>(nb, bf16);
-    case 6: return dec_by_nb<KS, 6>(nb, bf16);
-    case 8: return dec_by_nb<KS, 8>(nb, bf16);
+    case 2: return dec_by_nb<KS, 2>(nb, bf16, bt);
+    case 3: return dec_by_nb<KS, 3>(nb, bf16, bt);
+    case 4: return dec_by_nb<KS, 4>(nb, bf16, bt);
+    case 6: return dec_by_nb<KS, 6>(nb, bf16, bt);
+    case 8: return dec_by_nb<KS, 8>(nb, bf16, bt);
   }
   return nullptr;
 }
@@ -1547,8 +1563,8 @@ bool mfma_encode_supported(const ViewDev& X, const GaugeDev& G, const CodecDev& 
 
 bool mfma_decode_supported(int s, const ViewDev& Y, const GaugeDev& G, const CodecDev& c) {
   if (Y.d != kD || !group_ok(G.g) || !bits_ok(c.bits)) return false;
-  if (c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt != 1)  // tiles: fast decoder only (blocks in a group)
-    return c.bt == 16 && (c.n == 64 || c.n == 128) && G.g >= c.n;
+  if (c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt != 1)  // tiles: blocks inside a group, or centred groups
+    return c.bt == 16 && (c.n == 64 || c.n == 128) && (G.g >= c.n || G.g <= 32);
   if (c.backend == CG_BACKEND_KIVI) {
     if (c.win % kTok) return false;
     if (s == 0) return c.kg == kTok && G.g <= 32;  // key groups, gauge groups within one K-step pair
@@ -1628,11 +1644,11 @@ hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& 
       case 8: fn = fast_by_bits<8>(c.bits, nb, Y.bf16, bt); break;
     }
   }
-  if (!fn && bt == 1) {
+  if (!fn) {
     switch (ksteps(G.g)) {
-      case 2: fn = dec_by_bits<2>(c.bits, nb, Y.bf16); break;
-      case 4: fn = dec_by_bits<4>(c.bits, nb, Y.bf16); break;
-      case 8: fn = dec_by_bits<8>(c.bits, nb, Y.bf16); break;
+      case 2: fn = dec_by_bits<2>(c.bits, nb, Y.bf16, bt); break;
+      case 4: fn = dec_by_bits<4>(c.bits, nb, Y.bf16, bt); break;
+      case 8: fn = dec_by_bits<8>(c.bits, nb, Y.bf16, bt); break;
     }
   }
   if (!fn) return hipErrorInvalidValue;
