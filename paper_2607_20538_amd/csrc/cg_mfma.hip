@@ -810,8 +810,9 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
 // Channel order of the B fragments (and of the A fragments gathered to match): lane half hc
 // owns the 8 SEG channels [16 SEG s + 8 SEG hc, +8 SEG) of block segment s of the wave's K
 // range; K-step u of the segment takes, with b = 4, channels 8u + (0,4,1,5,2,6,3,7) of that
-// region (nibble pairs of one packed word), with b = 2 channels 16 (u/2) + 4 (u%2) +
-// (0,8,1,9,2,10,3,11) (2-bit pairs of one word), otherwise 8u + (0..7).
+// region (nibble pairs of one packed word; the same order with b = 6, pairs 24 bits apart),
+// with b = 2 channels 16 (u/2) + 4 (u%2) + (0,8,1,9,2,10,3,11) (2-bit pairs of one word; the
+// same order with b = 3, pairs 24 bits apart), otherwise 8u + (0..7).
 template <int NP, int KS, int BITS, int SEG>
 __device__ void load_a_perm(bf16x8_t (&A)[NP][KS], const MfmaArgs& a, int l, int h, int ch, int kbase, int hc) {
   const int g = a.g, r = ch / g;
@@ -833,14 +834,14 @@ __device__ void load_a_perm(bf16x8_t (&A)[NP][KS], const MfmaArgs& a, int l, int
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       u32x4_t f;
-      if constexpr (BITS == 4) {
+      if constexpr (BITS == 4 || BITS == 6) {
         // channels region + 8u + (0,4,1,5,2,6,3,7)
         const u32x4_t v = load8(p, region + 8 * u);
         f[0] = pair_lo(v[0], v[2]);
         f[1] = pair_hi(v[0], v[2]);
         f[2] = pair_lo(v[1], v[3]);
         f[3] = pair_hi(v[1], v[3]);
-      } else if constexpr (BITS == 2) {
+      } else if constexpr (BITS == 2 || BITS == 3) {
         // channels base + 4 (u & 1) + (0,8,1,9,2,10,3,11), base = region + 16 (u >> 1)
         const int base = region + 16 * (u >> 1);
         const u32x4_t lo = load8(p, base), hi = load8(p, base + 8);
@@ -884,6 +885,32 @@ __device__ __forceinline__ bf16x8_t code_frag(const uint32_t (&rw)[RW], int u, u
       f[2] = ((w >> 7) & m) | one;
       f[3] = ((w >> 9) & m) | one;
     }
+  } else if constexpr (BITS == 6) {
+    // codes 8u + (0,4,1,5,2,6,3,7) at mantissa bits 0..5 (B = 1 + q / 128; m = 0x003F003F):
+    // code 8u + j starts at byte 6u + 6j/8, bit 6j % 8 of the region and its partner 8u + j + 4
+    // three bytes later, so one byte permute (bytes o, o+1, o+3, o+4 of the word pair) puts
+    // the two exactly 16 bits apart; bytes past the region only reach masked-off bits
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int byte = 6 * u + (6 * j) / 8, r = (6 * j) % 8;
+      const int wi = byte >> 2, o = byte & 3;
+      const uint32_t sel = uint32_t(o) | (uint32_t(o + 1) << 8) | (uint32_t(o + 3) << 16) | (uint32_t(o + 4) << 24);
+      const uint32_t x = __builtin_amdgcn_perm(rw[wi + 1 < RW ? wi + 1 : wi], rw[wi], sel);
+      f[j] = ((x >> r) & m) | one;
+    }
+  } else if constexpr (BITS == 3) {
+    // codes 16 (u/2) + 4 (u%2) + (0,8,1,9,2,10,3,11) at mantissa bits 4..6 (m = 0x00700070):
+    // code j of a 16-code group starts at byte 3j/8, bit 3j % 8, its partner j + 8 three bytes
+    // later; one byte permute puts the pair 16 bits apart, one shift moves it to bit 4
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int j = 4 * (u & 1) + k, byte = 6 * (u >> 1) + (3 * j) / 8, r = (3 * j) % 8;
+      const int wi = byte >> 2, o = byte & 3;
+      const uint32_t sel = uint32_t(o) | (uint32_t(o + 1) << 8) | (uint32_t(o + 3) << 16) | (uint32_t(o + 4) << 24);
+      const uint32_t x = __builtin_amdgcn_perm(rw[wi + 1 < RW ? wi + 1 : wi], rw[wi], sel);
+      const uint32_t y = r <= 4 ? (x << (4 - r)) : (x >> (r - 4));
+      f[k] = (y & m) | one;
+    }
   } else if constexpr (BITS == 8) {
     // codes as themselves: bytes to binary32 (exact), high halves are the bf16 values
     const uint32_t w0 = rw[2 * u], w1 = rw[2 * u + 1];
@@ -893,7 +920,7 @@ __device__ __forceinline__ bf16x8_t code_frag(const uint32_t (&rw)[RW], int u, u
     f[2] = pk(float(w1 & 255u), float((w1 >> 8) & 255u));
     f[3] = pk(float((w1 >> 16) & 255u), float(w1 >> 24));
   } else {
-    // 3 or 6 bits: 8 codes of the LSB-first stream at bit 8 u BITS of the region
+    // other widths: 8 codes of the LSB-first stream at bit 8 u BITS of the region
     constexpr int b0 = 8 * BITS;
     const int bit = u * b0, wi = bit >> 5, sh = bit & 31;
     const uint64_t win = ((uint64_t(rw[wi + 1 < RW ? wi + 1 : wi]) << 32) | rw[wi]) >> sh;
@@ -1064,9 +1091,11 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
   for (int t = tb; t < min(te, tb + DS - 1); ++t) issue(t);
   __syncthreads();  // colsum
 
-  constexpr float kScale = BITS == 8 ? 1.0f : float(1 << BITS);  // sc / gamma per unit sc
+  // sc / gamma per unit sc: codes enter as 1 + q 2^-b (6 bits: 1 + q 2^-7), 8-bit codes as q
+  constexpr float kScale = BITS == 8 ? 1.0f : (BITS == 6 ? 128.0f : float(1 << BITS));
   // code_frag's constants, opaque to constant folding so that they stay in VGPRs
-  uint32_t one = 0x3F803F80u, fmask = BITS == 2 ? 0x00600060u : 0x00780078u;
+  uint32_t one = 0x3F803F80u,
+           fmask = BITS == 2 ? 0x00600060u : (BITS == 3 ? 0x00700070u : (BITS == 6 ? 0x003F003Fu : 0x00780078u));
   asm volatile("" : "+v"(one), "+v"(fmask));
   for (int t = tb; t < te; ++t) {
     const int P = (t - tb) & 1;
