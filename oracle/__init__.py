@@ -379,3 +379,30 @@ def spectral_stats(X: np.ndarray, G: np.ndarray, s: int, Tb: int = 16, tau: floa
         lf = float((energy[l] * rho).sum()) / (tot + eps)
         stats[l] = (lf, lsum / max(count, 1), 1.0 - lf, tot)
     return stats, energy
+
+
+# ------------------------------------------------------------------------------------------
+# decode-phase attention over a compressed cache (the consumer of the decoded history)
+# ------------------------------------------------------------------------------------------
+
+def attend(codec: Codec, G: np.ndarray, kcache: dict, vcache: dict, q: np.ndarray, lens, scale: float) -> np.ndarray:
+    """Single-query attention of every query head over the decoded K / V caches, binary64:
+    q [L][B][Hq][d] (Hq a multiple of the H cached heads, query head j reading KV head
+    j // (Hq / H)); batch row b attends to positions [0, lens[b]).  The caches decode with
+    kv_decode (binary32 X_hat = G^T Z_hat), then o = softmax(scale q K_hat^T) V_hat."""
+    L_, B, Hq, d = q.shape
+    H = kcache["codes"].shape[2]
+    grp = Hq // H
+    Tmax = int(max(lens))
+    Kh = kv_decode(codec, 0, G, kcache, 0, Tmax, lens=lens, out_bf16=False).astype(np.float64)
+    Vh = kv_decode(codec, 1, G, vcache, 0, Tmax, lens=lens, out_bf16=False).astype(np.float64)
+    out = np.zeros((L_, B, Hq, d))
+    for l in range(L_):
+        for b in range(B):
+            n = int(lens[b])
+            for j in range(Hq):
+                h = j // grp
+                s = scale * (Kh[l, b, h, :n] @ q[l, b, j].astype(np.float64))
+                p = np.exp(s - s.max())
+                out[l, b, j] = (p / p.sum()) @ Vh[l, b, h, :n]
+    return out

@@ -445,3 +445,49 @@ def test_spectral_energy_is_preserved_by_gauge_and_dct():
         assert abs(st[l, 3] - float((x[l] ** 2).sum())) <= 2e-6 * st[l, 3]
         assert abs(en[l].sum() - st[l, 3]) <= 1e-9 * st[l, 3]
         assert 0.0 < st[l, 0] < 1.0 and st[l, 1] > 0.0
+
+
+# ------------------------------------------------------------------------------------------
+# attention over the decoded cache
+# ------------------------------------------------------------------------------------------
+def test_attend_over_error_free_cache_is_plain_attention():
+    """Passthrough backend: the decoded cache is X to the gauge's rounding, so the oracle's
+    attention equals torch's scaled-dot-product attention on X (binary64)."""
+    import torch
+    L, B, H, grp, T, d = 1, 2, 2, 3, 40, 64
+    w, K, V = _tensor(T, d=d, B=B, H=H)
+    G = O.gauge_make(O.GAUGE_HAAR, L, H, d, 16, seed=31)
+    pc = O.Codec(backend=O.PASSTHROUGH)
+    kc, _ = O.kv_encode(pc, 0, K, G, T_cap=T)
+    vc, _ = O.kv_encode(pc, 1, V, G, T_cap=T)
+    rng = np.random.default_rng(5)
+    q = rng.standard_normal((L, B, H * grp, d)).astype(np.float32)
+    lens = [T, 23]
+    got = O.attend(pc, G, kc, vc, q, lens, 1 / np.sqrt(d))
+    x = lambda a: torch.from_numpy((a.astype(np.uint32) << 16).view(np.float32).astype(np.float64))
+    Kx, Vx = x(K), x(V)
+    for b in range(B):
+        n = lens[b]
+        qq = torch.from_numpy(q[0, b].astype(np.float64))[:, None, :]            # [Hq][1][d]
+        kk = Kx[0, b].repeat_interleave(grp, dim=0)[:, :n]                          # [Hq][n][d]
+        vv = Vx[0, b].repeat_interleave(grp, dim=0)[:, :n]
+        ref = torch.nn.functional.scaled_dot_product_attention(qq, kk, vv, scale=1 / np.sqrt(d))[:, 0]
+        np.testing.assert_allclose(got[0, b], ref.numpy(), rtol=0, atol=1e-5)
+
+
+def test_attend_closed_forms():
+    """Equal keys give equal weights (the output is the mean of the decoded values); a single
+    position gives its decoded value."""
+    L, B, H, T, d = 1, 1, 2, 32, 64
+    G = O.gauge_make(O.GAUGE_HAAR, L, H, d, 32, seed=32)
+    codec = O.Codec(backend=O.BLOCK_UNIFORM, bits=4, block_c=32)
+    w, _, V = _tensor(T, d=d, B=B, H=H)
+    K = np.ascontiguousarray(np.repeat(V[:, :, :, :1], T, axis=3))          # one key repeated
+    kc, _ = O.kv_encode(codec, 0, K, G, T_cap=T)
+    vc, _ = O.kv_encode(codec, 1, V, G, T_cap=T)
+    q = np.random.default_rng(6).standard_normal((L, B, H, d)).astype(np.float32)
+    Vh = O.kv_decode(codec, 1, G, vc, 0, T, out_bf16=False).astype(np.float64)
+    got = O.attend(codec, G, kc, vc, q, [T], 0.125)
+    np.testing.assert_allclose(got[0, 0], Vh[0, 0].mean(axis=1), rtol=0, atol=1e-12)
+    got1 = O.attend(codec, G, kc, vc, q, [1], 0.125)
+    np.testing.assert_allclose(got1[0, 0], Vh[0, 0, :, 0], rtol=0, atol=1e-12)
