@@ -228,6 +228,33 @@ size_t spectral_workspace_bytes(cg_gauge_shape shp, int32_t block_t);
 int32_t kv_spectral_stats(int32_t s, const cg_kv_view* X, const void* G_dev, cg_gauge_shape shp, int32_t block_t,
                           float tau, void* workspace, double* stats, double* energy, void* stream);
 
+/* Bytes of the device workspace kv_attend needs for nl layers, B batch rows, Hq query heads
+ * and caches of capacity T_cap (0: no workspace needed, or invalid arguments). */
+size_t attend_workspace_bytes(cg_gauge_shape shp, int32_t nl, int32_t B, int32_t Hq, int32_t T_cap);
+
+/* Decode-phase attention over the compressed caches, with the inverse gauge of section 3
+ * folded into the consumer instead of decoding Xhat (the paper notes that recovery can be
+ * folded into downstream operations; it times explicit recovery).  For layers [l0, l1), batch
+ * row b and query head j (KV head h = j / (Hq / H), grouped-query attention):
+ *     o = softmax(scale q Khat^T) Vhat  over the positions [0, n_b) the row holds,
+ * with Khat, Vhat the caches as kv_decode would return them in binary32.  Computed as
+ * s_t = (scale G_K q) . zhat^K_t and o = G_V^T sum_t p_t zhat^V_t (KIVI window and staged tile
+ * tokens enter raw), all in binary32; the cached codes are read once and nothing of size T is
+ * written.
+ * q, out: views [l1 - l0][B][Hq][1][d] (bf16 or binary32; Hq a positive multiple of shp.H);
+ * view layer i is cache layer l0 + i.  kc, vc: the K and V caches (same T_cap).  lens: device
+ * int32 [B] with n_b = lens[b] (a KIVI or tile cache then quantises the positions a cache of
+ * n_b tokens quantises; rows with lens[b] outside [0, T_cap] set CG_FLAG_POS_RANGE and attend
+ * to nothing), or NULL: every row holds kc->len (= vc->len) positions.  A row with no positions
+ * gets a zero output.  workspace: caller-owned device buffer of
+ * attend_workspace_bytes(shp, l1 - l0, B, Hq, T_cap) bytes, 16-byte aligned (may be NULL when
+ * that is 0); calls sharing one workspace on different streams race.
+ * Errors: CG_ERR_ARG, CG_ERR_SHAPE, CG_ERR_ALIGN, CG_ERR_UNSUPPORTED, CG_ERR_CAPACITY,
+ * CG_ERR_DEVICE. */
+int32_t kv_attend(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* kc, const cg_cache* vc,
+                  const void* G_dev, cg_gauge_shape shp, const cg_codec* codec, const int32_t* lens, float scale,
+                  const cg_kv_view* out, void* workspace, int32_t* err_flag, void* stream);
+
 /* Device self-test of the two binary32 steps of the quantiser the kernels compute without a
  * division (section 4.3 block range; the oracle divides): which = 0 compares the reciprocal
  * of every positive finite binary16 scale with correctly rounded 1/s; which = 1 compares the

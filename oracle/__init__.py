@@ -389,17 +389,24 @@ def attend(codec: Codec, G: np.ndarray, kcache: dict, vcache: dict, q: np.ndarra
     """Single-query attention of every query head over the decoded K / V caches, binary64:
     q [L][B][Hq][d] (Hq a multiple of the H cached heads, query head j reading KV head
     j // (Hq / H)); batch row b attends to positions [0, lens[b]).  The caches decode with
-    kv_decode (binary32 X_hat = G^T Z_hat), then o = softmax(scale q K_hat^T) V_hat."""
+    kv_decode (binary32 X_hat = G^T Z_hat), then o = softmax(scale q K_hat^T) V_hat.  A row
+    with no positions (lens[b] = 0) has an empty softmax; its output is taken as zero."""
+    if not np.issubdtype(q.dtype, np.floating):
+        raise TypeError("attend takes query values (a floating-point array), not bf16 bit patterns")
     L_, B, Hq, d = q.shape
     H = kcache["codes"].shape[2]
     grp = Hq // H
     Tmax = int(max(lens))
+    if Tmax == 0:
+        return np.zeros((L_, B, Hq, d))
     Kh = kv_decode(codec, 0, G, kcache, 0, Tmax, lens=lens, out_bf16=False).astype(np.float64)
     Vh = kv_decode(codec, 1, G, vcache, 0, Tmax, lens=lens, out_bf16=False).astype(np.float64)
     out = np.zeros((L_, B, Hq, d))
     for l in range(L_):
         for b in range(B):
             n = int(lens[b])
+            if n == 0:
+                continue
             for j in range(Hq):
                 h = j // grp
                 s = scale * (Kh[l, b, h, :n] @ q[l, b, j].astype(np.float64))

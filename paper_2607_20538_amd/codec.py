@@ -24,7 +24,8 @@ PASSTHROUGH, BLOCK_UNIFORM, KIVI = 0, 1, 2
 DTYPE_BF16, DTYPE_F32 = 0, 1
 
 EXPORTS = ["cg_status_str", "gauge_device_bytes", "gauge_make", "cache_bytes", "kv_encode", "kv_decode",
-           "kv_append_step", "spectral_workspace_bytes", "kv_spectral_stats", "cg_selftest"]
+           "kv_append_step", "spectral_workspace_bytes", "kv_spectral_stats", "attend_workspace_bytes", "kv_attend",
+           "cg_selftest"]
 
 
 class GaugeShape(C.Structure):
@@ -85,6 +86,11 @@ def lib() -> C.CDLL:
         L.spectral_workspace_bytes.restype = C.c_size_t
         L.kv_spectral_stats.argtypes = [i32, C.POINTER(KvView), p, GaugeShape, i32, C.c_float, p, p, p, p]
         L.kv_spectral_stats.restype = i32
+        L.attend_workspace_bytes.argtypes = [GaugeShape, i32, i32, i32, i32]
+        L.attend_workspace_bytes.restype = C.c_size_t
+        L.kv_attend.argtypes = [i32, i32, C.POINTER(KvView), C.POINTER(CacheStruct), C.POINTER(CacheStruct), p,
+                                GaugeShape, C.POINTER(CodecStruct), p, C.c_float, C.POINTER(KvView), p, p, p]
+        L.kv_attend.restype = i32
         L.cg_selftest.argtypes = [i32, p, p]
         L.cg_selftest.restype = i32
         _lib = L
@@ -243,3 +249,17 @@ def kv_spectral_stats(s: int, X, G_dev, shp: GaugeShape, block_t: int, tau: floa
     rc = lib().kv_spectral_stats(s, C.byref(v), _ptr(G_dev), shp, block_t, tau, _ptr(workspace), _ptr(stats),
                                  _ptr(energy), _stream(stream))
     _check("kv_spectral_stats", rc)
+
+
+def attend_workspace_bytes(shp: GaugeShape, nl: int, B: int, Hq: int, T_cap: int) -> int:
+    return int(lib().attend_workspace_bytes(shp, nl, B, Hq, T_cap))
+
+
+def kv_attend(l0: int, l1: int, q, kc: Cache, vc: Cache, G_dev, shp: GaugeShape, codec: Codec, lens, scale: float,
+              out, workspace=None, err_flag=None, stream=None):
+    """Decode-phase attention of q [l1-l0][B][Hq][1][d] over the compressed caches into out (same
+    shape); lens: device int32 [B] positions per row, or None for the caches' len."""
+    qv, ov, cs, kcs, vcs = view(q), view(out), codec.struct(), kc.struct(), vc.struct()
+    rc = lib().kv_attend(l0, l1, C.byref(qv), C.byref(kcs), C.byref(vcs), _ptr(G_dev), shp, C.byref(cs), _ptr(lens),
+                         float(scale), C.byref(ov), _ptr(workspace), _ptr(err_flag), _stream(stream))
+    _check("kv_attend", rc)

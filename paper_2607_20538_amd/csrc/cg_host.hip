@@ -1,6 +1,7 @@
 // Host side of the C ABI: argument validation, gauge construction (gauge_make), buffer
 // sizing and dispatch of the encode / decode / rolling-append kernels.
 #include <math.h>
+#include <algorithm>
 #include <stdlib.h>
 #include <string.h>
 
@@ -339,6 +340,18 @@ CacheDev cache_dev(const cg_cache* k) {
   return d;
 }
 
+// A query or output view of kv_attend: [nl][B][Hq][1][d], Hq a multiple of the KV heads.
+int32_t check_qview(const cg_kv_view* v, const cg_gauge_shape& s, int L) {
+  if (!v || !v->ptr) return CG_ERR_ARG;
+  if (v->dtype != CG_DTYPE_BF16 && v->dtype != CG_DTYPE_F32) return CG_ERR_ARG;
+  if (v->L != L || v->d != s.d || v->B <= 0 || v->T != 1 || v->H < s.H || v->H % s.H) return CG_ERR_SHAPE;
+  if (!aligned16(v->ptr)) return CG_ERR_ALIGN;
+  const int64_t unit = v->dtype == CG_DTYPE_BF16 ? 8 : 4;
+  if (v->stride_l % unit || v->stride_b % unit || v->stride_h % unit || v->stride_t % unit) return CG_ERR_ALIGN;
+  if (v->stride_l < 0 || v->stride_b < 0 || v->stride_h < 0 || v->stride_t < 0) return CG_ERR_ARG;
+  return CG_OK;
+}
+
 int kivi_tq(int T, const cg_codec* c) {
   return T < c->residual ? 0 : ((T - c->residual) / c->key_tokens) * c->key_tokens;
 }
@@ -606,6 +619,55 @@ int32_t kv_spectral_stats(int32_t s, const cg_kv_view* X, const void* G_dev, cg_
   if (X->T > 0 && !X->ptr) return CG_ERR_ARG;
   hipError_t e = launch_spectral(s, view_dev(X), gauge_dev(G_dev, shp), block_t, tau, workspace, stats, energy,
                                  force_generic(), static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
+}
+
+size_t attend_workspace_bytes(cg_gauge_shape shp, int32_t nl, int32_t B, int32_t Hq, int32_t T_cap) {
+  if (check_shape(shp) != CG_OK || nl <= 0 || B <= 0 || T_cap <= 0 || Hq < shp.H || Hq % shp.H) return 0;
+  return attend_plan(nl, B, shp.H, Hq, shp.d, T_cap).ws_bytes;
+}
+
+int32_t kv_attend(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* kc, const cg_cache* vc,
+                  const void* G_dev, cg_gauge_shape shp, const cg_codec* codec, const int32_t* lens, float scale,
+                  const cg_kv_view* out, void* workspace, int32_t* err_flag, void* stream) {
+  int32_t rc = check_shape(shp);
+  if (rc != CG_OK) return rc;
+  if (!G_dev || l0 < 0 || l1 <= l0 || l1 > shp.L || !isfinite(scale)) return CG_ERR_ARG;
+  if (!aligned16(G_dev)) return CG_ERR_ALIGN;
+  if (lens && (reinterpret_cast<uintptr_t>(lens) & 3u)) return CG_ERR_ALIGN;
+  if ((rc = check_codec(codec, shp.d)) != CG_OK) return rc;
+  const int nl = l1 - l0;
+  if ((rc = check_qview(q, shp, nl)) != CG_OK) return rc;
+  if ((rc = check_qview(out, shp, nl)) != CG_OK) return rc;
+  if (out->B != q->B || out->H != q->H) return CG_ERR_SHAPE;
+  const int B = q->B;
+  if ((rc = check_cache(kc, codec, shp, B)) != CG_OK) return rc;
+  if ((rc = check_cache(vc, codec, shp, B)) != CG_OK) return rc;
+  if (kc->T_cap != vc->T_cap) return CG_ERR_SHAPE;
+  if (!lens && (kc->len < 0 || kc->len > kc->T_cap || vc->len != kc->len)) return CG_ERR_CAPACITY;
+  const AttendPlan cap = attend_plan(nl, B, shp.H, q->H, shp.d, kc->T_cap);
+  if (cap.ws_bytes && (!workspace || !aligned16(workspace))) return workspace ? CG_ERR_ALIGN : CG_ERR_ARG;
+  if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
+  // rows of known length split over that length; device lengths over the capacity
+  const AttendPlan p = lens ? cap : attend_plan(nl, B, shp.H, q->H, shp.d, std::max(1, kc->len));
+  AttendDev a;
+  a.q = view_dev(q);
+  a.o = view_dev(out);
+  a.kc = cache_dev(kc);
+  a.vc = cache_dev(vc);
+  a.l0 = l0;
+  a.Hq = q->H;
+  a.grp = q->H / shp.H;
+  a.lens = lens;
+  a.len = kc->len;
+  a.scale = scale;
+  a.nsplit = p.nsplit;
+  a.chunk = p.chunk;
+  a.nqc = p.nqc;
+  a.part = static_cast<float*>(workspace);
+  a.err = err_flag;
+  hipError_t e = launch_attend(a, gauge_dev(G_dev, shp), codec_dev(codec), force_generic(),
+                               static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
 }
 

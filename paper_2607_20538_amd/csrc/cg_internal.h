@@ -109,6 +109,30 @@ SpecLayout spec_layout(const cg_gauge_shape& s, int Tb);
 hipError_t launch_spectral(int s, const ViewDev& X, const GaugeDev& G, int Tb, float tau, void* ws, double* stats,
                            double* energy, bool force_generic, hipStream_t st);
 
+// Decode-phase attention over the compressed caches (inverse gauge folded into the query and
+// the output).  Query heads j = h * grp + jj of KV head h read that head's K / V caches.
+struct AttendDev {
+  ViewDev q, o;          // [nl][B][Hq][1][d]
+  CacheDev kc, vc;
+  int l0, Hq, grp;       // cache layer of view layer 0, query heads, query heads per KV head
+  const int* lens;       // device [B] positions per batch row, or nullptr: every row holds `len`
+  int len;
+  float scale;
+  int nsplit, chunk;     // token splits per row and tokens per split (a multiple of 64)
+  int nqc;               // query chunks of at most 8 heads per workgroup
+  float* part;           // partial results [nl][B][Hq][nsplit][2 + 2d] when nsplit > 1
+  int* err;
+};
+struct AttendPlan {
+  int nsplit = 1, chunk = 64, nqc = 1;
+  size_t ws_bytes = 0;
+};
+// Split plan of a call covering `span` positions per row (the same rule sizes the workspace
+// from the capacity, so a plan for span <= T_cap never needs more than that workspace).
+AttendPlan attend_plan(int nl, int B, int H, int Hq, int d, int span);
+hipError_t launch_attend(const AttendDev& a, const GaugeDev& G, const CodecDev& c, bool force_generic,
+                         hipStream_t st);
+
 // Device self-test of the quantiser's division-free steps (which: 0 reciprocal, 1 division).
 hipError_t launch_selftest(int which, unsigned long long* bad, hipStream_t st);
 

@@ -10,7 +10,9 @@ regenerated on its own):
   * keys:    x = N(0, 1) * c[l, h, channel], with c = exp(sigma * N(0, 1)) drawn once per
              (l, h, channel) and the first k channels of a seeded permutation of the
              channels multiplied by m (outlier channels);
-  * bf16 caches round the float32 draws to bfloat16 with round-to-nearest-even.
+  * bf16 caches round the float32 draws to bfloat16 with round-to-nearest-even;
+  * decode-phase queries (attention over the cache): q ~ N(0, 1) per element, one vector per
+    (layer, batch row, query head).
 Streams are numpy Philox generators keyed through a SeedSequence of
 (seed, purpose, s, l, b, h).
 """
@@ -21,7 +23,7 @@ import os
 
 import numpy as np
 
-TAG_DATA, TAG_SCALE, TAG_NEW = 1, 2, 3
+TAG_DATA, TAG_SCALE, TAG_NEW, TAG_QUERY = 1, 2, 3, 4
 
 
 @dataclasses.dataclass(frozen=True)
@@ -159,6 +161,19 @@ def new_tokens(w: Workload, s: int, step: int, L: int | None = None, B: int | No
         for b in range(B):
             for h in range(H):
                 f[li, b, h] = kv_slice(w.data_seed, s, li, b, h, 1, w.d, w.keys, t_offset=step, tag=TAG_NEW)[0]
+    if w.dtype == "bf16":
+        return round_bf16_bits(f)
+    return f
+
+
+def queries(w: Workload, Hq: int, L: int | None = None, B: int | None = None, step: int = 0) -> np.ndarray:
+    """Decode-phase queries [L][B][Hq][d] (uint16 bf16 bits, or float32) of rolling step `step`."""
+    L = w.L if L is None else L
+    B = w.B if B is None else B
+    f = np.empty((L, B, Hq, w.d), dtype=np.float32)
+    for li in range(L):
+        for b in range(B):
+            f[li, b] = _rng(w.data_seed, TAG_QUERY, step, li, b, 0).standard_normal((Hq, w.d), dtype=np.float32)
     if w.dtype == "bf16":
         return round_bf16_bits(f)
     return f

@@ -205,6 +205,37 @@ def test_spectral_stats_reject_invalid_arguments():
     assert call(shp=cg.shape(1, 2, 64, 48)) == cg.CG_ERR_UNSUPPORTED
 
 
+def test_attend_rejects_invalid_arguments():
+    shp = cg.shape(2, 2, 64, 16)
+    q = _fake_view(L=1, H=4, T=1, strides=(256, 256, 64, 64))
+    k = _fake_cache(L=2, T_cap=64, len_=32)
+    assert cg.attend_workspace_bytes(shp, 1, 1, 4, 64) >= 0
+    assert cg.attend_workspace_bytes(shp, 1, 1, 3, 64) == 0      # Hq not a multiple of H
+    assert cg.attend_workspace_bytes(shp, 1, 1, 4, 4096) > 0      # few rows: the positions are split
+    f = cg.lib().kv_attend
+    ok = dict(l0=0, l1=1, q=q, kc=k, vc=k, codec=BU, lens=None, scale=0.125, out=q, ws=0x70000)
+    def call(**kw):
+        a = dict(ok, **kw)
+        cs = a["codec"].struct()
+        return f(a["l0"], a["l1"], C.byref(a["q"]), C.byref(a["kc"]), C.byref(a["vc"]), a.get("gdev", 0x50000),
+                 a.get("shp", shp), C.byref(cs), a["lens"], a["scale"], C.byref(a["out"]), a["ws"], None, None)
+    assert call(l1=3) == cg.CG_ERR_ARG
+    assert call(l0=1, l1=1) == cg.CG_ERR_ARG
+    assert call(scale=float("inf")) == cg.CG_ERR_ARG
+    assert call(gdev=0x50008) == cg.CG_ERR_ALIGN
+    assert call(lens=0x60002) == cg.CG_ERR_ALIGN
+    assert call(q=_fake_view(L=1, H=3, T=1)) == cg.CG_ERR_SHAPE                       # Hq % H
+    assert call(q=_fake_view(L=1, H=4, T=2)) == cg.CG_ERR_SHAPE                       # one query position
+    assert call(out=_fake_view(L=1, H=2, T=1)) == cg.CG_ERR_SHAPE                     # out heads != q heads
+    assert call(vc=_fake_cache(L=2, T_cap=32, len_=32)) == cg.CG_ERR_SHAPE            # capacities differ
+    assert call(kc=_fake_cache(L=2, T_cap=64, len_=65)) == cg.CG_ERR_CAPACITY         # len beyond capacity
+    assert call(vc=_fake_cache(L=2, T_cap=64, len_=16)) == cg.CG_ERR_CAPACITY         # K and V lengths differ
+    assert call(codec=cg.Codec(cg.BLOCK_UNIFORM, 5, 32)) == cg.CG_ERR_UNSUPPORTED
+    big = _fake_cache(L=2, T_cap=4096, len_=4096)
+    assert call(kc=big, vc=big, ws=None) == cg.CG_ERR_ARG                             # workspace needed
+    assert call(kc=big, vc=big, ws=0x70008) == cg.CG_ERR_ALIGN
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(cg, "LIB_PATH", str(tmp_path / "missing.so"))
     monkeypatch.setattr(cg, "_lib", None)
