@@ -36,7 +36,7 @@ def parse():
                     help="HBM traffic per launch measured with rocprofv3 counters (optional)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the timed region, run one plain 512 MiB device copy (counter calibration)")
-    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral"]),
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral", "attend"]),
                     help="llama8b (default) prints the headline line; the others print per-kernel timings of "
                          "the KIVI, rolling-step and 27B-sweep workloads")
     return ap.parse_args()
@@ -122,7 +122,7 @@ def other_workload(name, steps, warmup):
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral") else name]
+    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral") else ("rolling" if name == "attend" else name)]
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     out = {"workload": name, "shape": {"L": w.L, "B": w.B, "H": w.H, "T": w.T, "d": w.d}, "steps": steps}
 
@@ -198,6 +198,58 @@ def other_workload(name, steps, warmup):
                 torch.cuda.empty_cache()
             rows.append(row)
         out["runs"] = rows
+    elif name == "attend":
+        # the rolling step with the history consumed by fused decode-phase attention instead of
+        # being decoded to bf16: append one token per (layer, b, h), then attention of the
+        # grp = 4 query heads of every KV head (32 query heads over 8 KV heads) over the history
+        grp = 4
+        shp = cg.shape(w.L, w.H, w.d, w.g)
+        codec = cg.Codec(cg.BLOCK_UNIFORM, w.bits, w.block_c)
+        Gd = cg.alloc_gauge(shp)
+        cg.gauge_make(cg.GAUGE_HAAR, shp, seed=w.gauge_seed, G_host=None, G_dev=Gd)
+        T_cap = w.T + warmup + 2 * steps + 1
+        caches, news = [], []
+        for s in (0, 1):
+            X = layer_view(s)
+            c = cg.Cache(codec, s, w.L, w.B, w.H, T_cap, w.d)
+            cg.kv_encode(s, X, Gd, shp, codec, c, err_flag=err, stream=stream.cuda_stream)
+            torch.cuda.synchronize()
+            del X
+            caches.append(c)
+            nt = synth.kv_tensor(w, s, L=1, T=1, t_offset=w.T)
+            nt = torch.from_numpy(nt.view(np.int16)).view(torch.bfloat16).cuda()
+            news.append(nt.expand(w.L, w.B, w.H, 1, w.d))
+        q = torch.from_numpy(synth.queries(w, w.H * grp).view(np.int16)).view(torch.bfloat16).cuda()
+        q = q.reshape(w.L, w.B, w.H * grp, 1, w.d)
+        o = torch.empty((w.L, w.B, w.H * grp, 1, w.d), dtype=torch.bfloat16, device="cuda")
+        ws = torch.empty(max(16, cg.attend_workspace_bytes(shp, w.L, w.B, w.H * grp, T_cap)), dtype=torch.uint8,
+                         device="cuda")
+        pos = torch.full((w.B,), w.T, dtype=torch.int32, device="cuda")
+        lens = pos + 1
+        scale = 1.0 / float(np.sqrt(w.d))
+
+        def attend():
+            cg.kv_attend(0, w.L, q, caches[0], caches[1], Gd, shp, codec, lens, scale, o, ws, err_flag=err,
+                         stream=stream.cuda_stream)
+
+        def step():
+            cg.kv_append_step(0, w.L, news[0], news[1], pos, Gd, shp, codec, caches[0], caches[1], None, None,
+                              err_flag=err, stream=stream.cuda_stream)
+            attend()
+            pos.add_(1)
+            lens.add_(1)
+
+        ms = _timed(step, steps, warmup, stream)
+        # attention alone over the same history length (the positions the last step held)
+        ms_att = _timed(attend, steps, 0, stream)
+        nc, ns, _ = caches[0].nbytes
+        held = int(lens[0].item())
+        cache_bytes = 2 * (nc + ns) * held // T_cap          # K and V codes + side words read
+        out["step_ms"] = round(ms, 3)
+        out["attend_ms"] = round(ms_att, 3)
+        out["history_tokens"] = held
+        out["query_heads"] = w.H * grp
+        out["attend_GBps"] = round(cache_bytes / ms_att / 1e6, 1)
     else:  # rolling decode step
         shp = cg.shape(w.L, w.H, w.d, w.g)
         codec = cg.Codec(cg.BLOCK_UNIFORM, w.bits, w.block_c)

@@ -15,9 +15,11 @@
 // maximum, normaliser and unnormalised accumulators, and a combine kernel merges the splits and
 // applies G_V^T.  A row with no positions gets a zero output.
 #include <algorithm>
+#include <type_traits>
 
 #include "cg_internal.h"
 #include "cg_device.h"
+#include "cg_mfma_util.h"
 
 namespace cg {
 
@@ -94,7 +96,7 @@ __device__ void finalize_rows(const AttendDev& a, const GaugeDev& G, const float
     const float* z = acc + jj * d + r * g;
     float x = 0.0f;
     for (int j = 0; j < g; ++j) x = fmaf(Gc[size_t(j) * g], z[j], x);
-    x += accr[jj * d + i];
+    if (accr) x += accr[jj * d + i];
     const float ls = lsum[jj];
     const float o = ls > 0.0f ? x / ls : 0.0f;
     const size_t off = size_t(lv) * a.o.sl + size_t(b) * a.o.sb + size_t(hq0 + jj) * a.o.sh + i;
@@ -348,6 +350,490 @@ __global__ __launch_bounds__(kAThreads) void att_combine(AttendDev a, GaugeDev G
   finalize_rows(a, G, macc, maccr, mm + kJQ, nj, lv, b, h, hq0);
 }
 
+// ------------------------------------------------------------------------------------------
+// matrix-core kernel: bf16-free block-uniform caches with one range per token and block
+// (block_t = 1), d = 128, blocks of 64 or 128 channels (NBLK = 2 or 1 blocks per row)
+// ------------------------------------------------------------------------------------------
+// Both contractions run on v_mfma_f32_16x16x32_bf16 with the codes entering as the exact bf16
+// values B = 1 + q 2^-k (code_frag; 8-bit codes as q), so zhat = mn + sc k (B - 1) and
+//   scores  s_t = sum_blk [ (mn - k sc) Q_blk + k sc (qt . B_t)_blk ],  Q_blk = sum_blk qt
+//   values  sum_t p_t zhat_t,c = sum_t (p mn - w)_t + sum_t w_t B_t,c,  w_t = k p_t sc_t
+// where the binary32 operands qt (scale G_K q) and w enter as two bf16 planes hi + lo and the
+// offset terms Q and sum w are formed from the same planes, so the split only perturbs them by
+// 2^-17 relative (what multiplies B - 1, i.e. the code itself).
+//   scores: A = qt planes, rows (query j, block, plane), block rows zero outside their block;
+//           B = the codes of 16 tokens (lane = token n, lane group = 32-channel region);
+//           D lane (token n, group) holds the rows of query group (NBLK = 2) or of queries
+//           2 group, 2 group + 1 (NBLK = 1), folded in-lane with the token's side words.
+//   values: A = w planes, rows as above (w of the row's block), K = 32 tokens;
+//           B = for lane (column c, group) the codes of channel 8c + nt of tokens
+//           8 group .. 8 group + 7 (N-tile nt): each lane reads its 8-code chunk of 8 rows and
+//           builds the 8 N-tile fragments from them, a transpose done in registers.
+// A wave takes 32 positions per step (steps w, w + 4, ... of the split); the running maximum
+// of every query lives in the lanes of its D rows, the per-step probabilities and value side
+// words go through a small per-wave LDS buffer to the lanes building the value A operand.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4_t mfma16(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_mov<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp_mov<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp_mov<0x124>(v));  // row_ror:4
+  return fmaxf(v, dpp_mov<0x128>(v));  // row_ror:8
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_mov<0xB1>(v);
+  v += dpp_mov<0x4E>(v);
+  v += dpp_mov<0x124>(v);
+  return v + dpp_mov<0x128>(v);
+}
+
+// Channel (within a lane's 32-channel region) of element e of K-step u, in code_frag's order.
+template <int BITS>
+__device__ __forceinline__ int frag_chan(int u, int e) {
+  if constexpr (BITS == 4 || BITS == 6) return 8 * u + ((e & 1) ? 4 : 0) + (e >> 1);
+  else if constexpr (BITS == 2 || BITS == 3) return 16 * (u >> 1) + 4 * (u & 1) + ((e & 1) ? 8 : 0) + (e >> 1);
+  else return 8 * u + e;
+}
+
+// The 8-code chunk of channels 8c .. 8c + 7 of a packed row (BITS bytes from byte c BITS) from
+// the dword holding its first byte (w0) and the next one (w1), its first bit at `sh` of w0:
+// lo / hi = the chunk's bytes 0..3 / 4..7.
+template <int BITS>
+__device__ __forceinline__ void vchunk(uint32_t w0, uint32_t w1, uint32_t sh, uint32_t& lo, uint32_t& hi) {
+  if constexpr (BITS == 4) {
+    lo = w0;
+    hi = 0u;
+  } else if constexpr (BITS == 2) {
+    lo = w0 >> sh;
+    hi = 0u;
+  } else if constexpr (BITS == 8) {
+    lo = w0;
+    hi = w1;
+  } else {
+    lo = __builtin_amdgcn_alignbit(w1, w0, sh);
+    hi = w1 >> sh;
+  }
+}
+
+// Value B fragment of N-tile k: code k of the 8 tokens' chunks as bf16 1 + q 2^-BITS (8 bits: q
+// itself), token pair (2i, 2i + 1) in dword i.  4 and 6 bits: one byte permute puts the two
+// tokens' bytes holding code k 16 bits apart, one shift aligns the code with the mantissa.
+template <int BITS>
+__device__ __forceinline__ bf16x8_t vfrag(const uint32_t (&lo)[8], const uint32_t (&hi)[8], int k, uint32_t one) {
+  constexpr uint32_t M = (1u << BITS) - 1u;
+  u32x4_t f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t a0 = lo[2 * i], a1 = lo[2 * i + 1];
+    if constexpr (BITS == 4) {
+      // code k in byte k/2 (low nibble for even k)
+      const uint32_t b = uint32_t(k >> 1);
+      const uint32_t x = __builtin_amdgcn_perm(a1, a0, b | (0x0Cu << 8) | ((b + 4) << 16) | (0x0Cu << 24));
+      f[i] = (k & 1) ? (((x >> 1) & 0x00780078u) | one) : (((x << 3) & 0x00780078u) | one);
+    } else if constexpr (BITS == 6) {
+      const int bit = 6 * k, ob = bit >> 3, r = bit & 7;
+      uint32_t x;
+      if (ob <= 2 || (ob == 3 && r == 0)) {
+        // codes 0..4: bytes ob, ob + 1 (or byte 3 alone) of lo
+        const uint32_t o0 = uint32_t(ob), o1 = uint32_t(min(ob + 1, 3));
+        x = __builtin_amdgcn_perm(a1, a0, o0 | (o1 << 8) | ((o0 + 4) << 16) | ((o1 + 4) << 24));
+      } else if (ob == 3) {
+        // code 5 straddles byte 3 of lo and byte 0 of hi: bytes 3..6 of the chunk first
+        const uint32_t m0 = __builtin_amdgcn_alignbit(hi[2 * i], a0, 24);
+        const uint32_t m1 = __builtin_amdgcn_alignbit(hi[2 * i + 1], a1, 24);
+        x = __builtin_amdgcn_perm(m1, m0, 0x05040100u);
+      } else {
+        // codes 6, 7: bytes ob - 4, ob - 3 of hi
+        const uint32_t h0 = uint32_t(ob - 4), h1 = uint32_t(ob - 3);
+        x = __builtin_amdgcn_perm(hi[2 * i + 1], hi[2 * i], h0 | (h1 << 8) | ((h0 + 4) << 16) | ((h1 + 4) << 24));
+      }
+      // the code sits at bit r of each half: move it to mantissa bits 1..6
+      const uint32_t y = r >= 1 ? (x >> (r - 1)) : (x << 1);
+      f[i] = (y & 0x007E007Eu) | one;
+    } else {
+      const uint64_t c0w = (uint64_t(hi[2 * i]) << 32) | a0, c1w = (uint64_t(hi[2 * i + 1]) << 32) | a1;
+      const uint32_t c0 = uint32_t(c0w >> (BITS * k)) & M, c1 = uint32_t(c1w >> (BITS * k)) & M;
+      if constexpr (BITS == 8) {
+        f[i] = __builtin_amdgcn_perm(__float_as_uint(float(c1)), __float_as_uint(float(c0)), 0x07060302u);
+      } else {
+        f[i] = one | (c0 << (7 - BITS)) | (c1 << (23 - BITS));
+      }
+    }
+  }
+  return as_bf16x8(f);
+}
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// bf16 pair (RN(a), RN(b)), a in the low half (the hardware conversion, round to nearest even)
+__device__ __forceinline__ uint32_t pk_bf16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{a, b}), bf16x2_t));
+}
+
+// bf16 planes of v: hi = RN(v), lo = RN(v - hi)
+__device__ __forceinline__ void split2(float v, uint32_t& hi, uint32_t& lo) {
+  hi = f32_to_bf16_rne(v);
+  lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
+}
+
+template <int BITS, int NBLK>
+__global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G) {
+  constexpr int JQ = 8 / NBLK;                 // query heads per workgroup (16 A rows)
+  constexpr int NQL = 2 / NBLK;                // queries per D lane
+  constexpr int NB = kD / NBLK;                // channels per block
+  constexpr int RB = kD * BITS / 8;            // code bytes per row
+  constexpr float kSK = BITS == 8 ? 1.0f : (BITS == 6 ? 128.0f : float(1 << BITS));  // code_frag scale
+  constexpr float kSV = BITS == 8 ? 1.0f : float(1 << BITS);                           // vfrag scale
+  __shared__ __attribute__((aligned(16))) float qt[JQ][kD];
+  __shared__ __attribute__((aligned(16))) float macc[JQ][kD];
+  __shared__ float qsum[JQ][NBLK];
+  __shared__ __attribute__((aligned(16))) float pbuf[4][JQ][32];
+  __shared__ float abuf[4][JQ];
+  __shared__ __attribute__((aligned(16))) uint32_t vsd[4][NBLK][32];
+  __shared__ float offs[4][16][4];
+  __shared__ float ml[4][2][JQ];
+  __shared__ float mm[2][JQ];
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n = lane & 15, gq = lane >> 4;
+  const int H = a.kc.H, B = a.q.B;
+  const int sp = blockIdx.x;
+  int sv = blockIdx.y;
+  const int qc = sv % a.nqc;
+  sv /= a.nqc;
+  const int h = sv % H, b = (sv / H) % B, lv = sv / (H * B);
+  const int l = lv + a.l0;
+  const int j0 = qc * JQ, nj = min(JQ, a.grp - j0);
+  const int hq0 = h * a.grp + j0;
+  const size_t slc = (size_t(l) * a.kc.B + b) * H + h;
+  const size_t crow = slc * size_t(a.kc.T_cap);
+
+  if (threadIdx.x == 0 && a.lens && sp == 0 && qc == 0 && h == 0 && lv == 0) {
+    const int nn = a.lens[b];
+    if ((nn < 0 || nn > a.kc.T_cap) && a.err) atomicOr(a.err, CG_FLAG_POS_RANGE);
+  }
+  int held = a.lens ? a.lens[b] : a.len;
+  if (held < 0 || held > a.kc.T_cap) held = 0;
+  const int t_begin = sp * a.chunk, t_end = min(held, t_begin + a.chunk);
+
+  // 1. queries: macc <- q, qt <- scale G_K q, qsum <- the per-block sums of its two planes
+  for (int idx = threadIdx.x; idx < JQ * kD; idx += kAThreads) {
+    const int jj = idx / kD, ch = idx % kD;
+    float v = 0.0f;
+    if (jj < nj) {
+      const size_t off = size_t(lv) * a.q.sl + size_t(b) * a.q.sb + size_t(hq0 + jj) * a.q.sh + ch;
+      v = a.q.bf16 ? bf16_to_f32(((const uint16_t*)a.q.ptr)[off]) : ((const float*)a.q.ptr)[off];
+    }
+    macc[jj][ch] = v;
+  }
+  __syncthreads();
+  {
+    const int g = G.g;
+    for (int idx = threadIdx.x; idx < JQ * kD; idx += kAThreads) {
+      const int jj = idx / kD, i = idx % kD;
+      const int r = i / g, ii = i - r * g;
+      const float* Gr = G.f32 + gauge_block(l, 0, h, r, G.H, G.R) * g * g + size_t(ii) * g;
+      float z = 0.0f;
+      for (int j = 0; j < g; ++j) z = fmaf(Gr[j], macc[jj][r * g + j], z);
+      qt[jj][i] = a.scale * z;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < JQ * NBLK) {
+    const int jj = threadIdx.x / NBLK, k = threadIdx.x % NBLK;
+    float acc = 0.0f;
+    for (int ch = k * NB; ch < (k + 1) * NB; ++ch) {
+      uint32_t hi, lo;
+      split2(qt[jj][ch], hi, lo);
+      acc += bf16_to_f32(hi) + bf16_to_f32(lo);
+    }
+    qsum[jj][k] = acc;
+  }
+  __syncthreads();
+
+  // 2. score A fragments: row m = n -> (query, block, plane), region 32 gq
+  bf16x8_t AK[4];
+  {
+    const int j = n / (2 * NBLK), blk = (n / 2) % NBLK, plane = n & 1;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      u32x4_t f = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int ch = 32 * gq + frag_chan<BITS>(u, e);
+        uint32_t hi = 0u, lo = 0u;
+        if (ch / NB == blk) split2(qt[j][ch], hi, lo);
+        f[e >> 1] |= (plane ? lo : hi) << (16 * (e & 1));
+      }
+      AK[u] = as_bf16x8(f);
+    }
+  }
+  // the D rows of this lane: 4 gq + i -> query jr[i], block br[i], plane i & 1
+  float qrow[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = 4 * gq + i;
+    qrow[i] = qsum[m / (2 * NBLK)][(m / 2) % NBLK];
+  }
+  // value A rows: row m = n -> (query jw, block bw, plane pw)
+  const int jw = n / (2 * NBLK), bw = (n / 2) % NBLK, pw = n & 1;
+
+  float mrun[NQL], lp[NQL];
+#pragma unroll
+  for (int qi = 0; qi < NQL; ++qi) {
+    mrun[qi] = -INFINITY;
+    lp[qi] = 0.0f;
+  }
+  f32x4_t accV[8];
+#pragma unroll
+  for (int nt = 0; nt < 8; ++nt) accV[nt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  float offl = 0.0f;
+
+  uint32_t one = 0x3F803F80u,
+           fmask = BITS == 2 ? 0x00600060u : (BITS == 3 ? 0x00700070u : (BITS == 6 ? 0x003F003Fu : 0x00780078u));
+  asm volatile("" : "+v"(one), "+v"(fmask));
+
+  // per-lane constant parts of the addresses (byte offsets from a slice's first row)
+  const uint32_t koff = uint32_t(n) * RB + uint32_t(gq) * BITS * 4;    // key region of token n
+  const uint32_t vcb = uint32_t(n) * BITS;                             // value chunk byte in the row
+  const uint32_t voff = uint32_t(8 * gq) * RB + (vcb & ~3u);           // its first dword, token 8 gq
+  const uint32_t vsh = (vcb & 3u) * 8;                                 // chunk bit offset in that dword
+  const uint8_t* kslice = a.kc.codes + crow * RB;
+  const uint8_t* vslice = a.vc.codes + crow * RB;
+  const uint32_t* ksside = a.kc.side + crow * NBLK;
+  const uint32_t* vsside = a.vc.side + crow * NBLK;
+
+  // One 32-position step; FULL: all 32 positions lie before t_end (no clamping)
+  auto step = [&](int t0, auto fullc) {
+    constexpr bool FULL = decltype(fullc)::value;
+    const int lim = t_end - 1 - t0;  // last valid position offset in the step
+    auto clampt = [&](int x) { return FULL ? x : min(x, lim); };
+    const uint8_t* kb = kslice + size_t(t0) * RB;
+    const uint8_t* vb = vslice + size_t(t0) * RB;
+    // loads: key regions of tokens t0 + 16 sb + n, value chunks of tokens t0 + 8 gq + e
+    uint32_t rk[2][BITS];
+    uint32_t swk[2][NBLK];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+      const uint32_t* src = reinterpret_cast<const uint32_t*>(
+          kb + (FULL ? koff + 16u * sb * RB : uint32_t(clampt(16 * sb + n)) * RB + uint32_t(gq) * BITS * 4));
+#pragma unroll
+      for (int i = 0; i < BITS; ++i) rk[sb][i] = src[i];
+      const uint32_t* sd = ksside + size_t(t0) * NBLK + uint32_t(clampt(16 * sb + n)) * NBLK;
+#pragma unroll
+      for (int k = 0; k < NBLK; ++k) swk[sb][k] = sd[k];
+    }
+    uint32_t vw0[8], vw1[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t* src = reinterpret_cast<const uint32_t*>(
+          vb + (FULL ? voff + uint32_t(e) * RB : uint32_t(clampt(8 * gq + e)) * RB + (vcb & ~3u)));
+      vw0[e] = src[0];
+      // 4-bit chunks are one dword, 2-bit chunks half of one; the others may reach the next
+      // dword, which lies inside the row whenever the chunk needs it (the last chunk of a
+      // 3-bit row does not)
+      if constexpr (BITS == 6 || BITS == 8) vw1[e] = src[1];
+      else if constexpr (BITS == 3) vw1[e] = (n == 15) ? 0u : src[1];
+      else vw1[e] = 0u;
+    }
+    if (lane < 32 * NBLK) {
+      const int k = lane >> 5, t = lane & 31;
+      vsd[w][k][t] = vsside[(size_t(t0) + clampt(t)) * NBLK + k];
+    }
+
+    // scores of the two 16-token halves
+    float s[2][NQL];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+      f32x4_t d = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) d = mfma16(AK[u], code_frag<BITS, BITS>(rk[sb], u, one, fmask), d);
+      float gam[NBLK], bet[NBLK];
+#pragma unroll
+      for (int k = 0; k < NBLK; ++k) {
+        const float mn = f16_bits_to_f32(swk[sb][k] & 0xffffu), sc = f16_bits_to_f32(swk[sb][k] >> 16);
+        gam[k] = kSK * sc;
+        bet[k] = BITS == 8 ? mn : mn - gam[k];
+      }
+      const bool valid = FULL || 16 * sb + n <= lim;
+      if constexpr (NBLK == 2) {
+        const float v = fmaf(gam[0], d[0] + d[1], bet[0] * qrow[0]) + fmaf(gam[1], d[2] + d[3], bet[1] * qrow[2]);
+        s[sb][0] = valid ? v : -INFINITY;
+      } else {
+        s[sb][0] = valid ? fmaf(gam[0], d[0] + d[1], bet[0] * qrow[0]) : -INFINITY;
+        s[sb][1] = valid ? fmaf(gam[0], d[2] + d[3], bet[0] * qrow[2]) : -INFINITY;
+      }
+    }
+    // online softmax (queries of the lane's D rows)
+    float alpha[NQL];
+#pragma unroll
+    for (int qi = 0; qi < NQL; ++qi) {
+      const int j = NBLK == 2 ? gq : 2 * gq + qi;
+      const float mx = row16_max(fmaxf(s[0][qi], s[1][qi]));
+      const float mnew = fmaxf(mrun[qi], mx);
+      alpha[qi] = __expf(mrun[qi] - mnew);
+      const float p0 = __expf(s[0][qi] - mnew), p1 = __expf(s[1][qi] - mnew);
+      lp[qi] = fmaf(lp[qi], alpha[qi], p0 + p1);
+      mrun[qi] = mnew;
+      pbuf[w][j][n] = p0;
+      pbuf[w][j][16 + n] = p1;
+      if (n == 0) abuf[w][j] = alpha[qi];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    // rescale the value accumulators when a maximum moved
+    bool moved = false;
+#pragma unroll
+    for (int qi = 0; qi < NQL; ++qi) moved |= alpha[qi] != 1.0f;
+    if (__builtin_amdgcn_ballot_w64(moved)) {
+#pragma unroll
+      for (int nt = 0; nt < 8; ++nt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) accV[nt][i] *= alpha[NBLK == 2 ? 0 : (i >> 1)];
+      }
+    }
+    // value A fragment: w = kSV p sc of tokens 8 gq .. 8 gq + 7 for row (jw, bw, pw), split
+    // into bf16 planes by the hardware conversion (round to nearest even)
+    bf16x8_t AV;
+    {
+      const float4 pa = *reinterpret_cast<const float4*>(&pbuf[w][jw][8 * gq]);
+      const float4 pb = *reinterpret_cast<const float4*>(&pbuf[w][jw][8 * gq + 4]);
+      const uint4 sa = *reinterpret_cast<const uint4*>(&vsd[w][bw][8 * gq]);
+      const uint4 sb4 = *reinterpret_cast<const uint4*>(&vsd[w][bw][8 * gq + 4]);
+      const float pe[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
+      const uint32_t se[8] = {sa.x, sa.y, sa.z, sa.w, sb4.x, sb4.y, sb4.z, sb4.w};
+      float o = offl * abuf[w][jw];
+      u32x4_t f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float x0 = kSV * f16_bits_to_f32(se[2 * i] >> 16) * pe[2 * i];
+        const float x1 = kSV * f16_bits_to_f32(se[2 * i + 1] >> 16) * pe[2 * i + 1];
+        const uint32_t hi = pk_bf16(x0, x1);
+        const float h0 = __uint_as_float(hi << 16), h1 = __uint_as_float(hi & 0xffff0000u);
+        const uint32_t lo = pk_bf16(x0 - h0, x1 - h1);
+        f[i] = pw ? lo : hi;
+        const float mn0 = f16_bits_to_f32(se[2 * i] & 0xffffu), mn1 = f16_bits_to_f32(se[2 * i + 1] & 0xffffu);
+        if (pw == 0) {
+          o = BITS == 8 ? fmaf(pe[2 * i], mn0, o) : fmaf(pe[2 * i], mn0, o - h0);
+          o = BITS == 8 ? fmaf(pe[2 * i + 1], mn1, o) : fmaf(pe[2 * i + 1], mn1, o - h1);
+        } else if (BITS != 8) {
+          o -= __uint_as_float(lo << 16) + __uint_as_float(lo & 0xffff0000u);
+        }
+      }
+      offl = o;
+      AV = as_bf16x8(f);
+    }
+    uint32_t vlo[8], vhi[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) vchunk<BITS>(vw0[e], vw1[e], vsh, vlo[e], vhi[e]);
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) accV[nt] = mfma16(AV, vfrag<BITS>(vlo, vhi, nt, one), accV[nt]);
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+  };
+  int t0 = t_begin + 32 * w;
+  for (; t0 + 32 <= t_end; t0 += 128) step(t0, std::true_type{});
+  if (t0 < t_end) step(t0, std::false_type{});
+
+  // 3. per-wave results: maximum and sum per query, gauge-space value sums
+  float lsum[NQL];
+#pragma unroll
+  for (int qi = 0; qi < NQL; ++qi) lsum[qi] = row16_sum(lp[qi]);
+  offs[w][n][gq] = offl;
+  if (n == 0) {
+#pragma unroll
+    for (int qi = 0; qi < NQL; ++qi) {
+      const int j = NBLK == 2 ? gq : 2 * gq + qi;
+      ml[w][0][j] = mrun[qi];
+      ml[w][1][j] = lsum[qi];
+    }
+  }
+  for (int idx = threadIdx.x; idx < JQ * kD; idx += kAThreads) (&macc[0][0])[idx] = 0.0f;
+  __syncthreads();
+  // merge the four waves: factors exp(m_w - M) per query
+  float fq[NQL], offq[NQL][NBLK];
+#pragma unroll
+  for (int qi = 0; qi < NQL; ++qi) {
+    const int j = NBLK == 2 ? gq : 2 * gq + qi;
+    float M = -INFINITY;
+    for (int v = 0; v < 4; ++v) M = fmaxf(M, ml[v][0][j]);
+    fq[qi] = mrun[qi] == -INFINITY ? 0.0f : __expf(mrun[qi] - M);
+#pragma unroll
+    for (int k = 0; k < NBLK; ++k) {
+      float o = 0.0f;
+      const int r0 = j * 2 * NBLK + 2 * k;  // rows (j, k, hi) and (j, k, lo)
+      for (int g4 = 0; g4 < 4; ++g4) o += offs[w][r0][g4] + offs[w][r0 + 1][g4];
+      offq[qi][k] = o;
+    }
+  }
+  for (int v = 0; v < 4; ++v) {
+    if (w == v) {
+#pragma unroll
+      for (int nt = 0; nt < 8; ++nt) {
+        const int ch = 8 * n + nt;
+        if constexpr (NBLK == 2) {
+          const bool hiblk = ch >= NB;
+          const float val = (hiblk ? accV[nt][2] + accV[nt][3] : accV[nt][0] + accV[nt][1]) +
+                            (hiblk ? offq[0][1] : offq[0][0]);
+          macc[gq][ch] += fq[0] * val;
+        } else {
+          macc[2 * gq][ch] += fq[0] * (accV[nt][0] + accV[nt][1] + offq[0][0]);
+          macc[2 * gq + 1][ch] += fq[1] * (accV[nt][2] + accV[nt][3] + offq[1][0]);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x < JQ) {
+    const int jj = threadIdx.x;
+    float M = -INFINITY, L = 0.0f;
+    for (int v = 0; v < 4; ++v) M = fmaxf(M, ml[v][0][jj]);
+    for (int v = 0; v < 4; ++v) {
+      const float mv = ml[v][0][jj];
+      if (mv != -INFINITY) L += ml[v][1][jj] * __expf(mv - M);
+    }
+    mm[0][jj] = M;
+    mm[1][jj] = L;
+  }
+  __syncthreads();
+  if (a.nsplit == 1) {
+    finalize_rows(a, G, &macc[0][0], nullptr, mm[1], nj, lv, b, h, hq0);
+    return;
+  }
+  const size_t pstride = size_t(2 + 2 * kD);
+  for (int jj = 0; jj < nj; ++jj) {
+    float* P = a.part + ((((size_t(lv) * B + b) * a.Hq + hq0 + jj) * a.nsplit) + sp) * pstride;
+    for (int idx = threadIdx.x; idx < 2 + 2 * kD; idx += kAThreads) {
+      float v;
+      if (idx == 0) v = mm[0][jj];
+      else if (idx == 1) v = mm[1][jj];
+      else if (idx < 2 + kD) v = macc[jj][idx - 2];
+      else v = 0.0f;
+      P[idx] = v;
+    }
+  }
+}
+
+template <int BITS>
+const void* att_mfma_fn(int nblk) {
+  return nblk == 2 ? (const void*)att_mfma<BITS, 2> : (const void*)att_mfma<BITS, 1>;
+}
+
+const void* att_mfma_kernel(int bits, int nblk) {
+  switch (bits) {
+    case 2: return att_mfma_fn<2>(nblk);
+    case 3: return att_mfma_fn<3>(nblk);
+    case 4: return att_mfma_fn<4>(nblk);
+    case 6: return att_mfma_fn<6>(nblk);
+    default: return att_mfma_fn<8>(nblk);
+  }
+}
+
 hipError_t set_smem(const void* fn, size_t bytes) {
   if (bytes <= 65536) return hipSuccess;
   return hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
@@ -373,16 +859,33 @@ AttendPlan attend_plan(int nl, int B, int H, int Hq, int d, int span) {
   return p;
 }
 
+bool attend_mfma_supported(const AttendDev& a, const CodecDev& c) {
+  return c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt == 1 && a.q.d == kD && (c.n == 64 || c.n == 128) &&
+         (c.bits == 2 || c.bits == 3 || c.bits == 4 || c.bits == 6 || c.bits == 8);
+}
+
 hipError_t launch_attend(const AttendDev& a, const GaugeDev& G, const CodecDev& c, bool force_generic,
                          hipStream_t st) {
-  (void)force_generic;
   const int d = a.q.d;
   const int nrow = a.q.L * a.q.B * a.kc.H * a.nqc;
   if (nrow == 0) return hipSuccess;
-  const size_t smem = (size_t(4) * kJQ * d + 4 * kJQ * kATile + 10 * kJQ) * sizeof(float);
-  hipError_t e = set_smem((const void*)att_generic, smem);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(att_generic, dim3(a.nsplit, nrow), dim3(kAThreads), smem, st, a, G, c);
+  hipError_t e;
+  if (!force_generic && attend_mfma_supported(a, c)) {
+    // the matrix-core kernel takes 8 / NBLK query heads per workgroup
+    const int nblk = kD / c.n, jq = 8 / nblk;
+    AttendDev af = a;
+    af.nqc = (a.grp + jq - 1) / jq;
+    const int nrow_f = a.q.L * a.q.B * a.kc.H * af.nqc;
+    GaugeDev g2 = G;
+    void* args[] = {&af, &g2};
+    e = hipLaunchKernel(att_mfma_kernel(c.bits, nblk), dim3(a.nsplit, nrow_f), dim3(kAThreads), args, 0, st);
+    if (e != hipSuccess) return e;
+  } else {
+    const size_t smem = (size_t(4) * kJQ * d + 4 * kJQ * kATile + 10 * kJQ) * sizeof(float);
+    e = set_smem((const void*)att_generic, smem);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(att_generic, dim3(a.nsplit, nrow), dim3(kAThreads), smem, st, a, G, c);
+  }
   e = hipGetLastError();
   if (e != hipSuccess || a.nsplit == 1) return e;
   const size_t smem2 = (size_t(2) * kJQ * d + 2 * kJQ) * sizeof(float);

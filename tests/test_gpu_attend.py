@@ -139,11 +139,11 @@ def test_attend_host_length_bf16_output_and_layer_range(kernels):
     _check(got, ref[1:3], _vmax(st, oc, lens, 4)[1:3], bf16_out=True)
 
 
-@pytest.mark.parametrize("grp,d,g", [(1, 128, 32), (12, 128, 128), (4, 64, 16), (8, 256, 64)])
+@pytest.mark.parametrize("grp,d,g", [(1, 128, 32), (12, 128, 128), (2, 128, 8), (4, 64, 16), (8, 256, 64)])
 def test_attend_head_groupings_and_dims(kernels, grp, d, g):
     """Multi-head (grp = 1), more query heads per KV head than one workgroup takes (12), and
     other head dimensions."""
-    oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=4, block_c=32)
+    oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=4, block_c=32 if d == 64 else 64)
     st = _setup(oc, 97, 128, d=d, g=g, grp=grp, B=1)
     lens = [97]
     scale = 1.0 / np.sqrt(d)
