@@ -51,6 +51,17 @@ def algorithmic_bytes(w, s_count=1):
     return s_count * (elems * per_elem + gauge)
 
 
+def kernel_source_hash():
+    """First 16 hex digits of the SHA-256 of the matrix-core kernel sources (cg_mfma.hip followed by
+    its shared header cg_mfma_util.h)."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in ("cg_mfma.hip", "cg_mfma_util.h"):
+        h.update(open(os.path.join(ROOT, "paper_2607_20538_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
 def measured_traffic(path, kernel):
     """HBM bytes per launch of `kernel` from the rocprofv3 FETCH_SIZE / WRITE_SIZE summary (scaled
     by the copy-kernel calibration), or None when there is none or the kernel source has changed
@@ -59,8 +70,7 @@ def measured_traffic(path, kernel):
 
     try:
         tr = json.load(open(path))
-        src = os.path.join(ROOT, "paper_2607_20538_amd", "csrc", "cg_mfma.hip")
-        if hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != tr.get("source_sha256_16"):
+        if kernel_source_hash() != tr.get("source_sha256_16"):
             return None
         return int(tr[kernel]["bytes"])
     except (OSError, ValueError, KeyError, TypeError):

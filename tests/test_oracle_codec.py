@@ -491,3 +491,15 @@ def test_attend_closed_forms():
     np.testing.assert_allclose(got[0, 0], Vh[0, 0].mean(axis=1), rtol=0, atol=1e-12)
     got1 = O.attend(codec, G, kc, vc, q, [1], 0.125)
     np.testing.assert_allclose(got1[0, 0], Vh[0, 0, :, 0], rtol=0, atol=1e-12)
+    # a row with no positions: the empty softmax is taken as a zero output
+    assert (O.attend(codec, G, kc, vc, q, [0], 0.125) == 0).all()
+    # hard-max limit: with the value cache also serving as the key cache (decoded as keys, with
+    # the key gauge) and a scale large enough that the best score leads the next by more than
+    # 60 / scale, the output is the decoded value of the best position
+    big = O.attend(codec, G, vc, vc, q, [T], 1e3)
+    Kv = O.kv_decode(codec, 0, G, vc, 0, T, out_bf16=False).astype(np.float64)
+    sc = np.einsum("htc,hc->ht", Kv[0, 0], q[0, 0].astype(np.float64))
+    srt = np.sort(sc, axis=1)
+    for h in range(H):
+        assert (srt[h, -1] - srt[h, -2]) * 1e3 > 60
+        np.testing.assert_allclose(big[0, 0, h], Vh[0, 0, h, sc[h].argmax()], rtol=0, atol=1e-12)
