@@ -55,6 +55,20 @@
  *                   the window.
  *   passthrough     codes [L][B][H][T_cap][d] binary32 z (the error-free backend of the
  *                   paper's no-compression sanity rows, section 4.4).
+ *   zfp-style       codes [L][B][H][T_cap/4][d/4][2*b] bytes: one fixed-rate block of 16*b
+ *                   bits (LSB-first) per 4 consecutive tokens x 4 consecutive channels of z,
+ *                   the 2-D field with x = channel and y = token of the paper's zfp setup
+ *                   (section 4.3: n_x = d_l); no side or residual buffer.  A block is coded
+ *                   as zfp's published algorithm describes: a 0 bit for an all-zero block,
+ *                   else a 1 bit and the 8-bit biased block exponent e (|z| < 2^e, e >= -126),
+ *                   the values as 30-bit integers trunc(z 2^(30-e)), the 4-point transform
+ *                   1/16 [[4 4 4 4] [5 1 -1 -5] [-4 4 4 -4] [-2 6 -6 2]] by integer lifting
+ *                   along channels then tokens, coefficients in sequency order (i + j, then
+ *                   i^2 + j^2, then the token index), negabinary, and bit planes from the top
+ *                   (bits of significant coefficients, then group tests with the last
+ *                   candidate's 1 implied) until the 16*b bits are spent.  T_cap, t0 and the
+ *                   token counts of kv_encode / kv_decode must be multiples of 4; no append,
+ *                   no attention.
  *
  * Quantiser (section 4.3; every fp32 operation rounds to nearest even, no fused
  * multiply-add):  mn_h = binary16 rounded toward -inf of the block minimum (+0 for zero),
@@ -97,8 +111,8 @@ enum {
   CG_GAUGE_USER = 5       /* params = G itself (e.g. a trained gauge) */
 };
 
-/* backends (section 4.3) */
-enum { CG_BACKEND_PASSTHROUGH = 0, CG_BACKEND_BLOCK_UNIFORM = 1, CG_BACKEND_KIVI = 2 };
+/* backends (section 4.3; ZFP: the zfp-style fixed-rate transform codec, rate = bits) */
+enum { CG_BACKEND_PASSTHROUGH = 0, CG_BACKEND_BLOCK_UNIFORM = 1, CG_BACKEND_KIVI = 2, CG_BACKEND_ZFP = 3 };
 
 /* element types of a cg_kv_view */
 enum { CG_DTYPE_BF16 = 0, CG_DTYPE_F32 = 1 };
@@ -108,7 +122,7 @@ typedef struct cg_gauge_shape {
   int32_t L, H, d, g;
 } cg_gauge_shape;
 
-/* Backend parameters.  bits: b in {2,3,4,6,8}.  block_c: block-uniform channel block n
+/* Backend parameters.  bits: b in {2,3,4,6,8} (zfp-style: the rate in bits per value).  block_c: block-uniform channel block n
  * (n | d, n * b % 32 == 0).  key_tokens (Gk, KIVI keys: channel ranges over Gk tokens),
  * val_channels (KIVI values: token ranges over that many channels), residual (W, KIVI
  * full-precision window of recent tokens).  block_t: block-uniform tile tokens Tb in

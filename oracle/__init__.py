@@ -20,7 +20,7 @@ import numpy as np
 
 from . import build as _build
 
-PASSTHROUGH, BLOCK_UNIFORM, KIVI = 0, 1, 2
+PASSTHROUGH, BLOCK_UNIFORM, KIVI, ZFP = 0, 1, 2, 3
 GAUGE_IDENTITY, GAUGE_HAAR, GAUGE_DCT2, GAUGE_HADAMARD, GAUGE_EXPM, GAUGE_USER = range(6)
 FLAG_NONFINITE, FLAG_SIDE_OVERFLOW = 1, 2
 
@@ -60,6 +60,15 @@ def lib():
         L.orc_kv_encode.argtypes = [i] * 14 + [i, vp, vp, i, vp, vp, vp, i]
         L.orc_kv_decode.argtypes = [i] * 13 + [vp, i, vp, vp, vp, vp, i, i, i, vp]
         L.orc_kv_append.argtypes = [i] * 13 + [i, vp, vp, i, vp, vp, vp, vp]
+        L.orc_zfp_order.argtypes = [vp]
+        L.orc_zfp_fwd4.argtypes = [vp, i]
+        L.orc_zfp_inv4.argtypes = [vp, i]
+        L.orc_negabinary.argtypes = [C.c_int32]
+        L.orc_negabinary.restype = C.c_uint32
+        L.orc_from_negabinary.argtypes = [C.c_uint32]
+        L.orc_from_negabinary.restype = C.c_int32
+        L.orc_zfp_encode_block.argtypes = [vp, i, vp]
+        L.orc_zfp_decode_block.argtypes = [vp, i, vp]
         _lib = L
     return _lib
 
@@ -176,6 +185,52 @@ def unpack_codes(packed: np.ndarray, n: int, bits: int) -> np.ndarray:
 
 
 # ------------------------------------------------------------------------------------------
+# zfp-style fixed-rate block codec (the paper's zfp backend, from zfp's published algorithm)
+# ------------------------------------------------------------------------------------------
+
+def zfp_order() -> np.ndarray:
+    """Sequency order: position k of the coded coefficients holds block entry 4 j + i."""
+    out = np.zeros(16, dtype=np.int32)
+    lib().orc_zfp_order(_p(out))
+    return out
+
+
+def zfp_fwd4(v) -> np.ndarray:
+    a = np.ascontiguousarray(v, dtype=np.int32).copy()
+    lib().orc_zfp_fwd4(_p(a), 1)
+    return a
+
+
+def zfp_inv4(v) -> np.ndarray:
+    a = np.ascontiguousarray(v, dtype=np.int32).copy()
+    lib().orc_zfp_inv4(_p(a), 1)
+    return a
+
+
+def negabinary(i: int) -> int:
+    return int(lib().orc_negabinary(int(i)))
+
+
+def from_negabinary(u: int) -> int:
+    return int(lib().orc_from_negabinary(int(u)))
+
+
+def zfp_encode_block(v, rate: int):
+    """v: 16 float32 values, entry 4 j + i = channel i of token j.  Returns (2 rate bytes, flags)."""
+    a = np.ascontiguousarray(v, dtype=np.float32)
+    out = np.zeros(2 * rate, dtype=np.uint8)
+    flags = lib().orc_zfp_encode_block(_p(a), rate, _p(out))
+    return out, flags
+
+
+def zfp_decode_block(code, rate: int) -> np.ndarray:
+    c = np.ascontiguousarray(code, dtype=np.uint8)
+    out = np.zeros(16, dtype=np.float32)
+    lib().orc_zfp_decode_block(_p(c), rate, _p(out))
+    return out
+
+
+# ------------------------------------------------------------------------------------------
 # whole-cache codec over the library's byte layouts
 # ------------------------------------------------------------------------------------------
 
@@ -197,6 +252,9 @@ class Codec:
 def cache_layout(codec: Codec, s: int, L: int, B: int, H: int, T_cap: int, d: int) -> dict:
     """Shapes and dtypes of the (codes, side, residual) buffers of one K or V cache."""
     b = codec.bits
+    if codec.backend == ZFP:
+        # one 4 x 4 block (4 tokens x 4 channels) of 16 b bits per 4 tokens and 4 channels
+        return {"codes": ((L, B, H, T_cap // 4, d // 4, 2 * b), np.uint8), "side": None, "residual": None}
     if codec.backend == PASSTHROUGH:
         return {"codes": ((L, B, H, T_cap, d), np.float32), "side": None, "residual": None}
     if codec.backend == BLOCK_UNIFORM:
@@ -255,6 +313,8 @@ def kv_decode(codec: Codec, s: int, G: np.ndarray, cache: dict, t0: int, Tout: i
     g = G.shape[-1]
     if codec.backend == KIVI and s == 0:
         T_cap = cache["codes"].shape[3] * codec.key_tokens
+    elif codec.backend == ZFP:
+        T_cap = cache["codes"].shape[3] * 4
     else:
         T_cap = cache["codes"].shape[3]
     Gc = np.ascontiguousarray(G, dtype=np.float32)

@@ -20,7 +20,12 @@
  *     staging window),
  *   - KIVI-style quantisation: per-channel key ranges over token groups and
  *     per-token value ranges over channel groups, with a full-precision window
- *     of recent tokens.
+ *     of recent tokens,
+ *   - a zfp-style fixed-rate transform codec (the paper's primary backend is zfp at fixed
+ *     rates, section 4.3), written from the published description of zfp's algorithm
+ *     (block-floating-point alignment, decorrelating transform, sequency ordering,
+ *     negabinary, embedded bit-plane coding with group tests) over the 2-D field whose
+ *     x axis is the channel and whose y axis runs over the tokens.
  *
  * Precision: the gauge is "exact result, then round once to fp32": products of
  * fp32 by bf16/fp32 are exact in binary64 and the sums are carried in binary64.
@@ -45,7 +50,7 @@
 #define ORC_EARG (-1)
 #define ORC_ENOTORTH (-2)
 
-enum { ORC_BACKEND_PASSTHROUGH = 0, ORC_BACKEND_BLOCK_UNIFORM = 1, ORC_BACKEND_KIVI = 2 };
+enum { ORC_BACKEND_PASSTHROUGH = 0, ORC_BACKEND_BLOCK_UNIFORM = 1, ORC_BACKEND_KIVI = 2, ORC_BACKEND_ZFP = 3 };
 enum { ORC_GAUGE_IDENTITY = 0, ORC_GAUGE_HAAR = 1, ORC_GAUGE_DCT2 = 2, ORC_GAUGE_HADAMARD = 3,
        ORC_GAUGE_EXPM = 4, ORC_GAUGE_USER = 5 };
 
@@ -411,6 +416,201 @@ void orc_unpack_codes(const uint8_t* in, int n, int bits, uint8_t* q) {
 }
 
 /* ------------------------------------------------------------------------------------------ */
+/* zfp-style fixed-rate codec of 4 x 4 blocks (4 consecutive channels x 4 consecutive tokens), */
+/* following the published description of zfp (Lindstrom 2014):                                */
+/*   1. block exponent e: the smallest e with |v| < 2^e for every value (frexp exponent of the */
+/*      largest magnitude), at least -126; an all-zero block is one 0 bit;                     */
+/*   2. fixed point: i = trunc(v 2^(30 - e)), |i| < 2^30;                                      */
+/*   3. decorrelating transform along the channels, then along the tokens, each the 4-point   */
+/*      map A = 1/16 [[4 4 4 4] [5 1 -1 -5] [-4 4 4 -4] [-2 6 -6 2]] computed by integer      */
+/*      lifting (additions and halvings), inverse by the lifting steps undone in reverse;     */
+/*   4. coefficients ordered by sequency (i + j, then i^2 + j^2, then the token index j);     */
+/*   5. negabinary u = (i + 0xAAAAAAAA) ^ 0xAAAAAAAA;                                          */
+/*   6. bit planes 31 .. 0: the plane's bits of the coefficients already significant, then   */
+/*      group tests over the rest (a 1 bit says some remaining coefficient has a 1 in the     */
+/*      plane; then their bits one by one up to that 1, which becomes significant with the   */
+/*      ones before it; the last remaining coefficient's 1 is implied), until the budget of  */
+/*      16 rate bits per block (header included: 1 + 8 exponent bits) is spent.              */
+/* The bit stream of a block is LSB-first; blocks are 2 rate bytes each, so the rate is      */
+/* exact: rate bits per value.  Non-finite inputs flag NONFINITE and code a zero block.       */
+/* ------------------------------------------------------------------------------------------ */
+
+static int zfp_order[16];  /* sequency position -> block index 4 j + i */
+static int zfp_order_ready = 0;
+
+static void zfp_make_order(void) {
+  if (zfp_order_ready) return;
+  int idx[16];
+  for (int k = 0; k < 16; ++k) idx[k] = k;
+  /* insertion sort by (i + j, i^2 + j^2, j) */
+  for (int a = 1; a < 16; ++a) {
+    int v = idx[a], b = a - 1;
+    for (; b >= 0; --b) {
+      int p = idx[b];
+      int pi = p % 4, pj = p / 4, vi = v % 4, vj = v / 4;
+      int kp = (pi + pj) * 1000 + (pi * pi + pj * pj) * 10 + pj;
+      int kv = (vi + vj) * 1000 + (vi * vi + vj * vj) * 10 + vj;
+      if (kp <= kv) break;
+      idx[b + 1] = p;
+    }
+    idx[b + 1] = v;
+  }
+  memcpy(zfp_order, idx, sizeof idx);
+  zfp_order_ready = 1;
+}
+
+void orc_zfp_order(int* out) {
+  zfp_make_order();
+  memcpy(out, zfp_order, sizeof zfp_order);
+}
+
+/* two's-complement wrapping add / subtract / double and arithmetic halving on 32 bits */
+static int32_t wadd(int32_t a, int32_t b) { return (int32_t)((uint32_t)a + (uint32_t)b); }
+static int32_t wsub(int32_t a, int32_t b) { return (int32_t)((uint32_t)a - (uint32_t)b); }
+static int32_t wdbl(int32_t a) { return (int32_t)((uint32_t)a << 1); }
+static int32_t half(int32_t a) { return a >= 0 ? a / 2 : -((-(int64_t)a + 1) / 2); }  /* floor(a / 2) */
+
+/* forward 4-point transform of p[0], p[s], p[2s], p[3s] by lifting */
+void orc_zfp_fwd4(int32_t* p, int s) {
+  int32_t x = p[0], y = p[s], z = p[2 * s], w = p[3 * s];
+  /* averages and half-differences of the outer pair (x, w) and the inner pair (y, z) */
+  x = half(wadd(x, w)); w = wsub(w, x);
+  z = half(wadd(z, y)); y = wsub(y, z);
+  /* mean of the four; the even combination; the two odd ones */
+  x = half(wadd(x, z)); z = wsub(z, x);
+  w = half(wadd(w, y)); y = wsub(y, w);
+  /* final rotation of the two odd coefficients */
+  w = wadd(w, half(y)); y = wsub(y, half(w));
+  p[0] = x; p[s] = y; p[2 * s] = z; p[3 * s] = w;
+}
+
+/* the lifting steps above undone in reverse order */
+void orc_zfp_inv4(int32_t* p, int s) {
+  int32_t x = p[0], y = p[s], z = p[2 * s], w = p[3 * s];
+  y = wadd(y, half(w)); w = wsub(w, half(y));
+  y = wadd(y, w); w = wsub(wdbl(w), y);
+  z = wadd(z, x); x = wsub(wdbl(x), z);
+  y = wadd(y, z); z = wsub(wdbl(z), y);
+  w = wadd(w, x); x = wsub(wdbl(x), w);
+  p[0] = x; p[s] = y; p[2 * s] = z; p[3 * s] = w;
+}
+
+uint32_t orc_negabinary(int32_t i) { return ((uint32_t)i + 0xAAAAAAAAu) ^ 0xAAAAAAAAu; }
+int32_t orc_from_negabinary(uint32_t u) { return (int32_t)((u ^ 0xAAAAAAAAu) - 0xAAAAAAAAu); }
+
+typedef struct {
+  uint8_t* buf;
+  int pos, cap;
+} orc_bits;
+
+static int bits_put(orc_bits* w, int bit) {
+  if (w->pos >= w->cap) return 0;
+  if (bit) w->buf[w->pos >> 3] |= (uint8_t)(1u << (w->pos & 7));
+  w->pos++;
+  return 1;
+}
+static int bits_get(orc_bits* r, int* bit) {
+  if (r->pos >= r->cap) return 0;
+  *bit = (r->buf[r->pos >> 3] >> (r->pos & 7)) & 1;
+  r->pos++;
+  return 1;
+}
+
+/* v[4 j + i]: channel i, token j of the block.  out: 2 rate bytes (cleared here). */
+int orc_zfp_encode_block(const float* v, int rate, uint8_t* out) {
+  zfp_make_order();
+  const int maxbits = 16 * rate;
+  memset(out, 0, (size_t)(maxbits / 8));
+  orc_bits w = {out, 0, maxbits};
+  int flags = 0;
+  float amax = 0.0f;
+  for (int k = 0; k < 16; ++k) {
+    if (!isfinite(v[k])) flags |= ORC_FLAG_NONFINITE;
+    else if (fabsf(v[k]) > amax) amax = fabsf(v[k]);
+  }
+  if (flags || amax == 0.0f) {
+    bits_put(&w, 0);
+    return flags;
+  }
+  int e;
+  frexpf(amax, &e);
+  if (e < -126) e = -126;
+  bits_put(&w, 1);
+  for (int k = 0; k < 8; ++k) bits_put(&w, ((e + 127) >> k) & 1);
+  int32_t q[16];
+  for (int k = 0; k < 16; ++k) q[k] = (int32_t)ldexpf(v[k], 30 - e);  /* exact scaling, truncation */
+  for (int j = 0; j < 4; ++j) orc_zfp_fwd4(q + 4 * j, 1);  /* along the channels */
+  for (int i = 0; i < 4; ++i) orc_zfp_fwd4(q + i, 4);      /* along the tokens */
+  uint32_t u[16];
+  for (int k = 0; k < 16; ++k) u[k] = orc_negabinary(q[zfp_order[k]]);
+  int n = 0;
+  for (int plane = 31; plane >= 0; --plane) {
+    for (int c = 0; c < n; ++c)
+      if (!bits_put(&w, (u[c] >> plane) & 1)) return flags;
+    while (n < 16) {
+      int any = 0;
+      for (int c = n; c < 16; ++c) any |= (u[c] >> plane) & 1;
+      if (!bits_put(&w, any)) return flags;
+      if (!any) break;
+      for (;;) {
+        if (n == 15) {  /* the only candidate left holds the 1 */
+          n = 16;
+          break;
+        }
+        int bit = (u[n] >> plane) & 1;
+        if (!bits_put(&w, bit)) return flags;
+        n++;
+        if (bit) break;
+      }
+    }
+  }
+  return flags;
+}
+
+void orc_zfp_decode_block(const uint8_t* in, int rate, float* v) {
+  zfp_make_order();
+  orc_bits r = {(uint8_t*)in, 0, 16 * rate};
+  int bit;
+  for (int k = 0; k < 16; ++k) v[k] = 0.0f;
+  if (!bits_get(&r, &bit) || !bit) return;
+  int eb = 0;
+  for (int k = 0; k < 8; ++k) {
+    if (!bits_get(&r, &bit)) return;
+    eb |= bit << k;
+  }
+  const int e = eb - 127;
+  uint32_t u[16] = {0};
+  int n = 0, done = 0;
+  for (int plane = 31; plane >= 0 && !done; --plane) {
+    for (int c = 0; c < n && !done; ++c) {
+      if (!bits_get(&r, &bit)) done = 1;
+      else u[c] |= (uint32_t)bit << plane;
+    }
+    while (n < 16 && !done) {
+      int any;
+      if (!bits_get(&r, &any)) { done = 1; break; }
+      if (!any) break;
+      for (;;) {
+        if (n == 15) {
+          u[15] |= 1u << plane;
+          n = 16;
+          break;
+        }
+        if (!bits_get(&r, &bit)) { done = 1; break; }
+        if (bit) u[n] |= 1u << plane;
+        n++;
+        if (bit) break;
+      }
+    }
+  }
+  int32_t q[16];
+  for (int k = 0; k < 16; ++k) q[zfp_order[k]] = orc_from_negabinary(u[k]);
+  for (int i = 0; i < 4; ++i) orc_zfp_inv4(q + i, 4);
+  for (int j = 0; j < 4; ++j) orc_zfp_inv4(q + 4 * j, 1);
+  for (int k = 0; k < 16; ++k) v[k] = ldexpf((float)q[k], e - 30);
+}
+
+/* ------------------------------------------------------------------------------------------ */
 /* Whole-cache encode / decode / rolling append, over the byte layouts of the codec library:  */
 /*   X, Xhat     [L][B][H][T][d] contiguous, bf16 bits or binary32                            */
 /*   BU codes    [L][B][H][T_cap][d*b/8]  (blocks of n channels, LSB-first streams)           */
@@ -421,6 +621,8 @@ void orc_unpack_codes(const uint8_t* in, int n, int bits, uint8_t* q) {
 /*   KIVI keys   codes [L][B][H][T_cap/G][d][G*b/8], side [L][B][H][T_cap/G][d][2]            */
 /*   KIVI values as BU with n = value channel group                                           */
 /*   KIVI ring   [L][B][H][W + G][d] raw bf16, slot = t mod (W + G)                           */
+/*   zfp-style   codes [L][B][H][T_cap/4][d/4][2 rate] (one 4 x 4 block per 4 tokens x 4        */
+/*               channels), no side information                                               */
 /* where G is the key token group and W the full-precision window.  For a cache holding T     */
 /* tokens, KIVI quantises the first T_q = floor((T - W) / G) G tokens (0 when T < W).         */
 /* ------------------------------------------------------------------------------------------ */
@@ -441,6 +643,7 @@ static int check_layout(const orc_layout* o) {
   if (o->L <= 0 || o->B <= 0 || o->H <= 0 || o->d <= 0 || o->g <= 0 || o->d % o->g) return ORC_EARG;
   if (o->backend == ORC_BACKEND_PASSTHROUGH) return 0;
   if (o->bits < 1 || o->bits > 8) return ORC_EARG;
+  if (o->backend == ORC_BACKEND_ZFP) return (o->d % 4 || o->T_cap % 4) ? ORC_EARG : 0;
   if (o->backend == ORC_BACKEND_BLOCK_UNIFORM) {
     if (o->n <= 0 || o->n > 256 || o->d % o->n || (o->n * o->bits) % 8) return ORC_EARG;
     if (o->bt < 1 || o->bt > 256 || o->T_cap % o->bt) return ORC_EARG;
@@ -583,6 +786,7 @@ int orc_kv_encode(int backend, int bits, int n, int kg, int kvc, int win, int bt
   if (backend == ORC_BACKEND_KIVI && (t0 != 0 || !x_bf16)) return ORC_EARG;
   const int tile = backend == ORC_BACKEND_BLOCK_UNIFORM && bt > 1;
   if (tile && (t0 % bt || !x_bf16)) return ORC_EARG;
+  if (backend == ORC_BACKEND_ZFP && (t0 % 4 || T % 4)) return ORC_EARG;
   int R = d / g, flags = 0;
   size_t gsz = (size_t)R * g * g;
   float* x = (float*)malloc(sizeof(float) * d);
@@ -646,6 +850,26 @@ int orc_kv_encode(int backend, int bits, int n, int kg, int kvc, int win, int bt
           free(zt);
           continue;
         }
+        if (backend == ORC_BACKEND_ZFP) {
+          /* 4-token groups: gauge each token, then one block per 4 channels */
+          float* zt = (float*)malloc(sizeof(float) * 4 * (size_t)d);
+          const int bb = 2 * bits;
+          for (int t = 0; t < T; t += 4) {
+            for (int u = 0; u < 4; ++u) {
+              for (int c = 0; c < d; ++c) x[c] = load_x(X, x_bf16, xbase + (size_t)(t + u) * d + c);
+              orc_gauge_apply(d, g, Gs, x, zt + (size_t)u * d);
+            }
+            size_t grp = sl * (T_cap / 4) + (size_t)((t0 + t) / 4);
+            for (int cb = 0; cb < d / 4; ++cb) {
+              float v[16];
+              for (int j = 0; j < 4; ++j)
+                for (int i = 0; i < 4; ++i) v[4 * j + i] = zt[(size_t)j * d + 4 * cb + i];
+              flags |= orc_zfp_encode_block(v, bits, (uint8_t*)codes + (grp * (d / 4) + cb) * bb);
+            }
+          }
+          free(zt);
+          continue;
+        }
         for (int t = 0; t < T; ++t) {
           for (int c = 0; c < d; ++c) x[c] = load_x(X, x_bf16, xbase + (size_t)t * d + c);
           for (int c = 0; c < d; ++c)
@@ -675,10 +899,42 @@ int orc_kv_decode(int backend, int bits, int n, int kg, int kvc, int win, int bt
   if (check_layout(&o) || s < 0 || s > 1 || t0 < 0 || Tout < 0 || t0 + Tout > T_cap) return ORC_EARG;
   const int tile = backend == ORC_BACKEND_BLOCK_UNIFORM && bt > 1;
   if ((backend == ORC_BACKEND_KIVI || tile) && !lens) return ORC_EARG;
+  if (backend == ORC_BACKEND_ZFP && (t0 % 4 || Tout % 4)) return ORC_EARG;
   int R = d / g;
   size_t gsz = (size_t)R * g * g;
   float* zh = (float*)malloc(sizeof(float) * d);
   float* xh = (float*)malloc(sizeof(float) * d);
+  if (backend == ORC_BACKEND_ZFP) {
+    float* zt = (float*)malloc(sizeof(float) * 4 * (size_t)d);
+    const int bb = 2 * bits;
+    for (int l = 0; l < L; ++l)
+      for (int b = 0; b < B; ++b)
+        for (int h = 0; h < H; ++h) {
+          size_t sl = slice_index(&o, l, b, h);
+          const float* Gs = Gall + (((size_t)l * 2 + s) * H + h) * gsz;
+          int len = lens ? lens[b] : T_cap;
+          for (int u0 = 0; u0 < Tout; u0 += 4) {
+            size_t grp = sl * (T_cap / 4) + (size_t)((t0 + u0) / 4);
+            for (int cb = 0; cb < d / 4; ++cb) {
+              float v[16];
+              orc_zfp_decode_block((const uint8_t*)codes + (grp * (d / 4) + cb) * bb, bits, v);
+              for (int j = 0; j < 4; ++j)
+                for (int i = 0; i < 4; ++i) zt[(size_t)j * d + 4 * cb + i] = v[4 * j + i];
+            }
+            for (int j = 0; j < 4; ++j) {
+              if (t0 + u0 + j >= len) continue;
+              orc_gauge_inverse(d, g, Gs, zt + (size_t)j * d, xh);
+              size_t obase = (sl * (size_t)Tout + u0 + j) * d;
+              for (int c = 0; c < d; ++c) {
+                if (out_bf16) ((uint16_t*)Xhat)[obase + c] = orc_f32_to_bf16(xh[c]);
+                else ((float*)Xhat)[obase + c] = xh[c];
+              }
+            }
+          }
+        }
+    free(zt); free(zh); free(xh);
+    return 0;
+  }
   for (int l = 0; l < L; ++l)
     for (int b = 0; b < B; ++b)
       for (int h = 0; h < H; ++h) {
@@ -740,6 +996,7 @@ int orc_kv_append(int backend, int bits, int n, int kg, int kvc, int win, int bt
   if (check_layout(&o) || s < 0 || s > 1) return ORC_EARG;
   const int tile = backend == ORC_BACKEND_BLOCK_UNIFORM && bt > 1;
   if ((backend == ORC_BACKEND_KIVI || tile) && !x_bf16) return ORC_EARG;
+  if (backend == ORC_BACKEND_ZFP) return ORC_EARG;  /* whole 4-token groups only */
   for (int b = 0; b < B; ++b)
     if (pos[b] < 0 || pos[b] >= T_cap) return ORC_EARG;
   int R = d / g, flags = 0;

@@ -20,7 +20,7 @@ CG_OK, CG_ERR_ARG, CG_ERR_SHAPE, CG_ERR_ALIGN, CG_ERR_UNSUPPORTED, CG_ERR_NOT_OR
     CG_ERR_DEVICE = range(8)
 CG_FLAG_NONFINITE, CG_FLAG_SIDE_OVERFLOW, CG_FLAG_POS_RANGE = 1, 2, 4
 GAUGE_IDENTITY, GAUGE_HAAR, GAUGE_DCT2, GAUGE_HADAMARD, GAUGE_EXPM, GAUGE_USER = range(6)
-PASSTHROUGH, BLOCK_UNIFORM, KIVI = 0, 1, 2
+PASSTHROUGH, BLOCK_UNIFORM, KIVI, ZFP = 0, 1, 2, 3
 DTYPE_BF16, DTYPE_F32 = 0, 1
 
 EXPORTS = ["cg_status_str", "gauge_device_bytes", "gauge_make", "cache_bytes", "kv_encode", "kv_decode",

@@ -244,6 +244,8 @@ int32_t check_codec(const cg_codec* c, int d) {
       if (d % c->block_c || (c->block_c * c->bits) % 32 || c->block_c > 256) return CG_ERR_UNSUPPORTED;
       if (c->block_t < 1 || c->block_t > 32 || (c->block_t & (c->block_t - 1))) return CG_ERR_UNSUPPORTED;
       return CG_OK;
+    case CG_BACKEND_ZFP:
+      return bits_ok(c->bits) && d % 4 == 0 ? CG_OK : CG_ERR_UNSUPPORTED;
     case CG_BACKEND_KIVI:
       if (!bits_ok(c->bits)) return CG_ERR_UNSUPPORTED;
       if (c->key_tokens != 16 && c->key_tokens != 32 && c->key_tokens != 64) return CG_ERR_UNSUPPORTED;
@@ -271,7 +273,9 @@ int32_t check_cache(const cg_cache* k, const cg_codec* c, const cg_gauge_shape& 
   if (!k || !k->codes) return CG_ERR_ARG;
   if (k->L != s.L || k->H != s.H || k->d != s.d || k->B != B || k->T_cap <= 0) return CG_ERR_SHAPE;
   if (!aligned16(k->codes)) return CG_ERR_ALIGN;
-  if (c->backend != CG_BACKEND_PASSTHROUGH && (!k->side || !aligned16(k->side))) return CG_ERR_ARG;
+  if (c->backend != CG_BACKEND_PASSTHROUGH && c->backend != CG_BACKEND_ZFP && (!k->side || !aligned16(k->side)))
+    return CG_ERR_ARG;
+  if (c->backend == CG_BACKEND_ZFP && k->T_cap % 4) return CG_ERR_SHAPE;
   if (c->backend == CG_BACKEND_KIVI) {
     if (!k->residual || !aligned16(k->residual)) return CG_ERR_ARG;
     if (k->T_cap % c->key_tokens) return CG_ERR_SHAPE;
@@ -492,6 +496,10 @@ int32_t cache_bytes(const cg_codec* codec, int32_t s, int32_t L, int32_t B, int3
   const int b = codec->bits;
   switch (codec->backend) {
     case CG_BACKEND_PASSTHROUGH: c = slices * T_cap * d * 4; break;
+    case CG_BACKEND_ZFP:
+      if (T_cap % 4) return CG_ERR_SHAPE;
+      c = slices * (T_cap / 4) * (d / 4) * size_t(2 * b);
+      break;
     case CG_BACKEND_BLOCK_UNIFORM: {
       const int bt = codec->block_t;
       if (T_cap % bt) return CG_ERR_SHAPE;
@@ -538,6 +546,8 @@ int32_t kv_encode(int32_t s, const cg_kv_view* X, const void* G_dev, cg_gauge_sh
   } else if (codec->backend == CG_BACKEND_BLOCK_UNIFORM && codec->block_t > 1) {
     if (t0 % codec->block_t || X->dtype != CG_DTYPE_BF16) return CG_ERR_UNSUPPORTED;
     tq = (X->T / codec->block_t) * codec->block_t;
+  } else if (codec->backend == CG_BACKEND_ZFP) {
+    if (t0 % 4 || X->T % 4) return CG_ERR_UNSUPPORTED;  // whole 4-token block rows
   }
   if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
   hipError_t e = launch_encode(s, view_dev(X), 0, gauge_dev(G_dev, shp), codec_dev(codec), cache_dev(out), t0, tq,
@@ -558,6 +568,7 @@ int32_t kv_decode(int32_t s, const cg_cache* in, const void* G_dev, cg_gauge_sha
   if (int64_t(t0) + Xhat->T > in->T_cap) return CG_ERR_CAPACITY;
   const bool held = codec->backend == CG_BACKEND_KIVI || (codec->backend == CG_BACKEND_BLOCK_UNIFORM && codec->block_t > 1);
   if (held && (in->len < 0 || in->len > in->T_cap || int64_t(t0) + Xhat->T > in->len)) return CG_ERR_CAPACITY;
+  if (codec->backend == CG_BACKEND_ZFP && (t0 % 4 || Xhat->T % 4)) return CG_ERR_UNSUPPORTED;
   if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
   hipError_t e = launch_decode(s, cache_dev(in), 0, gauge_dev(G_dev, shp), codec_dev(codec), t0, in->len, nullptr,
                                view_dev(Xhat), err_flag, static_cast<hipStream_t>(stream));
@@ -574,6 +585,7 @@ int32_t kv_append_step(int32_t l0, int32_t l1, const cg_kv_view* k_new, const cg
   if (!aligned16(G_dev)) return CG_ERR_ALIGN;
   if ((reinterpret_cast<uintptr_t>(pos) & 3u)) return CG_ERR_ALIGN;
   if ((rc = check_codec(codec, shp.d)) != CG_OK) return rc;
+  if (codec->backend == CG_BACKEND_ZFP) return CG_ERR_UNSUPPORTED;  // blocks span 4 tokens
   const int nl = l1 - l0;
   if ((rc = check_view(k_new, shp, nl)) != CG_OK) return rc;
   if ((rc = check_view(v_new, shp, nl)) != CG_OK) return rc;
@@ -636,6 +648,7 @@ int32_t kv_attend(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* k
   if (!aligned16(G_dev)) return CG_ERR_ALIGN;
   if (lens && (reinterpret_cast<uintptr_t>(lens) & 3u)) return CG_ERR_ALIGN;
   if ((rc = check_codec(codec, shp.d)) != CG_OK) return rc;
+  if (codec->backend == CG_BACKEND_ZFP) return CG_ERR_UNSUPPORTED;
   const int nl = l1 - l0;
   if ((rc = check_qview(q, shp, nl)) != CG_OK) return rc;
   if ((rc = check_qview(out, shp, nl)) != CG_OK) return rc;

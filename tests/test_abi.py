@@ -236,6 +236,31 @@ def test_attend_rejects_invalid_arguments():
     assert call(kc=big, vc=big, ws=0x70008) == cg.CG_ERR_ALIGN
 
 
+def test_zfp_backend_sizes_and_restrictions():
+    z = cg.Codec(cg.ZFP, 4)
+    assert cg.cache_bytes(z, 0, 2, 3, 4, 64, 128) == (2 * 3 * 4 * 64 * 128 * 4 // 8, 0, 0)
+    assert cg.cache_bytes(cg.Codec(cg.ZFP, 3), 1, 1, 1, 1, 8, 64)[0] == 8 * 64 * 3 // 8
+    with pytest.raises(cg.CodecError) as e:
+        cg.cache_bytes(cg.Codec(cg.ZFP, 5), 0, 1, 1, 2, 64, 64)
+    assert e.value.status == cg.CG_ERR_UNSUPPORTED
+    with pytest.raises(cg.CodecError) as e:
+        cg.cache_bytes(z, 0, 1, 1, 2, 62, 64)
+    assert e.value.status == cg.CG_ERR_SHAPE
+    k = _fake_cache(T_cap=64, side=0, residual=0)
+    assert _encode(_fake_view(T=6), k, z) == cg.CG_ERR_UNSUPPORTED
+    assert _encode(_fake_view(T=8), k, z, t0=2) == cg.CG_ERR_UNSUPPORTED
+    assert _decode(_fake_view(T=6), k, z) == cg.CG_ERR_UNSUPPORTED
+    assert _encode(_fake_view(T=8), _fake_cache(T_cap=62, side=0), z) == cg.CG_ERR_SHAPE
+    shp = cg.shape(1, 2, 64, 16)
+    kn = _fake_view(L=1, T=1, strides=(128, 128, 64, 64))
+    cs = z.struct()
+    assert cg.lib().kv_append_step(0, 1, C.byref(kn), C.byref(kn), 0x60000, 0x50000, shp, C.byref(cs), C.byref(k),
+                                   C.byref(k), None, None, None, None) == cg.CG_ERR_UNSUPPORTED
+    q = _fake_view(L=1, H=2, T=1, strides=(128, 128, 64, 64))
+    assert cg.lib().kv_attend(0, 1, C.byref(q), C.byref(k), C.byref(k), 0x50000, shp, C.byref(cs), None, 0.1,
+                              C.byref(q), 0x70000, None, None) == cg.CG_ERR_UNSUPPORTED
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(cg, "LIB_PATH", str(tmp_path / "missing.so"))
     monkeypatch.setattr(cg, "_lib", None)
