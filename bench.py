@@ -36,7 +36,7 @@ def parse():
                     help="HBM traffic per launch measured with rocprofv3 counters (optional)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the timed region, run one plain 512 MiB device copy (counter calibration)")
-    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral", "attend"]),
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral", "attend", "zfp"]),
                     help="llama8b (default) prints the headline line; the others print per-kernel timings of "
                          "the KIVI, rolling-step and 27B-sweep workloads")
     return ap.parse_args()
@@ -132,7 +132,7 @@ def other_workload(name, steps, warmup):
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral") else ("rolling" if name == "attend" else name)]
+    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral", "zfp") else ("rolling" if name == "attend" else name)]
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     out = {"workload": name, "shape": {"L": w.L, "B": w.B, "H": w.H, "T": w.T, "d": w.d}, "steps": steps}
 
@@ -174,8 +174,9 @@ def other_workload(name, steps, warmup):
             del X
             torch.cuda.empty_cache()
         out["runs"] = rows
-    elif name in ("kivi", "gemma27b", "tiles"):
-        combos = {"kivi": [(w.g, w.bits)], "tiles": [(128, 4), (128, 3), (32, 4)]}.get(
+    elif name in ("kivi", "gemma27b", "tiles", "zfp"):
+        combos = {"kivi": [(w.g, w.bits)], "tiles": [(128, 4), (128, 3), (32, 4)],
+                  "zfp": [(128, r) for r in (2, 3, 4, 6, 8)]}.get(
             name, [(g, b) for g in (8, 32, 128) for b in (3, 4, 6)])
         rows = []
         for g, bits in combos:
@@ -186,6 +187,8 @@ def other_workload(name, steps, warmup):
                 codec = cg.Codec(cg.KIVI, bits, 64, w.key_tokens, w.val_channels, w.residual)
             elif name == "tiles":
                 codec = cg.Codec(cg.BLOCK_UNIFORM, bits, 128, block_t=16)
+            elif name == "zfp":
+                codec = cg.Codec(cg.ZFP, bits)
             else:
                 codec = cg.Codec(cg.BLOCK_UNIFORM, bits, w.block_c)
             row = {"g": g, "bits": bits}

@@ -25,33 +25,112 @@ __device__ __forceinline__ float load_x(const ViewDev& v, size_t off) {
   return v.bf16 ? bf16_to_f32(((const uint16_t*)v.ptr)[off]) : ((const float*)v.ptr)[off];
 }
 
-// zs[t][i] = sum_j G_{l,s,h,r}[i%g][j] xs[t][r*g + j] for t < ntok (binary32 FMA chain).
+// LDS row pitch of the token tiles (floats): a multiple of 4 so that rows stay 16-byte aligned
+// for vector reads, offset by 4 banks from row to row
+constexpr int kPad = 4;
+
+// zs[t][i] = sum_j G_{l,s,h,r}[i%g][j] xs[t][r*g + j] for t < ntok: one binary32 FMA chain per
+// element in increasing j.  With g a multiple of 4 each thread computes a 4-token x 4-channel
+// block, reading 4 consecutive j of 4 rows of G and of 4 token rows per step (16-byte loads).
 __device__ void gauge_tile(const float* xs, float* zs, int ntok, int d, int dp, const GaugeDev& G, int l, int s,
                            int h) {
   const int g = G.g;
-  for (int idx = threadIdx.x; idx < ntok * d; idx += blockDim.x) {
-    const int t = idx / d, i = idx - t * d;
-    const int r = i / g, ii = i - r * g;
-    const float* Gr = G.f32 + gauge_block(l, s, h, r, G.H, G.R) * g * g + size_t(ii) * g;
-    const float* xr = xs + t * dp + r * g;
-    float acc = 0.0f;
-    for (int j = 0; j < g; ++j) acc = fmaf(Gr[j], xr[j], acc);
-    zs[t * dp + i] = acc;
+  if (g % 4) {
+    for (int idx = threadIdx.x; idx < ntok * d; idx += blockDim.x) {
+      const int t = idx / d, i = idx - t * d;
+      const int r = i / g, ii = i - r * g;
+      const float* Gr = G.f32 + gauge_block(l, s, h, r, G.H, G.R) * g * g + size_t(ii) * g;
+      const float* xr = xs + t * dp + r * g;
+      float acc = 0.0f;
+      for (int j = 0; j < g; ++j) acc = fmaf(Gr[j], xr[j], acc);
+      zs[t * dp + i] = acc;
+    }
+    return;
+  }
+  const int ntb = (ntok + 3) / 4, ncb = d / 4;
+  for (int idx = threadIdx.x; idx < ntb * ncb; idx += blockDim.x) {
+    const int tb = idx / ncb, cb = idx - tb * ncb;
+    const int t0 = 4 * tb, i0 = 4 * cb, r = i0 / g;
+    const float* Gb = G.f32 + gauge_block(l, s, h, r, G.H, G.R) * g * g + size_t(i0 - r * g) * g;
+    const float4 zero = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    float acc[4][4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int a = 0; a < 4; ++a) acc[t][a] = 0.0f;
+    for (int j = 0; j < g; j += 4) {
+      float4 gv[4], xv[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) gv[a] = *reinterpret_cast<const float4*>(Gb + size_t(a) * g + j);
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        xv[t] = t0 + t < ntok ? *reinterpret_cast<const float4*>(xs + (t0 + t) * dp + r * g + j) : zero;
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          acc[t][a] = fmaf(gv[a].x, xv[t].x, acc[t][a]);
+          acc[t][a] = fmaf(gv[a].y, xv[t].y, acc[t][a]);
+          acc[t][a] = fmaf(gv[a].z, xv[t].z, acc[t][a]);
+          acc[t][a] = fmaf(gv[a].w, xv[t].w, acc[t][a]);
+        }
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      if (t0 + t < ntok) *reinterpret_cast<float4*>(zs + (t0 + t) * dp + i0) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
   }
 }
 
-// xs[t][i] = sum_j G_{l,s,h,r}[j][i%g] zs[t][r*g + j] (inverse gauge, G^T).
+// xs[t][i] = sum_j G_{l,s,h,r}[j][i%g] zs[t][r*g + j] (inverse gauge, G^T), the same chains and
+// blocking (4 consecutive columns of G are one 16-byte read of row j).
 __device__ void inverse_tile(const float* zs, float* xs, int ntok, int d, int dp, const GaugeDev& G, int l, int s,
                              int h) {
   const int g = G.g;
-  for (int idx = threadIdx.x; idx < ntok * d; idx += blockDim.x) {
-    const int t = idx / d, i = idx - t * d;
-    const int r = i / g, ii = i - r * g;
-    const float* Gr = G.f32 + gauge_block(l, s, h, r, G.H, G.R) * g * g + ii;
-    const float* zr = zs + t * dp + r * g;
-    float acc = 0.0f;
-    for (int j = 0; j < g; ++j) acc = fmaf(Gr[size_t(j) * g], zr[j], acc);
-    xs[t * dp + i] = acc;
+  if (g % 4) {
+    for (int idx = threadIdx.x; idx < ntok * d; idx += blockDim.x) {
+      const int t = idx / d, i = idx - t * d;
+      const int r = i / g, ii = i - r * g;
+      const float* Gr = G.f32 + gauge_block(l, s, h, r, G.H, G.R) * g * g + ii;
+      const float* zr = zs + t * dp + r * g;
+      float acc = 0.0f;
+      for (int j = 0; j < g; ++j) acc = fmaf(Gr[size_t(j) * g], zr[j], acc);
+      xs[t * dp + i] = acc;
+    }
+    return;
+  }
+  const int ntb = (ntok + 3) / 4, ncb = d / 4;
+  for (int idx = threadIdx.x; idx < ntb * ncb; idx += blockDim.x) {
+    const int tb = idx / ncb, cb = idx - tb * ncb;
+    const int t0 = 4 * tb, i0 = 4 * cb, r = i0 / g;
+    const float* Gb = G.f32 + gauge_block(l, s, h, r, G.H, G.R) * g * g + (i0 - r * g);
+    const float4 zero = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    float acc[4][4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int a = 0; a < 4; ++a) acc[t][a] = 0.0f;
+    for (int j = 0; j < g; j += 4) {
+      float4 gv[4], zv[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) gv[q] = *reinterpret_cast<const float4*>(Gb + size_t(j + q) * g);  // G[j+q][i0..i0+3]
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        zv[t] = t0 + t < ntok ? *reinterpret_cast<const float4*>(zs + (t0 + t) * dp + r * g + j) : zero;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const float zz[4] = {zv[t].x, zv[t].y, zv[t].z, zv[t].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[t][0] = fmaf(gv[q].x, zz[q], acc[t][0]);
+          acc[t][1] = fmaf(gv[q].y, zz[q], acc[t][1]);
+          acc[t][2] = fmaf(gv[q].z, zz[q], acc[t][2]);
+          acc[t][3] = fmaf(gv[q].w, zz[q], acc[t][3]);
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      if (t0 + t < ntok) *reinterpret_cast<float4*>(xs + (t0 + t) * dp + i0) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
   }
 }
 
@@ -377,7 +456,7 @@ __device__ void load_zfp(float* zs, int ntok, int d, int dp, int rate, const Cac
 __global__ __launch_bounds__(kThreads) void enc_generic(int s, ViewDev X, int l0, GaugeDev G, CodecDev c, CacheDev k,
                                                         int t0, int tq, int TT, int* err) {
   extern __shared__ float sm[];
-  const int d = X.d, dp = d + 1;
+  const int d = X.d, dp = d + kPad;
   float* xs = sm;
   float* zs = sm + TT * dp;
   const int sv = blockIdx.y;
@@ -447,7 +526,7 @@ __global__ __launch_bounds__(kThreads) void enc_generic(int s, ViewDev X, int l0
 __global__ __launch_bounds__(kThreads) void dec_generic(int s, CacheDev k, int l0, GaugeDev G, CodecDev c, int t0,
                                                         int len, const int* pos, ViewDev Y, int TT, int* err) {
   extern __shared__ float sm[];
-  const int d = Y.d, dp = d + 1;
+  const int d = Y.d, dp = d + kPad;
   float* zs = sm;
   float* xs = sm + TT * dp;
   const int sv = blockIdx.y;
@@ -534,7 +613,7 @@ __global__ __launch_bounds__(kThreads) void dec_generic(int s, CacheDev k, int l
 __global__ __launch_bounds__(kThreads) void append_generic(int s, ViewDev Xn, int l0, const int* pos, GaugeDev G,
                                                            CodecDev c, CacheDev k, int* err) {
   extern __shared__ float sm[];
-  const int d = Xn.d, dp = d + 1;
+  const int d = Xn.d, dp = d + kPad;
   const int sv = blockIdx.x;
   const int h = sv % Xn.H, b = (sv / Xn.H) % Xn.B, lv = sv / (Xn.H * Xn.B);
   const int l = lv + l0;
@@ -618,7 +697,7 @@ hipError_t launch_encode_generic(int s, const ViewDev& X, int l0, const GaugeDev
                                  const CacheDev& k, int t0, int tq, int* err, hipStream_t st) {
   if (X.T == 0) return hipSuccess;
   const int TT = tile_tokens(c);
-  const size_t smem = size_t(2) * TT * (X.d + 1) * sizeof(float);
+  const size_t smem = size_t(2) * TT * (X.d + kPad) * sizeof(float);
   hipError_t e = set_smem((const void*)enc_generic, smem);
   if (e != hipSuccess) return e;
   dim3 grid((X.T + TT - 1) / TT, X.L * X.B * X.H);
@@ -630,7 +709,7 @@ hipError_t launch_decode_generic(int s, const CacheDev& k, int l0, const GaugeDe
                                  int len, const int* pos, const ViewDev& Y, int* err, hipStream_t st) {
   if (Y.T == 0) return hipSuccess;
   const int TT = tile_tokens(c);
-  const size_t smem = size_t(2) * TT * (Y.d + 1) * sizeof(float);
+  const size_t smem = size_t(2) * TT * (Y.d + kPad) * sizeof(float);
   hipError_t e = set_smem((const void*)dec_generic, smem);
   if (e != hipSuccess) return e;
   dim3 grid((Y.T + TT - 1) / TT, Y.L * Y.B * Y.H);
@@ -641,7 +720,7 @@ hipError_t launch_decode_generic(int s, const CacheDev& k, int l0, const GaugeDe
 hipError_t launch_append(int s, const ViewDev& Xn, int l0, const int* pos, const GaugeDev& G, const CodecDev& c,
                          const CacheDev& k, int* err, hipStream_t st) {
   const int rows = c.backend == CG_BACKEND_KIVI ? c.kg : c.bt;
-  const size_t smem = size_t(2) * rows * (Xn.d + 1) * sizeof(float);
+  const size_t smem = size_t(2) * rows * (Xn.d + kPad) * sizeof(float);
   hipError_t e = set_smem((const void*)append_generic, smem);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(append_generic, dim3(Xn.L * Xn.B * Xn.H), dim3(kThreads), smem, st, s, Xn, l0, pos, G, c, k,

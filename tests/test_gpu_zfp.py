@@ -120,3 +120,42 @@ def test_nonfinite_input_flags_and_codes_a_zero_block():
     dev = _encode_gpu(X, 0, Gd, shp, oc, T, err=err)
     assert int(err.item()) & cg.CG_FLAG_NONFINITE
     np.testing.assert_array_equal(cache_to_host(dev, oc, 0)["codes"], orc["codes"])
+
+
+def test_full_size_sampled():
+    """Llama-3-8B-shaped K at rate 4 (32 layers, 8 heads, 8192 tokens, bf16, Haar g = 128) in one
+    kv_encode call, as bench.py --workload zfp times it: sampled 64-token windows of several
+    (layer, head) slices against the oracle under the fused criterion above, and every decoded
+    value finite."""
+    W = synth.WORKLOADS["llama8b"]
+    shp = cg.shape(W.L, W.H, W.d, W.g)
+    Gd = cg.alloc_gauge(shp)
+    cg.gauge_make(cg.GAUGE_HAAR, shp, seed=W.gauge_seed, G_host=None, G_dev=Gd)
+    G = O.gauge_make(O.GAUGE_HAAR, W.L, W.H, W.d, W.g, seed=W.gauge_seed)
+    I = O.gauge_make(O.GAUGE_IDENTITY, 1, 1, W.d, W.g)
+    oc = O.Codec(backend=O.ZFP, bits=4)
+    Xh = synth.kv_tensor(W, 0)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dev = _encode_gpu(Xh, 0, Gd, shp, oc, W.T, err=err)
+    assert int(err.item()) == 0
+    Y = torch.empty((W.L, W.B, W.H, W.T, W.d), dtype=torch.bfloat16, device="cuda")
+    cg.kv_decode(0, dev, Gd, shp, to_cg(oc), 0, Y)
+    torch.cuda.synchronize()
+    assert torch.isfinite(Y.float()).all()
+    nblk = W.d // 4
+    codes = dev.codes[: W.L * W.B * W.H * (W.T // 4) * nblk * 8].view(W.L * W.B * W.H, W.T // 4, nblk, 8)
+    for l, h in ((0, 0), (13, 5), (31, 7)):
+        for t0 in (0, 4096, W.T - 64):
+            Xs = np.ascontiguousarray(Xh[l:l + 1, :, h:h + 1, t0:t0 + 64])
+            Gs = np.ascontiguousarray(G[l:l + 1, :, h:h + 1])
+            orc, _ = O.kv_encode(oc, 0, Xs, Gs, T_cap=64)
+            got = {"codes": codes[(l * W.B) * W.H + h, t0 // 4:(t0 + 64) // 4].cpu().numpy().reshape(1, 1, 1, 16, nblk, 8),
+                   "side": None, "residual": None}
+            assert (got["codes"] != orc["codes"]).any(axis=-1).mean() <= 0.02
+            z = O.kv_encode(O.Codec(backend=O.PASSTHROUGH), 0, Xs, Gs, T_cap=64)[0]["codes"]
+            zo = O.kv_decode(oc, 0, I, orc, 0, 64, out_bf16=False)
+            zg = O.kv_decode(oc, 0, I, got, 0, 64, out_bf16=False)
+            blk = lambda a: a.reshape(16, 4, nblk, 4).transpose(0, 2, 1, 3).reshape(16, nblk, 16)
+            e_orc = np.abs(blk(zo) - blk(z)).max(-1)
+            d_gpu = np.abs(blk(zg) - blk(zo)).max(-1)
+            assert (d_gpu <= 2 * e_orc + np.abs(blk(z)).max(-1) * 2.0 ** -20).all()
