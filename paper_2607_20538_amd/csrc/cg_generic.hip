@@ -10,6 +10,7 @@
 // large-group bf16 block-uniform case.
 #include "cg_internal.h"
 #include "cg_device.h"
+#include "cg_zfp.h"
 
 namespace cg {
 
@@ -233,176 +234,6 @@ __device__ void store_rows_pass(const float* zs, int ntok, int d, int dp, const 
     const int t = idx / d, ch = idx - t * d;
     out[(slc * k.T_cap + pos0 + t) * d + ch] = zs[t * dp + ch];
   }
-}
-
-// ------------------------------------------------------------------------------------------
-// zfp-style fixed-rate blocks: 4 tokens x 4 channels of z, 16 rate bits each (zfp's published
-// algorithm: block exponent, 30-bit fixed point, lifted 4-point transform along channels then
-// tokens, sequency order, negabinary, embedded bit planes with group tests)
-// ------------------------------------------------------------------------------------------
-__device__ __forceinline__ int32_t wadd(int32_t a, int32_t b) { return int32_t(uint32_t(a) + uint32_t(b)); }
-__device__ __forceinline__ int32_t wsub(int32_t a, int32_t b) { return int32_t(uint32_t(a) - uint32_t(b)); }
-__device__ __forceinline__ int32_t wdbl(int32_t a) { return int32_t(uint32_t(a) << 1); }
-
-// 1/16 [[4 4 4 4] [5 1 -1 -5] [-4 4 4 -4] [-2 6 -6 2]] applied to (a, b, c, e) by lifting
-__device__ __forceinline__ void zfp_fwd4(int32_t& a, int32_t& b, int32_t& c, int32_t& e) {
-  a = wadd(a, e) >> 1; e = wsub(e, a);
-  c = wadd(c, b) >> 1; b = wsub(b, c);
-  a = wadd(a, c) >> 1; c = wsub(c, a);
-  e = wadd(e, b) >> 1; b = wsub(b, e);
-  e = wadd(e, b >> 1); b = wsub(b, e >> 1);
-}
-__device__ __forceinline__ void zfp_inv4(int32_t& a, int32_t& b, int32_t& c, int32_t& e) {
-  b = wadd(b, e >> 1); e = wsub(e, b >> 1);
-  b = wadd(b, e); e = wsub(wdbl(e), b);
-  c = wadd(c, a); a = wsub(wdbl(a), c);
-  b = wadd(b, c); c = wsub(wdbl(c), b);
-  e = wadd(e, a); a = wsub(wdbl(a), e);
-}
-
-// sequency position k -> block entry 4 j + i (by i + j, then i^2 + j^2, then j)
-constexpr int kZfpOrder[16] = {0, 1, 4, 5, 2, 8, 6, 9, 3, 12, 10, 7, 13, 11, 14, 15};
-
-__device__ __forceinline__ uint32_t word_of(const uint32_t (&w)[4], int i) {
-  return i == 0 ? w[0] : (i == 1 ? w[1] : (i == 2 ? w[2] : w[3]));
-}
-
-// v[4 j + i]: channel i of token j.  w: the block's 16 rate bits, LSB-first.  Returns flags.
-__device__ int zfp_encode_block(const float (&v)[16], int rate, uint32_t (&w)[4]) {
-  w[0] = w[1] = w[2] = w[3] = 0u;
-  const int cap = 16 * rate;
-  int pos = 0;
-  auto put = [&](uint32_t bit) {
-    if (pos >= cap) return false;
-    const uint32_t m = bit << (pos & 31);
-    const int i = pos >> 5;
-    w[0] |= i == 0 ? m : 0u;
-    w[1] |= i == 1 ? m : 0u;
-    w[2] |= i == 2 ? m : 0u;
-    w[3] |= i == 3 ? m : 0u;
-    ++pos;
-    return true;
-  };
-  int flags = 0;
-  float amax = 0.0f;
-#pragma unroll
-  for (int k = 0; k < 16; ++k) {
-    if (!isfinite(v[k])) flags = CG_FLAG_NONFINITE;
-    else amax = fmaxf(amax, fabsf(v[k]));
-  }
-  if (flags || amax == 0.0f) {
-    put(0u);
-    return flags;
-  }
-  int e;
-  frexpf(amax, &e);
-  e = max(e, -126);
-  put(1u);
-  for (int k = 0; k < 8; ++k) put(uint32_t((e + 127) >> k) & 1u);
-  int32_t q[16];
-#pragma unroll
-  for (int k = 0; k < 16; ++k) q[k] = int32_t(ldexpf(v[k], 30 - e));  // exact scaling, truncation
-#pragma unroll
-  for (int j = 0; j < 4; ++j) zfp_fwd4(q[4 * j], q[4 * j + 1], q[4 * j + 2], q[4 * j + 3]);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) zfp_fwd4(q[i], q[4 + i], q[8 + i], q[12 + i]);
-  uint32_t u[16];
-#pragma unroll
-  for (int k = 0; k < 16; ++k) u[k] = (uint32_t(q[kZfpOrder[k]]) + 0xAAAAAAAAu) ^ 0xAAAAAAAAu;
-  int n = 0;
-  for (int plane = 31; plane >= 0; --plane) {
-    uint32_t x = 0u;
-#pragma unroll
-    for (int c = 0; c < 16; ++c) x |= ((u[c] >> plane) & 1u) << c;
-    for (int c = 0; c < n; ++c)
-      if (!put((x >> c) & 1u)) return flags;
-    x >>= n;
-    while (n < 16) {
-      if (!put(x != 0u ? 1u : 0u)) return flags;
-      if (x == 0u) break;
-      for (;;) {
-        if (n == 15) {  // the only candidate left holds the 1
-          n = 16;
-          break;
-        }
-        const uint32_t bit = x & 1u;
-        if (!put(bit)) return flags;
-        x >>= 1;
-        ++n;
-        if (bit) break;
-      }
-    }
-  }
-  return flags;
-}
-
-__device__ void zfp_decode_block(const uint32_t (&w)[4], int rate, float (&v)[16]) {
-  const int cap = 16 * rate;
-  int pos = 0;
-  auto get = [&](uint32_t& bit) {
-    if (pos >= cap) return false;
-    bit = (word_of(w, pos >> 5) >> (pos & 31)) & 1u;
-    ++pos;
-    return true;
-  };
-#pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = 0.0f;
-  uint32_t bit;
-  if (!get(bit) || !bit) return;
-  int eb = 0;
-  for (int k = 0; k < 8; ++k) {
-    if (!get(bit)) return;
-    eb |= int(bit) << k;
-  }
-  const int e = eb - 127;
-  uint32_t u[16];
-#pragma unroll
-  for (int k = 0; k < 16; ++k) u[k] = 0u;
-  int n = 0;
-  bool done = false;
-  for (int plane = 31; plane >= 0 && !done; --plane) {
-    uint32_t x = 0u;
-    for (int c = 0; c < n; ++c) {
-      if (!get(bit)) {
-        done = true;
-        break;
-      }
-      x |= bit << c;
-    }
-    while (!done && n < 16) {
-      uint32_t any;
-      if (!get(any)) {
-        done = true;
-        break;
-      }
-      if (!any) break;
-      for (;;) {
-        if (n == 15) {
-          x |= 1u << 15;
-          n = 16;
-          break;
-        }
-        if (!get(bit)) {
-          done = true;
-          break;
-        }
-        x |= bit << n;
-        ++n;
-        if (bit) break;
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < 16; ++c) u[c] |= ((x >> c) & 1u) << plane;
-  }
-  int32_t q[16];
-#pragma unroll
-  for (int k = 0; k < 16; ++k) q[kZfpOrder[k]] = int32_t((u[k] ^ 0xAAAAAAAAu) - 0xAAAAAAAAu);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) zfp_inv4(q[i], q[4 + i], q[8 + i], q[12 + i]);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) zfp_inv4(q[4 * j], q[4 * j + 1], q[4 * j + 2], q[4 * j + 3]);
-#pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = ldexpf(float(q[k]), e - 30);
 }
 
 // zfp-style rows: tile rows [4u, 4u + 4) x channels [4cb, 4cb + 4) form block (pos0 / 4 + u, cb)

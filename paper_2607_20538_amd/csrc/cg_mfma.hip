@@ -34,6 +34,7 @@
 #include "cg_internal.h"
 #include "cg_device.h"
 #include "cg_mfma_util.h"
+#include "cg_zfp.h"
 
 namespace cg {
 
@@ -154,6 +155,7 @@ __device__ __forceinline__ float row16_max(float v) {
 constexpr int kModeBU = 0;     // block-uniform (or KIVI values: n = value channel group)
 constexpr int kModePass = 1;   // error-free backend: binary32 z
 constexpr int kModeKeys = 2;   // KIVI keys: one block per channel over a 32-token group
+constexpr int kModeZfp = 3;    // zfp-style fixed-rate blocks of 4 tokens x 4 channels (BITS = rate)
 
 // Software pipeline over 32-token tiles, one barrier per tile.  Iteration t:
 //   1. block-range partials of tile t from its accumulator (64-channel blocks: wave-pair
@@ -168,7 +170,8 @@ constexpr int kModeKeys = 2;   // KIVI keys: one block per channel over a 32-tok
 // the staged copy leaves with whole-line stores instead of 32 scattered row pieces.
 template <int NP, int KS, int BITS, int NB, int MODE, int TB = 1>
 __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a) {
-  constexpr bool PASS = MODE == kModePass, KEYS = MODE == kModeKeys;
+  constexpr bool PASS = MODE == kModePass, KEYS = MODE == kModeKeys, ZFP = MODE == kModeZfp;
+  constexpr bool QUANT = !PASS && !ZFP;  // block ranges, staged codes and side words
   // token-channel tiles: one range per TB tokens x NB channels (NB spans whole waves)
   constexpr bool TILE = TB > 1;
   static_assert(!TILE || (TB == 16 && MODE == kModeBU && (NB == 64 || NB == 128)), "tile shape");
@@ -177,8 +180,11 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
   __shared__ __attribute__((aligned(16))) uint8_t xtile[kStages][kTok * kRowBytes];
   __shared__ float2 red[2][4][kTok];  // per-wave (min, max) of each token, for 64-channel blocks
   // a tile's packed rows and side words, staged so that they leave as contiguous stores
-  __shared__ __attribute__((aligned(16))) uint8_t cstage[2][PASS ? 16 : kTok * RB];
-  __shared__ uint32_t sstage[2][PASS ? 1 : kTok * NBK];  // KIVI keys: NB = 32, one word per channel
+  __shared__ __attribute__((aligned(16))) uint8_t cstage[2][QUANT ? kTok * RB : 16];
+  __shared__ uint32_t sstage[2][QUANT ? kTok * NBK : 1];  // KIVI keys: NB = 32, one word per channel
+  // zfp-style: a tile's z (binary32), coded block by block once every wave has written it
+  constexpr int ZP = kD + 4;
+  __shared__ __attribute__((aligned(16))) float ztile[ZFP ? 2 : 1][ZFP ? kTok * ZP : 4];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n = lane & 31, hc = lane >> 5;
@@ -295,6 +301,25 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
     const int si = kThreads - 1 - tid;
     if (si < (kTok / TB) * NBK && (si / NBK) * TB < nlive) a.side[crow0 / TB * NBK + si] = sstage[P][si];
   };
+  // zfp-style: thread u * 32 + cb codes block (tokens 4u .. 4u+3, channels 4cb .. 4cb+3) of the
+  // staged tile; a tile's 256 blocks are one contiguous run of the cache
+  auto zflush = [&](int tile, auto parity) {
+    constexpr int P = decltype(parity)::value;
+    const int tid = int(threadIdx.x), u = tid >> 5, cb = tid & 31;
+    if (4 * u >= a.T - tile * kTok) return;  // token counts are multiples of 4
+    float v[16];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float4 q = *(const float4*)(&ztile[P][(4 * u + j) * ZP + 4 * cb]);
+      v[4 * j] = q.x; v[4 * j + 1] = q.y; v[4 * j + 2] = q.z; v[4 * j + 3] = q.w;
+    }
+    uint32_t wd[4];
+    flags |= zfp_encode_block(v, BITS, wd);
+    const size_t blk = (cslice * size_t(a.T_cap / 4) + (a.t0 + tile * kTok) / 4) * (kD / 4) + tid;
+    uint16_t* dst = reinterpret_cast<uint16_t*>(a.codes + blk * (2 * BITS));
+#pragma unroll
+    for (int r = 0; r < BITS; ++r) dst[r] = uint16_t(wd[r >> 1] >> (16 * (r & 1)));
+  };
   // one pipeline step; P = parity of (tile - tb) selects the accumulator, LDS buffer, register
   // stage and exchange slot at compile time
   auto step = [&](int tile, auto parity) {
@@ -309,7 +334,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
     // 1. block-range partials
     bool bad = false;
     float mn = z[0], mx = z[0];
-    if constexpr (!PASS) {
+    if constexpr (QUANT) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         bad |= z[e] != z[e];
@@ -337,14 +362,27 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
     __builtin_amdgcn_s_barrier();
     if (tile + kStages - 1 < te) issue(tile + kStages - 1);
     bfrags(tile + 1);
-    if constexpr (!PASS) {
+    if constexpr (QUANT) {
       if (tile > tb) flush(tile - 1, std::integral_constant<int, P ^ 1>());
+    } else if constexpr (ZFP) {
+      if (tile > tb) zflush(tile - 1, std::integral_constant<int, P ^ 1>());
     }
     // 5. next tile on the matrix core (past the range it reads a stale buffer and is unused),
     //    this tile's epilogue on the VALU; no branch until the stores
     acc[P ^ 1] = mfma_chain<NP, KS, KEYS>(A, Bf);
 
-    if constexpr (PASS) {
+    if constexpr (ZFP) {
+      // the lane's 16 channels of token n into the staged tile (coded after the next barrier)
+      (void)live;
+#pragma unroll
+      for (int i = 0; i < KS * NP; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+      }
+      float* zr = &ztile[P][n * ZP + 32 * w + 16 * hc];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) *(float4*)(zr + 4 * q) = make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
+    } else if constexpr (PASS) {
 #pragma unroll
       for (int i = 0; i < KS * NP; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -504,8 +542,13 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
     // the last tile's staging: every wave's LDS writes done, then the final contiguous stores
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(63));
     __builtin_amdgcn_s_barrier();
-    if ((te - tb) & 1) flush(te - 1, std::integral_constant<int, 0>());
-    else flush(te - 1, std::integral_constant<int, 1>());
+    if constexpr (ZFP) {
+      if ((te - tb) & 1) zflush(te - 1, std::integral_constant<int, 0>());
+      else zflush(te - 1, std::integral_constant<int, 1>());
+    } else {
+      if ((te - tb) & 1) flush(te - 1, std::integral_constant<int, 0>());
+      else flush(te - 1, std::integral_constant<int, 1>());
+    }
   }
   ring_copy();
   if (flags && a.err) atomicOr(a.err, flags);
@@ -1358,6 +1401,7 @@ void plan(MfmaArgs& m, int nslices, int T, const void* fn) {
 template <int KS, int BITS, int NB>
 void* enc_kernel(int mode, int bt) {
   if (mode == kModePass) return (void*)enc_mfma<kNP, KS, 8, 64, kModePass>;
+  if (mode == kModeZfp) return NB == 64 ? (void*)enc_mfma<kNP, KS, BITS, 64, kModeZfp> : nullptr;
   if (mode == kModeKeys) return (void*)enc_mfma<enc_planes(BITS), KS, BITS, 32, kModeKeys>;
   if constexpr (NB >= 64) {
     if (bt == 16) return (void*)enc_mfma<enc_planes(BITS), KS, BITS, NB, kModeBU, 16>;
@@ -1507,6 +1551,7 @@ bool bits_ok(int b) { return b == 2 || b == 3 || b == 4 || b == 6 || b == 8; }
 bool mfma_encode_supported(const ViewDev& X, const GaugeDev& G, const CodecDev& c) {
   if (!X.bf16 || X.d != kD || !group_ok(G.g)) return false;
   if (c.backend == CG_BACKEND_PASSTHROUGH) return true;
+  if (c.backend == CG_BACKEND_ZFP) return bits_ok(c.bits);
   if (c.backend == CG_BACKEND_KIVI)
     return bits_ok(c.bits) && c.kg == kTok && (c.kvc == 16 || c.kvc == 32 || c.kvc == 64) && c.win % kTok == 0;
   if (c.backend != CG_BACKEND_BLOCK_UNIFORM || !bits_ok(c.bits)) return false;
@@ -1539,12 +1584,13 @@ hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G
   m.codes = k.codes; m.side = k.side; m.T_cap = k.T_cap; m.cB = k.B; m.cH = k.H;
   m.err = err;
   const bool pass = c.backend == CG_BACKEND_PASSTHROUGH, kivi = c.backend == CG_BACKEND_KIVI;
+  const bool zfp = c.backend == CG_BACKEND_ZFP;
   const bool tiles = c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt > 1;
   m.tq = kivi || tiles ? tq : X.T;
   m.ring = k.ring;
   m.ring_slots = kivi ? c.win + c.kg : (tiles ? c.bt : 0);
-  const int mode = pass ? kModePass : (kivi && s == 0 ? kModeKeys : kModeBU);
-  const int nb = pass ? 64 : (kivi ? c.kvc : c.n), bits = pass ? 8 : c.bits, bt = tiles ? c.bt : 1;
+  const int mode = pass ? kModePass : (zfp ? kModeZfp : (kivi && s == 0 ? kModeKeys : kModeBU));
+  const int nb = pass || zfp ? 64 : (kivi ? c.kvc : c.n), bits = pass ? 8 : c.bits, bt = tiles ? c.bt : 1;
   void* fn = nullptr;
   switch (ksteps(G.g)) {
     case 2: fn = enc_by_bits<2>(bits, nb, mode, bt); break;
