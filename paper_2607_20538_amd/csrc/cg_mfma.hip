@@ -1370,6 +1370,124 @@ __global__ __launch_bounds__(kThreads, OUT_BF16 ? 3 : 2) void dec_keys(MfmaArgs 
 // above: a finer grid turns the same z error into more codes moved across a rounding
 // boundary (with two planes about 3e-5 of 4-bit codes but 1.4e-4 of 6-bit codes move, against
 // the 1e-4 budget).
+// ------------------------------------------------------------------------------------------
+// decode, zfp-style blocks (4 tokens x 4 channels of zhat, 16 RATE bits each)
+// ------------------------------------------------------------------------------------------
+// A workgroup owns a range of 32-token tiles of one slice.  Per tile, thread u * 32 + cb decodes
+// block (tokens 4u .. 4u+3, channels 4cb .. 4cb+3) into a binary32 LDS tile; after a barrier
+// wave w computes output channels 32w .. 32w+31 of the 32 tokens on the matrix cores: lane
+// (n, hc) splits its 8 channels of zhat per K-step into three bf16 planes by truncation (each
+// residual exact in binary32, so the planes sum to zhat) and the five plane products that
+// matter against the two G^T planes accumulate in binary32 (as the KIVI key decoder does).
+template <int KS, int RATE, bool OUT_BF16>
+__global__ __launch_bounds__(kThreads, 2) void dec_zfp(MfmaArgs a) {
+  constexpr int ZP = kD + 4;
+  constexpr int YB = OUT_BF16 ? 2 : 4;
+  __shared__ __attribute__((aligned(16))) float ztile[kTok * ZP];
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n = lane & 31, hc = lane >> 5;
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int slice = logical / a.chunks, chunk = logical - slice * a.chunks;
+  if (slice >= a.nslices) return;
+  const int h = slice % a.H, b = (slice / a.H) % a.B, lv = slice / (a.H * a.B);
+  const int l = lv + a.l0;
+  const int ntiles = (a.T + kTok - 1) / kTok;
+  const int tb = chunk * a.tiles_per_wg;
+  const int te = min(ntiles, tb + a.tiles_per_wg);
+  if (tb >= te) return;
+  char* ys = a.x + YB * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
+  const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
+
+  const int kbase = a.g >= 32 ? (32 * w / a.g) * a.g : 32 * w;
+  const int chA = 32 * w + 16 * ((n >> 2) & 1) + 4 * (n >> 3) + (n & 3);
+  bf16x8_t A[2][KS];
+  load_a<2, KS>(A, a, l, h, chA, kbase, hc);  // rows chA of the G^T planes
+
+  const int tid = int(threadIdx.x), u = tid >> 5, cb = tid & 31;
+  for (int t = tb; t < te; ++t) {
+    // 1. blocks -> zhat tile (the view's token count and offset are multiples of 4)
+    if (4 * u < a.T - t * kTok) {
+      const size_t blk = (cslice * size_t(a.T_cap / 4) + (a.t0 + t * kTok) / 4 + u) * (kD / 4) + cb;
+      const uint16_t* src = reinterpret_cast<const uint16_t*>(a.codes + blk * (2 * RATE));
+      uint32_t wd[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int r = 0; r < RATE; ++r) wd[r >> 1] |= uint32_t(src[r]) << (16 * (r & 1));
+      float v[16];
+      zfp_decode_block(wd, RATE, v);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *(float4*)(&ztile[(4 * u + j) * ZP + 4 * cb]) = make_float4(v[4 * j], v[4 * j + 1], v[4 * j + 2], v[4 * j + 3]);
+    }
+    __syncthreads();
+    // 2. xhat = G^T zhat for the lane's token n and channels 32w + 16hc + [0, 16)
+    f32x16_t acc = {};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const float* zr = &ztile[n * ZP + kbase + 16 * kk + 8 * hc];
+      const float4 z0 = *(const float4*)zr, z1 = *(const float4*)(zr + 4);
+      const float zh[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+      uint32_t bp[3][4];
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        uint32_t x0 = __float_as_uint(zh[2 * e2]), x1 = __float_as_uint(zh[2 * e2 + 1]);
+#pragma unroll
+        for (int p = 0; p < 3; ++p) {
+          bp[p][e2] = __builtin_amdgcn_perm(x1, x0, 0x07060302u);
+          if (p < 2) {
+            x0 = __float_as_uint(__uint_as_float(x0) - __uint_as_float(x0 & 0xffff0000u));
+            x1 = __float_as_uint(__uint_as_float(x1) - __uint_as_float(x1 & 0xffff0000u));
+          }
+        }
+      }
+      bf16x8_t B[3];
+#pragma unroll
+      for (int p = 0; p < 3; ++p) B[p] = as_bf16x8(u32x4_t{bp[p][0], bp[p][1], bp[p][2], bp[p][3]});
+      // plane products, smallest first: (1,1) (0,2) (1,0) (0,1) (0,0)
+      acc = mfma(A[1][kk], B[1], acc);
+      acc = mfma(A[0][kk], B[2], acc);
+      acc = mfma(A[1][kk], B[0], acc);
+      acc = mfma(A[0][kk], B[1], acc);
+      acc = mfma(A[0][kk], B[0], acc);
+    }
+    const int row = t * kTok + n;
+    if (row < a.T) {
+      char* yr = ys + int64_t(YB) * (int64_t(row) * a.st + 32 * w + 16 * hc);
+      if constexpr (OUT_BF16) {
+        typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+        typedef float f32x2_t __attribute__((ext_vector_type(2)));
+        uint32_t pk[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          pk[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{acc[2 * e], acc[2 * e + 1]}), bf16x2_t));
+        *(u32x4_t*)yr = u32x4_t{pk[0], pk[1], pk[2], pk[3]};
+        *(u32x4_t*)(yr + 16) = u32x4_t{pk[4], pk[5], pk[6], pk[7]};
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) *(float4*)(yr + 16 * q) = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
+      }
+    }
+    __syncthreads();  // the tile is read before the next one is decoded into it
+  }
+}
+
+template <int KS, int RATE>
+void* zfp_dec_kernel(bool bf16) {
+  return bf16 ? (void*)dec_zfp<KS, RATE, true> : (void*)dec_zfp<KS, RATE, false>;
+}
+
+template <int KS>
+void* zfp_dec_by_rate(int rate, bool bf16) {
+  switch (rate) {
+    case 2: return zfp_dec_kernel<KS, 2>(bf16);
+    case 3: return zfp_dec_kernel<KS, 3>(bf16);
+    case 4: return zfp_dec_kernel<KS, 4>(bf16);
+    case 6: return zfp_dec_kernel<KS, 6>(bf16);
+    case 8: return zfp_dec_kernel<KS, 8>(bf16);
+  }
+  return nullptr;
+}
+
 constexpr int kNP = kDecPlanes;
 constexpr int enc_planes(int bits) { return bits >= 6 ? 3 : 2; }
 
@@ -1561,6 +1679,7 @@ bool mfma_encode_supported(const ViewDev& X, const GaugeDev& G, const CodecDev& 
 
 bool mfma_decode_supported(int s, const ViewDev& Y, const GaugeDev& G, const CodecDev& c) {
   if (Y.d != kD || !group_ok(G.g) || !bits_ok(c.bits)) return false;
+  if (c.backend == CG_BACKEND_ZFP) return true;
   if (c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt != 1)  // tiles: blocks inside a group, or centred groups
     return c.bt == 16 && (c.n == 64 || c.n == 128) && (G.g >= c.n || G.g <= 32);
   if (c.backend == CG_BACKEND_KIVI) {
@@ -1629,6 +1748,19 @@ hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& 
     void* fn = keys_by_bits(c.bits, Y.bf16);
     if (!fn) return hipErrorInvalidValue;
     plan(m, Y.L * Y.B * Y.H, t0 % kTok + Y.T, fn);
+    const int nwg = ((m.nslices * m.chunks + 7) / 8) * 8;
+    void* args[] = {&m};
+    return hipLaunchKernel(fn, dim3(nwg), dim3(kThreads), args, 0, st);
+  }
+  if (c.backend == CG_BACKEND_ZFP) {
+    void* fn = nullptr;
+    switch (ksteps(G.g)) {
+      case 2: fn = zfp_dec_by_rate<2>(c.bits, Y.bf16); break;
+      case 4: fn = zfp_dec_by_rate<4>(c.bits, Y.bf16); break;
+      case 8: fn = zfp_dec_by_rate<8>(c.bits, Y.bf16); break;
+    }
+    if (!fn) return hipErrorInvalidValue;
+    plan(m, Y.L * Y.B * Y.H, Y.T, fn);
     const int nwg = ((m.nslices * m.chunks + 7) / 8) * 8;
     void* args[] = {&m};
     return hipLaunchKernel(fn, dim3(nwg), dim3(kThreads), args, 0, st);
