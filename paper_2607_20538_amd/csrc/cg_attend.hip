@@ -84,6 +84,62 @@ __device__ __forceinline__ float raw_at(const CacheDev& k, const CodecDev& c, si
   return bf16_to_f32(k.ring[(slc * ringsz + p % ringsz) * d + ch]);
 }
 
+// Channels ch0 .. ch0 + 7 (ch0 % 8 == 0) of cache position p: raw bf16 tokens (raw) or the
+// dequantised gauge-space values, with as few loads as the layout allows (one or two dwords of a
+// code row and one side word per block; eight streams for KIVI keys).
+__device__ __forceinline__ void load8(const CacheDev& k, const CodecDev& c, int s, size_t slc, int p, int ch0, int d,
+                                      bool raw, float (&out)[8]) {
+  if (raw) {
+    const int ringsz = c.backend == CG_BACKEND_KIVI ? c.win + c.kg : c.bt;
+    const uint4 v = *reinterpret_cast<const uint4*>(k.ring + (slc * ringsz + p % ringsz) * d + ch0);
+    const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      out[2 * e] = __uint_as_float(wv[e] << 16);
+      out[2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
+    }
+    return;
+  }
+  if (c.backend == CG_BACKEND_PASSTHROUGH) {
+    const float* src = (const float*)k.codes + (slc * k.T_cap + p) * d + ch0;
+    const float4 a0 = *reinterpret_cast<const float4*>(src), a1 = *reinterpret_cast<const float4*>(src + 4);
+    out[0] = a0.x; out[1] = a0.y; out[2] = a0.z; out[3] = a0.w;
+    out[4] = a1.x; out[5] = a1.y; out[6] = a1.z; out[7] = a1.w;
+    return;
+  }
+  const int bits = c.bits;
+  const uint32_t mask = (1u << bits) - 1u;
+  if (c.backend == CG_BACKEND_BLOCK_UNIFORM || s == 1) {
+    const int n = c.backend == CG_BACKEND_BLOCK_UNIFORM ? c.n : c.kvc;
+    const size_t row = slc * k.T_cap + p;
+    const int rw = d * bits / 32;  // dwords per code row (n b is a multiple of 32)
+    const uint32_t* w = reinterpret_cast<const uint32_t*>(k.codes + row * (d * bits / 8));
+    const int byte = ch0 * bits / 8, d0 = byte >> 2;
+    const uint64_t chunk = ((uint64_t(w[min(d0 + 1, rw - 1)]) << 32) | w[d0]) >> ((byte & 3) * 8);
+    const uint32_t* side = k.side + (c.bt > 1 ? slc * (k.T_cap / c.bt) + p / c.bt : row) * (d / n);
+    const uint32_t s0 = side[ch0 / n], s1 = side[(ch0 + 4) / n];  // blocks of 4 channels at least
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t sw = e < 4 ? s0 : s1;
+      const uint32_t q = uint32_t(chunk >> (bits * e)) & mask;
+      out[e] = dequantize(q, f16_bits_to_f32(sw & 0xffffu), f16_bits_to_f32(sw >> 16));
+    }
+    return;
+  }
+  // KIVI keys: one stream per (token group, channel)
+  const int kg = c.kg;
+  const size_t gi = slc * (k.T_cap / kg) + p / kg;
+  const int cb = kg * bits / 8, bit = (p % kg) * bits, wd = bit >> 5, off = bit & 31;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const uint32_t* st = reinterpret_cast<const uint32_t*>(k.codes + (gi * d + ch0 + e) * cb);
+    uint32_t v = st[wd] >> off;
+    if (off + bits > 32) v |= st[wd + 1] << (32 - off);
+    const uint32_t sw = k.side[gi * d + ch0 + e];
+    out[e] = dequantize(v & mask, f16_bits_to_f32(sw & 0xffffu), f16_bits_to_f32(sw >> 16));
+  }
+}
+
 // o_i = (sum_j G_V[j][i] acc_j + accr_i) / lsum for the group of channel i, written to the output
 // view (bf16 rounded to nearest even, or binary32).  acc: LDS [nj][d].
 __device__ void finalize_rows(const AttendDev& a, const GaugeDev& G, const float* acc, const float* accr,
@@ -109,22 +165,27 @@ __device__ void finalize_rows(const AttendDev& a, const GaugeDev& G, const float
 // general kernel: any backend, group size and head dimension; one workgroup per
 // (layer, batch row, KV head, query chunk, split)
 // ------------------------------------------------------------------------------------------
-// Wave w takes the 64-position steps w, w + 4, ... of the split.  Scores: lane = position, a
-// binary32 FMA chain over the channels of the dequantised key (gauge-space query for quantised
-// positions, the raw query for raw ones).  Values: lane = channel, the running accumulators of
-// every query head are rescaled by exp(m_old - m_new) and take p_t zhat^V_t (quantised) or
-// p_t x^V_t (raw) for every position of the step.
+// The workgroup walks its positions 64 at a time: the keys of the step are dequantised into an
+// LDS tile by all threads (consecutive threads on consecutive channels of a row), each
+// (position, query) score is a binary32 FMA chain over the channels read from LDS (gauge-space
+// query for quantised positions, the raw query for raw ones), one wave updates the running
+// maximum, the weights and the normalisers, the values of the step replace the keys in the
+// tile, and each thread folds the step into its (query, channel) accumulators (rescaled by
+// exp(m_old - m_new)), quantised positions into the gauge-space sums, raw ones into the raw sums.
+constexpr int kGTile = 64;  // positions per step
+constexpr int kGAcc = 8;    // (query, channel) accumulators per thread: kJQ * d / 256 for d <= 256
+
 __global__ __launch_bounds__(kAThreads) void att_generic(AttendDev a, GaugeDev G, CodecDev c) {
   extern __shared__ float sm[];
   const int d = a.q.d, H = a.kc.H, B = a.q.B;
-  float* qg = sm;                      // [kJQ][d] scale * G_K q
-  float* qr = qg + kJQ * d;            // [kJQ][d] scale * q
-  float* pw = qr + kJQ * d;            // [4][kJQ][64] probabilities of a step
-  float* macc = pw + 4 * kJQ * kATile;  // [kJQ][d] merged gauge-space accumulator
-  float* maccr = macc + kJQ * d;       // [kJQ][d] merged raw accumulator
-  float* ml = maccr + kJQ * d;         // [4][2][kJQ] per-wave max and sum, then [2][kJQ] merged
+  const int dp = d + 4;                 // tile row pitch (16-byte aligned rows)
+  float* qg = sm;                       // [kJQ][d] scale * G_K q
+  float* qr = qg + kJQ * d;             // [kJQ][d] scale * q
+  float* tile = qr + kJQ * d;           // [kGTile][dp] keys, then values of the step
+  float* pw = tile + kGTile * dp;       // [kJQ][kGTile] scores, then weights of the step
+  float* st = pw + kJQ * kGTile;        // [3][kJQ] running max, normaliser, step factor
 
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int sp = blockIdx.x;
   int sv = blockIdx.y;
   const int qc = sv % a.nqc;
@@ -135,7 +196,7 @@ __global__ __launch_bounds__(kAThreads) void att_generic(AttendDev a, GaugeDev G
   const int hq0 = h * a.grp + j0;  // first query head of this workgroup
   const size_t slc = (size_t(l) * a.kc.B + b) * H + h;
 
-  if (threadIdx.x == 0 && a.lens && sp == 0 && qc == 0 && h == 0 && lv == 0) {
+  if (tid == 0 && a.lens && sp == 0 && qc == 0 && h == 0 && lv == 0) {
     const int n = a.lens[b];
     if ((n < 0 || n > a.kc.T_cap) && a.err) atomicOr(a.err, CG_FLAG_POS_RANGE);
   }
@@ -143,7 +204,7 @@ __global__ __launch_bounds__(kAThreads) void att_generic(AttendDev a, GaugeDev G
   const int t_begin = sp * a.chunk, t_end = min(rs.held, t_begin + a.chunk);
 
   // 1. queries: raw (scaled) and gauged (z_i = sum_j G_K[i][j] q_j, scaled)
-  for (int idx = threadIdx.x; idx < kJQ * d; idx += kAThreads) {
+  for (int idx = tid; idx < kJQ * d; idx += kAThreads) {
     const int jj = idx / d, ch = idx - jj * d;
     float v = 0.0f;
     if (jj < nj) {
@@ -152,10 +213,14 @@ __global__ __launch_bounds__(kAThreads) void att_generic(AttendDev a, GaugeDev G
     }
     qr[idx] = v;
   }
+  if (tid < kJQ) {
+    st[tid] = -INFINITY;
+    st[kJQ + tid] = 0.0f;
+  }
   __syncthreads();
   {
     const int g = G.g;
-    for (int idx = threadIdx.x; idx < kJQ * d; idx += kAThreads) {
+    for (int idx = tid; idx < kJQ * d; idx += kAThreads) {
       const int jj = idx / d, i = idx - jj * d;
       const int r = i / g, ii = i - r * g;
       const float* Gr = G.f32 + gauge_block(l, 0, h, r, G.H, G.R) * g * g + size_t(ii) * g;
@@ -166,137 +231,151 @@ __global__ __launch_bounds__(kAThreads) void att_generic(AttendDev a, GaugeDev G
     }
   }
   __syncthreads();
-  for (int idx = threadIdx.x; idx < kJQ * d; idx += kAThreads) qr[idx] *= a.scale;
-  __syncthreads();
+  for (int idx = tid; idx < kJQ * d; idx += kAThreads) qr[idx] *= a.scale;
 
-  // 2. the wave's steps
-  constexpr int kCh = 4;  // channels per lane (d <= 256)
-  float m[kJQ], ls[kJQ], acc[kJQ][kCh], accr[kJQ][kCh];
+  // this thread's accumulators: pairs tid + 256 k -> (query jj, channel ch)
+  const int npair = kJQ * d;
+  float acc[kGAcc], accr[kGAcc];
 #pragma unroll
-  for (int jj = 0; jj < kJQ; ++jj) {
-    m[jj] = -INFINITY;
-    ls[jj] = 0.0f;
-#pragma unroll
-    for (int k = 0; k < kCh; ++k) acc[jj][k] = accr[jj][k] = 0.0f;
-  }
-  float* pwv = pw + w * kJQ * kATile;
-  for (int t0 = t_begin + kATile * w; t0 < t_end; t0 += 4 * kATile) {
-    const int p = t0 + lane;
-    const bool valid = p < t_end;
-    float s[kJQ];
-#pragma unroll
-    for (int jj = 0; jj < kJQ; ++jj) s[jj] = 0.0f;
-    if (valid) {
-      const bool raw = p >= rs.tq;
-      const float* qs = raw ? qr : qg;
-      for (int ch = 0; ch < d; ++ch) {
-        const float z = raw ? raw_at(a.kc, c, slc, p, ch, d) : zhat_at(a.kc, c, 0, slc, p, ch, d);
-#pragma unroll
-        for (int jj = 0; jj < kJQ; ++jj) s[jj] = fmaf(qs[jj * d + ch], z, s[jj]);
-      }
-    }
-    float alpha[kJQ];
-#pragma unroll
-    for (int jj = 0; jj < kJQ; ++jj) {
-      const float mx = wave_max(valid ? s[jj] : -INFINITY);
-      const float mnew = fmaxf(m[jj], mx);
-      alpha[jj] = __expf(m[jj] - mnew);  // exp(-inf) = 0 on the first step
-      const float pv = valid ? __expf(s[jj] - mnew) : 0.0f;
-      ls[jj] = ls[jj] * alpha[jj] + wave_sum(pv);
-      m[jj] = mnew;
-      pwv[jj * kATile + lane] = pv;
-    }
-    // the step's probabilities are read across lanes: order the LDS writes before the reads
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-#pragma unroll
-    for (int k = 0; k < kCh; ++k) {
-#pragma unroll
-      for (int jj = 0; jj < kJQ; ++jj) {
-        acc[jj][k] *= alpha[jj];
-        accr[jj][k] *= alpha[jj];
-      }
-    }
-    const int nt = min(kATile, t_end - t0);
-    for (int tt = 0; tt < nt; ++tt) {
-      const int pp = t0 + tt;
-      const bool raw = pp >= rs.tq;
-#pragma unroll
-      for (int k = 0; k < kCh; ++k) {
-        const int ch = lane + 64 * k;
-        if (ch < d) {
-          const float z = raw ? raw_at(a.vc, c, slc, pp, ch, d) : zhat_at(a.vc, c, 1, slc, pp, ch, d);
-#pragma unroll
-          for (int jj = 0; jj < kJQ; ++jj) {
-            const float pv = pwv[jj * kATile + tt];
-            if (raw) accr[jj][k] = fmaf(pv, z, accr[jj][k]);
-            else acc[jj][k] = fmaf(pv, z, acc[jj][k]);
-          }
-        }
-      }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-  }
+  for (int k = 0; k < kGAcc; ++k) acc[k] = accr[k] = 0.0f;
 
-  // 3. merge the four waves: M = max m_w, each wave's terms scaled by exp(m_w - M)
-  if (lane == 0) {
-#pragma unroll
-    for (int jj = 0; jj < kJQ; ++jj) {
-      ml[(w * 2 + 0) * kJQ + jj] = m[jj];
-      ml[(w * 2 + 1) * kJQ + jj] = ls[jj];
-    }
-  }
-  for (int idx = threadIdx.x; idx < 2 * kJQ * d; idx += kAThreads) macc[idx] = 0.0f;
-  __syncthreads();
-  float f[kJQ];
-#pragma unroll
-  for (int jj = 0; jj < kJQ; ++jj) {
-    float M = -INFINITY;
-    for (int v = 0; v < 4; ++v) M = fmaxf(M, ml[(v * 2) * kJQ + jj]);
-    f[jj] = m[jj] == -INFINITY ? 0.0f : __expf(m[jj] - M);
-  }
-  for (int v = 0; v < 4; ++v) {
-    if (w == v) {
-#pragma unroll
-      for (int k = 0; k < kCh; ++k) {
-        const int ch = lane + 64 * k;
-        if (ch < d) {
-#pragma unroll
-          for (int jj = 0; jj < kJQ; ++jj) {
-            macc[jj * d + ch] += f[jj] * acc[jj][k];
-            maccr[jj * d + ch] += f[jj] * accr[jj][k];
-          }
-        }
-      }
+  for (int t0 = t_begin; t0 < t_end; t0 += kGTile) {
+    const int nt = min(kGTile, t_end - t0);
+    __syncthreads();  // the previous step's values are folded; qr / qg written
+    // 2. keys of the step, 8 channels per thread
+    const int d8 = d / 8;
+    for (int idx = tid; idx < nt * d8; idx += kAThreads) {
+      const int t = idx / d8, c8 = idx - t * d8;
+      const int p = t0 + t;
+      float v[8];
+      load8(a.kc, c, 0, slc, p, 8 * c8, d, p >= rs.tq, v);
+      float* dst = tile + t * dp + 8 * c8;
+      *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
     }
     __syncthreads();
-  }
-  float* mm = ml + 8 * kJQ;  // merged [2][kJQ]
-  if (threadIdx.x < kJQ) {
-    const int jj = threadIdx.x;
-    float M = -INFINITY, L = 0.0f;
-    for (int v = 0; v < 4; ++v) M = fmaxf(M, ml[(v * 2) * kJQ + jj]);
-    for (int v = 0; v < 4; ++v) {
-      const float mv = ml[(v * 2) * kJQ + jj];
-      if (mv != -INFINITY) L += ml[(v * 2 + 1) * kJQ + jj] * __expf(mv - M);
+    // 3. scores: thread (position t, query pair jq, jq + 4) reads the key row once
+    {
+      const int t = tid & (kGTile - 1), jq = tid >> 6;
+      float s0 = -INFINITY, s1 = -INFINITY;
+      if (t < nt) {
+        const float* q = (t0 + t >= rs.tq ? qr : qg);
+        const float* q0 = q + jq * d;
+        const float* q1 = q + (jq + 4) * d;
+        const float* kr = tile + t * dp;
+        s0 = s1 = 0.0f;
+        for (int ch = 0; ch < d; ch += 4) {
+          const float4 kv = *reinterpret_cast<const float4*>(kr + ch);
+          const float4 a0 = *reinterpret_cast<const float4*>(q0 + ch);
+          const float4 a1 = *reinterpret_cast<const float4*>(q1 + ch);
+          s0 = fmaf(a0.x, kv.x, s0);
+          s0 = fmaf(a0.y, kv.y, s0);
+          s0 = fmaf(a0.z, kv.z, s0);
+          s0 = fmaf(a0.w, kv.w, s0);
+          s1 = fmaf(a1.x, kv.x, s1);
+          s1 = fmaf(a1.y, kv.y, s1);
+          s1 = fmaf(a1.z, kv.z, s1);
+          s1 = fmaf(a1.w, kv.w, s1);
+        }
+      }
+      pw[jq * kGTile + t] = s0;
+      pw[(jq + 4) * kGTile + t] = s1;
     }
-    mm[jj] = M;
-    mm[kJQ + jj] = L;
+    __syncthreads();
+    // 4. online softmax (wave 0, lane = position): new maximum, weights, normaliser, factor
+    if (w == 0) {
+      for (int jj = 0; jj < nj; ++jj) {
+        const float s = pw[jj * kGTile + lane];
+        const float mold = st[jj];
+        const float mnew = fmaxf(mold, wave_max(s));
+        const float pv = lane < nt ? __expf(s - mnew) : 0.0f;
+        const float sum = wave_sum(pv);
+        pw[jj * kGTile + lane] = pv;
+        if (lane == 0) {
+          const float alpha = __expf(mold - mnew);  // exp(-inf) = 0 on the first step
+          st[jj] = mnew;
+          st[kJQ + jj] = st[kJQ + jj] * alpha + sum;
+          st[2 * kJQ + jj] = alpha;
+        }
+      }
+    }
+    // 5. values of the step (the keys are no longer read)
+    for (int idx = tid; idx < nt * d8; idx += kAThreads) {
+      const int t = idx / d8, c8 = idx - t * d8;
+      const int p = t0 + t;
+      float v[8];
+      load8(a.vc, c, 1, slc, p, 8 * c8, d, p >= rs.tq, v);
+      float* dst = tile + t * dp + 8 * c8;
+      *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+    }
+    __syncthreads();
+    // 6. fold the step into the accumulators (quantised positions of the step come first)
+    const int nq = min(nt, max(0, rs.tq - t0));
+    int pj[kGAcc], pc[kGAcc];
+#pragma unroll
+    for (int k = 0; k < kGAcc; ++k) {
+      const int pi = tid + kAThreads * k;
+      pj[k] = pi < npair ? pi / d : kJQ;  // kJQ: no pair
+      pc[k] = pi < npair ? pi - pj[k] * d : 0;
+      const float alpha = pj[k] < nj ? st[2 * kJQ + pj[k]] : 0.0f;
+      acc[k] *= alpha;
+      accr[k] *= alpha;
+    }
+    if (kAThreads % d == 0) {
+      // every pair of this thread has channel tid % d: one tile read per position
+      const int ch = tid % d;
+      for (int t = 0; t < nq; ++t) {
+        const float v = tile[t * dp + ch];
+#pragma unroll
+        for (int k = 0; k < kGAcc; ++k)
+          if (pj[k] < nj) acc[k] = fmaf(pw[pj[k] * kGTile + t], v, acc[k]);
+      }
+      for (int t = nq; t < nt; ++t) {
+        const float v = tile[t * dp + ch];
+#pragma unroll
+        for (int k = 0; k < kGAcc; ++k)
+          if (pj[k] < nj) accr[k] = fmaf(pw[pj[k] * kGTile + t], v, accr[k]);
+      }
+    } else {
+      for (int t = 0; t < nt; ++t) {
+        const bool raw = t >= nq;
+#pragma unroll
+        for (int k = 0; k < kGAcc; ++k) {
+          if (pj[k] < nj) {
+            const float pv = pw[pj[k] * kGTile + t], v = tile[t * dp + pc[k]];
+            if (raw) accr[k] = fmaf(pv, v, accr[k]);
+            else acc[k] = fmaf(pv, v, acc[k]);
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // 7. results: the accumulators into LDS (qg / qr are free), then finalize or write partials
+  float* macc = qg;
+  float* maccr = qr;
+#pragma unroll
+  for (int k = 0; k < kGAcc; ++k) {
+    const int pi = tid + kAThreads * k;
+    if (pi < npair) {
+      macc[pi] = acc[k];
+      maccr[pi] = accr[k];
+    }
   }
   __syncthreads();
   if (a.nsplit == 1) {
-    finalize_rows(a, G, macc, maccr, mm + kJQ, nj, lv, b, h, hq0);
+    finalize_rows(a, G, macc, maccr, st + kJQ, nj, lv, b, h, hq0);
     return;
   }
-  // partial results of this split
   const size_t pstride = size_t(2 + 2 * d);
   for (int jj = 0; jj < nj; ++jj) {
     float* P = a.part + ((((size_t(lv) * B + b) * a.Hq + hq0 + jj) * a.nsplit) + sp) * pstride;
-    for (int idx = threadIdx.x; idx < 2 + 2 * d; idx += kAThreads) {
+    for (int idx = tid; idx < 2 + 2 * d; idx += kAThreads) {
       float v;
-      if (idx == 0) v = mm[jj];
-      else if (idx == 1) v = mm[kJQ + jj];
+      if (idx == 0) v = st[jj];
+      else if (idx == 1) v = st[kJQ + jj];
       else if (idx < 2 + d) v = macc[jj * d + idx - 2];
       else v = maccr[jj * d + idx - 2 - d];
       P[idx] = v;
@@ -881,7 +960,7 @@ hipError_t launch_attend(const AttendDev& a, const GaugeDev& G, const CodecDev& 
     e = hipLaunchKernel(att_mfma_kernel(c.bits, nblk), dim3(a.nsplit, nrow_f), dim3(kAThreads), args, 0, st);
     if (e != hipSuccess) return e;
   } else {
-    const size_t smem = (size_t(4) * kJQ * d + 4 * kJQ * kATile + 10 * kJQ) * sizeof(float);
+    const size_t smem = (size_t(2) * kJQ * d + size_t(kGTile) * (d + 4) + kJQ * kGTile + 3 * kJQ) * sizeof(float);
     e = set_smem((const void*)att_generic, smem);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(att_generic, dim3(a.nsplit, nrow), dim3(kAThreads), smem, st, a, G, c);
