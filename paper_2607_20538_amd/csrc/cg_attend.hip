@@ -1,7 +1,7 @@
 // Decode-phase attention over the compressed caches, with the inverse gauge folded into the
-// attention consumer instead of materialising Xhat (the deployment route the paper points to
-// when it notes that recovery can be folded into downstream operations, section 3 and the
-// discussion of its timings).
+// attention consumer instead of materialising Xhat (the deployment route the paper points to:
+// some recovery can be folded into downstream projections, section 4.1; its timings include
+// explicit recovery, which deployments can fuse, section 6).
 //
 // For one query q of KV head h (query heads h * grp .. h * grp + grp - 1 share that head, as in
 // grouped-query attention) over positions [0, len):
