@@ -153,6 +153,14 @@ typedef struct cg_cache {
   int32_t len;
 } cg_cache;
 
+/* Page table of paged caches: batch row b's positions [i P, (i + 1) P) live in cache batch row
+ * (pool page) pages[b * max_pages + i], positions [0, P), P = page_size; the cache's batch
+ * dimension counts pool pages and its T_cap equals P.  pages: device int32. */
+typedef struct cg_page_table {
+  const int32_t* pages;
+  int32_t max_pages, page_size;
+} cg_page_table;
+
 /* Static message for a status code. */
 const char* cg_status_str(int32_t status);
 
@@ -269,6 +277,41 @@ size_t attend_workspace_bytes(cg_gauge_shape shp, int32_t nl, int32_t B, int32_t
 int32_t kv_attend(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* kc, const cg_cache* vc,
                   const void* G_dev, cg_gauge_shape shp, const cg_codec* codec, const int32_t* lens, float scale,
                   const cg_kv_view* out, void* workspace, int32_t* err_flag, void* stream);
+
+/* Workspace bytes of kv_attend_paged: as attend_workspace_bytes for rows of
+ * max_pages * page_size positions. */
+size_t attend_paged_workspace_bytes(cg_gauge_shape shp, int32_t nl, int32_t B, int32_t Hq, int32_t max_pages,
+                                    int32_t page_size);
+
+/* kv_attend over paged caches (section 6 names paged-KV integration among the deployment
+ * specialisations): kc / vc are page pools (block-uniform with block_t = 1, or passthrough;
+ * their B counts pages, T_cap = page size, a multiple of 64), batch row b of q reads its
+ * positions [0, lens[b]) through the page table (lens: device int32 [B], required).  A row
+ * whose length exceeds max_pages * page_size, or whose table sends a position outside the
+ * pool, sets CG_FLAG_POS_RANGE (a page outside the pool contributes nothing).  Otherwise as
+ * kv_attend.  workspace: attend_paged_workspace_bytes bytes. */
+int32_t kv_attend_paged(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* kc, const cg_cache* vc,
+                        const cg_page_table* pages, const void* G_dev, cg_gauge_shape shp, const cg_codec* codec,
+                        const int32_t* lens, float scale, const cg_kv_view* out, void* workspace, int32_t* err_flag,
+                        void* stream);
+
+/* Encode into paged caches: Z = G X, B_c = C(Z) (section 3) for the X->T tokens of every batch
+ * row b of X (shape [L][B][H][T][d]), written at row b's positions [t0, t0 + X->T), i.e. into
+ * the pool pages the table assigns to them.  t0 % 32 == 0; block-uniform with block_t = 1, or
+ * passthrough; runs on the general kernels.  Positions past the table or pages outside the
+ * pool set CG_FLAG_POS_RANGE and skip that 32-position tile.  Errors: as kv_encode. */
+int32_t kv_encode_paged(int32_t s, const cg_kv_view* X, const cg_page_table* pages, const void* G_dev,
+                        cg_gauge_shape shp, const cg_codec* codec, const cg_cache* out, int32_t t0, int32_t* err_flag,
+                        void* stream);
+
+/* Rolling append into paged caches (section 4.4 step 1, through the page table): the new key
+ * and value token of every (layer, b, h) is encoded at position pos[b] of row b, i.e. at
+ * position pos[b] mod page_size of pool page pages[b * max_pages + pos[b] / page_size].
+ * Block-uniform with block_t = 1, or passthrough.  Positions past the table or pages outside
+ * the pool set CG_FLAG_POS_RANGE and skip that row.  Errors: as kv_append_step. */
+int32_t kv_append_paged(int32_t l0, int32_t l1, const cg_kv_view* k_new, const cg_kv_view* v_new, const int32_t* pos,
+                        const cg_page_table* pages, const void* G_dev, cg_gauge_shape shp, const cg_codec* codec,
+                        const cg_cache* kc, const cg_cache* vc, int32_t* err_flag, void* stream);
 
 /* Device self-test of the two binary32 steps of the quantiser the kernels compute without a
  * division (section 4.3 block range; the oracle divides): which = 0 compares the reciprocal

@@ -25,11 +25,15 @@ DTYPE_BF16, DTYPE_F32 = 0, 1
 
 EXPORTS = ["cg_status_str", "gauge_device_bytes", "gauge_make", "cache_bytes", "kv_encode", "kv_decode",
            "kv_append_step", "spectral_workspace_bytes", "kv_spectral_stats", "attend_workspace_bytes", "kv_attend",
-           "cg_selftest"]
+           "attend_paged_workspace_bytes", "kv_attend_paged", "kv_encode_paged", "kv_append_paged", "cg_selftest"]
 
 
 class GaugeShape(C.Structure):
     _fields_ = [("L", C.c_int32), ("H", C.c_int32), ("d", C.c_int32), ("g", C.c_int32)]
+
+
+class PageTable(C.Structure):
+    _fields_ = [("pages", C.c_void_p), ("max_pages", C.c_int32), ("page_size", C.c_int32)]
 
 
 class CodecStruct(C.Structure):
@@ -91,6 +95,19 @@ def lib() -> C.CDLL:
         L.kv_attend.argtypes = [i32, i32, C.POINTER(KvView), C.POINTER(CacheStruct), C.POINTER(CacheStruct), p,
                                 GaugeShape, C.POINTER(CodecStruct), p, C.c_float, C.POINTER(KvView), p, p, p]
         L.kv_attend.restype = i32
+        L.attend_paged_workspace_bytes.argtypes = [GaugeShape, i32, i32, i32, i32, i32]
+        L.attend_paged_workspace_bytes.restype = C.c_size_t
+        L.kv_attend_paged.argtypes = [i32, i32, C.POINTER(KvView), C.POINTER(CacheStruct), C.POINTER(CacheStruct),
+                                      C.POINTER(PageTable), p, GaugeShape, C.POINTER(CodecStruct), p, C.c_float,
+                                      C.POINTER(KvView), p, p, p]
+        L.kv_attend_paged.restype = i32
+        L.kv_encode_paged.argtypes = [i32, C.POINTER(KvView), C.POINTER(PageTable), p, GaugeShape,
+                                      C.POINTER(CodecStruct), C.POINTER(CacheStruct), i32, p, p]
+        L.kv_encode_paged.restype = i32
+        L.kv_append_paged.argtypes = [i32, i32, C.POINTER(KvView), C.POINTER(KvView), p, C.POINTER(PageTable), p,
+                                      GaugeShape, C.POINTER(CodecStruct), C.POINTER(CacheStruct),
+                                      C.POINTER(CacheStruct), p, p]
+        L.kv_append_paged.restype = i32
         L.cg_selftest.argtypes = [i32, p, p]
         L.cg_selftest.restype = i32
         _lib = L
@@ -263,3 +280,38 @@ def kv_attend(l0: int, l1: int, q, kc: Cache, vc: Cache, G_dev, shp: GaugeShape,
     rc = lib().kv_attend(l0, l1, C.byref(qv), C.byref(kcs), C.byref(vcs), _ptr(G_dev), shp, C.byref(cs), _ptr(lens),
                          float(scale), C.byref(ov), _ptr(workspace), _ptr(err_flag), _stream(stream))
     _check("kv_attend", rc)
+
+
+def page_table(pages, page_size: int) -> PageTable:
+    """cg_page_table of a device int32 tensor pages [B][max_pages]."""
+    return PageTable(_ptr(pages), int(pages.shape[1]), int(page_size))
+
+
+def attend_paged_workspace_bytes(shp: GaugeShape, nl: int, B: int, Hq: int, max_pages: int, page_size: int) -> int:
+    return int(lib().attend_paged_workspace_bytes(shp, nl, B, Hq, max_pages, page_size))
+
+
+def kv_attend_paged(l0: int, l1: int, q, kc: Cache, vc: Cache, pt: PageTable, G_dev, shp: GaugeShape, codec: Codec,
+                    lens, scale: float, out, workspace=None, err_flag=None, stream=None):
+    """kv_attend over page pools kc / vc (their B counts pages, T_cap = page size) through pt."""
+    qv, ov, cs, kcs, vcs = view(q), view(out), codec.struct(), kc.struct(), vc.struct()
+    rc = lib().kv_attend_paged(l0, l1, C.byref(qv), C.byref(kcs), C.byref(vcs), C.byref(pt), _ptr(G_dev), shp,
+                               C.byref(cs), _ptr(lens), float(scale), C.byref(ov), _ptr(workspace), _ptr(err_flag),
+                               _stream(stream))
+    _check("kv_attend_paged", rc)
+
+
+def kv_encode_paged(s: int, X, pt: PageTable, G_dev, shp: GaugeShape, codec: Codec, cache: Cache, t0: int = 0,
+                    err_flag=None, stream=None):
+    v, cs, ks = view(X), codec.struct(), cache.struct()
+    rc = lib().kv_encode_paged(s, C.byref(v), C.byref(pt), _ptr(G_dev), shp, C.byref(cs), C.byref(ks), t0,
+                               _ptr(err_flag), _stream(stream))
+    _check("kv_encode_paged", rc)
+
+
+def kv_append_paged(l0: int, l1: int, k_new, v_new, pos, pt: PageTable, G_dev, shp: GaugeShape, codec: Codec,
+                    kc: Cache, vc: Cache, err_flag=None, stream=None):
+    kn, vn, cs, kcs, vcs = view(k_new), view(v_new), codec.struct(), kc.struct(), vc.struct()
+    rc = lib().kv_append_paged(l0, l1, C.byref(kn), C.byref(vn), _ptr(pos), C.byref(pt), _ptr(G_dev), shp,
+                               C.byref(cs), C.byref(kcs), C.byref(vcs), _ptr(err_flag), _stream(stream))
+    _check("kv_append_paged", rc)

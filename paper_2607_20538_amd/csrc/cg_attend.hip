@@ -50,11 +50,32 @@ struct RowSpan {
 __device__ __forceinline__ RowSpan row_span(const AttendDev& a, const CodecDev& c, int b) {
   RowSpan r;
   r.held = a.lens ? a.lens[b] : a.len;
-  if (r.held < 0 || r.held > a.kc.T_cap) r.held = 0;
+  if (r.held < 0 || r.held > a.cap) r.held = 0;
   if (c.backend == CG_BACKEND_KIVI) r.tq = r.held < c.win ? 0 : ((r.held - c.win) / c.kg) * c.kg;
   else if (c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt > 1) r.tq = (r.held / c.bt) * c.bt;
   else r.tq = r.held;
   return r;
+}
+
+// Cache slice and position offset of the step of batch row b starting at position t0 (a
+// step never crosses a page): with a page table, the slice of the page holding t0 and the
+// page's first position; without, the row's own slice and 0.  Returns false (and flags) when
+// the table sends the step outside the pool.
+__device__ __forceinline__ bool step_slice(const AttendDev& a, int l, int b, int h, int t0, size_t& slc, int& off) {
+  if (!a.pt.pages) {
+    slc = (size_t(l) * a.kc.B + b) * a.kc.H + h;
+    off = 0;
+    return true;
+  }
+  const int lp = t0 / a.pt.page_size;
+  const int pg = lp < a.pt.max_pages ? a.pt.pages[size_t(b) * a.pt.max_pages + lp] : -1;
+  if (pg < 0 || pg >= a.kc.B) {
+    if (a.err) atomicOr(a.err, CG_FLAG_POS_RANGE);
+    return false;
+  }
+  slc = (size_t(l) * a.kc.B + pg) * a.kc.H + h;
+  off = lp * a.pt.page_size;
+  return true;
 }
 
 // zhat of channel ch at quantised cache position p of slice slc (section 4.3 decode).
@@ -194,11 +215,10 @@ __global__ __launch_bounds__(kAThreads) void att_generic(AttendDev a, GaugeDev G
   const int l = lv + a.l0;
   const int j0 = qc * kJQ, nj = min(kJQ, a.grp - j0);
   const int hq0 = h * a.grp + j0;  // first query head of this workgroup
-  const size_t slc = (size_t(l) * a.kc.B + b) * H + h;
 
   if (tid == 0 && a.lens && sp == 0 && qc == 0 && h == 0 && lv == 0) {
     const int n = a.lens[b];
-    if ((n < 0 || n > a.kc.T_cap) && a.err) atomicOr(a.err, CG_FLAG_POS_RANGE);
+    if ((n < 0 || n > a.cap) && a.err) atomicOr(a.err, CG_FLAG_POS_RANGE);
   }
   const RowSpan rs = row_span(a, c, b);
   const int t_begin = sp * a.chunk, t_end = min(rs.held, t_begin + a.chunk);
@@ -241,6 +261,9 @@ __global__ __launch_bounds__(kAThreads) void att_generic(AttendDev a, GaugeDev G
 
   for (int t0 = t_begin; t0 < t_end; t0 += kGTile) {
     const int nt = min(kGTile, t_end - t0);
+    size_t sslc;
+    int poff;
+    if (!step_slice(a, l, b, h, t0, sslc, poff)) continue;  // uniform over the workgroup
     __syncthreads();  // the previous step's values are folded; qr / qg written
     // 2. keys of the step, 8 channels per thread
     const int d8 = d / 8;
@@ -248,7 +271,7 @@ __global__ __launch_bounds__(kAThreads) void att_generic(AttendDev a, GaugeDev G
       const int t = idx / d8, c8 = idx - t * d8;
       const int p = t0 + t;
       float v[8];
-      load8(a.kc, c, 0, slc, p, 8 * c8, d, p >= rs.tq, v);
+      load8(a.kc, c, 0, sslc, p - poff, 8 * c8, d, p >= rs.tq, v);
       float* dst = tile + t * dp + 8 * c8;
       *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
       *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
@@ -304,7 +327,7 @@ __global__ __launch_bounds__(kAThreads) void att_generic(AttendDev a, GaugeDev G
       const int t = idx / d8, c8 = idx - t * d8;
       const int p = t0 + t;
       float v[8];
-      load8(a.vc, c, 1, slc, p, 8 * c8, d, p >= rs.tq, v);
+      load8(a.vc, c, 1, sslc, p - poff, 8 * c8, d, p >= rs.tq, v);
       float* dst = tile + t * dp + 8 * c8;
       *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
       *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
@@ -589,15 +612,13 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
   const int l = lv + a.l0;
   const int j0 = qc * JQ, nj = min(JQ, a.grp - j0);
   const int hq0 = h * a.grp + j0;
-  const size_t slc = (size_t(l) * a.kc.B + b) * H + h;
-  const size_t crow = slc * size_t(a.kc.T_cap);
 
   if (threadIdx.x == 0 && a.lens && sp == 0 && qc == 0 && h == 0 && lv == 0) {
     const int nn = a.lens[b];
-    if ((nn < 0 || nn > a.kc.T_cap) && a.err) atomicOr(a.err, CG_FLAG_POS_RANGE);
+    if ((nn < 0 || nn > a.cap) && a.err) atomicOr(a.err, CG_FLAG_POS_RANGE);
   }
   int held = a.lens ? a.lens[b] : a.len;
-  if (held < 0 || held > a.kc.T_cap) held = 0;
+  if (held < 0 || held > a.cap) held = 0;
   const int t_begin = sp * a.chunk, t_end = min(held, t_begin + a.chunk);
 
   // 1. queries: macc <- q, qt <- scale G_K q, qsum <- the per-block sums of its two planes
@@ -682,18 +703,21 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
   const uint32_t vcb = uint32_t(n) * BITS;                             // value chunk byte in the row
   const uint32_t voff = uint32_t(8 * gq) * RB + (vcb & ~3u);           // its first dword, token 8 gq
   const uint32_t vsh = (vcb & 3u) * 8;                                 // chunk bit offset in that dword
-  const uint8_t* kslice = a.kc.codes + crow * RB;
-  const uint8_t* vslice = a.vc.codes + crow * RB;
-  const uint32_t* ksside = a.kc.side + crow * NBLK;
-  const uint32_t* vsside = a.vc.side + crow * NBLK;
 
   // One 32-position step; FULL: all 32 positions lie before t_end (no clamping)
   auto step = [&](int t0, auto fullc) {
     constexpr bool FULL = decltype(fullc)::value;
     const int lim = t_end - 1 - t0;  // last valid position offset in the step
     auto clampt = [&](int x) { return FULL ? x : min(x, lim); };
-    const uint8_t* kb = kslice + size_t(t0) * RB;
-    const uint8_t* vb = vslice + size_t(t0) * RB;
+    // cache row of position t0 (a step never crosses a page)
+    size_t sslc;
+    int poff;
+    if (!step_slice(a, l, b, h, t0, sslc, poff)) return;  // uniform over the wave
+    const size_t srow = sslc * size_t(a.kc.T_cap) + (t0 - poff);
+    const uint8_t* kb = a.kc.codes + srow * RB;
+    const uint8_t* vb = a.vc.codes + srow * RB;
+    const uint32_t* ksd = a.kc.side + srow * NBLK;
+    const uint32_t* vsdg = a.vc.side + srow * NBLK;
     // loads: key regions of tokens t0 + 16 sb + n, value chunks of tokens t0 + 8 gq + e
     uint32_t rk[2][BITS];
     uint32_t swk[2][NBLK];
@@ -703,7 +727,7 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
           kb + (FULL ? koff + 16u * sb * RB : uint32_t(clampt(16 * sb + n)) * RB + uint32_t(gq) * BITS * 4));
 #pragma unroll
       for (int i = 0; i < BITS; ++i) rk[sb][i] = src[i];
-      const uint32_t* sd = ksside + size_t(t0) * NBLK + uint32_t(clampt(16 * sb + n)) * NBLK;
+      const uint32_t* sd = ksd + uint32_t(clampt(16 * sb + n)) * NBLK;
 #pragma unroll
       for (int k = 0; k < NBLK; ++k) swk[sb][k] = sd[k];
     }
@@ -722,7 +746,7 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
     }
     if (lane < 32 * NBLK) {
       const int k = lane >> 5, t = lane & 31;
-      vsd[w][k][t] = vsside[(size_t(t0) + clampt(t)) * NBLK + k];
+      vsd[w][k][t] = vsdg[size_t(clampt(t)) * NBLK + k];
     }
 
     // scores of the two 16-token halves

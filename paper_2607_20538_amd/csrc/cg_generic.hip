@@ -285,7 +285,7 @@ __device__ void load_zfp(float* zs, int ntok, int d, int dp, int rate, const Cac
 // encode
 // ------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void enc_generic(int s, ViewDev X, int l0, GaugeDev G, CodecDev c, CacheDev k,
-                                                        int t0, int tq, int TT, int* err) {
+                                                        int t0, int tq, int TT, int* err, PageDev pt) {
   extern __shared__ float sm[];
   const int d = X.d, dp = d + kPad;
   float* xs = sm;
@@ -295,7 +295,17 @@ __global__ __launch_bounds__(kThreads) void enc_generic(int s, ViewDev X, int l0
   const int l = lv + l0;
   const int tile0 = blockIdx.x * TT;
   const int ntok = min(TT, X.T - tile0);
-  const size_t slc = (size_t(l) * k.B + b) * k.H + h;
+  int crow = b;  // cache batch row: the page of a paged cache (a tile never crosses a page)
+  if (pt.pages) {
+    const int lp = (t0 + tile0) / pt.page_size;
+    crow = lp < pt.max_pages ? pt.pages[size_t(b) * pt.max_pages + lp] : -1;
+    if (crow < 0 || crow >= k.B) {
+      if (threadIdx.x == 0 && err) atomicOr(err, CG_FLAG_POS_RANGE);
+      return;
+    }
+    t0 -= lp * pt.page_size;  // positions inside the page
+  }
+  const size_t slc = (size_t(l) * k.B + crow) * k.H + h;
   const size_t xbase = size_t(lv) * X.sl + size_t(b) * X.sb + size_t(h) * X.sh;
 
   if (c.backend == CG_BACKEND_KIVI && tile0 >= tq) {
@@ -442,15 +452,26 @@ __global__ __launch_bounds__(kThreads) void dec_generic(int s, CacheDev k, int l
 // rolling append: one workgroup per (layer, b, h)
 // ------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void append_generic(int s, ViewDev Xn, int l0, const int* pos, GaugeDev G,
-                                                           CodecDev c, CacheDev k, int* err) {
+                                                           CodecDev c, CacheDev k, int* err, PageDev pt) {
   extern __shared__ float sm[];
   const int d = Xn.d, dp = d + kPad;
   const int sv = blockIdx.x;
   const int h = sv % Xn.H, b = (sv / Xn.H) % Xn.B, lv = sv / (Xn.H * Xn.B);
   const int l = lv + l0;
-  const size_t slc = (size_t(l) * k.B + b) * k.H + h;
   const size_t xbase = size_t(lv) * Xn.sl + size_t(b) * Xn.sb + size_t(h) * Xn.sh;
-  const int p = pos[b];
+  int p = pos[b];
+  int row = b;  // cache batch row (the page of a paged cache)
+  if (pt.pages) {
+    // the position's page; a position past the table or a page outside the pool is an error
+    const int lp = p >= 0 ? p / pt.page_size : -1;
+    row = lp >= 0 && lp < pt.max_pages ? pt.pages[size_t(b) * pt.max_pages + lp] : -1;
+    if (row < 0 || row >= k.B) {
+      if (threadIdx.x == 0 && err) atomicOr(err, CG_FLAG_POS_RANGE);
+      return;
+    }
+    p -= lp * pt.page_size;
+  }
+  const size_t slc = (size_t(l) * k.B + row) * k.H + h;
   if (p < 0 || p >= k.T_cap) {
     if (threadIdx.x == 0 && err) atomicOr(err, CG_FLAG_POS_RANGE);
     return;
@@ -525,14 +546,14 @@ hipError_t set_smem(const void* fn, size_t bytes) {
 }  // namespace
 
 hipError_t launch_encode_generic(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c,
-                                 const CacheDev& k, int t0, int tq, int* err, hipStream_t st) {
+                                 const CacheDev& k, int t0, int tq, int* err, hipStream_t st, const PageDev& pt) {
   if (X.T == 0) return hipSuccess;
   const int TT = tile_tokens(c);
   const size_t smem = size_t(2) * TT * (X.d + kPad) * sizeof(float);
   hipError_t e = set_smem((const void*)enc_generic, smem);
   if (e != hipSuccess) return e;
   dim3 grid((X.T + TT - 1) / TT, X.L * X.B * X.H);
-  hipLaunchKernelGGL(enc_generic, grid, dim3(kThreads), smem, st, s, X, l0, G, c, k, t0, tq, TT, err);
+  hipLaunchKernelGGL(enc_generic, grid, dim3(kThreads), smem, st, s, X, l0, G, c, k, t0, tq, TT, err, pt);
   return hipGetLastError();
 }
 
@@ -549,13 +570,13 @@ hipError_t launch_decode_generic(int s, const CacheDev& k, int l0, const GaugeDe
 }
 
 hipError_t launch_append(int s, const ViewDev& Xn, int l0, const int* pos, const GaugeDev& G, const CodecDev& c,
-                         const CacheDev& k, int* err, hipStream_t st) {
+                         const CacheDev& k, int* err, hipStream_t st, const PageDev& pt) {
   const int rows = c.backend == CG_BACKEND_KIVI ? c.kg : c.bt;
   const size_t smem = size_t(2) * rows * (Xn.d + kPad) * sizeof(float);
   hipError_t e = set_smem((const void*)append_generic, smem);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(append_generic, dim3(Xn.L * Xn.B * Xn.H), dim3(kThreads), smem, st, s, Xn, l0, pos, G, c, k,
-                     err);
+                     err, pt);
   return hipGetLastError();
 }
 

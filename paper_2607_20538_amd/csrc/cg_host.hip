@@ -1,6 +1,7 @@
 // Host side of the C ABI: argument validation, gauge construction (gauge_make), buffer
 // sizing and dispatch of the encode / decode / rolling-append kernels.
 #include <math.h>
+#include <climits>
 #include <algorithm>
 #include <stdlib.h>
 #include <string.h>
@@ -679,8 +680,132 @@ int32_t kv_attend(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* k
   a.nqc = p.nqc;
   a.part = static_cast<float*>(workspace);
   a.err = err_flag;
+  a.cap = kc->T_cap;
   hipError_t e = launch_attend(a, gauge_dev(G_dev, shp), codec_dev(codec), force_generic(),
                                static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
+}
+
+// page tables: block-uniform per-token blocks or passthrough, pages of a multiple of 64 positions
+static int32_t check_pages(const cg_page_table* pt, const cg_codec* codec, const cg_cache* kc) {
+  if (!pt || !pt->pages || pt->max_pages <= 0) return CG_ERR_ARG;
+  if (reinterpret_cast<uintptr_t>(pt->pages) & 3u) return CG_ERR_ALIGN;
+  const bool ok = codec->backend == CG_BACKEND_PASSTHROUGH ||
+                  (codec->backend == CG_BACKEND_BLOCK_UNIFORM && codec->block_t == 1);
+  if (!ok) return CG_ERR_UNSUPPORTED;
+  if (pt->page_size <= 0 || pt->page_size % 64 || pt->page_size != kc->T_cap) return CG_ERR_SHAPE;
+  return CG_OK;
+}
+
+size_t attend_paged_workspace_bytes(cg_gauge_shape shp, int32_t nl, int32_t B, int32_t Hq, int32_t max_pages,
+                                    int32_t page_size) {
+  if (max_pages <= 0 || page_size <= 0 || int64_t(max_pages) * page_size > INT32_MAX) return 0;
+  return attend_workspace_bytes(shp, nl, B, Hq, max_pages * page_size);
+}
+
+int32_t kv_attend_paged(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* kc, const cg_cache* vc,
+                        const cg_page_table* pages, const void* G_dev, cg_gauge_shape shp, const cg_codec* codec,
+                        const int32_t* lens, float scale, const cg_kv_view* out, void* workspace, int32_t* err_flag,
+                        void* stream) {
+  int32_t rc = check_shape(shp);
+  if (rc != CG_OK) return rc;
+  if (!G_dev || !lens || l0 < 0 || l1 <= l0 || l1 > shp.L || !isfinite(scale)) return CG_ERR_ARG;
+  if (!aligned16(G_dev)) return CG_ERR_ALIGN;
+  if (reinterpret_cast<uintptr_t>(lens) & 3u) return CG_ERR_ALIGN;
+  if ((rc = check_codec(codec, shp.d)) != CG_OK) return rc;
+  const int nl = l1 - l0;
+  if ((rc = check_qview(q, shp, nl)) != CG_OK) return rc;
+  if ((rc = check_qview(out, shp, nl)) != CG_OK) return rc;
+  if (out->B != q->B || out->H != q->H) return CG_ERR_SHAPE;
+  // the caches are page pools: their batch dimension counts pages
+  if (!kc || !vc) return CG_ERR_ARG;
+  if ((rc = check_cache(kc, codec, shp, kc->B)) != CG_OK) return rc;
+  if ((rc = check_cache(vc, codec, shp, kc->B)) != CG_OK) return rc;
+  if (kc->T_cap != vc->T_cap) return CG_ERR_SHAPE;
+  if ((rc = check_pages(pages, codec, kc)) != CG_OK) return rc;
+  if (int64_t(pages->max_pages) * pages->page_size > INT32_MAX) return CG_ERR_CAPACITY;
+  const int cap = pages->max_pages * pages->page_size;
+  const AttendPlan p = attend_plan(nl, q->B, shp.H, q->H, shp.d, cap);
+  if (p.ws_bytes && (!workspace || !aligned16(workspace))) return workspace ? CG_ERR_ALIGN : CG_ERR_ARG;
+  if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
+  AttendDev a;
+  a.q = view_dev(q);
+  a.o = view_dev(out);
+  a.kc = cache_dev(kc);
+  a.vc = cache_dev(vc);
+  a.l0 = l0;
+  a.Hq = q->H;
+  a.grp = q->H / shp.H;
+  a.lens = lens;
+  a.len = 0;
+  a.scale = scale;
+  a.nsplit = p.nsplit;
+  a.chunk = p.chunk;
+  a.nqc = p.nqc;
+  a.part = static_cast<float*>(workspace);
+  a.err = err_flag;
+  a.pt.pages = pages->pages;
+  a.pt.max_pages = pages->max_pages;
+  a.pt.page_size = pages->page_size;
+  a.cap = cap;
+  hipError_t e = launch_attend(a, gauge_dev(G_dev, shp), codec_dev(codec), force_generic(),
+                               static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
+}
+
+int32_t kv_encode_paged(int32_t s, const cg_kv_view* X, const cg_page_table* pages, const void* G_dev,
+                        cg_gauge_shape shp, const cg_codec* codec, const cg_cache* out, int32_t t0, int32_t* err_flag,
+                        void* stream) {
+  int32_t rc = check_shape(shp);
+  if (rc != CG_OK) return rc;
+  if (s < 0 || s > 1 || !G_dev) return CG_ERR_ARG;
+  if (!aligned16(G_dev)) return CG_ERR_ALIGN;
+  if ((rc = check_codec(codec, shp.d)) != CG_OK) return rc;
+  if ((rc = check_view(X, shp, shp.L)) != CG_OK) return rc;
+  if (!out) return CG_ERR_ARG;
+  if ((rc = check_cache(out, codec, shp, out->B)) != CG_OK) return rc;
+  if ((rc = check_pages(pages, codec, out)) != CG_OK) return rc;
+  if (t0 < 0) return CG_ERR_ARG;
+  if (t0 % 32) return CG_ERR_UNSUPPORTED;  // 32-position tiles stay inside one page
+  if (int64_t(t0) + X->T > int64_t(pages->max_pages) * pages->page_size) return CG_ERR_CAPACITY;
+  if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
+  PageDev pt;
+  pt.pages = pages->pages;
+  pt.max_pages = pages->max_pages;
+  pt.page_size = pages->page_size;
+  hipError_t e = launch_encode_generic(s, view_dev(X), 0, gauge_dev(G_dev, shp), codec_dev(codec), cache_dev(out), t0,
+                                       X->T, err_flag, static_cast<hipStream_t>(stream), pt);
+  return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
+}
+
+int32_t kv_append_paged(int32_t l0, int32_t l1, const cg_kv_view* k_new, const cg_kv_view* v_new, const int32_t* pos,
+                        const cg_page_table* pages, const void* G_dev, cg_gauge_shape shp, const cg_codec* codec,
+                        const cg_cache* kc, const cg_cache* vc, int32_t* err_flag, void* stream) {
+  int32_t rc = check_shape(shp);
+  if (rc != CG_OK) return rc;
+  if (!G_dev || !pos || l0 < 0 || l1 <= l0 || l1 > shp.L) return CG_ERR_ARG;
+  if (!aligned16(G_dev)) return CG_ERR_ALIGN;
+  if ((reinterpret_cast<uintptr_t>(pos) & 3u)) return CG_ERR_ALIGN;
+  if ((rc = check_codec(codec, shp.d)) != CG_OK) return rc;
+  const int nl = l1 - l0;
+  if ((rc = check_view(k_new, shp, nl)) != CG_OK) return rc;
+  if ((rc = check_view(v_new, shp, nl)) != CG_OK) return rc;
+  if (k_new->T != 1 || v_new->T != 1 || v_new->B != k_new->B) return CG_ERR_SHAPE;
+  if (!kc || !vc) return CG_ERR_ARG;
+  if ((rc = check_cache(kc, codec, shp, kc->B)) != CG_OK) return rc;
+  if ((rc = check_cache(vc, codec, shp, kc->B)) != CG_OK) return rc;
+  if (kc->T_cap != vc->T_cap) return CG_ERR_SHAPE;
+  if ((rc = check_pages(pages, codec, kc)) != CG_OK) return rc;
+  if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const GaugeDev G = gauge_dev(G_dev, shp);
+  const CodecDev c = codec_dev(codec);
+  PageDev pt;
+  pt.pages = pages->pages;
+  pt.max_pages = pages->max_pages;
+  pt.page_size = pages->page_size;
+  hipError_t e = launch_append(0, view_dev(k_new), l0, pos, G, c, cache_dev(kc), err_flag, st, pt);
+  if (e == hipSuccess) e = launch_append(1, view_dev(v_new), l0, pos, G, c, cache_dev(vc), err_flag, st, pt);
   return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
 }
 

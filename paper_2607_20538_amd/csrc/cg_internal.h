@@ -85,9 +85,18 @@ struct CacheDev {
   int L, B, H, T_cap, d;
 };
 
+// Paged caches: batch row b's position t lives in cache row (page, t mod page_size) with
+// page = pages[b * max_pages + t / page_size] (the cache's batch dimension is the page pool);
+// pages == nullptr: row b is cache batch row b.
+struct PageDev {
+  const int* pages = nullptr;
+  int max_pages = 0, page_size = 0;
+};
+
 // Generic (VALU) kernels: every supported configuration.
 hipError_t launch_encode_generic(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c,
-                                 const CacheDev& k, int t0, int tq, int* err, hipStream_t st);
+                                 const CacheDev& k, int t0, int tq, int* err, hipStream_t st,
+                                 const PageDev& pt = PageDev());
 hipError_t launch_decode_generic(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
                                  int len, const int* pos, const ViewDev& Y, int* err, hipStream_t st);
 
@@ -122,6 +131,8 @@ struct AttendDev {
   int nqc;               // query chunks of at most 8 heads per workgroup
   float* part;           // partial results [nl][B][Hq][nsplit][2 + 2d] when nsplit > 1
   int* err;
+  PageDev pt;            // paged caches (block-uniform per-token blocks or passthrough)
+  int cap;               // positions a row can hold: T_cap, or max_pages * page_size
 };
 struct AttendPlan {
   int nsplit = 1, chunk = 64, nqc = 1;
@@ -148,6 +159,6 @@ hipError_t launch_decode(int s, const CacheDev& k, int l0, const GaugeDev& G, co
                          const int* pos, const ViewDev& Y, int* err, hipStream_t st);
 // Rolling append of one token per (layer, b, h) at pos[b] (layer l of Xn is cache layer l + l0).
 hipError_t launch_append(int s, const ViewDev& Xn, int l0, const int* pos, const GaugeDev& G, const CodecDev& c,
-                         const CacheDev& k, int* err, hipStream_t st);
+                         const CacheDev& k, int* err, hipStream_t st, const PageDev& pt = PageDev());
 
 }  // namespace cg

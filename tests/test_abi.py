@@ -261,6 +261,47 @@ def test_zfp_backend_sizes_and_restrictions():
                               C.byref(q), 0x70000, None, None) == cg.CG_ERR_UNSUPPORTED
 
 
+def test_paged_entry_points_reject_invalid_arguments():
+    shp = cg.shape(2, 2, 64, 16)
+    q = _fake_view(L=1, H=4, T=1, strides=(256, 256, 64, 64))
+    pool = _fake_cache(L=2, B=5, T_cap=64)
+    pt = cg.PageTable(0x90000, 3, 64)
+    f = cg.lib().kv_attend_paged
+    def att(**kw):
+        a = dict(dict(q=q, kc=pool, vc=pool, pt=pt, codec=BU, lens=0x60000, ws=0x70000), **kw)
+        cs = a["codec"].struct()
+        ptr = None if a["pt"] is None else C.byref(a["pt"])
+        return f(0, 1, C.byref(a["q"]), C.byref(a["kc"]), C.byref(a["vc"]), ptr, 0x50000, shp, C.byref(cs),
+                 a["lens"], 0.1, C.byref(a["q"]), a["ws"], None, None)
+    assert att(lens=None) == cg.CG_ERR_ARG                                        # lengths required
+    assert att(pt=None) == cg.CG_ERR_ARG
+    assert att(pt=cg.PageTable(0, 3, 64)) == cg.CG_ERR_ARG
+    assert att(pt=cg.PageTable(0x90002, 3, 64)) == cg.CG_ERR_ALIGN
+    assert att(pt=cg.PageTable(0x90000, 3, 32)) == cg.CG_ERR_SHAPE               # page size != T_cap
+    assert att(pt=cg.PageTable(0x90000, 3, 96), kc=_fake_cache(L=2, B=5, T_cap=96),
+               vc=_fake_cache(L=2, B=5, T_cap=96)) == cg.CG_ERR_SHAPE             # not a multiple of 64
+    assert att(codec=cg.Codec(cg.KIVI, 3, 64, 32, 64, 128), kc=_fake_cache(L=2, B=5, T_cap=64),
+               vc=_fake_cache(L=2, B=5, T_cap=64)) == cg.CG_ERR_UNSUPPORTED       # windows are per row
+    assert att(codec=cg.Codec(cg.BLOCK_UNIFORM, 4, 32, block_t=16)) == cg.CG_ERR_UNSUPPORTED
+    assert att(vc=_fake_cache(L=2, B=4, T_cap=64)) == cg.CG_ERR_SHAPE            # pools differ
+    assert cg.attend_paged_workspace_bytes(shp, 1, 1, 4, 0, 64) == 0
+    assert cg.attend_paged_workspace_bytes(shp, 1, 1, 4, 64, 64) == cg.attend_workspace_bytes(shp, 1, 1, 4, 4096)
+    # paged encode: t0 on a 32-position boundary, within the table
+    X = _fake_view(L=2, T=32)
+    cs = BU.struct()
+    enc = cg.lib().kv_encode_paged
+    assert enc(0, C.byref(X), C.byref(pt), 0x50000, shp, C.byref(cs), C.byref(pool), 16, None, None) == cg.CG_ERR_UNSUPPORTED
+    assert enc(0, C.byref(X), C.byref(pt), 0x50000, shp, C.byref(cs), C.byref(pool), 192, None, None) == cg.CG_ERR_CAPACITY
+    assert enc(0, C.byref(X), None, 0x50000, shp, C.byref(cs), C.byref(pool), 0, None, None) == cg.CG_ERR_ARG
+    # paged append
+    kn = _fake_view(L=1, T=1, strides=(128, 128, 64, 64))
+    app = cg.lib().kv_append_paged
+    assert app(0, 1, C.byref(kn), C.byref(kn), None, C.byref(pt), 0x50000, shp, C.byref(cs), C.byref(pool),
+               C.byref(pool), None, None) == cg.CG_ERR_ARG
+    assert app(0, 1, C.byref(kn), C.byref(kn), 0x60000, C.byref(cg.PageTable(0x90000, 3, 32)), 0x50000, shp,
+               C.byref(cs), C.byref(pool), C.byref(pool), None, None) == cg.CG_ERR_SHAPE
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(cg, "LIB_PATH", str(tmp_path / "missing.so"))
     monkeypatch.setattr(cg, "_lib", None)
