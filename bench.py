@@ -36,7 +36,7 @@ def parse():
                     help="HBM traffic per launch measured with rocprofv3 counters (optional)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the timed region, run one plain 512 MiB device copy (counter calibration)")
-    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral", "attend", "zfp"]),
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral", "attend", "attend_paged", "zfp"]),
                     help="llama8b (default) prints the headline line; the others print per-kernel timings of "
                          "the KIVI, rolling-step and 27B-sweep workloads")
     return ap.parse_args()
@@ -132,7 +132,7 @@ def other_workload(name, steps, warmup):
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral", "zfp") else ("rolling" if name == "attend" else name)]
+    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral", "zfp") else ("rolling" if name in ("attend", "attend_paged") else name)]
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     out = {"workload": name, "shape": {"L": w.L, "B": w.B, "H": w.H, "T": w.T, "d": w.d}, "steps": steps}
 
@@ -211,6 +211,59 @@ def other_workload(name, steps, warmup):
                 torch.cuda.empty_cache()
             rows.append(row)
         out["runs"] = rows
+    elif name == "attend_paged":
+        # the attention workload over page pools: 256-position pages in a seeded random order,
+        # the history encoded through the page table, one paged append + paged attention per step
+        grp, P = 4, 256
+        shp = cg.shape(w.L, w.H, w.d, w.g)
+        codec = cg.Codec(cg.BLOCK_UNIFORM, w.bits, w.block_c)
+        Gd = cg.alloc_gauge(shp)
+        cg.gauge_make(cg.GAUGE_HAAR, shp, seed=w.gauge_seed, G_host=None, G_dev=Gd)
+        maxp = (w.T + warmup + 2 * steps + 1 + P - 1) // P
+        perm = np.random.default_rng(w.data_seed).permutation(w.B * maxp).astype(np.int32)
+        pages = torch.from_numpy(perm.reshape(w.B, maxp)).cuda()
+        pt = cg.page_table(pages, P)
+        pools, news = [], []
+        for s in (0, 1):
+            X = layer_view(s)
+            c = cg.Cache(codec, s, w.L, w.B * maxp, w.H, P, w.d)
+            cg.kv_encode_paged(s, X, pt, Gd, shp, codec, c, 0, err_flag=err, stream=stream.cuda_stream)
+            torch.cuda.synchronize()
+            del X
+            pools.append(c)
+            nt = synth.kv_tensor(w, s, L=1, T=1, t_offset=w.T)
+            nt = torch.from_numpy(nt.view(np.int16)).view(torch.bfloat16).cuda()
+            news.append(nt.expand(w.L, w.B, w.H, 1, w.d))
+        q = torch.from_numpy(synth.queries(w, w.H * grp).view(np.int16)).view(torch.bfloat16).cuda()
+        q = q.reshape(w.L, w.B, w.H * grp, 1, w.d)
+        o = torch.empty((w.L, w.B, w.H * grp, 1, w.d), dtype=torch.bfloat16, device="cuda")
+        ws = torch.empty(max(16, cg.attend_paged_workspace_bytes(shp, w.L, w.B, w.H * grp, maxp, P)),
+                         dtype=torch.uint8, device="cuda")
+        pos = torch.full((w.B,), w.T, dtype=torch.int32, device="cuda")
+        lens = pos + 1
+        scale = 1.0 / float(np.sqrt(w.d))
+
+        def attend():
+            cg.kv_attend_paged(0, w.L, q, pools[0], pools[1], pt, Gd, shp, codec, lens, scale, o, ws, err_flag=err,
+                               stream=stream.cuda_stream)
+
+        def step():
+            cg.kv_append_paged(0, w.L, news[0], news[1], pos, pt, Gd, shp, codec, pools[0], pools[1], err_flag=err,
+                               stream=stream.cuda_stream)
+            attend()
+            pos.add_(1)
+            lens.add_(1)
+
+        ms = _timed(step, steps, warmup, stream)
+        ms_att = _timed(attend, steps, 0, stream)
+        held = int(lens[0].item())
+        per_pos = 2 * (w.d * w.bits // 8 + 4 * (w.d // w.block_c))     # K and V codes + side words
+        out["step_ms"] = round(ms, 3)
+        out["attend_ms"] = round(ms_att, 3)
+        out["history_tokens"] = held
+        out["page_size"] = P
+        out["query_heads"] = w.H * grp
+        out["attend_GBps"] = round(w.L * w.B * w.H * held * per_pos / ms_att / 1e6, 1)
     elif name == "attend":
         # the rolling step with the history consumed by fused decode-phase attention instead of
         # being decoded to bf16: append one token per (layer, b, h), then attention of the
