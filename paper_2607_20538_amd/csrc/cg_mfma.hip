@@ -137,18 +137,34 @@ __device__ __forceinline__ f32x16_t mfma_chain(const bf16x8_t (&A)[NP][KS], cons
   return acc;
 }
 
+// Block ranges use the IEEE minimum / maximum (v_minimum3_f32 / v_maximum3_f32): equal to the
+// ordinary min / max on finite and infinite values, and NaN as soon as one element is NaN, so
+// a single test of the range flags a non-finite block (whose codes are unspecified).
+__device__ __forceinline__ float min_nan(float a, float b) { return __builtin_elementwise_minimum(a, b); }
+__device__ __forceinline__ float max_nan(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
 // min / max over the 16 lanes of a DPP row (quad swaps, then rotations by 4 and 8 lanes)
 __device__ __forceinline__ float row16_min(float v) {
-  v = fminf(v, dpp_mov<0xB1>(v));   // quad_perm [1,0,3,2]
-  v = fminf(v, dpp_mov<0x4E>(v));   // quad_perm [2,3,0,1]
-  v = fminf(v, dpp_mov<0x124>(v));  // row_ror:4
-  return fminf(v, dpp_mov<0x128>(v));  // row_ror:8
+  v = min_nan(v, dpp_mov<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = min_nan(v, dpp_mov<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = min_nan(v, dpp_mov<0x124>(v));  // row_ror:4
+  return min_nan(v, dpp_mov<0x128>(v));  // row_ror:8
 }
 __device__ __forceinline__ float row16_max(float v) {
-  v = fmaxf(v, dpp_mov<0xB1>(v));
-  v = fmaxf(v, dpp_mov<0x4E>(v));
-  v = fmaxf(v, dpp_mov<0x124>(v));
-  return fmaxf(v, dpp_mov<0x128>(v));
+  v = max_nan(v, dpp_mov<0xB1>(v));
+  v = max_nan(v, dpp_mov<0x4E>(v));
+  v = max_nan(v, dpp_mov<0x124>(v));
+  return max_nan(v, dpp_mov<0x128>(v));
+}
+
+// (min, max) of a lane and the lane 32 away.  v_permlane32_swap exchanges the upper half-wave
+// of one register with the lower half-wave of another; with both registers holding the value,
+// the two results hold, in every lane, the lane's own value and its partner's.
+__device__ __forceinline__ void halves_minmax(float& mn, float& mx) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(mn), __float_as_uint(mn), false, false);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+  mn = min_nan(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  mx = max_nan(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
 // encoder modes
@@ -331,24 +347,19 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
     const bool live = tok < (TILE ? a.tq : a.T);
     const size_t crow = cslice * a.T_cap + size_t(a.t0 + tok);
 
-    // 1. block-range partials
-    bool bad = false;
+    // 1. block-range partials (NaN-propagating: a NaN anywhere in the block reaches the range)
     float mn = z[0], mx = z[0];
     if constexpr (QUANT) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        bad |= z[e] != z[e];
-        mn = fminf(mn, z[e]);
-        mx = fmaxf(mx, z[e]);
+      for (int e = 1; e < 16; ++e) {
+        mn = min_nan(mn, z[e]);
+        mx = max_nan(mx, z[e]);
       }
       if constexpr (TILE) {  // the 16 tokens of the lane's tile: one DPP row
         mn = row16_min(mn);
         mx = row16_max(mx);
       }
-      if constexpr (NB >= 32) {
-        mn = fminf(mn, __shfl_xor(mn, 32));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-      }
+      if constexpr (NB >= 32) halves_minmax(mn, mx);
       if constexpr (TILE) {
         if (hc == 0 && (n & 15) == 0) red[P][w][n >> 4] = make_float2(mn, mx);
       } else if constexpr (NB == 64) {
@@ -396,7 +407,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
     } else if constexpr (KEYS) {
       // z^T: lane (n, hc) holds tokens 8i + 4hc + j (e = 4i + j) of channel chA; the block is
       // the channel over the tile's 32 tokens (in-lane 16 + the other half-wave's 16)
-      bad = bad || !(mn >= -3.0e38f && mx <= 3.0e38f);
+      const bool bad = !(mn >= -3.0e38f && mx <= 3.0e38f);  // NaN or +-inf in the block
       const Side sd = make_side(mn, mx, BITS);
       // the channel's LSB-first stream of 32 codes in token order (BITS words): this lane's
       // codes placed as if hc = 0 (token 8i + j at bit (8i + j) BITS), shifted by 4 BITS bits
@@ -439,15 +450,15 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
 #pragma unroll
         for (int o = 1; o < NB / 32; ++o) {
           const float2 v = red[P][w ^ o][n >> 4];
-          mn = fminf(mn, v.x);
-          mx = fmaxf(mx, v.y);
+          mn = min_nan(mn, v.x);
+          mx = max_nan(mx, v.y);
         }
       } else if constexpr (NB == 64) {
         const float2 o = red[P][w ^ 1][n];
-        mn = fminf(mn, o.x);
-        mx = fmaxf(mx, o.y);
+        mn = min_nan(mn, o.x);
+        mx = max_nan(mx, o.y);
       }
-      bad = bad || !(mn >= -3.0e38f && mx <= 3.0e38f);  // NaN or +-inf in the block
+      const bool bad = !(mn >= -3.0e38f && mx <= 3.0e38f);  // NaN or +-inf in the block
       const Side sd = make_side(mn, mx, BITS);
       float r[16];
 #pragma unroll
