@@ -9,8 +9,9 @@ synthetic tensors already resident in HBM.
 Prints one JSON line.  `value` is the round-trip throughput in logical bf16 bytes
 (2 bytes per K/V element) per second; `roofline` describes the dominant kernel against the
 HBM peak, with its algorithmic bytes per launch and the average launch time measured with
-HIP events on the stream the kernels run on; `cpu_baseline` times the CPU oracle on a
-bounded sample of the same workload.
+HIP events on the stream the kernels run on, and (`ceiling`) the rate the library's streaming
+probe reaches on the same read / write byte mix with no arithmetic; `cpu_baseline` times the
+CPU oracle on a bounded sample of the same workload.
 """
 import argparse
 import json
@@ -430,6 +431,31 @@ def main():
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic, "kernel": dom_name,
                 "kernel_ms": round(dom_ms, 4), "encode_ms": round(enc_ms, 4), "decode_ms": round(dec_ms, 4),
                 "alg_bytes_per_launch": int(alg)}
+
+    # HBM ceiling of each kernel's read / write mix: the library's streaming probe (LDS-direct
+    # loads through the encoder's tile ring, no arithmetic) moving the same bf16 and code bytes
+    elem_b, code_b = n_elem // 2 * 2, n_elem // 2 * w.bits // 8 + n_elem // 2 * 4 // w.block_c
+    scratch = torch.empty(code_b, dtype=torch.uint8, device="cuda")
+
+    def probe_gbps(src, rb, dst, wb, reps=20):
+        for _ in range(3):
+            cg.cg_stream_probe(src, rb, dst, wb, stream=stream.cuda_stream)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            cg.cg_stream_probe(src, rb, dst, wb, stream=stream.cuda_stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        return (rb + wb) / (a.elapsed_time(b) / reps * 1e-3) / 1e9
+
+    enc_ceil = probe_gbps(X[0], elem_b, scratch, code_b)
+    dec_ceil = probe_gbps(scratch, code_b, Y[0], elem_b)
+    dom_ceil = enc_ceil if dom_name == "kv_encode" else dec_ceil
+    roofline["ceiling"] = {"GBps": round(dom_ceil, 1), "frac": round(achieved / dom_ceil, 4),
+                           "kernel": "cg_stream_probe", "read_bytes": elem_b if dom_name == "kv_encode" else code_b,
+                           "write_bytes": code_b if dom_name == "kv_encode" else elem_b,
+                           "decode_GBps": round(alg / (dec_ms * 1e-3) / 1e9, 1), "decode_ceiling_GBps": round(dec_ceil, 1)}
+    del scratch
 
     if args.copy_probe:
         src = torch.empty(256 << 20, dtype=torch.int16, device="cuda")

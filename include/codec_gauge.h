@@ -323,6 +323,16 @@ int32_t kv_append_paged(int32_t l0, int32_t l1, const cg_kv_view* k_new, const c
  * on `stream`; a correct build adds 0.  Errors: CG_ERR_ARG, CG_ERR_ALIGN, CG_ERR_DEVICE. */
 int32_t cg_selftest(int32_t which, uint64_t* mismatches_dev, void* stream);
 
+/* Measurement aid, not part of the codec: the HBM ceiling against which the memory-bound
+ * kernels' rates are read.  Streams `read_bytes` (a positive multiple of 8192) from device
+ * buffer `src` through LDS with the LDS-direct loads and tile ring of the encoder, and writes
+ * `write_bytes` (a multiple of 16, may be 0) of data read back from those tiles to device
+ * buffer `dst`, the writes spread evenly over the reads, in one kernel on `stream`.  Both
+ * buffers are the caller's and 16-byte aligned; `dst`'s contents afterwards are unspecified.
+ * Timing the call with events on `stream` gives the rate one pass with that read / write mix
+ * can reach.  Errors: CG_ERR_ARG, CG_ERR_ALIGN, CG_ERR_DEVICE. */
+int32_t cg_stream_probe(const void* src, int64_t read_bytes, void* dst, int64_t write_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

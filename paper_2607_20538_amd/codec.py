@@ -25,7 +25,8 @@ DTYPE_BF16, DTYPE_F32 = 0, 1
 
 EXPORTS = ["cg_status_str", "gauge_device_bytes", "gauge_make", "cache_bytes", "kv_encode", "kv_decode",
            "kv_append_step", "spectral_workspace_bytes", "kv_spectral_stats", "attend_workspace_bytes", "kv_attend",
-           "attend_paged_workspace_bytes", "kv_attend_paged", "kv_encode_paged", "kv_append_paged", "cg_selftest"]
+           "attend_paged_workspace_bytes", "kv_attend_paged", "kv_encode_paged", "kv_append_paged", "cg_selftest",
+           "cg_stream_probe"]
 
 
 class GaugeShape(C.Structure):
@@ -110,6 +111,8 @@ def lib() -> C.CDLL:
         L.kv_append_paged.restype = i32
         L.cg_selftest.argtypes = [i32, p, p]
         L.cg_selftest.restype = i32
+        L.cg_stream_probe.argtypes = [p, C.c_int64, p, C.c_int64, p]
+        L.cg_stream_probe.restype = i32
         _lib = L
     return _lib
 
@@ -242,6 +245,15 @@ def cg_selftest(which: int, mismatches_dev, stream=None):
     """Adds the mismatch count of device self-test `which` to the uint64 device tensor."""
     rc = lib().cg_selftest(which, _ptr(mismatches_dev), _stream(stream))
     _check("cg_selftest", rc)
+
+
+def cg_stream_probe(src, read_bytes: int, dst, write_bytes: int, stream=None):
+    """Streams `read_bytes` of device tensor `src` and writes `write_bytes` into `dst` in one
+    kernel (the HBM ceiling of that read / write mix; `dst` is left unspecified)."""
+    if src.nbytes < read_bytes or (write_bytes and dst.nbytes < write_bytes):
+        raise ValueError("cg_stream_probe: buffer smaller than the byte count")
+    rc = lib().cg_stream_probe(_ptr(src), read_bytes, _ptr(dst), write_bytes, _stream(stream))
+    _check("cg_stream_probe", rc)
 
 
 def kv_append_step(l0: int, l1: int, k_new, v_new, pos, G_dev, shp: GaugeShape, codec: Codec, kc: Cache,

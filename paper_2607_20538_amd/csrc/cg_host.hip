@@ -817,4 +817,12 @@ int32_t cg_selftest(int32_t which, uint64_t* mismatches_dev, void* stream) {
   return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
 }
 
+int32_t cg_stream_probe(const void* src, int64_t read_bytes, void* dst, int64_t write_bytes, void* stream) {
+  if (!src || read_bytes <= 0 || read_bytes % 8192 || write_bytes < 0 || write_bytes % 16 || (write_bytes && !dst))
+    return CG_ERR_ARG;
+  if ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15u) return CG_ERR_ALIGN;
+  hipError_t e = launch_stream_probe(src, read_bytes, dst, write_bytes, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
+}
+
 }  // extern "C"

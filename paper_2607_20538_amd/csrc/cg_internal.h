@@ -144,6 +144,9 @@ AttendPlan attend_plan(int nl, int B, int H, int Hq, int d, int span);
 hipError_t launch_attend(const AttendDev& a, const GaugeDev& G, const CodecDev& c, bool force_generic,
                          hipStream_t st);
 
+// HBM streaming probe (read_bytes a multiple of 8 KB, write_bytes of 16 bytes).
+hipError_t launch_stream_probe(const void* src, int64_t read_bytes, void* dst, int64_t write_bytes, hipStream_t st);
+
 // Device self-test of the quantiser's division-free steps (which: 0 reciprocal, 1 division).
 hipError_t launch_selftest(int which, unsigned long long* bad, hipStream_t st);
 

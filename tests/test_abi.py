@@ -307,3 +307,14 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(cg, "_lib", None)
     with pytest.raises(ImportError):
         cg.lib()
+
+
+def test_stream_probe_rejects_bad_sizes_on_the_host():
+    L = cg.lib()
+    fake = C.c_void_p(1 << 20)  # never dereferenced: every case fails validation first
+    for rb, wb, st in ((0, 0, cg.CG_ERR_ARG), (8192 + 16, 0, cg.CG_ERR_ARG), (8192, 8, cg.CG_ERR_ARG),
+                       (8192, -16, cg.CG_ERR_ARG)):
+        assert L.cg_stream_probe(fake, rb, fake, wb, None) == st
+    assert L.cg_stream_probe(None, 8192, fake, 0, None) == cg.CG_ERR_ARG
+    assert L.cg_stream_probe(fake, 8192, None, 16, None) == cg.CG_ERR_ARG
+    assert L.cg_stream_probe(C.c_void_p((1 << 20) + 8), 8192, fake, 16, None) == cg.CG_ERR_ALIGN
