@@ -37,7 +37,7 @@ def parse():
                     help="HBM traffic per launch measured with rocprofv3 counters (optional)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the timed region, run one plain 512 MiB device copy (counter calibration)")
-    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral", "attend", "attend_paged", "zfp"]),
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral", "attend", "attend_paged", "attend_tiles", "zfp"]),
                     help="llama8b (default) prints the headline line; the others print per-kernel timings of "
                          "the KIVI, rolling-step and 27B-sweep workloads")
     return ap.parse_args()
@@ -133,7 +133,7 @@ def other_workload(name, steps, warmup):
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral", "zfp") else ("rolling" if name in ("attend", "attend_paged") else name)]
+    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral", "zfp") else ("rolling" if name in ("attend", "attend_paged", "attend_tiles") else name)]
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     out = {"workload": name, "shape": {"L": w.L, "B": w.B, "H": w.H, "T": w.T, "d": w.d}, "steps": steps}
 
@@ -265,16 +265,18 @@ def other_workload(name, steps, warmup):
         out["page_size"] = P
         out["query_heads"] = w.H * grp
         out["attend_GBps"] = round(w.L * w.B * w.H * held * per_pos / ms_att / 1e6, 1)
-    elif name == "attend":
+    elif name in ("attend", "attend_tiles"):
         # the rolling step with the history consumed by fused decode-phase attention instead of
         # being decoded to bf16: append one token per (layer, b, h), then attention of the
-        # grp = 4 query heads of every KV head (32 query heads over 8 KV heads) over the history
+        # grp = 4 query heads of every KV head (32 query heads over 8 KV heads) over the history;
+        # attend_tiles: one range per 16 tokens x 64 channels (appends stage the unfinished tile)
         grp = 4
+        bt = 16 if name == "attend_tiles" else 1
         shp = cg.shape(w.L, w.H, w.d, w.g)
-        codec = cg.Codec(cg.BLOCK_UNIFORM, w.bits, w.block_c)
+        codec = cg.Codec(cg.BLOCK_UNIFORM, w.bits, w.block_c, block_t=bt)
         Gd = cg.alloc_gauge(shp)
         cg.gauge_make(cg.GAUGE_HAAR, shp, seed=w.gauge_seed, G_host=None, G_dev=Gd)
-        T_cap = w.T + warmup + 2 * steps + 1
+        T_cap = (w.T + warmup + 2 * steps + 1 + 15) // 16 * 16
         caches, news = [], []
         for s in (0, 1):
             X = layer_view(s)
@@ -317,6 +319,7 @@ def other_workload(name, steps, warmup):
         out["history_tokens"] = held
         out["query_heads"] = w.H * grp
         out["attend_GBps"] = round(cache_bytes / ms_att / 1e6, 1)
+        out["block_t"] = bt
     else:  # rolling decode step
         shp = cg.shape(w.L, w.H, w.d, w.g)
         codec = cg.Codec(cg.BLOCK_UNIFORM, w.bits, w.block_c)

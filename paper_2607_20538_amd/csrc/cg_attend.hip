@@ -453,8 +453,9 @@ __global__ __launch_bounds__(kAThreads) void att_combine(AttendDev a, GaugeDev G
 }
 
 // ------------------------------------------------------------------------------------------
-// matrix-core kernel: bf16-free block-uniform caches with one range per token and block
-// (block_t = 1), d = 128, blocks of 64 or 128 channels (NBLK = 2 or 1 blocks per row)
+// matrix-core kernel: block-uniform caches with one range per token and block (TB = 1) or per
+// 16-token tile and block (TB = 16), d = 128, blocks of 64 or 128 channels (NBLK = 2 or 1
+// blocks per row)
 // ------------------------------------------------------------------------------------------
 // Both contractions run on v_mfma_f32_16x16x32_bf16 with the codes entering as the exact bf16
 // values B = 1 + q 2^-k (code_frag; 8-bit codes as q), so zhat = mn + sc k (B - 1) and
@@ -474,6 +475,10 @@ __global__ __launch_bounds__(kAThreads) void att_combine(AttendDev a, GaugeDev G
 // A wave takes 32 positions per step (steps w, w + 4, ... of the split); the running maximum
 // of every query lives in the lanes of its D rows, the per-step probabilities and value side
 // words go through a small per-wave LDS buffer to the lanes building the value A operand.
+// With tiles, a step covers two whole tiles (steps start at multiples of 32) and the side word
+// of a position is its tile's; the at most 15 staged raw positions after the last whole tile
+// are scored with the raw query by the workgroup whose split holds them, and enter the merge of
+// the waves as one more partial softmax with raw value sums.
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f32x4_t mfma16(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
@@ -583,8 +588,9 @@ __device__ __forceinline__ void split2(float v, uint32_t& hi, uint32_t& lo) {
   lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
 }
 
-template <int BITS, int NBLK>
+template <int BITS, int NBLK, int TB>
 __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G) {
+  static_assert(TB == 1 || TB == 16, "token tiles of 16");
   constexpr int JQ = 8 / NBLK;                 // query heads per workgroup (16 A rows)
   constexpr int NQL = 2 / NBLK;                // queries per D lane
   constexpr int NB = kD / NBLK;                // channels per block
@@ -600,6 +606,11 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
   __shared__ float offs[4][16][4];
   __shared__ float ml[4][2][JQ];
   __shared__ float mm[2][JQ];
+  // staged raw positions (tiles): scores then weights, per-query maximum and sum, value sums
+  constexpr int RJ = TB > 1 ? JQ : 1;
+  __shared__ float rs[RJ][16];
+  __shared__ float rml[2][RJ];
+  __shared__ __attribute__((aligned(16))) float accr[RJ][TB > 1 ? kD : 1];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n = lane & 15, gq = lane >> 4;
@@ -620,6 +631,9 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
   int held = a.lens ? a.lens[b] : a.len;
   if (held < 0 || held > a.cap) held = 0;
   const int t_begin = sp * a.chunk, t_end = min(held, t_begin + a.chunk);
+  // positions in whole tiles go through the matrix cores, the staged ones after them are raw
+  const int tq = TB > 1 ? held / TB * TB : held;
+  const int t_endq = min(t_end, tq);
 
   // 1. queries: macc <- q, qt <- scale G_K q, qsum <- the per-block sums of its two planes
   for (int idx = threadIdx.x; idx < JQ * kD; idx += kAThreads) {
@@ -707,7 +721,7 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
   // One 32-position step; FULL: all 32 positions lie before t_end (no clamping)
   auto step = [&](int t0, auto fullc) {
     constexpr bool FULL = decltype(fullc)::value;
-    const int lim = t_end - 1 - t0;  // last valid position offset in the step
+    const int lim = t_endq - 1 - t0;  // last valid position offset in the step
     auto clampt = [&](int x) { return FULL ? x : min(x, lim); };
     // cache row of position t0 (a step never crosses a page)
     size_t sslc;
@@ -716,8 +730,10 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
     const size_t srow = sslc * size_t(a.kc.T_cap) + (t0 - poff);
     const uint8_t* kb = a.kc.codes + srow * RB;
     const uint8_t* vb = a.vc.codes + srow * RB;
-    const uint32_t* ksd = a.kc.side + srow * NBLK;
-    const uint32_t* vsdg = a.vc.side + srow * NBLK;
+    // side words of the step's first position (tiles: of its tile; t0 is a multiple of 32)
+    const size_t sidx = TB > 1 ? sslc * size_t(a.kc.T_cap / TB) + (t0 - poff) / TB : srow;
+    const uint32_t* ksd = a.kc.side + sidx * NBLK;
+    const uint32_t* vsdg = a.vc.side + sidx * NBLK;
     // loads: key regions of tokens t0 + 16 sb + n, value chunks of tokens t0 + 8 gq + e
     uint32_t rk[2][BITS];
     uint32_t swk[2][NBLK];
@@ -727,7 +743,7 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
           kb + (FULL ? koff + 16u * sb * RB : uint32_t(clampt(16 * sb + n)) * RB + uint32_t(gq) * BITS * 4));
 #pragma unroll
       for (int i = 0; i < BITS; ++i) rk[sb][i] = src[i];
-      const uint32_t* sd = ksd + uint32_t(clampt(16 * sb + n)) * NBLK;
+      const uint32_t* sd = ksd + uint32_t(clampt(16 * sb + n) / TB) * NBLK;
 #pragma unroll
       for (int k = 0; k < NBLK; ++k) swk[sb][k] = sd[k];
     }
@@ -746,7 +762,7 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
     }
     if (lane < 32 * NBLK) {
       const int k = lane >> 5, t = lane & 31;
-      vsd[w][k][t] = vsdg[size_t(clampt(t)) * NBLK + k];
+      vsd[w][k][t] = vsdg[size_t(clampt(t) / TB) * NBLK + k];
     }
 
     // scores of the two 16-token halves
@@ -840,8 +856,47 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
     __builtin_amdgcn_wave_barrier();
   };
   int t0 = t_begin + 32 * w;
-  for (; t0 + 32 <= t_end; t0 += 128) step(t0, std::true_type{});
-  if (t0 < t_end) step(t0, std::false_type{});
+  for (; t0 + 32 <= t_endq; t0 += 128) step(t0, std::true_type{});
+  if (t0 < t_endq) step(t0, std::false_type{});
+
+  // staged raw positions [max(tq, t_begin), t_end) of this split (tiles only; at most 15): scores
+  // with the raw query (macc still holds q), their softmax part and raw value sums
+  if constexpr (TB > 1) {
+    const int r0 = max(tq, t_begin), nr = max(0, t_end - r0);
+    const size_t slc = (size_t(l) * a.kc.B + b) * a.kc.H + h;
+    if (threadIdx.x < JQ * 16) {
+      const int jj = threadIdx.x / 16, r = threadIdx.x % 16;
+      float sc = -INFINITY;
+      if (jj < nj && r < nr) {
+        const uint16_t* kr = a.kc.ring + (slc * TB + (r0 + r) % TB) * kD;
+        float acc = 0.0f;
+        for (int ch = 0; ch < kD; ++ch) acc = fmaf(macc[jj][ch], bf16_to_f32(kr[ch]), acc);
+        sc = a.scale * acc;
+      }
+      rs[jj][r] = sc;
+    }
+    __syncthreads();
+    if (threadIdx.x < JQ) {
+      const int jj = threadIdx.x;
+      float m = -INFINITY, sum = 0.0f;
+      for (int r = 0; r < nr; ++r) m = fmaxf(m, rs[jj][r]);
+      for (int r = 0; r < nr; ++r) {
+        const float pr = m == -INFINITY ? 0.0f : __expf(rs[jj][r] - m);
+        rs[jj][r] = pr;
+        sum += pr;
+      }
+      rml[0][jj] = m;
+      rml[1][jj] = sum;
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < JQ * kD; idx += kAThreads) {
+      const int jj = idx / kD, ch = idx % kD;
+      float acc = 0.0f;
+      for (int r = 0; r < nr; ++r)
+        acc = fmaf(rs[jj][r], bf16_to_f32(a.vc.ring[(slc * TB + (r0 + r) % TB) * kD + ch]), acc);
+      accr[jj][ch] = acc;
+    }
+  }
 
   // 3. per-wave results: maximum and sum per query, gauge-space value sums
   float lsum[NQL];
@@ -863,7 +918,7 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
 #pragma unroll
   for (int qi = 0; qi < NQL; ++qi) {
     const int j = NBLK == 2 ? gq : 2 * gq + qi;
-    float M = -INFINITY;
+    float M = TB > 1 ? rml[0][j < RJ ? j : 0] : -INFINITY;
     for (int v = 0; v < 4; ++v) M = fmaxf(M, ml[v][0][j]);
     fq[qi] = mrun[qi] == -INFINITY ? 0.0f : __expf(mrun[qi] - M);
 #pragma unroll
@@ -894,18 +949,30 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
   }
   if (threadIdx.x < JQ) {
     const int jj = threadIdx.x;
-    float M = -INFINITY, L = 0.0f;
+    float M = TB > 1 ? rml[0][jj < RJ ? jj : 0] : -INFINITY, L = 0.0f;
     for (int v = 0; v < 4; ++v) M = fmaxf(M, ml[v][0][jj]);
     for (int v = 0; v < 4; ++v) {
       const float mv = ml[v][0][jj];
       if (mv != -INFINITY) L += ml[v][1][jj] * __expf(mv - M);
     }
+    if constexpr (TB > 1) {
+      const float mr = rml[0][jj < RJ ? jj : 0];
+      if (mr != -INFINITY) L += rml[1][jj < RJ ? jj : 0] * __expf(mr - M);
+    }
     mm[0][jj] = M;
     mm[1][jj] = L;
   }
   __syncthreads();
+  if constexpr (TB > 1) {  // raw value sums to the common maximum
+    for (int idx = threadIdx.x; idx < JQ * kD; idx += kAThreads) {
+      const int jj = idx / kD, ch = idx % kD;
+      const float mr = rml[0][jj];
+      accr[jj][ch] = mr == -INFINITY ? 0.0f : accr[jj][ch] * __expf(mr - mm[0][jj]);
+    }
+    __syncthreads();
+  }
   if (a.nsplit == 1) {
-    finalize_rows(a, G, &macc[0][0], nullptr, mm[1], nj, lv, b, h, hq0);
+    finalize_rows(a, G, &macc[0][0], TB > 1 ? &accr[0][0] : nullptr, mm[1], nj, lv, b, h, hq0);
     return;
   }
   const size_t pstride = size_t(2 + 2 * kD);
@@ -916,24 +983,25 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
       if (idx == 0) v = mm[0][jj];
       else if (idx == 1) v = mm[1][jj];
       else if (idx < 2 + kD) v = macc[jj][idx - 2];
-      else v = 0.0f;
+      else v = TB > 1 ? accr[jj < RJ ? jj : 0][(idx - 2 - kD) % (TB > 1 ? kD : 1)] : 0.0f;
       P[idx] = v;
     }
   }
 }
 
 template <int BITS>
-const void* att_mfma_fn(int nblk) {
-  return nblk == 2 ? (const void*)att_mfma<BITS, 2> : (const void*)att_mfma<BITS, 1>;
+const void* att_mfma_fn(int nblk, int bt) {
+  if (bt > 1) return nblk == 2 ? (const void*)att_mfma<BITS, 2, 16> : (const void*)att_mfma<BITS, 1, 16>;
+  return nblk == 2 ? (const void*)att_mfma<BITS, 2, 1> : (const void*)att_mfma<BITS, 1, 1>;
 }
 
-const void* att_mfma_kernel(int bits, int nblk) {
+const void* att_mfma_kernel(int bits, int nblk, int bt) {
   switch (bits) {
-    case 2: return att_mfma_fn<2>(nblk);
-    case 3: return att_mfma_fn<3>(nblk);
-    case 4: return att_mfma_fn<4>(nblk);
-    case 6: return att_mfma_fn<6>(nblk);
-    default: return att_mfma_fn<8>(nblk);
+    case 2: return att_mfma_fn<2>(nblk, bt);
+    case 3: return att_mfma_fn<3>(nblk, bt);
+    case 4: return att_mfma_fn<4>(nblk, bt);
+    case 6: return att_mfma_fn<6>(nblk, bt);
+    default: return att_mfma_fn<8>(nblk, bt);
   }
 }
 
@@ -963,7 +1031,9 @@ AttendPlan attend_plan(int nl, int B, int H, int Hq, int d, int span) {
 }
 
 bool attend_mfma_supported(const AttendDev& a, const CodecDev& c) {
-  return c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt == 1 && a.q.d == kD && (c.n == 64 || c.n == 128) &&
+  // tiles of 16 tokens on contiguous caches (paged caches take per-token blocks only)
+  return c.backend == CG_BACKEND_BLOCK_UNIFORM && (c.bt == 1 || (c.bt == 16 && !a.pt.pages)) && a.q.d == kD &&
+         (c.n == 64 || c.n == 128) &&
          (c.bits == 2 || c.bits == 3 || c.bits == 4 || c.bits == 6 || c.bits == 8);
 }
 
@@ -981,7 +1051,7 @@ hipError_t launch_attend(const AttendDev& a, const GaugeDev& G, const CodecDev& 
     const int nrow_f = a.q.L * a.q.B * a.kc.H * af.nqc;
     GaugeDev g2 = G;
     void* args[] = {&af, &g2};
-    e = hipLaunchKernel(att_mfma_kernel(c.bits, nblk), dim3(a.nsplit, nrow_f), dim3(kAThreads), args, 0, st);
+    e = hipLaunchKernel(att_mfma_kernel(c.bits, nblk, c.bt), dim3(a.nsplit, nrow_f), dim3(kAThreads), args, 0, st);
     if (e != hipSuccess) return e;
   } else {
     const size_t smem = (size_t(2) * kJQ * d + size_t(kGTile) * (d + 4) + kJQ * kGTile + 3 * kJQ) * sizeof(float);

@@ -113,6 +113,10 @@ CASES = [
     ("bu8-n64-g32", O.Codec(backend=O.BLOCK_UNIFORM, bits=8, block_c=64), 32, 100, 128, [100, 99]),
     ("kivi3", O.Codec(backend=O.KIVI, bits=3, key_tokens=32, val_channels=64, residual=64), 32, 300, 320, [300, 150]),
     ("tile4-16", O.Codec(backend=O.BLOCK_UNIFORM, bits=4, block_c=64, block_t=16), 128, 250, 256, [250, 200]),
+    # tiles with 128-channel blocks (eight query heads per workgroup), a row shorter than one tile
+    # (staged positions only) and a row ending on a tile boundary
+    ("tile6-n128", O.Codec(backend=O.BLOCK_UNIFORM, bits=6, block_c=128, block_t=16), 128, 200, 224, [9, 192]),
+    ("tile3-n64", O.Codec(backend=O.BLOCK_UNIFORM, bits=3, block_c=64, block_t=16), 128, 161, 192, [161, 47]),
     ("pass", O.Codec(backend=O.PASSTHROUGH), 32, 130, 160, [130, 77]),
 ]
 
@@ -171,6 +175,21 @@ def test_attend_split_rows_and_edges(kernels):
     assert err2 == cg.CG_FLAG_POS_RANGE
     assert (got2[:, 1] == 0).all()
     np.testing.assert_array_equal(got2[:, [0, 2, 3]], got[:, [0, 2, 3]])
+
+
+@pytest.mark.parametrize("bits,n", [(4, 64), (8, 128)])
+def test_attend_split_rows_over_tiles(kernels, bits, n):
+    """Token-channel tiles on rows long enough to be split over positions: the staged positions
+    of a row fall into its last split and are merged with the other splits' partial results."""
+    oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=bits, block_c=n, block_t=16)
+    lens = [2500, 0, 13, 1811]
+    st = _setup(oc, 2500, 2560, B=4, H=1, g=128, lens=lens)
+    scale = 1.0 / np.sqrt(128)
+    ref = O.attend(oc, st["G"], st["kh"], st["vh"], st["qf"], lens, scale)
+    got, err = _attend_gpu(st, oc, lens, scale)
+    assert err == 0
+    _check(got, ref, _vmax(st, oc, lens, 4))
+    assert (got[:, 1] == 0).all()
 
 
 def test_attend_error_free_cache_equals_attention_on_x(kernels):
