@@ -262,14 +262,15 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
 #pragma unroll
       for (int q = 0; q < 2; ++q)
         __builtin_amdgcn_global_load_lds(dsrc[q] + off, (__attribute__((address_space(3))) void*)(dst + 4 * q * kRowBytes),
-                                         16, 0, 0);
+                                         16, 0, kLoadStreamPolicy);
     } else {
       // ragged last tile: rows past the view repeat its last token
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
         const int tok = min(tile * kTok + drow[q], a.T - 1);
         __builtin_amdgcn_global_load_lds(dsrc[q] + (int64_t(tok) - drow[q]) * tstride,
-                                         (__attribute__((address_space(3))) void*)(dst + 4 * q * kRowBytes), 16, 0, 0);
+                                         (__attribute__((address_space(3))) void*)(dst + 4 * q * kRowBytes), 16, 0,
+                                         kLoadStreamPolicy);
       }
     }
   };
@@ -746,7 +747,7 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
       const int row = gi / GPR, j = gi % GPR;
       if (row < nlive) {
         const u32x4_t v = *(const u32x4_t*)(&ystage[buf][row * kD * YB + 16 * (j ^ (row & (GPR - 1)))]);
-        *(u32x4_t*)(ys + YB * (size_t(tile * kTok + row) * a.st) + 16 * j) = v;
+        store_stream(ys + YB * (size_t(tile * kTok + row) * a.st) + 16 * j, v);
       }
     }
   };
@@ -1042,7 +1043,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
     char* yt = ys + tile * ytile;
     if (nlive == kTok) {
 #pragma unroll
-      for (int k = 0; k < F; ++k) *(u32x4_t*)(yt + yoff[k]) = *(const u32x4_t*)(&ystage[buf][ysrc[k]]);
+      for (int k = 0; k < F; ++k) store_stream(yt + yoff[k], *(const u32x4_t*)(&ystage[buf][ysrc[k]]));
     } else {
 #pragma unroll
       for (int k = 0; k < F; ++k) {
@@ -1050,7 +1051,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
         if (gi >= nlive * GPR) gi = (nlive - 1) * GPR + (gi % GPR);
         const int row = gi / GPR, j = gi % GPR;
         const u32x4_t v = *(const u32x4_t*)(&ystage[buf][row * kD * YB + 16 * (j ^ (row & (GPR - 1)))]);
-        *(u32x4_t*)(yt + int64_t(YB) * row * a.st + 16 * j) = v;
+        store_stream(yt + int64_t(YB) * row * a.st + 16 * j, v);
       }
     }
   };
@@ -1268,7 +1269,7 @@ __global__ __launch_bounds__(kThreads, OUT_BF16 ? 3 : 2) void dec_keys(MfmaArgs 
     char* yt = ys + int64_t(YB) * r0 * a.st;
     if (lo == 0 && hi == kTok) {
 #pragma unroll
-      for (int k = 0; k < F; ++k) *(u32x4_t*)(yt + yoff[k]) = *(const u32x4_t*)(stage + ysrc[k]);
+      for (int k = 0; k < F; ++k) store_stream(yt + yoff[k], *(const u32x4_t*)(stage + ysrc[k]));
     } else {
 #pragma unroll
       for (int k = 0; k < F; ++k) {
@@ -1276,7 +1277,7 @@ __global__ __launch_bounds__(kThreads, OUT_BF16 ? 3 : 2) void dec_keys(MfmaArgs 
         int row = gi / GPR;
         row = row < lo ? lo : (row >= hi ? hi - 1 : row);
         const u32x4_t v = *(const u32x4_t*)(stage + row * kD * YB + 16 * (j ^ (row & (GPR - 1))));
-        *(u32x4_t*)(yt + int64_t(YB) * row * a.st + 16 * j) = v;
+        store_stream(yt + int64_t(YB) * row * a.st + 16 * j, v);
       }
     }
   };

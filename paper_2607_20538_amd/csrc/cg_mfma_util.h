@@ -20,6 +20,14 @@ constexpr int kRowBytes = kD * 2;
 // LDS operations of the wave done) and no wait on expcnt
 constexpr int waitcnt_imm(int vm) { return (vm & 15) | ((vm >> 4) << 14) | (7 << 4) | (0 << 8); }
 
+// Cache policy of the large streams.  A kernel that reads one large stream and writes a small
+// one (or the reverse) streams faster when the large stream is marked non-temporal: the
+// encoder's bf16 tiles are loaded with the `nt` bit (the cache-policy operand of the LDS-direct
+// load), the decoders' bf16 / binary32 output rows leave as non-temporal stores; the small
+// streams (codes, side words) keep the default policy.
+constexpr int kLoadStreamPolicy = 2;  // cache-policy bits of global_load_lds: nt
+__device__ __forceinline__ void store_stream(void* p, const u32x4_t& v) { __builtin_nontemporal_store(v, (u32x4_t*)p); }
+
 __device__ __forceinline__ int xcd_remap(int bid, int nwg) {
   // workgroups are dealt round-robin to the 8 XCDs; give each XCD a contiguous range of
   // logical workgroups so that the ranges of one slice share an L2
