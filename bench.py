@@ -102,6 +102,88 @@ def cpu_baseline(w, G_host, layers):
                       f"{t_total:.1f} s single-threaded"}
 
 
+def workload_cpu_baseline(name, w, gpu):
+    """The oracle (single thread, as written) on a bounded sample of workload `name`, in the unit of
+    the workload's GPU figure: one layer and one batch row (every head) of K and V encoded and
+    decoded (GB/s of bf16 KV, round trip) for the codec workloads; for the rolling and attention
+    steps one (layer, batch row) of the step, extrapolated to the workload's L x B rows."""
+    import numpy as np
+
+    import oracle as O
+    from paper_2607_20538_amd import synth
+
+    if name in ("kivi", "gemma27b", "tiles", "zfp"):
+        g, bits = {"tiles": (128, 4), "zfp": (128, 4)}.get(name, (w.g, w.bits))
+        if name == "kivi":
+            oc = O.Codec(backend=O.KIVI, bits=bits, block_c=64, key_tokens=w.key_tokens,
+                         val_channels=w.val_channels, residual=w.residual)
+        elif name == "tiles":
+            oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=bits, block_c=128, block_t=16)
+        elif name == "zfp":
+            oc = O.Codec(backend=O.ZFP, bits=bits)
+        else:
+            oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=bits, block_c=w.block_c)
+        G = O.gauge_make(O.GAUGE_HAAR, 1, w.H, w.d, g, seed=w.gauge_seed)
+        t_total, elems = 0.0, 0
+        for s in (0, 1):
+            X = synth.kv_tensor(w, s, L=1, B=1)
+            t0 = time.perf_counter()
+            cache, _ = O.kv_encode(oc, s, X, G, T_cap=w.T)
+            O.kv_decode(oc, s, G, cache, 0, w.T, lens=np.array([w.T], dtype=np.int32), out_bf16=True)
+            t_total += time.perf_counter() - t0
+            elems += X.size
+        return {"value": round(elems * 2 / t_total / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                "sample": f"layer 0, batch row 0 ({w.H} heads x {w.T} tokens) of K and V at g = {g}, "
+                          f"{bits} bits ({elems} elements), encode + decode, {t_total:.1f} s single-threaded"}
+    if name in ("rolling", "attend", "attend_tiles", "attend_paged"):
+        # one (layer, batch row): its history encoded (untimed), then the step's work for it timed:
+        # append one token to K and V and decode the history (rolling), or attention of its grp = 4
+        # query heads per KV head over the history (attention steps; the oracle has no page table,
+        # so paged caches are timed as the contiguous ones they are equivalent to)
+        bt = 16 if name == "attend_tiles" else 1
+        oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=w.bits, block_c=w.block_c, block_t=bt)
+        G = O.gauge_make(O.GAUGE_HAAR, 1, w.H, w.d, w.g, seed=w.gauge_seed)
+        T_cap = w.T + 16
+        caches = []
+        for s in (0, 1):
+            X = synth.kv_tensor(w, s, L=1, B=1)
+            caches.append(O.kv_encode(oc, s, X, G, T_cap=T_cap)[0])
+            del X
+        t0 = time.perf_counter()
+        if name == "rolling":
+            for s in (0, 1):
+                xn = synth.kv_tensor(w, s, L=1, B=1, T=1, t_offset=w.T)[:, :, :, 0, :]
+                O.kv_append(oc, s, xn, G, caches[s], np.array([w.T], dtype=np.int32))
+                O.kv_decode(oc, s, G, caches[s], 0, w.T + 1, lens=np.array([w.T + 1], dtype=np.int32), out_bf16=True)
+            held = w.T + 1
+        else:
+            held = w.T
+            qv = synth.queries(w, 4 * w.H, L=1, B=1)
+            q = (qv.astype(np.uint32) << 16).view(np.float32) if qv.dtype == np.uint16 else qv
+            O.attend(oc, G, caches[0], caches[1], q, np.array([held], dtype=np.int32), 1.0 / np.sqrt(w.d))
+        t_row = time.perf_counter() - t0
+        rows = w.L * w.B
+        ms = t_row * rows * 1e3
+        out = {"value": round(ms, 1), "unit": "ms per step (extrapolated)", "cores": 1, "kind": "oracle",
+               "sample": f"layer 0, batch row 0 ({w.H} KV heads, {held}-position history): "
+                         + ("append one K / V token and decode the history" if name == "rolling"
+                            else "attention of 4 query heads per KV head")
+                         + f", {t_row:.1f} s single-threaded, x {rows} (layer, batch row) pairs"}
+        return out
+    if name == "spectral":
+        G = O.gauge_make(O.GAUGE_HAAR, 1, w.H, w.d, w.g, seed=w.gauge_seed)
+        t_total, elems = 0.0, 0
+        for s in (0, 1):
+            X = synth.kv_tensor(w, s, L=8)
+            t0 = time.perf_counter()
+            O.spectral_stats(X, np.repeat(G, 8, axis=0), s, 16, 0.04)
+            t_total += time.perf_counter() - t0
+            elems += X.size
+        return {"value": round(elems * 2 / t_total / 1e9, 4), "unit": "GB/s bf16 in", "cores": 1, "kind": "oracle",
+                "sample": f"layers 0-7 of K and V ({elems} elements), {t_total:.1f} s single-threaded"}
+    return None
+
+
 def _timed(fn, steps, warmup, stream):
     """Average milliseconds of fn() over `steps` launches (after `warmup`), HIP events on `stream`."""
     import torch
@@ -117,7 +199,19 @@ def _timed(fn, steps, warmup, stream):
     return a.elapsed_time(b) / steps
 
 
-def other_workload(name, steps, warmup):
+def copy_probe():
+    """One plain 512 MiB device-to-device copy: the reference dispatch that rocprofv3's FETCH_SIZE /
+    WRITE_SIZE counters are calibrated against."""
+    import torch
+
+    src = torch.empty(256 << 20, dtype=torch.int16, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def other_workload(name, steps, warmup, cpu=True, probe=False):
     """Per-kernel timings of the KIVI, rolling, 27B and token-channel tile workloads at their
     full shapes, from seeded synthetic K/V (synth.kv_tensor): eight distinct layers repeated to
     L layers for the KIVI, 27B and tile inputs (the tiles use the Llama-3-8B shape with one
@@ -352,6 +446,9 @@ def other_workload(name, steps, warmup):
         out["history_tokens"] = w.T
         out["decode_GBps"] = round(alg / ms / 1e6, 1)
     assert int(err.item()) == 0, f"device error flag {int(err.item())}"
+    if probe:
+        copy_probe()
+    out["cpu_baseline"] = workload_cpu_baseline(name, w, out) if cpu else None
     print(json.dumps(out), flush=True)
 
 
@@ -361,7 +458,7 @@ def main():
         if args.gpus != 1:
             print("bench.py measures one GPU", file=sys.stderr)
             sys.exit(2)
-        other_workload(args.workload, args.steps, args.warmup)
+        other_workload(args.workload, args.steps, args.warmup, cpu=not args.no_cpu_baseline, probe=args.copy_probe)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: the codec path has no "
@@ -461,11 +558,7 @@ def main():
     del scratch
 
     if args.copy_probe:
-        src = torch.empty(256 << 20, dtype=torch.int16, device="cuda")
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        copy_probe()
 
     cpu = None
     if not args.no_cpu_baseline:
