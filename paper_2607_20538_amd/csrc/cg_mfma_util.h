@@ -44,14 +44,20 @@ __device__ __forceinline__ f32x16_t mfma(const bf16x8_t& a, const bf16x8_t& b, c
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const u32x4_t& v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-// a lane's value moved through DPP (all rows and banks enabled)
+// a lane's value moved through DPP (all rows and banks enabled).  Every control used here
+// (quad permutes, row rotations, row mirror) reads a lane of the same row, so no lane is out of
+// bounds and the move needs no `old` value (which would cost a v_mov of it before each move).
 template <int CTRL>
 __device__ __forceinline__ float dpp_mov(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+  static_assert(CTRL <= 0xFF || (CTRL >= 0x121 && CTRL <= 0x12F) || CTRL == 0x140 || CTRL == 0x141,
+                "quad_perm, row_ror, row_mirror or row_half_mirror only");
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
 }
 template <int CTRL>
 __device__ __forceinline__ int dpp_mov_i(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+  static_assert(CTRL <= 0xFF || (CTRL >= 0x121 && CTRL <= 0x12F) || CTRL == 0x140 || CTRL == 0x141,
+                "quad_perm, row_ror, row_mirror or row_half_mirror only");
+  return __builtin_amdgcn_mov_dpp(v, CTRL, 0xF, 0xF, true);
 }
 
 // B fragment of K-step u of a region (RW packed words starting at the region's first channel)

@@ -11,13 +11,13 @@
 // Matrix-core path (bf16, d = 128, Tb = 16): the channel DCT is folded into the gauge,
 // M = C_d G (one dense 128 x 128 matrix per (layer, head), built in binary64 and split into
 // two bf16 planes), so one matrix-core chain per 32-token tile gives y = M x = C_d z for the
-// tile's tokens.  The lane holding token n keeps 16 consecutive frequencies v; the 16 tokens
-// of a block are the 16 lanes of one DPP row, and the lane at place u of its row produces
-// token frequency u.  The DCT's symmetry C[u][15 - t] = (-1)^u C[u][t] halves the work: each
-// lane j first forms w_j = y_j + (-1)^j y_{15-j} (row_mirror), and since the even rotations of
-// a row keep lane parity and meet each pair (t, 15 - t) once, U[u] is 8 multiply-adds of
-// w rotated by 0, 2, .., 14 lanes (row_ror) with per-lane coefficients.  Energies accumulate
-// per lane in binary64 and leave by atomic adds at the end of the workgroup.
+// tile's tokens.  The chain runs transposed (the tile as the A operand), so a lane holds one
+// channel-layout frequency v of 16 tokens; the lane pair exchanges half-waves so that each lane
+// holds the 16 tokens of one block, and the token DCT is an in-lane 16-point DCT by even / odd
+// splits (120 operations for 16 outputs).  Energies accumulate per lane in binary64 and leave
+// by atomic adds at the end of the workgroup; log(1 + |U| / tau) is summed as log2 (the
+// hardware's v_log_f32 on an argument >= 1) and scaled by ln 2 once.  The matrix-core chain of
+// tile t + 1 is issued before the VALU work of tile t (two accumulators).
 //
 // General path (any supported d and g, bf16 or binary32 input, Tb in {2, 4, 8, 16, 32}): one
 // workgroup per block, gauge, channel DCT and token DCT on the VALU in binary32 through LDS.
@@ -107,32 +107,79 @@ struct SpecArgs {
   int nslices, chunks, tiles_per_wg;
 };
 
-// rotation of a value by K lanes within its DPP row (K = 0: the value itself)
-template <int K>
-__device__ __forceinline__ float ror16(float v) {
-  if constexpr (K == 0) return v;
-  else return dpp_mov<0x120 + K>(v);
-}
-template <int K>
-__device__ __forceinline__ int ror16_i(int v) {
-  if constexpr (K == 0) return v;
-  else return dpp_mov_i<0x120 + K>(v);
-}
-
-// U[u] of the lane at place u of its row from the row's w values (rotations by 2K lanes)
-template <int... K>
-__device__ __forceinline__ float row_dct(float w, const float (&coef)[8], std::integer_sequence<int, K...>) {
-  float u = 0.0f;
-  ((u = fmaf(coef[K], ror16<2 * K>(w), u)), ...);
-  return u;
+// cos(pi x) at compile time: x reduced to [0, 1), then the Taylor series of cos at pi x
+// (|pi x| < pi: the 30 terms below are exact to binary64 rounding)
+constexpr double cos_pi(double x) {
+  while (x >= 2.0) x -= 2.0;
+  double sign = 1.0;
+  if (x >= 1.0) {  // cos(pi (x - 1)) = -cos(pi x)
+    x -= 1.0;
+    sign = -1.0;
+  }
+  const double th = 3.14159265358979323846 * x, th2 = th * th;
+  double term = 1.0, sum = 1.0;
+  for (int k = 1; k < 30; ++k) {
+    term *= -th2 / double((2 * k - 1) * (2 * k));
+    sum += term;
+  }
+  return sign * sum;
 }
 
-template <int... K>
-__device__ __forceinline__ void row_sources(int i, int (&src)[8], std::integer_sequence<int, K...>) {
-  ((src[K] = ror16_i<2 * K>(i)), ...);
+// Orthonormal 16-point DCT-II, U[u] = a_u sum_t y[t] cos(pi (2t + 1) u / 32) (a_0 = sqrt(1/16),
+// a_u = sqrt(2/16)), by its even / odd splits: with s[t] = y[t] + y[15 - t] and d[t] =
+// y[t] - y[15 - t] (t < 8), the odd outputs are an 8 x 8 product with d; with ss[t] = s[t] +
+// s[7 - t] and sd[t] = s[t] - s[7 - t] (t < 4), U[4m + 2] and U[4m] are 4 x 4 products with sd
+// and ss.  The tables hold a_u times the cosines.
+struct Dct16Tables {
+  float odd[8][8], e2[4][4], e4[4][4];
+};
+constexpr Dct16Tables make_dct16() {
+  Dct16Tables c{};
+  const double a0 = 0.25, a1 = 0.35355339059327376220;  // sqrt(1/16), sqrt(2/16)
+  for (int k = 0; k < 8; ++k)
+    for (int t = 0; t < 8; ++t) c.odd[k][t] = float(a1 * cos_pi((2.0 * t + 1.0) * (2.0 * k + 1.0) / 32.0));
+  for (int m = 0; m < 4; ++m)
+    for (int t = 0; t < 4; ++t) {
+      c.e2[m][t] = float(a1 * cos_pi((2.0 * t + 1.0) * (2.0 * m + 1.0) / 16.0));
+      c.e4[m][t] = float((m == 0 ? a0 : a1) * cos_pi((2.0 * t + 1.0) * m / 8.0));
+    }
+  return c;
+}
+constexpr Dct16Tables kDct16 = make_dct16();
+
+__device__ __forceinline__ void dct16(const float (&y)[16], float (&U)[16]) {
+  float s[8], d[8], ss[4], sd[4];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    s[t] = y[t] + y[15 - t];
+    d[t] = y[t] - y[15 - t];
+  }
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    ss[t] = s[t] + s[7 - t];
+    sd[t] = s[t] - s[7 - t];
+  }
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    float v = kDct16.odd[k][0] * d[0];
+#pragma unroll
+    for (int t = 1; t < 8; ++t) v = fmaf(kDct16.odd[k][t], d[t], v);
+    U[2 * k + 1] = v;
+  }
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    float v2 = kDct16.e2[m][0] * sd[0], v4 = kDct16.e4[m][0] * ss[0];
+#pragma unroll
+    for (int t = 1; t < 4; ++t) {
+      v2 = fmaf(kDct16.e2[m][t], sd[t], v2);
+      v4 = fmaf(kDct16.e4[m][t], ss[t], v4);
+    }
+    U[4 * m + 2] = v2;
+    U[4 * m] = v4;
+  }
 }
 
-__global__ __launch_bounds__(kThreads, 3) void spec_mfma(SpecArgs a) {
+__global__ __launch_bounds__(kThreads, 2) void spec_mfma(SpecArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t xtile[kSpecStages][kTok * kRowBytes];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -158,21 +205,6 @@ __global__ __launch_bounds__(kThreads, 3) void spec_mfma(SpecArgs a) {
     A[0][kk] = as_bf16x8(*(const u32x4_t*)(a.m0 + off));
     A[1][kk] = as_bf16x8(*(const u32x4_t*)(a.m1 + off));
   }
-  // token DCT: the lane at place i of its row produces frequency u = i; the w value rotated in
-  // from lane j = src[k] stands for token t = min(j, 15 - j), with the sign (-1)^u when j >= 8
-  // (w_j then holds (-1)^u times the pair sum of token 15 - j)
-  const int i = lane & 15;
-  int src[8];
-  row_sources(i, src, std::make_integer_sequence<int, 8>());
-  float coef[8];
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int j = src[k], t = j < 8 ? j : 15 - j;
-    const double sg = (j >= 8 && (i & 1)) ? -1.0 : 1.0;
-    coef[k] = float(sg * sqrt((i == 0 ? 1.0 : 2.0) / kSpecTb) * cospi((2.0 * t + 1.0) * i / (2.0 * kSpecTb)));
-  }
-  const float par = (i & 1) ? -1.0f : 1.0f;  // (-1)^j of this lane
-
   // LDS-direct tile loads as in the encoder: wave w moves rows 8w .. 8w+7 with two 1 KB
   // instructions; rows past the whole blocks repeat the last used row
   const int wu = __builtin_amdgcn_readfirstlane(w);
@@ -205,46 +237,79 @@ __global__ __launch_bounds__(kThreads, 3) void spec_mfma(SpecArgs a) {
 #pragma unroll
   for (int kk = 0; kk < 8; ++kk) boff[kk] = n * kRowBytes + 16 * swz(n, 2 * kk + hc);
 
+  // energy accumulators of the lane's entries (u = 0..15, v = chA): the lane pair (n, 0) and
+  // (n, 1) holds the same entries for the tile's two blocks
   double eacc[16];
 #pragma unroll
   for (int e = 0; e < 16; ++e) eacc[e] = 0.0;
   double lacc = 0.0;
-  for (int t = tb; t < min(te, tb + kSpecStages - 1); ++t) issue(t);
-  for (int t = tb; t < te; ++t) {
-    // tile t landed in every wave, every wave is done with the buffer tile t - 1 used
-    wait_tile(min(te - 1, t + kSpecStages - 2) - t);
-    __builtin_amdgcn_s_barrier();
-    if (t + kSpecStages - 1 < te) issue(t + kSpecStages - 1);
+  // y^T = x^T M^T of tile t on the matrix cores: the tile is the A operand and the planes of M
+  // the B operand, so lane (n, hc) holds channel chA of tokens 8 (e / 4) + 4 hc + e % 4
+  auto chain = [&](int t) {
     const uint8_t* src_t = xtile[(t - tb) % kSpecStages];
     f32x16_t acc = {};
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
       const bf16x8_t bv = as_bf16x8(*(const u32x4_t*)(src_t + boff[kk]));
-      acc = mfma(A[1][kk], bv, acc);
-      acc = mfma(A[0][kk], bv, acc);
+      acc = mfma(bv, A[1][kk], acc);
+      acc = mfma(bv, A[0][kk], acc);
     }
-    // token DCT of the lane's 16 frequencies v = 32w + 16hc + e over its row's block
-    const bool valid = 2 * t + (n >> 4) < a.nblk;
+    return acc;
+  };
+  // the lane pair exchanges half-waves (v_permlane32_swap) so that lane (n, hc) holds all 16
+  // tokens of block hc of the tile, then the token DCT runs in-lane; coefficients of a block past
+  // the whole ones count as 0 (no energy, log2 1 = 0)
+  auto epilogue = [&](int t, const f32x16_t& acc) {
+    float y[16];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[e]), __float_as_uint(acc[e + 8]), false, false);
+      y[8 * (e >> 2) + (e & 3)] = __uint_as_float(r[0]);
+      y[8 * (e >> 2) + 4 + (e & 3)] = __uint_as_float(r[1]);
+    }
+    float U[16];
+    dct16(y, U);
+    const bool valid = 2 * t + hc < a.nblk;
     float ls = 0.0f;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const float y = acc[e];
-      const float w = fmaf(par, dpp_mov<0x140>(y), y);  // row_mirror: y of lane 15 - j
-      const float u = row_dct(w, coef, std::make_integer_sequence<int, 8>());
-      if (valid) {
-        eacc[e] = fma(double(u), double(u), eacc[e]);
-        ls += __logf(1.0f + fabsf(u) * a.inv_tau);
-      }
+    for (int u = 0; u < 16; ++u) {
+      const float x = valid ? U[u] : 0.0f;
+      eacc[u] = fma(double(x), double(x), eacc[u]);
+      // log2 of an argument >= 1 (v_log_f32); the sum is scaled by ln 2 once, at the end
+      ls += __builtin_amdgcn_logf(fmaf(fabsf(x), a.inv_tau, 1.0f));
     }
     lacc += double(ls);
+  };
+  // software pipeline: the matrix-core chain of tile t + 1 runs while the VALU works on tile t
+  for (int t = tb; t < min(te, tb + kSpecStages - 1); ++t) issue(t);
+  wait_tile(min(te - 1, tb + kSpecStages - 2) - tb);
+  __builtin_amdgcn_s_barrier();
+  f32x16_t accs[2];
+  accs[0] = chain(tb);
+  auto step = [&](int t, auto parity) {
+    constexpr int P = decltype(parity)::value;
+    if (t + 1 < te) {
+      // tile t + 1 landed in every wave, every wave is done with the buffer tile t - 1 used
+      wait_tile(min(te - 1, t + kSpecStages - 2) - (t + 1));
+      __builtin_amdgcn_s_barrier();
+      if (t + kSpecStages - 1 < te) issue(t + kSpecStages - 1);
+      accs[P ^ 1] = chain(t + 1);
+    }
+    epilogue(t, accs[P]);
+  };
+  int t = tb;
+  for (; t + 1 < te; t += 2) {
+    step(t, std::integral_constant<int, 0>());
+    step(t + 1, std::integral_constant<int, 1>());
   }
-  // energy map entries (u = i, v = 32w + 16hc + e) and the log sum
-  double* accl = a.acc + size_t(l) * kSpecTb * kD + size_t(i) * kD + 32 * w + 16 * hc;
+  if (t < te) step(t, std::integral_constant<int, 0>());
+  // energy map entries (u, v = chA) and the log sum
+  double* accl = a.acc + size_t(l) * kSpecTb * kD + chA;
 #pragma unroll
-  for (int e = 0; e < 16; ++e) atomicAdd(accl + e, eacc[e]);
+  for (int u = 0; u < 16; ++u) atomicAdd(accl + u * kD, eacc[u]);
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) lacc += __shfl_xor(lacc, off);
-  if (lane == 0) atomicAdd(a.lsum + l, lacc);
+  if (lane == 0) atomicAdd(a.lsum + l, lacc * 0.69314718055994530942);  // log2 -> natural log
 }
 
 // General path: one workgroup per (slice, block).  xs, zs: [Tb][d + 1] binary32; ct:
