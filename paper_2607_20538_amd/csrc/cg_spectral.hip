@@ -47,9 +47,11 @@ __global__ void spec_init(double* acc, size_t nacc, double* lsum, int L, double*
 
 // M = C_d G_{l,s,h} (G block-diagonal over its R groups), products and sums in binary64 from
 // the binary32 DCT rows and gauge, rounded to binary32 and split into two bf16 planes.  One
-// workgroup per (l, h) stages C_d and the gauge blocks in LDS; thread t accumulates the 8 x 8
-// outputs rows 8 (t / 16) .., columns 8 (t % 16) .. (one gauge group: 8 | g).
-__global__ __launch_bounds__(256) void spec_mprep(int s, GaugeDev G, int H, const double* cd, uint16_t* m0,
+// workgroup of 1024 threads (four waves per SIMD to hide the LDS latency) per (l, h) stages C_d
+// and the gauge blocks in LDS; thread t accumulates the 4 x 4 outputs rows 4 (t / 32) ..,
+// columns 4 (t % 32) .. (one gauge group: 4 | g).
+constexpr int kMprepThreads = 1024;
+__global__ __launch_bounds__(kMprepThreads) void spec_mprep(int s, GaugeDev G, int H, const double* cd, uint16_t* m0,
                                                    uint16_t* m1) {
   __shared__ float cds[kD * kD];   // C_d rows
   __shared__ float gs[kD * kD];    // gs[a_global][j]: G_{r}[a][j - r g] for j in group r, a = a_global - r g
@@ -64,27 +66,27 @@ __global__ __launch_bounds__(256) void spec_mprep(int s, GaugeDev G, int H, cons
     gs[idx] = v;
   }
   __syncthreads();
-  const int i0 = 8 * (threadIdx.x / 16), j0 = 8 * (threadIdx.x % 16), r = j0 / g;
-  double acc[8][8];
+  const int i0 = 4 * (threadIdx.x / 32), j0 = 4 * (threadIdx.x % 32), r = j0 / g;
+  double acc[4][4];
 #pragma unroll
-  for (int p = 0; p < 8; ++p)
+  for (int p = 0; p < 4; ++p)
 #pragma unroll
-    for (int q = 0; q < 8; ++q) acc[p][q] = 0.0;
+    for (int q = 0; q < 4; ++q) acc[p][q] = 0.0;
   for (int a = r * g; a < r * g + g; ++a) {
-    double cv[8], gv[8];
+    double cv[4], gv[4];
 #pragma unroll
-    for (int p = 0; p < 8; ++p) cv[p] = double(cds[(i0 + p) * kD + a]);
+    for (int p = 0; p < 4; ++p) cv[p] = double(cds[(i0 + p) * kD + a]);  // two rows per wave: broadcasts
+    const float4 gq = *reinterpret_cast<const float4*>(&gs[a * kD + j0]);
+    gv[0] = gq.x; gv[1] = gq.y; gv[2] = gq.z; gv[3] = gq.w;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) gv[q] = double(gs[a * kD + j0 + q]);
+    for (int p = 0; p < 4; ++p)
 #pragma unroll
-    for (int p = 0; p < 8; ++p)
-#pragma unroll
-      for (int q = 0; q < 8; ++q) acc[p][q] = fma(cv[p], gv[q], acc[p][q]);
+      for (int q = 0; q < 4; ++q) acc[p][q] = fma(cv[p], gv[q], acc[p][q]);
   }
 #pragma unroll
-  for (int p = 0; p < 8; ++p)
+  for (int p = 0; p < 4; ++p)
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
+    for (int q = 0; q < 4; ++q) {
       const float v = float(acc[p][q]);
       const uint32_t hi = f32_to_bf16_rne(v);
       const uint32_t lo = f32_to_bf16_rne(v - __uint_as_float(hi << 16));
@@ -454,7 +456,7 @@ hipError_t launch_spectral(int s, const ViewDev& X, const GaugeDev& G, int Tb, f
     if (!force_generic && X.bf16 && X.d == kD && Tb == kSpecTb) {
       uint16_t* m0 = reinterpret_cast<uint16_t*>(base + lay.off_m[0]);
       uint16_t* m1 = reinterpret_cast<uint16_t*>(base + lay.off_m[1]);
-      hipLaunchKernelGGL(spec_mprep, dim3(X.L * X.H), dim3(256), 0, st, s, G, X.H, cd, m0, m1);
+      hipLaunchKernelGGL(spec_mprep, dim3(X.L * X.H), dim3(kMprepThreads), 0, st, s, G, X.H, cd, m0, m1);
       if ((e = hipGetLastError()) != hipSuccess) return e;
       SpecArgs a{};
       a.x = static_cast<const char*>(X.ptr);
