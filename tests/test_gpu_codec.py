@@ -141,7 +141,8 @@ def test_quantise_and_dequantise_are_bit_exact(backend, bits, n, dtype, kernels)
 FCASES = [(128, 4, 64, O.GAUGE_HAAR), (128, 6, 64, O.GAUGE_HAAR), (128, 3, 64, O.GAUGE_HAAR),
           (128, 4, 64, O.GAUGE_DCT2), (128, 4, 64, O.GAUGE_HADAMARD), (64, 4, 32, O.GAUGE_HAAR),
           (32, 3, 64, O.GAUGE_HAAR), (16, 4, 32, O.GAUGE_HAAR), (8, 4, 64, O.GAUGE_HAAR),
-          (8, 6, 64, O.GAUGE_HAAR), (32, 8, 32, O.GAUGE_HAAR), (128, 2, 64, O.GAUGE_HAAR)]
+          (8, 6, 64, O.GAUGE_HAAR), (32, 8, 32, O.GAUGE_HAAR), (128, 2, 64, O.GAUGE_HAAR),
+          (32, 4, 64, O.GAUGE_HAAR), (32, 6, 64, O.GAUGE_HAAR), (16, 4, 64, O.GAUGE_DCT2)]
 
 
 @pytest.mark.parametrize("g,bits,n,kind", FCASES)
