@@ -39,6 +39,32 @@ __device__ __forceinline__ uint32_t f16_bits_up(float v) {
   return bits == 0x8000u ? 0u : bits;
 }
 
+// The same two binary16 roundings by the hardware conversion under a directed rounding mode:
+// bits [3:2] of the MODE register set the rounding of binary16 and binary64 results (0
+// nearest even, 1 toward +inf, 2 toward -inf; the binary32 field, bits [1:0], is untouched).
+// The mode switch and the conversion are one asm block, so that the compiler neither resets
+// the mode for the conversion nor fuses the conversion into the instruction producing v (which
+// would round an unrounded product); s_nop 1 covers the wait states between s_setreg and a
+// VALU instruction that depends on the mode.  The mode is per wave and restored to nearest
+// even.  cg_selftest(2) checks both against f16_bits_down / f16_bits_up over every binary32
+// value of the binades the binary16 range meets.
+template <int MODE>
+__device__ __forceinline__ uint32_t f16_bits_directed_hw(float v) {
+  uint32_t bits;
+  asm volatile(
+      "s_setreg_imm32_b32 hwreg(HW_REG_MODE, 2, 2), %2\n\t"
+      "s_nop 1\n\t"
+      "v_cvt_f16_f32_e32 %0, %1\n\t"
+      "s_setreg_imm32_b32 hwreg(HW_REG_MODE, 2, 2), 0\n\t"
+      "s_nop 1"
+      : "=v"(bits)
+      : "v"(v), "i"(MODE));
+  bits &= 0xffffu;
+  return bits == 0x8000u ? 0u : bits;
+}
+__device__ __forceinline__ uint32_t f16_bits_down_hw(float v) { return f16_bits_directed_hw<2>(v); }
+__device__ __forceinline__ uint32_t f16_bits_up_hw(float v) { return f16_bits_directed_hw<1>(v); }
+
 // RN(a / (2^b - 1)) without a division: q0 = RN(a r) with r = RN(1 / d), the exact residual
 // e = a - q0 d (one FMA), then RN(q0 + e r) (Markstein's correction step).  cg_selftest(1)
 // checks it against correctly rounded division for every binary32 mantissa of the binades
@@ -67,14 +93,16 @@ struct Side {
   int flags;
 };
 
+// HW: the binary16 roundings by the hardware conversion under a directed mode (same results)
+template <bool HW = false>
 __device__ __forceinline__ Side make_side(float mn, float mx, int bits) {
 #pragma clang fp contract(off)
   Side s;
-  uint32_t mnb = f16_bits_down(mn);
+  uint32_t mnb = HW ? f16_bits_down_hw(mn) : f16_bits_down(mn);
   s.mn = f16_bits_to_f32(mnb);
   float diff = mx - s.mn;
   float s32 = div_by_qmax(diff, bits);           // = RN(diff / (2^b - 1))
-  uint32_t scb = f16_bits_up(s32);
+  uint32_t scb = HW ? f16_bits_up_hw(s32) : f16_bits_up(s32);
   s.sc = f16_bits_to_f32(scb);
   s.inv = (s.sc == 0.0f) ? 0.0f : rcp_of_f16(s.sc);  // = RN(1 / sc)
   s.word = mnb | (scb << 16);

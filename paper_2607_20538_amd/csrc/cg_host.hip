@@ -810,7 +810,7 @@ int32_t kv_append_paged(int32_t l0, int32_t l1, const cg_kv_view* k_new, const c
 }
 
 int32_t cg_selftest(int32_t which, uint64_t* mismatches_dev, void* stream) {
-  if ((which != 0 && which != 1) || !mismatches_dev) return CG_ERR_ARG;
+  if (which < 0 || which > 2 || !mismatches_dev) return CG_ERR_ARG;
   if (reinterpret_cast<uintptr_t>(mismatches_dev) & 7u) return CG_ERR_ALIGN;
   hipError_t e = launch_selftest(which, reinterpret_cast<unsigned long long*>(mismatches_dev),
                                  static_cast<hipStream_t>(stream));

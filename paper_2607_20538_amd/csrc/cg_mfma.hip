@@ -409,7 +409,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
       // z^T: lane (n, hc) holds tokens 8i + 4hc + j (e = 4i + j) of channel chA; the block is
       // the channel over the tile's 32 tokens (in-lane 16 + the other half-wave's 16)
       const bool bad = !(mn >= -3.0e38f && mx <= 3.0e38f);  // NaN or +-inf in the block
-      const Side sd = make_side(mn, mx, BITS);
+      const Side sd = make_side<true>(mn, mx, BITS);
       // the channel's LSB-first stream of 32 codes in token order (BITS words): this lane's
       // codes placed as if hc = 0 (token 8i + j at bit (8i + j) BITS), shifted by 4 BITS bits
       // for hc = 1, then the two half-wave patterns OR-ed together
@@ -460,7 +460,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
         mx = max_nan(mx, o.y);
       }
       const bool bad = !(mn >= -3.0e38f && mx <= 3.0e38f);  // NaN or +-inf in the block
-      const Side sd = make_side(mn, mx, BITS);
+      const Side sd = make_side<true>(mn, mx, BITS);
       float r[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) {

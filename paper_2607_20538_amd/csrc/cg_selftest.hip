@@ -1,6 +1,7 @@
 // Exhaustive device self-test of the binary32 steps of the quantiser that replace a division:
 // the block range divided by 2^b - 1 and the reciprocal of a binary16 scale must equal
-// correctly rounded division bit for bit (the CPU oracle divides with IEEE binary32 division).
+// correctly rounded division bit for bit (the CPU oracle divides with IEEE binary32 division);
+// and of the binary16 directed roundings done by the hardware conversion under a rounding mode.
 #include "cg_internal.h"
 #include "cg_device.h"
 
@@ -31,11 +32,32 @@ __global__ void selftest_div(unsigned long long* bad, int bits, uint32_t exp_lo,
   }
 }
 
+// binary16 rounding toward -inf / +inf by the hardware conversion under a directed mode
+// against the software rounding, for every binary32 value of both signs in binades
+// [exp_lo, exp_hi) (the binary16 subnormals through the overflow threshold)
+__global__ void selftest_f16_directed(unsigned long long* bad, uint32_t exp_lo, uint32_t exp_hi) {
+  const uint64_t n = uint64_t(exp_hi - exp_lo) << 24;
+  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += uint64_t(gridDim.x) * blockDim.x) {
+    const uint32_t u = ((exp_lo << 23) + uint32_t(i >> 1)) | (uint32_t(i & 1) << 31);
+    const float v = __uint_as_float(u);
+    if (f16_bits_down_hw(v) != f16_bits_down(v) || f16_bits_up_hw(v) != f16_bits_up(v)) atomicAdd(bad, 1ull);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_selftest(int which, unsigned long long* bad, hipStream_t st) {
   if (which == 0) {
     hipLaunchKernelGGL(selftest_rcp, dim3((0x7bff + 255) / 256), dim3(256), 0, st, bad);
+    return hipGetLastError();
+  }
+  if (which == 2) {
+    // binades 2^-33 .. 2^17 (values below round to 0 or the smallest subnormal, above to the
+    // largest finite value or infinity), plus zero and the binary32 subnormals (binade 0)
+    hipLaunchKernelGGL(selftest_f16_directed, dim3(4096), dim3(256), 0, st, bad, 94u, 145u);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(selftest_f16_directed, dim3(4096), dim3(256), 0, st, bad, 0u, 1u);
     return hipGetLastError();
   }
   const int widths[5] = {2, 3, 4, 6, 8};

@@ -495,11 +495,14 @@ def test_library_gauge_upload_matches_user_upload():
     assert torch.equal(a, b)
 
 
-@pytest.mark.parametrize("which", [0, 1])
+@pytest.mark.parametrize("which", [0, 1, 2])
 def test_division_free_quantiser_steps_are_correctly_rounded(which):
     """The kernels replace two binary32 divisions of the quantiser (range / (2^b - 1) and
     1 / scale) by multiply-and-correct sequences; the device self-test compares them with
-    correctly rounded division over every binary16 scale and every binary32 significand."""
+    correctly rounded division over every binary16 scale and every binary32 significand
+    (which = 0, 1).  which = 2: the matrix-core encoder's binary16 roundings toward -inf / +inf
+    by the hardware conversion under a directed rounding mode equal the software rounding for
+    every binary32 value of the binades the binary16 range meets."""
     bad = torch.zeros(1, dtype=torch.int64, device="cuda")
     cg.cg_selftest(which, bad)
     torch.cuda.synchronize()
