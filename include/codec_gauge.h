@@ -321,8 +321,8 @@ int32_t kv_append_paged(int32_t l0, int32_t l1, const cg_kv_view* k_new, const c
  * five, and counts the ranges whose binary16 scale (rounded up) would differ; which = 2
  * compares the binary16 roundings toward -inf and +inf (block minimum and scale) that the
  * matrix-core encoder takes from the hardware conversion under a directed rounding mode with
- * the exact software rounding, for every binary32 value of both signs in the binades from
- * 2^-33 to 2^17 and the binary32 subnormals, and counts the values where either differs.  Adds the
+ * the exact software rounding, for every binary32 bit pattern (zeros, subnormals, normals,
+ * infinities and NaNs of both signs), and counts the values where either differs.  Adds the
  * number of mismatches to the caller-zeroed device uint64 *mismatches_dev (8-byte aligned)
  * on `stream`; a correct build adds 0.  Errors: CG_ERR_ARG, CG_ERR_ALIGN, CG_ERR_DEVICE. */
 int32_t cg_selftest(int32_t which, uint64_t* mismatches_dev, void* stream);

@@ -46,8 +46,8 @@ __device__ __forceinline__ uint32_t f16_bits_up(float v) {
 // the mode for the conversion nor fuses the conversion into the instruction producing v (which
 // would round an unrounded product); s_nop 1 covers the wait states between s_setreg and a
 // VALU instruction that depends on the mode.  The mode is per wave and restored to nearest
-// even.  cg_selftest(2) checks both against f16_bits_down / f16_bits_up over every binary32
-// value of the binades the binary16 range meets.
+// even.  cg_selftest(2) checks both against f16_bits_down / f16_bits_up for every binary32
+// bit pattern.
 template <int MODE>
 __device__ __forceinline__ uint32_t f16_bits_directed_hw(float v) {
   uint32_t bits;

@@ -33,8 +33,8 @@ __global__ void selftest_div(unsigned long long* bad, int bits, uint32_t exp_lo,
 }
 
 // binary16 rounding toward -inf / +inf by the hardware conversion under a directed mode
-// against the software rounding, for every binary32 value of both signs in binades
-// [exp_lo, exp_hi) (the binary16 subnormals through the overflow threshold)
+// against the software rounding, for every binary32 value of both signs whose exponent field
+// lies in [exp_lo, exp_hi)
 __global__ void selftest_f16_directed(unsigned long long* bad, uint32_t exp_lo, uint32_t exp_hi) {
   const uint64_t n = uint64_t(exp_hi - exp_lo) << 24;
   for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += uint64_t(gridDim.x) * blockDim.x) {
@@ -52,12 +52,9 @@ hipError_t launch_selftest(int which, unsigned long long* bad, hipStream_t st) {
     return hipGetLastError();
   }
   if (which == 2) {
-    // binades 2^-33 .. 2^17 (values below round to 0 or the smallest subnormal, above to the
-    // largest finite value or infinity), plus zero and the binary32 subnormals (binade 0)
-    hipLaunchKernelGGL(selftest_f16_directed, dim3(4096), dim3(256), 0, st, bad, 94u, 145u);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(selftest_f16_directed, dim3(4096), dim3(256), 0, st, bad, 0u, 1u);
+    // every binary32 value of both signs with exponent field 0 .. 255: zeros, subnormals,
+    // normals, the infinities and the NaNs (a NaN converts to a NaN both ways)
+    hipLaunchKernelGGL(selftest_f16_directed, dim3(8192), dim3(256), 0, st, bad, 0u, 256u);
     return hipGetLastError();
   }
   const int widths[5] = {2, 3, 4, 6, 8};

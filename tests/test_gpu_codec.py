@@ -502,7 +502,7 @@ def test_division_free_quantiser_steps_are_correctly_rounded(which):
     correctly rounded division over every binary16 scale and every binary32 significand
     (which = 0, 1).  which = 2: the matrix-core encoder's binary16 roundings toward -inf / +inf
     by the hardware conversion under a directed rounding mode equal the software rounding for
-    every binary32 value of the binades the binary16 range meets."""
+    every binary32 bit pattern."""
     bad = torch.zeros(1, dtype=torch.int64, device="cuda")
     cg.cg_selftest(which, bad)
     torch.cuda.synchronize()
