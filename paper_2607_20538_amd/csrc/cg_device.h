@@ -136,6 +136,11 @@ __device__ __forceinline__ float quantize_t(float z, float mn, float inv) {
   return (z - mn) * inv;
 }
 
+// The code of t as an integer in one instruction: v_cvt_pk_u8_f32 rounds to nearest even and
+// saturates to [0, 255] (codes of at most 8 bits lie in [0, 2^b - 1] for finite blocks, so
+// this equals rint_even(t)), writing byte 0 of a zeroed word.
+__device__ __forceinline__ uint32_t code_u8(float t) { return __builtin_amdgcn_cvt_pk_u8_f32(t, 0, 0u); }
+
 // zhat = fl32(mn + q * sc); q * sc is exact in binary32.
 __device__ __forceinline__ float dequantize(uint32_t q, float mn, float sc) {
 #pragma clang fp contract(off)

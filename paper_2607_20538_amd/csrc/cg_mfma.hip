@@ -418,7 +418,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
       for (int i = 0; i < BITS; ++i) words[i] = 0;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const uint32_t q = uint32_t(quantize_rint(z[e], sd.mn, sd.inv));
+        const uint32_t q = code_u8(quantize_t(z[e], sd.mn, sd.inv));
         const int bit = (8 * (e >> 2) + (e & 3)) * BITS, wd = bit >> 5, off = bit & 31;
         words[wd] |= q << off;
         if (off + BITS > 32) words[wd + 1] |= q >> (32 - off);
@@ -464,9 +464,8 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
       float r[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        // the byte packing below rounds to nearest even itself (2, 4, 8 bits)
-        if constexpr (BITS == 2 || BITS == 4 || BITS == 8) r[e] = quantize_t(z[e], sd.mn, sd.inv);
-        else r[e] = quantize_rint(z[e], sd.mn, sd.inv);
+        // v_cvt_pk_u8_f32 below rounds to nearest even (packing bytes, or code_u8)
+        r[e] = quantize_t(z[e], sd.mn, sd.inv);
       }
       constexpr int NW = (BITS & 1) ? BITS : BITS / 2;  // words this lane stores
       uint32_t words[NW];
@@ -496,7 +495,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
       } else {
         uint32_t q[16];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) q[e] = uint32_t(r[e]);
+        for (int e = 0; e < 16; ++e) q[e] = code_u8(r[e]);
         if constexpr (BITS == 6) {
           pack16<BITS>(q, words);
         } else {
