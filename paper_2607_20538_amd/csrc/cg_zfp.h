@@ -110,7 +110,7 @@ __device__ int zfp_encode_block(const float (&v)[16], int rate, uint32_t (&w)[4]
     for (int plane = top; ok && plane >= 0; --plane) {
       uint32_t x = 0u;
 #pragma unroll
-      for (int c = 0; c < 16; ++c) x |= ((u[c] >> plane) & 1u) << c;
+      for (int c = 0; c < 16; ++c) x |= __builtin_amdgcn_ubfe(u[c], plane, 1) << c;  // v_bfe_u32 + v_lshl_or_b32
       if (n && !st.put(x, n)) break;
       x >>= n;
       while (n < 16) {
