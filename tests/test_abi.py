@@ -318,3 +318,13 @@ def test_stream_probe_rejects_bad_sizes_on_the_host():
     assert L.cg_stream_probe(None, 8192, fake, 0, None) == cg.CG_ERR_ARG
     assert L.cg_stream_probe(fake, 8192, None, 16, None) == cg.CG_ERR_ARG
     assert L.cg_stream_probe(C.c_void_p((1 << 20) + 8), 8192, fake, 16, None) == cg.CG_ERR_ALIGN
+
+
+def test_selftest_rejects_bad_arguments_on_the_host():
+    L = cg.lib()
+    fake = C.c_void_p(1 << 20)  # never dereferenced: every case fails validation first
+    for which in (-1, 3, 100):
+        assert L.cg_selftest(which, fake, None) == cg.CG_ERR_ARG
+    for which in (0, 1, 2):
+        assert L.cg_selftest(which, None, None) == cg.CG_ERR_ARG
+        assert L.cg_selftest(which, C.c_void_p((1 << 20) + 4), None) == cg.CG_ERR_ALIGN
