@@ -573,6 +573,15 @@ def main():
                                "block-uniform 4-bit n=64",
                    "elements": n_elem, "global_batch": w.B, "seq_len": w.T, "parallelism": "none"},
         "roofline": roofline,
+        # per direction, from the HIP-event launch averages: logical bf16 GB/s of the tensor a launch
+        # handles (K or V) and key / value vectors per second (one per (layer, batch, head, token))
+        "rates": {
+            "encode_logical_GBps": round(n_elem / (enc_ms * 1e-3) / 1e9, 1),
+            "decode_logical_GBps": round(n_elem / (dec_ms * 1e-3) / 1e9, 1),
+            "encode_token_heads_per_s": round(n_elem / 2 / w.d / (enc_ms * 1e-3), -6),
+            "decode_token_heads_per_s": round(n_elem / 2 / w.d / (dec_ms * 1e-3), -6),
+            "round_trip_token_heads_per_s": round(n_elem / w.d / (ms_step * 1e-3), -6),
+        },
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
