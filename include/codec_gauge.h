@@ -143,8 +143,9 @@ typedef struct cg_kv_view {
   int64_t stride_l, stride_b, stride_h, stride_t;  /* in elements */
 } cg_kv_view;
 
-/* One compressed K or V cache (device buffers sized by cache_bytes()).  len: tokens the
- * cache currently holds (host value, read by kv_decode for KIVI and block-uniform tiles). */
+/* One compressed K or V cache (device buffers sized by cache_bytes()).  len: tokens every
+ * batch row of the cache currently holds (host value, read by kv_decode for KIVI and
+ * block-uniform tiles when it is given no per-row lengths, and by kv_attend without lens). */
 typedef struct cg_cache {
   void* codes;
   void* side;      /* NULL for passthrough */
@@ -198,12 +199,18 @@ int32_t kv_encode(int32_t s, const cg_kv_view* X, const void* G_dev, cg_gauge_sh
                   const cg_cache* out, int32_t t0, int32_t* err_flag, void* stream);
 
 /* Decode: Zhat = D(B_c), Xhat = G^T Zhat (section 3) for cache positions
- * [t0, t0 + Xhat->T) into Xhat (bf16 rounded to nearest even, or binary32).  KIVI tokens
- * at or beyond T_q(in->len), and staged tokens of block-uniform tiles (at or beyond
- * floor(in->len / Tb) * Tb), come back bit for bit; both require t0 + Xhat->T <= in->len.
- * Errors: as kv_encode. */
+ * [t0, t0 + Xhat->T) into Xhat (bf16 rounded to nearest even, or binary32).
+ * lens (optional): device int32[B], the positions batch row b of the cache holds (the rows of
+ * one layer's [B x H x T x d] cache may hold different lengths, section 3), read on the
+ * device only: row b writes view rows for positions [t0, min(t0 + Xhat->T, lens[b])) and leaves
+ * the rest of its view rows untouched; a length outside [0, T_cap] sets CG_FLAG_POS_RANGE and
+ * the row writes nothing.  NULL: every row holds in->len positions.  A KIVI cache of length T
+ * quantises its first T_q(T) positions and keeps the rest in the window, a block-uniform tile
+ * cache its first floor(T / Tb) * Tb; window and staged positions come back bit for bit.
+ * Without lens, KIVI and tile caches require t0 + Xhat->T <= in->len (CG_ERR_CAPACITY).  The
+ * zfp-style backend takes no lens (CG_ERR_UNSUPPORTED).  Errors: as kv_encode. */
 int32_t kv_decode(int32_t s, const cg_cache* in, const void* G_dev, cg_gauge_shape shp, const cg_codec* codec,
-                  int32_t t0, const cg_kv_view* Xhat, int32_t* err_flag, void* stream);
+                  const int32_t* lens, int32_t t0, const cg_kv_view* Xhat, int32_t* err_flag, void* stream);
 
 /* Rolling compressed-history step (section 4.4: every new KV token passes through gauge,
  * backend, decode and inverse gauge), for layers [l0, l1):

@@ -80,7 +80,7 @@ def lib() -> C.CDLL:
         L.kv_encode.argtypes = [i32, C.POINTER(KvView), p, GaugeShape, C.POINTER(CodecStruct),
                                 C.POINTER(CacheStruct), i32, p, p]
         L.kv_encode.restype = i32
-        L.kv_decode.argtypes = [i32, C.POINTER(CacheStruct), p, GaugeShape, C.POINTER(CodecStruct), i32,
+        L.kv_decode.argtypes = [i32, C.POINTER(CacheStruct), p, GaugeShape, C.POINTER(CodecStruct), p, i32,
                                 C.POINTER(KvView), p, p]
         L.kv_decode.restype = i32
         L.kv_append_step.argtypes = [i32, i32, C.POINTER(KvView), C.POINTER(KvView), p, p, GaugeShape,
@@ -234,10 +234,11 @@ def kv_encode(s: int, X, G_dev, shp: GaugeShape, codec: Codec, cache: Cache, t0:
 
 
 def kv_decode(s: int, cache: Cache, G_dev, shp: GaugeShape, codec: Codec, t0: int, Xhat, err_flag=None,
-              stream=None):
+              stream=None, lens=None):
+    """lens: optional device int32 tensor [B] of per-row lengths (else every row holds cache.len)."""
     v, cs, ks = view(Xhat), codec.struct(), cache.struct()
-    rc = lib().kv_decode(s, C.byref(ks), _ptr(G_dev), shp, C.byref(cs), t0, C.byref(v), _ptr(err_flag),
-                         _stream(stream))
+    rc = lib().kv_decode(s, C.byref(ks), _ptr(G_dev), shp, C.byref(cs), _ptr(lens), t0, C.byref(v),
+                         _ptr(err_flag), _stream(stream))
     _check("kv_decode", rc)
 
 

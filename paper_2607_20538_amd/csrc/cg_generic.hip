@@ -365,7 +365,8 @@ __global__ __launch_bounds__(kThreads) void enc_generic(int s, ViewDev X, int l0
 // decode
 // ------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void dec_generic(int s, CacheDev k, int l0, GaugeDev G, CodecDev c, int t0,
-                                                        int len, const int* pos, ViewDev Y, int TT, int* err) {
+                                                        int len, const int* pos, int pos_add, ViewDev Y, int TT,
+                                                        int* err) {
   extern __shared__ float sm[];
   const int d = Y.d, dp = d + kPad;
   float* zs = sm;
@@ -378,15 +379,20 @@ __global__ __launch_bounds__(kThreads) void dec_generic(int s, CacheDev k, int l
   const size_t slc = (size_t(l) * k.B + b) * k.H + h;
   const size_t ybase = size_t(lv) * Y.sl + size_t(b) * Y.sb + size_t(h) * Y.sh;
 
-  // Positions the cache holds bound the rows written: pos[b] + 1 in a rolling step, `len` for
-  // a KIVI or tile cache, otherwise every requested position (the host checked the capacity).
+  // Positions the cache holds bound the rows written: pos[b] + pos_add per row (a rolling step's
+  // newest position + 1, or kv_decode's per-row lengths; outside [0, T_cap] the row is flagged
+  // and skipped), else `len` for a KIVI or tile cache, otherwise every requested position (the
+  // host checked the capacity).
   const bool kivi = c.backend == CG_BACKEND_KIVI;
   const bool tiles = c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt > 1;
   int held = INT_MAX;
   if (pos) {
-    const int p = pos[b];
-    if (p < 0 || p >= k.T_cap) return;  // flagged by the append kernel
-    held = p + 1;
+    const int hb = pos[b] + pos_add;
+    if (hb < 0 || hb > k.T_cap) {
+      if (err && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, CG_FLAG_POS_RANGE);
+      return;
+    }
+    held = hb;
   } else if (kivi || tiles) {
     held = len;
   }
@@ -445,7 +451,6 @@ __global__ __launch_bounds__(kThreads) void dec_generic(int s, CacheDev k, int l
       else ((float*)Y.ptr)[off] = bf16_to_f32(raw);
     }
   }
-  (void)err;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -558,14 +563,14 @@ hipError_t launch_encode_generic(int s, const ViewDev& X, int l0, const GaugeDev
 }
 
 hipError_t launch_decode_generic(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
-                                 int len, const int* pos, const ViewDev& Y, int* err, hipStream_t st) {
+                                 int len, const int* pos, int pos_add, const ViewDev& Y, int* err, hipStream_t st) {
   if (Y.T == 0) return hipSuccess;
   const int TT = tile_tokens(c);
   const size_t smem = size_t(2) * TT * (Y.d + kPad) * sizeof(float);
   hipError_t e = set_smem((const void*)dec_generic, smem);
   if (e != hipSuccess) return e;
   dim3 grid((Y.T + TT - 1) / TT, Y.L * Y.B * Y.H);
-  hipLaunchKernelGGL(dec_generic, grid, dim3(kThreads), smem, st, s, k, l0, G, c, t0, len, pos, Y, TT, err);
+  hipLaunchKernelGGL(dec_generic, grid, dim3(kThreads), smem, st, s, k, l0, G, c, t0, len, pos, pos_add, Y, TT, err);
   return hipGetLastError();
 }
 

@@ -380,10 +380,10 @@ hipError_t launch_encode(int s, const ViewDev& X, int l0, const GaugeDev& G, con
 }
 
 hipError_t launch_decode(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0, int len,
-                         const int* pos, const ViewDev& Y, int* err, hipStream_t st) {
+                         const int* pos, int pos_add, const ViewDev& Y, int* err, hipStream_t st) {
   if (!force_generic() && mfma_decode_supported(s, Y, G, c))
-    return launch_decode_mfma(s, k, l0, G, c, t0, len, pos, Y, err, st);
-  return launch_decode_generic(s, k, l0, G, c, t0, len, pos, Y, err, st);
+    return launch_decode_mfma(s, k, l0, G, c, t0, len, pos, pos_add, Y, err, st);
+  return launch_decode_generic(s, k, l0, G, c, t0, len, pos, pos_add, Y, err, st);
 }
 
 }  // namespace cg
@@ -557,7 +557,7 @@ int32_t kv_encode(int32_t s, const cg_kv_view* X, const void* G_dev, cg_gauge_sh
 }
 
 int32_t kv_decode(int32_t s, const cg_cache* in, const void* G_dev, cg_gauge_shape shp, const cg_codec* codec,
-                  int32_t t0, const cg_kv_view* Xhat, int32_t* err_flag, void* stream) {
+                  const int32_t* lens, int32_t t0, const cg_kv_view* Xhat, int32_t* err_flag, void* stream) {
   int32_t rc = check_shape(shp);
   if (rc != CG_OK) return rc;
   if (s < 0 || s > 1 || !G_dev) return CG_ERR_ARG;
@@ -567,11 +567,13 @@ int32_t kv_decode(int32_t s, const cg_cache* in, const void* G_dev, cg_gauge_sha
   if ((rc = check_cache(in, codec, shp, Xhat->B)) != CG_OK) return rc;
   if (t0 < 0) return CG_ERR_ARG;
   if (int64_t(t0) + Xhat->T > in->T_cap) return CG_ERR_CAPACITY;
+  if (lens && (reinterpret_cast<uintptr_t>(lens) & 3u)) return CG_ERR_ALIGN;
   const bool held = codec->backend == CG_BACKEND_KIVI || (codec->backend == CG_BACKEND_BLOCK_UNIFORM && codec->block_t > 1);
-  if (held && (in->len < 0 || in->len > in->T_cap || int64_t(t0) + Xhat->T > in->len)) return CG_ERR_CAPACITY;
-  if (codec->backend == CG_BACKEND_ZFP && (t0 % 4 || Xhat->T % 4)) return CG_ERR_UNSUPPORTED;
+  // with device row lengths the rows bound themselves on the device; else the host length does
+  if (!lens && held && (in->len < 0 || in->len > in->T_cap || int64_t(t0) + Xhat->T > in->len)) return CG_ERR_CAPACITY;
+  if (codec->backend == CG_BACKEND_ZFP && (lens || t0 % 4 || Xhat->T % 4)) return CG_ERR_UNSUPPORTED;
   if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
-  hipError_t e = launch_decode(s, cache_dev(in), 0, gauge_dev(G_dev, shp), codec_dev(codec), t0, in->len, nullptr,
+  hipError_t e = launch_decode(s, cache_dev(in), 0, gauge_dev(G_dev, shp), codec_dev(codec), t0, in->len, lens, 0,
                                view_dev(Xhat), err_flag, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
 }
@@ -607,9 +609,9 @@ int32_t kv_append_step(int32_t l0, int32_t l1, const cg_kv_view* k_new, const cg
   hipError_t e = launch_append(0, view_dev(k_new), l0, pos, G, c, cache_dev(kc), err_flag, st);
   if (e == hipSuccess) e = launch_append(1, view_dev(v_new), l0, pos, G, c, cache_dev(vc), err_flag, st);
   if (e == hipSuccess && k_hist)
-    e = launch_decode(0, cache_dev(kc), l0, G, c, 0, 0, pos, view_dev(k_hist), err_flag, st);
+    e = launch_decode(0, cache_dev(kc), l0, G, c, 0, 0, pos, 1, view_dev(k_hist), err_flag, st);
   if (e == hipSuccess && v_hist)
-    e = launch_decode(1, cache_dev(vc), l0, G, c, 0, 0, pos, view_dev(v_hist), err_flag, st);
+    e = launch_decode(1, cache_dev(vc), l0, G, c, 0, 0, pos, 1, view_dev(v_hist), err_flag, st);
   return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
 }
 

@@ -98,7 +98,7 @@ hipError_t launch_encode_generic(int s, const ViewDev& X, int l0, const GaugeDev
                                  const CacheDev& k, int t0, int tq, int* err, hipStream_t st,
                                  const PageDev& pt = PageDev());
 hipError_t launch_decode_generic(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
-                                 int len, const int* pos, const ViewDev& Y, int* err, hipStream_t st);
+                                 int len, const int* pos, int pos_add, const ViewDev& Y, int* err, hipStream_t st);
 
 // Matrix-core kernels: bf16, head dimension 128, block-uniform (n in {16, 32, 64}) or passthrough.
 bool mfma_encode_supported(const ViewDev& X, const GaugeDev& G, const CodecDev& c);
@@ -106,7 +106,7 @@ bool mfma_decode_supported(int s, const ViewDev& Y, const GaugeDev& G, const Cod
 hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c,
                               const CacheDev& k, int t0, int tq, int* err, hipStream_t st);
 hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
-                              int len, const int* pos, const ViewDev& Y, int* err, hipStream_t st);
+                              int len, const int* pos, int pos_add, const ViewDev& Y, int* err, hipStream_t st);
 
 // Spectral statistics (section 4.2): workspace sections (bytes from the start, 256-aligned):
 // energy sums binary64 [L][Tb][d], log sums binary64 [L], DCT-II rows binary64 [d][d], and for
@@ -156,10 +156,12 @@ hipError_t launch_selftest(int which, unsigned long long* bad, hipStream_t st);
 hipError_t launch_encode(int s, const ViewDev& X, int l0, const GaugeDev& G, const CodecDev& c, const CacheDev& k,
                          int t0, int tq, int* err, hipStream_t st);
 // Decode cache positions [t0, t0 + Y.T) into view Y (layer l of Y is cache layer l + l0).
-// If pos is non-NULL, batch row b holds pos[b] + 1 tokens and only positions <= pos[b] are
-// written; otherwise the cache holds `len` tokens (KIVI window split).
+// If pos is non-NULL, batch row b holds pos[b] + pos_add tokens (a rolling step passes its
+// positions with pos_add = 1, kv_decode its per-row lengths with pos_add = 0) and only the
+// positions it holds are written (a count outside [0, T_cap] flags CG_FLAG_POS_RANGE and skips
+// the row); otherwise every row holds `len` tokens (KIVI window and tile staging split).
 hipError_t launch_decode(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0, int len,
-                         const int* pos, const ViewDev& Y, int* err, hipStream_t st);
+                         const int* pos, int pos_add, const ViewDev& Y, int* err, hipStream_t st);
 // Rolling append of one token per (layer, b, h) at pos[b] (layer l of Xn is cache layer l + l0).
 hipError_t launch_append(int s, const ViewDev& Xn, int l0, const int* pos, const GaugeDev& G, const CodecDev& c,
                          const CacheDev& k, int* err, hipStream_t st, const PageDev& pt = PageDev());

@@ -29,6 +29,7 @@
 // computed once per workgroup in binary64.  Centring keeps the two terms small when a block
 // spans a group whose values sit far from the block's minimum (an outlier in another group
 // of the same block), where mn * colsum and sc * G^T q would cancel.
+#include <cstdlib>
 #include <type_traits>
 
 #include "cg_internal.h"
@@ -67,7 +68,10 @@ struct MfmaArgs {
   int kivi, win, kg, len;
   // work split
   int nslices, chunks, tiles_per_wg;
-  const int* pos;                // decode only: batch row b holds positions [0, pos[b]]
+  // decode only: batch row b holds positions [0, pos[b] + pos_add) (rolling step: pos_add = 1,
+  // the row's newest position; per-row lengths: pos_add = 0); NULL: every row holds `len`
+  const int* pos;
+  int pos_add;
   int* err;
 };
 
@@ -576,6 +580,18 @@ __device__ __forceinline__ int kivi_quantised_rows(const MfmaArgs& a, int held, 
   return max(0, min(Tv, tq - a.t0));
 }
 
+// Positions row b holds under per-row lengths: pos[b] + pos_add.  A length outside
+// [0, T_cap] sets CG_FLAG_POS_RANGE (once per slice) and the row is skipped.
+__device__ __forceinline__ bool row_held(const MfmaArgs& a, int b, int chunk, int& held) {
+  const int hb = a.pos[b] + a.pos_add;
+  if (hb < 0 || hb > a.T_cap) {
+    if (a.err && chunk == 0 && threadIdx.x == 0) atomicOr(a.err, CG_FLAG_POS_RANGE);
+    return false;
+  }
+  held = hb;
+  return true;
+}
+
 // View rows [r0, r1) copied from the window ring (bf16, slot = position mod ring_slots).
 template <bool OUT_BF16>
 __device__ void ring_rows(const MfmaArgs& a, size_t cslice, char* ys, int r0, int r1) {
@@ -630,10 +646,8 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
   int Tv = a.T;  // view tokens to write
   int held = a.kivi || TB > 1 ? a.len : INT_MAX;  // positions the cache holds
   if (a.pos) {
-    const int p = a.pos[b];
-    if (p < 0 || p >= a.T_cap) return;  // flagged by the append kernel
-    held = p + 1;
-    Tv = min(Tv, p + 1 - a.t0);
+    if (!row_held(a, b, chunk, held)) return;
+    Tv = min(Tv, held - a.t0);
   }
   const int ntiles = (Tv + kTok - 1) / kTok;
   const int tb = chunk * a.tiles_per_wg;
@@ -965,10 +979,8 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
   int Tv = a.T;
   int held = a.kivi || TB > 1 ? a.len : INT_MAX;  // positions the cache holds
   if (a.pos) {
-    const int p = a.pos[b];
-    if (p < 0 || p >= a.T_cap) return;  // flagged by the append kernel
-    held = p + 1;
-    Tv = min(Tv, p + 1 - a.t0);
+    if (!row_held(a, b, chunk, held)) return;
+    Tv = min(Tv, held - a.t0);
   }
   const int ntiles = (Tv + kTok - 1) / kTok;
   const int tb = chunk * a.tiles_per_wg;
@@ -1211,10 +1223,8 @@ __global__ __launch_bounds__(kThreads, OUT_BF16 ? 3 : 2) void dec_keys(MfmaArgs 
   int Tv = a.T;
   int held = a.len;
   if (a.pos) {
-    const int p = a.pos[b];
-    if (p < 0 || p >= a.T_cap) return;  // flagged by the append kernel
-    held = p + 1;
-    Tv = min(Tv, p + 1 - a.t0);
+    if (!row_held(a, b, chunk, held)) return;
+    Tv = min(Tv, held - a.t0);
   }
   if (Tv <= 0) return;
   char* ys = a.x + YB * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
@@ -1226,7 +1236,9 @@ __global__ __launch_bounds__(kThreads, OUT_BF16 ? 3 : 2) void dec_keys(MfmaArgs 
   const int tb = chunk * a.tiles_per_wg;
   const int te_all = min(ntiles, tb + a.tiles_per_wg);
   if (tb >= te_all) return;
-  const int te = min(te_all, (a.t0 + Tq + kTok - 1) / kTok - g0);
+  // key groups holding quantised view rows; none when Tq = 0 (a range that starts inside a group
+  // and lies in the window would otherwise keep that group, and its flush would have no live row)
+  const int te = Tq > 0 ? min(te_all, (a.t0 + Tq + kTok - 1) / kTok - g0) : 0;
   const int row_lo = max(0, kTok * (g0 + tb) - a.t0), row_hi = min(Tv, kTok * (g0 + te_all) - a.t0);
   if (tb >= te) {
     ring_rows<OUT_BF16>(a, cslice, ys, max(Tq, row_lo), row_hi);
@@ -1515,6 +1527,17 @@ int cu_count() {
 // Split the (slice, tile) space into workgroups: as many as can be resident at once (the
 // kernel's occupancy per CU times the CUs), each a contiguous tile range of one slice; the
 // count is padded to a multiple of 8 (XCD remap).
+//
+// CG_TILES_PER_WG=k (read at every launch) fixes the tiles per workgroup instead, so that small
+// inputs run the multi-tile pipeline (ring wrap, prefetch, overlapped flush, exact waits) that
+// the resident grid only reaches on large ones; the tests compare both geometries.
+int forced_tiles_per_wg() {
+  const char* e = getenv("CG_TILES_PER_WG");
+  if (!e || !*e) return 0;
+  const long v = strtol(e, nullptr, 10);
+  return v > 0 && v < (1 << 20) ? int(v) : 0;
+}
+
 void plan(MfmaArgs& m, int nslices, int T, const void* fn) {
   const int ntiles = (T + kTok - 1) / kTok;
   int occ = 0;
@@ -1523,6 +1546,7 @@ void plan(MfmaArgs& m, int nslices, int T, const void* fn) {
   int chunks = (target + nslices - 1) / nslices;
   chunks = chunks < 1 ? 1 : (chunks > ntiles ? ntiles : chunks);
   m.tiles_per_wg = (ntiles + chunks - 1) / chunks;
+  if (const int f = forced_tiles_per_wg()) m.tiles_per_wg = f < ntiles ? f : (ntiles > 0 ? ntiles : 1);
   m.chunks = (ntiles + m.tiles_per_wg - 1) / m.tiles_per_wg;
   m.nslices = nslices;
 }
@@ -1735,7 +1759,7 @@ hipError_t launch_encode_mfma(int s, const ViewDev& X, int l0, const GaugeDev& G
 }
 
 hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& G, const CodecDev& c, int t0,
-                              int len, const int* pos, const ViewDev& Y, int* err, hipStream_t st) {
+                              int len, const int* pos, int pos_add, const ViewDev& Y, int* err, hipStream_t st) {
   if (Y.T == 0) return hipSuccess;
   MfmaArgs m{};
   m.x = (char*)Y.ptr;
@@ -1746,6 +1770,7 @@ hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& 
   m.g32 = G.f32; m.cs8 = G.cs8; m.g = G.g; m.R = G.R; m.Hg = G.H;
   m.codes = k.codes; m.side = k.side; m.T_cap = k.T_cap; m.cB = k.B; m.cH = k.H;
   m.pos = pos;
+  m.pos_add = pos_add;
   m.err = err;
   m.kivi = c.backend == CG_BACKEND_KIVI;
   m.win = c.win;

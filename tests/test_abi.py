@@ -96,10 +96,10 @@ def _encode(view, cache, codec, shp=None, t0=0, s=0, gdev=0x50000, err=None):
     return cg.lib().kv_encode(s, C.byref(view), gdev, shp, C.byref(cs), C.byref(cache), t0, err, None)
 
 
-def _decode(view, cache, codec, shp=None, t0=0, s=0, gdev=0x50000):
+def _decode(view, cache, codec, shp=None, t0=0, s=0, gdev=0x50000, lens=None):
     shp = shp or cg.shape(1, 2, 64, 16)
     cs = codec.struct()
-    return cg.lib().kv_decode(s, C.byref(cache), gdev, shp, C.byref(cs), t0, C.byref(view), None, None)
+    return cg.lib().kv_decode(s, C.byref(cache), gdev, shp, C.byref(cs), lens, t0, C.byref(view), None, None)
 
 
 BU = cg.Codec(cg.BLOCK_UNIFORM, 4, 32)
@@ -158,6 +158,11 @@ def test_encode_decode_reject_ranges_and_modes():
         cg.cache_bytes(tile, 0, 1, 1, 2, 40, 64)
     assert e.value.status == cg.CG_ERR_SHAPE
     assert _decode(_fake_view(T=16), _fake_cache(T_cap=64, len_=8), tile) == cg.CG_ERR_CAPACITY
+    # device per-row lengths: 4-byte aligned; with them the host length no longer bounds the call
+    # (the rows bound themselves on the device), so only the pointer is checked here
+    assert _decode(_fake_view(T=16), _fake_cache(T_cap=64, len_=8), kivi, lens=0x70002) == cg.CG_ERR_ALIGN
+    assert _decode(_fake_view(T=16), _fake_cache(T_cap=64, len_=8), tile, lens=0x70001) == cg.CG_ERR_ALIGN
+    assert _decode(_fake_view(T=16), _fake_cache(T_cap=8), BU, lens=0x70000) == cg.CG_ERR_CAPACITY
 
 
 def test_append_step_rejects_invalid_arguments():
@@ -250,6 +255,7 @@ def test_zfp_backend_sizes_and_restrictions():
     assert _encode(_fake_view(T=6), k, z) == cg.CG_ERR_UNSUPPORTED
     assert _encode(_fake_view(T=8), k, z, t0=2) == cg.CG_ERR_UNSUPPORTED
     assert _decode(_fake_view(T=6), k, z) == cg.CG_ERR_UNSUPPORTED
+    assert _decode(_fake_view(T=8), k, z, lens=0x70000) == cg.CG_ERR_UNSUPPORTED   # whole 4-token rows
     assert _encode(_fake_view(T=8), _fake_cache(T_cap=62, side=0), z) == cg.CG_ERR_SHAPE
     shp = cg.shape(1, 2, 64, 16)
     kn = _fake_view(L=1, T=1, strides=(128, 128, 64, 64))

@@ -250,6 +250,27 @@ def test_kivi_key_decoder(g, bits):
         np.testing.assert_array_equal(_decode_gpu(ddev, 0, Gd, shp, oc, t0, n, torch.float32), out[:, :, :, t0:t0 + n])
 
 
+def test_kivi_window_only_range_inside_a_key_group_stays_in_its_view(kernels):
+    """Regression: a decode range that starts inside a key group and lies wholly in the window
+    (no quantised rows) once kept that group in the key decoder's pipeline, whose flush then
+    stored a row before the view.  Every row outside the view must keep its contents."""
+    T, T_cap = 300, 320
+    w = _workload(T=T, seed=0x5EED)
+    G, Gd, shp = _gauge(O.GAUGE_HAAR, 1, 2, 128, 32)
+    oc = O.Codec(backend=O.KIVI, bits=3, key_tokens=32, val_channels=64, residual=128)
+    tq = O.kivi_tq(T, oc)
+    X = synth.kv_tensor(w, 0)
+    orc, _ = O.kv_encode(oc, 0, X, G, T_cap=T_cap)
+    ddev = cache_to_dev(orc, oc, 0, 1, 2, 2, T_cap, 128, len_=T)
+    for t0, n in ((tq + 5, 20), (tq + 31, 1), (tq + 1, T - tq - 1)):
+        assert t0 % 32 and t0 >= tq
+        big = torch.full((1, 2, 2, n + 64, 128), 7.0, dtype=torch.bfloat16, device="cuda")
+        cg.kv_decode(0, ddev, Gd, shp, to_cg(oc), t0, big[:, :, :, 32:32 + n])
+        torch.cuda.synchronize()
+        assert bool((big[:, :, :, :32] == 7.0).all()) and bool((big[:, :, :, 32 + n:] == 7.0).all())
+        np.testing.assert_array_equal(out_host(big[:, :, :, 32:32 + n].contiguous()), X[:, :, :, t0:t0 + n])
+
+
 # ------------------------------------------------------------------------------------------
 # block-uniform token-channel tiles (one range per Tb x n block, unfinished tiles staged)
 # ------------------------------------------------------------------------------------------
