@@ -285,6 +285,23 @@ int32_t kv_attend(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* k
                   const void* G_dev, cg_gauge_shape shp, const cg_codec* codec, const int32_t* lens, float scale,
                   const cg_kv_view* out, void* workspace, int32_t* err_flag, void* stream);
 
+/* kv_attend for callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): the same arguments without the
+ * workspace, the same validation, split plan and results (bit for bit).  The partial results of
+ * split rows go to a device array the library owns: CG_ATTEND_NOALLOC_SCRATCH_BYTES (32 MiB) per
+ * device, created with the library's code object on a device and held until the process ends;
+ * the call allocates nothing.  A call whose split plan needs more than that
+ * (attend_workspace_bytes over the rows' span) returns CG_ERR_CAPACITY before anything is
+ * enqueued.  Every call on a device shares that device's array and every split writes its whole
+ * partial before the combine reads it, so nothing carries over between calls, but calls that
+ * overlap on one device (different streams, or host threads) race: serialise them.  The device
+ * address of the array is looked up once per device on the first call (CG_ERR_DEVICE if that
+ * fails).  Errors: as kv_attend, plus CG_ERR_CAPACITY for a plan beyond the scratch. */
+#define CG_ATTEND_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int32_t kv_attend_noalloc(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* kc, const cg_cache* vc,
+                          const void* G_dev, cg_gauge_shape shp, const cg_codec* codec, const int32_t* lens,
+                          float scale, const cg_kv_view* out, int32_t* err_flag, void* stream);
+
 /* Workspace bytes of kv_attend_paged: as attend_workspace_bytes for rows of
  * max_pages * page_size positions. */
 size_t attend_paged_workspace_bytes(cg_gauge_shape shp, int32_t nl, int32_t B, int32_t Hq, int32_t max_pages,

@@ -25,6 +25,7 @@ DTYPE_BF16, DTYPE_F32 = 0, 1
 
 EXPORTS = ["cg_status_str", "gauge_device_bytes", "gauge_make", "cache_bytes", "kv_encode", "kv_decode",
            "kv_append_step", "spectral_workspace_bytes", "kv_spectral_stats", "attend_workspace_bytes", "kv_attend",
+           "kv_attend_noalloc",
            "attend_paged_workspace_bytes", "kv_attend_paged", "kv_encode_paged", "kv_append_paged", "cg_selftest",
            "cg_stream_probe"]
 
@@ -96,6 +97,9 @@ def lib() -> C.CDLL:
         L.kv_attend.argtypes = [i32, i32, C.POINTER(KvView), C.POINTER(CacheStruct), C.POINTER(CacheStruct), p,
                                 GaugeShape, C.POINTER(CodecStruct), p, C.c_float, C.POINTER(KvView), p, p, p]
         L.kv_attend.restype = i32
+        L.kv_attend_noalloc.argtypes = [i32, i32, C.POINTER(KvView), C.POINTER(CacheStruct), C.POINTER(CacheStruct),
+                                        p, GaugeShape, C.POINTER(CodecStruct), p, C.c_float, C.POINTER(KvView), p, p]
+        L.kv_attend_noalloc.restype = i32
         L.attend_paged_workspace_bytes.argtypes = [GaugeShape, i32, i32, i32, i32, i32]
         L.attend_paged_workspace_bytes.restype = C.c_size_t
         L.kv_attend_paged.argtypes = [i32, i32, C.POINTER(KvView), C.POINTER(CacheStruct), C.POINTER(CacheStruct),
@@ -293,6 +297,15 @@ def kv_attend(l0: int, l1: int, q, kc: Cache, vc: Cache, G_dev, shp: GaugeShape,
     rc = lib().kv_attend(l0, l1, C.byref(qv), C.byref(kcs), C.byref(vcs), _ptr(G_dev), shp, C.byref(cs), _ptr(lens),
                          float(scale), C.byref(ov), _ptr(workspace), _ptr(err_flag), _stream(stream))
     _check("kv_attend", rc)
+
+
+def kv_attend_noalloc(l0: int, l1: int, q, kc: Cache, vc: Cache, G_dev, shp: GaugeShape, codec: Codec, lens,
+                      scale: float, out, err_flag=None, stream=None):
+    """kv_attend without a workspace: split rows' partials go to the library's device scratch."""
+    qv, ov, cs, kcs, vcs = view(q), view(out), codec.struct(), kc.struct(), vc.struct()
+    rc = lib().kv_attend_noalloc(l0, l1, C.byref(qv), C.byref(kcs), C.byref(vcs), _ptr(G_dev), shp, C.byref(cs),
+                                 _ptr(lens), float(scale), C.byref(ov), _ptr(err_flag), _stream(stream))
+    _check("kv_attend_noalloc", rc)
 
 
 def page_table(pages, page_size: int) -> PageTable:

@@ -15,6 +15,7 @@
 // maximum, normaliser and unnormalised accumulators, and a combine kernel merges the splits and
 // applies G_V^T.  A row with no positions gets a zero output.
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 #include "cg_internal.h"
@@ -1064,6 +1065,37 @@ hipError_t launch_attend(const AttendDev& a, const GaugeDev& G, const CodecDev& 
   const size_t smem2 = (size_t(2) * kJQ * d + 2 * kJQ) * sizeof(float);
   hipLaunchKernelGGL(att_combine, dim3(nrow), dim3(kAThreads), smem2, st, a, G);
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------------
+// scratch of kv_attend_noalloc: the split rows' partial results in a file-scope device array
+// (one per device the library runs on, held until the process ends).  Host code never passes
+// `scratch` itself to a kernel: its device address comes from hipGetSymbolAddress, once per
+// device, with that device current.
+// ------------------------------------------------------------------------------------------
+constexpr size_t kAttendScratchBytes = CG_ATTEND_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kAttendScratchBytes];
+
+size_t attend_scratch_bytes() { return kAttendScratchBytes; }
+
+hipError_t attend_scratch(void** ptr) {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 }  // namespace cg

@@ -642,9 +642,12 @@ size_t attend_workspace_bytes(cg_gauge_shape shp, int32_t nl, int32_t B, int32_t
   return attend_plan(nl, B, shp.H, Hq, shp.d, T_cap).ws_bytes;
 }
 
-int32_t kv_attend(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* kc, const cg_cache* vc,
-                  const void* G_dev, cg_gauge_shape shp, const cg_codec* codec, const int32_t* lens, float scale,
-                  const cg_kv_view* out, void* workspace, int32_t* err_flag, void* stream) {
+// kv_attend and kv_attend_noalloc: the same validation and split plan; the partial results of
+// split rows go to the caller's workspace, or (noalloc) to the library's device scratch.
+static int32_t attend_entry(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* kc, const cg_cache* vc,
+                            const void* G_dev, cg_gauge_shape shp, const cg_codec* codec, const int32_t* lens,
+                            float scale, const cg_kv_view* out, void* workspace, bool noalloc, int32_t* err_flag,
+                            void* stream) {
   int32_t rc = check_shape(shp);
   if (rc != CG_OK) return rc;
   if (!G_dev || l0 < 0 || l1 <= l0 || l1 > shp.L || !isfinite(scale)) return CG_ERR_ARG;
@@ -662,10 +665,15 @@ int32_t kv_attend(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* k
   if (kc->T_cap != vc->T_cap) return CG_ERR_SHAPE;
   if (!lens && (kc->len < 0 || kc->len > kc->T_cap || vc->len != kc->len)) return CG_ERR_CAPACITY;
   const AttendPlan cap = attend_plan(nl, B, shp.H, q->H, shp.d, kc->T_cap);
-  if (cap.ws_bytes && (!workspace || !aligned16(workspace))) return workspace ? CG_ERR_ALIGN : CG_ERR_ARG;
+  if (!noalloc && cap.ws_bytes && (!workspace || !aligned16(workspace))) return workspace ? CG_ERR_ALIGN : CG_ERR_ARG;
   if (err_flag && (reinterpret_cast<uintptr_t>(err_flag) & 3u)) return CG_ERR_ALIGN;
   // rows of known length split over that length; device lengths over the capacity
   const AttendPlan p = lens ? cap : attend_plan(nl, B, shp.H, q->H, shp.d, std::max(1, kc->len));
+  if (noalloc) {
+    if (p.ws_bytes > attend_scratch_bytes()) return CG_ERR_CAPACITY;
+    workspace = nullptr;
+    if (p.ws_bytes && attend_scratch(&workspace) != hipSuccess) return CG_ERR_DEVICE;
+  }
   AttendDev a;
   a.q = view_dev(q);
   a.o = view_dev(out);
@@ -686,6 +694,18 @@ int32_t kv_attend(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* k
   hipError_t e = launch_attend(a, gauge_dev(G_dev, shp), codec_dev(codec), force_generic(),
                                static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
+}
+
+int32_t kv_attend(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* kc, const cg_cache* vc,
+                  const void* G_dev, cg_gauge_shape shp, const cg_codec* codec, const int32_t* lens, float scale,
+                  const cg_kv_view* out, void* workspace, int32_t* err_flag, void* stream) {
+  return attend_entry(l0, l1, q, kc, vc, G_dev, shp, codec, lens, scale, out, workspace, false, err_flag, stream);
+}
+
+int32_t kv_attend_noalloc(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_cache* kc, const cg_cache* vc,
+                          const void* G_dev, cg_gauge_shape shp, const cg_codec* codec, const int32_t* lens,
+                          float scale, const cg_kv_view* out, int32_t* err_flag, void* stream) {
+  return attend_entry(l0, l1, q, kc, vc, G_dev, shp, codec, lens, scale, out, nullptr, true, err_flag, stream);
 }
 
 // page tables: block-uniform per-token blocks or passthrough, pages of a multiple of 64 positions

@@ -143,6 +143,11 @@ struct AttendPlan {
 AttendPlan attend_plan(int nl, int B, int H, int Hq, int d, int span);
 hipError_t launch_attend(const AttendDev& a, const GaugeDev& G, const CodecDev& c, bool force_generic,
                          hipStream_t st);
+// Library-owned scratch of kv_attend_noalloc: its size, and its device address on the current
+// device (looked up once per device; the address, never the array's host-side name, goes to
+// kernels).
+size_t attend_scratch_bytes();
+hipError_t attend_scratch(void** ptr);
 
 // HBM streaming probe (read_bytes a multiple of 8 KB, write_bytes of 16 bytes).
 hipError_t launch_stream_probe(const void* src, int64_t read_bytes, void* dst, int64_t write_bytes, hipStream_t st);

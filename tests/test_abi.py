@@ -241,6 +241,33 @@ def test_attend_rejects_invalid_arguments():
     assert call(kc=big, vc=big, ws=0x70008) == cg.CG_ERR_ALIGN
 
 
+def test_attend_noalloc_validates_like_kv_attend_and_rejects_plans_beyond_its_scratch():
+    """kv_attend_noalloc: the same validation as kv_attend (no workspace argument), and a split plan
+    needing more than the library's 32 MiB device scratch is refused before anything is enqueued
+    (or any device call made)."""
+    f = cg.lib().kv_attend_noalloc
+    def call(shp, q, kc, lens=None, l1=None, codec=BU, scale=0.125):
+        cs = codec.struct()
+        return f(0, q.L if l1 is None else l1, C.byref(q), C.byref(kc), C.byref(kc), 0x50000, shp, C.byref(cs),
+                 lens, scale, C.byref(q), None, None)
+    shp = cg.shape(2, 2, 64, 16)
+    q = _fake_view(L=1, H=4, T=1, strides=(256, 256, 64, 64))
+    k = _fake_cache(L=2, T_cap=64, len_=32)
+    assert call(shp, q, k, l1=3) == cg.CG_ERR_ARG
+    assert call(shp, q, k, scale=float("nan")) == cg.CG_ERR_ARG
+    assert call(shp, q, k, lens=0x60002) == cg.CG_ERR_ALIGN
+    assert call(shp, q, _fake_cache(L=2, T_cap=64, len_=65)) == cg.CG_ERR_CAPACITY
+    assert call(shp, q, k, codec=cg.Codec(cg.BLOCK_UNIFORM, 5, 32)) == cg.CG_ERR_UNSUPPORTED
+    # head_dim 256, 64 layers of one row, 8 query heads per KV head over 4096 positions: four splits
+    # per row and 33.7 MB of partial results
+    big = cg.shape(64, 8, 256, 128)
+    need = cg.attend_workspace_bytes(big, 64, 1, 64, 4096)
+    assert need > (32 << 20)
+    qb = _fake_view(L=64, B=1, H=64, T=1, d=256, strides=(64 * 256, 64 * 256, 256, 256))
+    kb = _fake_cache(L=64, B=1, H=8, T_cap=4096, d=256, len_=4096)
+    assert call(big, qb, kb, lens=0x60000) == cg.CG_ERR_CAPACITY
+
+
 def test_zfp_backend_sizes_and_restrictions():
     z = cg.Codec(cg.ZFP, 4)
     assert cg.cache_bytes(z, 0, 2, 3, 4, 64, 128) == (2 * 3 * 4 * 64 * 128 * 4 // 8, 0, 0)
