@@ -262,9 +262,9 @@ int32_t kv_spectral_stats(int32_t s, const cg_kv_view* X, const void* G_dev, cg_
 size_t attend_workspace_bytes(cg_gauge_shape shp, int32_t nl, int32_t B, int32_t Hq, int32_t T_cap);
 
 /* Decode-phase attention over the compressed caches, with the inverse gauge of section 3
- * folded into the consumer instead of decoding Xhat (section 4.1: some recovery can be folded
- * into downstream projections; section 6: the paper times explicit recovery and leaves kernel
- * fusion to deployments).  For layers [l0, l1), batch
+ * folded into the consumer instead of decoding Xhat (section 4.1 on where the recovery can go;
+ * section 6: the paper times explicit recovery and leaves kernel fusion to deployments).  For
+ * layers [l0, l1), batch
  * row b and query head j (KV head h = j / (Hq / H), grouped-query attention):
  *     o = softmax(scale q Khat^T) Vhat  over the positions [0, n_b) the row holds,
  * with Khat, Vhat the caches as kv_decode would return them in binary32.  Computed as

@@ -1,7 +1,6 @@
 // Decode-phase attention over the compressed caches, with the inverse gauge folded into the
-// attention consumer instead of materialising Xhat (the deployment route the paper points to:
-// some recovery can be folded into downstream projections, section 4.1; its timings include
-// explicit recovery, which deployments can fuse, section 6).
+// attention consumer instead of materialising Xhat: the paper leaves this fusion to deployments
+// (section 4.1 on where the recovery can go; section 6: its timings charge explicit recovery).
 //
 // For one query q of KV head h (query heads h * grp .. h * grp + grp - 1 share that head, as in
 // grouped-query attention) over positions [0, len):

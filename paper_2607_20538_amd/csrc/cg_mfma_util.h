@@ -60,6 +60,22 @@ __device__ __forceinline__ int dpp_mov_i(int v) {
   return __builtin_amdgcn_mov_dpp(v, CTRL, 0xF, 0xF, true);
 }
 
+// Block ranges use the IEEE minimum / maximum (v_minimum3_f32 / v_maximum3_f32): equal to the
+// ordinary min / max on finite and infinite values, and NaN as soon as one element is NaN, so
+// a single test of the range flags a non-finite block (whose codes are unspecified).
+__device__ __forceinline__ float min_nan(float a, float b) { return __builtin_elementwise_minimum(a, b); }
+__device__ __forceinline__ float max_nan(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
+// (min, max) of a lane and the lane 32 away.  v_permlane32_swap exchanges the upper half-wave
+// of one register with the lower half-wave of another; with both registers holding the value,
+// the two results hold, in every lane, the lane's own value and its partner's.
+__device__ __forceinline__ void halves_minmax(float& mn, float& mx) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(mn), __float_as_uint(mn), false, false);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+  mn = min_nan(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  mx = max_nan(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 // B fragment of K-step u of a region (RW packed words starting at the region's first channel)
 // `one` = 0x3F803F80 (the bf16 pair (1, 1)) and `m` = the mantissa field mask of the code
 // width, both held in VGPRs by the caller so that (x & m) | one selects the single
