@@ -280,7 +280,8 @@ def other_workload(name, steps, warmup, cpu=True, probe=False):
     stream = torch.cuda.current_stream()
     w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral", "zfp") else ("rolling" if name in ("attend", "attend_paged", "attend_tiles") else name)]
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
-    out = {"workload": name, "shape": {"L": w.L, "B": w.B, "H": w.H, "T": w.T, "d": w.d}, "steps": steps}
+    out = {"workload": name, "shape": {"L": w.L, "B": w.B, "H": w.H, "T": w.T, "d": w.d}, "steps": steps,
+           "kernels": os.environ.get("CG_KERNELS") or "default"}
 
     def layer_input(s):
         # the workload's first min(8, L) layers, repeated: 8 distinct layers of these shapes span
@@ -323,7 +324,7 @@ def other_workload(name, steps, warmup, cpu=True, probe=False):
     elif name in ("kivi", "gemma27b", "tiles", "zfp"):
         combos = {"kivi": [(w.g, w.bits)], "tiles": [(128, 4), (128, 3), (32, 4)],
                   "zfp": [(128, r) for r in (2, 3, 4, 6, 8)]}.get(
-            name, [(g, b) for g in (8, 32, 128) for b in (3, 4, 6)])
+            name, [(g, b) for g in (8, 16, 32, 128) for b in (3, 4, 6)])
         rows = []
         for g, bits in combos:
             shp = cg.shape(w.L, w.H, w.d, g)
