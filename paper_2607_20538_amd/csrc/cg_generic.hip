@@ -238,47 +238,44 @@ __device__ void store_rows_pass(const float* zs, int ntok, int d, int dp, const 
 
 // zfp-style rows: tile rows [4u, 4u + 4) x channels [4cb, 4cb + 4) form block (pos0 / 4 + u, cb)
 __device__ int store_zfp(const float* zs, int ntok, int d, int dp, int rate, const CacheDev& k, size_t slc,
-                         int pos0) {
-  int flags = 0;
-  const int nbc = d / 4;
-  for (int idx = threadIdx.x; idx < (ntok / 4) * nbc; idx += blockDim.x) {
-    const int u = idx / nbc, cb = idx - u * nbc;
-    float v[16];
+                         int pos0, const ZfpTables& tab) {
+  return zfp_by_rate(rate, [&](auto R) {
+    constexpr int RATE = decltype(R)::value;
+    int flags = 0;
+    const int nbc = d / 4;
+    for (int idx = threadIdx.x; idx < (ntok / 4) * nbc; idx += blockDim.x) {
+      const int u = idx / nbc, cb = idx - u * nbc;
+      float v[16];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[4 * j + i] = zs[(4 * u + j) * dp + 4 * cb + i];
-    uint32_t w[4];
-    flags |= zfp_encode_block(v, rate, w);
-    uint16_t* dst = reinterpret_cast<uint16_t*>(
-        k.codes + ((slc * (k.T_cap / 4) + pos0 / 4 + u) * nbc + cb) * size_t(2 * rate));
-    for (int r = 0; r < rate; ++r) dst[r] = uint16_t(word_of(w, r >> 1) >> (16 * (r & 1)));
-  }
-  return flags;
+        for (int i = 0; i < 4; ++i) v[4 * j + i] = zs[(4 * u + j) * dp + 4 * cb + i];
+      uint32_t w[4];
+      flags |= zfp_encode_block<RATE>(v, tab, w);
+      zfp_store<RATE>(k.codes + ((slc * (k.T_cap / 4) + pos0 / 4 + u) * nbc + cb) * size_t(2 * RATE), w);
+    }
+    return flags;
+  });
 }
 
-__device__ void load_zfp(float* zs, int ntok, int d, int dp, int rate, const CacheDev& k, size_t slc, int pos0) {
-  const int nbc = d / 4;
-  for (int idx = threadIdx.x; idx < (ntok / 4) * nbc; idx += blockDim.x) {
-    const int u = idx / nbc, cb = idx - u * nbc;
-    const uint16_t* src = reinterpret_cast<const uint16_t*>(
-        k.codes + ((slc * (k.T_cap / 4) + pos0 / 4 + u) * nbc + cb) * size_t(2 * rate));
-    uint32_t w[4] = {0u, 0u, 0u, 0u};
-    for (int r = 0; r < rate; ++r) {
-      const uint32_t m = uint32_t(src[r]) << (16 * (r & 1));
-      const int i = r >> 1;
-      w[0] |= i == 0 ? m : 0u;
-      w[1] |= i == 1 ? m : 0u;
-      w[2] |= i == 2 ? m : 0u;
-      w[3] |= i == 3 ? m : 0u;
+__device__ void load_zfp(float* zs, int ntok, int d, int dp, int rate, const CacheDev& k, size_t slc, int pos0,
+                         const ZfpTables& tab) {
+  zfp_by_rate(rate, [&](auto R) {
+    constexpr int RATE = decltype(R)::value;
+    const int nbc = d / 4;
+    for (int idx = threadIdx.x; idx < (ntok / 4) * nbc; idx += blockDim.x) {
+      const int u = idx / nbc, cb = idx - u * nbc;
+      uint32_t w[4];
+      zfp_load<RATE>(k.codes + ((slc * (k.T_cap / 4) + pos0 / 4 + u) * nbc + cb) * size_t(2 * RATE), w);
+      float v[16];
+      zfp_decode_block<RATE>(w, tab, v);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) zs[(4 * u + j) * dp + 4 * cb + i] = v[4 * j + i];
     }
-    float v[16];
-    zfp_decode_block(w, rate, v);
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) zs[(4 * u + j) * dp + 4 * cb + i] = v[4 * j + i];
-  }
+    return 0;
+  });
 }
 
 // ------------------------------------------------------------------------------------------
@@ -331,6 +328,8 @@ __global__ __launch_bounds__(kThreads) void enc_generic(int s, ViewDev X, int l0
     if (nq == 0) return;
   }
 
+  __shared__ ZfpTables ztab;
+  if (c.backend == CG_BACKEND_ZFP) zfp_tables_init(ztab);  // read after the barriers below
   int flags = 0;
   for (int idx = threadIdx.x; idx < TT * d; idx += blockDim.x) {
     const int t = idx / d, ch = idx - t * d;
@@ -348,7 +347,7 @@ __global__ __launch_bounds__(kThreads) void enc_generic(int s, ViewDev X, int l0
   if (c.backend == CG_BACKEND_PASSTHROUGH) {
     store_rows_pass(zs, ntok, d, dp, k, slc, t0 + tile0);
   } else if (c.backend == CG_BACKEND_ZFP) {
-    flags |= store_zfp(zs, ntok, d, dp, c.bits, k, slc, t0 + tile0);
+    flags |= store_zfp(zs, ntok, d, dp, c.bits, k, slc, t0 + tile0, ztab);
   } else if (tiles) {
     flags |= store_tiles(zs, nq / c.bt, c.bt, d, dp, c.n, c.bits, k, slc, t0 + tile0);
   } else if (c.backend == CG_BACKEND_BLOCK_UNIFORM) {
@@ -407,7 +406,12 @@ __global__ __launch_bounds__(kThreads) void dec_generic(int s, CacheDev k, int l
 
   // 1. dequantise the quantised rows into zs
   const int bits = c.bits;
-  if (c.backend == CG_BACKEND_ZFP) load_zfp(zs, nq, d, dp, bits, k, slc, p0);
+  if (c.backend == CG_BACKEND_ZFP) {  // the backend is the same for the whole workgroup
+    __shared__ ZfpTables ztab;
+    zfp_tables_init(ztab);
+    __syncthreads();
+    load_zfp(zs, nq, d, dp, bits, k, slc, p0, ztab);
+  }
   for (int idx = threadIdx.x; c.backend != CG_BACKEND_ZFP && idx < nq * d; idx += blockDim.x) {
     const int t = idx / d, ch = idx - t * d;
     const int p = p0 + t;

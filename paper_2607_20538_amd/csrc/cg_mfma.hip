@@ -175,7 +175,7 @@ constexpr int kModeZfp = 3;    // zfp-style fixed-rate blocks of 4 tokens x 4 ch
 // contiguous run of 32 RB bytes in the cache and its side words one run of 32 NBK words, so
 // the staged copy leaves with whole-line stores instead of 32 scattered row pieces.
 template <int NP, int KS, int BITS, int NB, int MODE, int TB = 1>
-__global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a) {
+__global__ __launch_bounds__(kThreads, NP == 2 && MODE != kModeZfp ? 3 : 2) void enc_mfma(MfmaArgs a) {
   constexpr bool PASS = MODE == kModePass, KEYS = MODE == kModeKeys, ZFP = MODE == kModeZfp;
   constexpr bool QUANT = !PASS && !ZFP;  // block ranges, staged codes and side words
   // token-channel tiles: one range per TB tokens x NB channels (NB spans whole waves)
@@ -191,6 +191,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
   // zfp-style: a tile's z (binary32), coded block by block once every wave has written it
   constexpr int ZP = kD + 4;
   __shared__ __attribute__((aligned(16))) float ztile[ZFP ? 2 : 1][ZFP ? kTok * ZP : 4];
+  __shared__ std::conditional_t<ZFP, ZfpTables, char> ztab;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n = lane & 31, hc = lane >> 5;
@@ -225,6 +226,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
     ring_copy();
     return;
   }
+  if constexpr (ZFP) zfp_tables_init(ztab);  // read after the prologue's barrier
 
   // K range of this wave's rows: the group of channels 32w.. (whole head for g = 128)
   const int kbase = a.g >= 32 ? (32 * w / a.g) * a.g : 32 * w;
@@ -309,8 +311,8 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
     if (si < (kTok / TB) * NBK && (si / NBK) * TB < nlive) a.side[crow0 / TB * NBK + si] = sstage[P][si];
   };
   // zfp-style: thread u * 32 + cb codes block (tokens 4u .. 4u+3, channels 4cb .. 4cb+3) of the
-  // staged tile; a tile's 256 blocks are one contiguous run of the cache
-  auto zflush = [&](int tile, auto parity) {
+  // staged tile; a tile's 256 blocks are one contiguous run of the cache (tab: the coder's tables)
+  auto zflush = [&](int tile, auto parity, const auto& tab) {
     constexpr int P = decltype(parity)::value;
     const int tid = int(threadIdx.x), u = tid >> 5, cb = tid & 31;
     if (4 * u >= a.T - tile * kTok) return;  // token counts are multiples of 4
@@ -321,11 +323,9 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
       v[4 * j] = q.x; v[4 * j + 1] = q.y; v[4 * j + 2] = q.z; v[4 * j + 3] = q.w;
     }
     uint32_t wd[4];
-    flags |= zfp_encode_block(v, BITS, wd);
+    flags |= zfp_encode_block<BITS>(v, tab, wd);
     const size_t blk = (cslice * size_t(a.T_cap / 4) + (a.t0 + tile * kTok) / 4) * (kD / 4) + tid;
-    uint16_t* dst = reinterpret_cast<uint16_t*>(a.codes + blk * (2 * BITS));
-#pragma unroll
-    for (int r = 0; r < BITS; ++r) dst[r] = uint16_t(wd[r >> 1] >> (16 * (r & 1)));
+    zfp_store<BITS>(a.codes + blk * (2 * BITS), wd);
   };
   // one pipeline step; P = parity of (tile - tb) selects the accumulator, LDS buffer, register
   // stage and exchange slot at compile time
@@ -367,7 +367,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
     if constexpr (QUANT) {
       if (tile > tb) flush(tile - 1, std::integral_constant<int, P ^ 1>());
     } else if constexpr (ZFP) {
-      if (tile > tb) zflush(tile - 1, std::integral_constant<int, P ^ 1>());
+      if (tile > tb) zflush(tile - 1, std::integral_constant<int, P ^ 1>(), ztab);
     }
     // 5. next tile on the matrix core (past the range it reads a stale buffer and is unused),
     //    this tile's epilogue on the VALU; no branch until the stores
@@ -544,8 +544,8 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(63));
     __builtin_amdgcn_s_barrier();
     if constexpr (ZFP) {
-      if ((te - tb) & 1) zflush(te - 1, std::integral_constant<int, 0>());
-      else zflush(te - 1, std::integral_constant<int, 1>());
+      if ((te - tb) & 1) zflush(te - 1, std::integral_constant<int, 0>(), ztab);
+      else zflush(te - 1, std::integral_constant<int, 1>(), ztab);
     } else {
       if ((te - tb) & 1) flush(te - 1, std::integral_constant<int, 0>());
       else flush(te - 1, std::integral_constant<int, 1>());
@@ -1393,6 +1393,7 @@ __global__ __launch_bounds__(kThreads, 2) void dec_zfp(MfmaArgs a) {
   constexpr int ZP = kD + 4;
   constexpr int YB = OUT_BF16 ? 2 : 4;
   __shared__ __attribute__((aligned(16))) float ztile[kTok * ZP];
+  __shared__ ZfpTables ztab;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n = lane & 31, hc = lane >> 5;
@@ -1414,16 +1415,16 @@ __global__ __launch_bounds__(kThreads, 2) void dec_zfp(MfmaArgs a) {
   load_a<2, KS>(A, a, l, h, chA, kbase, hc);  // rows chA of the G^T planes
 
   const int tid = int(threadIdx.x), u = tid >> 5, cb = tid & 31;
+  zfp_tables_init(ztab);
+  __syncthreads();
   for (int t = tb; t < te; ++t) {
     // 1. blocks -> zhat tile (the view's token count and offset are multiples of 4)
     if (4 * u < a.T - t * kTok) {
       const size_t blk = (cslice * size_t(a.T_cap / 4) + (a.t0 + t * kTok) / 4 + u) * (kD / 4) + cb;
-      const uint16_t* src = reinterpret_cast<const uint16_t*>(a.codes + blk * (2 * RATE));
-      uint32_t wd[4] = {0u, 0u, 0u, 0u};
-#pragma unroll
-      for (int r = 0; r < RATE; ++r) wd[r >> 1] |= uint32_t(src[r]) << (16 * (r & 1));
+      uint32_t wd[4];
+      zfp_load<RATE>(a.codes + blk * (2 * RATE), wd);
       float v[16];
-      zfp_decode_block(wd, RATE, v);
+      zfp_decode_block<RATE>(wd, ztab, v);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         *(float4*)(&ztile[(4 * u + j) * ZP + 4 * cb]) = make_float4(v[4 * j], v[4 * j + 1], v[4 * j + 2], v[4 * j + 3]);
