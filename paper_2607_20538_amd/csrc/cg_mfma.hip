@@ -1383,16 +1383,18 @@ __global__ __launch_bounds__(kThreads, OUT_BF16 ? 3 : 2) void dec_keys(MfmaArgs 
 // decode, zfp-style blocks (4 tokens x 4 channels of zhat, 16 RATE bits each)
 // ------------------------------------------------------------------------------------------
 // A workgroup owns a range of 32-token tiles of one slice.  Per tile, thread u * 32 + cb decodes
-// block (tokens 4u .. 4u+3, channels 4cb .. 4cb+3) into a binary32 LDS tile; after a barrier
-// wave w computes output channels 32w .. 32w+31 of the 32 tokens on the matrix cores: lane
-// (n, hc) splits its 8 channels of zhat per K-step into three bf16 planes by truncation (each
-// residual exact in binary32, so the planes sum to zhat) and the five plane products that
-// matter against the two G^T planes accumulate in binary32 (as the KIVI key decoder does).
+// block (tokens 4u .. 4u+3, channels 4cb .. 4cb+3) and splits each zhat into three bf16 planes
+// by truncation (each residual exact in binary32, so the planes sum to zhat), written to an LDS
+// tile per plane ([token][channel], 16-byte granules XOR-swizzled by token as in the encoder's
+// ring); after a barrier wave w computes output channels 32w .. 32w+31 of the 32 tokens on the
+// matrix cores, reading its B fragments of the three planes straight from LDS: the five plane
+// products that matter against the two G^T planes accumulate in binary32 (as the KIVI key
+// decoder does).  Splitting in the decoding thread does it once per value instead of once per
+// wave.
 template <int KS, int RATE, bool OUT_BF16>
 __global__ __launch_bounds__(kThreads, 2) void dec_zfp(MfmaArgs a) {
-  constexpr int ZP = kD + 4;
   constexpr int YB = OUT_BF16 ? 2 : 4;
-  __shared__ __attribute__((aligned(16))) float ztile[kTok * ZP];
+  __shared__ __attribute__((aligned(16))) uint8_t zpl[3][kTok * kRowBytes];
   __shared__ ZfpTables ztab;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -1413,12 +1415,15 @@ __global__ __launch_bounds__(kThreads, 2) void dec_zfp(MfmaArgs a) {
   const int chA = 32 * w + 16 * ((n >> 2) & 1) + 4 * (n >> 3) + (n & 3);
   bf16x8_t A[2][KS];
   load_a<2, KS>(A, a, l, h, chA, kbase, hc);  // rows chA of the G^T planes
+  int boff[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) boff[kk] = n * kRowBytes + 16 * swz(n, (kbase >> 3) + 2 * kk + hc);
 
   const int tid = int(threadIdx.x), u = tid >> 5, cb = tid & 31;
   zfp_tables_init(ztab);
   __syncthreads();
   for (int t = tb; t < te; ++t) {
-    // 1. blocks -> zhat tile (the view's token count and offset are multiples of 4)
+    // 1. blocks -> zhat planes (the view's token count and offset are multiples of 4)
     if (4 * u < a.T - t * kTok) {
       const size_t blk = (cslice * size_t(a.T_cap / 4) + (a.t0 + t * kTok) / 4 + u) * (kD / 4) + cb;
       uint32_t wd[4];
@@ -1426,33 +1431,34 @@ __global__ __launch_bounds__(kThreads, 2) void dec_zfp(MfmaArgs a) {
       float v[16];
       zfp_decode_block<RATE>(wd, ztab, v);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        *(float4*)(&ztile[(4 * u + j) * ZP + 4 * cb]) = make_float4(v[4 * j], v[4 * j + 1], v[4 * j + 2], v[4 * j + 3]);
+      for (int j = 0; j < 4; ++j) {
+        uint32_t pw[3][2];
+#pragma unroll
+        for (int e2 = 0; e2 < 2; ++e2) {
+          uint32_t x0 = __float_as_uint(v[4 * j + 2 * e2]), x1 = __float_as_uint(v[4 * j + 2 * e2 + 1]);
+#pragma unroll
+          for (int p = 0; p < 3; ++p) {
+            pw[p][e2] = __builtin_amdgcn_perm(x1, x0, 0x07060302u);
+            if (p < 2) {
+              x0 = __float_as_uint(__uint_as_float(x0) - __uint_as_float(x0 & 0xffff0000u));
+              x1 = __float_as_uint(__uint_as_float(x1) - __uint_as_float(x1 & 0xffff0000u));
+            }
+          }
+        }
+        const int row = 4 * u + j;
+        const int off = row * kRowBytes + 16 * swz(row, cb >> 1) + 8 * (cb & 1);
+#pragma unroll
+        for (int p = 0; p < 3; ++p) *(uint2*)(zpl[p] + off) = make_uint2(pw[p][0], pw[p][1]);
+      }
     }
     __syncthreads();
     // 2. xhat = G^T zhat for the lane's token n and channels 32w + 16hc + [0, 16)
     f32x16_t acc = {};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
-      const float* zr = &ztile[n * ZP + kbase + 16 * kk + 8 * hc];
-      const float4 z0 = *(const float4*)zr, z1 = *(const float4*)(zr + 4);
-      const float zh[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
-      uint32_t bp[3][4];
-#pragma unroll
-      for (int e2 = 0; e2 < 4; ++e2) {
-        uint32_t x0 = __float_as_uint(zh[2 * e2]), x1 = __float_as_uint(zh[2 * e2 + 1]);
-#pragma unroll
-        for (int p = 0; p < 3; ++p) {
-          bp[p][e2] = __builtin_amdgcn_perm(x1, x0, 0x07060302u);
-          if (p < 2) {
-            x0 = __float_as_uint(__uint_as_float(x0) - __uint_as_float(x0 & 0xffff0000u));
-            x1 = __float_as_uint(__uint_as_float(x1) - __uint_as_float(x1 & 0xffff0000u));
-          }
-        }
-      }
       bf16x8_t B[3];
 #pragma unroll
-      for (int p = 0; p < 3; ++p) B[p] = as_bf16x8(u32x4_t{bp[p][0], bp[p][1], bp[p][2], bp[p][3]});
+      for (int p = 0; p < 3; ++p) B[p] = as_bf16x8(*(const u32x4_t*)(zpl[p] + boff[kk]));
       // plane products, smallest first: (1,1) (0,2) (1,0) (0,1) (0,0)
       acc = mfma(A[1][kk], B[1], acc);
       acc = mfma(A[0][kk], B[2], acc);
@@ -1477,7 +1483,7 @@ __global__ __launch_bounds__(kThreads, 2) void dec_zfp(MfmaArgs a) {
         for (int q = 0; q < 4; ++q) *(float4*)(yr + 16 * q) = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
       }
     }
-    __syncthreads();  // the tile is read before the next one is decoded into it
+    __syncthreads();  // the planes are read before the next tile is decoded into them
   }
 }
 
