@@ -311,19 +311,23 @@ __global__ __launch_bounds__(kThreads, NP == 2 && MODE != kModeZfp ? 3 : 2) void
     if (si < (kTok / TB) * NBK && (si / NBK) * TB < nlive) a.side[crow0 / TB * NBK + si] = sstage[P][si];
   };
   // zfp-style: thread u * 32 + cb codes block (tokens 4u .. 4u+3, channels 4cb .. 4cb+3) of the
-  // staged tile; a tile's 256 blocks are one contiguous run of the cache (tab: the coder's tables)
-  auto zflush = [&](int tile, auto parity, const auto& tab) {
+  // staged tile: zload reads it from LDS, zfp_prepare (no branch) runs interleaved with the next
+  // tile's matrix-core chain, zcode codes the planes and stores the block; a tile's 256 blocks are
+  // one contiguous run of the cache (tab: the coder's tables)
+  auto zload = [&](auto parity, float (&v)[16]) {
     constexpr int P = decltype(parity)::value;
     const int tid = int(threadIdx.x), u = tid >> 5, cb = tid & 31;
-    if (4 * u >= a.T - tile * kTok) return;  // token counts are multiples of 4
-    float v[16];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const float4 q = *(const float4*)(&ztile[P][(4 * u + j) * ZP + 4 * cb]);
       v[4 * j] = q.x; v[4 * j + 1] = q.y; v[4 * j + 2] = q.z; v[4 * j + 3] = q.w;
     }
+  };
+  auto zcode = [&](int tile, const ZfpPrep& zp, const auto& tab) {
+    const int tid = int(threadIdx.x), u = tid >> 5;
+    if (4 * u >= a.T - tile * kTok) return;  // token counts are multiples of 4
     uint32_t wd[4];
-    flags |= zfp_encode_block<BITS>(v, tab, wd);
+    flags |= zfp_encode_planes<BITS>(zp, tab, wd);
     const size_t blk = (cslice * size_t(a.T_cap / 4) + (a.t0 + tile * kTok) / 4) * (kD / 4) + tid;
     zfp_store<BITS>(a.codes + blk * (2 * BITS), wd);
   };
@@ -366,21 +370,25 @@ __global__ __launch_bounds__(kThreads, NP == 2 && MODE != kModeZfp ? 3 : 2) void
     bfrags(tile + 1);
     if constexpr (QUANT) {
       if (tile > tb) flush(tile - 1, std::integral_constant<int, P ^ 1>());
-    } else if constexpr (ZFP) {
-      if (tile > tb) zflush(tile - 1, std::integral_constant<int, P ^ 1>(), ztab);
     }
+    float zv[ZFP ? 16 : 1];  // zfp-style: the thread's block of tile - 1 (unused at tile tb)
+    if constexpr (ZFP) zload(std::integral_constant<int, P ^ 1>(), zv);
     // 5. next tile on the matrix core (past the range it reads a stale buffer and is unused),
     //    this tile's epilogue on the VALU; no branch until the stores
     acc[P ^ 1] = mfma_chain<NP, KS, KEYS>(A, Bf);
 
     if constexpr (ZFP) {
+      // tile - 1's block: range, transform and top planes alongside the chain, then its planes;
       // the lane's 16 channels of token n into the staged tile (coded after the next barrier)
       (void)live;
+      ZfpPrep zp;
+      zfp_prepare(zv, zp);
 #pragma unroll
       for (int i = 0; i < KS * NP; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
       }
+      if (tile > tb) zcode(tile - 1, zp, ztab);
       float* zr = &ztile[P][n * ZP + 32 * w + 16 * hc];
 #pragma unroll
       for (int q = 0; q < 4; ++q) *(float4*)(zr + 4 * q) = make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
@@ -544,8 +552,12 @@ __global__ __launch_bounds__(kThreads, NP == 2 && MODE != kModeZfp ? 3 : 2) void
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(63));
     __builtin_amdgcn_s_barrier();
     if constexpr (ZFP) {
-      if ((te - tb) & 1) zflush(te - 1, std::integral_constant<int, 0>(), ztab);
-      else zflush(te - 1, std::integral_constant<int, 1>(), ztab);
+      float zv[16];
+      if ((te - tb) & 1) zload(std::integral_constant<int, 0>(), zv);
+      else zload(std::integral_constant<int, 1>(), zv);
+      ZfpPrep zp;
+      zfp_prepare(zv, zp);
+      zcode(te - 1, zp, ztab);
     } else {
       if ((te - tb) & 1) flush(te - 1, std::integral_constant<int, 0>());
       else flush(te - 1, std::integral_constant<int, 1>());

@@ -187,42 +187,61 @@ struct ZBits {
   }
 };
 
-// v[4 j + i]: channel i of token j.  w: the block's 16 RATE bits, LSB-first (words past the
-// block are 0).  Returns flags.
-template <int RATE>
-__host__ __device__ __forceinline__ int zfp_encode_block(const float (&v)[16], const ZfpTables& tb, uint32_t (&w)[4]) {
-  constexpr int CAP = ZBits<RATE>::kCap;
-  ZBits<RATE> st;
+// First half of the encoder, without a branch (so that it can be interleaved with other work):
+// block range, exponent, 30-bit fixed point, transform, negabinary, and the top eight planes.
+// v[4 j + i]: channel i of token j.
+struct ZfpPrep {
+  uint32_t u[16];   // negabinary coefficients in sequency order
+  uint32_t xp[4];   // planes top-7 .. top as plane_window holds them
+  int e, top;       // block exponent, highest plane with a set bit
+  bool coded;       // finite and not all zero
+  bool finite;
+};
+
+__host__ __device__ __forceinline__ void zfp_prepare(const float (&v)[16], ZfpPrep& z) {
   // NaN-propagating maximum of |v|: one test flags a non-finite block (coded as an empty block)
   float amax = fabsf(v[0]);
 #pragma unroll
   for (int k = 1; k < 16; ++k) amax = __builtin_elementwise_maximum(amax, fabsf(v[k]));
-  const bool finite = amax <= 3.40282347e38f;
-  if (finite && amax != 0.0f) {
-    int e;
-    frexpf(amax, &e);
-    e = e < -126 ? -126 : e;
-    int32_t q[16];
+  z.finite = amax <= 3.40282347e38f;
+  z.coded = z.finite && amax != 0.0f;
+  int e;
+  frexpf(amax, &e);
+  e = e < -126 ? -126 : e;
+  z.e = e;
+  int32_t q[16];
+  // exact scaling and truncation (|q| < 2^30 for a coded block; the clamp only keeps the
+  // conversion defined for the blocks that are not coded)
 #pragma unroll
-    for (int k = 0; k < 16; ++k) q[k] = int32_t(ldexpf(v[k], 30 - e));  // exact scaling, truncation
+  for (int k = 0; k < 16; ++k) q[k] = int32_t(fminf(fmaxf(ldexpf(v[k], 30 - e), -2147483648.0f), 2147483520.0f));
 #pragma unroll
-    for (int j = 0; j < 4; ++j) zfp_fwd4(q[4 * j], q[4 * j + 1], q[4 * j + 2], q[4 * j + 3]);
+  for (int j = 0; j < 4; ++j) zfp_fwd4(q[4 * j], q[4 * j + 1], q[4 * j + 2], q[4 * j + 3]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) zfp_fwd4(q[i], q[4 + i], q[8 + i], q[12 + i]);
-    uint32_t u[16], any = 0u;
+  for (int i = 0; i < 4; ++i) zfp_fwd4(q[i], q[4 + i], q[8 + i], q[12 + i]);
+  uint32_t any = 0u;
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      u[k] = (uint32_t(q[kZfpOrder[k]]) + 0xAAAAAAAAu) ^ 0xAAAAAAAAu;
-      any |= u[k];
-    }
-    st.put(1u | (uint32_t(e + 127) << 1), 0);
+  for (int k = 0; k < 16; ++k) {
+    z.u[k] = (uint32_t(q[kZfpOrder[k]]) + 0xAAAAAAAAu) ^ 0xAAAAAAAAu;
+    any |= z.u[k];
+  }
+  z.top = 31 - __builtin_clz(any | 1u);  // a coded block has |q| >= 2^29 somewhere, so any != 0
+  plane_window(z.u, z.top - 7, z.xp);
+}
+
+// Second half: the bit planes.  w: the block's 16 RATE bits, LSB-first (words past the block
+// are 0).  Returns flags.
+template <int RATE>
+__host__ __device__ __forceinline__ int zfp_encode_planes(const ZfpPrep& z, const ZfpTables& tb, uint32_t (&w)[4]) {
+  constexpr int CAP = ZBits<RATE>::kCap;
+  ZBits<RATE> st;
+  if (z.coded) {
+    st.put(1u | (uint32_t(z.e + 127) << 1), 0);
     // planes above the highest set bit: one 0 test bit each
-    const int top = 31 - __builtin_clz(any);  // any != 0: |q| >= 2^29 somewhere
-    int o = 9 + 31 - top, n = 0;
+    int o = 9 + 31 - z.top, n = 0;
     uint32_t X = 0u;
-    for (int P0 = top; P0 >= 0 && o < CAP; P0 -= 8) {
-      uint32_t xp[4];
-      plane_window(u, P0 - 7, xp);
+    uint32_t xp[4] = {z.xp[0], z.xp[1], z.xp[2], z.xp[3]};
+    for (int P0 = z.top; P0 >= 0 && o < CAP; P0 -= 8) {
+      if (P0 != z.top) plane_window(z.u, P0 - 7, xp);
 #pragma unroll
       for (int p = 7; p >= 0; --p) {
         if (P0 - 7 + p >= 0 && o < CAP) {
@@ -253,7 +272,14 @@ __host__ __device__ __forceinline__ int zfp_encode_block(const float (&v)[16], c
   w[1] = uint32_t(st.w0 >> 32);
   w[2] = uint32_t(st.w1);
   w[3] = uint32_t(st.w1 >> 32);
-  return finite ? 0 : CG_FLAG_NONFINITE;
+  return z.finite ? 0 : CG_FLAG_NONFINITE;
+}
+
+template <int RATE>
+__host__ __device__ __forceinline__ int zfp_encode_block(const float (&v)[16], const ZfpTables& tb, uint32_t (&w)[4]) {
+  ZfpPrep z;
+  zfp_prepare(v, z);
+  return zfp_encode_planes<RATE>(z, tb, w);
 }
 
 template <int RATE>
