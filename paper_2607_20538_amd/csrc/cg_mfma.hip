@@ -157,6 +157,28 @@ __device__ __forceinline__ float row16_max(float v) {
 }
 
 
+// 4 x 4 transpose of four-value groups across a DPP quad: lane r (= lane % 4) holds groups
+// M[r][c] = z[4c .. 4c+3]; afterwards v[4j .. 4j+3] = M[j][r] (lane j's group r).  Two
+// exchanges: slot c takes the partner's slot c ^ d from lane r ^ d where bit d of c ^ r is set
+// (d = 1, then 2), which moves M[r ^ (c ^ r)][c ^ (c ^ r)] = M[c][r] into slot c.
+__device__ __forceinline__ void quad_transpose(const float (&z)[16], int r, float (&v)[16]) {
+  float t[16];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float o = dpp_mov<0xB1>(z[4 * (c ^ 1) + i]);  // quad_perm [1,0,3,2]
+      t[4 * c + i] = ((c ^ r) & 1) ? o : z[4 * c + i];
+    }
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float o = dpp_mov<0x4E>(t[4 * (c ^ 2) + i]);  // quad_perm [2,3,0,1]
+      v[4 * c + i] = ((c ^ r) & 2) ? o : t[4 * c + i];
+    }
+}
+
 // encoder modes
 constexpr int kModeBU = 0;     // block-uniform (or KIVI values: n = value channel group)
 constexpr int kModePass = 1;   // error-free backend: binary32 z
@@ -175,7 +197,7 @@ constexpr int kModeZfp = 3;    // zfp-style fixed-rate blocks of 4 tokens x 4 ch
 // contiguous run of 32 RB bytes in the cache and its side words one run of 32 NBK words, so
 // the staged copy leaves with whole-line stores instead of 32 scattered row pieces.
 template <int NP, int KS, int BITS, int NB, int MODE, int TB = 1>
-__global__ __launch_bounds__(kThreads, NP == 2 && MODE != kModeZfp ? 3 : 2) void enc_mfma(MfmaArgs a) {
+__global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void enc_mfma(MfmaArgs a) {
   constexpr bool PASS = MODE == kModePass, KEYS = MODE == kModeKeys, ZFP = MODE == kModeZfp;
   constexpr bool QUANT = !PASS && !ZFP;  // block ranges, staged codes and side words
   // token-channel tiles: one range per TB tokens x NB channels (NB spans whole waves)
@@ -183,15 +205,19 @@ __global__ __launch_bounds__(kThreads, NP == 2 && MODE != kModeZfp ? 3 : 2) void
   static_assert(!TILE || (TB == 16 && MODE == kModeBU && (NB == 64 || NB == 128)), "tile shape");
   constexpr int RB = kD * BITS / 8;   // packed code bytes per token row
   constexpr int NBK = kD / NB;        // side words per token row (per tile row of tiles)
-  __shared__ __attribute__((aligned(16))) uint8_t xtile[kStages][kTok * kRowBytes];
+  // ring depth: the zfp-style coder is bound by its VALU work, so it keeps one tile fewer in
+  // flight and gives the LDS to the block transpose below (three workgroups per CU either way)
+  constexpr int ST = ZFP ? kStages - 1 : kStages;
+  __shared__ __attribute__((aligned(16))) uint8_t xtile[ST][kTok * kRowBytes];
   __shared__ float2 red[2][4][kTok];  // per-wave (min, max) of each token, for 64-channel blocks
   // a tile's packed rows and side words, staged so that they leave as contiguous stores
   __shared__ __attribute__((aligned(16))) uint8_t cstage[2][QUANT ? kTok * RB : 16];
   __shared__ uint32_t sstage[2][QUANT ? kTok * NBK : 1];  // KIVI keys: NB = 32, one word per channel
-  // zfp-style: a tile's z (binary32), coded block by block once every wave has written it
-  constexpr int ZP = kD + 4;
-  __shared__ __attribute__((aligned(16))) float ztile[ZFP ? 2 : 1][ZFP ? kTok * ZP : 4];
   __shared__ std::conditional_t<ZFP, ZfpTables, char> ztab;
+  // zfp-style: each wave's 32 tokens x 32 channels of z, written by token rows and read back as
+  // 4 x 4 blocks by the same wave (LDS operations of a wave complete in order, so no barrier)
+  constexpr int QP = 36;  // row pitch in floats (16-byte rows, rows 4 banks apart)
+  __shared__ __attribute__((aligned(16))) float zq[ZFP ? 4 : 1][ZFP ? kTok * QP : 4];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n = lane & 31, hc = lane >> 5;
@@ -248,7 +274,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 && MODE != kModeZfp ? 3 : 2) void
     dsrc[q] = xs + drow[q] * tstride + 16 * swz(drow[q], lane & 15);
   }
   auto issue = [&](int tile) {
-    uint8_t* dst = xtile[(tile - tb) % kStages] + 8 * wu * kRowBytes;
+    uint8_t* dst = xtile[(tile - tb) % ST] + 8 * wu * kRowBytes;
     if ((tile + 1) * kTok <= a.T) {
       const int64_t off = int64_t(tile) * kTok * tstride;
 #pragma unroll
@@ -284,14 +310,14 @@ __global__ __launch_bounds__(kThreads, NP == 2 && MODE != kModeZfp ? 3 : 2) void
   for (int kk = 0; kk < KS; ++kk) boff[kk] = n * kRowBytes + 16 * swz(n, (kbase >> 3) + 2 * kk + hc);
   bf16x8_t Bf[KS];
   auto bfrags = [&](int tile) {
-    const uint8_t* src = xtile[(tile - tb) % kStages];
+    const uint8_t* src = xtile[(tile - tb) % ST];
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) Bf[kk] = as_bf16x8(*(const u32x4_t*)(src + boff[kk]));
   };
 
-  // prologue: tiles tb .. tb+kStages-2 in flight, tile tb on the matrix core
-  for (int t = tb; t < min(te, tb + kStages - 1); ++t) issue(t);
-  wait_tile(tb, min(te - 1, tb + kStages - 2));
+  // prologue: tiles tb .. tb+ST-2 in flight, tile tb on the matrix core
+  for (int t = tb; t < min(te, tb + ST - 1); ++t) issue(t);
+  wait_tile(tb, min(te - 1, tb + ST - 2));
   __builtin_amdgcn_s_barrier();
   bfrags(tb);
   f32x16_t acc[2];
@@ -309,27 +335,6 @@ __global__ __launch_bounds__(kThreads, NP == 2 && MODE != kModeZfp ? 3 : 2) void
     // side words: one per (row, block), or per (tile of TB rows, block); t0 % TB == 0
     const int si = kThreads - 1 - tid;
     if (si < (kTok / TB) * NBK && (si / NBK) * TB < nlive) a.side[crow0 / TB * NBK + si] = sstage[P][si];
-  };
-  // zfp-style: thread u * 32 + cb codes block (tokens 4u .. 4u+3, channels 4cb .. 4cb+3) of the
-  // staged tile: zload reads it from LDS, zfp_prepare (no branch) runs interleaved with the next
-  // tile's matrix-core chain, zcode codes the planes and stores the block; a tile's 256 blocks are
-  // one contiguous run of the cache (tab: the coder's tables)
-  auto zload = [&](auto parity, float (&v)[16]) {
-    constexpr int P = decltype(parity)::value;
-    const int tid = int(threadIdx.x), u = tid >> 5, cb = tid & 31;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float4 q = *(const float4*)(&ztile[P][(4 * u + j) * ZP + 4 * cb]);
-      v[4 * j] = q.x; v[4 * j + 1] = q.y; v[4 * j + 2] = q.z; v[4 * j + 3] = q.w;
-    }
-  };
-  auto zcode = [&](int tile, const ZfpPrep& zp, const auto& tab) {
-    const int tid = int(threadIdx.x), u = tid >> 5;
-    if (4 * u >= a.T - tile * kTok) return;  // token counts are multiples of 4
-    uint32_t wd[4];
-    flags |= zfp_encode_planes<BITS>(zp, tab, wd);
-    const size_t blk = (cslice * size_t(a.T_cap / 4) + (a.t0 + tile * kTok) / 4) * (kD / 4) + tid;
-    zfp_store<BITS>(a.codes + blk * (2 * BITS), wd);
   };
   // one pipeline step; P = parity of (tile - tb) selects the accumulator, LDS buffer, register
   // stage and exchange slot at compile time
@@ -362,36 +367,50 @@ __global__ __launch_bounds__(kThreads, NP == 2 && MODE != kModeZfp ? 3 : 2) void
       }
     }
     // 2. tile+1 landed in every wave (and every wave is done with tile-1's buffer), refill
-    //    that buffer with tile+kStages-1, read tile+1's B fragments
-    if (tile + 1 < te) wait_tile(tile + 1, min(te - 1, tile + kStages - 2));
+    //    that buffer with tile+ST-1, read tile+1's B fragments
+    if (tile + 1 < te) wait_tile(tile + 1, min(te - 1, tile + ST - 2));
     else __builtin_amdgcn_s_waitcnt(waitcnt_imm(63));  // LDS writes only
     __builtin_amdgcn_s_barrier();
-    if (tile + kStages - 1 < te) issue(tile + kStages - 1);
+    if (tile + ST - 1 < te) issue(tile + ST - 1);
     bfrags(tile + 1);
     if constexpr (QUANT) {
       if (tile > tb) flush(tile - 1, std::integral_constant<int, P ^ 1>());
     }
-    float zv[ZFP ? 16 : 1];  // zfp-style: the thread's block of tile - 1 (unused at tile tb)
-    if constexpr (ZFP) zload(std::integral_constant<int, P ^ 1>(), zv);
     // 5. next tile on the matrix core (past the range it reads a stale buffer and is unused),
     //    this tile's epilogue on the VALU; no branch until the stores
     acc[P ^ 1] = mfma_chain<NP, KS, KEYS>(A, Bf);
 
     if constexpr (ZFP) {
-      // tile - 1's block: range, transform and top planes alongside the chain, then its planes;
-      // the lane's 16 channels of token n into the staged tile (coded after the next barrier)
+      // the lane's 4 x 4 block of this tile, through the wave's LDS region: tokens
+      // 4(n/4) .. +3 x channels 32w + 16hc + 4(n%4) .. +3; range, transform and top planes
+      // alongside the chain, then the planes (blocks past the view, at token counts that are
+      // multiples of 4, are skipped)
       (void)live;
+      float* zw = zq[w];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *(float4*)(zw + n * QP + 16 * hc + 4 * q) = make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
+      __builtin_amdgcn_wave_barrier();  // keep the reads after the writes
+      float v[16];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float4 t = *(const float4*)(zw + (4 * (n >> 2) + j) * QP + 16 * hc + 4 * (n & 3));
+        v[4 * j] = t.x; v[4 * j + 1] = t.y; v[4 * j + 2] = t.z; v[4 * j + 3] = t.w;
+      }
       ZfpPrep zp;
-      zfp_prepare(zv, zp);
+      zfp_prepare(v, zp);
 #pragma unroll
       for (int i = 0; i < KS * NP; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 20, 0);
       }
-      if (tile > tb) zcode(tile - 1, zp, ztab);
-      float* zr = &ztile[P][n * ZP + 32 * w + 16 * hc];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) *(float4*)(zr + 4 * q) = make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
+      if (tile * kTok + 4 * (n >> 2) < a.T) {
+        uint32_t wd[4];
+        flags |= zfp_encode_planes<BITS>(zp, ztab, wd);
+        const size_t blk = (cslice * size_t(a.T_cap / 4) + (a.t0 + tile * kTok) / 4 + (n >> 2)) * (kD / 4) +
+                           8 * w + 4 * hc + (n & 3);
+        zfp_store<BITS>(a.codes + blk * (2 * BITS), wd);
+      }
     } else if constexpr (PASS) {
 #pragma unroll
       for (int i = 0; i < KS * NP; ++i) {
@@ -547,21 +566,12 @@ __global__ __launch_bounds__(kThreads, NP == 2 && MODE != kModeZfp ? 3 : 2) void
     step(tile, std::integral_constant<int, 0>());
     if (tile + 1 < te) step(tile + 1, std::integral_constant<int, 1>());
   }
-  if constexpr (!PASS) {
+  if constexpr (QUANT) {
     // the last tile's staging: every wave's LDS writes done, then the final contiguous stores
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(63));
     __builtin_amdgcn_s_barrier();
-    if constexpr (ZFP) {
-      float zv[16];
-      if ((te - tb) & 1) zload(std::integral_constant<int, 0>(), zv);
-      else zload(std::integral_constant<int, 1>(), zv);
-      ZfpPrep zp;
-      zfp_prepare(zv, zp);
-      zcode(te - 1, zp, ztab);
-    } else {
-      if ((te - tb) & 1) flush(te - 1, std::integral_constant<int, 0>());
-      else flush(te - 1, std::integral_constant<int, 1>());
-    }
+    if ((te - tb) & 1) flush(te - 1, std::integral_constant<int, 0>());
+    else flush(te - 1, std::integral_constant<int, 1>());
   }
   ring_copy();
   if (flags && a.err) atomicOr(a.err, flags);
