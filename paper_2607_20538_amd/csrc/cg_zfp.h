@@ -282,23 +282,25 @@ __host__ __device__ __forceinline__ int zfp_encode_block(const float (&v)[16], c
   return zfp_encode_planes<RATE>(z, tb, w);
 }
 
+// First half of the decoder: the bit planes of a block's 16 RATE bits w (LSB-first, words past
+// the block 0) into the negabinary coefficients u (sequency order) and the block exponent e; an
+// empty block gives u = 0.
 template <int RATE>
-__host__ __device__ __forceinline__ void zfp_decode_block(const uint32_t (&w)[4], const ZfpTables& tb, float (&v)[16]) {
+__host__ __device__ __forceinline__ void zfp_decode_planes(const uint32_t (&w)[4], const ZfpTables& tb, uint32_t (&u)[16],
+                                                           int& e) {
   constexpr int CAP = ZBits<RATE>::kCap;
   ZBits<RATE> st;
   st.w0 = uint64_t(w[0]) | (uint64_t(w[1]) << 32);
   st.w1 = uint64_t(w[2]) | (uint64_t(w[3]) << 32);
   st.clip();
 #pragma unroll
-  for (int k = 0; k < 16; ++k) v[k] = 0.0f;
+  for (int k = 0; k < 16; ++k) u[k] = 0u;
+  e = 0;
   if (!(st.w0 & 1u)) return;
-  const int e = int((st.w0 >> 1) & 0xFFu) - 127;
+  e = int((st.w0 >> 1) & 0xFFu) - 127;
   // leading empty planes: one 0 test bit each
   const uint64_t lead = st.window(9);
   const int z = lead ? __builtin_ctzll(lead) : 64;
-  uint32_t u[16];
-#pragma unroll
-  for (int k = 0; k < 16; ++k) u[k] = 0u;
   int o = 9 + z, n = 0;
   for (int P0 = 31 - z; P0 >= 0 && o < CAP; P0 -= 8) {
     uint32_t xp[4] = {0u, 0u, 0u, 0u};
@@ -336,7 +338,7 @@ __host__ __device__ __forceinline__ void zfp_decode_block(const uint32_t (&w)[4]
           const int glen = implied ? 1 + L + __builtin_popcount(yl) : e1 + 2;
           const bool fits = o + n + glen <= CAP;
           const uint32_t yn = implied ? (yl | (fits ? 1u << L : 0u)) : y;
-          const bool t0 = (win >> n) & 1u;
+          const bool t0 = (uint32_t(win) >> n) & 1u;  // n < 16
           x = t0 ? V | (yn << n) : V;
           o += t0 ? n + glen : n + 1;
           n = t0 ? (implied ? 16 : n + dcount) : n;
@@ -346,6 +348,11 @@ __host__ __device__ __forceinline__ void zfp_decode_block(const uint32_t (&w)[4]
     }
     plane_unwindow(xp, P0 - 7, u);
   }
+}
+
+// Second half, without a branch: negabinary to two's complement, inverse transform, scaling.
+// v[4 j + i]: channel i of token j.
+__host__ __device__ __forceinline__ void zfp_decode_finish(const uint32_t (&u)[16], int e, float (&v)[16]) {
   int32_t q[16];
 #pragma unroll
   for (int k = 0; k < 16; ++k) q[kZfpOrder[k]] = int32_t((u[k] ^ 0xAAAAAAAAu) - 0xAAAAAAAAu);
@@ -355,6 +362,14 @@ __host__ __device__ __forceinline__ void zfp_decode_block(const uint32_t (&w)[4]
   for (int j = 0; j < 4; ++j) zfp_inv4(q[4 * j], q[4 * j + 1], q[4 * j + 2], q[4 * j + 3]);
 #pragma unroll
   for (int k = 0; k < 16; ++k) v[k] = ldexpf(float(q[k]), e - 30);
+}
+
+template <int RATE>
+__host__ __device__ __forceinline__ void zfp_decode_block(const uint32_t (&w)[4], const ZfpTables& tb, float (&v)[16]) {
+  uint32_t u[16];
+  int e;
+  zfp_decode_planes<RATE>(w, tb, u, e);
+  zfp_decode_finish(u, e, v);
 }
 
 // a block's 2 RATE bytes to / from the cache (blocks start at multiples of 2 RATE bytes)
