@@ -442,6 +442,110 @@ def spectral_stats(X: np.ndarray, G: np.ndarray, s: int, Tb: int = 16, tau: floa
 
 
 # ------------------------------------------------------------------------------------------
+# gradient of the training objective with respect to the gauge parameters (sections 4.1-4.2)
+# ------------------------------------------------------------------------------------------
+
+def expm64(W: np.ndarray) -> np.ndarray:
+    """exp(W) of a square matrix in binary64 from the power series exp(W) = sum_k W^k / k!:
+    W is halved s times until its 1-norm is at most 1/2, the series of W / 2^s is summed until a
+    term no longer changes the sum, and the sum is squared s times."""
+    W = np.asarray(W, dtype=np.float64)
+    n1 = float(np.abs(W).sum(axis=0).max()) if W.size else 0.0
+    s = 0
+    while n1 > 0.5:
+        n1 *= 0.5
+        s += 1
+    Ws = W / 2.0 ** s
+    term = np.eye(W.shape[0])
+    total = term.copy()
+    for k in range(1, 80):
+        term = term @ Ws / k
+        nxt = total + term
+        if np.array_equal(nxt, total):
+            break
+        total = nxt
+    for _ in range(s):
+        total = total @ total
+    return total
+
+
+def expm_frechet64(M: np.ndarray, E: np.ndarray) -> np.ndarray:
+    """Frechet derivative of the matrix exponential at M in the direction E,
+    L(M, E) = d/dh exp(M + h E) at h = 0: the top-right block of exp([[M, E], [0, M]])."""
+    n = M.shape[0]
+    W = np.zeros((2 * n, 2 * n))
+    W[:n, :n] = M
+    W[:n, n:] = E
+    W[n:, n:] = M
+    return expm64(W)[:n, n:]
+
+
+def gauge_from_params(A: np.ndarray) -> np.ndarray:
+    """G = exp(A - A^T) per block (section 4.1) in binary64: A [..][g][g] -> G [..][g][g]."""
+    A = np.asarray(A, dtype=np.float64)
+    G = np.zeros_like(A)
+    for idx in np.ndindex(*A.shape[:-2]):
+        G[idx] = expm64(A[idx] - A[idx].T)
+    return G
+
+
+def spectral_train_loss(X: np.ndarray, A: np.ndarray, s: int, Tb: int = 16, tau: float = 0.04,
+                        lam_f: float = 1.0, lam_r: float = 0.02, eps: float = 1e-12) -> np.ndarray:
+    """L_train = lam_f L_freq + lam_r L_rate per layer (section 4.2) of X' = G X with
+    G = exp(A - A^T) (section 4.1) taken in binary64 from the generators A [L][2][H][R][g][g]."""
+    stats, _ = spectral_stats(X, gauge_from_params(A), s, Tb, tau, eps)
+    return lam_f * stats[:, 0] + lam_r * stats[:, 1]
+
+
+def spectral_train_grad(X: np.ndarray, A: np.ndarray, s: int, Tb: int = 16, tau: float = 0.04,
+                        lam_f: float = 1.0, lam_r: float = 0.02, eps: float = 1e-12) -> np.ndarray:
+    """dL_train(l) / dA[l][s][h][r] as [L][H][R][g][g] (binary64), by the chain rule through the
+    objective of section 4.2 and the parameterisation of section 4.1, per layer l:
+      1. U = C_Tb Z C_d^T per block with Z = x G^T (the block's rows z_t = G x_t), and per layer
+         D = sum E + eps, L_freq = sum E rho / D, N = the layer's coefficient count;
+      2. dL/dU = lam_f 2 U (rho - L_freq) / D + lam_r sign(U) / (N (tau + |U|));
+      3. dL/dZ = C_Tb^T (dL/dU) C_d (both DCTs orthonormal);
+      4. dL/dG = sum over blocks of (dL/dZ)^T x, restricted to the gauge's diagonal blocks;
+      5. with S = A - A^T and G = exp(S): dL/dS = L(S^T, dL/dG), the adjoint of the Frechet
+         derivative of exp at S (for the trace inner product, <Y, L(S, E)> = <L(S^T, Y), E>);
+      6. dL/dA = dL/dS - (dL/dS)^T."""
+    L_, B, H, T, d = X.shape
+    R, g = A.shape[3], A.shape[-1]
+    Aa = np.asarray(A, dtype=np.float64)
+    G = gauge_from_params(Aa)
+    stats, energy = spectral_stats(X, G, s, Tb, tau, eps)
+    if X.dtype == np.uint16:
+        x = (X.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    else:
+        x = X.astype(np.float64)
+    nblk = T // Tb
+    Ct, Cd = dct2_matrix(Tb), dct2_matrix(d)
+    rho = spectral_radius(Tb, d)
+    grad = np.zeros((L_, H, R, g, g))
+    for l in range(L_):
+        D = float(energy[l].sum()) + eps
+        lf = float(stats[l, 0])
+        count = B * H * nblk * Tb * d
+        for h in range(H):
+            Gd = np.zeros((d, d))
+            for r in range(R):
+                Gd[r * g:(r + 1) * g, r * g:(r + 1) * g] = G[l, s, h, r]
+            dGd = np.zeros((d, d))
+            for b in range(B):
+                for k in range(nblk):
+                    xb = x[l, b, h, k * Tb:(k + 1) * Tb]
+                    U = Ct @ (xb @ Gd.T) @ Cd.T
+                    dU = lam_f * 2.0 * U * (rho - lf) / D + lam_r * np.sign(U) / (count * (tau + np.abs(U)))
+                    dZ = Ct.T @ dU @ Cd
+                    dGd += dZ.T @ xb
+            for r in range(R):
+                S = Aa[l, s, h, r] - Aa[l, s, h, r].T
+                dS = expm_frechet64(S.T, dGd[r * g:(r + 1) * g, r * g:(r + 1) * g])
+                grad[l, h, r] = dS - dS.T
+    return grad
+
+
+# ------------------------------------------------------------------------------------------
 # decode-phase attention over a compressed cache (the consumer of the decoded history)
 # ------------------------------------------------------------------------------------------
 
