@@ -508,7 +508,10 @@ def spectral_train_grad(X: np.ndarray, A: np.ndarray, s: int, Tb: int = 16, tau:
       4. dL/dG = sum over blocks of (dL/dZ)^T x, restricted to the gauge's diagonal blocks;
       5. with S = A - A^T and G = exp(S): dL/dS = L(S^T, dL/dG), the adjoint of the Frechet
          derivative of exp at S (for the trace inner product, <Y, L(S, E)> = <L(S^T, Y), E>);
-      6. dL/dA = dL/dS - (dL/dS)^T."""
+      6. dL/dA = dL/dS - (dL/dS)^T.
+    The -L_freq part of step 2 multiplies the gradient of the total energy sum E, which G and
+    the DCTs leave unchanged, so it contributes nothing for an exactly orthogonal G; it is kept
+    as the literal derivative of the quotient."""
     L_, B, H, T, d = X.shape
     R, g = A.shape[3], A.shape[-1]
     Aa = np.asarray(A, dtype=np.float64)
