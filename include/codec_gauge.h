@@ -257,6 +257,30 @@ size_t spectral_workspace_bytes(cg_gauge_shape shp, int32_t block_t);
 int32_t kv_spectral_stats(int32_t s, const cg_kv_view* X, const void* G_dev, cg_gauge_shape shp, int32_t block_t,
                           float tau, void* workspace, double* stats, double* energy, void* stream);
 
+/* Bytes of the device workspace kv_gauge_grad needs for this shape, B batch rows, T tokens and
+ * token block (0 if any is invalid or unsupported). */
+size_t gauge_grad_workspace_bytes(cg_gauge_shape shp, int32_t B, int32_t T, int32_t block_t);
+
+/* Gradient of the gauge training objective (section 4.2) with respect to the gauge generators
+ * of section 4.1 (G = exp(A - A^T) per (layer, cache type, head, group)), for cache type s:
+ *   L_train(l) = lambda_f L_freq(l) + lambda_r L_rate(l)   (the statistics of kv_spectral_stats
+ *                                                          of X' = G X, per layer l)
+ *   grad[l][h][r][i][j] = d L_train(l) / d A[l][s][h][r][i][j]
+ * X: a view [L][B][H][T][d] with L = shp.L (bf16 or binary32).  A: device binary32
+ * [L][2][H][R][g][g], the generators; G_dev: the gauge buffer gauge_make built from them
+ * (CG_GAUGE_EXPM with params A), which the statistics and the pass over X read.  The sign of a
+ * coefficient that is exactly 0 counts as 0 in the derivative of |U|.  stats: device binary64
+ * [L][4] receiving the statistics as kv_spectral_stats writes them.  grad: device binary64
+ * [L][H][R][g][g] (antisymmetric per block).  workspace: caller-owned device buffer of
+ * gauge_grad_workspace_bytes(shp, X->B, X->T, block_t) bytes, 16-byte aligned, whose contents
+ * the call overwrites (calls sharing one workspace on different streams race).  d a multiple of
+ * 16 and at most 128 (CG_ERR_UNSUPPORTED otherwise); block_t and tau as kv_spectral_stats;
+ * lambda_f, lambda_r finite (the paper uses 1.0 and 0.02).  Errors: CG_ERR_ARG, CG_ERR_SHAPE,
+ * CG_ERR_ALIGN, CG_ERR_UNSUPPORTED, CG_ERR_DEVICE. */
+int32_t kv_gauge_grad(int32_t s, const cg_kv_view* X, const float* A, const void* G_dev, cg_gauge_shape shp,
+                      int32_t block_t, float tau, float lambda_f, float lambda_r, void* workspace, double* stats,
+                      double* grad, void* stream);
+
 /* Bytes of the device workspace kv_attend needs for nl layers, B batch rows, Hq query heads
  * and caches of capacity T_cap (0: no workspace needed, or invalid arguments). */
 size_t attend_workspace_bytes(cg_gauge_shape shp, int32_t nl, int32_t B, int32_t Hq, int32_t T_cap);

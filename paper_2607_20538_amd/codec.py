@@ -24,7 +24,8 @@ PASSTHROUGH, BLOCK_UNIFORM, KIVI, ZFP = 0, 1, 2, 3
 DTYPE_BF16, DTYPE_F32 = 0, 1
 
 EXPORTS = ["cg_status_str", "gauge_device_bytes", "gauge_make", "cache_bytes", "kv_encode", "kv_decode",
-           "kv_append_step", "spectral_workspace_bytes", "kv_spectral_stats", "attend_workspace_bytes", "kv_attend",
+           "kv_append_step", "spectral_workspace_bytes", "kv_spectral_stats", "gauge_grad_workspace_bytes",
+           "kv_gauge_grad", "attend_workspace_bytes", "kv_attend",
            "kv_attend_noalloc",
            "attend_paged_workspace_bytes", "kv_attend_paged", "kv_encode_paged", "kv_append_paged", "cg_selftest",
            "cg_stream_probe"]
@@ -92,6 +93,11 @@ def lib() -> C.CDLL:
         L.spectral_workspace_bytes.restype = C.c_size_t
         L.kv_spectral_stats.argtypes = [i32, C.POINTER(KvView), p, GaugeShape, i32, C.c_float, p, p, p, p]
         L.kv_spectral_stats.restype = i32
+        L.gauge_grad_workspace_bytes.argtypes = [GaugeShape, i32, i32, i32]
+        L.gauge_grad_workspace_bytes.restype = C.c_size_t
+        L.kv_gauge_grad.argtypes = [i32, C.POINTER(KvView), p, p, GaugeShape, i32, C.c_float, C.c_float, C.c_float, p,
+                                    p, p, p]
+        L.kv_gauge_grad.restype = i32
         L.attend_workspace_bytes.argtypes = [GaugeShape, i32, i32, i32, i32]
         L.attend_workspace_bytes.restype = C.c_size_t
         L.kv_attend.argtypes = [i32, i32, C.POINTER(KvView), C.POINTER(CacheStruct), C.POINTER(CacheStruct), p,
@@ -283,6 +289,21 @@ def kv_spectral_stats(s: int, X, G_dev, shp: GaugeShape, block_t: int, tau: floa
     rc = lib().kv_spectral_stats(s, C.byref(v), _ptr(G_dev), shp, block_t, tau, _ptr(workspace), _ptr(stats),
                                  _ptr(energy), _stream(stream))
     _check("kv_spectral_stats", rc)
+
+
+def gauge_grad_workspace_bytes(shp: GaugeShape, B: int, T: int, block_t: int) -> int:
+    return int(lib().gauge_grad_workspace_bytes(shp, B, T, block_t))
+
+
+def kv_gauge_grad(s: int, X, A, G_dev, shp: GaugeShape, block_t: int, tau: float, lambda_f: float, lambda_r: float,
+                  workspace, stats, grad, stream=None):
+    """Gradient of the training objective (section 4.2) with respect to the generators A (device
+    float32 [L][2][H][R][g][g], G = exp(A - A^T)) into the device float64 tensors grad
+    [L][H][R][g][g] and stats [L][4]; workspace: device buffer of gauge_grad_workspace_bytes."""
+    v = view(X)
+    rc = lib().kv_gauge_grad(s, C.byref(v), _ptr(A), _ptr(G_dev), shp, block_t, tau, lambda_f, lambda_r,
+                             _ptr(workspace), _ptr(stats), _ptr(grad), _stream(stream))
+    _check("kv_gauge_grad", rc)
 
 
 def attend_workspace_bytes(shp: GaugeShape, nl: int, B: int, Hq: int, T_cap: int) -> int:

@@ -1,0 +1,396 @@
+// Gradient of the gauge training objective with respect to the gauge generators (sections 4.1
+// and 4.2): G = exp(S), S = A - A^T, per (layer, cache type, head, group), and per layer
+// L_train = lambda_f L_freq + lambda_r L_rate of X' = G X cut into Tb-token blocks, each Tb x d
+// block through the orthonormal 2-D DCT, U = C_Tb Z C_d^T.
+//
+// With M = C_d G (G block-diagonal over the head's groups) a block is U = C_Tb W, W = X M^T.
+//   dL/dU = lambda_f 2 U (rho - L_freq) / D + lambda_r sign(U) / (N (tau + |U|))
+//           (D = sum E + eps, N the layer's coefficient count, L_freq and sum E from the
+//           forward statistics of the same launch);
+//   dL/dW = C_Tb^T dL/dU;   dL/dM = sum over blocks of (dL/dW)^T X;   dL/dG = C_d^T dL/dM,
+//           restricted to the gauge's diagonal blocks;
+//   dL/dS = L(S^T, dL/dG), the adjoint of the Frechet derivative of exp at S, the top-right block
+//           of exp([[S^T, dL/dG], [0, S^T]]);   dL/dA = dL/dS - (dL/dS)^T.
+//
+// Kernels: grad_prep forms M in binary32 per (layer, head) (binary64 sums); grad_data runs the
+// blocks of a range of tokens of one (layer, batch row, head), recomputing W and U on the VALU in
+// binary32 through LDS, and accumulates its part of dL/dM in registers (a (d/16) x (d/16) tile
+// per thread), written as one partial per workgroup; grad_reduce sums the partials in a fixed
+// order (binary64, deterministic); grad_frechet forms dL/dG and the Frechet adjoint per gauge
+// block in binary64 (power series of the scaled block matrix by Horner's rule, then squaring).
+#include <algorithm>
+
+#include "cg_internal.h"
+#include "cg_device.h"
+
+namespace cg {
+
+namespace {
+
+constexpr int kGradThreads = 256;
+constexpr int kFrechetTerms = 16;  // series terms of exp(W / 2^s) with |W / 2^s|_1 <= 1/2
+
+// M = C_d G_{l,s,h} per (l, h), binary64 sums rounded to binary32: [L][H][d][d]
+__global__ __launch_bounds__(256) void grad_prep(int s, GaugeDev G, int H, int d, float* M) {
+  const int lh = blockIdx.y, l = lh / H, h = lh - l * H;
+  const int g = G.g;
+  for (int idx = blockIdx.x * blockDim.x + threadIdx.x; idx < d * d; idx += gridDim.x * blockDim.x) {
+    const int v = idx / d, c = idx - v * d, r = c / g, j = c - r * g;
+    double acc = 0.0;
+    for (int a = 0; a < g; ++a) {
+      const double cv = sqrt((v == 0 ? 1.0 : 2.0) / d) * cospi((2.0 * (r * g + a) + 1.0) * v / (2.0 * d));
+      acc = fma(cv, double(G.f32[((((size_t(l) * 2 + s) * G.H + h) * G.R + r) * g + a) * g + j]), acc);
+    }
+    M[size_t(lh) * d * d + idx] = float(acc);
+  }
+}
+
+struct GradArgs {
+  ViewDev X;
+  const float* M;        // [L][H][d][d]
+  const double* stats;   // [L][4] from the forward statistics
+  float* part;           // [L][H][B * chunks][d][d] partial dL/dM
+  int Tb, nblk, chunks, blocks_per_wg;
+  float inv_tau, tau, lam_f, lam_r;
+  double inv_count;      // 1 / (coefficients per layer)
+};
+
+// One workgroup per (layer, batch row, head, chunk of blocks); TD = d / 16: thread (ty, tx) owns
+// rows v in [TD ty, TD ty + TD) and columns k in [TD tx, TD tx + TD) of dL/dM.
+template <int TD>
+__global__ __launch_bounds__(kGradThreads) void grad_data(GradArgs a) {
+  extern __shared__ float sm[];
+  const int d = 16 * TD, dp = d + 1, Tb = a.Tb;
+  float* ms = sm;               // M rows [d][dp]
+  float* xs = ms + d * dp;      // block of X [Tb][dp]
+  float* ws = xs + Tb * dp;     // W, then dL/dW [Tb][dp]
+  float* us = ws + Tb * dp;     // U, then dL/dU [Tb][dp]
+  float* ct = us + Tb * dp;     // C_Tb [Tb][Tb]
+  const ViewDev& X = a.X;
+  const int wg = blockIdx.x, chunk = wg % a.chunks, sl = wg / a.chunks;
+  const int h = sl % X.H, b = (sl / X.H) % X.B, l = sl / (X.H * X.B);
+  const int tid = int(threadIdx.x), ty = tid >> 4, tx = tid & 15;
+  const int k0 = chunk * a.blocks_per_wg, k1 = min(a.nblk, k0 + a.blocks_per_wg);
+
+  const float* Mg = a.M + (size_t(l) * X.H + h) * d * d;
+  for (int idx = tid; idx < d * d; idx += kGradThreads) ms[(idx / d) * dp + idx % d] = Mg[idx];
+  for (int idx = tid; idx < Tb * Tb; idx += kGradThreads) {
+    const int u = idx / Tb, t = idx - u * Tb;
+    ct[idx] = float(sqrt((u == 0 ? 1.0 : 2.0) / Tb) * cospi((2.0 * t + 1.0) * u / (2.0 * Tb)));
+  }
+  const double lf = a.stats[4 * l + 0], D = a.stats[4 * l + 3] + 1e-12;
+  const float cf = float(2.0 * a.lam_f / D), lff = float(lf), cr = float(a.lam_r * a.inv_count);
+  float acc[TD][TD];
+#pragma unroll
+  for (int i = 0; i < TD; ++i)
+#pragma unroll
+    for (int j = 0; j < TD; ++j) acc[i][j] = 0.0f;
+  const size_t xbase = size_t(l) * X.sl + size_t(b) * X.sb + size_t(h) * X.sh;
+
+  for (int blk = k0; blk < k1; ++blk) {
+    __syncthreads();  // the previous block's buffers are read (and, at the start, M and C_Tb written)
+    for (int idx = tid; idx < Tb * d; idx += kGradThreads) {
+      const int t = idx / d, c = idx - t * d;
+      const size_t off = xbase + size_t(blk * Tb + t) * X.st + c;
+      xs[t * dp + c] = X.bf16 ? bf16_to_f32(((const uint16_t*)X.ptr)[off]) : ((const float*)X.ptr)[off];
+    }
+    __syncthreads();
+    // W = X M^T: 2 tokens x 4 frequencies per thread and step
+    for (int tile = tid; tile < (Tb / 2) * (d / 4); tile += kGradThreads) {
+      const int t0 = 2 * (tile / (d / 4)), v0 = 4 * (tile % (d / 4));
+      float w[2][4] = {};
+      for (int k = 0; k < d; ++k) {
+        const float x0 = xs[t0 * dp + k], x1 = xs[(t0 + 1) * dp + k];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float m = ms[(v0 + j) * dp + k];
+          w[0][j] = fmaf(x0, m, w[0][j]);
+          w[1][j] = fmaf(x1, m, w[1][j]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        ws[t0 * dp + v0 + j] = w[0][j];
+        ws[(t0 + 1) * dp + v0 + j] = w[1][j];
+      }
+    }
+    __syncthreads();
+    // U = C_Tb W, then dL/dU in place
+    for (int idx = tid; idx < Tb * d; idx += kGradThreads) {
+      const int u = idx / d, v = idx - u * d;
+      float U = 0.0f;
+      for (int t = 0; t < Tb; ++t) U = fmaf(ct[u * Tb + t], ws[t * dp + v], U);
+      const float fu = float(u) / float(Tb - 1), fv = float(v) / float(d - 1);
+      const float rho = sqrtf(fu * fu + fv * fv) * 0.70710678118654752f;
+      const float sg = U > 0.0f ? 1.0f : (U < 0.0f ? -1.0f : 0.0f);
+      us[u * dp + v] = cf * U * (rho - lff) + cr * sg / (a.tau + fabsf(U));
+    }
+    __syncthreads();
+    // dL/dW = C_Tb^T dL/dU
+    for (int idx = tid; idx < Tb * d; idx += kGradThreads) {
+      const int t = idx / d, v = idx - t * d;
+      float gw = 0.0f;
+      for (int u = 0; u < Tb; ++u) gw = fmaf(ct[u * Tb + t], us[u * dp + v], gw);
+      ws[t * dp + v] = gw;
+    }
+    __syncthreads();
+    // dL/dM += (dL/dW)^T X over the block's tokens
+    for (int t = 0; t < Tb; ++t) {
+      float gv[TD], xv[TD];
+#pragma unroll
+      for (int i = 0; i < TD; ++i) {
+        gv[i] = ws[t * dp + TD * ty + i];
+        xv[i] = xs[t * dp + TD * tx + i];
+      }
+#pragma unroll
+      for (int i = 0; i < TD; ++i)
+#pragma unroll
+        for (int j = 0; j < TD; ++j) acc[i][j] = fmaf(gv[i], xv[j], acc[i][j]);
+    }
+  }
+  float* out = a.part + ((size_t(l) * X.H + h) * (size_t(X.B) * a.chunks) + size_t(b) * a.chunks + chunk) * d * d;
+#pragma unroll
+  for (int i = 0; i < TD; ++i)
+#pragma unroll
+    for (int j = 0; j < TD; ++j) out[(TD * ty + i) * d + TD * tx + j] = acc[i][j];
+}
+
+// dL/dM per (layer, head): the partials summed in order, binary64
+__global__ __launch_bounds__(256) void grad_reduce(const float* part, int nparts, int d, double* dM) {
+  const int lh = blockIdx.y;
+  const size_t dd = size_t(d) * d;
+  for (size_t idx = blockIdx.x * size_t(blockDim.x) + threadIdx.x; idx < dd; idx += size_t(gridDim.x) * blockDim.x) {
+    double acc = 0.0;
+    for (int p = 0; p < nparts; ++p) acc += double(part[(size_t(lh) * nparts + p) * dd + idx]);
+    dM[size_t(lh) * dd + idx] = acc;
+  }
+}
+
+// C = A B (+ C when acc) for g x g row-major binary64 matrices in global memory, by the whole
+// workgroup: 32 x 32 output tiles, four outputs per thread, 32-wide K steps through LDS.
+// Callers separate dependent products with barriers.
+__device__ void wg_gemm(const double* A, const double* B, double* C, int g, bool acc) {
+  __shared__ double as[32][33], bs[32][33];
+  const int tid = int(threadIdx.x), r = tid >> 3, c4 = (tid & 7) * 4;
+  const int nt = (g + 31) / 32;
+  for (int tile = 0; tile < nt * nt; ++tile) {
+    const int i0 = 32 * (tile / nt), j0 = 32 * (tile % nt);
+    double o[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int k0 = 0; k0 < g; k0 += 32) {
+      __syncthreads();
+      for (int idx = tid; idx < 32 * 32; idx += kGradThreads) {
+        const int rr = idx >> 5, cc = idx & 31;
+        as[rr][cc] = (i0 + rr < g && k0 + cc < g) ? A[size_t(i0 + rr) * g + k0 + cc] : 0.0;
+        bs[rr][cc] = (k0 + rr < g && j0 + cc < g) ? B[size_t(k0 + rr) * g + j0 + cc] : 0.0;
+      }
+      __syncthreads();
+#pragma unroll 8
+      for (int k = 0; k < 32; ++k) {
+        const double av = as[r][k];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = fma(av, bs[k][c4 + q], o[q]);
+      }
+    }
+    if (i0 + r < g) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (j0 + c4 + q < g) {
+          double* p = C + size_t(i0 + r) * g + j0 + c4 + q;
+          *p = acc ? *p + o[q] : o[q];
+        }
+    }
+  }
+  __syncthreads();
+}
+
+// 1-norm (largest column sum of |.|) of a g x g matrix, by the whole workgroup
+__device__ double wg_norm1(const double* Mx, int g, double* red) {
+  double best = 0.0;
+  for (int j = int(threadIdx.x); j < g; j += kGradThreads) {
+    double s = 0.0;
+    for (int i = 0; i < g; ++i) s += fabs(Mx[size_t(i) * g + j]);
+    best = fmax(best, s);
+  }
+  red[threadIdx.x] = best;
+  __syncthreads();
+  for (int o = kGradThreads / 2; o > 0; o >>= 1) {
+    if (int(threadIdx.x) < o) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + o]);
+    __syncthreads();
+  }
+  const double v = red[0];
+  __syncthreads();
+  return v;
+}
+
+// One workgroup per gauge block (l, h, r): dL/dG from dL/dM, then the Frechet adjoint and
+// dL/dA.  work: six g x g binary64 matrices per block.
+__global__ __launch_bounds__(kGradThreads) void grad_frechet(const double* dM, const float* A, int s, int H, int R, int g,
+                                                             int d, double* work, double* grad) {
+  __shared__ double red[kGradThreads];
+  const int blk = blockIdx.x, r = blk % R, lh = blk / R, h = lh % H, l = lh / H;
+  const size_t gg = size_t(g) * g;
+  double* Mm = work + size_t(blk) * 6 * gg;
+  double* Es = Mm + gg;
+  double* P1 = Es + gg;
+  double* P2 = P1 + gg;
+  double* T1 = P2 + gg;
+  double* T2 = T1 + gg;
+  const double* dMl = dM + size_t(lh) * d * d;
+  const float* Ab = A + ((((size_t(l) * 2 + s) * H + h) * R + r) * gg);
+  for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
+    const int c = idx / g, k = idx - c * g;
+    double acc = 0.0;
+    for (int v = 0; v < d; ++v) {
+      const double cv = sqrt((v == 0 ? 1.0 : 2.0) / d) * cospi((2.0 * (r * g + c) + 1.0) * v / (2.0 * d));
+      acc = fma(cv, dMl[size_t(v) * d + r * g + k], acc);
+    }
+    Es[idx] = acc;                                          // dL/dG
+    Mm[idx] = double(Ab[size_t(k) * g + c]) - double(Ab[idx]);  // S^T = A^T - A
+  }
+  __syncthreads();
+  const double e = wg_norm1(Es, g, red);
+  double* out = grad + size_t(blk) * gg;
+  if (!(e > 0.0)) {
+    for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) out[idx] = 0.0;
+    return;
+  }
+  // W = [[S^T, E / e], [0, S^T]] halved sq times until its 1-norm (at most |S^T|_1 + 1) is <= 1/2
+  double nw = wg_norm1(Mm, g, red) + 1.0;
+  if (!isfinite(nw) || !isfinite(e)) {  // non-finite generators or statistics: no scaling ends
+    for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) out[idx] = __builtin_nan("");
+    return;
+  }
+  int sq = 0;
+  while (nw > 0.5) {
+    nw *= 0.5;
+    ++sq;
+  }
+  const double fm = ldexp(1.0, -sq), fe = fm / e;
+  for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
+    Mm[idx] *= fm;
+    Es[idx] *= fe;
+    P1[idx] = (idx / g == idx % g) ? 1.0 : 0.0;
+    P2[idx] = 0.0;
+  }
+  __syncthreads();
+  // exp(W) = [[P1, P2], [0, P1]] by Horner's rule: P <- I + W P / k for k = terms .. 1
+  for (int k = kFrechetTerms; k >= 1; --k) {
+    wg_gemm(Mm, P1, T1, g, false);
+    wg_gemm(Mm, P2, T2, g, false);
+    wg_gemm(Es, P1, T2, g, true);
+    const double ik = 1.0 / k;
+    for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
+      P1[idx] = ((idx / g == idx % g) ? 1.0 : 0.0) + T1[idx] * ik;
+      P2[idx] = T2[idx] * ik;
+    }
+    __syncthreads();
+  }
+  // squaring: [[P1, P2], [0, P1]]^2 = [[P1 P1, P1 P2 + P2 P1], [0, P1 P1]]
+  for (int q = 0; q < sq; ++q) {
+    wg_gemm(P1, P1, T1, g, false);
+    wg_gemm(P1, P2, T2, g, false);
+    wg_gemm(P2, P1, T2, g, true);
+    for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
+      P1[idx] = T1[idx];
+      P2[idx] = T2[idx];
+    }
+    __syncthreads();
+  }
+  // dL/dS = e P2, dL/dA = dL/dS - (dL/dS)^T
+  for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
+    const int i = idx / g, j = idx - i * g;
+    out[idx] = e * (P2[idx] - P2[size_t(j) * g + i]);
+  }
+}
+
+template <int TD>
+hipError_t launch_data(const GradArgs& a, int nwg, size_t smem, hipStream_t st) {
+  hipError_t e;
+  if (smem > 65536 &&
+      (e = hipFuncSetAttribute((const void*)grad_data<TD>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem)) !=
+          hipSuccess)
+    return e;
+  hipLaunchKernelGGL(grad_data<TD>, dim3(nwg), dim3(kGradThreads), smem, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+GradLayout grad_layout(const cg_gauge_shape& s, int B, int T, int Tb) {
+  GradLayout o;
+  const int nblk = Tb > 0 ? T / Tb : 0;
+  // about 1024 workgroups over the (layer, batch row, head) slices, at least 4 blocks each
+  const int nslices = s.L * B * s.H;
+  int chunks = std::max(1, (1024 + nslices - 1) / std::max(nslices, 1));
+  chunks = std::min(chunks, std::max(1, nblk / 4));
+  o.blocks_per_wg = nblk > 0 ? (nblk + chunks - 1) / chunks : 1;
+  o.chunks = nblk > 0 ? (nblk + o.blocks_per_wg - 1) / o.blocks_per_wg : 1;
+  const size_t dd = size_t(s.d) * s.d, gg = size_t(s.g) * s.g;
+  const size_t nlh = size_t(s.L) * s.H;
+  size_t off = align256(spec_layout(s, Tb).total);
+  o.off_m = off;
+  off = align256(off + nlh * dd * 4);
+  o.off_part = off;
+  off = align256(off + nlh * size_t(B) * o.chunks * dd * 4);
+  o.off_dm = off;
+  off = align256(off + nlh * dd * 8);
+  o.off_work = off;
+  off = align256(off + nlh * (s.d / s.g) * 6 * gg * 8);
+  o.total = off;
+  return o;
+}
+
+hipError_t launch_gauge_grad(int s, const ViewDev& X, const GaugeDev& G, const float* A, int Tb, float tau, float lam_f,
+                             float lam_r, void* ws, double* stats, double* grad, bool force_generic, hipStream_t st) {
+  const cg_gauge_shape shp{X.L, X.H, X.d, G.g};
+  hipError_t e = launch_spectral(s, X, G, Tb, tau, ws, stats, nullptr, force_generic, st);
+  if (e != hipSuccess) return e;
+  const GradLayout lay = grad_layout(shp, X.B, X.T, Tb);
+  char* base = static_cast<char*>(ws);
+  float* M = reinterpret_cast<float*>(base + lay.off_m);
+  float* part = reinterpret_cast<float*>(base + lay.off_part);
+  double* dM = reinterpret_cast<double*>(base + lay.off_dm);
+  double* work = reinterpret_cast<double*>(base + lay.off_work);
+  const int d = X.d, R = d / G.g, nblk = X.T / Tb;
+  hipLaunchKernelGGL(grad_prep, dim3((d * d + 255) / 256, X.L * X.H), dim3(256), 0, st, s, G, X.H, d, M);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  GradArgs a{};
+  a.X = X;
+  a.M = M;
+  a.stats = stats;
+  a.part = part;
+  a.Tb = Tb;
+  a.nblk = nblk;
+  a.chunks = lay.chunks;
+  a.blocks_per_wg = lay.blocks_per_wg;
+  a.tau = tau;
+  a.inv_tau = 1.0f / tau;
+  a.lam_f = lam_f;
+  a.lam_r = lam_r;
+  const double count = double(X.B) * X.H * nblk * Tb * d;
+  a.inv_count = count > 0 ? 1.0 / count : 0.0;
+  const int nwg = X.L * X.B * X.H * lay.chunks;
+  const size_t smem = (size_t(d) * (d + 1) + size_t(3) * Tb * (d + 1) + size_t(Tb) * Tb) * sizeof(float);
+  if (nblk > 0) {
+    switch (d / 16) {
+      case 1: e = launch_data<1>(a, nwg, smem, st); break;
+      case 2: e = launch_data<2>(a, nwg, smem, st); break;
+      case 3: e = launch_data<3>(a, nwg, smem, st); break;
+      case 4: e = launch_data<4>(a, nwg, smem, st); break;
+      case 5: e = launch_data<5>(a, nwg, smem, st); break;
+      case 6: e = launch_data<6>(a, nwg, smem, st); break;
+      case 7: e = launch_data<7>(a, nwg, smem, st); break;
+      case 8: e = launch_data<8>(a, nwg, smem, st); break;
+      default: return hipErrorInvalidValue;
+    }
+    if (e != hipSuccess) return e;
+  }
+  const int nparts = nblk > 0 ? X.B * lay.chunks : 0;
+  hipLaunchKernelGGL(grad_reduce, dim3((d * d + 255) / 256, X.L * X.H), dim3(256), 0, st, part, nparts, d, dM);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(grad_frechet, dim3(X.L * X.H * R), dim3(kGradThreads), 0, st, dM, A, s, X.H, R, G.g, d, work,
+                     grad);
+  return hipGetLastError();
+}
+
+}  // namespace cg

@@ -637,6 +637,31 @@ int32_t kv_spectral_stats(int32_t s, const cg_kv_view* X, const void* G_dev, cg_
   return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
 }
 
+size_t gauge_grad_workspace_bytes(cg_gauge_shape shp, int32_t B, int32_t T, int32_t block_t) {
+  if (check_shape(shp) != CG_OK || block_t < 2 || block_t > 32 || (block_t & (block_t - 1)) || B <= 0 || T < 0 ||
+      shp.d % 16 || shp.d > 128)
+    return 0;
+  return grad_layout(shp, B, T, block_t).total;
+}
+
+int32_t kv_gauge_grad(int32_t s, const cg_kv_view* X, const float* A, const void* G_dev, cg_gauge_shape shp,
+                      int32_t block_t, float tau, float lambda_f, float lambda_r, void* workspace, double* stats,
+                      double* grad, void* stream) {
+  int32_t rc = check_shape(shp);
+  if (rc != CG_OK) return rc;
+  if (s < 0 || s > 1 || !A || !G_dev || !workspace || !stats || !grad) return CG_ERR_ARG;
+  if (block_t < 2 || block_t > 32 || (block_t & (block_t - 1)) || shp.d % 16 || shp.d > 128) return CG_ERR_UNSUPPORTED;
+  if (!(tau > 0.0f) || !isfinite(tau) || !isfinite(lambda_f) || !isfinite(lambda_r)) return CG_ERR_ARG;
+  if (!aligned16(G_dev) || !aligned16(workspace) || (reinterpret_cast<uintptr_t>(A) & 3u) ||
+      (reinterpret_cast<uintptr_t>(stats) & 7u) || (reinterpret_cast<uintptr_t>(grad) & 7u))
+    return CG_ERR_ALIGN;
+  if ((rc = check_view(X, shp, shp.L)) != CG_OK) return rc;
+  if (X->T > 0 && !X->ptr) return CG_ERR_ARG;
+  hipError_t e = launch_gauge_grad(s, view_dev(X), gauge_dev(G_dev, shp), A, block_t, tau, lambda_f, lambda_r, workspace,
+                                   stats, grad, force_generic(), static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
+}
+
 size_t attend_workspace_bytes(cg_gauge_shape shp, int32_t nl, int32_t B, int32_t Hq, int32_t T_cap) {
   if (check_shape(shp) != CG_OK || nl <= 0 || B <= 0 || T_cap <= 0 || Hq < shp.H || Hq % shp.H) return 0;
   return attend_plan(nl, B, shp.H, Hq, shp.d, T_cap).ws_bytes;

@@ -118,6 +118,16 @@ SpecLayout spec_layout(const cg_gauge_shape& s, int Tb);
 hipError_t launch_spectral(int s, const ViewDev& X, const GaugeDev& G, int Tb, float tau, void* ws, double* stats,
                            double* energy, bool force_generic, hipStream_t st);
 
+// Gradient of the training objective with respect to the gauge generators: workspace layout
+// (the spectral statistics' own workspace first) and launch.
+struct GradLayout {
+  size_t off_m = 0, off_part = 0, off_dm = 0, off_work = 0, total = 0;
+  int chunks = 1, blocks_per_wg = 1;
+};
+GradLayout grad_layout(const cg_gauge_shape& s, int B, int T, int Tb);
+hipError_t launch_gauge_grad(int s, const ViewDev& X, const GaugeDev& G, const float* A, int Tb, float tau, float lam_f,
+                             float lam_r, void* ws, double* stats, double* grad, bool force_generic, hipStream_t st);
+
 // Decode-phase attention over the compressed caches (inverse gauge folded into the query and
 // the output).  Query heads j = h * grp + jj of KV head h read that head's K / V caches.
 struct AttendDev {

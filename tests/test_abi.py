@@ -210,6 +210,33 @@ def test_spectral_stats_reject_invalid_arguments():
     assert call(shp=cg.shape(1, 2, 64, 48)) == cg.CG_ERR_UNSUPPORTED
 
 
+def test_gauge_grad_rejects_invalid_arguments():
+    shp = cg.shape(1, 2, 64, 16)
+    v = _fake_view(T=32)
+    assert cg.gauge_grad_workspace_bytes(shp, 2, 32, 16) >= cg.spectral_workspace_bytes(shp, 16) > 0
+    assert cg.gauge_grad_workspace_bytes(shp, 2, 32, 3) == 0
+    assert cg.gauge_grad_workspace_bytes(cg.shape(1, 2, 40, 8), 2, 32, 16) == 0    # d not a multiple of 16
+    assert cg.gauge_grad_workspace_bytes(cg.shape(1, 2, 256, 16), 2, 32, 16) == 0  # d above 128
+    f = cg.lib().kv_gauge_grad
+    ok = dict(s=0, A=0x40000, blk=16, tau=0.04, lf=1.0, lr=0.02, ws=0x70000, stats=0x80000, grad=0x90000)
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["s"], C.byref(a.get("view", v)), a["A"], 0x50000, a.get("shp", shp), a["blk"], a["tau"], a["lf"],
+                 a["lr"], a["ws"], a["stats"], a["grad"], None)
+    assert call(blk=3) == cg.CG_ERR_UNSUPPORTED
+    assert call(shp=cg.shape(1, 2, 256, 16), view=_fake_view(d=256)) == cg.CG_ERR_UNSUPPORTED
+    assert call(tau=-1.0) == cg.CG_ERR_ARG
+    assert call(lf=float("inf")) == cg.CG_ERR_ARG
+    assert call(lr=float("nan")) == cg.CG_ERR_ARG
+    assert call(s=-1) == cg.CG_ERR_ARG
+    assert call(A=None) == cg.CG_ERR_ARG
+    assert call(grad=None) == cg.CG_ERR_ARG
+    assert call(A=0x40002) == cg.CG_ERR_ALIGN
+    assert call(grad=0x90004) == cg.CG_ERR_ALIGN
+    assert call(ws=0x70008) == cg.CG_ERR_ALIGN
+    assert call(view=_fake_view(H=3)) == cg.CG_ERR_SHAPE
+
+
 def test_attend_rejects_invalid_arguments():
     shp = cg.shape(2, 2, 64, 16)
     q = _fake_view(L=1, H=4, T=1, strides=(256, 256, 64, 64))
