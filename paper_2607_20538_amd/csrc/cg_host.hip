@@ -6,6 +6,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
+#include <thread>
 #include <vector>
 
 #include "cg_internal.h"
@@ -119,13 +121,18 @@ void hadamard(int g, double* Q) {
   for (size_t k = 0; k < size_t(g) * g; ++k) Q[k] *= s;
 }
 
+// C = A B (row-major g x g); each C[i][j] sums its products in increasing k, the loops run
+// along rows of B and C
 void matmul(int g, const double* A, const double* B, double* C) {
-  for (int i = 0; i < g; ++i)
-    for (int j = 0; j < g; ++j) {
-      double acc = 0.0;
-      for (int k = 0; k < g; ++k) acc += A[i * g + k] * B[k * g + j];
-      C[i * g + j] = acc;
+  for (int i = 0; i < g; ++i) {
+    double* c = C + size_t(i) * g;
+    for (int j = 0; j < g; ++j) c[j] = 0.0;
+    for (int k = 0; k < g; ++k) {
+      const double a = A[size_t(i) * g + k];
+      const double* b = B + size_t(k) * g;
+      for (int j = 0; j < g; ++j) c[j] += a * b[j];
     }
+  }
 }
 
 // exp(A - A^T) by scaling and squaring with the diagonal Pade(8,8) approximant; the
@@ -426,24 +433,49 @@ int32_t gauge_make(int32_t kind, cg_gauge_shape shp, uint64_t seed, const float*
   const GaugeLayout gl = gauge_layout(shp);
   const size_t gg = size_t(g) * g;
   std::vector<float> G32(gl.nblk * gg);
-  std::vector<double> Q(gg);
-  for (int64_t blk = 0; blk < gl.nblk; ++blk) {
-    switch (kind) {
-      case CG_GAUGE_IDENTITY:
-        for (size_t i = 0; i < gg; ++i) Q[i] = (i / g == i % g) ? 1.0 : 0.0;
-        break;
-      case CG_GAUGE_HAAR: haar(g, seed, uint64_t(blk), Q.data()); break;
-      case CG_GAUGE_DCT2: dct2(g, Q.data()); break;
-      case CG_GAUGE_HADAMARD: hadamard(g, Q.data()); break;
-      case CG_GAUGE_EXPM: expm_skew(g, params + blk * gg, Q.data()); break;
-      case CG_GAUGE_USER:
-        for (size_t i = 0; i < gg; ++i) Q[i] = params[blk * gg + i];
-        break;
+  std::atomic<bool> not_orth{false};
+  // blocks [b0, b1): each block depends only on its own index and parameters
+  auto blocks = [&](int64_t b0, int64_t b1) {
+    std::vector<double> Q(gg);
+    for (int64_t blk = b0; blk < b1; ++blk) {
+      switch (kind) {
+        case CG_GAUGE_IDENTITY:
+          for (size_t i = 0; i < gg; ++i) Q[i] = (i / g == i % g) ? 1.0 : 0.0;
+          break;
+        case CG_GAUGE_HAAR: haar(g, seed, uint64_t(blk), Q.data()); break;
+        case CG_GAUGE_DCT2: dct2(g, Q.data()); break;
+        case CG_GAUGE_HADAMARD: hadamard(g, Q.data()); break;
+        case CG_GAUGE_EXPM: expm_skew(g, params + blk * gg, Q.data()); break;
+        case CG_GAUGE_USER:
+          for (size_t i = 0; i < gg; ++i) Q[i] = params[blk * gg + i];
+          break;
+      }
+      float* out = &G32[blk * gg];
+      for (size_t i = 0; i < gg; ++i) out[i] = float(Q[i]);
+      if (kind == CG_GAUGE_USER && orth_error(g, out) > 1e-5) not_orth = true;
     }
-    float* out = &G32[blk * gg];
-    for (size_t i = 0; i < gg; ++i) out[i] = float(Q[i]);
-    if (kind == CG_GAUGE_USER && orth_error(g, out) > 1e-5) return CG_ERR_NOT_ORTHOGONAL;
+  };
+  // the exponential of a wide block costs O(g^3) per block: spread the blocks over host threads
+  // (at most 16; the serial loop when threads cannot be started)
+  int nth = 1;
+  if (kind == CG_GAUGE_EXPM && g >= 32)
+    nth = int(std::min<int64_t>(gl.nblk, std::max(1u, std::min(16u, std::thread::hardware_concurrency()))));
+  bool serial = nth <= 1;
+  if (!serial) {
+    try {
+      std::vector<std::thread> pool;
+      const int64_t per = (gl.nblk + nth - 1) / nth;
+      for (int t = 0; t < nth; ++t) {
+        const int64_t b0 = t * per, b1 = std::min<int64_t>(gl.nblk, b0 + per);
+        if (b0 < b1) pool.emplace_back(blocks, b0, b1);
+      }
+      for (auto& th : pool) th.join();
+    } catch (...) {
+      serial = true;
+    }
   }
+  if (serial) blocks(0, gl.nblk);
+  if (not_orth) return CG_ERR_NOT_ORTHOGONAL;
   (void)R;
   if (G_host) memcpy(G_host, G32.data(), G32.size() * sizeof(float));
   if (G_dev) {
