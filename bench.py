@@ -37,7 +37,7 @@ def parse():
                     help="HBM traffic per launch measured with rocprofv3 counters (optional)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the timed region, run one plain 512 MiB device copy (counter calibration)")
-    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral", "attend", "attend_paged", "attend_tiles", "zfp"]),
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral", "grad", "attend", "attend_paged", "attend_tiles", "zfp"]),
                     help="llama8b (default) prints the headline line; the others print per-kernel timings of "
                          "the KIVI, rolling-step and 27B-sweep workloads")
     return ap.parse_args()
@@ -221,6 +221,19 @@ def workload_cpu_baseline(name, w, gpu):
                             else "attention of 4 query heads per KV head")
                          + f", {t_row:.1f} s single-threaded, x {rows} (layer, batch row) pairs"}
         return out
+    if name == "grad":
+        # one (layer, head) slice of K, 256 tokens (16 blocks), 16-channel gauges, extrapolated to
+        # the tensor's L x B x H slices of T tokens
+        g, T = 16, 256
+        X = synth.kv_tensor(w, 0, L=1)[:, :, :1, :T]
+        A = 0.05 * np.random.default_rng(w.gauge_seed).standard_normal((1, 2, 1, w.d // g, g, g))
+        t0 = time.perf_counter()
+        O.spectral_train_grad(X, A, 0, Tb=16)
+        t1 = time.perf_counter() - t0
+        scale = w.L * w.B * w.H * (w.T / T)
+        return {"value": round(t1 * scale * 1e3, 1), "unit": "ms per tensor (extrapolated)", "cores": 1,
+                "kind": "oracle", "sample": f"layer 0, head 0 of K, {T} tokens, g = {g}: {t1:.2f} s single-threaded, "
+                                            f"x {scale:.0f} such slices"}
     if name == "spectral":
         G = O.gauge_make(O.GAUGE_HAAR, 1, w.H, w.d, w.g, seed=w.gauge_seed)
         t_total, elems = 0.0, 0
@@ -278,7 +291,7 @@ def other_workload(name, steps, warmup, cpu=True, probe=False):
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral", "zfp") else ("rolling" if name in ("attend", "attend_paged", "attend_tiles") else name)]
+    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral", "grad", "zfp") else ("rolling" if name in ("attend", "attend_paged", "attend_tiles") else name)]
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     out = {"workload": name, "shape": {"L": w.L, "B": w.B, "H": w.H, "T": w.T, "d": w.d}, "steps": steps,
            "kernels": os.environ.get("CG_KERNELS") or "default"}
@@ -319,6 +332,36 @@ def other_workload(name, steps, warmup, cpu=True, probe=False):
             rows[tag] = {"ms": round(ms, 3), "GBps_bf16_in": round(X.numel() * 2 / ms / 1e6, 1),
                          "L_freq_mean": round(float(st[:, 0].mean()), 6), "L_rate_mean": round(float(st[:, 1].mean()), 6)}
             del X
+            torch.cuda.empty_cache()
+        out["runs"] = rows
+    elif name == "grad":
+        # gradient of the section 4.2 objective with respect to the generators A of G = exp(A - A^T)
+        # (section 4.1) on the Llama-3-8B shape: full-head (g = 128) and 16-channel gauges,
+        # 16-token blocks, tau = 0.04, lambda_f = 1, lambda_r = 0.02; generators drawn N(0, 0.05^2)
+        rows = {}
+        for g in (128, 16):
+            shp = cg.shape(w.L, w.H, w.d, g)
+            A = (0.05 * np.random.default_rng(w.gauge_seed).standard_normal((w.L, 2, w.H, w.d // g, g, g))).astype(np.float32)
+            Gd = cg.alloc_gauge(shp)
+            t0 = time.perf_counter()
+            cg.gauge_make(cg.GAUGE_EXPM, shp, params=A, G_host=None, G_dev=Gd)
+            t_make = time.perf_counter() - t0
+            Ad = torch.from_numpy(A).cuda()
+            ws = torch.empty(cg.gauge_grad_workspace_bytes(shp, w.B, w.T, 16), dtype=torch.uint8, device="cuda")
+            stats = torch.empty((w.L, 4), dtype=torch.float64, device="cuda")
+            grad = torch.empty((w.L, w.H, w.d // g, g, g), dtype=torch.float64, device="cuda")
+            for s, tag in ((0, "K"), (1, "V")):
+                X = layer_input(s)
+                ms = _timed(lambda: cg.kv_gauge_grad(s, X, Ad, Gd, shp, 16, 0.04, 1.0, 0.02, ws, stats, grad,
+                                                     stream=stream.cuda_stream), steps, warmup, stream)
+                st = stats.cpu().numpy()
+                rows[f"g{g}_{tag}"] = {"ms": round(ms, 3), "GBps_bf16_in": round(X.numel() * 2 / ms / 1e6, 1),
+                                       "L_train_mean": round(float((st[:, 0] + 0.02 * st[:, 1]).mean()), 6),
+                                       "grad_max": float(grad.abs().max().item())}
+                del X
+                torch.cuda.empty_cache()
+            rows[f"g{g}_gauge_make_s"] = round(t_make, 2)
+            del ws, grad, Gd
             torch.cuda.empty_cache()
         out["runs"] = rows
     elif name in ("kivi", "gemma27b", "tiles", "zfp"):
