@@ -13,11 +13,15 @@
 //           of exp([[S^T, dL/dG], [0, S^T]]);   dL/dA = dL/dS - (dL/dS)^T.
 //
 // Kernels: grad_prep forms M in binary32 per (layer, head) (binary64 sums); grad_data runs the
-// blocks of a range of tokens of one (layer, batch row, head), recomputing W and U on the VALU in
-// binary32 through LDS, and accumulates its part of dL/dM in registers (a (d/16) x (d/16) tile
-// per thread), written as one partial per workgroup; grad_reduce sums the partials in a fixed
-// order (binary64, deterministic); grad_frechet forms dL/dG and the Frechet adjoint per gauge
-// block in binary64 (power series of the scaled block matrix by Horner's rule, then squaring).
+// blocks of a range of tokens of one (layer, batch row, head) on the VALU through LDS: X and M
+// in binary32, W, U, dL/dU and dL/dW in binary64 (the binary32 products accumulate exactly),
+// and accumulates its part of dL/dM in binary64 registers (a (d/16) x (d/16) tile per thread),
+// written as one partial per workgroup; grad_reduce sums the partials in a fixed order
+// (deterministic); grad_frechet forms dL/dG and the Frechet adjoint per gauge block in binary64
+// (power series of the scaled block matrix by Horner's rule, then squaring).
+// Binary64 through the data pass matters: dL/dA is the antisymmetric part of dL/dS, which for
+// smooth objectives is much smaller than the terms that cancel in it (about 40x on random
+// Llama-shaped data), so binary32 sums over a block's d channels would reach the result.
 #include <algorithm>
 
 #include "cg_internal.h"
@@ -49,7 +53,7 @@ struct GradArgs {
   ViewDev X;
   const float* M;        // [L][H][d][d]
   const double* stats;   // [L][4] from the forward statistics
-  float* part;           // [L][H][B * chunks][d][d] partial dL/dM
+  double* part;          // [L][H][B * chunks][d][d] partial dL/dM
   int Tb, nblk, chunks, blocks_per_wg;
   float inv_tau, tau, lam_f, lam_r;
   double inv_count;      // 1 / (coefficients per layer)
@@ -59,13 +63,13 @@ struct GradArgs {
 // rows v in [TD ty, TD ty + TD) and columns k in [TD tx, TD tx + TD) of dL/dM.
 template <int TD>
 __global__ __launch_bounds__(kGradThreads) void grad_data(GradArgs a) {
-  extern __shared__ float sm[];
+  extern __shared__ double smd[];
   const int d = 16 * TD, dp = d + 1, Tb = a.Tb;
-  float* ms = sm;               // M rows [d][dp]
-  float* xs = ms + d * dp;      // block of X [Tb][dp]
-  float* ws = xs + Tb * dp;     // W, then dL/dW [Tb][dp]
-  float* us = ws + Tb * dp;     // U, then dL/dU [Tb][dp]
-  float* ct = us + Tb * dp;     // C_Tb [Tb][Tb]
+  double* ws = smd;                                  // W, then dL/dW [Tb][dp]
+  double* us = ws + Tb * dp;                         // U, then dL/dU [Tb][dp]
+  float* ms = reinterpret_cast<float*>(us + Tb * dp);  // M rows [d][dp]
+  float* xs = ms + d * dp;                           // block of X [Tb][dp]
+  float* ct = xs + Tb * dp;                          // C_Tb [Tb][Tb]
   const ViewDev& X = a.X;
   const int wg = blockIdx.x, chunk = wg % a.chunks, sl = wg / a.chunks;
   const int h = sl % X.H, b = (sl / X.H) % X.B, l = sl / (X.H * X.B);
@@ -79,12 +83,12 @@ __global__ __launch_bounds__(kGradThreads) void grad_data(GradArgs a) {
     ct[idx] = float(sqrt((u == 0 ? 1.0 : 2.0) / Tb) * cospi((2.0 * t + 1.0) * u / (2.0 * Tb)));
   }
   const double lf = a.stats[4 * l + 0], D = a.stats[4 * l + 3] + 1e-12;
-  const float cf = float(2.0 * a.lam_f / D), lff = float(lf), cr = float(a.lam_r * a.inv_count);
-  float acc[TD][TD];
+  const double cf = 2.0 * a.lam_f / D, cr = a.lam_r * a.inv_count, tau = a.tau;
+  double acc[TD][TD];
 #pragma unroll
   for (int i = 0; i < TD; ++i)
 #pragma unroll
-    for (int j = 0; j < TD; ++j) acc[i][j] = 0.0f;
+    for (int j = 0; j < TD; ++j) acc[i][j] = 0.0;
   const size_t xbase = size_t(l) * X.sl + size_t(b) * X.sb + size_t(h) * X.sh;
 
   for (int blk = k0; blk < k1; ++blk) {
@@ -98,14 +102,14 @@ __global__ __launch_bounds__(kGradThreads) void grad_data(GradArgs a) {
     // W = X M^T: 2 tokens x 4 frequencies per thread and step
     for (int tile = tid; tile < (Tb / 2) * (d / 4); tile += kGradThreads) {
       const int t0 = 2 * (tile / (d / 4)), v0 = 4 * (tile % (d / 4));
-      float w[2][4] = {};
+      double w[2][4] = {};
       for (int k = 0; k < d; ++k) {
-        const float x0 = xs[t0 * dp + k], x1 = xs[(t0 + 1) * dp + k];
+        const double x0 = xs[t0 * dp + k], x1 = xs[(t0 + 1) * dp + k];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float m = ms[(v0 + j) * dp + k];
-          w[0][j] = fmaf(x0, m, w[0][j]);
-          w[1][j] = fmaf(x1, m, w[1][j]);
+          const double m = ms[(v0 + j) * dp + k];
+          w[0][j] = fma(x0, m, w[0][j]);
+          w[1][j] = fma(x1, m, w[1][j]);
         }
       }
 #pragma unroll
@@ -118,25 +122,25 @@ __global__ __launch_bounds__(kGradThreads) void grad_data(GradArgs a) {
     // U = C_Tb W, then dL/dU in place
     for (int idx = tid; idx < Tb * d; idx += kGradThreads) {
       const int u = idx / d, v = idx - u * d;
-      float U = 0.0f;
-      for (int t = 0; t < Tb; ++t) U = fmaf(ct[u * Tb + t], ws[t * dp + v], U);
-      const float fu = float(u) / float(Tb - 1), fv = float(v) / float(d - 1);
-      const float rho = sqrtf(fu * fu + fv * fv) * 0.70710678118654752f;
-      const float sg = U > 0.0f ? 1.0f : (U < 0.0f ? -1.0f : 0.0f);
-      us[u * dp + v] = cf * U * (rho - lff) + cr * sg / (a.tau + fabsf(U));
+      double U = 0.0;
+      for (int t = 0; t < Tb; ++t) U = fma(double(ct[u * Tb + t]), ws[t * dp + v], U);
+      const double fu = double(u) / (Tb - 1), fv = double(v) / (d - 1);
+      const double rho = sqrt(fu * fu + fv * fv) * 0.70710678118654752;
+      const double sg = U > 0.0 ? 1.0 : (U < 0.0 ? -1.0 : 0.0);
+      us[u * dp + v] = cf * U * (rho - lf) + cr * sg / (tau + fabs(U));
     }
     __syncthreads();
     // dL/dW = C_Tb^T dL/dU
     for (int idx = tid; idx < Tb * d; idx += kGradThreads) {
       const int t = idx / d, v = idx - t * d;
-      float gw = 0.0f;
-      for (int u = 0; u < Tb; ++u) gw = fmaf(ct[u * Tb + t], us[u * dp + v], gw);
+      double gw = 0.0;
+      for (int u = 0; u < Tb; ++u) gw = fma(double(ct[u * Tb + t]), us[u * dp + v], gw);
       ws[t * dp + v] = gw;
     }
     __syncthreads();
     // dL/dM += (dL/dW)^T X over the block's tokens
     for (int t = 0; t < Tb; ++t) {
-      float gv[TD], xv[TD];
+      double gv[TD], xv[TD];
 #pragma unroll
       for (int i = 0; i < TD; ++i) {
         gv[i] = ws[t * dp + TD * ty + i];
@@ -145,10 +149,10 @@ __global__ __launch_bounds__(kGradThreads) void grad_data(GradArgs a) {
 #pragma unroll
       for (int i = 0; i < TD; ++i)
 #pragma unroll
-        for (int j = 0; j < TD; ++j) acc[i][j] = fmaf(gv[i], xv[j], acc[i][j]);
+        for (int j = 0; j < TD; ++j) acc[i][j] = fma(gv[i], xv[j], acc[i][j]);
     }
   }
-  float* out = a.part + ((size_t(l) * X.H + h) * (size_t(X.B) * a.chunks) + size_t(b) * a.chunks + chunk) * d * d;
+  double* out = a.part + ((size_t(l) * X.H + h) * (size_t(X.B) * a.chunks) + size_t(b) * a.chunks + chunk) * d * d;
 #pragma unroll
   for (int i = 0; i < TD; ++i)
 #pragma unroll
@@ -156,12 +160,12 @@ __global__ __launch_bounds__(kGradThreads) void grad_data(GradArgs a) {
 }
 
 // dL/dM per (layer, head): the partials summed in order, binary64
-__global__ __launch_bounds__(256) void grad_reduce(const float* part, int nparts, int d, double* dM) {
+__global__ __launch_bounds__(256) void grad_reduce(const double* part, int nparts, int d, double* dM) {
   const int lh = blockIdx.y;
   const size_t dd = size_t(d) * d;
   for (size_t idx = blockIdx.x * size_t(blockDim.x) + threadIdx.x; idx < dd; idx += size_t(gridDim.x) * blockDim.x) {
     double acc = 0.0;
-    for (int p = 0; p < nparts; ++p) acc += double(part[(size_t(lh) * nparts + p) * dd + idx]);
+    for (int p = 0; p < nparts; ++p) acc += part[(size_t(lh) * nparts + p) * dd + idx];
     dM[size_t(lh) * dd + idx] = acc;
   }
 }
@@ -331,7 +335,7 @@ GradLayout grad_layout(const cg_gauge_shape& s, int B, int T, int Tb) {
   o.off_m = off;
   off = align256(off + nlh * dd * 4);
   o.off_part = off;
-  off = align256(off + nlh * size_t(B) * o.chunks * dd * 4);
+  off = align256(off + nlh * size_t(B) * o.chunks * dd * 8);
   o.off_dm = off;
   off = align256(off + nlh * dd * 8);
   o.off_work = off;
@@ -348,7 +352,7 @@ hipError_t launch_gauge_grad(int s, const ViewDev& X, const GaugeDev& G, const f
   const GradLayout lay = grad_layout(shp, X.B, X.T, Tb);
   char* base = static_cast<char*>(ws);
   float* M = reinterpret_cast<float*>(base + lay.off_m);
-  float* part = reinterpret_cast<float*>(base + lay.off_part);
+  double* part = reinterpret_cast<double*>(base + lay.off_part);
   double* dM = reinterpret_cast<double*>(base + lay.off_dm);
   double* work = reinterpret_cast<double*>(base + lay.off_work);
   const int d = X.d, R = d / G.g, nblk = X.T / Tb;
@@ -370,7 +374,8 @@ hipError_t launch_gauge_grad(int s, const ViewDev& X, const GaugeDev& G, const f
   const double count = double(X.B) * X.H * nblk * Tb * d;
   a.inv_count = count > 0 ? 1.0 / count : 0.0;
   const int nwg = X.L * X.B * X.H * lay.chunks;
-  const size_t smem = (size_t(d) * (d + 1) + size_t(3) * Tb * (d + 1) + size_t(Tb) * Tb) * sizeof(float);
+  const size_t smem = size_t(2) * Tb * (d + 1) * sizeof(double) +
+                      (size_t(d) * (d + 1) + size_t(Tb) * (d + 1) + size_t(Tb) * Tb) * sizeof(float);
   if (nblk > 0) {
     switch (d / 16) {
       case 1: e = launch_data<1>(a, nwg, smem, st); break;
