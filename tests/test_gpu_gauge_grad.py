@@ -132,3 +132,28 @@ def test_full_size_sampled_layers(g):
     for l in (0, 13, 31):
         ref = O.spectral_train_grad(np.ascontiguousarray(X[l:l + 1]), A[l:l + 1].astype(np.float64), 0, Tb=16)[0]
         assert np.abs(grad[l] - ref).max() <= TOL * np.abs(ref).max(), l
+
+
+def test_descent_steps_lower_the_objective():
+    """A few steps of gradient descent on the generators with the GPU's gradient (gauge_make
+    rebuilding G = exp(A - A^T) each step): the training objective of section 4.2 falls at every
+    step and the gauges stay orthogonal (section 4.1's parameterisation needs no penalty)."""
+    L_, B, H, T, d, g, Tb = 2, 1, 2, 128, 32, 16, 16
+    rng = np.random.default_rng(21)
+    # tokens with a low-frequency structure in a rotated channel basis, so the objective has room
+    base = np.cumsum(rng.standard_normal((L_, B, H, T, d)), axis=3) / np.sqrt(np.arange(1, T + 1))[None, None, None, :, None]
+    Q = np.linalg.qr(rng.standard_normal((d, d)))[0]
+    X = synth.round_bf16_bits((base @ Q.T).astype(np.float32))
+    A = np.zeros((L_, 2, H, d // g, g, g), dtype=np.float32)
+    losses = []
+    for _ in range(6):
+        grad, stats, _ = _run(X, A, 0, g, Tb)
+        losses.append(stats.reshape(L_, 4)[:, 0] + 0.02 * stats.reshape(L_, 4)[:, 1])
+        A[:, 0] -= (0.5 * grad).astype(np.float32)
+    losses = np.array(losses)
+    assert np.all(np.diff(losses, axis=0) < 0), losses
+    G, _ = cg.gauge_make(cg.GAUGE_EXPM, cg.shape(L_, H, d, g), params=A)
+    eye = np.eye(g, dtype=np.float64)
+    for idx in np.ndindex(*G.shape[:-2]):
+        Gb = G[idx].astype(np.float64)
+        assert np.abs(Gb.T @ Gb - eye).max() < 1e-5
