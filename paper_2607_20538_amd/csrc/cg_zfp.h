@@ -155,6 +155,15 @@ __host__ __device__ __forceinline__ void plane_unwindow(const uint32_t (&xp)[4],
   }
 }
 
+// p on every active lane of the wave (WAVE), or on this lane (the CPU build of this header, which
+// checks each path lane by lane).  The plane coders pick the short path of the last two
+// candidates for the whole wave: a wave whose lanes need different paths runs the general one.
+template <bool WAVE>
+__host__ __device__ __forceinline__ bool all_lanes(bool p) {
+  if constexpr (WAVE) return __builtin_amdgcn_ballot_w64(!p) == 0;
+  else return p;
+}
+
 // 16 RATE bits of one block held in one (RATE <= 4) or two 64-bit words, LSB-first
 template <int RATE>
 struct ZBits {
@@ -230,7 +239,7 @@ __host__ __device__ __forceinline__ void zfp_prepare(const float (&v)[16], ZfpPr
 
 // Second half: the bit planes.  w: the block's 16 RATE bits, LSB-first (words past the block
 // are 0).  Returns flags.
-template <int RATE>
+template <int RATE, bool WAVE = true>
 __host__ __device__ __forceinline__ int zfp_encode_planes(const ZfpPrep& z, const ZfpTables& tb, uint32_t (&w)[4]) {
   constexpr int CAP = ZBits<RATE>::kCap;
   ZBits<RATE> st;
@@ -246,9 +255,17 @@ __host__ __device__ __forceinline__ int zfp_encode_planes(const ZfpPrep& z, cons
       for (int p = 7; p >= 0; --p) {
         if (P0 - 7 + p >= 0 && o < CAP) {
           const uint32_t x = (xp[p >> 1] >> (16 * (p & 1))) & 0xFFFFu;
-          if (n == 16) {
-            st.put(x, o);
-            o += 16;
+          if (all_lanes<WAVE>(n >= 14)) {
+            // at most two candidates left.  n = 15: the last candidate's test bit is the plane's
+            // bit 15 (a 1 makes it significant, its 1 implied), so the plane is its 16 bits, as
+            // for n = 16.  n = 14: test bit, then coefficient 14's bit and, after a 1, the test
+            // for coefficient 15
+            const uint32_t y = x >> 14;
+            const uint32_t gb = y == 0 ? 0u : (y == 1 ? 3u : (y == 2 ? 1u : 7u));
+            const bool two = n == 14;
+            st.put(two ? (x & 0x3FFFu) | (gb << 14) : x, o);
+            o += two ? (y == 0 ? 15 : (y == 2 ? 16 : 17)) : 16;
+            n = two ? (y == 0 ? 14 : (y == 1 ? 15 : 16)) : ((x >> 15) ? 16 : n);
           } else {
             X |= x;
             const int n2 = 32 - __builtin_clz(X | 1u);
@@ -260,7 +277,7 @@ __host__ __device__ __forceinline__ int zfp_encode_planes(const ZfpPrep& z, cons
             const uint32_t G = 3u * F + 1u - (n2 == 16 ? 3u * hb : 2u * hb);
             const int m = __builtin_popcount(y);
             st.put(y ? V | (G << n) : V, o);
-            o += y ? n2 + m + (n2 < 16 ? 1 : -1) : n + 1;
+            o += y ? n2 + m + (n2 < 16 ? 1 : -1) : n + (n < 16 ? 1 : 0);
             n = y ? n2 : n;
           }
         }
@@ -275,17 +292,17 @@ __host__ __device__ __forceinline__ int zfp_encode_planes(const ZfpPrep& z, cons
   return z.finite ? 0 : CG_FLAG_NONFINITE;
 }
 
-template <int RATE>
+template <int RATE, bool WAVE = true>
 __host__ __device__ __forceinline__ int zfp_encode_block(const float (&v)[16], const ZfpTables& tb, uint32_t (&w)[4]) {
   ZfpPrep z;
   zfp_prepare(v, z);
-  return zfp_encode_planes<RATE>(z, tb, w);
+  return zfp_encode_planes<RATE, WAVE>(z, tb, w);
 }
 
 // First half of the decoder: the bit planes of a block's 16 RATE bits w (LSB-first, words past
 // the block 0) into the negabinary coefficients u (sequency order) and the block exponent e; an
 // empty block gives u = 0.
-template <int RATE>
+template <int RATE, bool WAVE = true>
 __host__ __device__ __forceinline__ void zfp_decode_planes(const uint32_t (&w)[4], const ZfpTables& tb, uint32_t (&u)[16],
                                                            int& e) {
   constexpr int CAP = ZBits<RATE>::kCap;
@@ -309,9 +326,20 @@ __host__ __device__ __forceinline__ void zfp_decode_planes(const uint32_t (&w)[4
       if (P0 - 7 + p >= 0 && o < CAP) {
         const uint64_t win = st.window(o);
         uint32_t x;
-        if (n == 16) {
-          x = uint32_t(win) & 0xFFFFu;
-          o += 16;
+        if (all_lanes<WAVE>(n >= 14)) {
+          // at most two candidates left.  n >= 15: the plane's 16 bits (for n = 15 the last
+          // candidate's test bit is its bit; a 1 read inside the budget implies the 1).  n = 14:
+          // test bit t; after a 1, coefficient 14's bit r0, and after a 1 there the test r1 for
+          // coefficient 15 (its 1 implied); after r0 = 0 coefficient 15's 1 is implied if r0 lay
+          // inside the budget
+          const uint32_t wl = uint32_t(win);
+          const uint32_t t = (wl >> 14) & 1u, r0 = (wl >> 15) & 1u, r1 = (wl >> 16) & 1u;
+          const uint32_t V = wl & 0x3FFFu;
+          const bool fits = o + 16 <= CAP, two = n == 14;
+          const uint32_t x14 = !t ? V : (r0 ? (V | (1u << 14) | (r1 << 15)) : (V | (fits ? 1u << 15 : 0u)));
+          x = two ? x14 : (wl & 0xFFFFu);
+          o += two ? (!t ? 15 : (r0 ? 17 : 16)) : 16;
+          n = two ? (!t ? 14 : (r0 ? (r1 ? 16 : 15) : 16)) : (((wl >> 15) & 1u) ? 16 : n);
         } else {
           const uint32_t V = uint32_t(win) & ((1u << n) - 1u);
           const uint32_t rest = uint32_t(win >> (n + 1));
@@ -332,16 +360,17 @@ __host__ __device__ __forceinline__ void zfp_decode_planes(const uint32_t (&w)[4
           const uint32_t y = uint32_t(tb.unspread[dm & 0xFFu]) | (uint32_t(tb.unspread[(dm >> 8) & 0xFFu]) << (8 - pc0)) |
                              (uint32_t(tb.unspread[(dm >> 16) & 0xFFu]) << (16 - pc1)) |
                              (uint32_t(tb.unspread[dm >> 24]) << (24 - pc2));
-          const int L = 15 - n;  // explicit candidates before the last one
+          const int L = 15 - n;  // explicit candidates before the last one (n < 16 here)
           const bool implied = dcount > L;
           const uint32_t yl = y & ((1u << L) - 1u);
           const int glen = implied ? 1 + L + __builtin_popcount(yl) : e1 + 2;
           const bool fits = o + n + glen <= CAP;
           const uint32_t yn = implied ? (yl | (fits ? 1u << L : 0u)) : y;
           const bool t0 = (uint32_t(win) >> n) & 1u;  // n < 16
-          x = t0 ? V | (yn << n) : V;
-          o += t0 ? n + glen : n + 1;
-          n = t0 ? (implied ? 16 : n + dcount) : n;
+          const bool all = n == 16;  // lanes whose candidates are all significant: 16 verbatim bits
+          x = all ? (uint32_t(win) & 0xFFFFu) : (t0 ? V | (yn << n) : V);
+          o += all ? 16 : (t0 ? n + glen : n + 1);
+          n = all ? 16 : (t0 ? (implied ? 16 : n + dcount) : n);
         }
         xp[p >> 1] |= x << (16 * (p & 1));
       }
@@ -364,11 +393,11 @@ __host__ __device__ __forceinline__ void zfp_decode_finish(const uint32_t (&u)[1
   for (int k = 0; k < 16; ++k) v[k] = ldexpf(float(q[k]), e - 30);
 }
 
-template <int RATE>
+template <int RATE, bool WAVE = true>
 __host__ __device__ __forceinline__ void zfp_decode_block(const uint32_t (&w)[4], const ZfpTables& tb, float (&v)[16]) {
   uint32_t u[16];
   int e;
-  zfp_decode_planes<RATE>(w, tb, u, e);
+  zfp_decode_planes<RATE, WAVE>(w, tb, u, e);
   zfp_decode_finish(u, e, v);
 }
 
