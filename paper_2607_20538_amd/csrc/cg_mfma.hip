@@ -679,11 +679,19 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
   bf16x8_t A[NP][KS];
   load_a<NP, KS>(A, a, l, h, chA, kbase, hc);  // a.gp holds the G^T planes for decode
 
-  // Centring: with groups no smaller than blocks every block is centred on its grid midpoint
-  // (code 2^(b-1)); with groups smaller than blocks (only g <= 32) every (token, group) is
-  // centred on the code of the group's first channel, so a group whose codes are all equal
-  // decodes from the midpoint term alone.
-  const bool gc = KS == 2 && a.g < NB;
+  // Centring.  Groups smaller than blocks (g <= 32, or g = 64 in 128-channel tiles): every
+  // (token, group) is centred on the code of the group's first channel, so a group whose codes
+  // are all equal decodes from the centre term alone.  Token-channel tiles with groups no
+  // smaller than blocks: every (token, block) is centred on the token's first code of the block.
+  // Either way the centre is a value of the token itself, so the centre term and the matrix-core
+  // sums of the offsets q - c stay of the order of the token's own values; a tile's range is set
+  // by 16 tokens, and centring its tokens on the tile's midpoint instead lets the two terms
+  // cancel to far below their size for a token far from that midpoint.  Other blocks (one
+  // token's channels) are centred on their grid midpoint (code 2^(b-1)).
+  const bool gc = a.g < NB;
+  const bool bc = TB > 1 && !gc;
+  const int gsegs = a.g >> 4;      // 16-channel staging segments per group (g >= 16)
+  constexpr int BSEGS = NB / 16;   // staging segments per block
   // column sums: per block (colsum[k][i] = sum_{j in block k} G[j][i]) or, when centring per
   // group, per group (colsum[0][i] = sum_{j in group(i)} G[j][i]), of the same split planes
   // the matrix core multiplies
@@ -714,8 +722,10 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
 #pragma unroll
     for (int i = 0; i + 1 < SEGW; ++i) cw[i] = __builtin_amdgcn_alignbit(cw[i + 1], cw[i], bit0 & 31);
     sw = a.side[crow / TB * NBK + st_blk];  // the token's block, or its tile's
-    // first code of a 32-channel group that starts in the previous segment (word aligned)
-    if (gc && a.g == 32 && (st_seg & 1)) cfirst = row[(32 * (st_seg >> 1) * BITS) >> 5] & ((1u << BITS) - 1u);
+    // first code of a 32- or 64-channel group, or of a tile block, that starts in an earlier
+    // segment (word aligned)
+    if (gc && a.g >= 32 && st_seg % gsegs) cfirst = row[(a.g * (st_seg / gsegs) * BITS) >> 5] & ((1u << BITS) - 1u);
+    if (bc && st_seg % BSEGS) cfirst = row[(NB * st_blk * BITS) >> 5] & ((1u << BITS) - 1u);
   };
   auto put = [&](int buf) {
     uint32_t q[16];
@@ -729,8 +739,11 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
     // centre of the first and second half of the segment
     int c0 = 1 << (BITS - 1), c1 = c0;
     if (gc) {
-      c0 = (a.g == 32 && (st_seg & 1)) ? int(cfirst) : int(q[0]);
+      c0 = (a.g >= 32 && st_seg % gsegs) ? int(cfirst) : int(q[0]);
       c1 = a.g == 8 ? int(q[8]) : c0;
+    } else if (bc) {
+      c0 = st_seg % BSEGS ? int(cfirst) : int(q[0]);
+      c1 = c0;
     }
     uint32_t v[8];
 #pragma unroll
@@ -752,9 +765,11 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
         mtile[buf][st_tok][2 * st_seg + 1] = mn + float(c1) * sc;
       } else if (a.g == 16) {
         mtile[buf][st_tok][st_seg] = mn + float(c0) * sc;
-      } else if ((st_seg & 1) == 0) {
-        mtile[buf][st_tok][st_seg >> 1] = mn + float(c0) * sc;
+      } else if (st_seg % gsegs == 0) {
+        mtile[buf][st_tok][st_seg / gsegs] = mn + float(c0) * sc;
       }
+    } else if (bc && st_seg % BSEGS == 0) {
+      mtile[buf][st_tok][st_blk] = f16_bits_to_f32(sw & 0xffffu) + float(c0) * f16_bits_to_f32(sw >> 16);
     }
   };
 
@@ -810,7 +825,7 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
       const int blk = (kbase + 16 * SEG * sgi) / NB;
       const uint32_t swd = stile[buf][n * NBK + blk];
       const float sc = f16_bits_to_f32(swd >> 16);
-      if (gc) {
+      if (gc || bc) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) y[e] = fmaf(sc, acc0[e] + acc1[e], y[e]);
       } else {
@@ -842,6 +857,21 @@ __global__ __launch_bounds__(kThreads, 2) void dec_mfma(MfmaArgs a) {
         for (int u = 0; u < 4; ++u) {
           const int e = 4 * q4 + u;
           y[e] = fmaf(e < 8 ? m0 : m1, cc[u], y[e]);
+        }
+      }
+    } else if (bc) {
+      // centre terms of the row's blocks (column sums of blocks outside its group are zero)
+      const int ch0 = 32 * w + 16 * hc;
+#pragma unroll
+      for (int k = 0; k < NBK; ++k) {
+        const float mk = mtile[buf][n][k];
+        const float4* cs = (const float4*)&colsum[k][ch0];
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 c = cs[q4];
+          const float cc[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) y[4 * q4 + u] = fmaf(mk, cc[u], y[4 * q4 + u]);
         }
       }
     }
@@ -959,11 +989,10 @@ constexpr int kDStages = 8;  // decoder LDS ring of code and side tiles (fewer f
 // Every wave issues exactly two loads per tile (codes, side words) and GPR stores per flush
 // (lanes past the written range repeat a live granule), so the number of vector-memory
 // operations younger than a tile's loads is known and waited for exactly.
-template <int NP, int KS, int BITS, int NB, bool OUT_BF16, int TB = 1>
+template <int NP, int KS, int BITS, int NB, bool OUT_BF16>
 __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a) {
   constexpr int RB = kD * BITS / 8;                  // code bytes per token row
-  constexpr int NBK = kD / NB;                       // side words per token row (per tile)
-  static_assert(TB == 1 || TB == 16, "token-channel tiles of 16 tokens");
+  constexpr int NBK = kD / NB;                       // side words per token row
   constexpr int SEG = (16 * KS < NB ? 16 * KS : NB) / 16;  // K-steps per block segment
   constexpr int NSEG = KS / SEG;
   constexpr int RW = SEG * BITS / 4;                 // packed words of a lane's region
@@ -985,7 +1014,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
   const int h = slice % a.H, b = (slice / a.H) % a.B, lv = slice / (a.H * a.B);
   const int l = lv + a.l0;
   int Tv = a.T;
-  int held = a.kivi || TB > 1 ? a.len : INT_MAX;  // positions the cache holds
+  int held = a.kivi ? a.len : INT_MAX;  // positions the cache holds
   if (a.pos) {
     if (!row_held(a, b, chunk, held)) return;
     Tv = min(Tv, held - a.t0);
@@ -997,9 +1026,8 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
   char* ys = a.x + YB * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
   const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
   const size_t crow0 = cslice * size_t(a.T_cap) + a.t0;
-  // KIVI / tiles: the quantised view rows [0, Tq) go through the pipeline, the window or
-  // staged rows after it
-  const int Tq = a.kivi ? kivi_quantised_rows(a, held, Tv) : (TB > 1 ? max(0, min(Tv, held / TB * TB - a.t0)) : Tv);
+  // KIVI: the quantised view rows [0, Tq) go through the pipeline, the window after it
+  const int Tq = a.kivi ? kivi_quantised_rows(a, held, Tv) : Tv;
   const int te = min(te_all, (Tq + kTok - 1) / kTok);
   if (tb >= te) {
     ring_rows<OUT_BF16>(a, cslice, ys, max(Tq, tb * kTok), min(Tv, te_all * kTok));
@@ -1034,14 +1062,7 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
     if (lane < 8 * BITS)
       __builtin_amdgcn_global_load_lds(a.codes + (row0 + min(cgrow, last)) * RB + 16 * cgpart,
                                        (__attribute__((address_space(3))) void*)(ctile[st] + 16 * 8 * BITS * w), 16, 0, 0);
-    if constexpr (TB > 1) {
-      // the (at most three) tiles the 32 rows touch, into this wave's own slots; tiles past
-      // the quantised rows repeat the last one
-      const size_t blk0 = row0 / TB, blast = (row0 + last) / TB;
-      if (lane < 3 * NBK)
-        __builtin_amdgcn_global_load_lds(a.side + min(blk0 + lane / NBK, blast) * NBK + lane % NBK,
-                                         (__attribute__((address_space(3))) void*)(stile[st] + 3 * NBK * w), 4, 0, 0);
-    } else if (lane < 8 * NBK) {
+    if (lane < 8 * NBK) {
       __builtin_amdgcn_global_load_lds(a.side + (row0 + min(swrow, last)) * NBK + swk,
                                        (__attribute__((address_space(3))) void*)(stile[st] + 8 * NBK * w), 4, 0, 0);
     }
@@ -1103,15 +1124,8 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
     if (t + DS - 1 < te) issue(t + DS - 1);
     const int st = (t - tb) % DS;
     uint32_t sw[NBK];
-    if constexpr (TB > 1) {
-      const size_t row0 = crow0 + size_t(t) * kTok;
-      const int bi = int((row0 + n) / TB - row0 / TB);
 #pragma unroll
-      for (int k = 0; k < NBK; ++k) sw[k] = stile[st][3 * NBK * w + bi * NBK + k];
-    } else {
-#pragma unroll
-      for (int k = 0; k < NBK; ++k) sw[k] = stile[st][n * NBK + k];
-    }
+    for (int k = 0; k < NBK; ++k) sw[k] = stile[st][n * NBK + k];
     float y[16];
 #pragma unroll
     for (int sgi = 0; sgi < NSEG; ++sgi) {
@@ -1200,17 +1214,20 @@ constexpr int keys_stages(int bits, bool bf16) {
   return room / stage > kDStages ? kDStages : room / stage;
 }
 
-// One tile is one key group (cache positions 32k .. 32k + 31); with gauge groups of at most 32
-// channels, wave w's contraction runs over its own 32 channels, so each wave dequantises
-// exactly the codes it multiplies.  Lane (n, hc) rebuilds zhat = fl(mn + q sc) of token n for
-// its 16 K-channels in binary32 (the dequantised value itself), splits it into three bf16
-// planes (exact: a binary32 value holds 24 significant bits), and the matrix core multiplies
-// them by the two G^T planes (plane products below 2^-24 of the leading term dropped).  The
-// error is thus relative to the group norm of zhat, whatever the channels' offsets; with the
-// identity gauge the result is zhat bit for bit.
+// One tile is one key group (cache positions 32k .. 32k + 31).  Wave w's contraction runs over
+// the gauge group(s) of its 32 output channels: its own 32 channels for groups of at most 32
+// (KS = 2), the 64 or 128 channels of its group otherwise (KS = 4, 8), each wave then
+// dequantising every code it multiplies (the code block is in LDS; the waves of a 64- or
+// 128-channel group repeat that work rather than exchange it behind a second barrier).  Lane
+// (n, hc) rebuilds zhat = fl(mn + q sc) of token n for its K-channels in binary32 (the
+// dequantised value itself), splits it into three bf16 planes (exact: a binary32 value holds
+// 24 significant bits), and the matrix core multiplies them by the two G^T planes (plane
+// products below 2^-24 of the leading term dropped).  The error is thus relative to the group
+// norm of zhat, whatever the channels' offsets; with the identity gauge the result is zhat bit
+// for bit.
 template <int NP, int KS, int BITS, bool OUT_BF16>
 __global__ __launch_bounds__(kThreads, OUT_BF16 ? 3 : 2) void dec_keys(MfmaArgs a) {
-  static_assert(KS == 2 && NP == 2, "groups of at most 32 channels, two gauge planes");
+  static_assert((KS == 2 || KS == 4 || KS == 8) && NP == 2, "K-steps of a gauge group, two gauge planes");
   constexpr int CB = 4 * BITS;                       // bytes of one channel's 32 codes
   constexpr int YB = OUT_BF16 ? 2 : 4;
   constexpr int GPR = kD * YB / 16;
@@ -1253,7 +1270,7 @@ __global__ __launch_bounds__(kThreads, OUT_BF16 ? 3 : 2) void dec_keys(MfmaArgs 
     return;
   }
 
-  const int kbase = 32 * w;  // groups of at most 32 channels: the wave's own channels
+  const int kbase = (32 * w) & ~(16 * KS - 1);  // first channel of the wave's gauge group(s)
   const int chA = 32 * w + 16 * ((n >> 2) & 1) + 4 * (n >> 3) + (n & 3);
   bf16x8_t A[NP][KS];
   load_a<NP, KS>(A, a, l, h, chA, kbase, hc);  // rows chA of the G^T planes, natural K order
@@ -1603,11 +1620,11 @@ void* enc_by_bits(int bits, int nb, int mode, int bt) {
   return nullptr;
 }
 
-// (token-channel tiles: blocks of 64 or 128 channels over groups of at most 32, centred per
-// (token, group))
+// (token-channel tiles: blocks of 64 or 128 channels, centred per (token, group) or per
+// (token, block))
 template <int KS, int BITS, int NB>
 void* dec_kernel(bool bf16, int bt) {
-  if constexpr (KS == 2 && NB >= 64) {
+  if constexpr (NB >= 64) {
     if (bt == 16) {
       if (bf16) return (void*)dec_mfma<kNP, KS, BITS, NB, true, 16>;
       return (void*)dec_mfma<kNP, KS, BITS, NB, false, 16>;
@@ -1648,18 +1665,11 @@ void* dec_by_bits(int bits, int nb, bool bf16, int bt) {
 int ksteps(int g) { return g >= 128 ? 8 : (g == 64 ? 4 : 2); }
 
 // dec_fast variants exist where a lane's code region is whole words and a wave's K range
-// holds at most two blocks
-// (token-channel tiles: blocks of 64 or 128 channels inside the gauge group)
+// holds at most two blocks (one token's blocks; token-channel tiles take the centred decoder)
 template <int KS, int BITS, int NB>
 void* fast_kernel(bool bf16, int bt) {
   constexpr int SEG = (16 * KS < NB ? 16 * KS : NB) / 16;
   if constexpr (SEG * BITS % 4 == 0 && KS / SEG <= 2) {
-    if constexpr (NB >= 64 && 16 * KS >= NB) {
-      if (bt == 16) {
-        if (bf16) return (void*)dec_fast<kNP, KS, BITS, NB, true, 16>;
-        return (void*)dec_fast<kNP, KS, BITS, NB, false, 16>;
-      }
-    }
     if constexpr (NB <= 64) {
       if (bt == 1) {
         if (bf16) return (void*)dec_fast<kNP, KS, BITS, NB, true>;
@@ -1693,19 +1703,20 @@ void* fast_by_bits(int bits, int nb, bool bf16, int bt) {
   return nullptr;
 }
 
-template <int BITS>
+template <int KS, int BITS>
 void* keys_kernel(bool bf16) {
-  if (bf16) return (void*)dec_keys<kNP, 2, BITS, true>;
-  return (void*)dec_keys<kNP, 2, BITS, false>;
+  if (bf16) return (void*)dec_keys<kNP, KS, BITS, true>;
+  return (void*)dec_keys<kNP, KS, BITS, false>;
 }
 
+template <int KS>
 void* keys_by_bits(int bits, bool bf16) {
   switch (bits) {
-    case 2: return keys_kernel<2>(bf16);
-    case 3: return keys_kernel<3>(bf16);
-    case 4: return keys_kernel<4>(bf16);
-    case 6: return keys_kernel<6>(bf16);
-    case 8: return keys_kernel<8>(bf16);
+    case 2: return keys_kernel<KS, 2>(bf16);
+    case 3: return keys_kernel<KS, 3>(bf16);
+    case 4: return keys_kernel<KS, 4>(bf16);
+    case 6: return keys_kernel<KS, 6>(bf16);
+    case 8: return keys_kernel<KS, 8>(bf16);
   }
   return nullptr;
 }
@@ -1731,10 +1742,10 @@ bool mfma_decode_supported(int s, const ViewDev& Y, const GaugeDev& G, const Cod
   if (Y.d != kD || !group_ok(G.g) || !bits_ok(c.bits)) return false;
   if (c.backend == CG_BACKEND_ZFP) return true;
   if (c.backend == CG_BACKEND_BLOCK_UNIFORM && c.bt != 1)  // tiles: blocks inside a group, or centred groups
-    return c.bt == 16 && (c.n == 64 || c.n == 128) && (G.g >= c.n || G.g <= 32);
+    return c.bt == 16 && (c.n == 64 || c.n == 128);
   if (c.backend == CG_BACKEND_KIVI) {
     if (c.win % kTok) return false;
-    if (s == 0) return c.kg == kTok && G.g <= 32;  // key groups, gauge groups within one K-step pair
+    if (s == 0) return c.kg == kTok;  // one tile per key group
     return c.kvc == 16 || c.kvc == 32 || c.kvc == 64;  // values: block-uniform rows
   }
   return c.backend == CG_BACKEND_BLOCK_UNIFORM && (c.n == 16 || c.n == 32 || c.n == 64);
@@ -1796,7 +1807,12 @@ hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& 
   m.ring_slots = bt > 1 ? bt : c.win + c.kg;
   if (m.kivi && s == 0) {
     // one tile per 32-position key group: the first may start before t0
-    void* fn = keys_by_bits(c.bits, Y.bf16);
+    void* fn = nullptr;
+    switch (ksteps(G.g)) {
+      case 2: fn = keys_by_bits<2>(c.bits, Y.bf16); break;
+      case 4: fn = keys_by_bits<4>(c.bits, Y.bf16); break;
+      case 8: fn = keys_by_bits<8>(c.bits, Y.bf16); break;
+    }
     if (!fn) return hipErrorInvalidValue;
     plan(m, Y.L * Y.B * Y.H, t0 % kTok + Y.T, fn);
     const int nwg = ((m.nslices * m.chunks + 7) / 8) * 8;
@@ -1818,8 +1834,8 @@ hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& 
   }
   const int nb = m.kivi ? c.kvc : c.n;
   void* fn = nullptr;
-  if (G.g >= nb) {
-    // blocks inside one group: codes feed the matrix core without conversion
+  if (G.g >= nb && bt == 1) {
+    // blocks (of one token) inside one group: codes feed the matrix core without conversion
     switch (ksteps(G.g)) {
       case 2: fn = fast_by_bits<2>(c.bits, nb, Y.bf16, bt); break;
       case 4: fn = fast_by_bits<4>(c.bits, nb, Y.bf16, bt); break;

@@ -222,11 +222,12 @@ def test_kivi_short_cache_decodes_as_a_copy(kernels):
         np.testing.assert_array_equal(_decode_gpu(dev, s, Gd, shp, oc, 0, T), X)
 
 
-@pytest.mark.parametrize("g", [8, 32])
+@pytest.mark.parametrize("g", [8, 32, 64, 128])
 @pytest.mark.parametrize("bits", [2, 3, 4, 6, 8])
 def test_kivi_key_decoder(g, bits):
-    """Key groups through the matrix-core key decoder (gauge groups of at most 32 channels)
-    at every width: binary32 out within the gauge tolerance of the oracle, bf16 out within a
+    """Key groups through the matrix-core key decoder (gauge groups inside a wave's 32 channels,
+    or 64 / 128-channel groups whose every wave dequantises the group's codes) at every width:
+    binary32 out within the gauge tolerance of the oracle, bf16 out within a
     bf16 ulp, window rows copied exactly, and sub-range decodes that start inside a key group
     or cover a single row agree with the full decode."""
     T, T_cap = 300, 320
@@ -302,7 +303,7 @@ def test_tile_quantise_and_dequantise_are_bit_exact(bits, n, bt, kernels):
             np.testing.assert_array_equal(out, ref)
 
 
-@pytest.mark.parametrize("g", [8, 32, 128])
+@pytest.mark.parametrize("g", [8, 32, 64, 128])
 @pytest.mark.parametrize("bits,n,bt", TILE_CASES[:3])
 def test_tile_fused_encoder_and_decoder(g, bits, n, bt, kernels):
     T, T_cap = 277, 288

@@ -86,8 +86,10 @@ CASES = [
     ("bu-g8-b6", O.BLOCK_UNIFORM, 8, 6, 64, 1),
     ("bu-g64-b4-n32", O.BLOCK_UNIFORM, 64, 4, 32, 1),
     ("kivi-g32-b3", O.KIVI, 32, 3, 64, 1),
+    ("kivi-g128-b4", O.KIVI, 128, 4, 64, 1),
     ("tile-g128-b4", O.BLOCK_UNIFORM, 128, 4, 128, 16),
     ("tile-g32-b3", O.BLOCK_UNIFORM, 32, 3, 64, 16),
+    ("tile-g64-b4-n128", O.BLOCK_UNIFORM, 64, 4, 128, 16),
     ("zfp-g128-r4", O.ZFP, 128, 4, 64, 1),
     ("pass-g128", O.PASSTHROUGH, 128, 8, 64, 1),
 ]
