@@ -37,7 +37,7 @@ def parse():
                     help="HBM traffic per launch measured with rocprofv3 counters (optional)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the timed region, run one plain 512 MiB device copy (counter calibration)")
-    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral", "grad", "attend", "attend_paged", "attend_tiles", "zfp"]),
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(["llama8b", "kivi", "rolling", "gemma27b", "tiles", "spectral", "grad", "attend", "attend_paged", "attend_tiles", "attend_kivi", "zfp"]),
                     help="llama8b (default) prints the headline line; the others print per-kernel timings of "
                          "the KIVI, rolling-step and 27B-sweep workloads")
     return ap.parse_args()
@@ -186,15 +186,19 @@ def workload_cpu_baseline(name, w, gpu):
         return {"value": round(elems * 2 / t_total / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
                 "sample": f"layer 0, batch row 0 ({w.H} heads x {w.T} tokens) of K and V at g = {g}, "
                           f"{bits} bits ({elems} elements), encode + decode, {t_total:.1f} s single-threaded"}
-    if name in ("rolling", "attend", "attend_tiles", "attend_paged"):
+    if name in ("rolling", "attend", "attend_tiles", "attend_paged", "attend_kivi"):
         # one (layer, batch row): its history encoded (untimed), then the step's work for it timed:
         # append one token to K and V and decode the history (rolling), or attention of its grp = 4
         # query heads per KV head over the history (attention steps; the oracle has no page table,
         # so paged caches are timed as the contiguous ones they are equivalent to)
         bt = 16 if name == "attend_tiles" else 1
-        oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=w.bits, block_c=w.block_c, block_t=bt)
+        if name == "attend_kivi":
+            oc = O.Codec(backend=O.KIVI, bits=w.bits, block_c=64, key_tokens=w.key_tokens,
+                         val_channels=w.val_channels, residual=w.residual)
+        else:
+            oc = O.Codec(backend=O.BLOCK_UNIFORM, bits=w.bits, block_c=w.block_c, block_t=bt)
         G = O.gauge_make(O.GAUGE_HAAR, 1, w.H, w.d, w.g, seed=w.gauge_seed)
-        T_cap = w.T + 16
+        T_cap = w.T + 32
         caches = []
         for s in (0, 1):
             X = synth.kv_tensor(w, s, L=1, B=1)
@@ -291,7 +295,9 @@ def other_workload(name, steps, warmup, cpu=True, probe=False):
 
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral", "grad", "zfp") else ("rolling" if name in ("attend", "attend_paged", "attend_tiles") else name)]
+    w = synth.WORKLOADS["llama8b" if name in ("tiles", "spectral", "grad", "zfp") else
+                        ("rolling" if name in ("attend", "attend_paged", "attend_tiles") else
+                         ("kivi" if name == "attend_kivi" else name))]
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     out = {"workload": name, "shape": {"L": w.L, "B": w.B, "H": w.H, "T": w.T, "d": w.d}, "steps": steps,
            "kernels": os.environ.get("CG_KERNELS") or "default"}
@@ -454,18 +460,22 @@ def other_workload(name, steps, warmup, cpu=True, probe=False):
         out["page_size"] = P
         out["query_heads"] = w.H * grp
         out["attend_GBps"] = round(w.L * w.B * w.H * held * per_pos / ms_att / 1e6, 1)
-    elif name in ("attend", "attend_tiles"):
+    elif name in ("attend", "attend_tiles", "attend_kivi"):
         # the rolling step with the history consumed by fused decode-phase attention instead of
         # being decoded to bf16: append one token per (layer, b, h), then attention of the
         # grp = 4 query heads of every KV head (32 query heads over 8 KV heads) over the history;
-        # attend_tiles: one range per 16 tokens x 64 channels (appends stage the unfinished tile)
+        # attend_tiles: one range per 16 tokens x 64 channels (appends stage the unfinished tile);
+        # attend_kivi: the KIVI-style cache of the KIVI workload (3 bits, g = 32, 128-token window)
         grp = 4
         bt = 16 if name == "attend_tiles" else 1
         shp = cg.shape(w.L, w.H, w.d, w.g)
-        codec = cg.Codec(cg.BLOCK_UNIFORM, w.bits, w.block_c, block_t=bt)
+        if name == "attend_kivi":
+            codec = cg.Codec(cg.KIVI, w.bits, 64, w.key_tokens, w.val_channels, w.residual)
+        else:
+            codec = cg.Codec(cg.BLOCK_UNIFORM, w.bits, w.block_c, block_t=bt)
         Gd = cg.alloc_gauge(shp)
         cg.gauge_make(cg.GAUGE_HAAR, shp, seed=w.gauge_seed, G_host=None, G_dev=Gd)
-        T_cap = (w.T + warmup + 2 * steps + 1 + 15) // 16 * 16
+        T_cap = (w.T + warmup + 2 * steps + 1 + 31) // 32 * 32
         caches, news = [], []
         for s in (0, 1):
             X = layer_view(s)

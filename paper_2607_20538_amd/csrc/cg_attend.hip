@@ -588,15 +588,18 @@ __device__ __forceinline__ void split2(float v, uint32_t& hi, uint32_t& lo) {
   lo = f32_to_bf16_rne(v - bf16_to_f32(hi));
 }
 
-template <int BITS, int NBLK, int TB>
+template <int BITS, int NBLK, int TB, bool KIVI = false>
 __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G) {
   static_assert(TB == 1 || TB == 16, "token tiles of 16");
+  static_assert(!KIVI || (TB == 1 && NBLK == 2), "KIVI: 32-position key groups, 64-channel value blocks");
+  constexpr bool RAW = TB > 1 || KIVI;         // raw bf16 positions after the quantised ones
   constexpr int JQ = 8 / NBLK;                 // query heads per workgroup (16 A rows)
   constexpr int NQL = 2 / NBLK;                // queries per D lane
   constexpr int NB = kD / NBLK;                // channels per block
   constexpr int RB = kD * BITS / 8;            // code bytes per row
   constexpr float kSK = BITS == 8 ? 1.0f : (BITS == 6 ? 128.0f : float(1 << BITS));  // code_frag scale
   constexpr float kSV = BITS == 8 ? 1.0f : float(1 << BITS);                           // vfrag scale
+  constexpr float kSK2 = BITS == 8 ? 1.0f : float(1 << BITS);                          // KIVI key scale
   __shared__ __attribute__((aligned(16))) float qt[JQ][kD];
   __shared__ __attribute__((aligned(16))) float macc[JQ][kD];
   __shared__ float qsum[JQ][NBLK];
@@ -606,11 +609,17 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
   __shared__ float offs[4][16][4];
   __shared__ float ml[4][2][JQ];
   __shared__ float mm[2][JQ];
-  // staged raw positions (tiles): scores then weights, per-query maximum and sum, value sums
-  constexpr int RJ = TB > 1 ? JQ : 1;
+  // raw positions (staged tile tokens, the KIVI window): scores then weights of a chunk of 16,
+  // running maximum and sum per query, the chunk's rescaling factor, value sums
+  constexpr int RJ = RAW ? JQ : 1;
   __shared__ float rs[RJ][16];
   __shared__ float rml[2][RJ];
-  __shared__ __attribute__((aligned(16))) float accr[RJ][TB > 1 ? kD : 1];
+  __shared__ float rfac[RJ];
+  __shared__ __attribute__((aligned(16))) float accr[RJ][RAW ? kD : 1];
+  // KIVI keys: the step's key group in a per-wave region (channel c's 32 codes in words
+  // [c BITS, c BITS + BITS), its side word)
+  __shared__ __attribute__((aligned(16))) uint32_t kgc[KIVI ? 4 : 1][KIVI ? kD * BITS : 1];
+  __shared__ __attribute__((aligned(16))) uint32_t kgs[KIVI ? 4 : 1][KIVI ? kD : 1];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n = lane & 15, gq = lane >> 4;
@@ -631,8 +640,9 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
   int held = a.lens ? a.lens[b] : a.len;
   if (held < 0 || held > a.cap) held = 0;
   const int t_begin = sp * a.chunk, t_end = min(held, t_begin + a.chunk);
-  // positions in whole tiles go through the matrix cores, the staged ones after them are raw
-  const int tq = TB > 1 ? held / TB * TB : held;
+  // positions in whole tiles / key groups go through the matrix cores, the staged tile tokens
+  // or the KIVI window after them are raw
+  const int tq = KIVI ? (held < a.win ? 0 : (held - a.win) / 32 * 32) : (TB > 1 ? held / TB * TB : held);
   const int t_endq = min(t_end, tq);
 
   // 1. queries: macc <- q, qt <- scale G_K q, qsum <- the per-block sums of its two planes
@@ -672,7 +682,7 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
 
   // 2. score A fragments: row m = n -> (query, block, plane), region 32 gq
   bf16x8_t AK[4];
-  {
+  if constexpr (!KIVI) {
     const int j = n / (2 * NBLK), blk = (n / 2) % NBLK, plane = n & 1;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -696,6 +706,15 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
   }
   // value A rows: row m = n -> (query jw, block bw, plane pw)
   const int jw = n / (2 * NBLK), bw = (n / 2) % NBLK, pw = n & 1;
+  // KIVI score rows use the same (query, block, plane) mapping: row n holds qt of its query at the
+  // 16 channels 64 bw + 32 v + 8 gq + i (K-steps 2 bw + v), zero at the other K-steps
+  float qk[KIVI ? 16 : 1];
+  if constexpr (KIVI) {
+#pragma unroll
+    for (int v = 0; v < 2; ++v)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) qk[8 * v + i] = qt[jw][64 * bw + 32 * v + 8 * gq + i];
+  }
 
   float mrun[NQL], lp[NQL];
 #pragma unroll
@@ -737,15 +756,26 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
     // loads: key regions of tokens t0 + 16 sb + n, value chunks of tokens t0 + 8 gq + e
     uint32_t rk[2][BITS];
     uint32_t swk[2][NBLK];
+    uint2 kcv[KIVI ? BITS : 1], ksv;
+    if constexpr (KIVI) {
+      // the step's key group (t0 is a multiple of 32): codes and side words of channels 2 lane,
+      // 2 lane + 1
+      const size_t gi = sslc * size_t(a.kc.T_cap / 32) + size_t(t0 - poff) / 32;
+      const uint2* src = reinterpret_cast<const uint2*>(a.kc.codes + (gi * kD + 2 * lane) * (4 * BITS));
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      const uint32_t* src = reinterpret_cast<const uint32_t*>(
-          kb + (FULL ? koff + 16u * sb * RB : uint32_t(clampt(16 * sb + n)) * RB + uint32_t(gq) * BITS * 4));
+      for (int i = 0; i < BITS; ++i) kcv[i] = src[i];
+      ksv = *reinterpret_cast<const uint2*>(a.kc.side + gi * kD + 2 * lane);
+    } else {
 #pragma unroll
-      for (int i = 0; i < BITS; ++i) rk[sb][i] = src[i];
-      const uint32_t* sd = ksd + uint32_t(clampt(16 * sb + n) / TB) * NBLK;
+      for (int sb = 0; sb < 2; ++sb) {
+        const uint32_t* src = reinterpret_cast<const uint32_t*>(
+            kb + (FULL ? koff + 16u * sb * RB : uint32_t(clampt(16 * sb + n)) * RB + uint32_t(gq) * BITS * 4));
 #pragma unroll
-      for (int k = 0; k < NBLK; ++k) swk[sb][k] = sd[k];
+        for (int i = 0; i < BITS; ++i) rk[sb][i] = src[i];
+        const uint32_t* sd = ksd + uint32_t(clampt(16 * sb + n) / TB) * NBLK;
+#pragma unroll
+        for (int k = 0; k < NBLK; ++k) swk[sb][k] = sd[k];
+      }
     }
     uint32_t vw0[8], vw1[8];
 #pragma unroll
@@ -767,6 +797,90 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
 
     // scores of the two 16-token halves
     float s[2][NQL];
+    if constexpr (KIVI) {
+      // the group to the wave's LDS region
+      uint2* dc = reinterpret_cast<uint2*>(&kgc[w][2 * lane * BITS]);
+#pragma unroll
+      for (int i = 0; i < BITS; ++i) dc[i] = kcv[i];
+      *reinterpret_cast<uint2*>(&kgs[w][2 * lane]) = ksv;
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      // A: a = qt sc of the row's channels as two bf16 planes (the row keeps plane pw); the
+      // codes enter as B = 1 + q 2^-b (8 bits: q), so with k = 2^b (8 bits: 1)
+      //   s_t = sum_c qt_c (mn_c + q_tc sc_c) = k (sum_c a_c B_tc + part),
+      //   part = sum_c qt_c mn_c / k - sum_c a_c   (8 bits: sum_c qt_c mn_c),
+      // each row adding its own terms of part (the mn term on plane-0 rows, each plane's entries
+      // of a on its own rows); part enters through one more product, its three bf16 planes
+      // against a B of ones, which sums the four lane groups of each row
+      u32x4_t fa[2];
+      float part = 0.0f;
+#pragma unroll
+      for (int v = 0; v < 2; ++v) {
+        const int c0 = 64 * bw + 32 * v + 8 * gq;
+        const u32x4_t sa = *reinterpret_cast<const u32x4_t*>(&kgs[w][c0]);
+        const u32x4_t sb4 = *reinterpret_cast<const u32x4_t*>(&kgs[w][c0 + 4]);
+        const uint32_t se[8] = {sa[0], sa[1], sa[2], sa[3], sb4[0], sb4[1], sb4[2], sb4[3]};
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2) {
+          const float q0 = qk[8 * v + 2 * e2], q1 = qk[8 * v + 2 * e2 + 1];
+          const float x0 = q0 * f16_bits_to_f32(se[2 * e2] >> 16), x1 = q1 * f16_bits_to_f32(se[2 * e2 + 1] >> 16);
+          const uint32_t hi = pk_bf16(x0, x1);
+          const float h0 = __uint_as_float(hi << 16), h1 = __uint_as_float(hi & 0xffff0000u);
+          const uint32_t lo = pk_bf16(x0 - h0, x1 - h1);
+          fa[v][e2] = pw ? lo : hi;
+          if (pw == 0) {
+            part = fmaf(q0, f16_bits_to_f32(se[2 * e2] & 0xffffu) * (1.0f / kSK2), part);
+            part = fmaf(q1, f16_bits_to_f32(se[2 * e2 + 1] & 0xffffu) * (1.0f / kSK2), part);
+            if constexpr (BITS != 8) part -= h0 + h1;
+          } else if constexpr (BITS != 8) {
+            part -= __uint_as_float(lo << 16) + __uint_as_float(lo & 0xffff0000u);
+          }
+        }
+      }
+      const u32x4_t zero4 = {0u, 0u, 0u, 0u};
+      bf16x8_t AKk[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) AKk[u] = as_bf16x8((u >> 1) == bw ? fa[u & 1] : zero4);
+      uint32_t p0, p1, p2;
+      split2(part, p0, p1);
+      p2 = f32_to_bf16_rne(part - bf16_to_f32(p0) - bf16_to_f32(p1));
+      const bf16x8_t AO = as_bf16x8(u32x4_t{p0 | (p1 << 16), p2, 0u, 0u});
+      const bf16x8_t BONE = as_bf16x8(u32x4_t{one, one, one, one});
+      constexpr uint32_t QM = (1u << BITS) - 1u;
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb) {
+        // token 16 sb + n: its code of channel c at bit `off` of word `wd` of c's stream
+        const int bit = (16 * sb + n) * BITS, wd = bit >> 5, off = bit & 31;
+        const int wd1 = min(wd + 1, BITS - 1);  // a code straddling words never ends a stream
+        f32x4_t d = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          u32x4_t f;
+#pragma unroll
+          for (int e2 = 0; e2 < 4; ++e2) {
+            uint32_t q[2];
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+              const int c = 32 * u + 8 * gq + 2 * e2 + hh;
+              const uint32_t w0 = kgc[w][c * BITS + wd];
+              uint32_t v;
+              if constexpr (32 % BITS == 0) v = w0 >> off;
+              else v = __builtin_amdgcn_alignbit(kgc[w][c * BITS + wd1], w0, off);
+              q[hh] = v & QM;
+            }
+            if constexpr (BITS == 8) {
+              f[e2] = __builtin_amdgcn_perm(__float_as_uint(float(q[1])), __float_as_uint(float(q[0])), 0x07060302u);
+            } else {
+              f[e2] = one | (q[0] << (7 - BITS)) | (q[1] << (23 - BITS));
+            }
+          }
+          d = mfma16(AKk[u], as_bf16x8(f), d);
+        }
+        d = mfma16(AO, BONE, d);
+        const bool valid = FULL || 16 * sb + n <= lim;
+        s[sb][0] = valid ? kSK2 * ((d[0] + d[1]) + (d[2] + d[3])) : -INFINITY;
+      }
+    } else {
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) {
       f32x4_t d = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -787,6 +901,7 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
         s[sb][0] = valid ? fmaf(gam[0], d[0] + d[1], bet[0] * qrow[0]) : -INFINITY;
         s[sb][1] = valid ? fmaf(gam[0], d[2] + d[3], bet[0] * qrow[2]) : -INFINITY;
       }
+    }
     }
     // online softmax (queries of the lane's D rows)
     float alpha[NQL];
@@ -859,42 +974,57 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
   for (; t0 + 32 <= t_endq; t0 += 128) step(t0, std::true_type{});
   if (t0 < t_endq) step(t0, std::false_type{});
 
-  // staged raw positions [max(tq, t_begin), t_end) of this split (tiles only; at most 15): scores
-  // with the raw query (macc still holds q), their softmax part and raw value sums
-  if constexpr (TB > 1) {
+  // raw positions [max(tq, t_begin), t_end) of this split (staged tile tokens, at most 15; the
+  // KIVI window, at most win + 31), in chunks of 16: scores with the raw query (macc still holds
+  // q), a running maximum and sum per query, raw value sums rescaled as the maximum moves
+  if constexpr (RAW) {
+    const int ringsz = KIVI ? a.win + 32 : TB;
     const int r0 = max(tq, t_begin), nr = max(0, t_end - r0);
     const size_t slc = (size_t(l) * a.kc.B + b) * a.kc.H + h;
-    if (threadIdx.x < JQ * 16) {
-      const int jj = threadIdx.x / 16, r = threadIdx.x % 16;
-      float sc = -INFINITY;
-      if (jj < nj && r < nr) {
-        const uint16_t* kr = a.kc.ring + (slc * TB + (r0 + r) % TB) * kD;
-        float acc = 0.0f;
-        for (int ch = 0; ch < kD; ++ch) acc = fmaf(macc[jj][ch], bf16_to_f32(kr[ch]), acc);
-        sc = a.scale * acc;
-      }
-      rs[jj][r] = sc;
+    if (threadIdx.x < RJ) {
+      rml[0][threadIdx.x] = -INFINITY;
+      rml[1][threadIdx.x] = 0.0f;
     }
-    __syncthreads();
-    if (threadIdx.x < JQ) {
-      const int jj = threadIdx.x;
-      float m = -INFINITY, sum = 0.0f;
-      for (int r = 0; r < nr; ++r) m = fmaxf(m, rs[jj][r]);
-      for (int r = 0; r < nr; ++r) {
-        const float pr = m == -INFINITY ? 0.0f : __expf(rs[jj][r] - m);
-        rs[jj][r] = pr;
-        sum += pr;
+    for (int idx = threadIdx.x; idx < RJ * kD; idx += kAThreads) (&accr[0][0])[idx] = 0.0f;
+    for (int c0 = 0; c0 < nr; c0 += 16) {
+      const int nc = min(16, nr - c0);
+      __syncthreads();
+      if (threadIdx.x < JQ * 16) {
+        const int jj = threadIdx.x / 16, r = threadIdx.x % 16;
+        float sc = -INFINITY;
+        if (jj < nj && r < nc) {
+          const uint16_t* kr = a.kc.ring + (slc * ringsz + (r0 + c0 + r) % ringsz) * kD;
+          float acc = 0.0f;
+          for (int ch = 0; ch < kD; ++ch) acc = fmaf(macc[jj][ch], bf16_to_f32(kr[ch]), acc);
+          sc = a.scale * acc;
+        }
+        rs[jj][r] = sc;
       }
-      rml[0][jj] = m;
-      rml[1][jj] = sum;
-    }
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < JQ * kD; idx += kAThreads) {
-      const int jj = idx / kD, ch = idx % kD;
-      float acc = 0.0f;
-      for (int r = 0; r < nr; ++r)
-        acc = fmaf(rs[jj][r], bf16_to_f32(a.vc.ring[(slc * TB + (r0 + r) % TB) * kD + ch]), acc);
-      accr[jj][ch] = acc;
+      __syncthreads();
+      if (threadIdx.x < JQ) {
+        const int jj = threadIdx.x;
+        const float mo = rml[0][jj];
+        float m = mo;
+        for (int r = 0; r < nc; ++r) m = fmaxf(m, rs[jj][r]);
+        const float f = mo == -INFINITY ? 0.0f : __expf(mo - m);
+        float sum = rml[1][jj] * f;
+        for (int r = 0; r < nc; ++r) {
+          const float pr = m == -INFINITY ? 0.0f : __expf(rs[jj][r] - m);
+          rs[jj][r] = pr;
+          sum += pr;
+        }
+        rml[0][jj] = m;
+        rml[1][jj] = sum;
+        rfac[jj] = f;
+      }
+      __syncthreads();
+      for (int idx = threadIdx.x; idx < JQ * kD; idx += kAThreads) {
+        const int jj = idx / kD, ch = idx % kD;
+        float acc = accr[jj][ch] * rfac[jj];
+        for (int r = 0; r < nc; ++r)
+          acc = fmaf(rs[jj][r], bf16_to_f32(a.vc.ring[(slc * ringsz + (r0 + c0 + r) % ringsz) * kD + ch]), acc);
+        accr[jj][ch] = acc;
+      }
     }
   }
 
@@ -918,7 +1048,7 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
 #pragma unroll
   for (int qi = 0; qi < NQL; ++qi) {
     const int j = NBLK == 2 ? gq : 2 * gq + qi;
-    float M = TB > 1 ? rml[0][j < RJ ? j : 0] : -INFINITY;
+    float M = RAW ? rml[0][j < RJ ? j : 0] : -INFINITY;
     for (int v = 0; v < 4; ++v) M = fmaxf(M, ml[v][0][j]);
     fq[qi] = mrun[qi] == -INFINITY ? 0.0f : __expf(mrun[qi] - M);
 #pragma unroll
@@ -949,13 +1079,13 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
   }
   if (threadIdx.x < JQ) {
     const int jj = threadIdx.x;
-    float M = TB > 1 ? rml[0][jj < RJ ? jj : 0] : -INFINITY, L = 0.0f;
+    float M = RAW ? rml[0][jj < RJ ? jj : 0] : -INFINITY, L = 0.0f;
     for (int v = 0; v < 4; ++v) M = fmaxf(M, ml[v][0][jj]);
     for (int v = 0; v < 4; ++v) {
       const float mv = ml[v][0][jj];
       if (mv != -INFINITY) L += ml[v][1][jj] * __expf(mv - M);
     }
-    if constexpr (TB > 1) {
+    if constexpr (RAW) {
       const float mr = rml[0][jj < RJ ? jj : 0];
       if (mr != -INFINITY) L += rml[1][jj < RJ ? jj : 0] * __expf(mr - M);
     }
@@ -963,7 +1093,7 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
     mm[1][jj] = L;
   }
   __syncthreads();
-  if constexpr (TB > 1) {  // raw value sums to the common maximum
+  if constexpr (RAW) {  // raw value sums to the common maximum
     for (int idx = threadIdx.x; idx < JQ * kD; idx += kAThreads) {
       const int jj = idx / kD, ch = idx % kD;
       const float mr = rml[0][jj];
@@ -972,7 +1102,7 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
     __syncthreads();
   }
   if (a.nsplit == 1) {
-    finalize_rows(a, G, &macc[0][0], TB > 1 ? &accr[0][0] : nullptr, mm[1], nj, lv, b, h, hq0);
+    finalize_rows(a, G, &macc[0][0], RAW ? &accr[0][0] : nullptr, mm[1], nj, lv, b, h, hq0);
     return;
   }
   const size_t pstride = size_t(2 + 2 * kD);
@@ -983,25 +1113,26 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
       if (idx == 0) v = mm[0][jj];
       else if (idx == 1) v = mm[1][jj];
       else if (idx < 2 + kD) v = macc[jj][idx - 2];
-      else v = TB > 1 ? accr[jj < RJ ? jj : 0][(idx - 2 - kD) % (TB > 1 ? kD : 1)] : 0.0f;
+      else v = RAW ? accr[jj < RJ ? jj : 0][(idx - 2 - kD) % (RAW ? kD : 1)] : 0.0f;
       P[idx] = v;
     }
   }
 }
 
 template <int BITS>
-const void* att_mfma_fn(int nblk, int bt) {
+const void* att_mfma_fn(int nblk, int bt, bool kivi) {
+  if (kivi) return (const void*)att_mfma<BITS, 2, 1, true>;
   if (bt > 1) return nblk == 2 ? (const void*)att_mfma<BITS, 2, 16> : (const void*)att_mfma<BITS, 1, 16>;
   return nblk == 2 ? (const void*)att_mfma<BITS, 2, 1> : (const void*)att_mfma<BITS, 1, 1>;
 }
 
-const void* att_mfma_kernel(int bits, int nblk, int bt) {
+const void* att_mfma_kernel(int bits, int nblk, int bt, bool kivi) {
   switch (bits) {
-    case 2: return att_mfma_fn<2>(nblk, bt);
-    case 3: return att_mfma_fn<3>(nblk, bt);
-    case 4: return att_mfma_fn<4>(nblk, bt);
-    case 6: return att_mfma_fn<6>(nblk, bt);
-    default: return att_mfma_fn<8>(nblk, bt);
+    case 2: return att_mfma_fn<2>(nblk, bt, kivi);
+    case 3: return att_mfma_fn<3>(nblk, bt, kivi);
+    case 4: return att_mfma_fn<4>(nblk, bt, kivi);
+    case 6: return att_mfma_fn<6>(nblk, bt, kivi);
+    default: return att_mfma_fn<8>(nblk, bt, kivi);
   }
 }
 
@@ -1031,10 +1162,12 @@ AttendPlan attend_plan(int nl, int B, int H, int Hq, int d, int span) {
 }
 
 bool attend_mfma_supported(const AttendDev& a, const CodecDev& c) {
+  const bool bits = c.bits == 2 || c.bits == 3 || c.bits == 4 || c.bits == 6 || c.bits == 8;
+  // KIVI: 32-position key groups, 64-channel value blocks, contiguous caches
+  if (c.backend == CG_BACKEND_KIVI) return a.q.d == kD && c.kg == 32 && c.kvc == 64 && !a.pt.pages && bits;
   // tiles of 16 tokens on contiguous caches (paged caches take per-token blocks only)
   return c.backend == CG_BACKEND_BLOCK_UNIFORM && (c.bt == 1 || (c.bt == 16 && !a.pt.pages)) && a.q.d == kD &&
-         (c.n == 64 || c.n == 128) &&
-         (c.bits == 2 || c.bits == 3 || c.bits == 4 || c.bits == 6 || c.bits == 8);
+         (c.n == 64 || c.n == 128) && bits;
 }
 
 hipError_t launch_attend(const AttendDev& a, const GaugeDev& G, const CodecDev& c, bool force_generic,
@@ -1044,14 +1177,17 @@ hipError_t launch_attend(const AttendDev& a, const GaugeDev& G, const CodecDev& 
   if (nrow == 0) return hipSuccess;
   hipError_t e;
   if (!force_generic && attend_mfma_supported(a, c)) {
-    // the matrix-core kernel takes 8 / NBLK query heads per workgroup
-    const int nblk = kD / c.n, jq = 8 / nblk;
+    // the matrix-core kernel takes 8 / NBLK query heads per workgroup (NBLK value blocks per row)
+    const bool kivi = c.backend == CG_BACKEND_KIVI;
+    const int nblk = kD / (kivi ? c.kvc : c.n), jq = 8 / nblk;
     AttendDev af = a;
     af.nqc = (a.grp + jq - 1) / jq;
+    af.win = kivi ? c.win : 0;
     const int nrow_f = a.q.L * a.q.B * a.kc.H * af.nqc;
     GaugeDev g2 = G;
     void* args[] = {&af, &g2};
-    e = hipLaunchKernel(att_mfma_kernel(c.bits, nblk, c.bt), dim3(a.nsplit, nrow_f), dim3(kAThreads), args, 0, st);
+    e = hipLaunchKernel(att_mfma_kernel(c.bits, nblk, c.bt, kivi), dim3(a.nsplit, nrow_f), dim3(kAThreads), args, 0,
+                        st);
     if (e != hipSuccess) return e;
   } else {
     const size_t smem = (size_t(2) * kJQ * d + size_t(kGTile) * (d + 4) + kJQ * kGTile + 3 * kJQ) * sizeof(float);

@@ -748,6 +748,7 @@ static int32_t attend_entry(int32_t l0, int32_t l1, const cg_kv_view* q, const c
   a.part = static_cast<float*>(workspace);
   a.err = err_flag;
   a.cap = kc->T_cap;
+  a.win = 0;
   hipError_t e = launch_attend(a, gauge_dev(G_dev, shp), codec_dev(codec), force_generic(),
                                static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;
@@ -827,6 +828,7 @@ int32_t kv_attend_paged(int32_t l0, int32_t l1, const cg_kv_view* q, const cg_ca
   a.pt.max_pages = pages->max_pages;
   a.pt.page_size = pages->page_size;
   a.cap = cap;
+  a.win = 0;
   hipError_t e = launch_attend(a, gauge_dev(G_dev, shp), codec_dev(codec), force_generic(),
                                static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CG_OK : CG_ERR_DEVICE;

@@ -143,6 +143,7 @@ struct AttendDev {
   int* err;
   PageDev pt;            // paged caches (block-uniform per-token blocks or passthrough)
   int cap;               // positions a row can hold: T_cap, or max_pages * page_size
+  int win;               // KIVI window (set by the launch for the matrix-core kernel)
 };
 struct AttendPlan {
   int nsplit = 1, chunk = 64, nqc = 1;

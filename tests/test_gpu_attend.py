@@ -112,6 +112,15 @@ CASES = [
     ("bu2-n128-g64", O.Codec(backend=O.BLOCK_UNIFORM, bits=2, block_c=128), 64, 200, 224, [150, 200]),
     ("bu8-n64-g32", O.Codec(backend=O.BLOCK_UNIFORM, bits=8, block_c=64), 32, 100, 128, [100, 99]),
     ("kivi3", O.Codec(backend=O.KIVI, bits=3, key_tokens=32, val_channels=64, residual=64), 32, 300, 320, [300, 150]),
+    # KIVI on the matrix cores at every width: rows wholly in the window (100, and 159 = window +
+    # 31), a row with one key group, windows of 32 and 128 positions, two splits per row
+    ("kivi2-g128", O.Codec(backend=O.KIVI, bits=2, key_tokens=32, val_channels=64, residual=128), 128, 420, 448,
+     [420, 100]),
+    ("kivi4-g16", O.Codec(backend=O.KIVI, bits=4, key_tokens=32, val_channels=64, residual=128), 16, 300, 320,
+     [300, 161]),
+    ("kivi6-g64", O.Codec(backend=O.KIVI, bits=6, key_tokens=32, val_channels=64, residual=32), 64, 260, 288, [260, 33]),
+    ("kivi8-g32", O.Codec(backend=O.KIVI, bits=8, key_tokens=32, val_channels=64, residual=128), 32, 200, 224,
+     [200, 159]),
     ("tile4-16", O.Codec(backend=O.BLOCK_UNIFORM, bits=4, block_c=64, block_t=16), 128, 250, 256, [250, 200]),
     # tiles with 128-channel blocks (eight query heads per workgroup), a row shorter than one tile
     # (staged positions only) and a row ending on a tile boundary

@@ -2,8 +2,8 @@
 and kernels, with the split rows' partial results in the library's device scratch instead of a
 caller workspace, so the outputs must agree bit for bit.  Two calls in a row, the second with a
 smaller input (the scratch keeps the first call's partials), on the matrix-core attention kernel
-(block-uniform) and on the general kernel (KIVI), with device row lengths and with the caches'
-host length."""
+(block-uniform; KIVI with 64-channel value blocks) and on the general kernel (KIVI with 32-channel
+value blocks), with device row lengths and with the caches' host length."""
 import ctypes as C
 
 import numpy as np
@@ -70,7 +70,7 @@ CALLS = [
     (cg.Codec(cg.BLOCK_UNIFORM, 4, 64), (2, 1, 8, 4, 4096, 4096, 128), [4096]),
     (cg.Codec(cg.BLOCK_UNIFORM, 4, 64), (1, 2, 8, 4, 1000, 1024, 128), None),
     (cg.Codec(cg.KIVI, 3, 64, 32, 64, 128), (2, 1, 4, 4, 3000, 3072, 32), [2990]),
-    (cg.Codec(cg.KIVI, 3, 64, 32, 64, 128), (1, 1, 4, 4, 700, 768, 32), None),
+    (cg.Codec(cg.KIVI, 3, 64, 32, 32, 128), (1, 1, 4, 4, 700, 768, 32), None),
 ]
 
 
