@@ -1204,6 +1204,298 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
 }
 
 // ------------------------------------------------------------------------------------------
+// decode, token-channel tiles (one range per 16 tokens x NB channels), bf16 output
+// ------------------------------------------------------------------------------------------
+// Every token is centred on a code of its own (the per-token centring of dec_mfma): on its first
+// code of each gauge group when groups are smaller than blocks (GC), else on its first code of
+// each block.  The 32 code rows of a view tile are consecutive cache rows, so they stream into an
+// LDS ring as one contiguous block by LDS-direct loads (each wave also takes the side words of the
+// at most three 16-token tiles the rows touch into a slot of its own), with the ring's waits
+// counted exactly as in dec_fast.  In the iteration before a tile's matrix-core step, thread
+// (row r, segment s) converts the 16 codes of channels 16 s .. 16 s + 15 of row r to the bf16
+// offsets q - c (exact) in a double-buffered tile, and writes the centre value mn + c sc and the
+// block's scale beside it.  The waves multiply the offsets by the two G^T planes; the fold adds sc
+// times each block segment's sums and the centre terms through per-group or per-block column sums.
+// Ring depth: code + side stages within what is left of 52 KB, so that three workgroups fit per
+// CU (with two the decoder runs about 40% slower: it waits on its loads), at most kDStages.
+constexpr int tile_stages(int bits) {
+  const int fixed = 2 * kTok * kRowBytes + 2 * kTok * kD * 2 + 2 * kD * 4 + 2 * kTok * (kD / 8) * 4 +
+                    2 * kTok * 2 * 4;
+  const int stage = kTok * kD * bits / 8 + 4 * 3 * 2 * 4;
+  const int room = 52 * 1024 - fixed;
+  return room / stage > kDStages ? kDStages : room / stage;
+}
+
+template <int NP, int KS, int BITS, int NB>
+__global__ __launch_bounds__(kThreads, 3) void dec_tile(MfmaArgs a) {
+  constexpr int TB = 16;
+  constexpr int RB = kD * BITS / 8;            // code bytes per row
+  constexpr int NBK = kD / NB;                 // blocks per row
+  constexpr bool GC = 16 * KS < NB;            // groups smaller than blocks: centred per group
+  constexpr int KR = 16 * KS;                  // K range of a wave (its gauge group, or groups)
+  constexpr int SEG = (KR < NB ? KR : NB) / 16;  // K-steps per block segment of that range
+  constexpr int NSEG = KS / SEG;
+  constexpr int GPR = kD * 2 / 16;             // 16-byte granules per bf16 output row
+  constexpr int F = kTok * GPR / kThreads;     // stores per thread per flush
+  constexpr int DS = tile_stages(BITS);
+  static_assert(DS >= 3, "LDS ring too shallow");
+  static_assert(NB == 64 || NB == 128, "tiles of 64 or 128 channels");
+  __shared__ __attribute__((aligned(16))) uint8_t ctile[DS][kTok * RB];   // code rows
+  __shared__ __attribute__((aligned(16))) uint32_t stile[DS][4 * 3 * NBK];  // side words, per wave
+  __shared__ __attribute__((aligned(16))) uint8_t qtile[2][kTok * kRowBytes];  // offsets q - c, bf16
+  __shared__ float ctr[2][kTok][kD / 8];       // centre values per (row, group or block)
+  __shared__ float scl[2][kTok][NBK];          // block scales per row
+  __shared__ __attribute__((aligned(16))) float colsum[GC ? 1 : NBK][kD];
+  __shared__ __attribute__((aligned(16))) uint8_t ystage[2][kTok * kD * 2];
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n = lane & 31, hc = lane >> 5;
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int slice = logical / a.chunks, chunk = logical - slice * a.chunks;
+  if (slice >= a.nslices) return;
+  const int h = slice % a.H, b = (slice / a.H) % a.B, lv = slice / (a.H * a.B);
+  const int l = lv + a.l0;
+  int Tv = a.T;
+  int held = a.len;  // positions the cache holds
+  if (a.pos) {
+    if (!row_held(a, b, chunk, held)) return;
+    Tv = min(Tv, held - a.t0);
+  }
+  const int ntiles = (Tv + kTok - 1) / kTok;
+  const int tb = chunk * a.tiles_per_wg;
+  const int te_all = min(ntiles, tb + a.tiles_per_wg);
+  if (tb >= te_all) return;
+  char* ys = a.x + 2 * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
+  const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
+  const size_t crow0 = cslice * size_t(a.T_cap) + a.t0;
+  // the quantised view rows [0, Tq) go through the pipeline, the staged rows after them are copied
+  const int Tq = max(0, min(Tv, held / TB * TB - a.t0));
+  const int te = min(te_all, (Tq + kTok - 1) / kTok);
+  if (tb >= te) {
+    ring_rows<true>(a, cslice, ys, max(Tq, tb * kTok), min(Tv, te_all * kTok));
+    return;
+  }
+  const int Tv_all = Tv;
+  Tv = Tq;
+
+  const int kbase = a.g >= 32 ? (32 * w / a.g) * a.g : 32 * w;
+  const int chA = 32 * w + 16 * ((n >> 2) & 1) + 4 * (n >> 3) + (n & 3);
+  bf16x8_t A[NP][KS];
+  load_a<NP, KS>(A, a, l, h, chA, kbase, hc);  // a.gp holds the G^T planes for decode
+  // column sums of the planes the matrix core multiplies: per group (GC) or per block
+  for (int idx = threadIdx.x; idx < (GC ? 1 : NBK) * kD; idx += kThreads) {
+    const int k = idx / kD, i = idx - k * kD;
+    const int r = i / a.g;
+    colsum[k][i] = seg_colsum(a, l, h, i, GC ? r * a.g : k * NB, GC ? (r + 1) * a.g : (k + 1) * NB);
+  }
+
+  // LDS-direct loads: wave w moves granules [8 BITS w, 8 BITS (w + 1)) of the tile's code block
+  // (row gi / BITS, part gi % BITS; rows past the view repeat its last row) and, into its own
+  // slot, the side words of the (at most three) 16-token tiles the rows touch (tiles past the
+  // quantised rows repeat the last one)
+  const int cgi = 8 * BITS * w + lane, cgrow = cgi / BITS, cgpart = cgi % BITS;
+  auto issue = [&](int tile) {
+    const int st = (tile - tb) % DS;
+    const int last = Tv - 1 - tile * kTok;
+    const size_t row0 = crow0 + size_t(tile) * kTok;
+    if (lane < 8 * BITS)
+      __builtin_amdgcn_global_load_lds(a.codes + (row0 + min(cgrow, last)) * RB + 16 * cgpart,
+                                       (__attribute__((address_space(3))) void*)(ctile[st] + 16 * 8 * BITS * w), 16, 0, 0);
+    const size_t blk0 = row0 / TB, blast = (row0 + last) / TB;
+    if (lane < 3 * NBK)
+      __builtin_amdgcn_global_load_lds(a.side + min(blk0 + lane / NBK, blast) * NBK + lane % NBK,
+                                       (__attribute__((address_space(3))) void*)(stile[st] + 3 * NBK * w), 4, 0, 0);
+  };
+  int64_t yoff[F];
+  int ysrc[F];
+#pragma unroll
+  for (int k = 0; k < F; ++k) {
+    const int gi = int(threadIdx.x) + k * kThreads, row = gi / GPR, j = gi % GPR;
+    yoff[k] = int64_t(2) * row * a.st + 16 * j;
+    ysrc[k] = row * kD * 2 + 16 * (j ^ (row & (GPR - 1)));
+  }
+  const int64_t ytile = int64_t(2) * kTok * a.st;
+  auto flush = [&](int tile, int buf) {
+    const int nlive = min(kTok, Tv - tile * kTok);
+    char* yt = ys + tile * ytile;
+    if (nlive == kTok) {
+#pragma unroll
+      for (int k = 0; k < F; ++k) store_stream(yt + yoff[k], *(const u32x4_t*)(&ystage[buf][ysrc[k]]));
+    } else {
+#pragma unroll
+      for (int k = 0; k < F; ++k) {
+        int gi = int(threadIdx.x) + k * kThreads;
+        if (gi >= nlive * GPR) gi = (nlive - 1) * GPR + (gi % GPR);
+        const int row = gi / GPR, j = gi % GPR;
+        const u32x4_t v = *(const u32x4_t*)(&ystage[buf][row * kD * 2 + 16 * (j ^ (row & (GPR - 1)))]);
+        store_stream(yt + int64_t(2) * row * a.st + 16 * j, v);
+      }
+    }
+  };
+  // vector-memory operations of this wave issued after the loads of tile X, at the wait of
+  // iteration t (before its barrier): the prologue's later loads, then per iteration i < t its
+  // flush (F stores, i > tb) and its loads (2, i + DS - 1 < te)
+  const int pe = min(te, tb + DS - 1);
+  auto younger = [&](int X, int t) {
+    // steady state: X's loads came from iteration X - (DS - 1) >= tb, and every iteration since
+    // flushed and issued
+    if (X - (DS - 1) >= tb && t + DS - 2 < te) return (t - (X - (DS - 1)) - 1) * (F + 2);
+    int c = 0, i = tb;
+    if (X < pe) c = 2 * (pe - 1 - X);
+    else i = X - (DS - 1) + 1;
+    for (; i < t; ++i) c += (i > tb ? F : 0) + (i + DS - 1 < te ? 2 : 0);
+    return c;
+  };
+
+  // conversion of a tile's codes: thread (row cr, segment cs)
+  const int cr = threadIdx.x >> 3, cs = threadIdx.x & 7;
+  const int cblk = (16 * cs) / NB;                 // block of the segment
+  constexpr int SEGW = (16 * BITS + 31) / 32 + 1;  // words covering one 16-code segment
+  constexpr uint32_t QM = (1u << BITS) - 1u;
+  auto convert = [&](int tile, int buf) {
+    const int st = (tile - tb) % DS;
+    const int rr = min(cr, Tv - 1 - tile * kTok);  // rows past the view repeat the last one
+    const uint32_t* row = reinterpret_cast<const uint32_t*>(ctile[st] + rr * RB);
+    const int bit0 = 16 * cs * BITS;
+    uint32_t cw[SEGW];
+#pragma unroll
+    for (int i = 0; i < SEGW; ++i) {
+      const int wi = (bit0 >> 5) + i;
+      cw[i] = wi < kD * BITS / 32 ? row[wi] : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i + 1 < SEGW; ++i) cw[i] = __builtin_amdgcn_alignbit(cw[i + 1], cw[i], bit0 & 31);
+    uint32_t q[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int bit = e * BITS, wd = bit >> 5, off = bit & 31;
+      uint32_t v = cw[wd] >> off;
+      if (off + BITS > 32) v |= cw[wd + 1] << (32 - off);
+      q[e] = v & QM;
+    }
+    // centres: the unit's first code (in this segment, or word-aligned at the unit's start)
+    int c0, c1;
+    if constexpr (GC) {
+      const int gsegs = a.g >> 4;
+      if (a.g == 8) {
+        c0 = int(q[0]);
+        c1 = int(q[8]);
+      } else {
+        c0 = (cs % gsegs) ? int(row[(a.g * (cs / gsegs) * BITS) >> 5] & QM) : int(q[0]);
+        c1 = c0;
+      }
+    } else {
+      constexpr int BSEGS = NB / 16;
+      c0 = (cs % BSEGS) ? int(row[(NB * cblk * BITS) >> 5] & QM) : int(q[0]);
+      c1 = c0;
+    }
+    uint32_t v[8];
+#pragma unroll
+    for (int e = 0; e < 16; e += 2) {
+      const int c = e < 8 ? c0 : c1;
+      v[e >> 1] = (__float_as_uint(float(int(q[e]) - c)) >> 16) | ((__float_as_uint(float(int(q[e + 1]) - c)) >> 16) << 16);
+    }
+    uint8_t* rowp = &qtile[buf][cr * kRowBytes];
+    *(u32x4_t*)(rowp + 16 * swz(cr, 2 * cs)) = u32x4_t{v[0], v[1], v[2], v[3]};
+    *(u32x4_t*)(rowp + 16 * swz(cr, 2 * cs + 1)) = u32x4_t{v[4], v[5], v[6], v[7]};
+    // side word of the row's 16-token tile (this wave's copy of the slot)
+    const size_t crow = crow0 + size_t(tile) * kTok + rr;
+    const int bi = int(crow / TB - (crow0 + size_t(tile) * kTok) / TB);
+    const uint32_t sw = stile[st][3 * NBK * w + bi * NBK + cblk];
+    const float mn = f16_bits_to_f32(sw & 0xffffu), sc = f16_bits_to_f32(sw >> 16);
+    if ((16 * cs) % NB == 0) scl[buf][cr][cblk] = sc;
+    if constexpr (GC) {
+      const int gsegs = a.g >> 4;
+      if (a.g == 8) {
+        ctr[buf][cr][2 * cs] = mn + float(c0) * sc;
+        ctr[buf][cr][2 * cs + 1] = mn + float(c1) * sc;
+      } else if (cs % gsegs == 0) {
+        ctr[buf][cr][cs / gsegs] = mn + float(c0) * sc;
+      }
+    } else if (cs % (NB / 16) == 0) {
+      ctr[buf][cr][cblk] = mn + float(c0) * sc;
+    }
+  };
+
+  for (int t = tb; t < pe; ++t) issue(t);
+  wait_vm_atmost(younger(tb, tb));
+  __syncthreads();  // tile tb's loads, colsum
+  convert(tb, 0);
+  for (int t = tb; t < te; ++t) {
+    const int P = (t - tb) & 1;
+    if (t + 1 < te) wait_vm_atmost(younger(t + 1, t));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_imm(63));
+    __builtin_amdgcn_s_barrier();
+    if (t > tb) flush(t - 1, P ^ 1);
+    if (t + DS - 1 < te) issue(t + DS - 1);
+    if (t + 1 < te) convert(t + 1, P ^ 1);
+    const uint8_t* rowp = &qtile[P][n * kRowBytes];
+    float y[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) y[e] = 0.0f;
+#pragma unroll
+    for (int sgi = 0; sgi < NSEG; ++sgi) {
+      f32x16_t acc0 = {}, acc1 = {};
+#pragma unroll
+      for (int u = 0; u < SEG; ++u) {
+        const int kk = sgi * SEG + u;
+        const int j = (kbase >> 3) + 2 * kk + hc;
+        const bf16x8_t bv = as_bf16x8(*(const u32x4_t*)(rowp + 16 * swz(n, j)));
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          if ((u * NP + p) & 1) acc1 = mfma(A[p][kk], bv, acc1);
+          else acc0 = mfma(A[p][kk], bv, acc0);
+        }
+      }
+      const float sc = scl[P][n][(kbase + 16 * SEG * sgi) / NB];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) y[e] = fmaf(sc, acc0[e] + acc1[e], y[e]);
+    }
+    // centre terms (column sums of groups or blocks outside the output's group are zero)
+    const int ch0 = 32 * w + 16 * hc;
+    if constexpr (GC) {
+      const float m0 = ctr[P][n][ch0 / a.g];
+      const float m1 = ctr[P][n][(ch0 + 8) / a.g];
+      const float4* csp = (const float4*)&colsum[0][ch0];
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const float4 c = csp[q4];
+        const float cc[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) y[4 * q4 + u] = fmaf(4 * q4 + u < 8 ? m0 : m1, cc[u], y[4 * q4 + u]);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < NBK; ++k) {
+        const float mk = ctr[P][n][k];
+        const float4* csp = (const float4*)&colsum[k][ch0];
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 c = csp[q4];
+          const float cc[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) y[4 * q4 + u] = fmaf(mk, cc[u], y[4 * q4 + u]);
+        }
+      }
+    }
+    uint8_t* yrow = &ystage[P][n * kD * 2];
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    uint32_t pk[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      pk[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{y[2 * e], y[2 * e + 1]}), bf16x2_t));
+    const int j0 = 4 * w + 2 * hc;
+    *(u32x4_t*)(yrow + 16 * (j0 ^ (n & (GPR - 1)))) = u32x4_t{pk[0], pk[1], pk[2], pk[3]};
+    *(u32x4_t*)(yrow + 16 * ((j0 + 1) ^ (n & (GPR - 1)))) = u32x4_t{pk[4], pk[5], pk[6], pk[7]};
+  }
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(63));
+  __builtin_amdgcn_s_barrier();
+  flush(te - 1, (te - 1 - tb) & 1);
+  ring_rows<true>(a, cslice, ys, max(Tq, tb * kTok), min(Tv_all, te_all * kTok));
+}
+
+// ------------------------------------------------------------------------------------------
 // decode, KIVI keys (per-channel ranges over 32-token groups), groups of at most 32 channels
 // ------------------------------------------------------------------------------------------
 // LDS ring depth: code + side stages within what is left of 52 KB (three workgroups per CU)
@@ -1621,12 +1913,12 @@ void* enc_by_bits(int bits, int nb, int mode, int bt) {
 }
 
 // (token-channel tiles: blocks of 64 or 128 channels, centred per (token, group) or per
-// (token, block))
+// (token, block); bf16 output on the tile decoder's LDS ring)
 template <int KS, int BITS, int NB>
 void* dec_kernel(bool bf16, int bt) {
   if constexpr (NB >= 64) {
     if (bt == 16) {
-      if (bf16) return (void*)dec_mfma<kNP, KS, BITS, NB, true, 16>;
+      if (bf16) return (void*)dec_tile<kNP, KS, BITS, NB>;
       return (void*)dec_mfma<kNP, KS, BITS, NB, false, 16>;
     }
   }
