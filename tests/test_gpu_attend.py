@@ -201,6 +201,22 @@ def test_attend_split_rows_over_tiles(kernels, bits, n):
     assert (got[:, 1] == 0).all()
 
 
+@pytest.mark.parametrize("bits,win", [(3, 128), (4, 32)])
+def test_attend_split_rows_over_kivi_caches(kernels, bits, win):
+    """KIVI caches on rows long enough to be split over positions: key groups in every split,
+    the window's raw positions in the last one; an empty row, a row inside the window, and 12
+    query heads per KV head (three query chunks of the matrix-core kernel)."""
+    oc = O.Codec(backend=O.KIVI, bits=bits, key_tokens=32, val_channels=64, residual=win)
+    lens = [2500, 0, 13, 1811]
+    st = _setup(oc, 2500, 2560, B=4, H=1, g=32, grp=12, lens=lens)
+    scale = 1.0 / np.sqrt(128)
+    ref = O.attend(oc, st["G"], st["kh"], st["vh"], st["qf"], lens, scale)
+    got, err = _attend_gpu(st, oc, lens, scale)
+    assert err == 0
+    _check(got, ref, _vmax(st, oc, lens, 12))
+    assert (got[:, 1] == 0).all()
+
+
 def test_attend_error_free_cache_equals_attention_on_x(kernels):
     """Passthrough backend with the identity gauge: the fused path is plain attention over the
     bf16 cache (torch's, in float64 on the CPU)."""
