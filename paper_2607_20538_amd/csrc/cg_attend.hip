@@ -616,9 +616,11 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
   __shared__ float rml[2][RJ];
   __shared__ float rfac[RJ];
   __shared__ __attribute__((aligned(16))) float accr[RJ][RAW ? kD : 1];
-  // KIVI keys: the step's key group in a per-wave region (channel c's 32 codes in words
-  // [c BITS, c BITS + BITS), its side word)
-  __shared__ __attribute__((aligned(16))) uint32_t kgc[KIVI ? 4 : 1][KIVI ? kD * BITS : 1];
+  // KIVI keys: the step's key group in a per-wave region, token-major (row t: the bf16 B values
+  // of channels 2i, 2i + 1 in word i; rows of 68 words, so the 16-byte reads of 16 tokens and the
+  // word writes of 64 lanes both spread over all banks), and the side word of each channel
+  constexpr int KROW = 68;
+  __shared__ __attribute__((aligned(16))) uint32_t ktk[KIVI ? 4 : 1][KIVI ? 32 * KROW : 1];
   __shared__ __attribute__((aligned(16))) uint32_t kgs[KIVI ? 4 : 1][KIVI ? kD : 1];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -798,10 +800,32 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
     // scores of the two 16-token halves
     float s[2][NQL];
     if constexpr (KIVI) {
-      // the group to the wave's LDS region
-      uint2* dc = reinterpret_cast<uint2*>(&kgc[w][2 * lane * BITS]);
+      // the group to the wave's LDS region: this lane's two channel streams (words 0 .. BITS - 1
+      // of channel 2 lane, then those of channel 2 lane + 1) become, for every token t, the bf16
+      // pair of B values of the two channels: 1 + q 2^-b (8 bits: q)
+      constexpr uint32_t QM = (1u << BITS) - 1u;
+      uint32_t sw2[2 * BITS];
 #pragma unroll
-      for (int i = 0; i < BITS; ++i) dc[i] = kcv[i];
+      for (int i = 0; i < BITS; ++i) {
+        sw2[2 * i] = kcv[i].x;
+        sw2[2 * i + 1] = kcv[i].y;
+      }
+#pragma unroll
+      for (int t = 0; t < 32; ++t) {
+        const int bit = t * BITS, wd = bit >> 5, off = bit & 31;
+        uint32_t qa, qb;
+        if (off + BITS <= 32) {
+          qa = (sw2[wd] >> off) & QM;
+          qb = (sw2[BITS + wd] >> off) & QM;
+        } else {
+          qa = __builtin_amdgcn_alignbit(sw2[wd + 1], sw2[wd], off) & QM;
+          qb = __builtin_amdgcn_alignbit(sw2[BITS + wd + 1], sw2[BITS + wd], off) & QM;
+        }
+        uint32_t pr;
+        if constexpr (BITS == 8) pr = __builtin_amdgcn_perm(__float_as_uint(float(qb)), __float_as_uint(float(qa)), 0x07060302u);
+        else pr = one | (qa << (7 - BITS)) | (qb << (23 - BITS));
+        ktk[w][t * KROW + lane] = pr;
+      }
       *reinterpret_cast<uint2*>(&kgs[w][2 * lane]) = ksv;
       __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
       __builtin_amdgcn_wave_barrier();
@@ -846,36 +870,13 @@ __global__ __launch_bounds__(kAThreads, 2) void att_mfma(AttendDev a, GaugeDev G
       p2 = f32_to_bf16_rne(part - bf16_to_f32(p0) - bf16_to_f32(p1));
       const bf16x8_t AO = as_bf16x8(u32x4_t{p0 | (p1 << 16), p2, 0u, 0u});
       const bf16x8_t BONE = as_bf16x8(u32x4_t{one, one, one, one});
-      constexpr uint32_t QM = (1u << BITS) - 1u;
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb) {
-        // token 16 sb + n: its code of channel c at bit `off` of word `wd` of c's stream
-        const int bit = (16 * sb + n) * BITS, wd = bit >> 5, off = bit & 31;
-        const int wd1 = min(wd + 1, BITS - 1);  // a code straddling words never ends a stream
+        // token 16 sb + n: channels 32 u + 8 gq .. + 7 are words 16 u + 4 gq .. + 3 of its row
+        const uint32_t* kr = &ktk[w][(16 * sb + n) * KROW + 4 * gq];
         f32x4_t d = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          u32x4_t f;
-#pragma unroll
-          for (int e2 = 0; e2 < 4; ++e2) {
-            uint32_t q[2];
-#pragma unroll
-            for (int hh = 0; hh < 2; ++hh) {
-              const int c = 32 * u + 8 * gq + 2 * e2 + hh;
-              const uint32_t w0 = kgc[w][c * BITS + wd];
-              uint32_t v;
-              if constexpr (32 % BITS == 0) v = w0 >> off;
-              else v = __builtin_amdgcn_alignbit(kgc[w][c * BITS + wd1], w0, off);
-              q[hh] = v & QM;
-            }
-            if constexpr (BITS == 8) {
-              f[e2] = __builtin_amdgcn_perm(__float_as_uint(float(q[1])), __float_as_uint(float(q[0])), 0x07060302u);
-            } else {
-              f[e2] = one | (q[0] << (7 - BITS)) | (q[1] << (23 - BITS));
-            }
-          }
-          d = mfma16(AKk[u], as_bf16x8(f), d);
-        }
+        for (int u = 0; u < 4; ++u) d = mfma16(AKk[u], as_bf16x8(*reinterpret_cast<const u32x4_t*>(kr + 16 * u)), d);
         d = mfma16(AO, BONE, d);
         const bool valid = FULL || 16 * sb + n <= lim;
         s[sb][0] = valid ? kSK2 * ((d[0] + d[1]) + (d[2] + d[3])) : -INFINITY;
