@@ -1204,44 +1204,48 @@ __global__ __launch_bounds__(kThreads, NP == 2 ? 3 : 2) void dec_fast(MfmaArgs a
 }
 
 // ------------------------------------------------------------------------------------------
-// decode, token-channel tiles (one range per 16 tokens x NB channels), bf16 output
+// decode centred per token, bf16 output: token-channel tiles (TB = 16: one range per 16 tokens x
+// NB channels), and per-token blocks spanning gauge groups (TB = 1, g < n)
 // ------------------------------------------------------------------------------------------
 // Every token is centred on a code of its own (the per-token centring of dec_mfma): on its first
-// code of each gauge group when groups are smaller than blocks (GC), else on its first code of
-// each block.  The 32 code rows of a view tile are consecutive cache rows, so they stream into an
-// LDS ring as one contiguous block by LDS-direct loads (each wave also takes the side words of the
-// at most three 16-token tiles the rows touch into a slot of its own), with the ring's waits
-// counted exactly as in dec_fast.  In the iteration before a tile's matrix-core step, thread
-// (row r, segment s) converts the 16 codes of channels 16 s .. 16 s + 15 of row r to the bf16
-// offsets q - c (exact) in a double-buffered tile, and writes the centre value mn + c sc and the
-// block's scale beside it.  The waves multiply the offsets by the two G^T planes; the fold adds sc
-// times each block segment's sums and the centre terms through per-group or per-block column sums.
+// code of each gauge group when groups are smaller than blocks (GC), else (tiles only) on its
+// first code of each block.  The 32 code rows of a view tile are consecutive cache rows, so they
+// stream into an LDS ring as one contiguous block by LDS-direct loads, with the side words beside
+// them (per-token blocks: the rows' words, spread over the waves; tiles: each wave takes the words
+// of the at most three 16-token tiles the rows touch into a slot of its own); the ring's waits are
+// counted exactly as in dec_fast.  In the iteration before a tile's matrix-core step, thread (row
+// r, segment s) converts the 16 codes of channels 16 s .. 16 s + 15 of row r to the bf16 offsets
+// q - c (exact) in a double-buffered tile, and writes the centre value mn + c sc and the block's
+// scale beside it.  The waves multiply the offsets by the two G^T planes; the fold adds sc times
+// each block segment's sums and the centre terms through per-group or per-block column sums.
 // Ring depth: code + side stages within what is left of 52 KB, so that three workgroups fit per
-// CU (with two the decoder runs about 40% slower: it waits on its loads), at most kDStages.
-constexpr int tile_stages(int bits) {
+// CU (with two the tile decoder ran about 40% slower: it waits on its loads), at most kDStages.
+constexpr int centred_stages(int bits, int nbk, int tb) {
   const int fixed = 2 * kTok * kRowBytes + 2 * kTok * kD * 2 + 2 * kD * 4 + 2 * kTok * (kD / 8) * 4 +
-                    2 * kTok * 2 * 4;
-  const int stage = kTok * kD * bits / 8 + 4 * 3 * 2 * 4;
+                    2 * kTok * nbk * 4;
+  const int stage = kTok * kD * bits / 8 + (tb > 1 ? 4 * 3 * nbk : kTok * nbk) * 4;
   const int room = 52 * 1024 - fixed;
   return room / stage > kDStages ? kDStages : room / stage;
 }
 
-template <int NP, int KS, int BITS, int NB>
-__global__ __launch_bounds__(kThreads, 3) void dec_tile(MfmaArgs a) {
-  constexpr int TB = 16;
+template <int NP, int KS, int BITS, int NB, int TB>
+__global__ __launch_bounds__(kThreads, 3) void dec_centred(MfmaArgs a) {
   constexpr int RB = kD * BITS / 8;            // code bytes per row
   constexpr int NBK = kD / NB;                 // blocks per row
-  constexpr bool GC = 16 * KS < NB;            // groups smaller than blocks: centred per group
+  // groups smaller than blocks: centred per group (per-token blocks take this kernel only then,
+  // with groups of at most 32 channels)
+  constexpr bool GC = TB > 1 ? 16 * KS < NB : true;
   constexpr int KR = 16 * KS;                  // K range of a wave (its gauge group, or groups)
   constexpr int SEG = (KR < NB ? KR : NB) / 16;  // K-steps per block segment of that range
   constexpr int NSEG = KS / SEG;
   constexpr int GPR = kD * 2 / 16;             // 16-byte granules per bf16 output row
   constexpr int F = kTok * GPR / kThreads;     // stores per thread per flush
-  constexpr int DS = tile_stages(BITS);
+  constexpr int DS = centred_stages(BITS, NBK, TB);
+  constexpr int SW = TB > 1 ? 4 * 3 * NBK : kTok * NBK;  // side words of a stage
   static_assert(DS >= 3, "LDS ring too shallow");
-  static_assert(NB == 64 || NB == 128, "tiles of 64 or 128 channels");
+  static_assert(TB == 16 ? (NB == 64 || NB == 128) : (TB == 1 && KS == 2 && NB <= 64), "tile or centred block shape");
   __shared__ __attribute__((aligned(16))) uint8_t ctile[DS][kTok * RB];   // code rows
-  __shared__ __attribute__((aligned(16))) uint32_t stile[DS][4 * 3 * NBK];  // side words, per wave
+  __shared__ __attribute__((aligned(16))) uint32_t stile[DS][SW];         // side words
   __shared__ __attribute__((aligned(16))) uint8_t qtile[2][kTok * kRowBytes];  // offsets q - c, bf16
   __shared__ float ctr[2][kTok][kD / 8];       // centre values per (row, group or block)
   __shared__ float scl[2][kTok][NBK];          // block scales per row
@@ -1256,7 +1260,7 @@ __global__ __launch_bounds__(kThreads, 3) void dec_tile(MfmaArgs a) {
   const int h = slice % a.H, b = (slice / a.H) % a.B, lv = slice / (a.H * a.B);
   const int l = lv + a.l0;
   int Tv = a.T;
-  int held = a.len;  // positions the cache holds
+  int held = a.kivi || TB > 1 ? a.len : INT_MAX;  // positions the cache holds
   if (a.pos) {
     if (!row_held(a, b, chunk, held)) return;
     Tv = min(Tv, held - a.t0);
@@ -1268,8 +1272,9 @@ __global__ __launch_bounds__(kThreads, 3) void dec_tile(MfmaArgs a) {
   char* ys = a.x + 2 * (size_t(lv) * a.sl + size_t(b) * a.sb + size_t(h) * a.sh);
   const size_t cslice = (size_t(l) * a.cB + b) * a.cH + h;
   const size_t crow0 = cslice * size_t(a.T_cap) + a.t0;
-  // the quantised view rows [0, Tq) go through the pipeline, the staged rows after them are copied
-  const int Tq = max(0, min(Tv, held / TB * TB - a.t0));
+  // KIVI / tiles: the quantised view rows [0, Tq) go through the pipeline, the window or staged
+  // rows after them are copied
+  const int Tq = a.kivi ? kivi_quantised_rows(a, held, Tv) : (TB > 1 ? max(0, min(Tv, held / TB * TB - a.t0)) : Tv);
   const int te = min(te_all, (Tq + kTok - 1) / kTok);
   if (tb >= te) {
     ring_rows<true>(a, cslice, ys, max(Tq, tb * kTok), min(Tv, te_all * kTok));
@@ -1290,10 +1295,11 @@ __global__ __launch_bounds__(kThreads, 3) void dec_tile(MfmaArgs a) {
   }
 
   // LDS-direct loads: wave w moves granules [8 BITS w, 8 BITS (w + 1)) of the tile's code block
-  // (row gi / BITS, part gi % BITS; rows past the view repeat its last row) and, into its own
-  // slot, the side words of the (at most three) 16-token tiles the rows touch (tiles past the
-  // quantised rows repeat the last one)
+  // (row gi / BITS, part gi % BITS; rows past the view repeat its last row) and side words: per-token
+  // blocks the words of rows 8 w .. 8 w + 7; tiles, into its own slot, the words of the (at most
+  // three) 16-token tiles the rows touch (tiles past the quantised rows repeat the last one)
   const int cgi = 8 * BITS * w + lane, cgrow = cgi / BITS, cgpart = cgi % BITS;
+  const int swi = 8 * NBK * w + lane, swrow = swi / NBK, swk = swi % NBK;
   auto issue = [&](int tile) {
     const int st = (tile - tb) % DS;
     const int last = Tv - 1 - tile * kTok;
@@ -1301,10 +1307,15 @@ __global__ __launch_bounds__(kThreads, 3) void dec_tile(MfmaArgs a) {
     if (lane < 8 * BITS)
       __builtin_amdgcn_global_load_lds(a.codes + (row0 + min(cgrow, last)) * RB + 16 * cgpart,
                                        (__attribute__((address_space(3))) void*)(ctile[st] + 16 * 8 * BITS * w), 16, 0, 0);
-    const size_t blk0 = row0 / TB, blast = (row0 + last) / TB;
-    if (lane < 3 * NBK)
-      __builtin_amdgcn_global_load_lds(a.side + min(blk0 + lane / NBK, blast) * NBK + lane % NBK,
-                                       (__attribute__((address_space(3))) void*)(stile[st] + 3 * NBK * w), 4, 0, 0);
+    if constexpr (TB > 1) {
+      const size_t blk0 = row0 / TB, blast = (row0 + last) / TB;
+      if (lane < 3 * NBK)
+        __builtin_amdgcn_global_load_lds(a.side + min(blk0 + lane / NBK, blast) * NBK + lane % NBK,
+                                         (__attribute__((address_space(3))) void*)(stile[st] + 3 * NBK * w), 4, 0, 0);
+    } else if (lane < 8 * NBK) {
+      __builtin_amdgcn_global_load_lds(a.side + (row0 + min(swrow, last)) * NBK + swk,
+                                       (__attribute__((address_space(3))) void*)(stile[st] + 8 * NBK * w), 4, 0, 0);
+    }
   };
   int64_t yoff[F];
   int ysrc[F];
@@ -1398,10 +1409,15 @@ __global__ __launch_bounds__(kThreads, 3) void dec_tile(MfmaArgs a) {
     uint8_t* rowp = &qtile[buf][cr * kRowBytes];
     *(u32x4_t*)(rowp + 16 * swz(cr, 2 * cs)) = u32x4_t{v[0], v[1], v[2], v[3]};
     *(u32x4_t*)(rowp + 16 * swz(cr, 2 * cs + 1)) = u32x4_t{v[4], v[5], v[6], v[7]};
-    // side word of the row's 16-token tile (this wave's copy of the slot)
-    const size_t crow = crow0 + size_t(tile) * kTok + rr;
-    const int bi = int(crow / TB - (crow0 + size_t(tile) * kTok) / TB);
-    const uint32_t sw = stile[st][3 * NBK * w + bi * NBK + cblk];
+    // side word of the row's block (tiles: of its 16-token tile, in this wave's copy of the slot)
+    uint32_t sw;
+    if constexpr (TB > 1) {
+      const size_t crow = crow0 + size_t(tile) * kTok + rr;
+      const int bi = int(crow / TB - (crow0 + size_t(tile) * kTok) / TB);
+      sw = stile[st][3 * NBK * w + bi * NBK + cblk];
+    } else {
+      sw = stile[st][rr * NBK + cblk];
+    }
     const float mn = f16_bits_to_f32(sw & 0xffffu), sc = f16_bits_to_f32(sw >> 16);
     if ((16 * cs) % NB == 0) scl[buf][cr][cblk] = sc;
     if constexpr (GC) {
@@ -1913,17 +1929,21 @@ void* enc_by_bits(int bits, int nb, int mode, int bt) {
 }
 
 // (token-channel tiles: blocks of 64 or 128 channels, centred per (token, group) or per
-// (token, block); bf16 output on the tile decoder's LDS ring)
+// (token, block); per-token blocks spanning groups centred per (token, group); bf16 output on
+// dec_centred's LDS ring)
 template <int KS, int BITS, int NB>
-void* dec_kernel(bool bf16, int bt) {
+void* dec_kernel(bool bf16, int bt, bool gsmall) {
   if constexpr (NB >= 64) {
     if (bt == 16) {
-      if (bf16) return (void*)dec_tile<kNP, KS, BITS, NB>;
+      if (bf16) return (void*)dec_centred<kNP, KS, BITS, NB, 16>;
       return (void*)dec_mfma<kNP, KS, BITS, NB, false, 16>;
     }
   }
   if constexpr (NB <= 64) {
     if (bt == 1) {
+      if constexpr (KS == 2 && centred_stages(BITS, kD / NB, 1) >= 3) {
+        if (bf16 && gsmall) return (void*)dec_centred<kNP, KS, BITS, NB, 1>;
+      }
       if (bf16) return (void*)dec_mfma<kNP, KS, BITS, NB, true>;
       return (void*)dec_mfma<kNP, KS, BITS, NB, false>;
     }
@@ -1932,24 +1952,24 @@ void* dec_kernel(bool bf16, int bt) {
 }
 
 template <int KS, int BITS>
-void* dec_by_nb(int nb, bool bf16, int bt) {
+void* dec_by_nb(int nb, bool bf16, int bt, bool gsmall) {
   switch (nb) {
-    case 16: return dec_kernel<KS, BITS, 16>(bf16, bt);
-    case 32: return dec_kernel<KS, BITS, 32>(bf16, bt);
-    case 64: return dec_kernel<KS, BITS, 64>(bf16, bt);
-    case 128: return dec_kernel<KS, BITS, 128>(bf16, bt);
+    case 16: return dec_kernel<KS, BITS, 16>(bf16, bt, gsmall);
+    case 32: return dec_kernel<KS, BITS, 32>(bf16, bt, gsmall);
+    case 64: return dec_kernel<KS, BITS, 64>(bf16, bt, gsmall);
+    case 128: return dec_kernel<KS, BITS, 128>(bf16, bt, gsmall);
   }
   return nullptr;
 }
 
 template <int KS>
-void* dec_by_bits(int bits, int nb, bool bf16, int bt) {
+void* dec_by_bits(int bits, int nb, bool bf16, int bt, bool gsmall) {
   switch (bits) {
-    case 2: return dec_by_nb<KS, 2>(nb, bf16, bt);
-    case 3: return dec_by_nb<KS, 3>(nb, bf16, bt);
-    case 4: return dec_by_nb<KS, 4>(nb, bf16, bt);
-    case 6: return dec_by_nb<KS, 6>(nb, bf16, bt);
-    case 8: return dec_by_nb<KS, 8>(nb, bf16, bt);
+    case 2: return dec_by_nb<KS, 2>(nb, bf16, bt, gsmall);
+    case 3: return dec_by_nb<KS, 3>(nb, bf16, bt, gsmall);
+    case 4: return dec_by_nb<KS, 4>(nb, bf16, bt, gsmall);
+    case 6: return dec_by_nb<KS, 6>(nb, bf16, bt, gsmall);
+    case 8: return dec_by_nb<KS, 8>(nb, bf16, bt, gsmall);
   }
   return nullptr;
 }
@@ -2136,9 +2156,9 @@ hipError_t launch_decode_mfma(int s, const CacheDev& k, int l0, const GaugeDev& 
   }
   if (!fn) {
     switch (ksteps(G.g)) {
-      case 2: fn = dec_by_bits<2>(c.bits, nb, Y.bf16, bt); break;
-      case 4: fn = dec_by_bits<4>(c.bits, nb, Y.bf16, bt); break;
-      case 8: fn = dec_by_bits<8>(c.bits, nb, Y.bf16, bt); break;
+      case 2: fn = dec_by_bits<2>(c.bits, nb, Y.bf16, bt, G.g < nb); break;
+      case 4: fn = dec_by_bits<4>(c.bits, nb, Y.bf16, bt, G.g < nb); break;
+      case 8: fn = dec_by_bits<8>(c.bits, nb, Y.bf16, bt, G.g < nb); break;
     }
   }
   if (!fn) return hipErrorInvalidValue;
