@@ -170,16 +170,26 @@ __global__ __launch_bounds__(256) void grad_reduce(const double* part, int npart
   }
 }
 
-// C = A B (+ C when acc) for g x g row-major binary64 matrices in global memory, by the whole
-// workgroup: 32 x 32 output tiles, four outputs per thread, 32-wide K steps through LDS.
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+
+// C (+)= A B for g x g binary64 matrices in global memory, by the whole workgroup, through 32 x 32
+// LDS tiles.  With g a multiple of 32 each of the four waves takes one 16 x 16 quarter of the
+// output tile on the matrix cores (v_mfma_f64_16x16x4f64: binary64 products and sums; lane l
+// supplies A[l % 16][l / 16] and B[l / 16][l % 16] of each 16 x 4 by 4 x 16 step and holds
+// D[4 v + l / 16][l % 16], v < 4); otherwise binary64 FMAs on the VALU, four outputs per thread.
 // Callers separate dependent products with barriers.
 __device__ void wg_gemm(const double* A, const double* B, double* C, int g, bool acc) {
+  static_assert(kGradThreads == 256, "four waves, one output quarter each");
   __shared__ double as[32][33], bs[32][33];
   const int tid = int(threadIdx.x), r = tid >> 3, c4 = (tid & 7) * 4;
+  const int lane = tid & 63, w = tid >> 6, qi = (w >> 1) * 16, qj = (w & 1) * 16;
+  const int mi = lane & 15, mk = lane >> 4;
+  const bool mf = (g & 31) == 0;
   const int nt = (g + 31) / 32;
   for (int tile = 0; tile < nt * nt; ++tile) {
     const int i0 = 32 * (tile / nt), j0 = 32 * (tile % nt);
     double o[4] = {0.0, 0.0, 0.0, 0.0};
+    f64x4_t dq = {0.0, 0.0, 0.0, 0.0};
     for (int k0 = 0; k0 < g; k0 += 32) {
       __syncthreads();
       for (int idx = tid; idx < 32 * 32; idx += kGradThreads) {
@@ -188,14 +198,26 @@ __device__ void wg_gemm(const double* A, const double* B, double* C, int g, bool
         bs[rr][cc] = (k0 + rr < g && j0 + cc < g) ? B[size_t(k0 + rr) * g + j0 + cc] : 0.0;
       }
       __syncthreads();
-#pragma unroll 8
-      for (int k = 0; k < 32; ++k) {
-        const double av = as[r][k];
+      if (mf) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = fma(av, bs[k][c4 + q], o[q]);
+        for (int kk = 0; kk < 32; kk += 4)
+          dq = __builtin_amdgcn_mfma_f64_16x16x4f64(as[qi + mi][kk + mk], bs[kk + mk][qj + mi], dq, 0, 0, 0);
+      } else {
+#pragma unroll 8
+        for (int k = 0; k < 32; ++k) {
+          const double av = as[r][k];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) o[q] = fma(av, bs[k][c4 + q], o[q]);
+        }
       }
     }
-    if (i0 + r < g) {
+    if (mf) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        double* p = C + size_t(i0 + qi + 4 * v + mk) * g + j0 + qj + mi;
+        *p = acc ? *p + dq[v] : dq[v];
+      }
+    } else if (i0 + r < g) {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         if (j0 + c4 + q < g) {
