@@ -229,6 +229,77 @@ __device__ void wg_gemm(const double* A, const double* B, double* C, int g, bool
   __syncthreads();
 }
 
+// C (+)= A B for g a multiple of 64: 64 x 64 output tiles, each wave a 32 x 32 quarter of four
+// 16 x 16 matrix-core tiles (lanes as in wg_gemm), 32-wide K chunks through LDS.  Each thread
+// loads its share of the next chunk (the next tile's first one after a tile's last) into
+// registers while the waves multiply the current one, so the global loads' latency overlaps 32
+// products per wave (a second register stage spills).  Callers separate dependent products with barriers; C is neither A nor B.
+__device__ void wg_gemm64(const double* A, const double* B, double* C, int g, bool acc) {
+  static_assert(kGradThreads == 256, "four waves, one output quarter each");
+  __shared__ double as[64][33], bs[32][65];
+  const int tid = int(threadIdx.x), lane = tid & 63, w = tid >> 6;
+  const int qi = (w >> 1) * 32, qj = (w & 1) * 32, mi = lane & 15, mk = lane >> 4;
+  const int nt = g / 64, nk = g / 32, niter = nt * nt * nk;
+  double ra[8], rb[8];
+  auto fetch = [&](int it) {
+    const int tile = it / nk, k0 = 32 * (it % nk), i0 = 64 * (tile / nt), j0 = 64 * (tile % nt);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int idx = tid + kGradThreads * q;
+      ra[q] = A[size_t(i0 + (idx >> 5)) * g + k0 + (idx & 31)];
+      rb[q] = B[size_t(k0 + (idx >> 6)) * g + j0 + (idx & 63)];
+    }
+  };
+  f64x4_t dq[2][2];
+  fetch(0);
+  for (int it = 0; it < niter; ++it) {
+    const int tile = it / nk, kc = it % nk, i0 = 64 * (tile / nt), j0 = 64 * (tile % nt);
+    if (kc == 0) {
+#pragma unroll
+      for (int ti = 0; ti < 2; ++ti)
+#pragma unroll
+        for (int tj = 0; tj < 2; ++tj) dq[ti][tj] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+    }
+    __syncthreads();  // the previous chunk's reads are done
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int idx = tid + kGradThreads * q;
+      as[idx >> 5][idx & 31] = ra[q];
+      bs[idx >> 6][idx & 63] = rb[q];
+    }
+    __syncthreads();
+    if (it + 1 < niter) fetch(it + 1);
+#pragma unroll
+    for (int kk = 0; kk < 32; kk += 4) {
+      const double a0 = as[qi + mi][kk + mk], a1 = as[qi + 16 + mi][kk + mk];
+      const double b0 = bs[kk + mk][qj + mi], b1 = bs[kk + mk][qj + 16 + mi];
+      dq[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, dq[0][0], 0, 0, 0);
+      dq[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, dq[0][1], 0, 0, 0);
+      dq[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, dq[1][0], 0, 0, 0);
+      dq[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, dq[1][1], 0, 0, 0);
+    }
+    if (kc == nk - 1) {
+#pragma unroll
+      for (int ti = 0; ti < 2; ++ti)
+#pragma unroll
+        for (int tj = 0; tj < 2; ++tj)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            double* p = C + size_t(i0 + qi + 16 * ti + 4 * v + mk) * g + j0 + qj + 16 * tj + mi;
+            *p = acc ? *p + dq[ti][tj][v] : dq[ti][tj][v];
+          }
+    }
+  }
+  __syncthreads();
+}
+
+// The product for any supported g: 64 x 64 matrix-core tiles when g is a multiple of 64, else
+// wg_gemm's 32 x 32 tiles.
+__device__ void wg_product(const double* A, const double* B, double* C, int g, bool acc) {
+  if ((g & 63) == 0) wg_gemm64(A, B, C, g, acc);
+  else wg_gemm(A, B, C, g, acc);
+}
+
 // 1-norm (largest column sum of |.|) of a g x g matrix, by the whole workgroup
 __device__ double wg_norm1(const double* Mx, int g, double* red) {
   double best = 0.0;
@@ -301,9 +372,9 @@ __global__ __launch_bounds__(kGradThreads) void grad_frechet(const double* dM, c
   __syncthreads();
   // exp(W) = [[P1, P2], [0, P1]] by Horner's rule: P <- I + W P / k for k = terms .. 1
   for (int k = kFrechetTerms; k >= 1; --k) {
-    wg_gemm(Mm, P1, T1, g, false);
-    wg_gemm(Mm, P2, T2, g, false);
-    wg_gemm(Es, P1, T2, g, true);
+    wg_product(Mm, P1, T1, g, false);
+    wg_product(Mm, P2, T2, g, false);
+    wg_product(Es, P1, T2, g, true);
     const double ik = 1.0 / k;
     for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
       P1[idx] = ((idx / g == idx % g) ? 1.0 : 0.0) + T1[idx] * ik;
@@ -313,9 +384,9 @@ __global__ __launch_bounds__(kGradThreads) void grad_frechet(const double* dM, c
   }
   // squaring: [[P1, P2], [0, P1]]^2 = [[P1 P1, P1 P2 + P2 P1], [0, P1 P1]]
   for (int q = 0; q < sq; ++q) {
-    wg_gemm(P1, P1, T1, g, false);
-    wg_gemm(P1, P2, T2, g, false);
-    wg_gemm(P2, P1, T2, g, true);
+    wg_product(P1, P1, T1, g, false);
+    wg_product(P1, P2, T2, g, false);
+    wg_product(P2, P1, T2, g, true);
     for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
       P1[idx] = T1[idx];
       P2[idx] = T2[idx];
