@@ -34,17 +34,30 @@ namespace {
 constexpr int kGradThreads = 256;
 constexpr int kFrechetTerms = 16;  // series terms of exp(W / 2^s) with |W / 2^s|_1 <= 1/2
 
+// cos(pi k / (2 d)) for k < 4 d, by the workgroup into LDS: the orthonormal DCT-II entry
+// C_d[v][c] = sqrt((v ? 2 : 1) / d) cos(pi (2 c + 1) v / (2 d)) is that table at ((2 c + 1) v) mod 4 d
+// (the argument is a multiple of 1 / (2 d), exact in binary64, and the cosine has period 2 pi).
+constexpr int kMaxD = 128;
+__device__ void dct_table(double* tab, int d) {
+  for (int k = int(threadIdx.x); k < 4 * d; k += int(blockDim.x)) tab[k] = cospi(double(k) / (2.0 * d));
+  __syncthreads();
+}
+__device__ __forceinline__ double dct_entry(const double* tab, int d, int v, int c) {
+  return sqrt((v == 0 ? 1.0 : 2.0) / d) * tab[((2 * c + 1) * v) % (4 * d)];
+}
+
 // M = C_d G_{l,s,h} per (l, h), binary64 sums rounded to binary32: [L][H][d][d]
 __global__ __launch_bounds__(256) void grad_prep(int s, GaugeDev G, int H, int d, float* M) {
+  __shared__ double tab[4 * kMaxD];
+  dct_table(tab, d);
   const int lh = blockIdx.y, l = lh / H, h = lh - l * H;
   const int g = G.g;
   for (int idx = blockIdx.x * blockDim.x + threadIdx.x; idx < d * d; idx += gridDim.x * blockDim.x) {
     const int v = idx / d, c = idx - v * d, r = c / g, j = c - r * g;
     double acc = 0.0;
-    for (int a = 0; a < g; ++a) {
-      const double cv = sqrt((v == 0 ? 1.0 : 2.0) / d) * cospi((2.0 * (r * g + a) + 1.0) * v / (2.0 * d));
-      acc = fma(cv, double(G.f32[((((size_t(l) * 2 + s) * G.H + h) * G.R + r) * g + a) * g + j]), acc);
-    }
+    for (int a = 0; a < g; ++a)
+      acc = fma(dct_entry(tab, d, v, r * g + a), double(G.f32[((((size_t(l) * 2 + s) * G.H + h) * G.R + r) * g + a) * g + j]),
+                acc);
     M[size_t(lh) * d * d + idx] = float(acc);
   }
 }
@@ -159,6 +172,116 @@ __global__ __launch_bounds__(kGradThreads) void grad_data(GradArgs a) {
     for (int j = 0; j < TD; ++j) out[(TD * ty + i) * d + TD * tx + j] = acc[i][j];
 }
 
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+
+// The data pass on the binary64 matrix cores for d = 128, Tb = 16 (v_mfma_f64_16x16x4f64: lane l
+// supplies A[l % 16][l / 16] and B[l / 16][l % 16] of each 16 x 4 by 4 x 16 step and holds
+// D[4 v + l / 16][l % 16], v < 4).  Wave w takes frequencies [32 w, 32 w + 32) of W = X M^T, two
+// 16 x 16 tiles over K = 128 channels (A = the block of X, B = rows of M, binary32 from LDS,
+// exact in binary64); per tile U = C_Tb W and dL/dW = C_Tb^T dL/dU with constant DCT fragments as
+// A and the previous result as B (item s of a 16 x 16 result is the B fragment of K-step s); then
+// dL/dM rows [32 w, 32 w + 32) += (dL/dW)^T X over the block's tokens, the items of dL/dW serving
+// as the A fragments of its transpose.  Each thread loads its share of the next block of X into
+// registers while the waves multiply the current one.
+__global__ __launch_bounds__(kGradThreads) void grad_data_mfma(GradArgs a) {
+  constexpr int d = 128, Tb = 16, MP = 132;  // rows of M and X padded to 132 words
+  extern __shared__ float smf[];
+  float* ms = smf;            // M [d][MP]
+  float* xs = ms + d * MP;    // block of X [Tb][MP]
+  const ViewDev& X = a.X;
+  const int wg = blockIdx.x, chunk = wg % a.chunks, sl = wg / a.chunks;
+  const int h = sl % X.H, b = (sl / X.H) % X.B, l = sl / (X.H * X.B);
+  const int tid = int(threadIdx.x), lane = tid & 63, w = tid >> 6, mi = lane & 15, mk = lane >> 4;
+  const int k0 = chunk * a.blocks_per_wg, k1 = min(a.nblk, k0 + a.blocks_per_wg);
+
+  const float* Mg = a.M + (size_t(l) * X.H + h) * d * d;
+  for (int idx = tid; idx < d * d; idx += kGradThreads) ms[(idx / d) * MP + idx % d] = Mg[idx];
+  // DCT fragments: cu[s] = C[mi][4 s + mk] (A of C W), cv[s] = C[4 s + mk][mi] (A of C^T dL/dU)
+  double cu[4], cv[4];
+#pragma unroll
+  for (int st = 0; st < 4; ++st) {
+    const int t = 4 * st + mk;
+    cu[st] = sqrt((mi == 0 ? 1.0 : 2.0) / Tb) * cospi((2.0 * t + 1.0) * mi / (2.0 * Tb));
+    cv[st] = sqrt((t == 0 ? 1.0 : 2.0) / Tb) * cospi((2.0 * mi + 1.0) * t / (2.0 * Tb));
+  }
+  const double lf = a.stats[4 * l + 0], D = a.stats[4 * l + 3] + 1e-12;
+  const double cf = 2.0 * a.lam_f / D, cr = a.lam_r * a.inv_count, tau = a.tau;
+  f64x4_t acc[2][8];
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+    for (int jt = 0; jt < 8; ++jt) acc[nt][jt] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+  const size_t xbase = size_t(l) * X.sl + size_t(b) * X.sb + size_t(h) * X.sh;
+  float rx[8];
+  auto fetch = [&](int blk) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int idx = tid + kGradThreads * q, t = idx >> 7, c = idx & 127;
+      const size_t off = xbase + size_t(blk * Tb + t) * X.st + c;
+      rx[q] = X.bf16 ? bf16_to_f32(((const uint16_t*)X.ptr)[off]) : ((const float*)X.ptr)[off];
+    }
+  };
+  if (k0 < k1) fetch(k0);
+  for (int blk = k0; blk < k1; ++blk) {
+    __syncthreads();  // the previous block's X is read (and, at the start, M written)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int idx = tid + kGradThreads * q;
+      xs[(idx >> 7) * MP + (idx & 127)] = rx[q];
+    }
+    __syncthreads();
+    if (blk + 1 < k1) fetch(blk + 1);
+    // W tiles: tokens x frequencies 32 w .. 32 w + 15 and 32 w + 16 .. 32 w + 31, two independent
+    // chains sharing the A fragment
+    f64x4_t wt[2] = {{0.0, 0.0, 0.0, 0.0}, {0.0, 0.0, 0.0, 0.0}};
+#pragma unroll 8
+    for (int st = 0; st < 32; ++st) {
+      const double xa = double(xs[mi * MP + 4 * st + mk]);
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt)
+        wt[nt] = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, double(ms[(32 * w + 16 * nt + mi) * MP + 4 * st + mk]),
+                                                      wt[nt], 0, 0, 0);
+    }
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      const int n0 = 32 * w + 16 * nt;
+      const f64x4_t wd = wt[nt];
+      // U = C_Tb W, then dL/dU per element (token frequency 4 v + mk, frequency n0 + mi)
+      f64x4_t ud = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+      for (int st = 0; st < 4; ++st) ud = __builtin_amdgcn_mfma_f64_16x16x4f64(cu[st], wd[st], ud, 0, 0, 0);
+      f64x4_t gu;
+      const double fv = double(n0 + mi) / (d - 1);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const double fu = double(4 * v + mk) / (Tb - 1);
+        const double rho = sqrt(fu * fu + fv * fv) * 0.70710678118654752;
+        const double U = ud[v];
+        const double sg = U > 0.0 ? 1.0 : (U < 0.0 ? -1.0 : 0.0);
+        gu[v] = cf * U * (rho - lf) + cr * sg / (tau + fabs(U));
+      }
+      // dL/dW = C_Tb^T dL/dU
+      f64x4_t gw = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+      for (int st = 0; st < 4; ++st) gw = __builtin_amdgcn_mfma_f64_16x16x4f64(cv[st], gu[st], gw, 0, 0, 0);
+      // dL/dM rows n0 .. n0 + 15 += (dL/dW)^T X
+#pragma unroll
+      for (int jt = 0; jt < 8; ++jt)
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+          acc[nt][jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(gw[st], double(xs[(4 * st + mk) * MP + 16 * jt + mi]),
+                                                             acc[nt][jt], 0, 0, 0);
+    }
+  }
+  double* out = a.part + ((size_t(l) * X.H + h) * (size_t(X.B) * a.chunks) + size_t(b) * a.chunks + chunk) * d * d;
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+    for (int jt = 0; jt < 8; ++jt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) out[size_t(32 * w + 16 * nt + 4 * v + mk) * d + 16 * jt + mi] = acc[nt][jt][v];
+}
+
 // dL/dM per (layer, head): the partials summed in order, binary64
 __global__ __launch_bounds__(256) void grad_reduce(const double* part, int nparts, int d, double* dM) {
   const int lh = blockIdx.y;
@@ -169,8 +292,6 @@ __global__ __launch_bounds__(256) void grad_reduce(const double* part, int npart
     dM[size_t(lh) * dd + idx] = acc;
   }
 }
-
-typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
 // C (+)= A B for g x g binary64 matrices in global memory, by the whole workgroup, through 32 x 32
 // LDS tiles.  With g a multiple of 32 each of the four waves takes one 16 x 16 quarter of the
@@ -293,10 +414,12 @@ __device__ void wg_gemm64(const double* A, const double* B, double* C, int g, bo
   __syncthreads();
 }
 
-// The product for any supported g: 64 x 64 matrix-core tiles when g is a multiple of 64, else
-// wg_gemm's 32 x 32 tiles.
+// The product: 64 x 64 matrix-core tiles (WIDE, g a multiple of 64), else wg_gemm's 32 x 32 tiles
+// (a separate instantiation, so that small groups keep the register budget that lets several
+// blocks share a CU).
+template <bool WIDE>
 __device__ void wg_product(const double* A, const double* B, double* C, int g, bool acc) {
-  if ((g & 63) == 0) wg_gemm64(A, B, C, g, acc);
+  if constexpr (WIDE) wg_gemm64(A, B, C, g, acc);
   else wg_gemm(A, B, C, g, acc);
 }
 
@@ -321,9 +444,12 @@ __device__ double wg_norm1(const double* Mx, int g, double* red) {
 
 // One workgroup per gauge block (l, h, r): dL/dG from dL/dM, then the Frechet adjoint and
 // dL/dA.  work: six g x g binary64 matrices per block.
+template <bool WIDE>
 __global__ __launch_bounds__(kGradThreads) void grad_frechet(const double* dM, const float* A, int s, int H, int R, int g,
                                                              int d, double* work, double* grad) {
   __shared__ double red[kGradThreads];
+  __shared__ double tab[4 * kMaxD];
+  dct_table(tab, d);
   const int blk = blockIdx.x, r = blk % R, lh = blk / R, h = lh % H, l = lh / H;
   const size_t gg = size_t(g) * g;
   double* Mm = work + size_t(blk) * 6 * gg;
@@ -337,10 +463,7 @@ __global__ __launch_bounds__(kGradThreads) void grad_frechet(const double* dM, c
   for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
     const int c = idx / g, k = idx - c * g;
     double acc = 0.0;
-    for (int v = 0; v < d; ++v) {
-      const double cv = sqrt((v == 0 ? 1.0 : 2.0) / d) * cospi((2.0 * (r * g + c) + 1.0) * v / (2.0 * d));
-      acc = fma(cv, dMl[size_t(v) * d + r * g + k], acc);
-    }
+    for (int v = 0; v < d; ++v) acc = fma(dct_entry(tab, d, v, r * g + c), dMl[size_t(v) * d + r * g + k], acc);
     Es[idx] = acc;                                          // dL/dG
     Mm[idx] = double(Ab[size_t(k) * g + c]) - double(Ab[idx]);  // S^T = A^T - A
   }
@@ -372,9 +495,9 @@ __global__ __launch_bounds__(kGradThreads) void grad_frechet(const double* dM, c
   __syncthreads();
   // exp(W) = [[P1, P2], [0, P1]] by Horner's rule: P <- I + W P / k for k = terms .. 1
   for (int k = kFrechetTerms; k >= 1; --k) {
-    wg_product(Mm, P1, T1, g, false);
-    wg_product(Mm, P2, T2, g, false);
-    wg_product(Es, P1, T2, g, true);
+    wg_product<WIDE>(Mm, P1, T1, g, false);
+    wg_product<WIDE>(Mm, P2, T2, g, false);
+    wg_product<WIDE>(Es, P1, T2, g, true);
     const double ik = 1.0 / k;
     for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
       P1[idx] = ((idx / g == idx % g) ? 1.0 : 0.0) + T1[idx] * ik;
@@ -384,9 +507,9 @@ __global__ __launch_bounds__(kGradThreads) void grad_frechet(const double* dM, c
   }
   // squaring: [[P1, P2], [0, P1]]^2 = [[P1 P1, P1 P2 + P2 P1], [0, P1 P1]]
   for (int q = 0; q < sq; ++q) {
-    wg_product(P1, P1, T1, g, false);
-    wg_product(P1, P2, T2, g, false);
-    wg_product(P2, P1, T2, g, true);
+    wg_product<WIDE>(P1, P1, T1, g, false);
+    wg_product<WIDE>(P1, P2, T2, g, false);
+    wg_product<WIDE>(P2, P1, T2, g, true);
     for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
       P1[idx] = T1[idx];
       P2[idx] = T2[idx];
@@ -469,7 +592,14 @@ hipError_t launch_gauge_grad(int s, const ViewDev& X, const GaugeDev& G, const f
   const int nwg = X.L * X.B * X.H * lay.chunks;
   const size_t smem = size_t(2) * Tb * (d + 1) * sizeof(double) +
                       (size_t(d) * (d + 1) + size_t(Tb) * (d + 1) + size_t(Tb) * Tb) * sizeof(float);
-  if (nblk > 0) {
+  if (nblk > 0 && d == 128 && Tb == 16 && !force_generic) {
+    const size_t smf = size_t(128 + 16) * 132 * sizeof(float);
+    if ((e = hipFuncSetAttribute((const void*)grad_data_mfma, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smf)) !=
+        hipSuccess)
+      return e;
+    hipLaunchKernelGGL(grad_data_mfma, dim3(nwg), dim3(kGradThreads), smf, st, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  } else if (nblk > 0) {
     switch (d / 16) {
       case 1: e = launch_data<1>(a, nwg, smem, st); break;
       case 2: e = launch_data<2>(a, nwg, smem, st); break;
@@ -486,8 +616,12 @@ hipError_t launch_gauge_grad(int s, const ViewDev& X, const GaugeDev& G, const f
   const int nparts = nblk > 0 ? X.B * lay.chunks : 0;
   hipLaunchKernelGGL(grad_reduce, dim3((d * d + 255) / 256, X.L * X.H), dim3(256), 0, st, part, nparts, d, dM);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(grad_frechet, dim3(X.L * X.H * R), dim3(kGradThreads), 0, st, dM, A, s, X.H, R, G.g, d, work,
-                     grad);
+  if (G.g % 64 == 0)
+    hipLaunchKernelGGL(grad_frechet<true>, dim3(X.L * X.H * R), dim3(kGradThreads), 0, st, dM, A, s, X.H, R, G.g, d,
+                       work, grad);
+  else
+    hipLaunchKernelGGL(grad_frechet<false>, dim3(X.L * X.H * R), dim3(kGradThreads), 0, st, dM, A, s, X.H, R, G.g, d,
+                       work, grad);
   return hipGetLastError();
 }
 
