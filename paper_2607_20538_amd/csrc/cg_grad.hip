@@ -18,7 +18,7 @@
 // and accumulates its part of dL/dM in binary64 registers (a (d/16) x (d/16) tile per thread),
 // written as one partial per workgroup; grad_reduce sums the partials in a fixed order
 // (deterministic); grad_frechet forms dL/dG and the Frechet adjoint per gauge block in binary64
-// (power series of the scaled block matrix by Horner's rule, then squaring).
+// (power series of the scaled block matrix by the Paterson-Stockmeyer scheme, then squaring).
 // Binary64 through the data pass matters: dL/dA is the antisymmetric part of dL/dS, which for
 // smooth objectives is much smaller than the terms that cancel in it (about 40x on random
 // Llama-shaped data), so binary32 sums over a block's d channels would reach the result.
@@ -33,17 +33,26 @@ namespace {
 
 constexpr int kGradThreads = 256;
 constexpr int kFrechetTerms = 16;  // series terms of exp(W / 2^s) with |W / 2^s|_1 <= 1/2
+// 1 / k!, by successive binary64 divisions (evaluated by the compiler)
+constexpr double inv_fact(int k) {
+  double r = 1.0;
+  for (int i = 2; i <= k; ++i) r /= i;
+  return r;
+}
 
 // cos(pi k / (2 d)) for k < 4 d, by the workgroup into LDS: the orthonormal DCT-II entry
 // C_d[v][c] = sqrt((v ? 2 : 1) / d) cos(pi (2 c + 1) v / (2 d)) is that table at ((2 c + 1) v) mod 4 d
 // (the argument is a multiple of 1 / (2 d), exact in binary64, and the cosine has period 2 pi).
+// Along a row (v fixed) the index advances by 2 v, along a column (c fixed) by 2 c + 1, both
+// below 2 d, so loops step it with one conditional wrap instead of a division.
 constexpr int kMaxD = 128;
 __device__ void dct_table(double* tab, int d) {
   for (int k = int(threadIdx.x); k < 4 * d; k += int(blockDim.x)) tab[k] = cospi(double(k) / (2.0 * d));
   __syncthreads();
 }
-__device__ __forceinline__ double dct_entry(const double* tab, int d, int v, int c) {
-  return sqrt((v == 0 ? 1.0 : 2.0) / d) * tab[((2 * c + 1) * v) % (4 * d)];
+__device__ __forceinline__ int dct_step(int k, int step, int d) {
+  k += step;
+  return k >= 4 * d ? k - 4 * d : k;
 }
 
 // M = C_d G_{l,s,h} per (l, h), binary64 sums rounded to binary32: [L][H][d][d]
@@ -52,12 +61,17 @@ __global__ __launch_bounds__(256) void grad_prep(int s, GaugeDev G, int H, int d
   dct_table(tab, d);
   const int lh = blockIdx.y, l = lh / H, h = lh - l * H;
   const int g = G.g;
+  const double n0 = sqrt(1.0 / d), n1 = sqrt(2.0 / d);
   for (int idx = blockIdx.x * blockDim.x + threadIdx.x; idx < d * d; idx += gridDim.x * blockDim.x) {
     const int v = idx / d, c = idx - v * d, r = c / g, j = c - r * g;
+    const double nv = v == 0 ? n0 : n1;
+    const float* Gc = G.f32 + (((size_t(l) * 2 + s) * G.H + h) * G.R + r) * g * g + j;
+    int k = ((2 * r * g + 1) * v) % (4 * d);  // entry (v, r g + a) for a = 0
     double acc = 0.0;
-    for (int a = 0; a < g; ++a)
-      acc = fma(dct_entry(tab, d, v, r * g + a), double(G.f32[((((size_t(l) * 2 + s) * G.H + h) * G.R + r) * g + a) * g + j]),
-                acc);
+    for (int a = 0; a < g; ++a) {
+      acc = fma(nv * tab[k], double(Gc[size_t(a) * g]), acc);
+      k = dct_step(k, 2 * v, d);
+    }
     M[size_t(lh) * d * d + idx] = float(acc);
   }
 }
@@ -414,26 +428,90 @@ __device__ void wg_gemm64(const double* A, const double* B, double* C, int g, bo
   __syncthreads();
 }
 
-// The product: 64 x 64 matrix-core tiles (WIDE, g a multiple of 64), else wg_gemm's 32 x 32 tiles
-// (a separate instantiation, so that small groups keep the register budget that lets several
-// blocks share a CU).
-template <bool WIDE>
+// C (+)= A B for g = 128 by a 1024-thread workgroup: wave w (of 16) takes the 32 x 32 output
+// quarter at (32 (w / 4), 32 (w % 4)) as four 16 x 16 matrix-core tiles (lanes as in wg_gemm); the
+// whole 128 x 32 chunk of A and 32 x 128 chunk of B of each K step sit in LDS, and each thread
+// loads its four + four entries of the next chunk into registers while the waves multiply.
+// Sixteen waves per CU (four per SIMD) hide the latencies one wave per SIMD leaves exposed.
+constexpr int kWideThreads = 1024;
+__device__ void wg_gemm128(const double* A, const double* B, double* C, bool acc) {
+  __shared__ double as[128][33], bs[32][129];
+  const int tid = int(threadIdx.x), lane = tid & 63, w = tid >> 6;
+  const int qi = (w >> 2) * 32, qj = (w & 3) * 32, mi = lane & 15, mk = lane >> 4;
+  double ra[4], rb[4];
+  auto fetch = [&](int k0) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = tid + kWideThreads * q;
+      ra[q] = A[(idx >> 5) * 128 + k0 + (idx & 31)];  // 32-bit offsets from uniform bases
+      rb[q] = B[(k0 + (idx >> 7)) * 128 + (idx & 127)];
+    }
+  };
+  f64x4_t dq[2][2];
+#pragma unroll
+  for (int ti = 0; ti < 2; ++ti)
+#pragma unroll
+    for (int tj = 0; tj < 2; ++tj) dq[ti][tj] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+  fetch(0);
+#pragma unroll 1
+  for (int kc = 0; kc < 4; ++kc) {
+    __syncthreads();  // the previous chunk's reads are done
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = tid + kWideThreads * q;
+      as[idx >> 5][idx & 31] = ra[q];
+      bs[idx >> 7][idx & 127] = rb[q];
+    }
+    __syncthreads();
+    if (kc < 3) fetch(32 * (kc + 1));
+#pragma unroll
+    for (int kk = 0; kk < 32; kk += 4) {
+      const double a0 = as[qi + mi][kk + mk], a1 = as[qi + 16 + mi][kk + mk];
+      const double b0 = bs[kk + mk][qj + mi], b1 = bs[kk + mk][qj + 16 + mi];
+      dq[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, dq[0][0], 0, 0, 0);
+      dq[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, dq[0][1], 0, 0, 0);
+      dq[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, dq[1][0], 0, 0, 0);
+      dq[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, dq[1][1], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int ti = 0; ti < 2; ++ti)
+#pragma unroll
+    for (int tj = 0; tj < 2; ++tj)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        double* p = C + ((qi + 16 * ti + 4 * v + mk) * 128 + qj + 16 * tj + mi);
+        *p = acc ? *p + dq[ti][tj][v] : dq[ti][tj][v];
+      }
+  __syncthreads();
+}
+
+// Products of the Frechet kernel by gauge width: kFrechet128 (g = 128, 1024 threads),
+// kFrechet64 (g a multiple of 64, 64 x 64 tiles), kFrechetSmall (wg_gemm's 32 x 32 tiles; a
+// separate instantiation, so that small groups keep the register budget that lets several blocks
+// share a CU).
+enum { kFrechetSmall = 0, kFrechet64 = 1, kFrechet128 = 2 };
+template <int MODE>
+constexpr int frechet_threads() { return MODE == kFrechet128 ? kWideThreads : kGradThreads; }
+template <int MODE>
 __device__ void wg_product(const double* A, const double* B, double* C, int g, bool acc) {
-  if constexpr (WIDE) wg_gemm64(A, B, C, g, acc);
+  if constexpr (MODE == kFrechet128) wg_gemm128(A, B, C, acc);
+  else if constexpr (MODE == kFrechet64) wg_gemm64(A, B, C, g, acc);
   else wg_gemm(A, B, C, g, acc);
 }
 
-// 1-norm (largest column sum of |.|) of a g x g matrix, by the whole workgroup
+// 1-norm (largest column sum of |.|) of a g x g matrix, by the whole workgroup of NT threads
+template <int NT>
 __device__ double wg_norm1(const double* Mx, int g, double* red) {
   double best = 0.0;
-  for (int j = int(threadIdx.x); j < g; j += kGradThreads) {
+  for (int j = int(threadIdx.x); j < g; j += NT) {
     double s = 0.0;
     for (int i = 0; i < g; ++i) s += fabs(Mx[size_t(i) * g + j]);
     best = fmax(best, s);
   }
   red[threadIdx.x] = best;
   __syncthreads();
-  for (int o = kGradThreads / 2; o > 0; o >>= 1) {
+  for (int o = NT / 2; o > 0; o >>= 1) {
     if (int(threadIdx.x) < o) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + o]);
     __syncthreads();
   }
@@ -443,41 +521,54 @@ __device__ double wg_norm1(const double* Mx, int g, double* red) {
 }
 
 // One workgroup per gauge block (l, h, r): dL/dG from dL/dM, then the Frechet adjoint and
-// dL/dA.  work: six g x g binary64 matrices per block.
-template <bool WIDE>
-__global__ __launch_bounds__(kGradThreads) void grad_frechet(const double* dM, const float* A, int s, int H, int R, int g,
+// dL/dA.  work: twelve g x g binary64 matrices per block.
+template <int MODE>
+__global__ __launch_bounds__(frechet_threads<MODE>()) void grad_frechet(const double* dM, const float* A, int s, int H, int R, int g,
                                                              int d, double* work, double* grad) {
-  __shared__ double red[kGradThreads];
+  constexpr int NT = frechet_threads<MODE>();
+  __shared__ double red[NT];
   __shared__ double tab[4 * kMaxD];
   dct_table(tab, d);
   const int blk = blockIdx.x, r = blk % R, lh = blk / R, h = lh % H, l = lh / H;
   const size_t gg = size_t(g) * g;
-  double* Mm = work + size_t(blk) * 6 * gg;
+  const double n0 = sqrt(1.0 / d), n1 = sqrt(2.0 / d);
+  double* Mm = work + size_t(blk) * 12 * gg;  // W = [[Mm, Es], [0, Mm]], then its powers 2..4
   double* Es = Mm + gg;
-  double* P1 = Es + gg;
+  double* S2 = Es + gg;
+  double* D2 = S2 + gg;
+  double* S3 = D2 + gg;
+  double* D3 = S3 + gg;
+  double* S4 = D3 + gg;
+  double* D4 = S4 + gg;
+  double* P1 = D4 + gg;  // the running polynomial [[P1, P2], [0, P1]]
   double* P2 = P1 + gg;
   double* T1 = P2 + gg;
   double* T2 = T1 + gg;
   const double* dMl = dM + size_t(lh) * d * d;
   const float* Ab = A + ((((size_t(l) * 2 + s) * H + h) * R + r) * gg);
-  for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
+#pragma nounroll
+  for (int idx = int(threadIdx.x); idx < int(gg); idx += NT) {
     const int c = idx / g, k = idx - c * g;
-    double acc = 0.0;
-    for (int v = 0; v < d; ++v) acc = fma(dct_entry(tab, d, v, r * g + c), dMl[size_t(v) * d + r * g + k], acc);
+    const int step = 2 * (r * g + c) + 1;  // column r g + c of C_d, rows v = 0, 1, ...
+    double acc = n0 * dMl[r * g + k];       // the table's entry 0 is cos 0 = 1
+    for (int v = 1, ti = step; v < d; ++v, ti = dct_step(ti, step, d))
+      acc = fma(n1 * tab[ti], dMl[size_t(v) * d + r * g + k], acc);
     Es[idx] = acc;                                          // dL/dG
     Mm[idx] = double(Ab[size_t(k) * g + c]) - double(Ab[idx]);  // S^T = A^T - A
   }
   __syncthreads();
-  const double e = wg_norm1(Es, g, red);
+  const double e = wg_norm1<NT>(Es, g, red);
   double* out = grad + size_t(blk) * gg;
   if (!(e > 0.0)) {
-    for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) out[idx] = 0.0;
+#pragma nounroll
+    for (int idx = int(threadIdx.x); idx < int(gg); idx += NT) out[idx] = 0.0;
     return;
   }
   // W = [[S^T, E / e], [0, S^T]] halved sq times until its 1-norm (at most |S^T|_1 + 1) is <= 1/2
-  double nw = wg_norm1(Mm, g, red) + 1.0;
+  double nw = wg_norm1<NT>(Mm, g, red) + 1.0;
   if (!isfinite(nw) || !isfinite(e)) {  // non-finite generators or statistics: no scaling ends
-    for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) out[idx] = __builtin_nan("");
+#pragma nounroll
+    for (int idx = int(threadIdx.x); idx < int(gg); idx += NT) out[idx] = __builtin_nan("");
     return;
   }
   int sq = 0;
@@ -486,38 +577,59 @@ __global__ __launch_bounds__(kGradThreads) void grad_frechet(const double* dM, c
     ++sq;
   }
   const double fm = ldexp(1.0, -sq), fe = fm / e;
-  for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
+#pragma nounroll
+  for (int idx = int(threadIdx.x); idx < int(gg); idx += NT) {
     Mm[idx] *= fm;
     Es[idx] *= fe;
-    P1[idx] = (idx / g == idx % g) ? 1.0 : 0.0;
-    P2[idx] = 0.0;
   }
   __syncthreads();
-  // exp(W) = [[P1, P2], [0, P1]] by Horner's rule: P <- I + W P / k for k = terms .. 1
-  for (int k = kFrechetTerms; k >= 1; --k) {
-    wg_product<WIDE>(Mm, P1, T1, g, false);
-    wg_product<WIDE>(Mm, P2, T2, g, false);
-    wg_product<WIDE>(Es, P1, T2, g, true);
-    const double ik = 1.0 / k;
-    for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
-      P1[idx] = ((idx / g == idx % g) ? 1.0 : 0.0) + T1[idx] * ik;
-      P2[idx] = T2[idx] * ik;
+  // exp(W) ~= sum_{k <= 16} W^k / k! (Paterson-Stockmeyer): with B_j = sum_{i < 4} W^i / (4j + i)!,
+  // p = B_0 + W^4 (B_1 + W^4 (B_2 + W^4 (B_3 + W^4 / 16!))), then p squared sq times.  Matrices of
+  // the form [[X, Y], [0, X]] (powers of W, polynomials in W) are held as their two g x g parts; a
+  // product of two is [[X X', X Y' + Y X'], [0, X X']], three g x g products.  Steps: W^2, W^3,
+  // W^4 (0-2), three products by W^4 (3-5), each followed by adding B_j, then the squarings.  One
+  // call site of the product keeps a single inlined copy of it (and its register budget).
+  static_assert(kFrechetTerms == 16, "four groups of four terms and W^16");
+  // P = B_j + c (Ts, Td): after a product by W^4 (c = 1), or for j = 3 from W^4 itself (c = 1 / 16!)
+  auto add_b = [&](int j, const double* Ts, const double* Td, double c) {
+    const double c0 = j == 3 ? inv_fact(12) : (j == 2 ? inv_fact(8) : (j == 1 ? inv_fact(4) : 1.0));
+    const double c1 = j == 3 ? inv_fact(13) : (j == 2 ? inv_fact(9) : (j == 1 ? inv_fact(5) : 1.0));
+    const double c2 = j == 3 ? inv_fact(14) : (j == 2 ? inv_fact(10) : (j == 1 ? inv_fact(6) : inv_fact(2)));
+    const double c3 = j == 3 ? inv_fact(15) : (j == 2 ? inv_fact(11) : (j == 1 ? inv_fact(7) : inv_fact(3)));
+#pragma nounroll
+    for (int idx = int(threadIdx.x); idx < int(gg); idx += NT) {
+      const double id = (idx / g == idx % g) ? c0 : 0.0;
+      P1[idx] = id + c1 * Mm[idx] + c2 * S2[idx] + c3 * S3[idx] + c * Ts[idx];
+      P2[idx] = c1 * Es[idx] + c2 * D2[idx] + c3 * D3[idx] + c * Td[idx];
     }
     __syncthreads();
-  }
-  // squaring: [[P1, P2], [0, P1]]^2 = [[P1 P1, P1 P2 + P2 P1], [0, P1 P1]]
-  for (int q = 0; q < sq; ++q) {
-    wg_product<WIDE>(P1, P1, T1, g, false);
-    wg_product<WIDE>(P1, P2, T2, g, false);
-    wg_product<WIDE>(P2, P1, T2, g, true);
-    for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
-      P1[idx] = T1[idx];
-      P2[idx] = T2[idx];
+  };
+  for (int step = 0; step < 6 + sq; ++step) {
+    const double *Xs, *Xd, *Ys, *Yd;
+    double *Cs, *Cd;
+    if (step == 0) { Xs = Mm; Xd = Es; Ys = Mm; Yd = Es; Cs = S2; Cd = D2; }
+    else if (step == 1) { Xs = S2; Xd = D2; Ys = Mm; Yd = Es; Cs = S3; Cd = D3; }
+    else if (step == 2) { Xs = S2; Xd = D2; Ys = S2; Yd = D2; Cs = S4; Cd = D4; }
+    else if (step < 6) { Xs = S4; Xd = D4; Ys = P1; Yd = P2; Cs = T1; Cd = T2; }
+    else { Xs = P1; Xd = P2; Ys = P1; Yd = P2; Cs = T1; Cd = T2; }
+    if (step == 3) add_b(3, S4, D4, inv_fact(16));
+#pragma unroll 1
+    for (int q = 0; q < 3; ++q)  // Cs = Xs Ys, Cd = Xs Yd + Xd Ys
+      wg_product<MODE>(q == 2 ? Xd : Xs, q == 0 ? Ys : (q == 1 ? Yd : Ys), q == 0 ? Cs : Cd, g, q == 2);
+    if (step >= 3 && step < 6) {
+      add_b(5 - step, T1, T2, 1.0);
+    } else if (step >= 6) {
+#pragma nounroll
+      for (int idx = int(threadIdx.x); idx < int(gg); idx += NT) {
+        P1[idx] = T1[idx];
+        P2[idx] = T2[idx];
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
   // dL/dS = e P2, dL/dA = dL/dS - (dL/dS)^T
-  for (int idx = int(threadIdx.x); idx < int(gg); idx += kGradThreads) {
+#pragma nounroll
+  for (int idx = int(threadIdx.x); idx < int(gg); idx += NT) {
     const int i = idx / g, j = idx - i * g;
     out[idx] = e * (P2[idx] - P2[size_t(j) * g + i]);
   }
@@ -555,7 +667,7 @@ GradLayout grad_layout(const cg_gauge_shape& s, int B, int T, int Tb) {
   o.off_dm = off;
   off = align256(off + nlh * dd * 8);
   o.off_work = off;
-  off = align256(off + nlh * (s.d / s.g) * 6 * gg * 8);
+  off = align256(off + nlh * (s.d / s.g) * 12 * gg * 8);
   o.total = off;
   return o;
 }
@@ -616,12 +728,15 @@ hipError_t launch_gauge_grad(int s, const ViewDev& X, const GaugeDev& G, const f
   const int nparts = nblk > 0 ? X.B * lay.chunks : 0;
   hipLaunchKernelGGL(grad_reduce, dim3((d * d + 255) / 256, X.L * X.H), dim3(256), 0, st, part, nparts, d, dM);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (G.g % 64 == 0)
-    hipLaunchKernelGGL(grad_frechet<true>, dim3(X.L * X.H * R), dim3(kGradThreads), 0, st, dM, A, s, X.H, R, G.g, d,
-                       work, grad);
+  if (G.g == 128)
+    hipLaunchKernelGGL(grad_frechet<kFrechet128>, dim3(X.L * X.H * R), dim3(kWideThreads), 0, st, dM, A, s, X.H, R, G.g,
+                       d, work, grad);
+  else if (G.g % 64 == 0)
+    hipLaunchKernelGGL(grad_frechet<kFrechet64>, dim3(X.L * X.H * R), dim3(kGradThreads), 0, st, dM, A, s, X.H, R, G.g,
+                       d, work, grad);
   else
-    hipLaunchKernelGGL(grad_frechet<false>, dim3(X.L * X.H * R), dim3(kGradThreads), 0, st, dM, A, s, X.H, R, G.g, d,
-                       work, grad);
+    hipLaunchKernelGGL(grad_frechet<kFrechetSmall>, dim3(X.L * X.H * R), dim3(kGradThreads), 0, st, dM, A, s, X.H, R,
+                       G.g, d, work, grad);
   return hipGetLastError();
 }
 
