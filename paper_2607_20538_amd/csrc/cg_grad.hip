@@ -190,26 +190,34 @@ typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
 // The data pass on the binary64 matrix cores for d = 128, Tb = 16 (v_mfma_f64_16x16x4f64: lane l
 // supplies A[l % 16][l / 16] and B[l / 16][l % 16] of each 16 x 4 by 4 x 16 step and holds
-// D[4 v + l / 16][l % 16], v < 4).  Wave w takes frequencies [32 w, 32 w + 32) of W = X M^T, two
-// 16 x 16 tiles over K = 128 channels (A = the block of X, B = rows of M, binary32 from LDS,
-// exact in binary64); per tile U = C_Tb W and dL/dW = C_Tb^T dL/dU with constant DCT fragments as
-// A and the previous result as B (item s of a 16 x 16 result is the B fragment of K-step s); then
-// dL/dM rows [32 w, 32 w + 32) += (dL/dW)^T X over the block's tokens, the items of dL/dW serving
-// as the A fragments of its transpose.  Each thread loads its share of the next block of X into
+// D[4 v + l / 16][l % 16], v < 4), by 512-thread workgroups: wave w takes frequencies
+// [16 w, 16 w + 16) of W = X M^T, one 16 x 16 tile over K = 128 channels (A = the block of X from
+// LDS, B = the wave's 16 rows of M, held in registers; both exact in binary64); then U = C_Tb W and
+// dL/dW = C_Tb^T dL/dU with constant DCT fragments as A and the previous result as B (item s of a
+// 16 x 16 result is the B fragment of K-step s); then dL/dM rows [16 w, 16 w + 16) += (dL/dW)^T X
+// over the block's tokens, the items of dL/dW serving as the A fragments of its transpose.  Eight
+// waves keep two per SIMD (a wave's 16 rows of dL/dM take 64 accumulator registers), so one wave's
+// matrix-core chain runs while the other's loads and dL/dU arithmetic wait.  The block of X is
+// converted to binary64 once, as it is staged; each thread loads its share of the next block into
 // registers while the waves multiply the current one.
-__global__ __launch_bounds__(kGradThreads) void grad_data_mfma(GradArgs a) {
-  constexpr int d = 128, Tb = 16, MP = 132;  // rows of M and X padded to 132 words
-  extern __shared__ float smf[];
-  float* ms = smf;            // M [d][MP]
-  float* xs = ms + d * MP;    // block of X [Tb][MP]
+constexpr int kDataThreads = 512;
+__global__ __launch_bounds__(kDataThreads) void grad_data_mfma(GradArgs a) {
+  constexpr int d = 128, Tb = 16, XP = 130;  // rows of the staged block padded to 130 doubles
+  extern __shared__ double smd2[];
+  double* xs = smd2;           // block of X [Tb][XP], binary64
+  double* rw = xs + Tb * XP;   // frequency weights [Tb][d]
   const ViewDev& X = a.X;
   const int wg = blockIdx.x, chunk = wg % a.chunks, sl = wg / a.chunks;
   const int h = sl % X.H, b = (sl / X.H) % X.B, l = sl / (X.H * X.B);
   const int tid = int(threadIdx.x), lane = tid & 63, w = tid >> 6, mi = lane & 15, mk = lane >> 4;
+  const int n0 = 16 * w;  // this wave's frequencies
   const int k0 = chunk * a.blocks_per_wg, k1 = min(a.nblk, k0 + a.blocks_per_wg);
 
-  const float* Mg = a.M + (size_t(l) * X.H + h) * d * d;
-  for (int idx = tid; idx < d * d; idx += kGradThreads) ms[(idx / d) * MP + idx % d] = Mg[idx];
+  // B fragments of W = X M^T: mf[s] = M[n0 + mi][4 s + mk]
+  const float* Mg = a.M + ((size_t(l) * X.H + h) * d + n0 + mi) * d + mk;
+  double mf[32];
+#pragma unroll
+  for (int st = 0; st < 32; ++st) mf[st] = double(Mg[4 * st]);
   // DCT fragments: cu[s] = C[mi][4 s + mk] (A of C W), cv[s] = C[4 s + mk][mi] (A of C^T dL/dU)
   double cu[4], cv[4];
 #pragma unroll
@@ -220,80 +228,74 @@ __global__ __launch_bounds__(kGradThreads) void grad_data_mfma(GradArgs a) {
   }
   const double lf = a.stats[4 * l + 0], D = a.stats[4 * l + 3] + 1e-12;
   const double cf = 2.0 * a.lam_f / D, cr = a.lam_r * a.inv_count, tau = a.tau;
-  f64x4_t acc[2][8];
+  // the L_freq factor of dL/dU per coefficient, the same for every block of the layer:
+  // rw[u][v] = 2 lambda_f (rho(u, v) - L_freq) / D
+  for (int idx = tid; idx < Tb * d; idx += kDataThreads) {
+    const int u = idx >> 7, v = idx & 127;
+    const double fu = double(u) / (Tb - 1), fv = double(v) / (d - 1);
+    rw[idx] = cf * (sqrt(fu * fu + fv * fv) * 0.70710678118654752 - lf);
+  }
+  f64x4_t acc[8];
 #pragma unroll
-  for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-    for (int jt = 0; jt < 8; ++jt) acc[nt][jt] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+  for (int jt = 0; jt < 8; ++jt) acc[jt] = f64x4_t{0.0, 0.0, 0.0, 0.0};
   const size_t xbase = size_t(l) * X.sl + size_t(b) * X.sb + size_t(h) * X.sh;
-  float rx[8];
+  constexpr int XQ = Tb * d / kDataThreads;  // entries of a block of X per thread
+  float rx[XQ];
   auto fetch = [&](int blk) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int idx = tid + kGradThreads * q, t = idx >> 7, c = idx & 127;
+    for (int q = 0; q < XQ; ++q) {
+      const int idx = tid + kDataThreads * q, t = idx >> 7, c = idx & 127;
       const size_t off = xbase + size_t(blk * Tb + t) * X.st + c;
       rx[q] = X.bf16 ? bf16_to_f32(((const uint16_t*)X.ptr)[off]) : ((const float*)X.ptr)[off];
     }
   };
   if (k0 < k1) fetch(k0);
   for (int blk = k0; blk < k1; ++blk) {
-    __syncthreads();  // the previous block's X is read (and, at the start, M written)
+    __syncthreads();  // the previous block's X is read (and, at the start, rw written)
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int idx = tid + kGradThreads * q;
-      xs[(idx >> 7) * MP + (idx & 127)] = rx[q];
+    for (int q = 0; q < XQ; ++q) {
+      const int idx = tid + kDataThreads * q;
+      xs[(idx >> 7) * XP + (idx & 127)] = double(rx[q]);
     }
     __syncthreads();
     if (blk + 1 < k1) fetch(blk + 1);
-    // W tiles: tokens x frequencies 32 w .. 32 w + 15 and 32 w + 16 .. 32 w + 31, two independent
-    // chains sharing the A fragment
-    f64x4_t wt[2] = {{0.0, 0.0, 0.0, 0.0}, {0.0, 0.0, 0.0, 0.0}};
-#pragma unroll 8
-    for (int st = 0; st < 32; ++st) {
-      const double xa = double(xs[mi * MP + 4 * st + mk]);
+    // W tile: tokens x frequencies n0 .. n0 + 15
+    f64x4_t wd = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
-        wt[nt] = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, double(ms[(32 * w + 16 * nt + mi) * MP + 4 * st + mk]),
-                                                      wt[nt], 0, 0, 0);
+    for (int st = 0; st < 32; ++st)
+      wd = __builtin_amdgcn_mfma_f64_16x16x4f64(xs[mi * XP + 4 * st + mk], mf[st], wd, 0, 0, 0);
+    // U = C_Tb W (token frequency 4 v + mk, frequency n0 + mi)
+    f64x4_t ud = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int st = 0; st < 4; ++st) ud = __builtin_amdgcn_mfma_f64_16x16x4f64(cu[st], wd[st], ud, 0, 0, 0);
+    // dL/dU = U rw + lambda_r sign(U) / (N (tau + |U|)); the reciprocal by the hardware's
+    // estimate and two Newton steps (each squares the relative error: below 2^-52 after two)
+    f64x4_t gu;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const double U = ud[v], q = tau + fabs(U);
+      double r = __builtin_amdgcn_rcp(q);
+      r = fma(r, fma(-q, r, 1.0), r);
+      r = fma(r, fma(-q, r, 1.0), r);
+      const double sg = U > 0.0 ? cr : (U < 0.0 ? -cr : 0.0);
+      gu[v] = fma(U, rw[(4 * v + mk) * d + n0 + mi], sg * r);
     }
+    // dL/dW = C_Tb^T dL/dU
+    f64x4_t gw = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      const int n0 = 32 * w + 16 * nt;
-      const f64x4_t wd = wt[nt];
-      // U = C_Tb W, then dL/dU per element (token frequency 4 v + mk, frequency n0 + mi)
-      f64x4_t ud = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-      for (int st = 0; st < 4; ++st) ud = __builtin_amdgcn_mfma_f64_16x16x4f64(cu[st], wd[st], ud, 0, 0, 0);
-      f64x4_t gu;
-      const double fv = double(n0 + mi) / (d - 1);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const double fu = double(4 * v + mk) / (Tb - 1);
-        const double rho = sqrt(fu * fu + fv * fv) * 0.70710678118654752;
-        const double U = ud[v];
-        const double sg = U > 0.0 ? 1.0 : (U < 0.0 ? -1.0 : 0.0);
-        gu[v] = cf * U * (rho - lf) + cr * sg / (tau + fabs(U));
-      }
-      // dL/dW = C_Tb^T dL/dU
-      f64x4_t gw = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-      for (int st = 0; st < 4; ++st) gw = __builtin_amdgcn_mfma_f64_16x16x4f64(cv[st], gu[st], gw, 0, 0, 0);
-      // dL/dM rows n0 .. n0 + 15 += (dL/dW)^T X
-#pragma unroll
-      for (int jt = 0; jt < 8; ++jt)
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-          acc[nt][jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(gw[st], double(xs[(4 * st + mk) * MP + 16 * jt + mi]),
-                                                             acc[nt][jt], 0, 0, 0);
-    }
-  }
-  double* out = a.part + ((size_t(l) * X.H + h) * (size_t(X.B) * a.chunks) + size_t(b) * a.chunks + chunk) * d * d;
-#pragma unroll
-  for (int nt = 0; nt < 2; ++nt)
+    for (int st = 0; st < 4; ++st) gw = __builtin_amdgcn_mfma_f64_16x16x4f64(cv[st], gu[st], gw, 0, 0, 0);
+    // dL/dM rows n0 .. n0 + 15 += (dL/dW)^T X
 #pragma unroll
     for (int jt = 0; jt < 8; ++jt)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) out[size_t(32 * w + 16 * nt + 4 * v + mk) * d + 16 * jt + mi] = acc[nt][jt][v];
+      for (int st = 0; st < 4; ++st)
+        acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(gw[st], xs[(4 * st + mk) * XP + 16 * jt + mi], acc[jt], 0, 0, 0);
+  }
+  double* out = a.part + ((size_t(l) * X.H + h) * (size_t(X.B) * a.chunks) + size_t(b) * a.chunks + chunk) * d * d;
+#pragma unroll
+  for (int jt = 0; jt < 8; ++jt)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) out[size_t(n0 + 4 * v + mk) * d + 16 * jt + mi] = acc[jt][v];
 }
 
 // dL/dM per (layer, head): the partials summed in order, binary64
@@ -705,11 +707,11 @@ hipError_t launch_gauge_grad(int s, const ViewDev& X, const GaugeDev& G, const f
   const size_t smem = size_t(2) * Tb * (d + 1) * sizeof(double) +
                       (size_t(d) * (d + 1) + size_t(Tb) * (d + 1) + size_t(Tb) * Tb) * sizeof(float);
   if (nblk > 0 && d == 128 && Tb == 16 && !force_generic) {
-    const size_t smf = size_t(128 + 16) * 132 * sizeof(float);
+    const size_t smf = (size_t(16) * 130 + size_t(16) * 128) * sizeof(double);
     if ((e = hipFuncSetAttribute((const void*)grad_data_mfma, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smf)) !=
         hipSuccess)
       return e;
-    hipLaunchKernelGGL(grad_data_mfma, dim3(nwg), dim3(kGradThreads), smf, st, a);
+    hipLaunchKernelGGL(grad_data_mfma, dim3(nwg), dim3(kDataThreads), smf, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   } else if (nblk > 0) {
     switch (d / 16) {
