@@ -241,9 +241,16 @@ __global__ __launch_bounds__(kThreads, 2) void spec_mfma(SpecArgs a) {
 
   // energy accumulators of the lane's entries (u = 0..15, v = chA): the lane pair (n, 0) and
   // (n, 1) holds the same entries for the tile's two blocks
+  // (squares summed in binary32 over at most kFold tiles, then added to the binary64 totals:
+  // the terms are positive, so the binary32 partial is within kFold 2^-24 of its value)
+  constexpr int kFold = 8;
   double eacc[16];
+  float ef[16];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) eacc[e] = 0.0;
+  for (int e = 0; e < 16; ++e) {
+    eacc[e] = 0.0;
+    ef[e] = 0.0f;
+  }
   double lacc = 0.0;
   // y^T = x^T M^T of tile t on the matrix cores: the tile is the A operand and the planes of M
   // the B operand, so lane (n, hc) holds channel chA of tokens 8 (e / 4) + 4 hc + e % 4
@@ -276,11 +283,18 @@ __global__ __launch_bounds__(kThreads, 2) void spec_mfma(SpecArgs a) {
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
       const float x = valid ? U[u] : 0.0f;
-      eacc[u] = fma(double(x), double(x), eacc[u]);
+      ef[u] = fmaf(x, x, ef[u]);
       // log2 of an argument >= 1 (v_log_f32); the sum is scaled by ln 2 once, at the end
       ls += __builtin_amdgcn_logf(fmaf(fabsf(x), a.inv_tau, 1.0f));
     }
     lacc += double(ls);
+    if ((t - tb) % kFold == kFold - 1 || t == te - 1) {
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        eacc[u] += double(ef[u]);
+        ef[u] = 0.0f;
+      }
+    }
   };
   // software pipeline: the matrix-core chain of tile t + 1 runs while the VALU works on tile t
   for (int t = tb; t < min(te, tb + kSpecStages - 1); ++t) issue(t);
