@@ -61,10 +61,14 @@ def _run(X, A, s, g, Tb, lam_f=1.0, lam_r=0.02, tau=0.04):
 
 
 # (L, B, H, T, d, g, Tb, dtype): ragged token tails, one to eight gauge groups, head widths with
-# 1 .. 8 accumulator rows per thread, every supported token block of the matrix-free pass
+# 1 .. 8 accumulator rows per thread, every supported token block of the matrix-free pass; d = 128
+# with 16-token blocks (the matrix-core data pass, bf16 and binary32 input) at g = 128, 64 and 32
+# (each width's Frechet products)
 CASES = [
     (2, 2, 2, 40, 64, 16, 16, "bf16"),
     (1, 1, 2, 64, 128, 128, 16, "bf16"),
+    (1, 1, 2, 56, 128, 64, 16, "bf16"),
+    (1, 2, 1, 80, 128, 32, 16, "f32"),
     (1, 2, 1, 52, 16, 8, 8, "f32"),
     (2, 1, 1, 70, 96, 32, 32, "f32"),
     (1, 1, 1, 36, 32, 32, 4, "bf16"),
