@@ -1730,18 +1730,22 @@ __global__ __launch_bounds__(kThreads, OUT_BF16 ? 3 : 2) void dec_keys(MfmaArgs 
 // decode, zfp-style blocks (4 tokens x 4 channels of zhat, 16 RATE bits each)
 // ------------------------------------------------------------------------------------------
 // A workgroup owns a range of 32-token tiles of one slice.  Per tile, thread u * 32 + cb decodes
-// block (tokens 4u .. 4u+3, channels 4cb .. 4cb+3) and splits each zhat into three bf16 planes
-// by truncation (each residual exact in binary32, so the planes sum to zhat), written to an LDS
-// tile per plane ([token][channel], 16-byte granules XOR-swizzled by token as in the encoder's
-// ring); after a barrier wave w computes output channels 32w .. 32w+31 of the 32 tokens on the
-// matrix cores, reading its B fragments of the three planes straight from LDS: the five plane
-// products that matter against the two G^T planes accumulate in binary32 (as the KIVI key
-// decoder does).  Splitting in the decoding thread does it once per value instead of once per
-// wave.
+// block (tokens 4u .. 4u+3, channels 4cb .. 4cb+3) and splits each zhat into bf16 planes, written
+// to an LDS tile per plane ([token][channel], 16-byte granules XOR-swizzled by token as in the
+// encoder's ring); after a barrier wave w computes output channels 32w .. 32w+31 of the 32 tokens
+// on the matrix cores, reading its B fragments straight from LDS: the plane products that matter
+// against the two G^T planes accumulate in binary32 (as the KIVI key decoder does).  Splitting in
+// the decoding thread does it once per value instead of once per wave.
+//   binary32 output: three planes by truncation (each residual exact, so the planes sum to zhat),
+//     five products;
+//   bf16 output: the truncated high plane and the rounded-to-nearest residual (the dropped part
+//     at most 2^-16 of the value, so with G orthogonal at most 2^-16 of the group's norm in any
+//     output, below the final rounding to bf16), three products.
 template <int KS, int RATE, bool OUT_BF16>
 __global__ __launch_bounds__(kThreads, 2) void dec_zfp(MfmaArgs a) {
   constexpr int YB = OUT_BF16 ? 2 : 4;
-  __shared__ __attribute__((aligned(16))) uint8_t zpl[3][kTok * kRowBytes];
+  constexpr int NPL = OUT_BF16 ? 2 : 3;  // planes of zhat
+  __shared__ __attribute__((aligned(16))) uint8_t zpl[NPL][kTok * kRowBytes];
   __shared__ ZfpTables ztab;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -1779,14 +1783,21 @@ __global__ __launch_bounds__(kThreads, 2) void dec_zfp(MfmaArgs a) {
       zfp_decode_block<RATE>(wd, ztab, v);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        uint32_t pw[3][2];
+        uint32_t pw[NPL][2];
 #pragma unroll
         for (int e2 = 0; e2 < 2; ++e2) {
           uint32_t x0 = __float_as_uint(v[4 * j + 2 * e2]), x1 = __float_as_uint(v[4 * j + 2 * e2 + 1]);
 #pragma unroll
-          for (int p = 0; p < 3; ++p) {
-            pw[p][e2] = __builtin_amdgcn_perm(x1, x0, 0x07060302u);
-            if (p < 2) {
+          for (int p = 0; p < NPL; ++p) {
+            if (OUT_BF16 && p == NPL - 1) {
+              typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+              typedef float f32x2_t __attribute__((ext_vector_type(2)));
+              pw[p][e2] = __builtin_bit_cast(
+                  uint32_t, __builtin_convertvector((f32x2_t{__uint_as_float(x0), __uint_as_float(x1)}), bf16x2_t));
+            } else {
+              pw[p][e2] = __builtin_amdgcn_perm(x1, x0, 0x07060302u);
+            }
+            if (p < NPL - 1) {
               x0 = __float_as_uint(__uint_as_float(x0) - __uint_as_float(x0 & 0xffff0000u));
               x1 = __float_as_uint(__uint_as_float(x1) - __uint_as_float(x1 & 0xffff0000u));
             }
@@ -1795,7 +1806,7 @@ __global__ __launch_bounds__(kThreads, 2) void dec_zfp(MfmaArgs a) {
         const int row = 4 * u + j;
         const int off = row * kRowBytes + 16 * swz(row, cb >> 1) + 8 * (cb & 1);
 #pragma unroll
-        for (int p = 0; p < 3; ++p) *(uint2*)(zpl[p] + off) = make_uint2(pw[p][0], pw[p][1]);
+        for (int p = 0; p < NPL; ++p) *(uint2*)(zpl[p] + off) = make_uint2(pw[p][0], pw[p][1]);
       }
     }
     __syncthreads();
@@ -1803,12 +1814,15 @@ __global__ __launch_bounds__(kThreads, 2) void dec_zfp(MfmaArgs a) {
     f32x16_t acc = {};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
-      bf16x8_t B[3];
+      bf16x8_t B[NPL];
 #pragma unroll
-      for (int p = 0; p < 3; ++p) B[p] = as_bf16x8(*(const u32x4_t*)(zpl[p] + boff[kk]));
-      // plane products, smallest first: (1,1) (0,2) (1,0) (0,1) (0,0)
-      acc = mfma(A[1][kk], B[1], acc);
-      acc = mfma(A[0][kk], B[2], acc);
+      for (int p = 0; p < NPL; ++p) B[p] = as_bf16x8(*(const u32x4_t*)(zpl[p] + boff[kk]));
+      // plane products, smallest first: (1,1) (0,2) (1,0) (0,1) (0,0); with two planes of
+      // zhat (1,0) (0,1) (0,0)
+      if constexpr (NPL == 3) {
+        acc = mfma(A[1][kk], B[1], acc);
+        acc = mfma(A[0][kk], B[2], acc);
+      }
       acc = mfma(A[1][kk], B[0], acc);
       acc = mfma(A[0][kk], B[1], acc);
       acc = mfma(A[0][kk], B[0], acc);
