@@ -1738,9 +1738,10 @@ __global__ __launch_bounds__(kThreads, OUT_BF16 ? 3 : 2) void dec_keys(MfmaArgs 
 // the decoding thread does it once per value instead of once per wave.
 //   binary32 output: three planes by truncation (each residual exact, so the planes sum to zhat),
 //     five products;
-//   bf16 output: the truncated high plane and the rounded-to-nearest residual (the dropped part
-//     at most 2^-16 of the value, so with G orthogonal at most 2^-16 of the group's norm in any
-//     output, below the final rounding to bf16), three products.
+//   bf16 output: the truncated high plane and the rounded-to-nearest residual, three products.
+//     The dropped part is at most 2^-16 of each value, so with G orthogonal an output moves by at
+//     most 2^-16 of the group's norm and typically by 2^-16 / sqrt(3 g) of it (independent
+//     rounding errors), against the bf16 criterion of one ulp plus 1e-5 of the group's norm.
 template <int KS, int RATE, bool OUT_BF16>
 __global__ __launch_bounds__(kThreads, 2) void dec_zfp(MfmaArgs a) {
   constexpr int YB = OUT_BF16 ? 2 : 4;
