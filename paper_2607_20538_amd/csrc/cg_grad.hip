@@ -637,6 +637,137 @@ __global__ __launch_bounds__(frechet_threads<MODE>()) void grad_frechet(const do
   }
 }
 
+// The same Frechet step for g <= 16: one wave per gauge block, every matrix in LDS, zero-padded to
+// 16 x 16 (rows padded to 17 doubles against bank conflicts), each product four
+// v_mfma_f64_16x16x4f64 steps (lanes as in wg_gemm).  Products of zero-padded matrices are zero
+// outside the g x g part and the identity is placed on that part only, so the padding stays zero
+// and the g x g part follows grad_frechet step for step (norms, scaling, series, squarings),
+// without the global work area or the workgroup-wide tiles a 16 x 16 product does not fill.
+constexpr int kF16 = 16, kF16P = 17;
+__global__ __launch_bounds__(64) void grad_frechet16(const double* dM, const float* A, int s, int H, int R, int g, int d,
+                                                     double* grad) {
+  __shared__ double tab[4 * kMaxD];
+  __shared__ double mt[12][kF16 * kF16P];
+  dct_table(tab, d);
+  const int lane = int(threadIdx.x), mi = lane & 15, mk = lane >> 4;
+  const int blk = blockIdx.x, r = blk % R, lh = blk / R, h = lh % H, l = lh / H;
+  const int gg = g * g;
+  const double n0 = sqrt(1.0 / d), n1 = sqrt(2.0 / d);
+  double *Mm = mt[0], *Es = mt[1], *S2 = mt[2], *D2 = mt[3], *S3 = mt[4], *D3 = mt[5];
+  double *S4 = mt[6], *D4 = mt[7], *P1 = mt[8], *P2 = mt[9], *T1 = mt[10], *T2 = mt[11];
+  auto at = [](int i, int j) { return i * kF16P + j; };
+  const double* dMl = dM + size_t(lh) * d * d;
+  const float* Ab = A + ((((size_t(l) * 2 + s) * H + h) * R + r) * size_t(gg));
+  // dL/dG = C_d^T dL/dM on the block and S^T = A^T - A, zero outside g x g
+#pragma unroll 1
+  for (int q = 0; q < 4; ++q) {
+    const int idx = lane + 64 * q, c = idx >> 4, k = idx & 15;
+    double es = 0.0, mm = 0.0;
+    if (c < g && k < g) {
+      const int step = 2 * (r * g + c) + 1;  // column r g + c of C_d, rows v = 0, 1, ...
+      double acc = n0 * dMl[r * g + k];
+      for (int v = 1, ti = step; v < d; ++v, ti = dct_step(ti, step, d))
+        acc = fma(n1 * tab[ti], dMl[size_t(v) * d + r * g + k], acc);
+      es = acc;
+      mm = double(Ab[k * g + c]) - double(Ab[c * g + k]);
+    }
+    Es[at(c, k)] = es;
+    Mm[at(c, k)] = mm;
+  }
+  __syncthreads();
+  // 1-norm: lane j < 16 sums column j in row order, then the largest over the wave
+  auto norm1 = [&](const double* X) {
+    double sum = 0.0;
+    if (lane < kF16)
+      for (int i = 0; i < kF16; ++i) sum += fabs(X[at(i, lane)]);
+    for (int o = 32; o > 0; o >>= 1) sum = fmax(sum, __shfl_xor(sum, o));
+    return sum;
+  };
+  const double e = norm1(Es);
+  double* out = grad + size_t(blk) * gg;
+  if (!(e > 0.0)) {
+    for (int idx = lane; idx < gg; idx += 64) out[idx] = 0.0;
+    return;
+  }
+  double nw = norm1(Mm) + 1.0;
+  if (!isfinite(nw) || !isfinite(e)) {
+    for (int idx = lane; idx < gg; idx += 64) out[idx] = __builtin_nan("");
+    return;
+  }
+  int sq = 0;
+  while (nw > 0.5) {
+    nw *= 0.5;
+    ++sq;
+  }
+  const double fm = ldexp(1.0, -sq), fe = fm / e;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int idx = lane + 64 * q, o = at(idx >> 4, idx & 15);
+    Mm[o] *= fm;
+    Es[o] *= fe;
+  }
+  __syncthreads();
+  // C (+)= X Y, 16 x 16
+  auto prod = [&](const double* X, const double* Y, double* C, bool acc) {
+    f64x4_t dq = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+      dq = __builtin_amdgcn_mfma_f64_16x16x4f64(X[at(mi, 4 * st + mk)], Y[at(4 * st + mk, mi)], dq, 0, 0, 0);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      double* p = C + at(4 * v + mk, mi);
+      *p = acc ? *p + dq[v] : dq[v];
+    }
+    __syncthreads();
+  };
+  // [[Cs, Cd], [0, Cs]] = [[Xs, Xd], [0, Xs]] [[Ys, Yd], [0, Ys]]
+  auto blk_prod = [&](const double* Xs, const double* Xd, const double* Ys, const double* Yd, double* Cs, double* Cd) {
+    prod(Xs, Ys, Cs, false);
+    prod(Xs, Yd, Cd, false);
+    prod(Xd, Ys, Cd, true);
+  };
+  // P = B_j + c (Ts, Td), as in grad_frechet, the identity on the g x g part only
+  auto add_b = [&](int j, const double* Ts, const double* Td, double c) {
+    const double c0 = j == 3 ? inv_fact(12) : (j == 2 ? inv_fact(8) : (j == 1 ? inv_fact(4) : 1.0));
+    const double c1 = j == 3 ? inv_fact(13) : (j == 2 ? inv_fact(9) : (j == 1 ? inv_fact(5) : 1.0));
+    const double c2 = j == 3 ? inv_fact(14) : (j == 2 ? inv_fact(10) : (j == 1 ? inv_fact(6) : inv_fact(2)));
+    const double c3 = j == 3 ? inv_fact(15) : (j == 2 ? inv_fact(11) : (j == 1 ? inv_fact(7) : inv_fact(3)));
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = lane + 64 * q, i = idx >> 4, jj = idx & 15, o = at(i, jj);
+      const double id = (i == jj && i < g) ? c0 : 0.0;
+      P1[o] = id + c1 * Mm[o] + c2 * S2[o] + c3 * S3[o] + c * Ts[o];
+      P2[o] = c1 * Es[o] + c2 * D2[o] + c3 * D3[o] + c * Td[o];
+    }
+    __syncthreads();
+  };
+  blk_prod(Mm, Es, Mm, Es, S2, D2);
+  blk_prod(S2, D2, Mm, Es, S3, D3);
+  blk_prod(S2, D2, S2, D2, S4, D4);
+  add_b(3, S4, D4, inv_fact(16));
+#pragma unroll 1
+  for (int j = 2; j >= 0; --j) {
+    blk_prod(S4, D4, P1, P2, T1, T2);
+    add_b(j, T1, T2, 1.0);
+  }
+#pragma unroll 1
+  for (int q = 0; q < sq; ++q) {
+    blk_prod(P1, P2, P1, P2, T1, T2);
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq) {
+      const int idx = lane + 64 * qq, o = at(idx >> 4, idx & 15);
+      P1[o] = T1[o];
+      P2[o] = T2[o];
+    }
+    __syncthreads();
+  }
+  // dL/dS = e P2, dL/dA = dL/dS - (dL/dS)^T
+  for (int idx = lane; idx < gg; idx += 64) {
+    const int i = idx / g, j = idx - i * g;
+    out[idx] = e * (P2[at(i, j)] - P2[at(j, i)]);
+  }
+}
+
 template <int TD>
 hipError_t launch_data(const GradArgs& a, int nwg, size_t smem, hipStream_t st) {
   hipError_t e;
@@ -733,6 +864,8 @@ hipError_t launch_gauge_grad(int s, const ViewDev& X, const GaugeDev& G, const f
   if (G.g == 128)
     hipLaunchKernelGGL(grad_frechet<kFrechet128>, dim3(X.L * X.H * R), dim3(kWideThreads), 0, st, dM, A, s, X.H, R, G.g,
                        d, work, grad);
+  else if (G.g <= kF16)
+    hipLaunchKernelGGL(grad_frechet16, dim3(X.L * X.H * R), dim3(64), 0, st, dM, A, s, X.H, R, G.g, d, grad);
   else if (G.g % 64 == 0)
     hipLaunchKernelGGL(grad_frechet<kFrechet64>, dim3(X.L * X.H * R), dim3(kGradThreads), 0, st, dM, A, s, X.H, R, G.g,
                        d, work, grad);
