@@ -92,7 +92,7 @@ def _check_fused_blocks(got_codes, X, s, G, z_gpu, oc, g):
     np.testing.assert_array_equal(got_codes, ref["codes"])
 
 
-@pytest.mark.parametrize("rate", [3, 4, 8])
+@pytest.mark.parametrize("rate", [2, 3, 4, 6, 8])
 @pytest.mark.parametrize("g", [32, 128])
 def test_fused_with_gauge(rate, g):
     T = 132
