@@ -23,6 +23,7 @@
 // smooth objectives is much smaller than the terms that cancel in it (about 40x on random
 // Llama-shaped data), so binary32 sums over a block's d channels would reach the result.
 #include <algorithm>
+#include <type_traits>
 
 #include "cg_internal.h"
 #include "cg_device.h"
@@ -201,6 +202,7 @@ typedef double f64x4_t __attribute__((ext_vector_type(4)));
 // converted to binary64 once, as it is staged; each thread loads its share of the next block into
 // registers while the waves multiply the current one.
 constexpr int kDataThreads = 512;
+template <bool BF16>
 __global__ __launch_bounds__(kDataThreads) void grad_data_mfma(GradArgs a) {
   constexpr int d = 128, Tb = 16, XP = 130;  // rows of the staged block padded to 130 doubles
   extern __shared__ double smd2[];
@@ -238,18 +240,25 @@ __global__ __launch_bounds__(kDataThreads) void grad_data_mfma(GradArgs a) {
   f64x4_t acc[8];
 #pragma unroll
   for (int jt = 0; jt < 8; ++jt) acc[jt] = f64x4_t{0.0, 0.0, 0.0, 0.0};
-  const size_t xbase = size_t(l) * X.sl + size_t(b) * X.sb + size_t(h) * X.sh;
+  // this thread's entries of a block of X: tokens tid / 128 + 4 q, channel tid % 128; the
+  // pointer steps by one block of tokens per fetch
+  typedef std::conditional_t<BF16, uint16_t, float> xt;
   constexpr int XQ = Tb * d / kDataThreads;  // entries of a block of X per thread
+  static_assert(kDataThreads % d == 0, "whole token rows per pass");
+  const xt* xp = static_cast<const xt*>(X.ptr) + size_t(l) * X.sl + size_t(b) * X.sb + size_t(h) * X.sh +
+                 size_t(k0 * Tb + (tid >> 7)) * X.st + (tid & 127);
+  const size_t qstride = size_t(kDataThreads / d) * X.st, bstride = size_t(Tb) * X.st;
   float rx[XQ];
-  auto fetch = [&](int blk) {
+  auto fetch = [&]() {
 #pragma unroll
     for (int q = 0; q < XQ; ++q) {
-      const int idx = tid + kDataThreads * q, t = idx >> 7, c = idx & 127;
-      const size_t off = xbase + size_t(blk * Tb + t) * X.st + c;
-      rx[q] = X.bf16 ? bf16_to_f32(((const uint16_t*)X.ptr)[off]) : ((const float*)X.ptr)[off];
+      const xt v = xp[q * qstride];
+      if constexpr (BF16) rx[q] = bf16_to_f32(v);
+      else rx[q] = v;
     }
+    xp += bstride;
   };
-  if (k0 < k1) fetch(k0);
+  if (k0 < k1) fetch();
   for (int blk = k0; blk < k1; ++blk) {
     __syncthreads();  // the previous block's X is read (and, at the start, rw written)
 #pragma unroll
@@ -258,7 +267,7 @@ __global__ __launch_bounds__(kDataThreads) void grad_data_mfma(GradArgs a) {
       xs[(idx >> 7) * XP + (idx & 127)] = double(rx[q]);
     }
     __syncthreads();
-    if (blk + 1 < k1) fetch(blk + 1);
+    if (blk + 1 < k1) fetch();
     // W tile: tokens x frequencies n0 .. n0 + 15
     f64x4_t wd = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
@@ -839,10 +848,10 @@ hipError_t launch_gauge_grad(int s, const ViewDev& X, const GaugeDev& G, const f
                       (size_t(d) * (d + 1) + size_t(Tb) * (d + 1) + size_t(Tb) * Tb) * sizeof(float);
   if (nblk > 0 && d == 128 && Tb == 16 && !force_generic) {
     const size_t smf = (size_t(16) * 130 + size_t(16) * 128) * sizeof(double);
-    if ((e = hipFuncSetAttribute((const void*)grad_data_mfma, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smf)) !=
-        hipSuccess)
-      return e;
-    hipLaunchKernelGGL(grad_data_mfma, dim3(nwg), dim3(kDataThreads), smf, st, a);
+    const void* fn = X.bf16 ? (const void*)grad_data_mfma<true> : (const void*)grad_data_mfma<false>;
+    if ((e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smf)) != hipSuccess) return e;
+    void* args[] = {&a};
+    if ((e = hipLaunchKernel(fn, dim3(nwg), dim3(kDataThreads), args, smf, st)) != hipSuccess) return e;
     if ((e = hipGetLastError()) != hipSuccess) return e;
   } else if (nblk > 0) {
     switch (d / 16) {
