@@ -557,15 +557,49 @@ __global__ __launch_bounds__(frechet_threads<MODE>()) void grad_frechet(const do
   double* T2 = T1 + gg;
   const double* dMl = dM + size_t(lh) * d * d;
   const float* Ab = A + ((((size_t(l) * 2 + s) * H + h) * R + r) * gg);
+  // dL/dG = C_d^T dL/dM on the block (entry (c, k) sums over v in order) and S^T = A^T - A
+  constexpr int QW = 16;  // most outputs per thread on the shared-load path (g^2 / NT: 16 at g = 128 and 64)
+  if (NT % g == 0 && int(gg) / NT <= QW) {
+    // thread tid: column k = tid % g of rows c = tid / g + (NT / g) q, so one load of
+    // dL/dM[v][r g + k] serves all of them
+    const int k = int(threadIdx.x) % g, c0 = int(threadIdx.x) / g, cs = NT / g, nq = int(gg) / NT;
+    double acc[QW];
+    int ti[QW], stp[QW];
+#pragma unroll
+    for (int q = 0; q < QW; ++q) {
+      stp[q] = 2 * (r * g + c0 + cs * q) + 1;  // column r g + c of C_d, rows v = 0, 1, ...
+      ti[q] = stp[q];
+      acc[q] = 0.0;
+    }
+    const double m0 = dMl[r * g + k];
+#pragma unroll
+    for (int q = 0; q < QW; ++q) acc[q] = n0 * m0;  // the table's entry 0 is cos 0 = 1
+    for (int v = 1; v < d; ++v) {
+      const double m = dMl[size_t(v) * d + r * g + k];
+#pragma unroll
+      for (int q = 0; q < QW; ++q) {
+        if (q < nq) acc[q] = fma(n1 * tab[ti[q]], m, acc[q]);
+        ti[q] = dct_step(ti[q], stp[q], d);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < QW; ++q)
+      if (q < nq) {
+        const int c = c0 + cs * q, idx = c * g + k;
+        Es[idx] = acc[q];                                          // dL/dG
+        Mm[idx] = double(Ab[size_t(k) * g + c]) - double(Ab[idx]);  // S^T = A^T - A
+      }
+  } else {
 #pragma nounroll
-  for (int idx = int(threadIdx.x); idx < int(gg); idx += NT) {
-    const int c = idx / g, k = idx - c * g;
-    const int step = 2 * (r * g + c) + 1;  // column r g + c of C_d, rows v = 0, 1, ...
-    double acc = n0 * dMl[r * g + k];       // the table's entry 0 is cos 0 = 1
-    for (int v = 1, ti = step; v < d; ++v, ti = dct_step(ti, step, d))
-      acc = fma(n1 * tab[ti], dMl[size_t(v) * d + r * g + k], acc);
-    Es[idx] = acc;                                          // dL/dG
-    Mm[idx] = double(Ab[size_t(k) * g + c]) - double(Ab[idx]);  // S^T = A^T - A
+    for (int idx = int(threadIdx.x); idx < int(gg); idx += NT) {
+      const int c = idx / g, k = idx - c * g;
+      const int step = 2 * (r * g + c) + 1;
+      double acc = n0 * dMl[r * g + k];
+      for (int v = 1, ti = step; v < d; ++v, ti = dct_step(ti, step, d))
+        acc = fma(n1 * tab[ti], dMl[size_t(v) * d + r * g + k], acc);
+      Es[idx] = acc;
+      Mm[idx] = double(Ab[size_t(k) * g + c]) - double(Ab[idx]);
+    }
   }
   __syncthreads();
   const double e = wg_norm1<NT>(Es, g, red);
@@ -667,21 +701,36 @@ __global__ __launch_bounds__(64) void grad_frechet16(const double* dM, const flo
   auto at = [](int i, int j) { return i * kF16P + j; };
   const double* dMl = dM + size_t(lh) * d * d;
   const float* Ab = A + ((((size_t(l) * 2 + s) * H + h) * R + r) * size_t(gg));
-  // dL/dG = C_d^T dL/dM on the block and S^T = A^T - A, zero outside g x g
-#pragma unroll 1
-  for (int q = 0; q < 4; ++q) {
-    const int idx = lane + 64 * q, c = idx >> 4, k = idx & 15;
-    double es = 0.0, mm = 0.0;
-    if (c < g && k < g) {
-      const int step = 2 * (r * g + c) + 1;  // column r g + c of C_d, rows v = 0, 1, ...
-      double acc = n0 * dMl[r * g + k];
-      for (int v = 1, ti = step; v < d; ++v, ti = dct_step(ti, step, d))
-        acc = fma(n1 * tab[ti], dMl[size_t(v) * d + r * g + k], acc);
-      es = acc;
-      mm = double(Ab[k * g + c]) - double(Ab[c * g + k]);
+  // dL/dG = C_d^T dL/dM on the block and S^T = A^T - A, zero outside g x g: lane holds column
+  // k = lane % 16 of rows c = lane / 16 + 4 q, so one load of dL/dM[v][r g + k] serves its four
+  // entries (each summed over v in order)
+  {
+    const int k = lane & 15, c0 = lane >> 4;
+    const bool kin = k < g;
+    double acc[4];
+    int ti[4], stp[4];
+    const double m0 = kin ? dMl[r * g + k] : 0.0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      stp[q] = 2 * (r * g + c0 + 4 * q) + 1;  // column r g + c of C_d, rows v = 0, 1, ...
+      ti[q] = stp[q];
+      acc[q] = n0 * m0;                        // the table's entry 0 is cos 0 = 1
     }
-    Es[at(c, k)] = es;
-    Mm[at(c, k)] = mm;
+    for (int v = 1; v < d; ++v) {
+      const double m = kin ? dMl[size_t(v) * d + r * g + k] : 0.0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc[q] = fma(n1 * tab[ti[q]], m, acc[q]);
+        ti[q] = dct_step(ti[q], stp[q], d);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int c = c0 + 4 * q;
+      const bool in = kin && c < g;
+      Es[at(c, k)] = in ? acc[q] : 0.0;
+      Mm[at(c, k)] = in ? double(Ab[k * g + c]) - double(Ab[c * g + k]) : 0.0;
+    }
   }
   __syncthreads();
   // 1-norm: lane j < 16 sums column j in row order, then the largest over the wave
