@@ -56,25 +56,39 @@ __device__ __forceinline__ int dct_step(int k, int step, int d) {
   return k >= 4 * d ? k - 4 * d : k;
 }
 
-// M = C_d G_{l,s,h} per (l, h), binary64 sums rounded to binary32: [L][H][d][d]
+// M = C_d G_{l,s,h} per (l, h), binary64 sums rounded to binary32: [L][H][d][d].  Thread gi of a
+// head computes column c = gi % d of the rows v = gi / d + (d / 8) q, q < 8, so each entry of G
+// it loads serves eight sums (each over a in order).
+constexpr int kPrepRows = 8;
 __global__ __launch_bounds__(256) void grad_prep(int s, GaugeDev G, int H, int d, float* M) {
   __shared__ double tab[4 * kMaxD];
   dct_table(tab, d);
   const int lh = blockIdx.y, l = lh / H, h = lh - l * H;
-  const int g = G.g;
+  const int g = G.g, vs = d / kPrepRows;
   const double n0 = sqrt(1.0 / d), n1 = sqrt(2.0 / d);
-  for (int idx = blockIdx.x * blockDim.x + threadIdx.x; idx < d * d; idx += gridDim.x * blockDim.x) {
-    const int v = idx / d, c = idx - v * d, r = c / g, j = c - r * g;
-    const double nv = v == 0 ? n0 : n1;
-    const float* Gc = G.f32 + (((size_t(l) * 2 + s) * G.H + h) * G.R + r) * g * g + j;
-    int k = ((2 * r * g + 1) * v) % (4 * d);  // entry (v, r g + a) for a = 0
-    double acc = 0.0;
-    for (int a = 0; a < g; ++a) {
-      acc = fma(nv * tab[k], double(Gc[size_t(a) * g]), acc);
-      k = dct_step(k, 2 * v, d);
-    }
-    M[size_t(lh) * d * d + idx] = float(acc);
+  const int gi = blockIdx.x * blockDim.x + threadIdx.x;
+  if (gi >= d * vs) return;
+  const int c = gi % d, vb = gi / d, r = c / g, j = c - r * g;
+  const float* Gc = G.f32 + (((size_t(l) * 2 + s) * G.H + h) * G.R + r) * g * g + j;
+  double acc[kPrepRows], nv[kPrepRows];
+  int k[kPrepRows];
+#pragma unroll
+  for (int q = 0; q < kPrepRows; ++q) {
+    const int v = vb + vs * q;
+    nv[q] = v == 0 ? n0 : n1;
+    k[q] = ((2 * r * g + 1) * v) % (4 * d);  // entry (v, r g + a) for a = 0
+    acc[q] = 0.0;
   }
+  for (int a = 0; a < g; ++a) {
+    const double gv = double(Gc[size_t(a) * g]);
+#pragma unroll
+    for (int q = 0; q < kPrepRows; ++q) {
+      acc[q] = fma(nv[q] * tab[k[q]], gv, acc[q]);
+      k[q] = dct_step(k[q], 2 * (vb + vs * q), d);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < kPrepRows; ++q) M[size_t(lh) * d * d + size_t(vb + vs * q) * d + c] = float(acc[q]);
 }
 
 struct GradArgs {
@@ -875,7 +889,7 @@ hipError_t launch_gauge_grad(int s, const ViewDev& X, const GaugeDev& G, const f
   double* dM = reinterpret_cast<double*>(base + lay.off_dm);
   double* work = reinterpret_cast<double*>(base + lay.off_work);
   const int d = X.d, R = d / G.g, nblk = X.T / Tb;
-  hipLaunchKernelGGL(grad_prep, dim3((d * d + 255) / 256, X.L * X.H), dim3(256), 0, st, s, G, X.H, d, M);
+  hipLaunchKernelGGL(grad_prep, dim3((d * (d / kPrepRows) + 255) / 256, X.L * X.H), dim3(256), 0, st, s, G, X.H, d, M);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   GradArgs a{};
   a.X = X;
