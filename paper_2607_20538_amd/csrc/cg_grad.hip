@@ -573,7 +573,16 @@ __global__ __launch_bounds__(frechet_threads<MODE>()) void grad_frechet(const do
   const float* Ab = A + ((((size_t(l) * 2 + s) * H + h) * R + r) * gg);
   // dL/dG = C_d^T dL/dM on the block (entry (c, k) sums over v in order) and S^T = A^T - A
   constexpr int QW = 16;  // most outputs per thread on the shared-load path (g^2 / NT: 16 at g = 128 and 64)
-  if (NT % g == 0 && int(gg) / NT <= QW) {
+  if (MODE == kFrechet128 && g == d) {
+    // one group per head: dL/dG = C_d^T dL/dM as one product, C_d^T staged in T1 from the table
+    for (int idx = int(threadIdx.x); idx < int(gg); idx += NT) {
+      const int c = idx / g, v = idx - c * g;
+      T1[idx] = (v == 0 ? n0 : n1) * tab[((2 * c + 1) * v) % (4 * d)];
+      Mm[idx] = double(Ab[size_t(v) * g + c]) - double(Ab[idx]);  // S^T = A^T - A
+    }
+    __syncthreads();
+    wg_product<MODE>(T1, dMl, Es, g, false);
+  } else if (NT % g == 0 && int(gg) / NT <= QW) {
     // thread tid: column k = tid % g of rows c = tid / g + (NT / g) q, so one load of
     // dL/dM[v][r g + k] serves all of them
     const int k = int(threadIdx.x) % g, c0 = int(threadIdx.x) / g, cs = NT / g, nq = int(gg) / NT;
