@@ -262,14 +262,11 @@ __global__ __launch_bounds__(kDataThreads) void grad_data_mfma(GradArgs a) {
   const xt* xp = static_cast<const xt*>(X.ptr) + size_t(l) * X.sl + size_t(b) * X.sb + size_t(h) * X.sh +
                  size_t(k0 * Tb + (tid >> 7)) * X.st + (tid & 127);
   const size_t qstride = size_t(kDataThreads / d) * X.st, bstride = size_t(Tb) * X.st;
-  float rx[XQ];
+  // raw entries, converted only when staged, so the loads stay in flight through the block
+  xt rx[XQ];
   auto fetch = [&]() {
 #pragma unroll
-    for (int q = 0; q < XQ; ++q) {
-      const xt v = xp[q * qstride];
-      if constexpr (BF16) rx[q] = bf16_to_f32(v);
-      else rx[q] = v;
-    }
+    for (int q = 0; q < XQ; ++q) rx[q] = xp[q * qstride];
     xp += bstride;
   };
   if (k0 < k1) fetch();
@@ -278,7 +275,10 @@ __global__ __launch_bounds__(kDataThreads) void grad_data_mfma(GradArgs a) {
 #pragma unroll
     for (int q = 0; q < XQ; ++q) {
       const int idx = tid + kDataThreads * q;
-      xs[(idx >> 7) * XP + (idx & 127)] = double(rx[q]);
+      float v;
+      if constexpr (BF16) v = bf16_to_f32(rx[q]);
+      else v = rx[q];
+      xs[(idx >> 7) * XP + (idx & 127)] = double(v);
     }
     __syncthreads();
     if (blk + 1 < k1) fetch();
