@@ -453,23 +453,37 @@ __device__ void wg_gemm64(const double* A, const double* B, double* C, int g, bo
   __syncthreads();
 }
 
-// C (+)= A B for g = 128 by a 1024-thread workgroup: wave w (of 16) takes the 32 x 32 output
-// quarter at (32 (w / 4), 32 (w % 4)) as four 16 x 16 matrix-core tiles (lanes as in wg_gemm); the
-// whole 128 x 32 chunk of A and 32 x 128 chunk of B of each K step sit in LDS, and each thread
-// loads its four + four entries of the next chunk into registers while the waves multiply.
-// Sixteen waves per CU (four per SIMD) hide the latencies one wave per SIMD leaves exposed.
+// C = A1 B1 (+ A2 B2 when A2 is not null) for g = 128 by a 1024-thread workgroup: wave w (of 16)
+// takes the 32 x 32 output quarter at (32 (w / 4), 32 (w % 4)) as four 16 x 16 matrix-core tiles
+// (lanes as in wg_gemm); the 128 x 32 chunks of A and the 32 x 128 chunks of B of each K step sit
+// in LDS, and each thread loads its entries of the next chunks into registers while the waves
+// multiply.  Sixteen waves per CU (four per SIMD) hide the latencies one wave per SIMD leaves
+// exposed; the second product in the same pass reads no partial C back (the work matrices live
+// in HBM, so the kernel's time follows their traffic).
 constexpr int kWideThreads = 1024;
-__device__ void wg_gemm128(const double* A, const double* B, double* C, bool acc) {
-  __shared__ double as[128][33], bs[32][129];
+struct Gemm128Lds {
+  double as[2][128][33], bs[2][32][129];  // the K step's chunks of A1, A2 and B1, B2
+};
+template <bool TWO>
+__device__ void wg_gemm128(Gemm128Lds& L, const double* A1, const double* B1, const double* A2, const double* B2,
+                           double* C) {
+  auto& as = L.as;
+  auto& bs = L.bs;
+  constexpr bool two = TWO;
   const int tid = int(threadIdx.x), lane = tid & 63, w = tid >> 6;
   const int qi = (w >> 2) * 32, qj = (w & 3) * 32, mi = lane & 15, mk = lane >> 4;
-  double ra[4], rb[4];
+  double ra[TWO ? 2 : 1][4], rb[TWO ? 2 : 1][4];
   auto fetch = [&](int k0) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int idx = tid + kWideThreads * q;
-      ra[q] = A[(idx >> 5) * 128 + k0 + (idx & 31)];  // 32-bit offsets from uniform bases
-      rb[q] = B[(k0 + (idx >> 7)) * 128 + (idx & 127)];
+      // 32-bit offsets from uniform bases
+      ra[0][q] = A1[(idx >> 5) * 128 + k0 + (idx & 31)];
+      rb[0][q] = B1[(k0 + (idx >> 7)) * 128 + (idx & 127)];
+      if constexpr (two) {
+        ra[1][q] = A2[(idx >> 5) * 128 + k0 + (idx & 31)];
+        rb[1][q] = B2[(k0 + (idx >> 7)) * 128 + (idx & 127)];
+      }
     }
   };
   f64x4_t dq[2][2];
@@ -484,19 +498,26 @@ __device__ void wg_gemm128(const double* A, const double* B, double* C, bool acc
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int idx = tid + kWideThreads * q;
-      as[idx >> 5][idx & 31] = ra[q];
-      bs[idx >> 7][idx & 127] = rb[q];
+      as[0][idx >> 5][idx & 31] = ra[0][q];
+      bs[0][idx >> 7][idx & 127] = rb[0][q];
+      if constexpr (two) {
+        as[1][idx >> 5][idx & 31] = ra[1][q];
+        bs[1][idx >> 7][idx & 127] = rb[1][q];
+      }
     }
     __syncthreads();
     if (kc < 3) fetch(32 * (kc + 1));
+#pragma unroll 1
+    for (int pr = 0; pr < (two ? 2 : 1); ++pr) {
 #pragma unroll
-    for (int kk = 0; kk < 32; kk += 4) {
-      const double a0 = as[qi + mi][kk + mk], a1 = as[qi + 16 + mi][kk + mk];
-      const double b0 = bs[kk + mk][qj + mi], b1 = bs[kk + mk][qj + 16 + mi];
-      dq[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, dq[0][0], 0, 0, 0);
-      dq[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, dq[0][1], 0, 0, 0);
-      dq[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, dq[1][0], 0, 0, 0);
-      dq[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, dq[1][1], 0, 0, 0);
+      for (int kk = 0; kk < 32; kk += 4) {
+        const double a0 = as[pr][qi + mi][kk + mk], a1 = as[pr][qi + 16 + mi][kk + mk];
+        const double b0 = bs[pr][kk + mk][qj + mi], b1 = bs[pr][kk + mk][qj + 16 + mi];
+        dq[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, dq[0][0], 0, 0, 0);
+        dq[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, dq[0][1], 0, 0, 0);
+        dq[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, dq[1][0], 0, 0, 0);
+        dq[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, dq[1][1], 0, 0, 0);
+      }
     }
   }
 #pragma unroll
@@ -504,10 +525,7 @@ __device__ void wg_gemm128(const double* A, const double* B, double* C, bool acc
 #pragma unroll
     for (int tj = 0; tj < 2; ++tj)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        double* p = C + ((qi + 16 * ti + 4 * v + mk) * 128 + qj + 16 * tj + mi);
-        *p = acc ? *p + dq[ti][tj][v] : dq[ti][tj][v];
-      }
+      for (int v = 0; v < 4; ++v) C[(qi + 16 * ti + 4 * v + mk) * 128 + qj + 16 * tj + mi] = dq[ti][tj][v];
   __syncthreads();
 }
 
@@ -520,8 +538,7 @@ template <int MODE>
 constexpr int frechet_threads() { return MODE == kFrechet128 ? kWideThreads : kGradThreads; }
 template <int MODE>
 __device__ void wg_product(const double* A, const double* B, double* C, int g, bool acc) {
-  if constexpr (MODE == kFrechet128) wg_gemm128(A, B, C, acc);
-  else if constexpr (MODE == kFrechet64) wg_gemm64(A, B, C, g, acc);
+  if constexpr (MODE == kFrechet64) wg_gemm64(A, B, C, g, acc);
   else wg_gemm(A, B, C, g, acc);
 }
 
@@ -553,6 +570,8 @@ __global__ __launch_bounds__(frechet_threads<MODE>()) void grad_frechet(const do
   constexpr int NT = frechet_threads<MODE>();
   __shared__ double red[NT];
   __shared__ double tab[4 * kMaxD];
+  __shared__ std::conditional_t<MODE == kFrechet128, Gemm128Lds, char> glds_store;
+  auto* glds = &glds_store;
   dct_table(tab, d);
   const int blk = blockIdx.x, r = blk % R, lh = blk / R, h = lh % H, l = lh / H;
   const size_t gg = size_t(g) * g;
@@ -581,7 +600,7 @@ __global__ __launch_bounds__(frechet_threads<MODE>()) void grad_frechet(const do
       Mm[idx] = double(Ab[size_t(v) * g + c]) - double(Ab[idx]);  // S^T = A^T - A
     }
     __syncthreads();
-    wg_product<MODE>(T1, dMl, Es, g, false);
+    if constexpr (MODE == kFrechet128) wg_gemm128<false>(*glds, T1, dMl, nullptr, nullptr, Es);
   } else if (NT % g == 0 && int(gg) / NT <= QW) {
     // thread tid: column k = tid % g of rows c = tid / g + (NT / g) q, so one load of
     // dL/dM[v][r g + k] serves all of them
@@ -672,6 +691,8 @@ __global__ __launch_bounds__(frechet_threads<MODE>()) void grad_frechet(const do
     }
     __syncthreads();
   };
+  // the running polynomial and the product's target swap after each squaring instead of copying
+  double *Pc1 = P1, *Pc2 = P2, *Tc1 = T1, *Tc2 = T2;
   for (int step = 0; step < 6 + sq; ++step) {
     const double *Xs, *Xd, *Ys, *Yd;
     double *Cs, *Cd;
@@ -679,27 +700,29 @@ __global__ __launch_bounds__(frechet_threads<MODE>()) void grad_frechet(const do
     else if (step == 1) { Xs = S2; Xd = D2; Ys = Mm; Yd = Es; Cs = S3; Cd = D3; }
     else if (step == 2) { Xs = S2; Xd = D2; Ys = S2; Yd = D2; Cs = S4; Cd = D4; }
     else if (step < 6) { Xs = S4; Xd = D4; Ys = P1; Yd = P2; Cs = T1; Cd = T2; }
-    else { Xs = P1; Xd = P2; Ys = P1; Yd = P2; Cs = T1; Cd = T2; }
+    else { Xs = Pc1; Xd = Pc2; Ys = Pc1; Yd = Pc2; Cs = Tc1; Cd = Tc2; }
     if (step == 3) add_b(3, S4, D4, inv_fact(16));
+    if constexpr (MODE == kFrechet128) {
+      // Cs = Xs Ys, then Cd = Xs Yd + Xd Ys in one pass
+      wg_gemm128<false>(*glds, Xs, Ys, nullptr, nullptr, Cs);
+      wg_gemm128<true>(*glds, Xs, Yd, Xd, Ys, Cd);
+    } else {
 #pragma unroll 1
-    for (int q = 0; q < 3; ++q)  // Cs = Xs Ys, Cd = Xs Yd + Xd Ys
-      wg_product<MODE>(q == 2 ? Xd : Xs, q == 0 ? Ys : (q == 1 ? Yd : Ys), q == 0 ? Cs : Cd, g, q == 2);
+      for (int q = 0; q < 3; ++q)  // Cs = Xs Ys, Cd = Xs Yd + Xd Ys
+        wg_product<MODE>(q == 2 ? Xd : Xs, q == 0 ? Ys : (q == 1 ? Yd : Ys), q == 0 ? Cs : Cd, g, q == 2);
+    }
     if (step >= 3 && step < 6) {
       add_b(5 - step, T1, T2, 1.0);
     } else if (step >= 6) {
-#pragma nounroll
-      for (int idx = int(threadIdx.x); idx < int(gg); idx += NT) {
-        P1[idx] = T1[idx];
-        P2[idx] = T2[idx];
-      }
-      __syncthreads();
+      double* t = Pc1; Pc1 = Tc1; Tc1 = t;
+      t = Pc2; Pc2 = Tc2; Tc2 = t;
     }
   }
   // dL/dS = e P2, dL/dA = dL/dS - (dL/dS)^T
 #pragma nounroll
   for (int idx = int(threadIdx.x); idx < int(gg); idx += NT) {
     const int i = idx / g, j = idx - i * g;
-    out[idx] = e * (P2[idx] - P2[size_t(j) * g + i]);
+    out[idx] = e * (Pc2[idx] - Pc2[size_t(j) * g + i]);
   }
 }
 
