@@ -47,53 +47,54 @@ __global__ void spec_init(double* acc, size_t nacc, double* lsum, int L, double*
 
 // M = C_d G_{l,s,h} (G block-diagonal over its R groups), products and sums in binary64 from
 // the binary32 DCT rows and gauge, rounded to binary32 and split into two bf16 planes.  One
-// workgroup of 1024 threads (four waves per SIMD to hide the LDS latency) per (l, h) stages C_d
-// and the gauge blocks in LDS; thread t accumulates the 4 x 4 outputs rows 4 (t / 32) ..,
-// columns 4 (t % 32) .. (one gauge group: 4 | g).
+// workgroup of 1024 threads per (l, h) stages C_d (row pitch 129 floats, so that a fragment's 16
+// rows fall in 16 banks) and the gauge blocks in LDS; wave w (of 16) takes the 32 x 32 quarter
+// of M at (32 (w / 4), 32 (w % 4)) as four 16 x 16 binary64 matrix-core tiles
+// (v_mfma_f64_16x16x4f64: lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16] of each step
+// and holds D[4 v + l / 16][l % 16]), the K range of a tile limited to the gauge rows its
+// columns read (gs is zero outside a column's group).
 constexpr int kMprepThreads = 1024;
+constexpr int kCdPitch = kD + 1;
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
 __global__ __launch_bounds__(kMprepThreads) void spec_mprep(int s, GaugeDev G, int H, const double* cd, uint16_t* m0,
                                                    uint16_t* m1) {
-  __shared__ float cds[kD * kD];   // C_d rows
-  __shared__ float gs[kD * kD];    // gs[a_global][j]: G_{r}[a][j - r g] for j in group r, a = a_global - r g
+  __shared__ float cds[kD * kCdPitch];  // C_d rows
+  __shared__ float gs[kD * kD];         // gs[a_global][j]: G_{r}[a][j - r g] for j in group r, a = a_global - r g
   const int lh = blockIdx.x, l = lh / H, h = lh - l * H;
   const int g = G.g;
   for (int idx = threadIdx.x; idx < kD * kD; idx += blockDim.x) {
-    cds[idx] = float(cd[idx]);
     const int ag = idx / kD, j = idx - ag * kD, r = j / g;
+    cds[ag * kCdPitch + j] = float(cd[idx]);
     const int a = ag - r * g;
     float v = 0.0f;
     if (a >= 0 && a < g) v = G.f32[((((size_t(l) * 2 + s) * G.H + h) * G.R + r) * g + a) * g + (j - r * g)];
     gs[idx] = v;
   }
   __syncthreads();
-  const int i0 = 4 * (threadIdx.x / 32), j0 = 4 * (threadIdx.x % 32), r = j0 / g;
-  double acc[4][4];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, mi = lane & 15, mk = lane >> 4;
+  const int qi = (w >> 2) * 32, qj = (w & 3) * 32;
+  const int kw = g > 16 ? g : 16;  // K range of a 16-column tile: its group, or the groups it spans
 #pragma unroll
-  for (int p = 0; p < 4; ++p)
+  for (int tj = 0; tj < 2; ++tj) {
+    const int j0 = qj + 16 * tj, ks = (j0 / kw) * kw;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) acc[p][q] = 0.0;
-  for (int a = r * g; a < r * g + g; ++a) {
-    double cv[4], gv[4];
+    for (int ti = 0; ti < 2; ++ti) {
+      const int i0 = qi + 16 * ti;
+      f64x4_t dq = {0.0, 0.0, 0.0, 0.0};
+      for (int k = ks; k < ks + kw; k += 4)
+        dq = __builtin_amdgcn_mfma_f64_16x16x4f64(double(cds[(i0 + mi) * kCdPitch + k + mk]),
+                                                  double(gs[(k + mk) * kD + j0 + mi]), dq, 0, 0, 0);
 #pragma unroll
-    for (int p = 0; p < 4; ++p) cv[p] = double(cds[(i0 + p) * kD + a]);  // two rows per wave: broadcasts
-    const float4 gq = *reinterpret_cast<const float4*>(&gs[a * kD + j0]);
-    gv[0] = gq.x; gv[1] = gq.y; gv[2] = gq.z; gv[3] = gq.w;
-#pragma unroll
-    for (int p = 0; p < 4; ++p)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) acc[p][q] = fma(cv[p], gv[q], acc[p][q]);
-  }
-#pragma unroll
-  for (int p = 0; p < 4; ++p)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float v = float(acc[p][q]);
-      const uint32_t hi = f32_to_bf16_rne(v);
-      const uint32_t lo = f32_to_bf16_rne(v - __uint_as_float(hi << 16));
-      const size_t off = (size_t(lh) * kD + i0 + p) * kD + j0 + q;
-      m0[off] = uint16_t(hi);
-      m1[off] = uint16_t(lo);
+      for (int v = 0; v < 4; ++v) {
+        const float x = float(dq[v]);
+        const uint32_t hi = f32_to_bf16_rne(x);
+        const uint32_t lo = f32_to_bf16_rne(x - __uint_as_float(hi << 16));
+        const size_t off = (size_t(lh) * kD + i0 + 4 * v + mk) * kD + j0 + mi;
+        m0[off] = uint16_t(hi);
+        m1[off] = uint16_t(lo);
+      }
     }
+  }
 }
 
 struct SpecArgs {
