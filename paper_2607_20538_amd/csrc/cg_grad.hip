@@ -16,9 +16,11 @@
 // blocks of a range of tokens of one (layer, batch row, head) on the VALU through LDS: X and M
 // in binary32, W, U, dL/dU and dL/dW in binary64 (the binary32 products accumulate exactly),
 // and accumulates its part of dL/dM in binary64 registers (a (d/16) x (d/16) tile per thread),
-// written as one partial per workgroup; grad_reduce sums the partials in a fixed order
+// written as one partial per workgroup; grad_data_mfma does the same for d = 128 with 16-token
+// blocks on the binary64 matrix cores; grad_reduce sums the partials in a fixed order
 // (deterministic); grad_frechet forms dL/dG and the Frechet adjoint per gauge block in binary64
-// (power series of the scaled block matrix by the Paterson-Stockmeyer scheme, then squaring).
+// (power series of the scaled block matrix by the Paterson-Stockmeyer scheme, then squaring),
+// and grad_frechet16 does the same for groups of at most 16 channels in one wave, in LDS.
 // Binary64 through the data pass matters: dL/dA is the antisymmetric part of dL/dS, which for
 // smooth objectives is much smaller than the terms that cancel in it (about 40x on random
 // Llama-shaped data), so binary32 sums over a block's d channels would reach the result.
