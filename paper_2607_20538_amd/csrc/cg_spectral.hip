@@ -22,6 +22,7 @@
 // General path (any supported d and g, bf16 or binary32 input, Tb in {2, 4, 8, 16, 32}): one
 // workgroup per block, gauge, channel DCT and token DCT on the VALU in binary32 through LDS.
 #include <algorithm>
+#include <cstdlib>
 #include <utility>
 
 #include "cg_internal.h"
@@ -490,6 +491,13 @@ hipError_t launch_spectral(int s, const ViewDev& X, const GaugeDev& G, int Tb, f
       int chunks = (occ * cu_count_spec() + a.nslices - 1) / a.nslices;
       chunks = std::min(std::max(chunks, 1), ntiles);
       a.tiles_per_wg = (ntiles + chunks - 1) / chunks;
+      // CG_TILES_PER_WG=k fixes the tiles per workgroup, as for the codec kernels, so that small
+      // inputs run the multi-tile loop (the software pipeline, the periodic fold of the binary32
+      // energy partials) that the resident grid only reaches on large ones
+      if (const char* f = getenv("CG_TILES_PER_WG")) {
+        const long k = strtol(f, nullptr, 10);
+        if (k > 0 && k < (1 << 20)) a.tiles_per_wg = int(std::min<long>(k, std::max(ntiles, 1)));
+      }
       a.chunks = (ntiles + a.tiles_per_wg - 1) / a.tiles_per_wg;
       const int nwg = ((a.nslices * a.chunks + 7) / 8) * 8;
       void* args[] = {&a};

@@ -51,8 +51,10 @@ def _check(got, ref, rtol=5e-5):
     |dU_uv,b| <= 2^-17 ||y_u,b|| with y_u,b the block's token-frequency-u row (M orthonormal), and
     |dE_uv| <= 2^-16 sum_b |U_uv,b| ||y_u,b|| <= 2^-16 sqrt(E_uv E_u.) (Cauchy-Schwarz over the
     blocks; E_u. = sum_v E_uv).  The binary32 token DCT adds a rounding of a few 2^-24 of each
-    column's norm, bounded the same way by 2^-19 sqrt(E_uv E_.v); binary64 sums (in any order)
-    add nothing visible."""
+    column's norm, bounded the same way by 2^-19 sqrt(E_uv E_.v).  The matrix-core kernel sums the
+    squares of at most eight tiles in binary32 before its binary64 totals: positive terms, so each
+    partial is within 8 2^-24 of its value, inside the 1e-6 relative term; binary64 sums (in any
+    order) add nothing visible."""
     st, en = got
     rs, re = ref
     np.testing.assert_allclose(st[:, 0], rs[:, 0], rtol=rtol, atol=1e-12)     # L_freq
@@ -63,6 +65,18 @@ def _check(got, ref, rtol=5e-5):
     e_col = re.sum(axis=1, keepdims=True)                                     # E_.v
     tol = 2.0 ** -16 * np.sqrt(re * e_row) + 2.0 ** -19 * np.sqrt(re * e_col) + 1e-6 * re + 1e-300
     assert np.all(np.abs(en - re) <= tol), float((np.abs(en - re) / tol).max())
+
+
+def test_spectral_stats_with_many_tiles_per_workgroup(monkeypatch):
+    """The matrix-core kernel with 20 tiles per workgroup (CG_TILES_PER_WG): 22 tiles per slice,
+    so one workgroup folds its binary32 energy partials after tiles 8 and 16 and at its last
+    tile, and the next takes the ragged rest."""
+    monkeypatch.setenv("CG_TILES_PER_WG", "20")
+    w = synth.Workload("spec", L=1, B=2, H=2, T=700, d=128, dtype="bf16", g=128, backend="bu", bits=4,
+                       data_seed=0x5ED)
+    X = synth.kv_tensor(w, 0)
+    G = O.gauge_make(O.GAUGE_HAAR, 1, 2, 128, 128, seed=9)
+    _check(_run(X, G, 0, 16), O.spectral_stats(X, G, 0, Tb=16))
 
 
 @pytest.mark.parametrize("g", [128, 32, 8])
